@@ -1,0 +1,211 @@
+"""ctypes wrapper of the CPU oracle (oracle/evox_ref.c).
+
+TEST INFRASTRUCTURE ONLY: imported by tests/, __graft_entry__.smoke() and the
+cpu_baseline leg of bench.py, never by the product package.  All arrays are
+numpy, C-contiguous, row-major [N, D] (row pitch D).
+"""
+import ctypes
+import os
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libevox_ref.so")
+
+SPHERE, ACKLEY, RASTRIGIN, GRIEWANK, ROSENBROCK, SCHWEFEL = range(6)
+FN_NAMES = ("sphere", "ackley", "rastrigin", "griewank", "rosenbrock", "schwefel")
+
+
+class RefParams(ctypes.Structure):
+    _fields_ = [
+        ("fn", ctypes.c_int32), ("clamp_x", ctypes.c_int32),
+        ("N", ctypes.c_int64), ("D", ctypes.c_int64),
+        ("lb", ctypes.c_float), ("ub", ctypes.c_float),
+        ("v_lo", ctypes.c_float), ("v_hi", ctypes.c_float),
+        ("w", ctypes.c_float), ("c1", ctypes.c_float), ("c2", ctypes.c_float),
+        ("phi", ctypes.c_float), ("vmax", ctypes.c_float), ("pad_", ctypes.c_float),
+        ("seed", ctypes.c_uint64),
+    ]
+
+
+_lib = None
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            from . import build as _b
+            _b.build()
+        L = ctypes.CDLL(LIB_PATH)
+        u32, i64, u64, f32 = ctypes.c_uint32, ctypes.c_int64, ctypes.c_uint64, ctypes.c_float
+        P = ctypes.c_void_p
+        L.evox_ref_philox4x32_10.argtypes = [P, P, P]
+        L.evox_ref_philox_word.argtypes = [u64, u32, u32, u32, u32, ctypes.c_int]
+        L.evox_ref_philox_word.restype = u32
+        L.evox_ref_u01.argtypes = [u32]
+        L.evox_ref_u01.restype = f32
+        L.evox_ref_u01_array.argtypes = [P, i64, P]
+        L.evox_ref_eval_row_f64.argtypes = [ctypes.c_int, P, i64]
+        L.evox_ref_eval_row_f64.restype = ctypes.c_double
+        L.evox_ref_eval.argtypes = [ctypes.c_int, P, i64, i64, i64, P]
+        L.evox_ref_argmin.argtypes = [P, i64]
+        L.evox_ref_argmin.restype = i64
+        L.evox_ref_init_uniform.argtypes = [u64, ctypes.c_int, i64, i64, f32, f32, P]
+        L.evox_ref_pso_init.argtypes = [P, P, P, P, P, P, P, P]
+        L.evox_ref_pso_step.argtypes = [P, i64, i64, P, P, P, P, P, P, P]
+        L.evox_ref_colmean.argtypes = [P, i64, i64, P]
+        L.evox_ref_perm.argtypes = [u64, i64, i64, P]
+        L.evox_ref_cso_init.argtypes = [P, P, P, P]
+        L.evox_ref_cso_step.argtypes = [P, i64, i64, P, P, P, P, P, P]
+        _lib = L
+    return _lib
+
+
+def _ptr(a):
+    return a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _f32(a):
+    a = np.ascontiguousarray(a, dtype=np.float32)
+    return a
+
+
+def philox4x32_10(ctr, key):
+    """Four output words of Philox4x32-10 for counter ctr[4], key key[2]."""
+    c = np.ascontiguousarray(ctr, dtype=np.uint32)
+    k = np.ascontiguousarray(key, dtype=np.uint32)
+    out = np.zeros(4, dtype=np.uint32)
+    lib().evox_ref_philox4x32_10(_ptr(c), _ptr(k), _ptr(out))
+    return out
+
+
+def philox_word(seed, c0, c1, c2, c3, word):
+    return int(lib().evox_ref_philox_word(seed, c0, c1, c2, c3, word))
+
+
+def u01(w):
+    return float(lib().evox_ref_u01(int(w)))
+
+
+def u01_array(words):
+    w = np.ascontiguousarray(words, dtype=np.uint32)
+    out = np.zeros(w.shape, dtype=np.float32)
+    lib().evox_ref_u01_array(_ptr(w), w.size, _ptr(out))
+    return out
+
+
+def eval_row_f64(fn, x):
+    x = _f32(x)
+    return float(lib().evox_ref_eval_row_f64(fn, _ptr(x), x.shape[-1]))
+
+
+def evaluate(fn, X):
+    """fp32 fitness of every row of X [N, D] (fp64 inside, rounded once)."""
+    X = _f32(X)
+    N, D = X.shape
+    out = np.zeros(N, dtype=np.float32)
+    rc = lib().evox_ref_eval(fn, _ptr(X), N, D, D, _ptr(out))
+    if rc != 0:
+        raise ValueError(f"evox_ref_eval rc={rc}")
+    return out
+
+
+def argmin(f):
+    f = _f32(f)
+    return int(lib().evox_ref_argmin(_ptr(f), f.shape[0]))
+
+
+def init_uniform(seed, stream, N, D, lo, hi):
+    out = np.zeros((N, D), dtype=np.float32)
+    lib().evox_ref_init_uniform(seed, stream, N, D, lo, hi, _ptr(out))
+    return out
+
+
+def make_params(fn, N, D, lb, ub, v_lo=0.0, v_hi=0.0, w=0.6, c1=1.5, c2=1.5, phi=0.1,
+                vmax=0.0, clamp_x=0, seed=0):
+    return RefParams(fn=fn, clamp_x=clamp_x, N=N, D=D, lb=lb, ub=ub, v_lo=v_lo, v_hi=v_hi,
+                     w=w, c1=c1, c2=c2, phi=phi, vmax=vmax, pad_=0.0, seed=seed)
+
+
+class PSO:
+    """Oracle PSO state: x, v, p, pf, g, gf, gi and the generation counter t."""
+
+    def __init__(self, params: RefParams):
+        self.P = params
+        N, D = params.N, params.D
+        self.x = np.zeros((N, D), np.float32)
+        self.v = np.zeros((N, D), np.float32)
+        self.p = np.zeros((N, D), np.float32)
+        self.pf = np.zeros(N, np.float32)
+        self.g = np.zeros(D, np.float32)
+        self._gf = ctypes.c_float(0.0)
+        self._gi = ctypes.c_int64(0)
+        self.t = 0
+        rc = lib().evox_ref_pso_init(ctypes.byref(self.P), _ptr(self.x), _ptr(self.v),
+                                     _ptr(self.p), _ptr(self.pf), _ptr(self.g),
+                                     ctypes.byref(self._gf), ctypes.byref(self._gi))
+        if rc != 0:
+            raise ValueError(f"evox_ref_pso_init rc={rc}")
+
+    @property
+    def gf(self):
+        return self._gf.value
+
+    @property
+    def gi(self):
+        return self._gi.value
+
+    def step(self, n_gens):
+        for a in (self.x, self.v, self.p, self.pf, self.g):
+            assert a.flags.c_contiguous and a.dtype == np.float32
+        rc = lib().evox_ref_pso_step(ctypes.byref(self.P), self.t, n_gens, _ptr(self.x),
+                                     _ptr(self.v), _ptr(self.p), _ptr(self.pf), _ptr(self.g),
+                                     ctypes.byref(self._gf), ctypes.byref(self._gi))
+        if rc != 0:
+            raise ValueError(f"evox_ref_pso_step rc={rc}")
+        self.t += n_gens
+
+
+def colmean(X):
+    X = _f32(X)
+    N, D = X.shape
+    out = np.zeros(D, np.float32)
+    lib().evox_ref_colmean(_ptr(X), N, D, _ptr(out))
+    return out
+
+
+def perm(seed, t, N):
+    out = np.zeros(N, np.int64)
+    lib().evox_ref_perm(seed, t, N, _ptr(out))
+    return out
+
+
+class CSO:
+    """Oracle CSO state: x, v, fit and the generation counter t."""
+
+    def __init__(self, params: RefParams):
+        self.P = params
+        N, D = params.N, params.D
+        self.x = np.zeros((N, D), np.float32)
+        self.v = np.zeros((N, D), np.float32)
+        self.fit = np.zeros(N, np.float32)
+        self.loser = np.zeros(N, np.uint8)
+        self.best_fit = float("nan")
+        self.best_idx = -1
+        self.t = 0
+        rc = lib().evox_ref_cso_init(ctypes.byref(self.P), _ptr(self.x), _ptr(self.v),
+                                     _ptr(self.fit))
+        if rc != 0:
+            raise ValueError(f"evox_ref_cso_init rc={rc}")
+
+    def step(self, n_gens):
+        bf = ctypes.c_float(0.0)
+        bi = ctypes.c_int64(0)
+        rc = lib().evox_ref_cso_step(ctypes.byref(self.P), self.t, n_gens, _ptr(self.x),
+                                     _ptr(self.v), _ptr(self.fit), ctypes.byref(bf),
+                                     ctypes.byref(bi), _ptr(self.loser))
+        if rc != 0:
+            raise ValueError(f"evox_ref_cso_step rc={rc}")
+        self.best_fit, self.best_idx = bf.value, bi.value
+        self.t += n_gens

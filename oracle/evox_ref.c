@@ -1,0 +1,449 @@
+/*
+ * evox_ref.c -- the CPU oracle for one generation of PSO / CSO over a
+ * population matrix X[N,D] (EvoX, arXiv 2301.12457).
+ *
+ * TEST INFRASTRUCTURE ONLY.  Only tests/, __graft_entry__.smoke() and the
+ * cpu_baseline leg of bench.py may load this library.  The product path
+ * (the HIP library) never calls it and shares no code, header, table or
+ * constant generator with it.
+ *
+ * Plain, slow, single-threaded C.  Everything follows the algorithm step by
+ * step in the order of the ask-evaluate-tell loop (Sec. IV-B, Eq. (1)-(3)):
+ * ask = produce the population to evaluate, evaluate = fitness per candidate,
+ * tell = selection / state update.  The paper prints no update rules and no
+ * benchmark formulas; the readings used here are:
+ *
+ *   - PSO: global-best PSO with inertia weight (the PSO of Sec. VII-A-1,
+ *     Kennedy & Eberhart as cited there).  Per element
+ *         v <- w v + c1 r1 (p - x) + c2 r2 (g - x),   x <- x + v
+ *     with r1, r2 ~ U[0,1) drawn per element.  The population state is fp32;
+ *     the element update is done in fp32 with fused multiply-adds placed
+ *     exactly as in pso_move_element() below.
+ *   - CSO: the competitive swarm optimizer listed in Table II (Cheng & Jin):
+ *     random pairs, the loser learns from the winner and the swarm mean.
+ *   - Benchmark functions: textbook definitions, evaluated in fp64 from the
+ *     fp32 inputs, sequential sum in index order, rounded once to fp32.
+ *   - Random numbers: Philox4x32-10 (Salmon, Moraes, Dror, Shaw, "Parallel
+ *     random numbers: as easy as 1, 2, 3", SC'11), written from its
+ *     published definition.  The paper itself names only JAX's rbg
+ *     generator (Sec. VII); the counter layout below is this build's own.
+ *
+ * Build: gcc -O2 -ffp-contract=off -fPIC -shared (no fast-math): every float
+ * operation is one IEEE rounding, fma only where fmaf() is written.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+/* ------------------------------------------------------------------------ */
+/* Philox4x32-10 (SC'11 paper, Sec. "Philox").                               */
+/* ------------------------------------------------------------------------ */
+
+/* Round multipliers and Weyl key increments, as published. */
+#define PHILOX_M4x32_0 0xD2511F53u
+#define PHILOX_M4x32_1 0xCD9E8D57u
+#define PHILOX_W32_0 0x9E3779B9u
+#define PHILOX_W32_1 0xBB67AE85u
+
+void evox_ref_philox4x32_10(const uint32_t ctr[4], const uint32_t key[2], uint32_t out[4])
+{
+    uint32_t x0 = ctr[0], x1 = ctr[1], x2 = ctr[2], x3 = ctr[3];
+    uint32_t k0 = key[0], k1 = key[1];
+    for (int round = 0; round < 10; ++round) {
+        if (round > 0) {
+            k0 += PHILOX_W32_0;
+            k1 += PHILOX_W32_1;
+        }
+        uint64_t p0 = (uint64_t)PHILOX_M4x32_0 * (uint64_t)x0;
+        uint64_t p1 = (uint64_t)PHILOX_M4x32_1 * (uint64_t)x2;
+        uint32_t hi0 = (uint32_t)(p0 >> 32), lo0 = (uint32_t)p0;
+        uint32_t hi1 = (uint32_t)(p1 >> 32), lo1 = (uint32_t)p1;
+        uint32_t y0 = hi1 ^ x1 ^ k0;
+        uint32_t y1 = lo1;
+        uint32_t y2 = hi0 ^ x3 ^ k1;
+        uint32_t y3 = lo0;
+        x0 = y0; x1 = y1; x2 = y2; x3 = y3;
+    }
+    out[0] = x0; out[1] = x1; out[2] = x2; out[3] = x3;
+}
+
+/* One 32-bit word of Philox(key = seed, counter = (c0, c1, c2, c3)). */
+uint32_t evox_ref_philox_word(uint64_t seed, uint32_t c0, uint32_t c1, uint32_t c2,
+                              uint32_t c3, int word)
+{
+    uint32_t ctr[4] = {c0, c1, c2, c3};
+    uint32_t key[2] = {(uint32_t)seed, (uint32_t)(seed >> 32)};
+    uint32_t out[4];
+    evox_ref_philox4x32_10(ctr, key, out);
+    return out[word & 3];
+}
+
+/* u32 -> U[0,1): the top 24 bits, times 2^-24.  Exact in fp32. */
+float evox_ref_u01(uint32_t w)
+{
+    return (float)(w >> 8) * 0x1p-24f;
+}
+
+/* Elementwise u01 over an array of words. */
+void evox_ref_u01_array(const uint32_t *w, int64_t n, float *out)
+{
+    for (int64_t i = 0; i < n; ++i) out[i] = evox_ref_u01(w[i]);
+}
+
+/* Random-stream identifiers (the counter's fourth word). */
+enum { STREAM_INIT_X = 0, STREAM_INIT_V = 1, STREAM_PSO = 2, STREAM_CSO = 3,
+       STREAM_PERM = 4 };
+
+/* Draw k of K for element (i, j) at generation t in stream s:
+ * word (j mod 4) of Philox(seed, (K*floor(j/4) + k, i, t, s)). */
+static float draw(uint64_t seed, int64_t i, int64_t j, int K, int k, int64_t t, int s)
+{
+    uint32_t c0 = (uint32_t)(K * (j / 4) + k);
+    return evox_ref_u01(evox_ref_philox_word(seed, c0, (uint32_t)i, (uint32_t)t,
+                                             (uint32_t)s, (int)(j % 4)));
+}
+
+/* ------------------------------------------------------------------------ */
+/* Benchmark functions (Problem.evaluate, Sec. IV-A, Table I).  Sphere is   */
+/* the function of Sec. VII-A-1; the others are the usual textbook ones.    */
+/* fp64 throughout, sum in index order.                                      */
+/* ------------------------------------------------------------------------ */
+
+enum { FN_SPHERE = 0, FN_ACKLEY, FN_RASTRIGIN, FN_GRIEWANK, FN_ROSENBROCK, FN_SCHWEFEL,
+       FN_COUNT };
+
+static const double kPi = 3.14159265358979323846;
+
+/* sum_i x_i^2 */
+static double sphere(const float *x, int64_t D)
+{
+    double s = 0.0;
+    for (int64_t i = 0; i < D; ++i) {
+        double xi = x[i];
+        s += xi * xi;
+    }
+    return s;
+}
+
+/* -a exp(-b sqrt(mean x^2)) - exp(mean cos(c x)) + a + e, a=20, b=0.2, c=2 pi */
+static double ackley(const float *x, int64_t D)
+{
+    const double a = 20.0, b = 0.2, c = 2.0 * kPi;
+    double s1 = 0.0, s2 = 0.0;
+    for (int64_t i = 0; i < D; ++i) {
+        double xi = x[i];
+        s1 += xi * xi;
+        s2 += cos(c * xi);
+    }
+    double n = (double)D;
+    return -a * exp(-b * sqrt(s1 / n)) - exp(s2 / n) + a + exp(1.0);
+}
+
+/* A D + sum_i (x_i^2 - A cos(2 pi x_i)), A = 10 */
+static double rastrigin(const float *x, int64_t D)
+{
+    const double A = 10.0;
+    double s = A * (double)D;
+    for (int64_t i = 0; i < D; ++i) {
+        double xi = x[i];
+        s += xi * xi - A * cos(2.0 * kPi * xi);
+    }
+    return s;
+}
+
+/* 1 + sum_i x_i^2 / 4000 - prod_i cos(x_i / sqrt(i)), i = 1..D */
+static double griewank(const float *x, int64_t D)
+{
+    double s = 0.0, p = 1.0;
+    for (int64_t i = 0; i < D; ++i) {
+        double xi = x[i];
+        s += xi * xi / 4000.0;
+        p *= cos(xi / sqrt((double)(i + 1)));
+    }
+    return 1.0 + s - p;
+}
+
+/* sum_{i=1}^{D-1} 100 (x_{i+1} - x_i^2)^2 + (1 - x_i)^2 */
+static double rosenbrock(const float *x, int64_t D)
+{
+    double s = 0.0;
+    for (int64_t i = 0; i + 1 < D; ++i) {
+        double xi = x[i], xn = x[i + 1];
+        double t1 = xn - xi * xi;
+        double t2 = 1.0 - xi;
+        s += 100.0 * t1 * t1 + t2 * t2;
+    }
+    return s;
+}
+
+/* 418.9829 D - sum_i x_i sin(sqrt(|x_i|)) */
+static double schwefel(const float *x, int64_t D)
+{
+    double s = 0.0;
+    for (int64_t i = 0; i < D; ++i) {
+        double xi = x[i];
+        s += xi * sin(sqrt(fabs(xi)));
+    }
+    return 418.9829 * (double)D - s;
+}
+
+/* Unrounded fp64 fitness of one row. */
+double evox_ref_eval_row_f64(int fn, const float *x, int64_t D)
+{
+    switch (fn) {
+    case FN_SPHERE: return sphere(x, D);
+    case FN_ACKLEY: return ackley(x, D);
+    case FN_RASTRIGIN: return rastrigin(x, D);
+    case FN_GRIEWANK: return griewank(x, D);
+    case FN_ROSENBROCK: return rosenbrock(x, D);
+    case FN_SCHWEFEL: return schwefel(x, D);
+    default: return NAN;
+    }
+}
+
+/* Fitness of N rows of X (row pitch ldx >= D), rounded once to fp32. */
+int evox_ref_eval(int fn, const float *X, int64_t N, int64_t D, int64_t ldx, float *out)
+{
+    if (fn < 0 || fn >= FN_COUNT || N < 0 || D < 1 || ldx < D) return -1;
+    for (int64_t i = 0; i < N; ++i) out[i] = (float)evox_ref_eval_row_f64(fn, X + i * ldx, D);
+    return 0;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Selection: index of the best fitness.                                     */
+/* Order: smaller value first, lower index on ties, -0 == +0, NaN after      */
+/* everything (an all-NaN array gives index 0).                              */
+/* ------------------------------------------------------------------------ */
+
+static int better(float a, int64_t ia, float b, int64_t ib)
+{
+    if (isnan(a)) return isnan(b) && ia < ib;
+    if (isnan(b)) return 1;
+    if (a < b) return 1;
+    if (b < a) return 0;
+    return ia < ib;
+}
+
+int64_t evox_ref_argmin(const float *f, int64_t N)
+{
+    int64_t best = 0;
+    for (int64_t i = 1; i < N; ++i)
+        if (better(f[i], i, f[best], best)) best = i;
+    return best;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Parameters (the immutable hyperparameters theta of Sec. IV-B).            */
+/* ------------------------------------------------------------------------ */
+
+typedef struct {
+    int32_t fn;         /* benchmark function id */
+    int32_t clamp_x;    /* nonzero: clamp positions to [lb, ub] after a move */
+    int64_t N, D;       /* population size, dimension */
+    float lb, ub;       /* initial box (and the clamp box) */
+    float v_lo, v_hi;   /* initial velocity box; both 0 means v = 0 */
+    float w, c1, c2;    /* PSO inertia and acceleration coefficients */
+    float phi;          /* CSO social factor */
+    float vmax;         /* PSO velocity clamp; <= 0 means none */
+    float pad_;
+    uint64_t seed;      /* Philox key */
+} evox_ref_params;
+
+/* Algorithm.setup (Sec. IV-A): uniform initial population and velocity.
+ * x_ij = lb + u (ub - lb), u from stream 0; v_ij likewise from stream 1. */
+static float uniform_in(float u, float lo, float hi)
+{
+    return fmaf(u, hi - lo, lo);
+}
+
+void evox_ref_init_uniform(uint64_t seed, int stream, int64_t N, int64_t D, float lo, float hi,
+                           float *out)
+{
+    for (int64_t i = 0; i < N; ++i)
+        for (int64_t j = 0; j < D; ++j)
+            out[i * D + j] = uniform_in(draw(seed, i, j, 1, 0, 0, stream), lo, hi);
+}
+
+static void init_xv(const evox_ref_params *P, float *x, float *v)
+{
+    evox_ref_init_uniform(P->seed, STREAM_INIT_X, P->N, P->D, P->lb, P->ub, x);
+    if (P->v_lo == 0.0f && P->v_hi == 0.0f)
+        memset(v, 0, sizeof(float) * (size_t)(P->N * P->D));
+    else
+        evox_ref_init_uniform(P->seed, STREAM_INIT_V, P->N, P->D, P->v_lo, P->v_hi, v);
+}
+
+/* ------------------------------------------------------------------------ */
+/* PSO                                                                       */
+/* State: x, v (current), p, pf (personal bests), g, gf, gi (global best).   */
+/* ------------------------------------------------------------------------ */
+
+int evox_ref_pso_init(const evox_ref_params *P, float *x, float *v, float *p, float *pf,
+                      float *g, float *gf, int64_t *gi)
+{
+    if (P->N < 1 || P->D < 1) return -1;
+    init_xv(P, x, v);
+    memcpy(p, x, sizeof(float) * (size_t)(P->N * P->D));
+    for (int64_t i = 0; i < P->N; ++i) pf[i] = INFINITY;
+    *gf = INFINITY;
+    *gi = 0;
+    memcpy(g, p, sizeof(float) * (size_t)P->D);
+    return 0;
+}
+
+/* One velocity/position update of one element. */
+static void pso_move_element(const evox_ref_params *P, float r1, float r2, float xv, float vv,
+                             float pv, float gv, float *xn_out, float *vn_out)
+{
+    float a = P->c1 * r1;
+    float b = P->c2 * r2;
+    float d1 = pv - xv;
+    float d2 = gv - xv;
+    float vn = fmaf(b, d2, fmaf(a, d1, P->w * vv));
+    if (P->vmax > 0.0f) vn = fminf(fmaxf(vn, -P->vmax), P->vmax);
+    float xn = xv + vn;
+    if (P->clamp_x) xn = fminf(fmaxf(xn, P->lb), P->ub);
+    *xn_out = xn;
+    *vn_out = vn;
+}
+
+/* n_gens ask-evaluate-tell iterations starting at generation t0.
+ * Each one: evaluate x (Problem.evaluate); personal bests take strictly
+ * better values (tell); the global best is the best personal best; then
+ * every particle moves (the next ask). */
+int evox_ref_pso_step(const evox_ref_params *P, int64_t t0, int64_t n_gens, float *x, float *v,
+                      float *p, float *pf, float *g, float *gf, int64_t *gi)
+{
+    const int64_t N = P->N, D = P->D;
+    if (N < 1 || D < 1 || n_gens < 0 || P->fn < 0 || P->fn >= FN_COUNT) return -1;
+    for (int64_t t = t0; t < t0 + n_gens; ++t) {
+        for (int64_t i = 0; i < N; ++i) {
+            float f = (float)evox_ref_eval_row_f64(P->fn, x + i * D, D);
+            if (f < pf[i]) {
+                pf[i] = f;
+                memcpy(p + i * D, x + i * D, sizeof(float) * (size_t)D);
+            }
+        }
+        *gi = evox_ref_argmin(pf, N);
+        *gf = pf[*gi];
+        memcpy(g, p + *gi * D, sizeof(float) * (size_t)D);
+        for (int64_t i = 0; i < N; ++i) {
+            for (int64_t j = 0; j < D; ++j) {
+                float r1 = draw(P->seed, i, j, 2, 0, t, STREAM_PSO);
+                float r2 = draw(P->seed, i, j, 2, 1, t, STREAM_PSO);
+                int64_t e = i * D + j;
+                pso_move_element(P, r1, r2, x[e], v[e], p[e], g[j], &x[e], &v[e]);
+            }
+        }
+    }
+    return 0;
+}
+
+/* ------------------------------------------------------------------------ */
+/* CSO                                                                       */
+/* State: x, v, fit (fitness of the current x).                              */
+/* ------------------------------------------------------------------------ */
+
+/* Column mean: fp64 sum in row order, fp64 divide, one rounding to fp32. */
+void evox_ref_colmean(const float *X, int64_t N, int64_t D, float *xbar)
+{
+    for (int64_t j = 0; j < D; ++j) {
+        double s = 0.0;
+        for (int64_t i = 0; i < N; ++i) s += (double)X[i * D + j];
+        xbar[j] = (float)(s / (double)N);
+    }
+}
+
+typedef struct {
+    uint32_t key;
+    int64_t idx;
+} keyed;
+
+static int keyed_cmp(const void *pa, const void *pb)
+{
+    const keyed *a = (const keyed *)pa, *b = (const keyed *)pb;
+    if (a->key != b->key) return a->key < b->key ? -1 : 1;
+    return (a->idx > b->idx) - (a->idx < b->idx);
+}
+
+/* Random permutation of 0..N-1 at generation t: sort the individuals by the
+ * key (Philox word from stream 4), lower index first among equal keys. */
+void evox_ref_perm(uint64_t seed, int64_t t, int64_t N, int64_t *perm)
+{
+    keyed *kv = (keyed *)malloc(sizeof(keyed) * (size_t)(N > 0 ? N : 1));
+    for (int64_t i = 0; i < N; ++i) {
+        kv[i].key = evox_ref_philox_word(seed, (uint32_t)(i / 4), 0u, (uint32_t)t,
+                                         STREAM_PERM, (int)(i % 4));
+        kv[i].idx = i;
+    }
+    qsort(kv, (size_t)N, sizeof(keyed), keyed_cmp);
+    for (int64_t i = 0; i < N; ++i) perm[i] = kv[i].idx;
+    free(kv);
+}
+
+/* Pair (a, b): b wins when its fitness is strictly lower, or when a's is
+ * NaN and b's is not; otherwise a wins (ties go to a). */
+static int second_wins(float fa, float fb)
+{
+    return fb < fa || (isnan(fa) && !isnan(fb));
+}
+
+int evox_ref_cso_init(const evox_ref_params *P, float *x, float *v, float *fit)
+{
+    if (P->N < 1 || P->D < 1 || P->fn < 0 || P->fn >= FN_COUNT) return -1;
+    init_xv(P, x, v);
+    return evox_ref_eval(P->fn, x, P->N, P->D, P->D, fit);
+}
+
+/* n_gens CSO iterations from generation t0.  Each: swarm mean of the current
+ * positions; random pairing; each loser l moves toward its winner w and the
+ * mean,
+ *     v_l <- R1 v_l + R2 (x_w - x_l) + phi R3 (xbar - x_l),  x_l <- x_l + v_l,
+ * and only the losers are re-evaluated.  Afterwards (best_fit, best_idx) is
+ * the best of the current swarm.  loser_flag (nullable, N bytes) receives 1
+ * for the rows updated by the last generation. */
+int evox_ref_cso_step(const evox_ref_params *P, int64_t t0, int64_t n_gens, float *x, float *v,
+                      float *fit, float *best_fit, int64_t *best_idx, uint8_t *loser_flag)
+{
+    const int64_t N = P->N, D = P->D;
+    if (N < 1 || D < 1 || n_gens < 0 || P->fn < 0 || P->fn >= FN_COUNT) return -1;
+    float *xbar = (float *)malloc(sizeof(float) * (size_t)D);
+    int64_t *perm = (int64_t *)malloc(sizeof(int64_t) * (size_t)N);
+    uint8_t *is_loser = (uint8_t *)calloc((size_t)N, 1);
+    for (int64_t t = t0; t < t0 + n_gens; ++t) {
+        evox_ref_colmean(x, N, D, xbar);
+        evox_ref_perm(P->seed, t, N, perm);
+        memset(is_loser, 0, (size_t)N);
+        for (int64_t k = 0; k < N / 2; ++k) {
+            int64_t a = perm[2 * k], b = perm[2 * k + 1];
+            int64_t w = a, l = b;
+            if (second_wins(fit[a], fit[b])) { w = b; l = a; }
+            is_loser[l] = 1;
+            for (int64_t j = 0; j < D; ++j) {
+                float R1 = draw(P->seed, l, j, 3, 0, t, STREAM_CSO);
+                float R2 = draw(P->seed, l, j, 3, 1, t, STREAM_CSO);
+                float R3 = draw(P->seed, l, j, 3, 2, t, STREAM_CSO);
+                float xl = x[l * D + j], xw = x[w * D + j], vl = v[l * D + j];
+                float t0v = R1 * vl;
+                float t1v = fmaf(R2, xw - xl, t0v);
+                float c = P->phi * R3;
+                float vn = fmaf(c, xbar[j] - xl, t1v);
+                float xn = xl + vn;
+                if (P->clamp_x) xn = fminf(fmaxf(xn, P->lb), P->ub);
+                v[l * D + j] = vn;
+                x[l * D + j] = xn;
+            }
+        }
+        for (int64_t i = 0; i < N; ++i)
+            if (is_loser[i]) fit[i] = (float)evox_ref_eval_row_f64(P->fn, x + i * D, D);
+    }
+    int64_t bi = evox_ref_argmin(fit, N);
+    *best_idx = bi;
+    *best_fit = fit[bi];
+    if (loser_flag) memcpy(loser_flag, is_loser, (size_t)N);
+    free(xbar);
+    free(perm);
+    free(is_loser);
+    return 0;
+}
