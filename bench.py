@@ -1,0 +1,213 @@
+"""Benchmark of the MI355X PSO / CSO generation hot path.
+
+One step = one Workflow.step call of the workload's full generation count
+(evox_pso_step / evox_cso_step(state, gens)), or one evaluation pass for the
+evaluation-only workload, on inputs resident in HBM.  Prints one JSON line.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+"""
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+from paper_2301_12457_amd.workloads import WORKLOADS, normal_matrix_torch  # noqa: E402
+
+METRIC = "individual·dim updates/sec per fused generation; % of HBM peak GB/s"
+UNIT = "individual·dim updates/s"
+HBM_PEAK_GBS = 8000.0
+DEFAULT_WORKLOAD = "pso_rastrigin_1e5x1e3"
+KERNEL_SOURCES = ("paper_2301_12457_amd/csrc/evox_device.hpp",
+                  "paper_2301_12457_amd/csrc/evox_kernels.hpp")
+
+
+def kernel_hash():
+    h = hashlib.sha256()
+    for rel in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def traffic_from_profile(name, launches_bytes_unit):
+    """HBM bytes per launch of the dominant kernel from the committed PMC
+    summary, if it was taken on the current kernel sources."""
+    path = os.path.join(ROOT, "profiles", f"{name}_traffic.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        t = json.load(f)
+    if t.get("kernel_sha") != kernel_hash():
+        return None
+    return (t["fetch_kib_per_dispatch"] + t["write_kib_per_dispatch"]) * 1024.0 * t["copy_scale"]
+
+
+def pso_bytes_per_launch(w, launches, improved_rows):
+    # read x, v, pbest and write x, v (20 B per element); read pfit (4 B per
+    # row); write pbest row and pfit of each improved row
+    imp = improved_rows / max(launches, 1)
+    return 20.0 * w.N * w.D + 4.0 * w.N + (4.0 * w.D + 4.0) * imp
+
+
+def cso_bytes_per_launch(w):
+    # per pair: read winner row, loser x and v, write loser x and v
+    # (20 B per pair element = 10 B per individual element); fitness of both
+    # and the permutation entries (4 B each), write loser fitness
+    pairs = w.N // 2
+    return 20.0 * pairs * w.D + pairs * (4 * 2 + 4 * 2 + 4)
+
+
+def cpu_baseline(w, budget_s=12.0):
+    """The oracle, single-threaded, on a bounded sample of the workload."""
+    import oracle
+    fn = {"sphere": 0, "ackley": 1, "rastrigin": 2, "griewank": 3, "rosenbrock": 4,
+          "schwefel": 5}[w.fn]
+    if w.algo == "eval":
+        import numpy as np
+        from paper_2301_12457_amd.workloads import normal_matrix_np
+        rows = 20_000
+        X = normal_matrix_np(rows, w.D, w.x_mu, w.x_sigma, w.seed)
+        t0 = time.perf_counter()
+        n = 0
+        while time.perf_counter() - t0 < budget_s:
+            oracle.evaluate(fn, X)
+            n += 1
+        dt = time.perf_counter() - t0
+        return {"value": rows * w.D * n / dt, "unit": UNIT, "cores": 1, "kind": "oracle",
+                "sample": f"{rows} of {w.N} rows x D={w.D}, {n} evaluation passes, {dt:.1f} s"}
+    rows = min(w.N, 2000 if w.algo == "pso" else 20_000)
+    P = oracle.make_params(fn, rows, w.D, w.lb, w.ub, v_lo=w.v_lo, v_hi=w.v_hi, w=w.w, c1=w.c1,
+                           c2=w.c2, phi=w.phi, vmax=w.vmax, seed=w.seed)
+    s = oracle.PSO(P) if w.algo == "pso" else oracle.CSO(P)
+    s.step(1)
+    t0 = time.perf_counter()
+    gens = 0
+    while time.perf_counter() - t0 < budget_s and gens < w.gens:
+        s.step(1)
+        gens += 1
+    dt = time.perf_counter() - t0
+    return {"value": rows * w.D * gens / dt, "unit": UNIT, "cores": 1, "kind": "oracle",
+            "sample": f"{rows} of {w.N} individuals x D={w.D}, {gens} generations, {dt:.1f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", default=DEFAULT_WORKLOAD, choices=sorted(WORKLOADS))
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calib-copy-mib", type=int, default=0,
+                    help="also run a plain device copy of this size (HBM-counter calibration)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for {args.gpus}): this build has no "
+              "multi-GPU path", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2301_12457_amd as evox
+
+    w = WORKLOADS[args.workload]
+    torch.cuda.set_device(0)
+    stream = torch.cuda.current_stream()
+    fn = evox.FN_IDS[w.fn]
+
+    if w.algo == "eval":
+        X = normal_matrix_torch(w.N, w.D, w.x_mu, w.x_sigma, w.seed)
+        out = torch.empty(w.N, dtype=torch.float32, device="cuda")
+        bf = torch.empty(1, dtype=torch.float32, device="cuda")
+        bi = torch.empty(1, dtype=torch.int64, device="cuda")
+        scratch = torch.empty(evox.evox_eval_argmin_scratch_bytes(w.N) // 4 + 64,
+                              dtype=torch.int32, device="cuda")
+
+        def step():
+            evox.evox_eval_argmin(fn, X, w.N, w.D, w.D, out, bf, bi, scratch)
+        swarm = None
+    else:
+        algo = evox.PSO if w.algo == "pso" else evox.CSO
+        P = evox.make_params(algo, fn, w.N, w.D, w.lb, w.ub, v_lo=w.v_lo, v_hi=w.v_hi, w=w.w,
+                             c1=w.c1, c2=w.c2, phi=w.phi, vmax=w.vmax, seed=w.seed)
+        swarm = evox.Swarm(P)
+
+        def step():
+            swarm.step(w.gens)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    print(f"[bench] {w.name}: warmup done", file=sys.stderr, flush=True)
+
+    if swarm is not None:
+        swarm.profile(True)
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    ev0.record(stream)
+    for _ in range(args.steps):
+        step()
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms = ev0.elapsed_time(ev1) / args.steps
+    print(f"[bench] timed {args.steps} steps: {ms:.3f} ms/step (wall {wall:.3f} s)",
+          file=sys.stderr, flush=True)
+
+    gens = w.gens if w.algo != "eval" else 1
+    value = w.N * w.D * gens / (ms / 1e3)
+    roofline = None
+    if swarm is not None:
+        fused_ms, launches, improved = swarm.profile_read()
+        swarm.profile(False)
+        if launches > 0:
+            avg_ms = fused_ms / launches
+            bytes_per = (pso_bytes_per_launch(w, launches, improved) if w.algo == "pso"
+                         else cso_bytes_per_launch(w))
+            achieved = bytes_per / (avg_ms / 1e3) / 1e9
+            kname = "k_pso_fused" if w.algo == "pso" else "k_cso"
+            traffic = traffic_from_profile(w.name, bytes_per)
+            roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
+                        "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                        "traffic": traffic, "kernel": kname,
+                        "avg_launch_us": round(avg_ms * 1e3, 2), "launches": launches,
+                        "algorithmic_bytes_per_launch": bytes_per}
+    else:
+        bytes_per = 4.0 * w.N * w.D + 4.0 * w.N
+        achieved = bytes_per / (ms / 1e3) / 1e9
+        roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
+                    "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                    "traffic": traffic_from_profile(w.name, bytes_per), "kernel": "k_eval",
+                    "avg_launch_us": round(ms * 1e3, 2), "launches": args.steps,
+                    "algorithmic_bytes_per_launch": bytes_per}
+
+    if args.calib_copy_mib:
+        n = args.calib_copy_mib * (1 << 20) // 4
+        a = torch.ones(n, dtype=torch.float32, device="cuda")
+        b = torch.empty_like(a)
+        for _ in range(3):
+            b.copy_(a)
+        torch.cuda.synchronize()
+
+    base = None
+    if not args.no_cpu_baseline:
+        base = cpu_baseline(w)
+        print(f"[bench] cpu baseline: {base}", file=sys.stderr, flush=True)
+
+    line = {
+        "metric": METRIC, "value": value, "unit": UNIT, "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "config": {"workload": w.name, "algo": w.algo, "fn": w.fn, "N": w.N, "D": w.D,
+                   "generations_per_step": gens, "seed": w.seed},
+        "roofline": roofline, "cpu_baseline": base,
+    }
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,214 @@
+/*
+ * evox.h -- C ABI of the MI355X (gfx950) population-optimizer hot path.
+ *
+ * EvoX (arXiv 2301.12457) states an evolutionary algorithm as a stream of
+ * state transitions (Sec. IV-B, Eq. (1)-(3)):
+ *     T_pop, S = ask(S);   T_fit, S = evaluate(S, T_pop);   S = tell(S, T_fit)
+ * with the stateful signature (state, ...) -> (result, state) and the
+ * Algorithm / Problem / Workflow modules of Table I (setup, ask, tell,
+ * evaluate, init, step).  This library implements that loop for two swarm
+ * algorithms over an fp32 population matrix X[N, D]:
+ *   - PSO (global-best, inertia weight; the PSO of the single-objective
+ *     experiment, Sec. VII-A-1),
+ *   - CSO, the competitive swarm optimizer listed in Table II,
+ * on six benchmark functions (Sphere, the function of Sec. VII-A-1, and the
+ * textbook Ackley, Rastrigin, Griewank, Rosenbrock and Schwefel).
+ *
+ * Everything runs in hand-written HIP kernels; every call enqueues work on the
+ * caller's HIP stream and returns without waiting, except evox_best and
+ * evox_profile_read, which synchronize that stream.
+ *
+ * Ownership: every device buffer is allocated by the caller and only borrowed
+ * by the library.  The library allocates no device memory; evox_state_create
+ * allocates one host-side handle, freed by evox_state_destroy.
+ *
+ * Errors: every int-returning call returns EVOX_OK (0) or a negative
+ * evox_status.  A call that fails validation enqueues nothing and leaves the
+ * state unchanged.  evox_last_error() gives a message for the calling thread's
+ * last failure.  Kernel faults are asynchronous and surface at the next
+ * synchronizing call as EVOX_EHIP.
+ *
+ * Random numbers: Philox4x32-10 (Salmon et al., SC'11) keyed by the 64-bit
+ * seed (key = (low word, high word)).  Draw k of K for element (i, j) at
+ * generation t in stream s is word (j mod 4) of
+ *     Philox(seed, counter = (K * floor(j / 4) + k, i, t, s)),
+ * mapped to [0, 1) as (word >> 8) * 2^-24.  Streams: 0 initial positions,
+ * 1 initial velocities, 2 PSO (K = 2: r1, r2), 3 CSO (K = 3: R1, R2, R3, row i
+ * = the loser), 4 CSO pairing keys (key of individual i = word (i mod 4) of
+ * Philox(seed, (floor(i / 4), 0, t, 4))).
+ */
+#ifndef EVOX_H
+#define EVOX_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Benchmark functions (Problem.evaluate).  F(x) for x in R^D:
+ *   SPHERE      sum x_i^2
+ *   ACKLEY      -20 exp(-0.2 sqrt(mean x_i^2)) - exp(mean cos(2 pi x_i)) + 20 + e
+ *   RASTRIGIN   10 D + sum (x_i^2 - 10 cos(2 pi x_i))
+ *   GRIEWANK    1 + sum x_i^2 / 4000 - prod cos(x_i / sqrt(i)),  i = 1..D
+ *   ROSENBROCK  sum_{i<D} 100 (x_{i+1} - x_i^2)^2 + (1 - x_i)^2
+ *   SCHWEFEL    418.9829 D - sum x_i sin(sqrt(|x_i|))                        */
+enum evox_fn {
+    EVOX_SPHERE = 0,
+    EVOX_ACKLEY = 1,
+    EVOX_RASTRIGIN = 2,
+    EVOX_GRIEWANK = 3,
+    EVOX_ROSENBROCK = 4,
+    EVOX_SCHWEFEL = 5
+};
+
+enum evox_algo { EVOX_PSO = 0, EVOX_CSO = 1 };
+
+enum evox_status {
+    EVOX_OK = 0,
+    EVOX_EINVAL = -1, /* bad argument: size, null pointer, unknown id, wrong algorithm */
+    EVOX_EHIP = -2,   /* HIP runtime or launch error */
+    EVOX_ENOSPC = -3, /* scratch buffer smaller than evox_scratch_bytes() */
+    EVOX_EALIGN = -4  /* a device pointer or row pitch is not 16-byte aligned */
+};
+
+/* Largest dimension D supported by the generation kernels. */
+#define EVOX_MAX_D 32768
+
+/* Immutable hyperparameters (theta of Sec. IV-B), fixed at creation. */
+typedef struct evox_params {
+    int32_t algo;     /* EVOX_PSO or EVOX_CSO */
+    int32_t fn_id;    /* enum evox_fn */
+    int64_t N;        /* population size, >= 1 (CSO: >= 2), < 2^31 */
+    int64_t D;        /* dimension, 1 .. EVOX_MAX_D */
+    int64_t ldx;      /* row pitch of x, v, pbest in floats: ldx >= D, ldx % 4 == 0 */
+    float lb, ub;     /* initial positions ~ U[lb, ub): x = fma(u, ub - lb, lb) */
+    float v_lo, v_hi; /* initial velocities ~ U[v_lo, v_hi); both 0 gives v = 0 */
+    float w, c1, c2;  /* PSO inertia and acceleration coefficients */
+    float phi;        /* CSO social factor */
+    float vmax;       /* PSO velocity clamp to [-vmax, vmax]; <= 0: none */
+    int32_t clamp_x;  /* nonzero: positions clamped to [lb, ub] after each move */
+    uint64_t seed;    /* Philox key */
+} evox_params;
+
+/* Caller-owned device buffers, borrowed by the state (row-major, pitch ldx;
+ * the padding columns D..ldx-1 are kept at zero by the library).
+ *   PSO: x, v, pbest [N][ldx]; pfit [N]; gbest [ldx]; fit [N] optional (the
+ *        fitness of the last evaluated positions); xbar unused.
+ *   CSO: x, v [N][ldx]; fit [N]; xbar [ldx] (swarm mean of x); pbest, pfit,
+ *        gbest unused.
+ * Every array pointer must be 16-byte aligned.  scratch must hold
+ * evox_scratch_bytes(params) bytes, 256-byte aligned, and must not be used by
+ * anything else while the state exists. */
+typedef struct evox_buffers {
+    float *x, *v, *pbest, *pfit, *fit, *gbest, *xbar;
+    void *scratch;
+    size_t scratch_bytes;
+} evox_buffers;
+
+typedef struct evox_state evox_state; /* opaque host-side handle */
+
+/* Bytes of device scratch the state needs for these parameters (0 if the
+ * parameters are invalid). */
+size_t evox_scratch_bytes(const evox_params *params);
+
+/* Algorithm.setup + Workflow.init (Sec. IV-A, Table I): validates, fills the
+ * buffers with the generation-0 state on `hip_stream` and returns the handle.
+ *   PSO: x, v drawn as above, pbest = x, pfit = +inf, best = (+inf, 0),
+ *        gbest = row 0 of pbest.
+ *   CSO: x, v drawn as above, fit = F(x), xbar = column mean of x (fp64 sum,
+ *        one rounding), best = argmin of fit.
+ * The generation counter starts at 0. */
+int evox_state_create(const evox_params *params, const evox_buffers *buffers, void *hip_stream,
+                      evox_state **out);
+
+/* Frees the host handle only; the caller's buffers are untouched. */
+int evox_state_destroy(evox_state *state);
+
+/* Problem.evaluate (Sec. IV-A): out[i] = F(X_i) for i < N over a dense
+ * row-major X [N][D] (device pointer), fp32 out [N] (device pointer).  The
+ * result is within 1e-5 relative of the fp64 value (relative to the
+ * function's scale: see the tests).  Any alignment of X is accepted. */
+int evox_eval(int fn_id, const float *X, int64_t N, int64_t D, float *out, void *hip_stream);
+
+/* evox_eval with an explicit row pitch ldx >= D (floats). */
+int evox_eval_ld(int fn_id, const float *X, int64_t N, int64_t D, int64_t ldx, float *out,
+                 void *hip_stream);
+
+/* Scratch bytes evox_eval_argmin needs for N rows. */
+size_t evox_eval_argmin_scratch_bytes(int64_t N);
+
+/* Evaluation plus selection of the best candidate: out as evox_eval_ld, and
+ * (best_fit_dev[0], best_idx_dev[0]) = the lexicographic minimum of
+ * (out[i], i): smaller value first, lower index on ties, -0 == +0, NaN after
+ * every number (all NaN gives index 0).  best_fit_dev / best_idx_dev are
+ * device pointers (float, int64); scratch is caller device memory of
+ * evox_eval_argmin_scratch_bytes(N) bytes, 256-byte aligned. */
+int evox_eval_argmin(int fn_id, const float *X, int64_t N, int64_t D, int64_t ldx, float *out,
+                     float *best_fit_dev, int64_t *best_idx_dev, void *scratch,
+                     size_t scratch_bytes, void *hip_stream);
+
+/* Workflow.step x n_gens for PSO (Sec. IV-A, Table I; Eq. (1)-(3)).  One
+ * generation t: evaluate x (fitness f); where f_i < pfit_i strictly, pbest_i =
+ * x_i and pfit_i = f_i; the global best is the minimum of pfit in the argmin
+ * order above and gbest is a copy of that pbest row; then every element moves
+ *     a = c1 r1;  b = c2 r2;  vn = fma(b, g - x, fma(a, p - x, w v))
+ *     vn = clamp(vn, -vmax, vmax) if vmax > 0;  x = x + vn (clamped if clamp_x)
+ * with r1, r2 from stream 2 at generation t.  After the call x holds the
+ * moved, not yet evaluated positions, and the generation counter has grown by
+ * n_gens.  step(a) then step(b) equals step(a + b) bit for bit. */
+int evox_pso_step(evox_state *state, int64_t n_gens);
+
+/* Workflow.step x n_gens for CSO.  One generation t: xbar is the mean of the
+ * current positions; individuals are paired by a random permutation (sort by
+ * (stream-4 key, index)): pairs (perm[2k], perm[2k+1]), k < floor(N/2); the
+ * second wins when its fitness is strictly lower (or the first's is NaN and
+ * its own is not); each loser l moves toward its winner w and the mean
+ *     t0 = R1 v;  t1 = fma(R2, x_w - x_l, t0);  vn = fma(phi R3, xbar - x_l, t1)
+ *     x_l = x_l + vn (clamped if clamp_x)
+ * with R1..R3 from stream 3 at generation t, and only the losers are
+ * re-evaluated.  Winners and an unpaired individual are untouched.  xbar is
+ * then refreshed from the new positions. */
+int evox_cso_step(evox_state *state, int64_t n_gens);
+
+/* If the caller has changed x (or fit) of a CSO state, recompute xbar from x
+ * and, when refit is nonzero, fit = F(x). */
+int evox_cso_refresh(evox_state *state, int refit);
+
+/* Best solution so far (what a Monitor would record, Sec. IV-B).  Waits for
+ * the state's stream.  PSO: (gf, gi) of the last evaluated generation and,
+ * if best_x_host is non-null, the gbest row (D floats) copied to host memory.
+ * CSO: argmin of the current fitness and that individual's row.  Before any
+ * PSO generation: (+inf, 0) and row 0 of pbest. */
+int evox_best(evox_state *state, float *best_fit, int64_t *best_idx, float *best_x_host);
+
+/* Generations completed so far. */
+int64_t evox_generation(const evox_state *state);
+
+/* Layout the kernels use for dimension D: threads per row and float4 chunks
+ * per thread (for tests and reports). */
+int evox_row_layout(int64_t D, int32_t *threads_per_row, int32_t *chunks_per_thread);
+
+/* Diagnostic: out[4 k + m] = word m of Philox(seed, (k, c1, c2, c3)) for
+ * k < n_ctr, computed by the device Philox the kernels use (device out). */
+int evox_philox_fill(uint64_t seed, uint32_t c1, uint32_t c2, uint32_t c3, int64_t n_ctr,
+                     uint32_t *out_dev, void *hip_stream);
+
+/* Timing of the generation kernels with HIP events on the state's stream.
+ * evox_profile(state, 1) starts recording (clears the totals), 0 stops.
+ * evox_profile_read waits for the stream and returns the summed duration of
+ * the fused generation-kernel launches, their count, and the number of rows
+ * whose personal best improved in those launches (PSO). */
+int evox_profile(evox_state *state, int enable);
+int evox_profile_read(evox_state *state, double *fused_ms, int64_t *fused_launches,
+                      int64_t *improved_rows);
+
+const char *evox_strerror(int code);
+const char *evox_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* EVOX_H */

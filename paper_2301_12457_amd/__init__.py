@@ -1,0 +1,243 @@
+"""Python binding of the gfx950 EvoX hot path (libevox.so, C ABI in include/evox.h).
+
+Argument marshalling only: torch supplies device memory and the HIP stream,
+every step of the path runs in the library's kernels.  Importing this module
+does not touch the GPU; the first call that needs the library loads it and
+raises if it has not been built (python paper_2301_12457_amd/build.py).
+"""
+import ctypes
+import math
+import os
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libevox.so")
+
+SPHERE, ACKLEY, RASTRIGIN, GRIEWANK, ROSENBROCK, SCHWEFEL = range(6)
+FN_IDS = {"sphere": SPHERE, "ackley": ACKLEY, "rastrigin": RASTRIGIN, "griewank": GRIEWANK,
+          "rosenbrock": ROSENBROCK, "schwefel": SCHWEFEL}
+PSO, CSO = 0, 1
+OK, EINVAL, EHIP, ENOSPC, EALIGN = 0, -1, -2, -3, -4
+MAX_D = 32768
+
+# every symbol include/evox.h declares
+EXPORTS = (
+    "evox_scratch_bytes", "evox_state_create", "evox_state_destroy", "evox_eval", "evox_eval_ld",
+    "evox_eval_argmin_scratch_bytes", "evox_eval_argmin", "evox_pso_step", "evox_cso_step",
+    "evox_cso_refresh", "evox_best", "evox_generation", "evox_row_layout", "evox_philox_fill",
+    "evox_profile", "evox_profile_read", "evox_strerror", "evox_last_error",
+)
+
+
+class EvoxError(RuntimeError):
+    def __init__(self, code, msg):
+        super().__init__(f"evox error {code}: {msg}")
+        self.code = code
+
+
+class Params(ctypes.Structure):
+    _fields_ = [
+        ("algo", ctypes.c_int32), ("fn_id", ctypes.c_int32),
+        ("N", ctypes.c_int64), ("D", ctypes.c_int64), ("ldx", ctypes.c_int64),
+        ("lb", ctypes.c_float), ("ub", ctypes.c_float),
+        ("v_lo", ctypes.c_float), ("v_hi", ctypes.c_float),
+        ("w", ctypes.c_float), ("c1", ctypes.c_float), ("c2", ctypes.c_float),
+        ("phi", ctypes.c_float), ("vmax", ctypes.c_float),
+        ("clamp_x", ctypes.c_int32),
+        ("seed", ctypes.c_uint64),
+    ]
+
+
+class Buffers(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in ("x", "v", "pbest", "pfit", "fit", "gbest", "xbar")] + [
+        ("scratch", ctypes.c_void_p), ("scratch_bytes", ctypes.c_size_t)]
+
+
+_lib = None
+
+
+def lib():
+    """The loaded libevox.so (raises if it is not built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with "
+                               "`python paper_2301_12457_amd/build.py` (no fallback exists)")
+        L = ctypes.CDLL(LIB_PATH)
+        P, i32, i64, u32, u64, sz = (ctypes.c_void_p, ctypes.c_int, ctypes.c_int64,
+                                     ctypes.c_uint32, ctypes.c_uint64, ctypes.c_size_t)
+        sig = {
+            "evox_scratch_bytes": ([P], sz),
+            "evox_state_create": ([P, P, P, P], i32),
+            "evox_state_destroy": ([P], i32),
+            "evox_eval": ([i32, P, i64, i64, P, P], i32),
+            "evox_eval_ld": ([i32, P, i64, i64, i64, P, P], i32),
+            "evox_eval_argmin_scratch_bytes": ([i64], sz),
+            "evox_eval_argmin": ([i32, P, i64, i64, i64, P, P, P, P, sz, P], i32),
+            "evox_pso_step": ([P, i64], i32),
+            "evox_cso_step": ([P, i64], i32),
+            "evox_cso_refresh": ([P, i32], i32),
+            "evox_best": ([P, P, P, P], i32),
+            "evox_generation": ([P], i64),
+            "evox_row_layout": ([i64, P, P], i32),
+            "evox_philox_fill": ([u64, u32, u32, u32, i64, P, P], i32),
+            "evox_profile": ([P, i32], i32),
+            "evox_profile_read": ([P, P, P, P], i32),
+            "evox_strerror": ([i32], ctypes.c_char_p),
+            "evox_last_error": ([], ctypes.c_char_p),
+        }
+        for name, (args, res) in sig.items():
+            f = getattr(L, name)
+            f.argtypes = args
+            f.restype = res
+        _lib = L
+    return _lib
+
+
+def _check(rc):
+    if rc != OK:
+        raise EvoxError(rc, lib().evox_last_error().decode())
+    return rc
+
+
+def _stream(stream=None):
+    import torch
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _ptr(t):
+    return ctypes.c_void_p(t.data_ptr()) if t is not None else None
+
+
+def row_layout(D):
+    g, n = ctypes.c_int32(0), ctypes.c_int32(0)
+    _check(lib().evox_row_layout(D, ctypes.byref(g), ctypes.byref(n)))
+    return g.value, n.value
+
+
+def evox_eval(fn_id, X, out, stream=None):
+    """out[i] = F(X[i]) on the GPU (X: contiguous [N, D] float32 device tensor)."""
+    assert X.dim() == 2 and X.is_contiguous()
+    _check(lib().evox_eval(fn_id, _ptr(X), X.shape[0], X.shape[1], _ptr(out), _stream(stream)))
+    return out
+
+
+def evox_eval_ld(fn_id, X, N, D, ldx, out, stream=None):
+    _check(lib().evox_eval_ld(fn_id, _ptr(X), N, D, ldx, _ptr(out), _stream(stream)))
+    return out
+
+
+def evox_eval_argmin(fn_id, X, N, D, ldx, out, best_fit, best_idx, scratch, stream=None):
+    """Fitness of every row plus (best_fit[0], best_idx[0]) = argmin, on the GPU."""
+    _check(lib().evox_eval_argmin(fn_id, _ptr(X), N, D, ldx, _ptr(out), _ptr(best_fit),
+                                  _ptr(best_idx), _ptr(scratch), scratch.numel() * scratch.element_size(),
+                                  _stream(stream)))
+    return out
+
+
+def evox_eval_argmin_scratch_bytes(N):
+    return int(lib().evox_eval_argmin_scratch_bytes(N))
+
+
+def evox_philox_fill(seed, c1, c2, c3, n_ctr, out, stream=None):
+    _check(lib().evox_philox_fill(seed, c1, c2, c3, n_ctr, _ptr(out), _stream(stream)))
+    return out
+
+
+def pitch(D):
+    return (D + 3) // 4 * 4
+
+
+def make_params(algo, fn_id, N, D, lb, ub, v_lo=0.0, v_hi=0.0, w=0.6, c1=1.5, c2=1.5, phi=0.1,
+                vmax=0.0, clamp_x=0, seed=0, ldx=None):
+    return Params(algo=algo, fn_id=fn_id, N=N, D=D, ldx=pitch(D) if ldx is None else ldx,
+                  lb=lb, ub=ub, v_lo=v_lo, v_hi=v_hi, w=w, c1=c1, c2=c2, phi=phi, vmax=vmax,
+                  clamp_x=clamp_x, seed=seed)
+
+
+def evox_scratch_bytes(params):
+    return int(lib().evox_scratch_bytes(ctypes.byref(params)))
+
+
+class Swarm:
+    """A PSO or CSO state over torch-allocated device buffers.
+
+    x, v (and pbest) are [N, ldx] float32 tensors whose first D columns are the
+    population; pfit / fit are [N]; gbest / xbar are [ldx].
+    """
+
+    def __init__(self, params: Params, device="cuda", stream=None):
+        import torch
+        self.P = params
+        self.stream = stream if stream is not None else torch.cuda.current_stream(device)
+        N, ldx = params.N, params.ldx
+        f32 = dict(dtype=torch.float32, device=device)
+        self.x = torch.empty((N, ldx), **f32)
+        self.v = torch.empty((N, ldx), **f32)
+        if params.algo == PSO:
+            self.pbest = torch.empty((N, ldx), **f32)
+            self.pfit = torch.empty((N,), **f32)
+            self.gbest = torch.empty((ldx,), **f32)
+            self.fit = torch.empty((N,), **f32)
+            self.xbar = None
+        else:
+            self.pbest = self.pfit = self.gbest = None
+            self.fit = torch.empty((N,), **f32)
+            self.xbar = torch.empty((ldx,), **f32)
+        nbytes = evox_scratch_bytes(params)
+        if nbytes == 0:
+            _check(EINVAL)
+        self.scratch = torch.empty((nbytes + 255) // 256 * 256 // 4, dtype=torch.int32, device=device)
+        self.buffers = Buffers(x=_ptr(self.x), v=_ptr(self.v), pbest=_ptr(self.pbest),
+                               pfit=_ptr(self.pfit), fit=_ptr(self.fit), gbest=_ptr(self.gbest),
+                               xbar=_ptr(self.xbar), scratch=_ptr(self.scratch),
+                               scratch_bytes=self.scratch.numel() * 4)
+        self.handle = ctypes.c_void_p()
+        _check(lib().evox_state_create(ctypes.byref(self.P), ctypes.byref(self.buffers),
+                                       _stream(self.stream), ctypes.byref(self.handle)))
+
+    def __del__(self):
+        h = getattr(self, "handle", None)
+        if h and _lib is not None:
+            _lib.evox_state_destroy(h)
+            self.handle = None
+
+    @property
+    def D(self):
+        return self.P.D
+
+    @property
+    def t(self):
+        return int(lib().evox_generation(self.handle))
+
+    def step(self, n_gens=1):
+        if self.P.algo == PSO:
+            _check(lib().evox_pso_step(self.handle, n_gens))
+        else:
+            _check(lib().evox_cso_step(self.handle, n_gens))
+
+    def refresh(self, refit=True):
+        _check(lib().evox_cso_refresh(self.handle, 1 if refit else 0))
+
+    def best(self, with_x=False):
+        import numpy as np
+        f = ctypes.c_float(0.0)
+        i = ctypes.c_int64(0)
+        xb = np.zeros(self.P.D, np.float32) if with_x else None
+        _check(lib().evox_best(self.handle, ctypes.byref(f), ctypes.byref(i),
+                               xb.ctypes.data_as(ctypes.c_void_p) if with_x else None))
+        return (f.value, i.value, xb) if with_x else (f.value, i.value)
+
+    def profile(self, enable):
+        _check(lib().evox_profile(self.handle, 1 if enable else 0))
+
+    def profile_read(self):
+        ms, n, imp = ctypes.c_double(0), ctypes.c_int64(0), ctypes.c_int64(0)
+        _check(lib().evox_profile_read(self.handle, ctypes.byref(ms), ctypes.byref(n),
+                                       ctypes.byref(imp)))
+        return ms.value, n.value, imp.value
+
+    def view(self, name):
+        """The [N, D] (or [D]) part of a buffer, without the padding columns."""
+        t = getattr(self, name)
+        return t[..., :self.P.D]

@@ -1,0 +1,538 @@
+// C ABI of the gfx950 population-optimizer hot path (include/evox.h):
+// validation, scratch planning, and the launch sequences of one generation.
+#include "evox.h"
+
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <limits>
+#include <utility>
+#include <vector>
+
+#include "evox_launch.hpp"
+
+using namespace evox;
+
+namespace {
+
+thread_local char g_err[512] = "";
+
+int fail(int code, const char *fmt, ...)
+{
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_err, sizeof g_err, fmt, ap);
+    va_end(ap);
+    return code;
+}
+
+int hip_fail(hipError_t e, const char *what)
+{
+    return fail(EVOX_EHIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+bool aligned16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
+size_t round256(size_t n) { return (n + 255) & ~(size_t)255; }
+
+// Buckets for the pairing sort: about 8-16 individuals per bucket.
+int perm_bits(int64_t N)
+{
+    int bits = 0;
+    while ((N >> bits) > 16 && bits < 20) ++bits;
+    return bits;
+}
+
+// Per-block fp64 column-sum rows of the CSO kernels: at most 2^23 doubles.
+int cso_grid_cap(int64_t ldx)
+{
+    int64_t cap = ((int64_t)1 << 23) / ldx;
+    if (cap > kGridCap) cap = kGridCap;
+    if (cap < 64) cap = 64;
+    return (int)cap;
+}
+
+int grid_for(int64_t groups, int G, int cap)
+{
+    const int64_t rpb = block_for(G) / G;
+    int64_t g = (groups + rpb - 1) / rpb;
+    if (g > cap) g = cap;
+    if (g < 1) g = 1;
+    return (int)g;
+}
+
+struct Plan {
+    int G = 0, nit = 0, grid = 0, cso_grid = 0, colsum_grid = 0, bits = 0;
+    size_t best = 0, pval = 0, pidx = 0, pcnt = 0;
+    size_t hist = 0, offs = 0, cursor = 0, tkey = 0, tidx = 0, perm = 0, xsum = 0;
+    size_t total = 0;
+};
+
+int make_plan(const evox_params *P, Plan *pl)
+{
+    if (!P) return fail(EVOX_EINVAL, "params is null");
+    if (P->algo != EVOX_PSO && P->algo != EVOX_CSO) return fail(EVOX_EINVAL, "unknown algo %d", P->algo);
+    if (P->fn_id < 0 || P->fn_id >= FN_COUNT) return fail(EVOX_EINVAL, "unknown fn_id %d", P->fn_id);
+    const int64_t nmin = P->algo == EVOX_CSO ? 2 : 1;
+    if (P->N < nmin || P->N >= ((int64_t)1 << 31))
+        return fail(EVOX_EINVAL, "N = %lld out of range [%lld, 2^31)", (long long)P->N, (long long)nmin);
+    if (P->D < 1 || P->D > EVOX_MAX_D)
+        return fail(EVOX_EINVAL, "D = %lld out of range [1, %d]", (long long)P->D, EVOX_MAX_D);
+    if (P->ldx < P->D || (P->ldx & 3))
+        return fail(EVOX_EINVAL, "ldx = %lld must be >= D and a multiple of 4", (long long)P->ldx);
+    Plan p;
+    if (!row_layout(P->D, &p.G, &p.nit)) return fail(EVOX_EINVAL, "no row layout for D = %lld", (long long)P->D);
+    p.grid = grid_for(P->N, p.G, kGridCap);
+    size_t off = 0;
+    auto take = [&](size_t bytes) {
+        const size_t at = off;
+        off = round256(off + bytes);
+        return at;
+    };
+    p.best = take(sizeof(DevBest));
+    p.pval = take(sizeof(float) * kGridCap);
+    p.pidx = take(sizeof(int64_t) * kGridCap);
+    p.pcnt = take(sizeof(uint32_t) * kGridCap);
+    if (P->algo == EVOX_CSO) {
+        const int cap = cso_grid_cap(P->ldx);
+        p.cso_grid = grid_for(P->N / 2 + (P->N & 1), p.G, cap);
+        p.colsum_grid = grid_for(P->N, p.G, cap);
+        p.bits = perm_bits(P->N);
+        const size_t nb = (size_t)1 << p.bits;
+        p.hist = take(4 * nb);
+        p.offs = take(4 * (nb + 1));
+        p.cursor = take(4 * nb);
+        p.tkey = take(4 * (size_t)P->N);
+        p.tidx = take(4 * (size_t)P->N);
+        p.perm = take(4 * (size_t)P->N);
+        p.xsum = take(sizeof(double) * (size_t)cap * (size_t)P->ldx);
+    }
+    p.total = off;
+    *pl = p;
+    return EVOX_OK;
+}
+
+}  // namespace
+
+struct evox_state {
+    evox_params P;
+    evox_buffers B;
+    hipStream_t stream;
+    int64_t t;
+    Plan pl;
+    uint32_t k0, k1;
+    DevBest *best;
+    float *pval;
+    int64_t *pidx;
+    uint32_t *pcnt;
+    uint32_t *hist, *offs, *cursor, *tkey, *tidx, *perm;
+    double *xsum;
+    // profiling of the fused generation kernel
+    bool prof;
+    std::vector<std::pair<hipEvent_t, hipEvent_t>> ev;
+    size_t ev_used;
+    uint64_t improved_base;
+};
+
+namespace {
+
+template <typename T>
+T *at(void *base, size_t off)
+{
+    return reinterpret_cast<T *>(static_cast<char *>(base) + off);
+}
+
+// Enqueue `launch` bracketed by profiling events when enabled.
+template <typename F>
+hipError_t timed(evox_state *s, F &&launch)
+{
+    if (!s->prof) return launch();
+    if (s->ev_used == s->ev.size()) {
+        hipEvent_t a, b;
+        hipError_t e = hipEventCreate(&a);
+        if (e != hipSuccess) return e;
+        e = hipEventCreate(&b);
+        if (e != hipSuccess) return e;
+        s->ev.emplace_back(a, b);
+    }
+    auto &pr = s->ev[s->ev_used++];
+    hipError_t e = hipEventRecord(pr.first, s->stream);
+    if (e != hipSuccess) return e;
+    e = launch();
+    if (e != hipSuccess) return e;
+    return hipEventRecord(pr.second, s->stream);
+}
+
+hipError_t best_init(evox_state *s, float f, int64_t i) { return launch_best_init(s->best, f, i, s->stream); }
+
+PsoArgs pso_args(evox_state *s)
+{
+    const evox_params &P = s->P;
+    PsoArgs a{};
+    a.x = s->B.x;
+    a.v = s->B.v;
+    a.p = s->B.pbest;
+    a.pf = s->B.pfit;
+    a.fit = s->B.fit;
+    a.gbest = s->B.gbest;
+    a.N = P.N;
+    a.D = P.D;
+    a.ldx = P.ldx;
+    a.w = P.w;
+    a.c1 = P.c1;
+    a.c2 = P.c2;
+    a.vmax = P.vmax;
+    a.lb = P.lb;
+    a.ub = P.ub;
+    a.vclamp = P.vmax > 0.0f;
+    a.xclamp = P.clamp_x != 0;
+    a.k0 = s->k0;
+    a.k1 = s->k1;
+    a.t = 0;
+    a.pval = s->pval;
+    a.pidx = s->pidx;
+    a.pcnt = s->pcnt;
+    return a;
+}
+
+// CSO: fit (optional), swarm mean and best of the current positions.
+int cso_refresh(evox_state *s, bool refit)
+{
+    const evox_params &P = s->P;
+    const Plan &pl = s->pl;
+    hipError_t e;
+    if (refit) {
+        EvalArgs ea{s->B.x, P.N, P.D, P.ldx, s->B.fit, nullptr, nullptr};
+        if ((e = launch_eval(P.fn_id, pl.G, true, ea, pl.grid, s->stream)) != hipSuccess)
+            return hip_fail(e, "evaluate");
+    }
+    if ((e = launch_colsum(pl.G, s->B.x, P.N, P.D, P.ldx, s->xsum, pl.colsum_grid, s->stream)) != hipSuccess)
+        return hip_fail(e, "column sums");
+    if ((e = launch_cso_mean(s->xsum, pl.colsum_grid, P.N, P.D, P.ldx, s->B.xbar, s->stream)) != hipSuccess)
+        return hip_fail(e, "swarm mean");
+    const int ng = argmin_partials_grid(P.N);
+    if ((e = launch_argmin_partials(s->B.fit, P.N, s->pval, s->pidx, ng, s->stream)) != hipSuccess)
+        return hip_fail(e, "select");
+    if ((e = launch_select(s->pval, s->pidx, nullptr, ng, nullptr, 0, nullptr, s->best, nullptr, nullptr,
+                           s->stream)) != hipSuccess)
+        return hip_fail(e, "select");
+    return EVOX_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t evox_scratch_bytes(const evox_params *params)
+{
+    Plan pl;
+    if (make_plan(params, &pl) != EVOX_OK) return 0;
+    return pl.total;
+}
+
+int evox_state_create(const evox_params *params, const evox_buffers *b, void *hip_stream,
+                      evox_state **out)
+{
+    if (!out) return fail(EVOX_EINVAL, "out is null");
+    *out = nullptr;
+    Plan pl;
+    int rc = make_plan(params, &pl);
+    if (rc != EVOX_OK) return rc;
+    const evox_params &P = *params;
+    if (!b) return fail(EVOX_EINVAL, "buffers is null");
+    if (!b->x || !b->v || !b->scratch) return fail(EVOX_EINVAL, "x, v and scratch are required");
+    if (P.algo == EVOX_PSO && (!b->pbest || !b->pfit || !b->gbest))
+        return fail(EVOX_EINVAL, "PSO needs pbest, pfit and gbest");
+    if (P.algo == EVOX_CSO && (!b->fit || !b->xbar)) return fail(EVOX_EINVAL, "CSO needs fit and xbar");
+    const void *ptrs[] = {b->x, b->v, b->pbest, b->pfit, b->fit, b->gbest, b->xbar};
+    for (const void *p : ptrs)
+        if (p && !aligned16(p)) return fail(EVOX_EALIGN, "buffer %p is not 16-byte aligned", p);
+    if (((uintptr_t)b->scratch & 255u) != 0) return fail(EVOX_EALIGN, "scratch is not 256-byte aligned");
+    if (b->scratch_bytes < pl.total)
+        return fail(EVOX_ENOSPC, "scratch has %zu bytes, needs %zu", b->scratch_bytes, pl.total);
+
+    evox_state *s = new evox_state();
+    s->P = P;
+    s->B = *b;
+    s->stream = (hipStream_t)hip_stream;
+    s->t = 0;
+    s->pl = pl;
+    s->k0 = (uint32_t)P.seed;
+    s->k1 = (uint32_t)(P.seed >> 32);
+    s->best = at<DevBest>(b->scratch, pl.best);
+    s->pval = at<float>(b->scratch, pl.pval);
+    s->pidx = at<int64_t>(b->scratch, pl.pidx);
+    s->pcnt = at<uint32_t>(b->scratch, pl.pcnt);
+    s->hist = s->offs = s->cursor = s->tkey = s->tidx = s->perm = nullptr;
+    s->xsum = nullptr;
+    if (P.algo == EVOX_CSO) {
+        s->hist = at<uint32_t>(b->scratch, pl.hist);
+        s->offs = at<uint32_t>(b->scratch, pl.offs);
+        s->cursor = at<uint32_t>(b->scratch, pl.cursor);
+        s->tkey = at<uint32_t>(b->scratch, pl.tkey);
+        s->tidx = at<uint32_t>(b->scratch, pl.tidx);
+        s->perm = at<uint32_t>(b->scratch, pl.perm);
+        s->xsum = at<double>(b->scratch, pl.xsum);
+    }
+    s->prof = false;
+    s->ev_used = 0;
+    s->improved_base = 0;
+
+    hipError_t e;
+    InitArgs ia{b->x, b->v, P.algo == EVOX_PSO ? b->pbest : nullptr, P.N, P.D, P.ldx, P.lb, P.ub,
+                P.v_lo, P.v_hi, P.v_lo == 0.0f && P.v_hi == 0.0f, s->k0, s->k1};
+    if ((e = launch_init(ia, s->stream)) != hipSuccess) {
+        delete s;
+        return hip_fail(e, "init");
+    }
+    if (P.algo == EVOX_PSO) {
+        if ((e = best_init(s, std::numeric_limits<float>::infinity(), 0)) != hipSuccess ||
+            (e = launch_fill(b->pfit, P.N, std::numeric_limits<float>::infinity(), s->stream)) != hipSuccess ||
+            (e = launch_copy_row(b->pbest, b->gbest, P.ldx, s->stream)) != hipSuccess) {
+            delete s;
+            return hip_fail(e, "init");
+        }
+    } else {
+        const size_t nb = (size_t)1 << pl.bits;
+        if ((e = launch_zero_u32(s->hist, (int64_t)nb, s->stream)) != hipSuccess ||
+            (e = best_init(s, std::numeric_limits<float>::infinity(), 0)) != hipSuccess) {
+            delete s;
+            return hip_fail(e, "init");
+        }
+        rc = cso_refresh(s, true);
+        if (rc != EVOX_OK) {
+            delete s;
+            return rc;
+        }
+    }
+    *out = s;
+    return EVOX_OK;
+}
+
+int evox_state_destroy(evox_state *s)
+{
+    if (!s) return fail(EVOX_EINVAL, "state is null");
+    for (auto &pr : s->ev) {
+        hipEventDestroy(pr.first);
+        hipEventDestroy(pr.second);
+    }
+    delete s;
+    return EVOX_OK;
+}
+
+static int eval_common(int fn_id, const float *X, int64_t N, int64_t D, int64_t ldx, float *out,
+                       float *pval, int64_t *pidx, hipStream_t st, int *grid_out)
+{
+    if (fn_id < 0 || fn_id >= FN_COUNT) return fail(EVOX_EINVAL, "unknown fn_id %d", fn_id);
+    if (N < 0 || N >= ((int64_t)1 << 31)) return fail(EVOX_EINVAL, "N = %lld out of range", (long long)N);
+    if (D < 1 || D > EVOX_MAX_D) return fail(EVOX_EINVAL, "D = %lld out of range [1, %d]", (long long)D, EVOX_MAX_D);
+    if (ldx < D) return fail(EVOX_EINVAL, "ldx = %lld < D", (long long)ldx);
+    if (N > 0 && (!X || !out)) return fail(EVOX_EINVAL, "X and out are required");
+    int G, nit;
+    if (!row_layout(D, &G, &nit)) return fail(EVOX_EINVAL, "no row layout for D = %lld", (long long)D);
+    const int grid = grid_for(N, G, kGridCap);
+    if (grid_out) *grid_out = grid;
+    if (N == 0) return EVOX_OK;
+    const bool vec = (ldx & 3) == 0 && aligned16(X);
+    EvalArgs a{X, N, D, ldx, out, pval, pidx};
+    hipError_t e = launch_eval(fn_id, G, vec, a, grid, st);
+    if (e != hipSuccess) return hip_fail(e, "evaluate");
+    return EVOX_OK;
+}
+
+int evox_eval(int fn_id, const float *X, int64_t N, int64_t D, float *out, void *hip_stream)
+{
+    return eval_common(fn_id, X, N, D, D, out, nullptr, nullptr, (hipStream_t)hip_stream, nullptr);
+}
+
+int evox_eval_ld(int fn_id, const float *X, int64_t N, int64_t D, int64_t ldx, float *out,
+                 void *hip_stream)
+{
+    return eval_common(fn_id, X, N, D, ldx, out, nullptr, nullptr, (hipStream_t)hip_stream, nullptr);
+}
+
+size_t evox_eval_argmin_scratch_bytes(int64_t)
+{
+    return round256(sizeof(float) * kGridCap) + round256(sizeof(int64_t) * kGridCap);
+}
+
+int evox_eval_argmin(int fn_id, const float *X, int64_t N, int64_t D, int64_t ldx, float *out,
+                     float *best_fit_dev, int64_t *best_idx_dev, void *scratch, size_t scratch_bytes,
+                     void *hip_stream)
+{
+    if (N < 1) return fail(EVOX_EINVAL, "N = %lld: selection needs at least one row", (long long)N);
+    if (!best_fit_dev || !best_idx_dev || !scratch) return fail(EVOX_EINVAL, "best outputs and scratch are required");
+    if (((uintptr_t)scratch & 255u) != 0) return fail(EVOX_EALIGN, "scratch is not 256-byte aligned");
+    if (scratch_bytes < evox_eval_argmin_scratch_bytes(N))
+        return fail(EVOX_ENOSPC, "scratch has %zu bytes, needs %zu", scratch_bytes, evox_eval_argmin_scratch_bytes(N));
+    float *pval = at<float>(scratch, 0);
+    int64_t *pidx = at<int64_t>(scratch, round256(sizeof(float) * kGridCap));
+    int grid = 0;
+    hipStream_t st = (hipStream_t)hip_stream;
+    int rc = eval_common(fn_id, X, N, D, ldx, out, pval, pidx, st, &grid);
+    if (rc != EVOX_OK) return rc;
+    hipError_t e = launch_select(pval, pidx, nullptr, grid, nullptr, 0, nullptr, nullptr, best_fit_dev,
+                                 best_idx_dev, st);
+    if (e != hipSuccess) return hip_fail(e, "select");
+    return EVOX_OK;
+}
+
+int evox_pso_step(evox_state *s, int64_t n_gens)
+{
+    if (!s) return fail(EVOX_EINVAL, "state is null");
+    if (s->P.algo != EVOX_PSO) return fail(EVOX_EINVAL, "evox_pso_step on a CSO state");
+    if (n_gens < 0) return fail(EVOX_EINVAL, "n_gens = %lld < 0", (long long)n_gens);
+    if (s->t + n_gens >= ((int64_t)1 << 32)) return fail(EVOX_EINVAL, "generation counter would pass 2^32");
+    if (n_gens == 0) return EVOX_OK;
+    const Plan &pl = s->pl;
+    const int fn = s->P.fn_id;
+    PsoArgs a = pso_args(s);
+    hipError_t e;
+    // generation t: evaluate x_t, personal and global bests
+    if ((e = launch_pso(fn, pl.G, PSO_EVAL, a, pl.grid, s->stream)) != hipSuccess) return hip_fail(e, "pso eval");
+    if ((e = launch_select(s->pval, s->pidx, s->pcnt, pl.grid, s->B.pbest, s->P.ldx, s->B.gbest, s->best,
+                           nullptr, nullptr, s->stream)) != hipSuccess)
+        return hip_fail(e, "select");
+    for (int64_t k = 1; k < n_gens; ++k) {
+        a.t = (uint32_t)(s->t + k - 1);  // move of generation t+k-1, evaluation of t+k
+        e = timed(s, [&] { return launch_pso(fn, pl.G, PSO_FUSED, a, pl.grid, s->stream); });
+        if (e != hipSuccess) return hip_fail(e, "pso generation");
+        if ((e = launch_select(s->pval, s->pidx, s->pcnt, pl.grid, s->B.pbest, s->P.ldx, s->B.gbest,
+                               s->best, nullptr, nullptr, s->stream)) != hipSuccess)
+            return hip_fail(e, "select");
+    }
+    a.t = (uint32_t)(s->t + n_gens - 1);
+    if ((e = launch_pso(fn, pl.G, PSO_MOVE, a, pl.grid, s->stream)) != hipSuccess) return hip_fail(e, "pso move");
+    s->t += n_gens;
+    return EVOX_OK;
+}
+
+int evox_cso_step(evox_state *s, int64_t n_gens)
+{
+    if (!s) return fail(EVOX_EINVAL, "state is null");
+    if (s->P.algo != EVOX_CSO) return fail(EVOX_EINVAL, "evox_cso_step on a PSO state");
+    if (n_gens < 0) return fail(EVOX_EINVAL, "n_gens = %lld < 0", (long long)n_gens);
+    if (s->t + n_gens >= ((int64_t)1 << 32)) return fail(EVOX_EINVAL, "generation counter would pass 2^32");
+    const evox_params &P = s->P;
+    const Plan &pl = s->pl;
+    hipError_t e;
+    for (int64_t k = 0; k < n_gens; ++k) {
+        const uint32_t t = (uint32_t)(s->t + k);
+        PermArgs pa{P.N, pl.bits, s->k0, s->k1, t, s->hist, s->offs, s->cursor, s->tkey, s->tidx, s->perm};
+        if ((e = launch_perm(pa, s->stream)) != hipSuccess) return hip_fail(e, "pairing");
+        CsoArgs ca{s->B.x, s->B.v, s->B.fit, s->B.xbar, s->perm, P.N, P.D, P.ldx, P.phi, P.lb, P.ub,
+                   P.clamp_x != 0, s->k0, s->k1, t, s->pval, s->pidx, s->xsum};
+        e = timed(s, [&] { return launch_cso(P.fn_id, pl.G, ca, pl.cso_grid, s->stream); });
+        if (e != hipSuccess) return hip_fail(e, "cso generation");
+        if ((e = launch_cso_mean(s->xsum, pl.cso_grid, P.N, P.D, P.ldx, s->B.xbar, s->stream)) != hipSuccess)
+            return hip_fail(e, "swarm mean");
+        if ((e = launch_select(s->pval, s->pidx, nullptr, pl.cso_grid, nullptr, 0, nullptr, s->best, nullptr,
+                               nullptr, s->stream)) != hipSuccess)
+            return hip_fail(e, "select");
+    }
+    s->t += n_gens;
+    return EVOX_OK;
+}
+
+int evox_cso_refresh(evox_state *s, int refit)
+{
+    if (!s) return fail(EVOX_EINVAL, "state is null");
+    if (s->P.algo != EVOX_CSO) return fail(EVOX_EINVAL, "evox_cso_refresh on a PSO state");
+    return cso_refresh(s, refit != 0);
+}
+
+int evox_best(evox_state *s, float *best_fit, int64_t *best_idx, float *best_x_host)
+{
+    if (!s) return fail(EVOX_EINVAL, "state is null");
+    DevBest h{};
+    hipError_t e = hipMemcpyAsync(&h, s->best, sizeof h, hipMemcpyDeviceToHost, s->stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(s->stream);
+    if (e != hipSuccess) return hip_fail(e, "read best");
+    if (best_fit) *best_fit = h.f;
+    if (best_idx) *best_idx = h.i;
+    if (best_x_host) {
+        const float *src = s->P.algo == EVOX_PSO ? s->B.gbest : s->B.x + h.i * s->P.ldx;
+        e = hipMemcpyAsync(best_x_host, src, sizeof(float) * (size_t)s->P.D, hipMemcpyDeviceToHost, s->stream);
+        if (e == hipSuccess) e = hipStreamSynchronize(s->stream);
+        if (e != hipSuccess) return hip_fail(e, "read best row");
+    }
+    return EVOX_OK;
+}
+
+int64_t evox_generation(const evox_state *s) { return s ? s->t : -1; }
+
+int evox_row_layout(int64_t D, int32_t *threads_per_row, int32_t *chunks_per_thread)
+{
+    int G, nit;
+    if (!row_layout(D, &G, &nit) || D > EVOX_MAX_D) return fail(EVOX_EINVAL, "no row layout for D = %lld", (long long)D);
+    if (threads_per_row) *threads_per_row = G;
+    if (chunks_per_thread) *chunks_per_thread = nit;
+    return EVOX_OK;
+}
+
+int evox_philox_fill(uint64_t seed, uint32_t c1, uint32_t c2, uint32_t c3, int64_t n_ctr,
+                     uint32_t *out_dev, void *hip_stream)
+{
+    if (n_ctr < 0 || n_ctr > ((int64_t)1 << 32)) return fail(EVOX_EINVAL, "n_ctr out of range");
+    if (n_ctr == 0) return EVOX_OK;
+    if (!out_dev) return fail(EVOX_EINVAL, "out is null");
+    if (!aligned16(out_dev)) return fail(EVOX_EALIGN, "out is not 16-byte aligned");
+    hipError_t e = launch_philox_fill((uint32_t)seed, (uint32_t)(seed >> 32), c1, c2, c3, n_ctr, out_dev,
+                                      (hipStream_t)hip_stream);
+    if (e != hipSuccess) return hip_fail(e, "philox fill");
+    return EVOX_OK;
+}
+
+int evox_profile(evox_state *s, int enable)
+{
+    if (!s) return fail(EVOX_EINVAL, "state is null");
+    if (enable) {
+        s->ev_used = 0;
+        DevBest h{};
+        hipError_t e = hipMemcpyAsync(&h, s->best, sizeof h, hipMemcpyDeviceToHost, s->stream);
+        if (e == hipSuccess) e = hipStreamSynchronize(s->stream);
+        if (e != hipSuccess) return hip_fail(e, "profile start");
+        s->improved_base = h.improved;
+    }
+    s->prof = enable != 0;
+    return EVOX_OK;
+}
+
+int evox_profile_read(evox_state *s, double *fused_ms, int64_t *fused_launches, int64_t *improved_rows)
+{
+    if (!s) return fail(EVOX_EINVAL, "state is null");
+    hipError_t e = hipStreamSynchronize(s->stream);
+    if (e != hipSuccess) return hip_fail(e, "profile read");
+    double ms = 0.0;
+    for (size_t k = 0; k < s->ev_used; ++k) {
+        float m = 0.0f;
+        e = hipEventElapsedTime(&m, s->ev[k].first, s->ev[k].second);
+        if (e != hipSuccess) return hip_fail(e, "event time");
+        ms += m;
+    }
+    DevBest h{};
+    e = hipMemcpy(&h, s->best, sizeof h, hipMemcpyDeviceToHost);
+    if (e != hipSuccess) return hip_fail(e, "profile read");
+    if (fused_ms) *fused_ms = ms;
+    if (fused_launches) *fused_launches = (int64_t)s->ev_used;
+    if (improved_rows) *improved_rows = (int64_t)(h.improved - s->improved_base);
+    return EVOX_OK;
+}
+
+const char *evox_strerror(int code)
+{
+    switch (code) {
+    case EVOX_OK: return "ok";
+    case EVOX_EINVAL: return "invalid argument";
+    case EVOX_EHIP: return "HIP runtime error";
+    case EVOX_ENOSPC: return "scratch buffer too small";
+    case EVOX_EALIGN: return "misaligned pointer or pitch";
+    default: return "unknown error";
+    }
+}
+
+const char *evox_last_error(void) { return g_err; }
+
+}  // extern "C"

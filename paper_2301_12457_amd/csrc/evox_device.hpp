@@ -1,0 +1,345 @@
+// Device-side building blocks of the gfx950 generation kernels: Philox,
+// benchmark-function row reductions, row layout, and the argmin order.
+//
+// Data layout: a population matrix is row-major fp32 with a row pitch ldx
+// (multiple of 4 floats, 16-byte aligned rows).  One row is handled by a
+// group of G consecutive lanes (G a power of two, 4..1024); lane g of the
+// group holds the float4 chunks c = g + G * it, it = 0..MAXIT-1, i.e. the
+// elements 4c..4c+3.  Every wave load instruction therefore reads G * 16
+// contiguous bytes of a row (128-bit loads, fully coalesced), and a row's
+// fitness is a per-lane partial over its chunks followed by a butterfly over
+// the G lanes (DPP/ds_swizzle shuffles) and, for G > 64, an LDS step across
+// the waves of the row.  The reduction order depends only on D, so every
+// kernel that evaluates a row produces bit-identical fitness.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+namespace evox {
+
+enum { FN_SPHERE = 0, FN_ACKLEY, FN_RASTRIGIN, FN_GRIEWANK, FN_ROSENBROCK, FN_SCHWEFEL, FN_COUNT };
+
+// Random-stream ids (fourth Philox counter word).
+enum { STREAM_INIT_X = 0, STREAM_INIT_V = 1, STREAM_PSO = 2, STREAM_CSO = 3, STREAM_PERM = 4 };
+
+constexpr int kBlock = 256;     // threads per block when a row takes <= 256 lanes
+constexpr int kGridCap = 2048;  // blocks per launch at most (8 per CU on 256 CUs)
+constexpr int kMaxG = 1024;
+
+__host__ __device__ constexpr int block_for(int G) { return G > kBlock ? G : kBlock; }
+__host__ __device__ constexpr int maxit_for(int G) { return G == kMaxG ? 8 : 4; }
+
+// Threads per row and chunks per thread for dimension D: the smallest G that
+// needs at most 4 chunks per lane (8 at G = 1024).  Returns false when D is
+// beyond what one row group holds in registers.
+inline bool row_layout(int64_t D, int *G_out, int *nit_out)
+{
+    if (D < 1) return false;
+    const int64_t c4 = (D + 3) / 4;
+    int G = 4;
+    while (G < kMaxG && (c4 + G - 1) / G > 4) G *= 2;
+    const int64_t nit = (c4 + G - 1) / G;
+    if (nit > maxit_for(G)) return false;
+    *G_out = G;
+    *nit_out = (int)nit;
+    return true;
+}
+
+// ---------------------------------------------------------------------------
+// Philox4x32-10 (Salmon, Moraes, Dror, Shaw, SC'11): ten rounds of two
+// 32x32->64 multiplies and key xors, Weyl-incremented key.  Everything stays
+// in registers; the key is wave-uniform (SGPRs).
+// ---------------------------------------------------------------------------
+struct U4 {
+    uint32_t x, y, z, w;
+};
+
+__device__ __forceinline__ U4 philox(uint32_t c0, uint32_t c1, uint32_t c2, uint32_t c3,
+                                     uint32_t k0, uint32_t k1)
+{
+#pragma unroll
+    for (int r = 0; r < 10; ++r) {
+        const uint64_t m0 = (uint64_t)0xD2511F53u * (uint64_t)c0;
+        const uint64_t m1 = (uint64_t)0xCD9E8D57u * (uint64_t)c2;
+        const uint32_t n0 = (uint32_t)(m1 >> 32) ^ c1 ^ k0;
+        const uint32_t n2 = (uint32_t)(m0 >> 32) ^ c3 ^ k1;
+        c1 = (uint32_t)m1;
+        c3 = (uint32_t)m0;
+        c0 = n0;
+        c2 = n2;
+        k0 += 0x9E3779B9u;
+        k1 += 0xBB67AE85u;
+    }
+    return U4{c0, c1, c2, c3};
+}
+
+// Top 24 bits times 2^-24: exact, in [0, 1).
+__device__ __forceinline__ float u01(uint32_t w) { return (float)(w >> 8) * 0x1p-24f; }
+
+__device__ __forceinline__ float comp(const float4 &v, int e)
+{
+    return e == 0 ? v.x : e == 1 ? v.y : e == 2 ? v.z : v.w;
+}
+__device__ __forceinline__ float wcomp(const U4 &v, int e)
+{
+    return u01(e == 0 ? v.x : e == 1 ? v.y : e == 2 ? v.z : v.w);
+}
+
+// ---------------------------------------------------------------------------
+// Trigonometry.  cos(2 pi r) / sin(2 pi r) by exact reduction of r to
+// [-1/2, 1/2] (r - rint(r) is exact in fp32) and the hardware v_cos_f32 /
+// v_sin_f32, whose input is in revolutions.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ float cos_rev(float r)
+{
+    return __builtin_amdgcn_cosf(r - __builtin_rintf(r));
+}
+__device__ __forceinline__ float sin_rev(float r)
+{
+    return __builtin_amdgcn_sinf(r - __builtin_rintf(r));
+}
+
+// ---------------------------------------------------------------------------
+// Benchmark functions as row reductions.  Acc holds up to two partials; the
+// per-element step sees x_j, its right neighbour x_{j+1} (Rosenbrock) and the
+// 0-based index j; combine() merges two lanes' partials; finish() gives F.
+// ---------------------------------------------------------------------------
+struct Acc {
+    float a, b;
+};
+
+template <int FN>
+struct Fn;
+
+template <>
+struct Fn<FN_SPHERE> {  // sum x^2
+    static constexpr bool kNeighbour = false;
+    __device__ static Acc init() { return {0.f, 0.f}; }
+    __device__ static void elem(Acc &s, float x, float, int64_t) { s.a = fmaf(x, x, s.a); }
+    __device__ static Acc combine(Acc p, Acc q) { return {p.a + q.a, 0.f}; }
+    __device__ static float finish(Acc s, int64_t) { return s.a; }
+};
+
+template <>
+struct Fn<FN_ACKLEY> {  // a = sum x^2, b = sum cos(2 pi x)
+    static constexpr bool kNeighbour = false;
+    __device__ static Acc init() { return {0.f, 0.f}; }
+    __device__ static void elem(Acc &s, float x, float, int64_t)
+    {
+        s.a = fmaf(x, x, s.a);
+        s.b += cos_rev(x);
+    }
+    __device__ static Acc combine(Acc p, Acc q) { return {p.a + q.a, p.b + q.b}; }
+    __device__ static float finish(Acc s, int64_t D)
+    {
+        const float n = (float)D;
+        const float e1 = expf(-0.2f * sqrtf(s.a / n));
+        const float e2 = expf(s.b / n);
+        return (20.0f - 20.0f * e1) + (2.71828182845904523536f - e2);
+    }
+};
+
+template <>
+struct Fn<FN_RASTRIGIN> {  // a = sum (x^2 - 10 cos(2 pi x))
+    static constexpr bool kNeighbour = false;
+    __device__ static Acc init() { return {0.f, 0.f}; }
+    __device__ static void elem(Acc &s, float x, float, int64_t)
+    {
+        s.a += fmaf(x, x, -10.0f * cos_rev(x));
+    }
+    __device__ static Acc combine(Acc p, Acc q) { return {p.a + q.a, 0.f}; }
+    __device__ static float finish(Acc s, int64_t D) { return 10.0f * (float)D + s.a; }
+};
+
+template <>
+struct Fn<FN_GRIEWANK> {  // a = sum x^2, b = prod cos(x / sqrt(j + 1))
+    static constexpr bool kNeighbour = false;
+    __device__ static Acc init() { return {0.f, 1.f}; }
+    __device__ static void elem(Acc &s, float x, float, int64_t j)
+    {
+        s.a = fmaf(x, x, s.a);
+        s.b *= cosf(x * rsqrtf((float)(j + 1)));
+    }
+    __device__ static Acc combine(Acc p, Acc q) { return {p.a + q.a, p.b * q.b}; }
+    __device__ static float finish(Acc s, int64_t) { return (1.0f - s.b) + s.a * (1.0f / 4000.0f); }
+};
+
+template <>
+struct Fn<FN_ROSENBROCK> {  // sum_{j < D-1} 100 (x_{j+1} - x_j^2)^2 + (1 - x_j)^2
+    static constexpr bool kNeighbour = true;
+    __device__ static Acc init() { return {0.f, 0.f}; }
+    __device__ static void elem(Acc &s, float x, float xn, int64_t)
+    {
+        const float d = fmaf(-x, x, xn);  // one rounding of x_{j+1} - x_j^2
+        const float o = 1.0f - x;
+        s.a += fmaf(100.0f * d, d, o * o);
+    }
+    __device__ static Acc combine(Acc p, Acc q) { return {p.a + q.a, 0.f}; }
+    __device__ static float finish(Acc s, int64_t) { return s.a; }
+};
+
+template <>
+struct Fn<FN_SCHWEFEL> {  // a = sum x sin(sqrt|x|)
+    static constexpr bool kNeighbour = false;
+    __device__ static Acc init() { return {0.f, 0.f}; }
+    __device__ static void elem(Acc &s, float x, float, int64_t)
+    {
+        const float r = sqrtf(fabsf(x)) * 0.159154943091895335769f;  // revolutions
+        s.a = fmaf(x, sin_rev(r), s.a);
+    }
+    __device__ static Acc combine(Acc p, Acc q) { return {p.a + q.a, 0.f}; }
+    __device__ static float finish(Acc s, int64_t D) { return 418.9829f * (float)D - s.a; }
+};
+
+// ---------------------------------------------------------------------------
+// Row fitness from the registers of a G-lane group.  xr[it] holds chunk
+// g + G*it (zeros outside the row).  All lanes of the group return F.
+// nbr: LDS scratch of block_for(G) * MAXIT floats, used for the Rosenbrock
+// neighbour when a row spans several waves; red: LDS of block_for(G)/64 * 2
+// floats for the cross-wave step.  Must be reached by every thread of the
+// block (it contains barriers when G > 64).
+// ---------------------------------------------------------------------------
+template <int G>
+__device__ __forceinline__ float shfl_xor_g(float v, int m)
+{
+    return __shfl_xor(v, m, G < 64 ? G : 64);
+}
+
+template <int FN, int G, int MAXIT>
+__device__ __forceinline__ float row_fitness(const float4 (&xr)[MAXIT], int g, int64_t D,
+                                             float *nbr, float *red)
+{
+    using F = Fn<FN>;
+    const int tid = threadIdx.x;
+    // right neighbour of the last element of each chunk
+    float nb[MAXIT];
+    if constexpr (F::kNeighbour) {
+        if constexpr (G <= 64) {
+#pragma unroll
+            for (int it = 0; it < MAXIT; ++it) {
+                const float same = __shfl(xr[it].x, (g + 1) & (G - 1), G);
+                const float next = it + 1 < MAXIT ? __shfl(xr[it + 1 < MAXIT ? it + 1 : it].x, 0, G)
+                                                  : 0.0f;
+                nb[it] = g == G - 1 ? next : same;
+            }
+        } else {
+            const int base = (tid / G) * G * MAXIT;
+#pragma unroll
+            for (int it = 0; it < MAXIT; ++it) nbr[base + it * G + g] = xr[it].x;
+            __syncthreads();
+#pragma unroll
+            for (int it = 0; it < MAXIT; ++it) {
+                const int k = it * G + g + 1;
+                nb[it] = k < G * MAXIT ? nbr[base + k] : 0.0f;
+            }
+            __syncthreads();
+        }
+    } else {
+#pragma unroll
+        for (int it = 0; it < MAXIT; ++it) nb[it] = 0.0f;
+    }
+
+    Acc s = F::init();
+#pragma unroll
+    for (int it = 0; it < MAXIT; ++it) {
+        const int64_t j0 = 4 * ((int64_t)g + (int64_t)G * it);
+        const float4 v = xr[it];
+        const float n4[4] = {v.y, v.z, v.w, nb[it]};
+        const int64_t lim = F::kNeighbour ? D - 1 : D;  // last element has no pair
+        if (j0 + 3 < lim) {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) F::elem(s, comp(v, e), n4[e], j0 + e);
+        } else {
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+                if (j0 + e < lim) F::elem(s, comp(v, e), n4[e], j0 + e);
+        }
+    }
+    // butterfly over the lanes of the row inside one wave
+#pragma unroll
+    for (int m = (G < 64 ? G : 64) / 2; m >= 1; m >>= 1) {
+        Acc o{shfl_xor_g<G>(s.a, m), shfl_xor_g<G>(s.b, m)};
+        s = F::combine(s, o);
+    }
+    if constexpr (G > 64) {
+        constexpr int W = G / 64;  // waves per row
+        const int wave = tid / 64;
+        if ((tid & 63) == 0) {
+            red[2 * wave] = s.a;
+            red[2 * wave + 1] = s.b;
+        }
+        __syncthreads();
+        const int w0 = (wave / W) * W;
+        Acc t{red[2 * w0], red[2 * w0 + 1]};
+#pragma unroll
+        for (int q = 1; q < W; ++q) t = F::combine(t, Acc{red[2 * (w0 + q)], red[2 * (w0 + q) + 1]});
+        __syncthreads();
+        s = t;
+    }
+    return F::finish(s, D);
+}
+
+// ---------------------------------------------------------------------------
+// Selection order: smaller value, then lower index; -0 == +0; NaN after all
+// numbers.  A total order, so any reduction tree gives the same winner.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ bool cand_better(float a, int64_t ia, float b, int64_t ib)
+{
+    const bool na = a != a, nb = b != b;
+    if (na || nb) return (na && nb) ? ia < ib : nb;
+    if (a < b) return true;
+    if (b < a) return false;
+    return ia < ib;
+}
+
+__device__ __forceinline__ int64_t shfl_xor_i64(int64_t v, int m)
+{
+    const int lo = __shfl_xor((int)(uint32_t)v, m, 64);
+    const int hi = __shfl_xor((int)(uint32_t)((uint64_t)v >> 32), m, 64);
+    return (int64_t)(((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo);
+}
+
+// Block-wide argmin (and a count sum) of per-thread candidates; thread 0
+// gets the result.  sv/si/sc: LDS of blockDim/64 entries each.
+__device__ __forceinline__ void block_argmin(float &v, int64_t &i, uint32_t &cnt, float *sv,
+                                             int64_t *si, uint32_t *sc)
+{
+#pragma unroll
+    for (int m = 32; m >= 1; m >>= 1) {
+        const float ov = __shfl_xor(v, m, 64);
+        const int64_t oi = shfl_xor_i64(i, m);
+        cnt += (uint32_t)__shfl_xor((int)cnt, m, 64);
+        if (cand_better(ov, oi, v, i)) {
+            v = ov;
+            i = oi;
+        }
+    }
+    const int wave = threadIdx.x / 64, nw = blockDim.x / 64;
+    if ((threadIdx.x & 63) == 0) {
+        sv[wave] = v;
+        si[wave] = i;
+        sc[wave] = cnt;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        for (int q = 1; q < nw; ++q) {
+            cnt += sc[q];
+            if (cand_better(sv[q], si[q], v, i)) {
+                v = sv[q];
+                i = si[q];
+            }
+        }
+    }
+}
+
+// Result of a selection, kept in device scratch.
+struct DevBest {
+    float f;
+    int32_t pad;
+    int64_t i;
+    uint64_t improved;  // PSO: rows whose personal best improved, summed
+};
+
+}  // namespace evox

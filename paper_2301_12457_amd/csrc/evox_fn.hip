@@ -1,0 +1,15 @@
+// One benchmark function's instantiation of the generation kernels
+// (compiled once per function with -DEVOX_FN=<id>).
+#include "evox_kernels.hpp"
+
+#ifndef EVOX_FN
+#error "compile with -DEVOX_FN=<function id>"
+#endif
+
+namespace evox {
+
+template hipError_t launch_pso_t<EVOX_FN>(int, int, const PsoArgs &, int, hipStream_t);
+template hipError_t launch_eval_t<EVOX_FN>(int, bool, const EvalArgs &, int, hipStream_t);
+template hipError_t launch_cso_t<EVOX_FN>(int, const CsoArgs &, int, hipStream_t);
+
+}  // namespace evox

@@ -1,0 +1,415 @@
+// Kernel templates over (benchmark function, lanes per row) of the gfx950
+// generation path, and their per-function launchers.  evox_fn.hip
+// instantiates them once per function so the six compile in parallel.
+//
+// PSO.  Generation t of the ask-evaluate-tell loop (Sec. IV-B, Eq. (1)-(3))
+// needs a grid-wide reduction (the global best) between "evaluate + personal
+// best" and "move".  The kernels cut the loop there:
+//   k_pso<EVAL>   evaluate x_t, update personal bests, block argmin partials
+//   k_select      grid argmin over the partials, copy the gbest row
+//   k_pso<FUSED>  move(t) -> x_{t+1}, evaluate x_{t+1}, personal bests,
+//                 block argmin partials, all from one read of x, v, pbest
+//   k_pso<MOVE>   the final move of a call (nothing to evaluate after it)
+// so an n-generation call is EVAL, select, (n-1) x (FUSED, select), MOVE:
+// one HBM pass of 20 B per element per generation (read x, v, p; write x, v)
+// plus 4 B per element of rows whose personal best improved.
+//
+// CSO.  k_cso: one row group per pair (perm[2k], perm[2k+1]) of the
+// competitive swarm optimizer (Table II); the loser reads its winner's row
+// (a random gather), its own x and v, moves, writes x and v, is re-evaluated
+// from registers, and both rows' new values are accumulated into per-block
+// fp64 column sums for the next swarm mean: 20 B per pair element, i.e. 10 B
+// per individual element.
+#pragma once
+
+#include "evox_launch.hpp"
+
+namespace evox {
+
+// ---------------------------------------------------------------------------
+// The PSO generation kernel (modes above).  Grid-stride over groups of
+// block_for(G) / G rows; the loop bound is uniform over the block, so the
+// barriers inside row_fitness are reached by every thread.
+// ---------------------------------------------------------------------------
+template <int FN, int G, int MODE>
+__global__ __launch_bounds__(block_for(G)) void k_pso(PsoArgs a)
+{
+    constexpr int B = block_for(G), RPB = B / G, MAXIT = maxit_for(G);
+    constexpr bool MOVE = MODE != PSO_EVAL, EVAL = MODE != PSO_MOVE;
+    __shared__ float nbr[(FN == FN_ROSENBROCK && G > 64) ? B * MAXIT : 1];
+    __shared__ float red[2 * (B / 64)];
+    __shared__ float sv[B / 64];
+    __shared__ int64_t si[B / 64];
+    __shared__ uint32_t sc[B / 64];
+
+    const int tid = threadIdx.x, g = tid % G, slot = tid / G;
+    const int64_t C4 = (a.D + 3) >> 2;
+    float bv = __builtin_nanf("");
+    int64_t bi = INT64_MAX;
+    uint32_t nimp = 0;
+
+    for (int64_t rb = (int64_t)blockIdx.x * RPB; rb < a.N; rb += (int64_t)gridDim.x * RPB) {
+        const int64_t row = rb + slot;
+        const bool active = row < a.N;
+        float4 xr[MAXIT];
+#pragma unroll
+        for (int it = 0; it < MAXIT; ++it) {
+            const int64_t c = g + (int64_t)G * it;
+            float4 xn = make_float4(0.f, 0.f, 0.f, 0.f);
+            if (active && c < C4) {
+                const int64_t off = row * a.ldx + 4 * c;
+                const float4 xv = *reinterpret_cast<const float4 *>(a.x + off);
+                if constexpr (MOVE) {
+                    const float4 vv = *reinterpret_cast<const float4 *>(a.v + off);
+                    const float4 pv = *reinterpret_cast<const float4 *>(a.p + off);
+                    const float4 gv = *reinterpret_cast<const float4 *>(a.gbest + 4 * c);
+                    const U4 r1 = philox((uint32_t)(2 * c), (uint32_t)row, a.t, STREAM_PSO, a.k0, a.k1);
+                    const U4 r2 =
+                        philox((uint32_t)(2 * c + 1), (uint32_t)row, a.t, STREAM_PSO, a.k0, a.k1);
+                    float xo[4], vo[4];
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        const float xe = comp(xv, e);
+                        const float A = a.c1 * wcomp(r1, e);
+                        const float Bc = a.c2 * wcomp(r2, e);
+                        float nv = fmaf(Bc, comp(gv, e) - xe, fmaf(A, comp(pv, e) - xe, a.w * comp(vv, e)));
+                        if (a.vclamp) nv = fminf(fmaxf(nv, -a.vmax), a.vmax);
+                        float nx = xe + nv;
+                        if (a.xclamp) nx = fminf(fmaxf(nx, a.lb), a.ub);
+                        const bool in = 4 * c + e < a.D;
+                        xo[e] = in ? nx : 0.0f;
+                        vo[e] = in ? nv : 0.0f;
+                    }
+                    xn = make_float4(xo[0], xo[1], xo[2], xo[3]);
+                    *reinterpret_cast<float4 *>(a.x + off) = xn;
+                    *reinterpret_cast<float4 *>(a.v + off) = make_float4(vo[0], vo[1], vo[2], vo[3]);
+                } else {
+                    xn = xv;
+                }
+            }
+            xr[it] = xn;
+        }
+        if constexpr (EVAL) {
+            const float f = row_fitness<FN, G, MAXIT>(xr, g, a.D, nbr, red);
+            if (active) {
+                const float pold = a.pf[row];
+                const bool imp = f < pold;
+                if (imp) {
+#pragma unroll
+                    for (int it = 0; it < MAXIT; ++it) {
+                        const int64_t c = g + (int64_t)G * it;
+                        if (c < C4) *reinterpret_cast<float4 *>(a.p + row * a.ldx + 4 * c) = xr[it];
+                    }
+                }
+                if (g == 0) {
+                    if (imp) a.pf[row] = f;
+                    if (a.fit) a.fit[row] = f;
+                    const float nf = imp ? f : pold;
+                    if (cand_better(nf, row, bv, bi)) {
+                        bv = nf;
+                        bi = row;
+                    }
+                    nimp += imp ? 1u : 0u;
+                }
+            }
+        }
+    }
+    if constexpr (EVAL) {
+        block_argmin(bv, bi, nimp, sv, si, sc);
+        if (tid == 0) {
+            a.pval[blockIdx.x] = bv;
+            a.pidx[blockIdx.x] = bi;
+            a.pcnt[blockIdx.x] = nimp;
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Problem.evaluate over any row pitch / alignment; optional block partials
+// of the selection.  VEC: 16-byte aligned rows, float4 loads.
+// ---------------------------------------------------------------------------
+template <int FN, int G, bool VEC>
+__global__ __launch_bounds__(block_for(G)) void k_eval(EvalArgs a)
+{
+    constexpr int B = block_for(G), RPB = B / G, MAXIT = maxit_for(G);
+    __shared__ float nbr[(FN == FN_ROSENBROCK && G > 64) ? B * MAXIT : 1];
+    __shared__ float red[2 * (B / 64)];
+    __shared__ float sv[B / 64];
+    __shared__ int64_t si[B / 64];
+    __shared__ uint32_t sc[B / 64];
+
+    const int tid = threadIdx.x, g = tid % G, slot = tid / G;
+    const int64_t C4 = (a.D + 3) >> 2;
+    float bv = __builtin_nanf("");
+    int64_t bi = INT64_MAX;
+    uint32_t dummy = 0;
+
+    for (int64_t rb = (int64_t)blockIdx.x * RPB; rb < a.N; rb += (int64_t)gridDim.x * RPB) {
+        const int64_t row = rb + slot;
+        const bool active = row < a.N;
+        float4 xr[MAXIT];
+#pragma unroll
+        for (int it = 0; it < MAXIT; ++it) {
+            const int64_t c = g + (int64_t)G * it;
+            float4 xv = make_float4(0.f, 0.f, 0.f, 0.f);
+            if (active && c < C4) {
+                const float *src = a.X + row * a.ldx + 4 * c;
+                if constexpr (VEC) {
+                    xv = *reinterpret_cast<const float4 *>(src);
+                } else {
+                    const int64_t left = a.D - 4 * c;
+                    xv.x = src[0];
+                    if (left > 1) xv.y = src[1];
+                    if (left > 2) xv.z = src[2];
+                    if (left > 3) xv.w = src[3];
+                }
+            }
+            xr[it] = xv;
+        }
+        const float f = row_fitness<FN, G, MAXIT>(xr, g, a.D, nbr, red);
+        if (active && g == 0) {
+            a.out[row] = f;
+            if (cand_better(f, row, bv, bi)) {
+                bv = f;
+                bi = row;
+            }
+        }
+    }
+    if (a.pval) {
+        block_argmin(bv, bi, dummy, sv, si, sc);
+        if (tid == 0) {
+            a.pval[blockIdx.x] = bv;
+            a.pidx[blockIdx.x] = bi;
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Column sums of a block's rows: per-thread fp64 sums cs[it][e] of column
+// 4 (g + G it) + e over the rows the thread handled are reduced over the
+// block's row slots in slot order and written to xsum[blockIdx][*].
+// lds: block_for(G) * 4 doubles when G < 256.
+// ---------------------------------------------------------------------------
+template <int G, int MAXIT>
+__device__ __forceinline__ void block_colsum_write(const double (&cs)[MAXIT][4], int64_t D,
+                                                  int64_t ldx, double *xsum, double *lds)
+{
+    constexpr int B = block_for(G), RPB = B / G;
+    const int tid = threadIdx.x, g = tid % G, slot = tid / G;
+    double *dst = xsum + (int64_t)blockIdx.x * ldx;
+    if constexpr (RPB == 1) {
+#pragma unroll
+        for (int it = 0; it < MAXIT; ++it)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const int64_t j = 4 * ((int64_t)g + (int64_t)G * it) + e;
+                if (j < D) dst[j] = cs[it][e];
+            }
+    } else {
+#pragma unroll
+        for (int it = 0; it < MAXIT; ++it) {
+            if (4 * (int64_t)G * it >= D) break;  // uniform
+#pragma unroll
+            for (int e = 0; e < 4; ++e) lds[slot * 4 * G + 4 * g + e] = cs[it][e];
+            __syncthreads();
+            for (int q = tid; q < 4 * G; q += B) {
+                double s = lds[q];
+                for (int r = 1; r < RPB; ++r) s += lds[r * 4 * G + q];
+                const int64_t j = 4 * (int64_t)G * it + q;
+                if (j < D) dst[j] = s;
+            }
+            __syncthreads();
+        }
+    }
+}
+
+template <int FN, int G>
+__global__ __launch_bounds__(block_for(G)) void k_cso(CsoArgs a)
+{
+    constexpr int B = block_for(G), RPB = B / G, MAXIT = maxit_for(G);
+    __shared__ float nbr[(FN == FN_ROSENBROCK && G > 64) ? B * MAXIT : 1];
+    __shared__ float red[2 * (B / 64)];
+    __shared__ float sv[B / 64];
+    __shared__ int64_t si[B / 64];
+    __shared__ uint32_t sc[B / 64];
+    __shared__ double lds[RPB > 1 ? B * 4 : 1];
+
+    const int tid = threadIdx.x, g = tid % G, slot = tid / G;
+    const int64_t C4 = (a.D + 3) >> 2;
+    const int64_t NP = a.N / 2, NG = NP + (a.N & 1);  // pair groups (+ the unpaired one)
+    float bv = __builtin_nanf("");
+    int64_t bi = INT64_MAX;
+    uint32_t dummy = 0;
+    double cs[MAXIT][4];
+#pragma unroll
+    for (int it = 0; it < MAXIT; ++it)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) cs[it][e] = 0.0;
+
+    for (int64_t kb = (int64_t)blockIdx.x * RPB; kb < NG; kb += (int64_t)gridDim.x * RPB) {
+        const int64_t k = kb + slot;
+        const bool active = k < NG;
+        const bool paired = k < NP;
+        int64_t w = 0, l = 0;
+        float fw = 0.0f;
+        if (active) {
+            if (paired) {
+                const int64_t p0 = a.perm[2 * k], p1 = a.perm[2 * k + 1];
+                const float f0 = a.fit[p0], f1 = a.fit[p1];
+                const bool second = f1 < f0 || (f0 != f0 && f1 == f1);
+                w = second ? p1 : p0;
+                l = second ? p0 : p1;
+                fw = second ? f1 : f0;
+            } else {
+                w = a.perm[a.N - 1];
+                fw = a.fit[w];
+            }
+        }
+        float4 xr[MAXIT];
+#pragma unroll
+        for (int it = 0; it < MAXIT; ++it) {
+            const int64_t c = g + (int64_t)G * it;
+            float4 xn = make_float4(0.f, 0.f, 0.f, 0.f);
+            if (active && c < C4) {
+                const float4 xw = *reinterpret_cast<const float4 *>(a.x + w * a.ldx + 4 * c);
+                if (paired) {
+                    const int64_t off = l * a.ldx + 4 * c;
+                    const float4 xl = *reinterpret_cast<const float4 *>(a.x + off);
+                    const float4 vl = *reinterpret_cast<const float4 *>(a.v + off);
+                    const float4 xb = *reinterpret_cast<const float4 *>(a.xbar + 4 * c);
+                    const U4 R1 = philox((uint32_t)(3 * c), (uint32_t)l, a.t, STREAM_CSO, a.k0, a.k1);
+                    const U4 R2 = philox((uint32_t)(3 * c + 1), (uint32_t)l, a.t, STREAM_CSO, a.k0, a.k1);
+                    const U4 R3 = philox((uint32_t)(3 * c + 2), (uint32_t)l, a.t, STREAM_CSO, a.k0, a.k1);
+                    float xo[4], vo[4];
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        const float xle = comp(xl, e);
+                        const float t0 = wcomp(R1, e) * comp(vl, e);
+                        const float t1 = fmaf(wcomp(R2, e), comp(xw, e) - xle, t0);
+                        const float cc = a.phi * wcomp(R3, e);
+                        const float nv = fmaf(cc, comp(xb, e) - xle, t1);
+                        float nx = xle + nv;
+                        if (a.xclamp) nx = fminf(fmaxf(nx, a.lb), a.ub);
+                        const bool in = 4 * c + e < a.D;
+                        xo[e] = in ? nx : 0.0f;
+                        vo[e] = in ? nv : 0.0f;
+                    }
+                    xn = make_float4(xo[0], xo[1], xo[2], xo[3]);
+                    *reinterpret_cast<float4 *>(a.x + off) = xn;
+                    *reinterpret_cast<float4 *>(a.v + off) = make_float4(vo[0], vo[1], vo[2], vo[3]);
+                }
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    cs[it][e] += (double)comp(xw, e);
+                    if (paired) cs[it][e] += (double)comp(xn, e);
+                }
+            }
+            xr[it] = xn;
+        }
+        const float f = row_fitness<FN, G, MAXIT>(xr, g, a.D, nbr, red);
+        if (active && g == 0) {
+            if (cand_better(fw, w, bv, bi)) {
+                bv = fw;
+                bi = w;
+            }
+            if (paired) {
+                a.fit[l] = f;
+                if (cand_better(f, l, bv, bi)) {
+                    bv = f;
+                    bi = l;
+                }
+            }
+        }
+    }
+    block_argmin(bv, bi, dummy, sv, si, sc);
+    if (tid == 0) {
+        a.pval[blockIdx.x] = bv;
+        a.pidx[blockIdx.x] = bi;
+    }
+    __syncthreads();
+    block_colsum_write<G, MAXIT>(cs, a.D, a.ldx, a.xsum, lds);
+}
+
+// Column sums of all rows of x (the swarm mean at creation / refresh).
+template <int G>
+__global__ __launch_bounds__(block_for(G)) void k_colsum(const float *x, int64_t N, int64_t D,
+                                                        int64_t ldx, double *xsum)
+{
+    constexpr int B = block_for(G), RPB = B / G, MAXIT = maxit_for(G);
+    __shared__ double lds[RPB > 1 ? B * 4 : 1];
+    const int tid = threadIdx.x, g = tid % G, slot = tid / G;
+    const int64_t C4 = (D + 3) >> 2;
+    double cs[MAXIT][4];
+#pragma unroll
+    for (int it = 0; it < MAXIT; ++it)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) cs[it][e] = 0.0;
+    for (int64_t rb = (int64_t)blockIdx.x * RPB; rb < N; rb += (int64_t)gridDim.x * RPB) {
+        const int64_t row = rb + slot;
+        if (row >= N) continue;
+#pragma unroll
+        for (int it = 0; it < MAXIT; ++it) {
+            const int64_t c = g + (int64_t)G * it;
+            if (c < C4) {
+                const float4 xv = *reinterpret_cast<const float4 *>(x + row * ldx + 4 * c);
+#pragma unroll
+                for (int e = 0; e < 4; ++e) cs[it][e] += (double)comp(xv, e);
+            }
+        }
+    }
+    block_colsum_write<G, MAXIT>(cs, D, ldx, xsum, lds);
+}
+
+#define EVOX_G_CASES(M, ...)                                                                      \
+    switch (G) {                                                                                  \
+    case 4: M(4, __VA_ARGS__); break;                                                             \
+    case 8: M(8, __VA_ARGS__); break;                                                             \
+    case 16: M(16, __VA_ARGS__); break;                                                           \
+    case 32: M(32, __VA_ARGS__); break;                                                           \
+    case 64: M(64, __VA_ARGS__); break;                                                           \
+    case 128: M(128, __VA_ARGS__); break;                                                         \
+    case 256: M(256, __VA_ARGS__); break;                                                         \
+    case 512: M(512, __VA_ARGS__); break;                                                         \
+    case 1024: M(1024, __VA_ARGS__); break;                                                       \
+    default: return hipErrorInvalidValue;                                                         \
+    }
+
+#define EVOX_LAUNCH_PSO(GG, MODEE) \
+    hipLaunchKernelGGL((k_pso<FN, GG, MODEE>), dim3(grid), dim3(block_for(GG)), 0, s, a)
+#define EVOX_LAUNCH_EVAL(GG, VECC) \
+    hipLaunchKernelGGL((k_eval<FN, GG, VECC>), dim3(grid), dim3(block_for(GG)), 0, s, a)
+#define EVOX_LAUNCH_CSO(GG, UNUSED) \
+    hipLaunchKernelGGL((k_cso<FN, GG>), dim3(grid), dim3(block_for(GG)), 0, s, a)
+
+template <int FN>
+hipError_t launch_pso_t(int G, int mode, const PsoArgs &a, int grid, hipStream_t s)
+{
+    if (mode == PSO_EVAL) {
+        EVOX_G_CASES(EVOX_LAUNCH_PSO, PSO_EVAL)
+    } else if (mode == PSO_FUSED) {
+        EVOX_G_CASES(EVOX_LAUNCH_PSO, PSO_FUSED)
+    } else {
+        EVOX_G_CASES(EVOX_LAUNCH_PSO, PSO_MOVE)
+    }
+    return hipGetLastError();
+}
+
+template <int FN>
+hipError_t launch_eval_t(int G, bool vec, const EvalArgs &a, int grid, hipStream_t s)
+{
+    if (vec) {
+        EVOX_G_CASES(EVOX_LAUNCH_EVAL, true)
+    } else {
+        EVOX_G_CASES(EVOX_LAUNCH_EVAL, false)
+    }
+    return hipGetLastError();
+}
+
+template <int FN>
+hipError_t launch_cso_t(int G, const CsoArgs &a, int grid, hipStream_t s)
+{
+    EVOX_G_CASES(EVOX_LAUNCH_CSO, 0)
+    return hipGetLastError();
+}
+
+}  // namespace evox

@@ -1,0 +1,75 @@
+"""The benchmark workloads and seeded synthetic inputs.
+
+Holds none of the method's arithmetic: only the sizes and hyperparameters of
+each workload and seeded generators of input matrices, shared by the tests
+and the benchmark.  The populations of the PSO / CSO workloads are drawn by
+the method itself (Philox streams 0 and 1 at creation); the evaluation-only
+workload reads a matrix generated here.
+
+The shapes stand in for the paper's large-scale numerical experiments
+(Sec. VII-A-1: population and dimension scaling on Sphere, populations up to
+about a million): synthetic, seeded, no dataset.
+"""
+import math
+from dataclasses import dataclass, field
+
+PSO, CSO, EVAL = "pso", "cso", "eval"
+
+
+@dataclass(frozen=True)
+class Workload:
+    name: str
+    algo: str
+    fn: str
+    N: int
+    D: int
+    gens: int
+    seed: int
+    lb: float = 0.0
+    ub: float = 0.0
+    v_lo: float = 0.0
+    v_hi: float = 0.0
+    w: float = 0.6
+    c1: float = 1.5
+    c2: float = 1.5
+    phi: float = 0.1
+    vmax: float = 0.0
+    x_mu: float = 0.0      # evaluation-only input: x ~ N(x_mu, x_sigma^2)
+    x_sigma: float = 0.0
+
+
+WORKLOADS = {
+    "pso_sphere_100x10": Workload("pso_sphere_100x10", PSO, "sphere", 100, 10, 100, 0,
+                                  lb=-32.0, ub=32.0),
+    "pso_ackley_1e4x1e3": Workload("pso_ackley_1e4x1e3", PSO, "ackley", 10_000, 1_000, 1_000, 1,
+                                   lb=-32.768, ub=32.768, v_lo=-1.0, v_hi=1.0),
+    "pso_rastrigin_1e5x1e3": Workload("pso_rastrigin_1e5x1e3", PSO, "rastrigin", 100_000, 1_000,
+                                      200, 2, lb=-5.12, ub=5.12, vmax=0.2 * 10.24),
+    "cso_griewank_1e6x100": Workload("cso_griewank_1e6x100", CSO, "griewank", 1_000_000, 100, 200,
+                                     3, lb=-600.0, ub=600.0, phi=0.1),
+    "eval_rosenbrock_1m_x1e3": Workload("eval_rosenbrock_1m_x1e3", EVAL, "rosenbrock", 1_048_576,
+                                        1_000, 1, 4, x_mu=1.0, x_sigma=0.5),
+}
+
+
+def normal_matrix_torch(N, D, mu, sigma, seed, device="cuda", ldx=None):
+    """Seeded x ~ N(mu, sigma^2) of shape [N, ldx] (padding zero), made on the device."""
+    import torch
+    ldx = D if ldx is None else ldx
+    g = torch.Generator(device=device)
+    g.manual_seed(seed)
+    X = torch.zeros((N, ldx), dtype=torch.float32, device=device)
+    X[:, :D].normal_(mu, sigma, generator=g)
+    return X
+
+
+def uniform_matrix_np(N, D, lo, hi, seed):
+    import numpy as np
+    rng = np.random.default_rng(seed)
+    return rng.uniform(lo, hi, size=(N, D)).astype(np.float32)
+
+
+def normal_matrix_np(N, D, mu, sigma, seed):
+    import numpy as np
+    rng = np.random.default_rng(seed)
+    return rng.normal(mu, sigma, size=(N, D)).astype(np.float32)

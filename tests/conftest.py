@@ -49,3 +49,17 @@ def u01_exact(words):
     """The top 24 bits of each word divided by 2^24 (exact in fp32)."""
     w = np.asarray(words, dtype=np.uint64)
     return ((w >> np.uint64(8)).astype(np.float64) / float(1 << 24)).astype(np.float32)
+
+
+@pytest.fixture(scope="session")
+def evox_gpu():
+    """The HIP library on cuda:0.  Fails (does not skip) without a GPU or library."""
+    import torch
+    import paper_2301_12457_amd as m
+    if not torch.cuda.is_available():
+        pytest.fail("GPU test run without a GPU")
+    if not os.path.exists(m.LIB_PATH):
+        pytest.fail(f"{m.LIB_PATH} is not built")
+    m.lib()
+    torch.cuda.init()
+    return m

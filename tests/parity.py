@@ -1,0 +1,77 @@
+"""Tolerances and comparison helpers of the GPU-vs-oracle parity tests.
+
+Fitness tolerance (reading of "fp32 fitness within 1e-5 relative"):
+    |F_gpu - F_ref| <= 1e-5 * max(|F_ref|, S(x))
+with S the magnitude of the terms the function sums, so that exact
+cancellation at an optimum does not demand unbounded relative accuracy:
+    Sphere, Rosenbrock  S = |F|              (non-negative terms)
+    Ackley              S = 20 + e
+    Rastrigin           S = 20 D + sum x^2
+    Griewank            S = 2 + sum x^2 / 4000
+    Schwefel            S = 418.9829 D + sum |x|
+"""
+import math
+
+import numpy as np
+
+REL = 1e-5
+SPHERE, ACKLEY, RASTRIGIN, GRIEWANK, ROSENBROCK, SCHWEFEL = range(6)
+
+
+def scale(fn, X, f_ref):
+    X = np.asarray(X, dtype=np.float64)
+    D = X.shape[1]
+    f = np.abs(np.asarray(f_ref, dtype=np.float64))
+    if fn in (SPHERE, ROSENBROCK):
+        return f
+    if fn == ACKLEY:
+        return np.maximum(f, 20.0 + math.e)
+    if fn == RASTRIGIN:
+        return np.maximum(f, 20.0 * D + (X * X).sum(1))
+    if fn == GRIEWANK:
+        return np.maximum(f, 2.0 + (X * X).sum(1) / 4000.0)
+    if fn == SCHWEFEL:
+        return np.maximum(f, 418.9829 * D + np.abs(X).sum(1))
+    raise ValueError(fn)
+
+
+def tol(fn, X, f_ref):
+    return REL * scale(fn, X, f_ref)
+
+
+def fitness_ok(fn, X, f_gpu, f_ref):
+    """Boolean mask of rows whose GPU fitness is within tolerance."""
+    f_gpu = np.asarray(f_gpu, dtype=np.float64)
+    f_ref = np.asarray(f_ref, dtype=np.float64)
+    both_inf = np.isinf(f_gpu) & np.isinf(f_ref) & (np.sign(f_gpu) == np.sign(f_ref))
+    both_nan = np.isnan(f_gpu) & np.isnan(f_ref)
+    with np.errstate(invalid="ignore"):
+        close = np.abs(f_gpu - f_ref) <= tol(fn, X, f_ref)
+    return close | both_inf | both_nan
+
+
+def assert_fitness(fn, X, f_gpu, f_ref, what=""):
+    ok = fitness_ok(fn, X, f_gpu, f_ref)
+    if not ok.all():
+        bad = np.nonzero(~ok)[0][:5]
+        rows = [(int(i), float(f_gpu[i]), float(f_ref[i])) for i in bad]
+        raise AssertionError(f"{what}: {int((~ok).sum())} rows out of tolerance, e.g. {rows}")
+
+
+def index_ok(fn, X_rows, f_ref_all, i_gpu, i_ref):
+    """Selected index: equal, or a tolerance tie (the two candidates' oracle
+    values are within the fitness tolerance of each other)."""
+    if i_gpu == i_ref:
+        return True
+    a, b = float(f_ref_all[i_gpu]), float(f_ref_all[i_ref])
+    t = REL * max(abs(a), abs(b), float(scale(fn, X_rows, [b]).max()))
+    return abs(a - b) <= t
+
+
+def ulp_diff(a, b):
+    """Distance in units in the last place between float32 arrays."""
+    ai = np.asarray(a, np.float32).view(np.int32).astype(np.int64)
+    bi = np.asarray(b, np.float32).view(np.int32).astype(np.int64)
+    ai = np.where(ai < 0, -(ai & 0x7FFFFFFF), ai)
+    bi = np.where(bi < 0, -(bi & 0x7FFFFFFF), bi)
+    return np.abs(ai - bi)

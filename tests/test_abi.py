@@ -1,0 +1,117 @@
+"""The C-ABI library loads, exports every symbol include/evox.h declares, and
+rejects invalid arguments on the host side (no GPU needed: validation runs
+before any HIP call)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from conftest import ROOT
+
+HEADER = os.path.join(ROOT, "include", "evox.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(evox_[a-z0-9_]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def evox():
+    import paper_2301_12457_amd as m
+    if not os.path.exists(m.LIB_PATH):
+        from paper_2301_12457_amd import build
+        build.build()
+    return m
+
+
+def test_exports_every_declared_symbol(evox):
+    L = evox.lib()
+    names = declared_functions()
+    assert len(names) >= 15
+    for n in names:
+        assert hasattr(L, n), n
+    assert sorted(evox.EXPORTS) == names
+
+
+def test_struct_layouts_match_header(evox):
+    # evox_params: 2 x int32, 3 x int64, 9 floats, int32, (pad), uint64
+    assert ctypes.sizeof(evox.Params) == 80
+    assert evox.Params.seed.offset == 72
+    assert ctypes.sizeof(evox.Buffers) == 9 * 8
+
+
+def test_row_layout_policy(evox):
+    assert evox.row_layout(1) == (4, 1)
+    assert evox.row_layout(10) == (4, 1)
+    assert evox.row_layout(100) == (8, 4)
+    assert evox.row_layout(1000) == (64, 4)
+    assert evox.row_layout(1001) == (64, 4)
+    assert evox.row_layout(32768) == (1024, 8)
+    for D in list(range(1, 300)) + [1023, 1024, 1025, 4096, 4097, 16385, 32767]:
+        G, nit = evox.row_layout(D)
+        assert G * nit * 4 >= D and nit <= (8 if G == 1024 else 4)
+        assert G == 4 or (G // 2) * (8 if G // 2 == 1024 else 4) * 4 < D or nit > 1
+    with pytest.raises(evox.EvoxError):
+        evox.row_layout(32769)
+
+
+def test_scratch_bytes(evox):
+    p = evox.make_params(evox.PSO, evox.SPHERE, 100, 10, -1, 1)
+    assert evox.evox_scratch_bytes(p) > 0
+    c = evox.make_params(evox.CSO, evox.GRIEWANK, 1_000_000, 100, -600, 600)
+    n = evox.evox_scratch_bytes(c)
+    assert n >= 3 * 4 * 1_000_000  # keys, indices, permutation
+    bad = evox.make_params(evox.PSO, 9, 100, 10, -1, 1)
+    assert evox.evox_scratch_bytes(bad) == 0
+
+
+@pytest.mark.parametrize("field,value", [("N", 0), ("D", 0), ("D", 40000), ("ldx", 6),
+                                         ("fn_id", 6), ("algo", 3)])
+def test_create_rejects_bad_params(evox, field, value):
+    p = evox.make_params(evox.PSO, evox.SPHERE, 8, 5, -1, 1)
+    setattr(p, field, value)
+    b = evox.Buffers()
+    h = ctypes.c_void_p()
+    rc = evox.lib().evox_state_create(ctypes.byref(p), ctypes.byref(b), None, ctypes.byref(h))
+    assert rc == evox.EINVAL
+    assert evox.lib().evox_last_error().decode()
+    assert not h.value
+
+
+def test_create_rejects_missing_and_misaligned_buffers(evox):
+    p = evox.make_params(evox.PSO, evox.SPHERE, 8, 5, -1, 1)
+    b = evox.Buffers()
+    h = ctypes.c_void_p()
+    L = evox.lib()
+    assert L.evox_state_create(ctypes.byref(p), ctypes.byref(b), None, ctypes.byref(h)) == evox.EINVAL
+    need = evox.evox_scratch_bytes(p)
+    b = evox.Buffers(x=0x1000, v=0x2000, pbest=0x3000, pfit=0x4000, gbest=0x5008, scratch=0x10000,
+                     scratch_bytes=need)
+    assert L.evox_state_create(ctypes.byref(p), ctypes.byref(b), None, ctypes.byref(h)) == evox.EALIGN
+    b.gbest = 0x5000
+    b.scratch_bytes = need - 1
+    assert L.evox_state_create(ctypes.byref(p), ctypes.byref(b), None, ctypes.byref(h)) == evox.ENOSPC
+    c = evox.make_params(evox.CSO, evox.SPHERE, 1, 5, -1, 1)    # CSO needs a pair
+    assert L.evox_state_create(ctypes.byref(c), ctypes.byref(b), None, ctypes.byref(h)) == evox.EINVAL
+
+
+def test_eval_rejects_bad_args(evox):
+    L = evox.lib()
+    assert L.evox_eval(7, None, 1, 1, None, None) == evox.EINVAL
+    assert L.evox_eval(0, None, 1, 0, None, None) == evox.EINVAL
+    assert L.evox_eval(0, None, 5, 3, None, None) == evox.EINVAL
+    assert L.evox_eval(0, None, 0, 3, None, None) == evox.OK     # empty: nothing to do
+    assert L.evox_eval_ld(0, None, 0, 8, 4, None, None) == evox.EINVAL
+    assert L.evox_eval_argmin(0, None, 0, 3, 3, None, None, None, None, 0, None) == evox.EINVAL
+
+
+def test_null_state_is_rejected(evox):
+    L = evox.lib()
+    assert L.evox_pso_step(None, 1) == evox.EINVAL
+    assert L.evox_cso_step(None, 1) == evox.EINVAL
+    assert L.evox_best(None, None, None, None) == evox.EINVAL
+    assert L.evox_generation(None) == -1
+    assert L.evox_strerror(evox.ENOSPC).decode() == "scratch buffer too small"

@@ -1,0 +1,133 @@
+"""GPU parity of the CSO generation against the oracle.
+
+The pairing permutation is integer work and must match exactly; the loser
+update is bit-exact given the same swarm mean; the mean itself is an fp64 sum
+in a different order on each side and must agree to 1 ulp; fitness within
+the fitness tolerance; the reported best index exactly.
+"""
+import numpy as np
+import pytest
+import torch
+
+from parity import assert_fitness, index_ok, ulp_diff
+
+pytestmark = pytest.mark.gpu
+
+
+def pair(evox, ref, fn, N, D, seed, lb, ub, **kw):
+    g = evox.Swarm(evox.make_params(evox.CSO, fn, N, D, lb, ub, seed=seed, **kw))
+    r = ref.CSO(ref.make_params(fn, N, D, lb, ub, seed=seed, **kw))
+    return g, r
+
+
+def host(t, D):
+    return t[..., :D].cpu().numpy()
+
+
+def compare(g, r, fn, what, strict=True):
+    D = r.P.D
+    x, v, f = host(g.x, D), host(g.v, D), g.fit.cpu().numpy()
+    if strict:
+        bad = np.nonzero((x != r.x).any(1))[0]
+        assert bad.size == 0, f"{what}: x differs in rows {bad[:8]}"
+        assert np.array_equal(v, r.v), f"{what}: v differs"
+    assert_fitness(fn, r.x, f, r.fit, f"{what}: fit")
+    bf, bi = g.best()
+    if r.t > 0:
+        assert index_ok(fn, r.x, r.fit, bi, r.best_idx), f"{what}: best {bi} vs {r.best_idx}"
+        assert bi == r.best_idx, f"{what}: best index {bi} vs {r.best_idx} (tolerance tie)"
+
+
+def test_init_matches(evox_gpu, ref):
+    g, r = pair(evox_gpu, ref, 3, 101, 100, 3, -600.0, 600.0)
+    torch.cuda.synchronize()
+    assert np.array_equal(host(g.x, 100), r.x)
+    assert np.all(host(g.v, 100) == 0)
+    assert_fitness(3, r.x, g.fit.cpu().numpy(), r.fit, "init fit")
+    assert ulp_diff(host(g.xbar, 100), ref.colmean(r.x)).max() <= 1
+    bf, bi = g.best()
+    assert index_ok(3, r.x, r.fit, bi, ref.argmin(r.fit))
+
+
+CASES = [
+    dict(fn=3, N=1000, D=100, seed=3, lb=-600.0, ub=600.0, gens=20),
+    dict(fn=0, N=101, D=10, seed=0, lb=-32.0, ub=32.0, gens=40),
+    dict(fn=1, N=64, D=37, seed=1, lb=-32.768, ub=32.768, v_lo=-1.0, v_hi=1.0, gens=20),
+    dict(fn=2, N=33, D=257, seed=2, lb=-5.12, ub=5.12, gens=15),
+    dict(fn=4, N=12, D=1001, seed=4, lb=-2.0, ub=2.0, gens=10),
+    dict(fn=5, N=7, D=3, seed=5, lb=-500.0, ub=500.0, clamp_x=1, gens=30),
+    dict(fn=4, N=5, D=2050, seed=6, lb=-2.0, ub=2.0, gens=6),
+    dict(fn=0, N=2, D=1, seed=8, lb=-1.0, ub=1.0, gens=10),
+]
+
+
+@pytest.mark.parametrize("case", CASES, ids=[f"fn{c['fn']}-{c['N']}x{c['D']}" for c in CASES])
+def test_generations_match_oracle(evox_gpu, ref, case):
+    c = dict(case)
+    gens = c.pop("gens")
+    print(f"cso {c} gens={gens}", flush=True)
+    g, r = pair(evox_gpu, ref, **c)
+    for t in range(gens):
+        xbar_ref = ref.colmean(r.x)
+        assert ulp_diff(host(g.xbar, c["D"]), xbar_ref).max() <= 1, f"generation {t}: mean"
+        strict = np.array_equal(host(g.xbar, c["D"]), xbar_ref)
+        g.step(1)
+        r.step(1)
+        compare(g, r, c["fn"], f"generation {t}", strict=strict)
+        if not strict:   # a 1-ulp mean difference moves the losers slightly: stop here
+            break
+    assert g.t == r.t
+
+
+def test_winners_untouched_and_losers_counted(evox_gpu, ref):
+    g, _ = pair(evox_gpu, ref, 3, 999, 20, 5, -600.0, 600.0, v_lo=-1.0, v_hi=1.0)
+    x0, v0, f0 = g.x.clone(), g.v.clone(), g.fit.clone()
+    g.step(1)
+    changed = (g.x != x0).any(1) | (g.v != v0).any(1)
+    assert int(changed.sum()) <= 999 // 2
+    assert int(changed.sum()) >= 999 // 2 - 5       # a loser may by chance not move
+    same = ~changed
+    assert torch.equal(g.fit[same & (g.fit == f0)], f0[same & (g.fit == f0)])
+
+
+def test_multi_generation_call_equals_single_steps(evox_gpu, ref):
+    kw = dict(fn=3, N=500, D=30, seed=12, lb=-600.0, ub=600.0)
+    a, _ = pair(evox_gpu, ref, **kw)
+    b, _ = pair(evox_gpu, ref, **kw)
+    a.step(20)
+    for n in (3, 9, 8):
+        b.step(n)
+    for name in ("x", "v", "fit", "xbar"):
+        assert torch.equal(getattr(a, name), getattr(b, name)), name
+    assert a.best() == b.best()
+
+
+def test_loser_velocity_exposes_r2(evox_gpu, ref):
+    N, D, seed = 40, 9, 31
+    g, r = pair(evox_gpu, ref, 0, N, D, seed, -1.0, 1.0, phi=0.0)
+    side = (np.arange(N) % 2 == 0)
+    xs = np.where(side[:, None], 1.0, 0.0).astype(np.float32) * np.ones((N, D), np.float32)
+    fs = np.where(side, 0.0, 1.0).astype(np.float32)
+    g.x[:, :D] = torch.from_numpy(xs).cuda()
+    g.v.zero_()
+    g.fit.copy_(torch.from_numpy(fs).cuda())
+    g.refresh(refit=False)
+    r.x[:] = xs
+    r.v[:] = 0.0
+    r.fit[:] = fs
+    g.step(1)
+    r.step(1)
+    assert np.array_equal(host(g.v, D), r.v)
+    assert np.array_equal(host(g.x, D), r.x)
+
+
+def test_refresh_after_external_edit(evox_gpu, ref):
+    g, r = pair(evox_gpu, ref, 2, 64, 16, 2, -5.12, 5.12)
+    rng = np.random.default_rng(0)
+    X = rng.uniform(-1, 1, size=(64, 16)).astype(np.float32)
+    g.x[:, :16] = torch.from_numpy(X).cuda()
+    g.refresh(refit=True)
+    r.x[:] = X
+    r.fit[:] = ref.evaluate(2, X)
+    assert_fitness(2, X, g.fit.cpu().numpy(), r.fit, "refit")
+    assert ulp_diff(host(g.xbar, 16), ref.colmean(X)).max() <= 1

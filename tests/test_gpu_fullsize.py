@@ -1,0 +1,85 @@
+"""GPU parity at the full benchmark sizes, in the launch configuration the
+benchmark times (the same library calls, grid and row layout).
+
+The oracle is single-threaded, so the PSO / CSO workloads are compared over
+their first generations (every element, bit for bit) rather than the whole
+run; the evaluation-only workload is compared on every row.
+"""
+import numpy as np
+import pytest
+import torch
+
+from parity import assert_fitness, index_ok, ulp_diff
+
+from paper_2301_12457_amd.workloads import WORKLOADS, normal_matrix_torch
+
+pytestmark = pytest.mark.gpu
+
+
+def swarm_pair(evox, ref, w):
+    algo = evox.PSO if w.algo == "pso" else evox.CSO
+    fn = evox.FN_IDS[w.fn]
+    kw = dict(v_lo=w.v_lo, v_hi=w.v_hi, w=w.w, c1=w.c1, c2=w.c2, phi=w.phi, vmax=w.vmax,
+              seed=w.seed)
+    g = evox.Swarm(evox.make_params(algo, fn, w.N, w.D, w.lb, w.ub, **kw))
+    Ref = ref.PSO if w.algo == "pso" else ref.CSO
+    r = Ref(ref.make_params(fn, w.N, w.D, w.lb, w.ub, **kw))
+    return g, r, fn
+
+
+@pytest.mark.parametrize("name,gens", [("pso_sphere_100x10", 100), ("pso_ackley_1e4x1e3", 4),
+                                       ("pso_rastrigin_1e5x1e3", 2)])
+def test_pso_workload_first_generations(evox_gpu, ref, name, gens):
+    w = WORKLOADS[name]
+    print(f"{name}: {gens} generations", flush=True)
+    g, r, fn = swarm_pair(evox_gpu, ref, w)
+    D = w.D
+    g.step(gens)
+    r.step(gens)
+    assert np.array_equal(g.x[:, :D].cpu().numpy(), r.x)
+    assert np.array_equal(g.v[:, :D].cpu().numpy(), r.v)
+    assert np.array_equal(g.pbest[:, :D].cpu().numpy(), r.p)
+    assert_fitness(fn, r.p, g.pfit.cpu().numpy(), r.pf, name)
+    gf, gi = g.best()
+    assert index_ok(fn, r.p, r.pf, gi, r.gi) and gi == r.gi
+
+
+def test_cso_workload_first_generations(evox_gpu, ref):
+    w = WORKLOADS["cso_griewank_1e6x100"]
+    g, r, fn = swarm_pair(evox_gpu, ref, w)
+    D = w.D
+    assert np.array_equal(g.x[:, :D].cpu().numpy(), r.x)
+    xbar0 = ref.colmean(r.x)
+    assert ulp_diff(g.xbar[:D].cpu().numpy(), xbar0).max() <= 1
+    exact_mean = np.array_equal(g.xbar[:D].cpu().numpy(), xbar0)
+    g.step(1)
+    r.step(1)
+    x = g.x[:, :D].cpu().numpy()
+    if exact_mean:
+        assert np.array_equal(x, r.x)
+        assert np.array_equal(g.v[:, :D].cpu().numpy(), r.v)
+    else:
+        assert np.allclose(x, r.x, rtol=1e-5, atol=1e-3)
+    assert_fitness(fn, r.x, g.fit.cpu().numpy(), r.fit, "cso fit")
+    bf, bi = g.best()
+    assert index_ok(fn, r.x, r.fit, bi, r.best_idx)
+
+
+def test_eval_workload_every_row(evox_gpu, ref):
+    w = WORKLOADS["eval_rosenbrock_1m_x1e3"]
+    fn = evox_gpu.FN_IDS[w.fn]
+    X = normal_matrix_torch(w.N, w.D, w.x_mu, w.x_sigma, w.seed)
+    out = torch.empty(w.N, dtype=torch.float32, device="cuda")
+    bf = torch.empty(1, dtype=torch.float32, device="cuda")
+    bi = torch.empty(1, dtype=torch.int64, device="cuda")
+    scratch = torch.empty(evox_gpu.evox_eval_argmin_scratch_bytes(w.N) // 4 + 64, dtype=torch.int32,
+                          device="cuda")
+    evox_gpu.evox_eval_argmin(fn, X, w.N, w.D, w.D, out, bf, bi, scratch)
+    Xh = X.cpu().numpy()
+    del X
+    f_ref = ref.evaluate(fn, Xh)
+    f_gpu = out.cpu().numpy()
+    assert_fitness(fn, Xh, f_gpu, f_ref, "rosenbrock 1M")
+    i_ref = ref.argmin(f_ref)
+    assert int(bi.item()) == i_ref
+    assert float(bf.item()) == f_gpu[i_ref]

@@ -1,0 +1,119 @@
+"""GPU parity of the PSO generation against the oracle.
+
+Both sides start from the same seed (the initial population is drawn by the
+method itself, so it must match bit for bit), then run generation by
+generation.  Positions and velocities are compared bit for bit, personal-best
+fitness within the fitness tolerance, and the global-best index exactly
+(a tolerance tie would be reported as such).
+"""
+import numpy as np
+import pytest
+import torch
+
+from parity import assert_fitness, index_ok
+
+pytestmark = pytest.mark.gpu
+
+
+def pair(evox, ref, fn, N, D, seed, lb, ub, **kw):
+    g = evox.Swarm(evox.make_params(evox.PSO, fn, N, D, lb, ub, seed=seed, **kw))
+    r = ref.PSO(ref.make_params(fn, N, D, lb, ub, seed=seed, **kw))
+    return g, r
+
+
+def host(t, D):
+    return t[..., :D].cpu().numpy()
+
+
+def compare_state(g, r, fn, what):
+    D = r.P.D
+    x, v, p = host(g.x, D), host(g.v, D), host(g.pbest, D)
+    assert np.array_equal(x, r.x), f"{what}: x differs in rows {np.nonzero((x != r.x).any(1))[0][:8]}"
+    assert np.array_equal(v, r.v), f"{what}: v differs"
+    assert np.array_equal(p, r.p), f"{what}: pbest differs"
+    pf = g.pfit.cpu().numpy()
+    assert_fitness(fn, r.p, pf, r.pf, f"{what}: pfit")
+    gf, gi, gx = g.best(with_x=True)
+    assert index_ok(fn, r.p, r.pf, gi, r.gi), f"{what}: gbest {gi} vs {r.gi}"
+    assert gi == r.gi, f"{what}: gbest index {gi} vs {r.gi} (tolerance tie)"
+    assert np.array_equal(gx, r.g), f"{what}: gbest row"
+    assert_fitness(fn, r.p[[gi]], [gf], [r.gf], f"{what}: gf")
+
+
+def test_init_is_bit_exact(evox_gpu, ref):
+    g, r = pair(evox_gpu, ref, 1, 37, 13, 1, -32.768, 32.768, v_lo=-1.0, v_hi=1.0)
+    torch.cuda.synchronize()
+    assert np.array_equal(host(g.x, 13), r.x)
+    assert np.array_equal(host(g.v, 13), r.v)
+    assert np.array_equal(host(g.pbest, 13), r.p)
+    assert np.all(np.isinf(g.pfit.cpu().numpy()))
+    assert np.all(g.x[:, 13:].cpu().numpy() == 0)       # padding kept at zero
+    f, i = g.best()
+    assert np.isinf(f) and i == 0
+
+
+# configs: the 100 x 10 Sphere workload, every function at ragged shapes, and
+# the velocity clamp / position clamp options
+CASES = [
+    dict(fn=0, N=100, D=10, seed=0, lb=-32.0, ub=32.0, gens=100),
+    dict(fn=1, N=64, D=37, seed=1, lb=-32.768, ub=32.768, v_lo=-1.0, v_hi=1.0, gens=30),
+    dict(fn=2, N=50, D=100, seed=2, lb=-5.12, ub=5.12, vmax=2.048, gens=30),
+    dict(fn=3, N=33, D=129, seed=3, lb=-600.0, ub=600.0, gens=30),
+    dict(fn=4, N=20, D=1001, seed=4, lb=-2.0, ub=2.0, gens=20),
+    dict(fn=5, N=17, D=5, seed=5, lb=-500.0, ub=500.0, clamp_x=1, gens=40),
+    dict(fn=0, N=3, D=4100, seed=6, lb=-1.0, ub=1.0, gens=8),
+    dict(fn=4, N=2, D=2050, seed=7, lb=-2.0, ub=2.0, gens=8),
+]
+
+
+@pytest.mark.parametrize("case", CASES, ids=[f"fn{c['fn']}-{c['N']}x{c['D']}" for c in CASES])
+def test_generations_match_oracle(evox_gpu, ref, case):
+    c = dict(case)
+    gens = c.pop("gens")
+    print(f"pso {c} gens={gens}", flush=True)
+    g, r = pair(evox_gpu, ref, **c)
+    for t in range(gens):
+        g.step(1)
+        r.step(1)
+        compare_state(g, r, c["fn"], f"generation {t}")
+    assert g.t == r.t == gens
+
+
+def test_multi_generation_call_equals_single_steps(evox_gpu, ref):
+    kw = dict(fn=2, N=40, D=64, seed=9, lb=-5.12, ub=5.12, vmax=2.048)
+    a, r = pair(evox_gpu, ref, **kw)
+    b = evox_gpu.Swarm(evox_gpu.make_params(evox_gpu.PSO, kw["fn"], kw["N"], kw["D"], kw["lb"],
+                                             kw["ub"], seed=kw["seed"], vmax=kw["vmax"]))
+    a.step(25)
+    for n in (1, 4, 7, 13):
+        b.step(n)
+    r.step(25)
+    for name in ("x", "v", "pbest", "pfit", "gbest"):
+        assert torch.equal(getattr(a, name), getattr(b, name)), name
+    assert a.best() == b.best()
+    compare_state(a, r, kw["fn"], "after 25")
+
+
+def test_velocity_exposes_r1_and_r2(evox_gpu, ref):
+    N, D, seed = 9, 23, 77
+    for c1, c2 in ((1.0, 0.0), (0.0, 1.0)):
+        g, r = pair(evox_gpu, ref, 0, N, D, seed, -1.0, 1.0, w=0.0, c1=c1, c2=c2)
+        g.x[:, :D] = 0.0
+        g.pbest[:, :D] = 1.0
+        g.pfit.fill_(-np.inf)
+        r.x[:] = 0.0
+        r.p[:] = 1.0
+        r.pf[:] = -np.inf
+        g.step(1)
+        r.step(1)
+        v = host(g.v, D)
+        assert np.array_equal(v, r.v)
+        assert v.min() >= 0.0 and v.max() < 1.0 and len(np.unique(v)) > N * D // 2
+
+
+def test_single_particle(evox_gpu, ref):
+    g, r = pair(evox_gpu, ref, 2, 1, 30, 11, -5.12, 5.12)
+    for t in range(10):
+        g.step(1)
+        r.step(1)
+        compare_state(g, r, 2, f"generation {t}")
