@@ -102,6 +102,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD, choices=sorted(WORKLOADS))
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--ldx", type=int, default=0,
+                    help="row pitch in floats (default: D rounded up to a multiple of 4)")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="also run a plain device copy of this size (HBM-counter calibration)")
     args = ap.parse_args()
@@ -132,7 +134,8 @@ def main():
     else:
         algo = evox.PSO if w.algo == "pso" else evox.CSO
         P = evox.make_params(algo, fn, w.N, w.D, w.lb, w.ub, v_lo=w.v_lo, v_hi=w.v_hi, w=w.w,
-                             c1=w.c1, c2=w.c2, phi=w.phi, vmax=w.vmax, seed=w.seed)
+                             c1=w.c1, c2=w.c2, phi=w.phi, vmax=w.vmax, seed=w.seed,
+                             ldx=args.ldx or None)
         swarm = evox.Swarm(P)
 
         def step():
@@ -203,6 +206,7 @@ def main():
         "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "f32", "data": "synthetic",
         "config": {"workload": w.name, "algo": w.algo, "fn": w.fn, "N": w.N, "D": w.D,
+                   "ldx": (swarm.P.ldx if swarm is not None else w.D),
                    "generations_per_step": gens, "seed": w.seed},
         "roofline": roofline, "cpu_baseline": base,
     }

@@ -80,7 +80,7 @@ enum evox_status {
 typedef struct evox_params {
     int32_t algo;     /* EVOX_PSO or EVOX_CSO */
     int32_t fn_id;    /* enum evox_fn */
-    int64_t N;        /* population size, >= 1 (CSO: >= 2), < 2^31 */
+    int64_t N;        /* population size: PSO 1 .. 2^31 - 1, CSO 2 .. 2^24 */
     int64_t D;        /* dimension, 1 .. EVOX_MAX_D */
     int64_t ldx;      /* row pitch of x, v, pbest in floats: ldx >= D, ldx % 4 == 0 */
     float lb, ub;     /* initial positions ~ U[lb, ub): x = fma(u, ub - lb, lb) */
@@ -186,9 +186,11 @@ int evox_best(evox_state *state, float *best_fit, int64_t *best_idx, float *best
 /* Generations completed so far. */
 int64_t evox_generation(const evox_state *state);
 
-/* Layout the kernels use for dimension D: threads per row and float4 chunks
- * per thread (for tests and reports). */
-int evox_row_layout(int64_t D, int32_t *threads_per_row, int32_t *chunks_per_thread);
+/* Layout the kernels of algorithm `algo` use for dimension D: threads per
+ * row and float4 chunks per thread (for tests and reports).  PSO (and
+ * evox_eval) use up to 4 chunks per thread, CSO one chunk per thread up to
+ * D = 4096; both reach 1024 threads x 8 chunks at D = EVOX_MAX_D. */
+int evox_row_layout(int32_t algo, int64_t D, int32_t *threads_per_row, int32_t *chunks_per_thread);
 
 /* Diagnostic: out[4 k + m] = word m of Philox(seed, (k, c1, c2, c3)) for
  * k < n_ctr, computed by the device Philox the kernels use (device out). */

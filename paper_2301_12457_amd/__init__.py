@@ -78,7 +78,7 @@ def lib():
             "evox_cso_refresh": ([P, i32], i32),
             "evox_best": ([P, P, P, P], i32),
             "evox_generation": ([P], i64),
-            "evox_row_layout": ([i64, P, P], i32),
+            "evox_row_layout": ([i32, i64, P, P], i32),
             "evox_philox_fill": ([u64, u32, u32, u32, i64, P, P], i32),
             "evox_profile": ([P, i32], i32),
             "evox_profile_read": ([P, P, P, P], i32),
@@ -109,9 +109,9 @@ def _ptr(t):
     return ctypes.c_void_p(t.data_ptr()) if t is not None else None
 
 
-def row_layout(D):
+def row_layout(D, algo=PSO):
     g, n = ctypes.c_int32(0), ctypes.c_int32(0)
-    _check(lib().evox_row_layout(D, ctypes.byref(g), ctypes.byref(n)))
+    _check(lib().evox_row_layout(algo, D, ctypes.byref(g), ctypes.byref(n)))
     return g.value, n.value
 
 

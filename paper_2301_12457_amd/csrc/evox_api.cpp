@@ -37,24 +37,25 @@ int hip_fail(hipError_t e, const char *what)
 bool aligned16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
 size_t round256(size_t n) { return (n + 255) & ~(size_t)255; }
 
-// Buckets for the pairing sort: about 8-16 individuals per bucket.
+// Superbuckets of the pairing sort: about 512-1024 individuals each.
 int perm_bits(int64_t N)
 {
     int bits = 0;
-    while ((N >> bits) > 16 && bits < 20) ++bits;
+    while ((N >> bits) > 1024 && bits < kPermMaxBits) ++bits;
     return bits;
 }
 
-// Per-block fp64 column-sum rows of the CSO kernels: at most 2^23 doubles.
+// Blocks of the CSO kernels (one fp64 column-sum row each): at most 16384
+// and at most 2^24 doubles of partial sums.
 int cso_grid_cap(int64_t ldx)
 {
-    int64_t cap = ((int64_t)1 << 23) / ldx;
-    if (cap > kGridCap) cap = kGridCap;
+    int64_t cap = ((int64_t)1 << 24) / ldx;
+    if (cap > 16384) cap = 16384;
     if (cap < 64) cap = 64;
     return (int)cap;
 }
 
-int grid_for(int64_t groups, int G, int cap)
+int grid_for(int64_t groups, int G, int64_t cap)
 {
     const int64_t rpb = block_for(G) / G;
     int64_t g = (groups + rpb - 1) / rpb;
@@ -64,9 +65,11 @@ int grid_for(int64_t groups, int G, int cap)
 }
 
 struct Plan {
-    int G = 0, nit = 0, grid = 0, cso_grid = 0, colsum_grid = 0, bits = 0;
-    size_t best = 0, pval = 0, pidx = 0, pcnt = 0;
-    size_t hist = 0, offs = 0, cursor = 0, tkey = 0, tidx = 0, perm = 0, xsum = 0;
+    Layout L{0, 0, 0};
+    int grid = 0, cso_grid = 0, colsum_grid = 0, bits = 0;
+    size_t best = 0, slots = 0;
+    size_t hist = 0, offs = 0, cursor = 0, tkey = 0, tidx = 0, perm = 0, xsum = 0, s1 = 0, ticket = 0;
+    int64_t xsum_rows = 0;
     size_t total = 0;
 };
 
@@ -80,11 +83,14 @@ int make_plan(const evox_params *P, Plan *pl)
         return fail(EVOX_EINVAL, "N = %lld out of range [%lld, 2^31)", (long long)P->N, (long long)nmin);
     if (P->D < 1 || P->D > EVOX_MAX_D)
         return fail(EVOX_EINVAL, "D = %lld out of range [1, %d]", (long long)P->D, EVOX_MAX_D);
+    if (P->algo == EVOX_CSO && P->N > kCsoMaxN)
+        return fail(EVOX_EINVAL, "CSO N = %lld above %lld", (long long)P->N, (long long)kCsoMaxN);
     if (P->ldx < P->D || (P->ldx & 3))
         return fail(EVOX_EINVAL, "ldx = %lld must be >= D and a multiple of 4", (long long)P->ldx);
     Plan p;
-    if (!row_layout(P->D, &p.G, &p.nit)) return fail(EVOX_EINVAL, "no row layout for D = %lld", (long long)P->D);
-    p.grid = grid_for(P->N, p.G, kGridCap);
+    const int family = P->algo == EVOX_CSO ? LAYOUT_NARROW : LAYOUT_WIDE;
+    if (!row_layout(P->D, family, &p.L)) return fail(EVOX_EINVAL, "no row layout for D = %lld", (long long)P->D);
+    p.grid = grid_for(P->N, p.L.G, kMaxGrid);
     size_t off = 0;
     auto take = [&](size_t bytes) {
         const size_t at = off;
@@ -92,13 +98,11 @@ int make_plan(const evox_params *P, Plan *pl)
         return at;
     };
     p.best = take(sizeof(DevBest));
-    p.pval = take(sizeof(float) * kGridCap);
-    p.pidx = take(sizeof(int64_t) * kGridCap);
-    p.pcnt = take(sizeof(uint32_t) * kGridCap);
+    p.slots = take(sizeof(SelSlots));
     if (P->algo == EVOX_CSO) {
         const int cap = cso_grid_cap(P->ldx);
-        p.cso_grid = grid_for(P->N / 2 + (P->N & 1), p.G, cap);
-        p.colsum_grid = grid_for(P->N, p.G, cap);
+        p.cso_grid = grid_for(P->N / 2 + (P->N & 1), p.L.G, cap);
+        p.colsum_grid = grid_for(P->N, p.L.G, cap);
         p.bits = perm_bits(P->N);
         const size_t nb = (size_t)1 << p.bits;
         p.hist = take(4 * nb);
@@ -107,7 +111,10 @@ int make_plan(const evox_params *P, Plan *pl)
         p.tkey = take(4 * (size_t)P->N);
         p.tidx = take(4 * (size_t)P->N);
         p.perm = take(4 * (size_t)P->N);
+        p.xsum_rows = cap;
         p.xsum = take(sizeof(double) * (size_t)cap * (size_t)P->ldx);
+        p.s1 = take(sizeof(double) * (size_t)kMeanStages * (size_t)P->ldx);
+        p.ticket = take(sizeof(uint32_t) * (size_t)((P->ldx + 63) / 64));
     }
     p.total = off;
     *pl = p;
@@ -124,11 +131,9 @@ struct evox_state {
     Plan pl;
     uint32_t k0, k1;
     DevBest *best;
-    float *pval;
-    int64_t *pidx;
-    uint32_t *pcnt;
-    uint32_t *hist, *offs, *cursor, *tkey, *tidx, *perm;
-    double *xsum;
+    SelSlots *slots;
+    uint32_t *hist, *offs, *cursor, *tkey, *tidx, *perm, *ticket;
+    double *xsum, *s1;
     // profiling of the fused generation kernel
     bool prof;
     std::vector<std::pair<hipEvent_t, hipEvent_t>> ev;
@@ -191,10 +196,13 @@ PsoArgs pso_args(evox_state *s)
     a.k0 = s->k0;
     a.k1 = s->k1;
     a.t = 0;
-    a.pval = s->pval;
-    a.pidx = s->pidx;
-    a.pcnt = s->pcnt;
+    a.slots = s->slots;
     return a;
+}
+
+MeanArgs mean_args(evox_state *s, int nparts)
+{
+    return MeanArgs{s->xsum, nparts, s->P.N, s->P.D, s->P.ldx, s->B.xbar, s->s1, s->ticket};
 }
 
 // CSO: fit (optional), swarm mean and best of the current positions.
@@ -204,19 +212,17 @@ int cso_refresh(evox_state *s, bool refit)
     const Plan &pl = s->pl;
     hipError_t e;
     if (refit) {
-        EvalArgs ea{s->B.x, P.N, P.D, P.ldx, s->B.fit, nullptr, nullptr};
-        if ((e = launch_eval(P.fn_id, pl.G, true, ea, pl.grid, s->stream)) != hipSuccess)
+        EvalArgs ea{s->B.x, P.N, P.D, P.ldx, s->B.fit, nullptr};
+        if ((e = launch_eval(P.fn_id, pl.L, true, ea, pl.grid, s->stream)) != hipSuccess)
             return hip_fail(e, "evaluate");
     }
-    if ((e = launch_colsum(pl.G, s->B.x, P.N, P.D, P.ldx, s->xsum, pl.colsum_grid, s->stream)) != hipSuccess)
+    if ((e = launch_colsum(pl.L, s->B.x, P.N, P.D, P.ldx, s->xsum, pl.colsum_grid, s->stream)) != hipSuccess)
         return hip_fail(e, "column sums");
-    if ((e = launch_cso_mean(s->xsum, pl.colsum_grid, P.N, P.D, P.ldx, s->B.xbar, s->stream)) != hipSuccess)
+    if ((e = launch_cso_mean(mean_args(s, pl.colsum_grid), s->stream)) != hipSuccess)
         return hip_fail(e, "swarm mean");
-    const int ng = argmin_partials_grid(P.N);
-    if ((e = launch_argmin_partials(s->B.fit, P.N, s->pval, s->pidx, ng, s->stream)) != hipSuccess)
+    if ((e = launch_argmin_slots(s->B.fit, P.N, s->slots, s->stream)) != hipSuccess)
         return hip_fail(e, "select");
-    if ((e = launch_select(s->pval, s->pidx, nullptr, ng, nullptr, 0, nullptr, s->best, nullptr, nullptr,
-                           s->stream)) != hipSuccess)
+    if ((e = launch_select(s->slots, nullptr, 0, nullptr, s->best, nullptr, nullptr, s->stream)) != hipSuccess)
         return hip_fail(e, "select");
     return EVOX_OK;
 }
@@ -262,11 +268,10 @@ int evox_state_create(const evox_params *params, const evox_buffers *b, void *hi
     s->k0 = (uint32_t)P.seed;
     s->k1 = (uint32_t)(P.seed >> 32);
     s->best = at<DevBest>(b->scratch, pl.best);
-    s->pval = at<float>(b->scratch, pl.pval);
-    s->pidx = at<int64_t>(b->scratch, pl.pidx);
-    s->pcnt = at<uint32_t>(b->scratch, pl.pcnt);
+    s->slots = at<SelSlots>(b->scratch, pl.slots);
     s->hist = s->offs = s->cursor = s->tkey = s->tidx = s->perm = nullptr;
-    s->xsum = nullptr;
+    s->xsum = s->s1 = nullptr;
+    s->ticket = nullptr;
     if (P.algo == EVOX_CSO) {
         s->hist = at<uint32_t>(b->scratch, pl.hist);
         s->offs = at<uint32_t>(b->scratch, pl.offs);
@@ -275,15 +280,31 @@ int evox_state_create(const evox_params *params, const evox_buffers *b, void *hi
         s->tidx = at<uint32_t>(b->scratch, pl.tidx);
         s->perm = at<uint32_t>(b->scratch, pl.perm);
         s->xsum = at<double>(b->scratch, pl.xsum);
+        s->s1 = at<double>(b->scratch, pl.s1);
+        s->ticket = at<uint32_t>(b->scratch, pl.ticket);
     }
     s->prof = false;
     s->ev_used = 0;
     s->improved_base = 0;
+    if (P.algo == EVOX_CSO) {
+        // persistent grid for the pair kernel: every block resident at once
+        int dev = 0, cus = 0;
+        if (hipGetDevice(&dev) == hipSuccess &&
+            hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess) {
+            const int occ = occupancy_cso(P.fn_id, pl.L);
+            const int64_t resident = (int64_t)cus * (occ > 0 ? occ : 1);
+            if (resident < s->pl.cso_grid) s->pl.cso_grid = (int)resident;
+        }
+    }
 
     hipError_t e;
     InitArgs ia{b->x, b->v, P.algo == EVOX_PSO ? b->pbest : nullptr, P.N, P.D, P.ldx, P.lb, P.ub,
                 P.v_lo, P.v_hi, P.v_lo == 0.0f && P.v_hi == 0.0f, s->k0, s->k1};
     if ((e = launch_init(ia, s->stream)) != hipSuccess) {
+        delete s;
+        return hip_fail(e, "init");
+    }
+    if ((e = launch_slots_init(s->slots, s->stream)) != hipSuccess) {
         delete s;
         return hip_fail(e, "init");
     }
@@ -297,6 +318,8 @@ int evox_state_create(const evox_params *params, const evox_buffers *b, void *hi
     } else {
         const size_t nb = (size_t)1 << pl.bits;
         if ((e = launch_zero_u32(s->hist, (int64_t)nb, s->stream)) != hipSuccess ||
+            (e = launch_zero_u32(s->cursor, (int64_t)nb, s->stream)) != hipSuccess ||
+            (e = launch_zero_u32(s->ticket, (P.ldx + 63) / 64, s->stream)) != hipSuccess ||
             (e = best_init(s, std::numeric_limits<float>::infinity(), 0)) != hipSuccess) {
             delete s;
             return hip_fail(e, "init");
@@ -315,66 +338,69 @@ int evox_state_destroy(evox_state *s)
 {
     if (!s) return fail(EVOX_EINVAL, "state is null");
     for (auto &pr : s->ev) {
-        hipEventDestroy(pr.first);
-        hipEventDestroy(pr.second);
+        (void)hipEventDestroy(pr.first);
+        (void)hipEventDestroy(pr.second);
     }
     delete s;
     return EVOX_OK;
 }
 
 static int eval_common(int fn_id, const float *X, int64_t N, int64_t D, int64_t ldx, float *out,
-                       float *pval, int64_t *pidx, hipStream_t st, int *grid_out)
+                       SelSlots *slots, hipStream_t st)
 {
     if (fn_id < 0 || fn_id >= FN_COUNT) return fail(EVOX_EINVAL, "unknown fn_id %d", fn_id);
     if (N < 0 || N >= ((int64_t)1 << 31)) return fail(EVOX_EINVAL, "N = %lld out of range", (long long)N);
     if (D < 1 || D > EVOX_MAX_D) return fail(EVOX_EINVAL, "D = %lld out of range [1, %d]", (long long)D, EVOX_MAX_D);
     if (ldx < D) return fail(EVOX_EINVAL, "ldx = %lld < D", (long long)ldx);
     if (N > 0 && (!X || !out)) return fail(EVOX_EINVAL, "X and out are required");
-    int G, nit;
-    if (!row_layout(D, &G, &nit)) return fail(EVOX_EINVAL, "no row layout for D = %lld", (long long)D);
-    const int grid = grid_for(N, G, kGridCap);
-    if (grid_out) *grid_out = grid;
+    Layout L;
+    if (!row_layout(D, LAYOUT_WIDE, &L)) return fail(EVOX_EINVAL, "no row layout for D = %lld", (long long)D);
+    const int grid = grid_for(N, L.G, kMaxGrid);
     if (N == 0) return EVOX_OK;
     const bool vec = (ldx & 3) == 0 && aligned16(X);
-    EvalArgs a{X, N, D, ldx, out, pval, pidx};
-    hipError_t e = launch_eval(fn_id, G, vec, a, grid, st);
+    EvalArgs a{X, N, D, ldx, out, slots};
+    hipError_t e = launch_eval(fn_id, L, vec, a, grid, st);
     if (e != hipSuccess) return hip_fail(e, "evaluate");
     return EVOX_OK;
 }
 
 int evox_eval(int fn_id, const float *X, int64_t N, int64_t D, float *out, void *hip_stream)
 {
-    return eval_common(fn_id, X, N, D, D, out, nullptr, nullptr, (hipStream_t)hip_stream, nullptr);
+    return eval_common(fn_id, X, N, D, D, out, nullptr, (hipStream_t)hip_stream);
 }
 
 int evox_eval_ld(int fn_id, const float *X, int64_t N, int64_t D, int64_t ldx, float *out,
                  void *hip_stream)
 {
-    return eval_common(fn_id, X, N, D, ldx, out, nullptr, nullptr, (hipStream_t)hip_stream, nullptr);
+    return eval_common(fn_id, X, N, D, ldx, out, nullptr, (hipStream_t)hip_stream);
 }
 
 size_t evox_eval_argmin_scratch_bytes(int64_t)
 {
-    return round256(sizeof(float) * kGridCap) + round256(sizeof(int64_t) * kGridCap);
+    return round256(sizeof(SelSlots));
 }
 
 int evox_eval_argmin(int fn_id, const float *X, int64_t N, int64_t D, int64_t ldx, float *out,
                      float *best_fit_dev, int64_t *best_idx_dev, void *scratch, size_t scratch_bytes,
                      void *hip_stream)
 {
-    if (N < 1) return fail(EVOX_EINVAL, "N = %lld: selection needs at least one row", (long long)N);
+    if (N < 1 || N >= ((int64_t)1 << 31))
+        return fail(EVOX_EINVAL, "N = %lld out of range [1, 2^31) for a selection", (long long)N);
     if (!best_fit_dev || !best_idx_dev || !scratch) return fail(EVOX_EINVAL, "best outputs and scratch are required");
     if (((uintptr_t)scratch & 255u) != 0) return fail(EVOX_EALIGN, "scratch is not 256-byte aligned");
     if (scratch_bytes < evox_eval_argmin_scratch_bytes(N))
         return fail(EVOX_ENOSPC, "scratch has %zu bytes, needs %zu", scratch_bytes, evox_eval_argmin_scratch_bytes(N));
-    float *pval = at<float>(scratch, 0);
-    int64_t *pidx = at<int64_t>(scratch, round256(sizeof(float) * kGridCap));
-    int grid = 0;
+    SelSlots *slots = at<SelSlots>(scratch, 0);
     hipStream_t st = (hipStream_t)hip_stream;
-    int rc = eval_common(fn_id, X, N, D, ldx, out, pval, pidx, st, &grid);
+    // validate before enqueueing anything
+    int rc = eval_common(fn_id, nullptr, 0, D, ldx, nullptr, nullptr, st);
     if (rc != EVOX_OK) return rc;
-    hipError_t e = launch_select(pval, pidx, nullptr, grid, nullptr, 0, nullptr, nullptr, best_fit_dev,
-                                 best_idx_dev, st);
+    if (!X || !out) return fail(EVOX_EINVAL, "X and out are required");
+    hipError_t e = launch_slots_init(slots, st);
+    if (e != hipSuccess) return hip_fail(e, "select init");
+    rc = eval_common(fn_id, X, N, D, ldx, out, slots, st);
+    if (rc != EVOX_OK) return rc;
+    e = launch_select(slots, nullptr, 0, nullptr, nullptr, best_fit_dev, best_idx_dev, st);
     if (e != hipSuccess) return hip_fail(e, "select");
     return EVOX_OK;
 }
@@ -391,20 +417,20 @@ int evox_pso_step(evox_state *s, int64_t n_gens)
     PsoArgs a = pso_args(s);
     hipError_t e;
     // generation t: evaluate x_t, personal and global bests
-    if ((e = launch_pso(fn, pl.G, PSO_EVAL, a, pl.grid, s->stream)) != hipSuccess) return hip_fail(e, "pso eval");
-    if ((e = launch_select(s->pval, s->pidx, s->pcnt, pl.grid, s->B.pbest, s->P.ldx, s->B.gbest, s->best,
-                           nullptr, nullptr, s->stream)) != hipSuccess)
+    if ((e = launch_pso(fn, pl.L, PSO_EVAL, a, pl.grid, s->stream)) != hipSuccess) return hip_fail(e, "pso eval");
+    if ((e = launch_select(s->slots, s->B.pbest, s->P.ldx, s->B.gbest, s->best, nullptr, nullptr,
+                           s->stream)) != hipSuccess)
         return hip_fail(e, "select");
     for (int64_t k = 1; k < n_gens; ++k) {
         a.t = (uint32_t)(s->t + k - 1);  // move of generation t+k-1, evaluation of t+k
-        e = timed(s, [&] { return launch_pso(fn, pl.G, PSO_FUSED, a, pl.grid, s->stream); });
+        e = timed(s, [&] { return launch_pso(fn, pl.L, PSO_FUSED, a, pl.grid, s->stream); });
         if (e != hipSuccess) return hip_fail(e, "pso generation");
-        if ((e = launch_select(s->pval, s->pidx, s->pcnt, pl.grid, s->B.pbest, s->P.ldx, s->B.gbest,
-                               s->best, nullptr, nullptr, s->stream)) != hipSuccess)
+        if ((e = launch_select(s->slots, s->B.pbest, s->P.ldx, s->B.gbest, s->best, nullptr, nullptr,
+                               s->stream)) != hipSuccess)
             return hip_fail(e, "select");
     }
     a.t = (uint32_t)(s->t + n_gens - 1);
-    if ((e = launch_pso(fn, pl.G, PSO_MOVE, a, pl.grid, s->stream)) != hipSuccess) return hip_fail(e, "pso move");
+    if ((e = launch_pso(fn, pl.L, PSO_MOVE, a, pl.grid, s->stream)) != hipSuccess) return hip_fail(e, "pso move");
     s->t += n_gens;
     return EVOX_OK;
 }
@@ -423,13 +449,13 @@ int evox_cso_step(evox_state *s, int64_t n_gens)
         PermArgs pa{P.N, pl.bits, s->k0, s->k1, t, s->hist, s->offs, s->cursor, s->tkey, s->tidx, s->perm};
         if ((e = launch_perm(pa, s->stream)) != hipSuccess) return hip_fail(e, "pairing");
         CsoArgs ca{s->B.x, s->B.v, s->B.fit, s->B.xbar, s->perm, P.N, P.D, P.ldx, P.phi, P.lb, P.ub,
-                   P.clamp_x != 0, s->k0, s->k1, t, s->pval, s->pidx, s->xsum};
-        e = timed(s, [&] { return launch_cso(P.fn_id, pl.G, ca, pl.cso_grid, s->stream); });
+                   P.clamp_x != 0, s->k0, s->k1, t, s->slots, s->xsum};
+        e = timed(s, [&] { return launch_cso(P.fn_id, pl.L, ca, pl.cso_grid, s->stream); });
         if (e != hipSuccess) return hip_fail(e, "cso generation");
-        if ((e = launch_cso_mean(s->xsum, pl.cso_grid, P.N, P.D, P.ldx, s->B.xbar, s->stream)) != hipSuccess)
+        if ((e = launch_cso_mean(mean_args(s, pl.cso_grid), s->stream)) != hipSuccess)
             return hip_fail(e, "swarm mean");
-        if ((e = launch_select(s->pval, s->pidx, nullptr, pl.cso_grid, nullptr, 0, nullptr, s->best, nullptr,
-                               nullptr, s->stream)) != hipSuccess)
+        if ((e = launch_select(s->slots, nullptr, 0, nullptr, s->best, nullptr, nullptr, s->stream)) !=
+            hipSuccess)
             return hip_fail(e, "select");
     }
     s->t += n_gens;
@@ -463,12 +489,14 @@ int evox_best(evox_state *s, float *best_fit, int64_t *best_idx, float *best_x_h
 
 int64_t evox_generation(const evox_state *s) { return s ? s->t : -1; }
 
-int evox_row_layout(int64_t D, int32_t *threads_per_row, int32_t *chunks_per_thread)
+int evox_row_layout(int32_t algo, int64_t D, int32_t *threads_per_row, int32_t *chunks_per_thread)
 {
-    int G, nit;
-    if (!row_layout(D, &G, &nit) || D > EVOX_MAX_D) return fail(EVOX_EINVAL, "no row layout for D = %lld", (long long)D);
-    if (threads_per_row) *threads_per_row = G;
-    if (chunks_per_thread) *chunks_per_thread = nit;
+    if (algo != EVOX_PSO && algo != EVOX_CSO) return fail(EVOX_EINVAL, "unknown algo %d", algo);
+    Layout L;
+    if (D > EVOX_MAX_D || !row_layout(D, algo == EVOX_CSO ? LAYOUT_NARROW : LAYOUT_WIDE, &L))
+        return fail(EVOX_EINVAL, "no row layout for D = %lld", (long long)D);
+    if (threads_per_row) *threads_per_row = L.G;
+    if (chunks_per_thread) *chunks_per_thread = L.nit;
     return EVOX_OK;
 }
 

@@ -4,14 +4,15 @@
 //
 // Pairing (CSO).  The permutation is the order of the individuals by
 // (key, index), key_i = Philox stream-4 word of individual i at generation t.
-// Keys are uniform 32-bit numbers, so a bucket sort does it in four light
-// passes:
-//   k_perm_hist     count the keys per bucket (top `bits` key bits)
-//   k_perm_scan     exclusive scan of the counts -> bucket offsets
-//   k_perm_scatter  place (key, index) into its bucket
-//   k_perm_rank     rank each entry inside its bucket by (key, index) and
-//                   write the index to its final position
-// Buckets hold 8-16 entries on average, so the in-bucket rank is a short scan.
+// Keys are uniform 32-bit numbers, so a superbucket sort does it in three
+// light passes over 4096-individual chunks:
+//   k_perm_count  per-superbucket counts (top `bits` key bits; LDS
+//                 histogram, one global atomic per nonempty bucket)
+//   k_perm_place  scan of the counts, per-block range reservation, and
+//                 placement of (key, index) into the superbucket ranges
+//   k_perm_sort   one block per superbucket (~1000 entries): counting sort on
+//                 the next 8 key bits in LDS, then ranks inside sub-buckets,
+//                 written as the permutation
 #include "evox_kernels.hpp"
 
 namespace evox {
@@ -60,31 +61,30 @@ hipError_t launch_init(const InitArgs &a, hipStream_t s)
 }
 
 // ---------------------------------------------------------------------------
-// Second pass of the selection: one block reduces the partials, stores the
-// result, and copies the selected row (ldx floats) to row_out.
+// Second pass of the selection: one block reduces the kSlots keys (and the
+// improved-row counts), resets them for the next launch, stores the result,
+// and copies the selected row (ldx floats) to row_out.
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(1024) void k_select(const float *pval, const int64_t *pidx,
-                                                 const uint32_t *pcnt, int n, const float *rows,
-                                                 int64_t ldx, float *row_out, DevBest *best,
-                                                 float *bf_out, int64_t *bi_out)
+__global__ __launch_bounds__(1024) void k_select(SelSlots *sl, const float *rows, int64_t ldx,
+                                                 float *row_out, DevBest *best, float *bf_out,
+                                                 int64_t *bi_out)
 {
-    __shared__ float sv[16];
-    __shared__ int64_t si[16];
+    __shared__ uint64_t sk[16];
     __shared__ uint32_t sc[16];
     __shared__ int64_t sel;
-    float v = __builtin_nanf("");
-    int64_t i = INT64_MAX;
+    uint64_t k = kNoKey;
     uint32_t cnt = 0;
-    for (int q = threadIdx.x; q < n; q += blockDim.x) {
-        if (cand_better(pval[q], pidx[q], v, i)) {
-            v = pval[q];
-            i = pidx[q];
-        }
-        if (pcnt) cnt += pcnt[q];
+    for (int q = threadIdx.x; q < kSlots; q += blockDim.x) {
+        const uint64_t kq = sl->key[q];
+        k = kq < k ? kq : k;
+        cnt += sl->cnt[q];
+        sl->key[q] = kNoKey;
+        sl->cnt[q] = 0;
     }
-    block_argmin(v, i, cnt, sv, si, sc);
+    block_min_key(k, cnt, sk, sc);
     if (threadIdx.x == 0) {
-        if (i == INT64_MAX) i = 0;
+        const float v = key_value(k);
+        const int64_t i = k == kNoKey ? 0 : key_index(k);
         if (best) {
             best->f = v;
             best->i = i;
@@ -101,12 +101,25 @@ __global__ __launch_bounds__(1024) void k_select(const float *pval, const int64_
     }
 }
 
-hipError_t launch_select(const float *pval, const int64_t *pidx, const uint32_t *pcnt, int nparts,
-                         const float *rows, int64_t ldx, float *row_out, DevBest *best,
-                         float *best_f_out, int64_t *best_i_out, hipStream_t s)
+hipError_t launch_select(SelSlots *slots, const float *rows, int64_t ldx, float *row_out,
+                         DevBest *best, float *best_f_out, int64_t *best_i_out, hipStream_t s)
 {
-    hipLaunchKernelGGL(k_select, dim3(1), dim3(1024), 0, s, pval, pidx, pcnt, nparts, rows, ldx,
-                       row_out, best, best_f_out, best_i_out);
+    hipLaunchKernelGGL(k_select, dim3(1), dim3(1024), 0, s, slots, rows, ldx, row_out, best,
+                       best_f_out, best_i_out);
+    return hipGetLastError();
+}
+
+__global__ __launch_bounds__(1024) void k_slots_init(SelSlots *sl)
+{
+    for (int q = threadIdx.x; q < kSlots; q += blockDim.x) {
+        sl->key[q] = kNoKey;
+        sl->cnt[q] = 0;
+    }
+}
+
+hipError_t launch_slots_init(SelSlots *slots, hipStream_t s)
+{
+    hipLaunchKernelGGL(k_slots_init, dim3(1), dim3(1024), 0, s, slots);
     return hipGetLastError();
 }
 
@@ -169,33 +182,23 @@ hipError_t launch_zero_u32(uint32_t *dst, int64_t n, hipStream_t s)
 }
 
 // First pass of the selection over a stored fitness array.
-__global__ __launch_bounds__(256) void k_argmin_partials(const float *f, int64_t n, float *pval,
-                                                         int64_t *pidx)
+__global__ __launch_bounds__(256) void k_argmin_slots(const float *f, int64_t n, SelSlots *sl)
 {
-    __shared__ float sv[4];
-    __shared__ int64_t si[4];
+    __shared__ uint64_t sk[4];
     __shared__ uint32_t sc[4];
-    float v = __builtin_nanf("");
-    int64_t i = INT64_MAX;
-    uint32_t dummy = 0;
-    for (int64_t j = (int64_t)blockIdx.x * 256 + threadIdx.x; j < n; j += (int64_t)gridDim.x * 256)
-        if (cand_better(f[j], j, v, i)) {
-            v = f[j];
-            i = j;
-        }
-    block_argmin(v, i, dummy, sv, si, sc);
-    if (threadIdx.x == 0) {
-        pval[blockIdx.x] = v;
-        pidx[blockIdx.x] = i;
+    uint64_t k = kNoKey;
+    uint32_t none = 0;
+    for (int64_t j = (int64_t)blockIdx.x * 256 + threadIdx.x; j < n; j += (int64_t)gridDim.x * 256) {
+        const uint64_t kj = sel_key(f[j], j);
+        k = kj < k ? kj : k;
     }
+    block_min_key(k, none, sk, sc);
+    if (threadIdx.x == 0) slot_commit(sl, k, 0);
 }
 
-int argmin_partials_grid(int64_t N) { return (int)flat_grid(N); }
-
-hipError_t launch_argmin_partials(const float *f, int64_t N, float *pval, int64_t *pidx, int grid,
-                                  hipStream_t s)
+hipError_t launch_argmin_slots(const float *f, int64_t N, SelSlots *slots, hipStream_t s)
 {
-    hipLaunchKernelGGL(k_argmin_partials, dim3(grid), dim3(256), 0, s, f, N, pval, pidx);
+    hipLaunchKernelGGL(k_argmin_slots, dim3(flat_grid(N)), dim3(256), 0, s, f, N, slots);
     return hipGetLastError();
 }
 
@@ -228,129 +231,238 @@ __device__ __forceinline__ uint32_t bucket_of(uint32_t key, int bits)
     return bits ? key >> (32 - bits) : 0u;
 }
 
-__global__ __launch_bounds__(256) void k_perm_hist(PermArgs a)
+// Keys of the 16 individuals 4 * (4 * (blockIdx * 256) + r * 256 + tid) + e,
+// r, e < 4, handled by one thread of a perm block (4096 per block).
+template <typename F>
+__device__ __forceinline__ void for_block_keys(const PermArgs &a, F &&f)
 {
-    const int64_t nq = (a.N + 3) / 4;
-    for (int64_t q = (int64_t)blockIdx.x * 256 + threadIdx.x; q < nq; q += (int64_t)gridDim.x * 256) {
-        const U4 r = philox((uint32_t)q, 0u, a.t, STREAM_PERM, a.k0, a.k1);
-        const uint32_t k4[4] = {r.x, r.y, r.z, r.w};
+    const int64_t q0 = (int64_t)blockIdx.x * (kPermChunk / 4);
 #pragma unroll
-        for (int e = 0; e < 4; ++e)
-            if (4 * q + e < a.N) atomicAdd(&a.hist[bucket_of(k4[e], a.bits)], 1u);
+    for (int r = 0; r < 4; ++r) {
+        const int64_t q = q0 + r * 256 + threadIdx.x;
+        if (4 * q < a.N) {
+            const U4 w = philox((uint32_t)q, 0u, a.t, STREAM_PERM, a.k0, a.k1);
+            const uint32_t k4[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+                if (4 * q + e < a.N) f(k4[e], 4 * q + e);
+        }
     }
 }
 
-// One block: offs[b] = sum of hist[0..b), offs[nb] = N, cursor = offs, and
-// the counts are cleared for the next generation.
-__global__ __launch_bounds__(1024) void k_perm_scan(PermArgs a)
+// Pass 1: per-superbucket counts (LDS histogram per block, then one global
+// atomic per nonempty bucket).
+__global__ __launch_bounds__(256) void k_perm_count(PermArgs a)
 {
-    __shared__ uint32_t part[1024];
-    const int64_t nb = (int64_t)1 << a.bits;
-    const int64_t per = (nb + 1023) / 1024;
-    const int64_t lo = threadIdx.x * per, hi = lo + per < nb ? lo + per : nb;
-    uint32_t s = 0;
-    for (int64_t b = lo; b < hi; ++b) s += a.hist[b];
-    part[threadIdx.x] = s;
+    __shared__ uint32_t h[kPermMaxBuckets];
+    const int nb = 1 << a.bits;
+    for (int b = threadIdx.x; b < nb; b += 256) h[b] = 0;
     __syncthreads();
-    // Hillis-Steele inclusive scan over the 1024 thread sums
-    for (int off = 1; off < 1024; off <<= 1) {
-        const uint32_t v = threadIdx.x >= off ? part[threadIdx.x - off] : 0u;
-        __syncthreads();
-        part[threadIdx.x] += v;
-        __syncthreads();
-    }
-    uint32_t run = threadIdx.x ? part[threadIdx.x - 1] : 0u;
-    for (int64_t b = lo; b < hi; ++b) {
-        const uint32_t c = a.hist[b];
-        a.offs[b] = run;
-        a.cursor[b] = run;
-        a.hist[b] = 0u;
-        run += c;
-    }
-    if (threadIdx.x == 0) a.offs[nb] = (uint32_t)a.N;
+    for_block_keys(a, [&](uint32_t key, int64_t) { atomicAdd(&h[bucket_of(key, a.bits)], 1u); });
+    __syncthreads();
+    for (int b = threadIdx.x; b < nb; b += 256)
+        if (h[b]) atomicAdd(&a.hist[b], h[b]);
 }
 
-__global__ __launch_bounds__(256) void k_perm_scatter(PermArgs a)
+// Exclusive scan of n <= kPermMaxBuckets counts into off (LDS), 256 threads.
+__device__ __forceinline__ void lds_exclusive_scan(const uint32_t *cnt, int n, uint32_t *off)
 {
-    const int64_t nq = (a.N + 3) / 4;
-    for (int64_t q = (int64_t)blockIdx.x * 256 + threadIdx.x; q < nq; q += (int64_t)gridDim.x * 256) {
-        const U4 r = philox((uint32_t)q, 0u, a.t, STREAM_PERM, a.k0, a.k1);
-        const uint32_t k4[4] = {r.x, r.y, r.z, r.w};
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            const int64_t i = 4 * q + e;
-            if (i < a.N) {
-                const uint32_t pos = atomicAdd(&a.cursor[bucket_of(k4[e], a.bits)], 1u);
-                a.tkey[pos] = k4[e];
-                a.tidx[pos] = (uint32_t)i;
+    __shared__ uint32_t tsum[256];
+    const int per = (n + 255) / 256, lo = threadIdx.x * per;
+    const int hi = lo + per < n ? lo + per : n;
+    uint32_t s = 0;
+    for (int b = lo; b < hi; ++b) s += cnt[b];
+    tsum[threadIdx.x] = s;
+    __syncthreads();
+    for (int d = 1; d < 256; d <<= 1) {
+        const uint32_t v = threadIdx.x >= d ? tsum[threadIdx.x - d] : 0u;
+        __syncthreads();
+        tsum[threadIdx.x] += v;
+        __syncthreads();
+    }
+    uint32_t run = threadIdx.x ? tsum[threadIdx.x - 1] : 0u;
+    for (int b = lo; b < hi; ++b) {
+        off[b] = run;
+        run += cnt[b];
+    }
+    __syncthreads();
+}
+
+// Pass 2: every block scans the counts (block 0 also publishes the offsets),
+// reserves a range per bucket for its own keys, and places (key, index).
+__global__ __launch_bounds__(256) void k_perm_place(PermArgs a)
+{
+    __shared__ uint32_t cnt[kPermMaxBuckets];
+    __shared__ uint32_t off[kPermMaxBuckets];
+    const int nb = 1 << a.bits;
+    for (int b = threadIdx.x; b < nb; b += 256) cnt[b] = a.hist[b];
+    __syncthreads();
+    lds_exclusive_scan(cnt, nb, off);
+    if (blockIdx.x == 0) {
+        for (int b = threadIdx.x; b < nb; b += 256) a.offs[b] = off[b];
+        if (threadIdx.x == 0) a.offs[nb] = (uint32_t)a.N;
+    }
+    for (int b = threadIdx.x; b < nb; b += 256) cnt[b] = 0;
+    __syncthreads();
+    for_block_keys(a, [&](uint32_t key, int64_t) { atomicAdd(&cnt[bucket_of(key, a.bits)], 1u); });
+    __syncthreads();
+    for (int b = threadIdx.x; b < nb; b += 256)
+        if (cnt[b]) off[b] += atomicAdd(&a.cursor[b], cnt[b]);
+    __syncthreads();
+    for_block_keys(a, [&](uint32_t key, int64_t i) {
+        const uint32_t pos = atomicAdd(&off[bucket_of(key, a.bits)], 1u);
+        a.tkey[pos] = key;
+        a.tidx[pos] = (uint32_t)i;
+    });
+}
+
+// Pass 3: one block per superbucket orders its entries by (key, index):
+// a counting sort on the next 8 key bits (256 sub-buckets of ~4 entries) in
+// LDS, then each entry's rank inside its sub-bucket by comparison, written
+// as the permutation.  The bucket's count and cursor are then cleared for
+// the next generation.  A bucket larger than the LDS capacity (not expected
+// for uniform keys) is ranked directly in global memory instead.
+__global__ __launch_bounds__(256) void k_perm_sort(PermArgs a)
+{
+    __shared__ uint32_t K[kPermSortCap], I[kPermSortCap];
+    __shared__ uint32_t cnt[256], start[256], cur[256];
+    const int b = blockIdx.x;
+    const uint32_t lo = a.offs[b], n = a.hist[b];
+    const int shift = 24 - a.bits;  // the 8 key bits below the superbucket bits
+    if (n <= (uint32_t)kPermSortCap) {
+        cnt[threadIdx.x] = 0;
+        __syncthreads();
+        for (uint32_t q = threadIdx.x; q < n; q += 256)
+            atomicAdd(&cnt[(a.tkey[lo + q] >> shift) & 255u], 1u);
+        __syncthreads();
+        if (threadIdx.x < 64) {  // exclusive scan of 256 counts by one wave, 4 per lane
+            const int l = threadIdx.x;
+            const uint32_t c0 = cnt[4 * l], c1 = cnt[4 * l + 1], c2 = cnt[4 * l + 2], c3 = cnt[4 * l + 3];
+            uint32_t tot = c0 + c1 + c2 + c3, inc = tot;
+            for (int d = 1; d < 64; d <<= 1) {
+                const uint32_t o = __shfl_up(inc, d, 64);
+                if (l >= d) inc += o;
             }
+            uint32_t ex = inc - tot;
+            start[4 * l] = ex;
+            start[4 * l + 1] = ex + c0;
+            start[4 * l + 2] = ex + c0 + c1;
+            start[4 * l + 3] = ex + c0 + c1 + c2;
+        }
+        __syncthreads();
+        cur[threadIdx.x] = start[threadIdx.x];
+        __syncthreads();
+        for (uint32_t q = threadIdx.x; q < n; q += 256) {
+            const uint32_t key = a.tkey[lo + q];
+            const uint32_t pos = atomicAdd(&cur[(key >> shift) & 255u], 1u);
+            K[pos] = key;
+            I[pos] = a.tidx[lo + q];
+        }
+        __syncthreads();
+        for (uint32_t q = threadIdx.x; q < n; q += 256) {
+            const uint32_t key = K[q], idx = I[q], sb = (key >> shift) & 255u;
+            const uint32_t s0 = start[sb], s1 = s0 + cnt[sb];
+            uint32_t rank = 0;
+            for (uint32_t r = s0; r < s1; ++r) rank += (K[r] < key || (K[r] == key && I[r] < idx)) ? 1u : 0u;
+            a.perm[lo + s0 + rank] = idx;
+        }
+    } else {
+        for (uint32_t p = threadIdx.x; p < n; p += 256) {
+            const uint32_t key = a.tkey[lo + p], idx = a.tidx[lo + p];
+            uint32_t rank = 0;
+            for (uint32_t q = 0; q < n; ++q) {
+                const uint32_t kq = a.tkey[lo + q], iq = a.tidx[lo + q];
+                rank += (kq < key || (kq == key && iq < idx)) ? 1u : 0u;
+            }
+            a.perm[lo + rank] = idx;
         }
     }
-}
-
-__global__ __launch_bounds__(256) void k_perm_rank(PermArgs a)
-{
-    for (int64_t p = (int64_t)blockIdx.x * 256 + threadIdx.x; p < a.N; p += (int64_t)gridDim.x * 256) {
-        const uint32_t key = a.tkey[p], idx = a.tidx[p];
-        const uint32_t b = bucket_of(key, a.bits);
-        const uint32_t lo = a.offs[b], hi = a.offs[b + 1];
-        uint32_t rank = 0;
-        for (uint32_t q = lo; q < hi; ++q) {
-            const uint32_t kq = a.tkey[q], iq = a.tidx[q];
-            rank += (kq < key || (kq == key && iq < idx)) ? 1u : 0u;
-        }
-        a.perm[lo + rank] = idx;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        a.hist[b] = 0;
+        a.cursor[b] = 0;
     }
 }
 
 hipError_t launch_perm(const PermArgs &a, hipStream_t s)
 {
-    const int64_t nq = (a.N + 3) / 4;
-    int64_t g1 = (nq + 255) / 256, g2 = (a.N + 255) / 256;
-    if (g1 > kGridCap) g1 = kGridCap;
-    if (g2 > kGridCap) g2 = kGridCap;
-    hipLaunchKernelGGL(k_perm_hist, dim3((unsigned)g1), dim3(256), 0, s, a);
-    hipLaunchKernelGGL(k_perm_scan, dim3(1), dim3(1024), 0, s, a);
-    hipLaunchKernelGGL(k_perm_scatter, dim3((unsigned)g1), dim3(256), 0, s, a);
-    hipLaunchKernelGGL(k_perm_rank, dim3((unsigned)g2), dim3(256), 0, s, a);
+    const unsigned chunks = (unsigned)((a.N + kPermChunk - 1) / kPermChunk);
+    const unsigned nb = 1u << a.bits;
+    hipLaunchKernelGGL(k_perm_count, dim3(chunks), dim3(256), 0, s, a);
+    hipLaunchKernelGGL(k_perm_place, dim3(chunks), dim3(256), 0, s, a);
+    hipLaunchKernelGGL(k_perm_sort, dim3(nb), dim3(256), 0, s, a);
     return hipGetLastError();
 }
 
-// xbar_j = (sum over the partial rows, in order) / N, rounded once; zero in
-// the padding columns.  Block: 64 columns x 4 partial-row lanes.
-__global__ __launch_bounds__(256) void k_cso_mean(const double *xsum, int nparts, int64_t N,
-                                                  int64_t D, int64_t ldx, float *xbar)
+// xbar = (sum of the per-block partial rows) / N, rounded once, in two
+// stages.  Block (tile, rg) of 64 columns x 4 lanes: lane l sums partial rows
+// rg + S (l + 4 u), u = 0, 1, ... (S = kMeanStages) in that order, the four
+// lanes are added in lane order into s1[rg].  The last block of a tile to
+// finish sums s1[0..S) the same way (lane l: stages l + 4 u) and writes the
+// mean.  Padding columns get 0.  Loads go out in batches of 8.
+__device__ __forceinline__ double strided_sum(const double *base, int64_t first, int64_t step,
+                                              int64_t end, int64_t pitch)
+{
+    double s = 0.0;
+    for (int64_t q0 = first; q0 < end; q0 += 8 * step) {
+        double v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const int64_t q = q0 + u * step;
+            v[u] = q < end ? __hip_atomic_load(base + q * pitch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)
+                           : 0.0;
+        }
+#pragma unroll
+        for (int u = 0; u < 8; ++u) s += v[u];
+    }
+    return s;
+}
+
+__global__ __launch_bounds__(256) void k_cso_mean(MeanArgs m)
 {
     __shared__ double part[4][64];
+    __shared__ int last;
     const int col = threadIdx.x & 63, lane = threadIdx.x >> 6;
-    const int64_t j = (int64_t)blockIdx.x * 64 + col;
+    const int64_t tile = blockIdx.x, rg = blockIdx.y;
+    const int64_t j = tile * 64 + col;
     double s = 0.0;
-    if (j < D)
-        for (int q = lane; q < nparts; q += 4) s += xsum[(int64_t)q * ldx + j];
+    if (j < m.D) s = strided_sum(m.xsum + j, rg + (int64_t)kMeanStages * lane, 4 * kMeanStages, m.nparts, m.ldx);
     part[lane][col] = s;
     __syncthreads();
-    if (lane == 0 && j < ldx) {
-        const double t = ((part[0][col] + part[1][col]) + part[2][col]) + part[3][col];
-        xbar[j] = j < D ? (float)(t / (double)N) : 0.0f;
+    if (lane == 0 && j < m.D)
+        m.s1[rg * m.ldx + j] = ((part[0][col] + part[1][col]) + part[2][col]) + part[3][col];
+    __threadfence();
+    __syncthreads();
+    if (threadIdx.x == 0) last = atomicAdd(&m.ticket[tile], 1u) == (uint32_t)(kMeanStages - 1);
+    __syncthreads();
+    if (last) {
+        __threadfence();
+        double t = 0.0;
+        if (j < m.D) t = strided_sum(m.s1 + j, lane, 4, kMeanStages, m.ldx);
+        part[lane][col] = t;
+        __syncthreads();
+        if (lane == 0 && j < m.ldx) {
+            const double u = ((part[0][col] + part[1][col]) + part[2][col]) + part[3][col];
+            m.xbar[j] = j < m.D ? (float)(u / (double)m.N) : 0.0f;
+        }
+        if (threadIdx.x == 0) m.ticket[tile] = 0;
     }
 }
 
-hipError_t launch_cso_mean(const double *xsum, int nparts, int64_t N, int64_t D, int64_t ldx,
-                           float *xbar, hipStream_t s)
+hipError_t launch_cso_mean(const MeanArgs &m, hipStream_t s)
 {
-    const int64_t grid = (ldx + 63) / 64;
-    hipLaunchKernelGGL(k_cso_mean, dim3((unsigned)grid), dim3(256), 0, s, xsum, nparts, N, D, ldx,
-                       xbar);
+    const unsigned tiles = (unsigned)((m.ldx + 63) / 64);
+    hipLaunchKernelGGL(k_cso_mean, dim3(tiles, kMeanStages), dim3(256), 0, s, m);
     return hipGetLastError();
 }
 
-#define EVOX_LAUNCH_COLSUM(GG, UNUSED) \
-    hipLaunchKernelGGL((k_colsum<GG>), dim3(grid), dim3(block_for(GG)), 0, s, x, N, D, ldx, xsum)
+#define EVOX_LAUNCH_COLSUM(GG, MM, UNUSED) \
+    hipLaunchKernelGGL((k_colsum<GG, MM>), dim3(grid), dim3(block_for(GG)), 0, s, x, N, D, ldx, xsum)
 
-hipError_t launch_colsum(int G, const float *x, int64_t N, int64_t D, int64_t ldx, double *xsum,
+hipError_t launch_colsum(Layout L, const float *x, int64_t N, int64_t D, int64_t ldx, double *xsum,
                          int grid, hipStream_t s)
 {
-    EVOX_G_CASES(EVOX_LAUNCH_COLSUM, 0)
+    switch (L.G * 16 + L.maxit) { EVOX_NARROW_CASES(EVOX_LAUNCH_COLSUM, 0) default: return hipErrorInvalidValue; }
     return hipGetLastError();
 }
 
@@ -365,23 +477,36 @@ hipError_t launch_colsum(int G, const float *x, int64_t N, int64_t D, int64_t ld
     default: return hipErrorInvalidValue;                                                         \
     }
 
-hipError_t launch_pso(int fn, int G, int mode, const PsoArgs &a, int grid, hipStream_t s)
+hipError_t launch_pso(int fn, Layout L, int mode, const PsoArgs &a, int grid, hipStream_t s)
 {
     if (mode == PSO_MOVE) fn = FN_SPHERE;  // the move does not evaluate
-#define EVOX_CALL_PSO(F) launch_pso_t<F>(G, mode, a, grid, s)
+#define EVOX_CALL_PSO(F) launch_pso_t<F>(L, mode, a, grid, s)
     EVOX_FN_SWITCH(EVOX_CALL_PSO)
 }
 
-hipError_t launch_eval(int fn, int G, bool vec, const EvalArgs &a, int grid, hipStream_t s)
+hipError_t launch_eval(int fn, Layout L, bool vec, const EvalArgs &a, int grid, hipStream_t s)
 {
-#define EVOX_CALL_EVAL(F) launch_eval_t<F>(G, vec, a, grid, s)
+#define EVOX_CALL_EVAL(F) launch_eval_t<F>(L, vec, a, grid, s)
     EVOX_FN_SWITCH(EVOX_CALL_EVAL)
 }
 
-hipError_t launch_cso(int fn, int G, const CsoArgs &a, int grid, hipStream_t s)
+hipError_t launch_cso(int fn, Layout L, const CsoArgs &a, int grid, hipStream_t s)
 {
-#define EVOX_CALL_CSO(F) launch_cso_t<F>(G, a, grid, s)
+#define EVOX_CALL_CSO(F) launch_cso_t<F>(L, a, grid, s)
     EVOX_FN_SWITCH(EVOX_CALL_CSO)
+}
+
+int occupancy_cso(int fn, Layout L)
+{
+    switch (fn) {
+    case FN_SPHERE: return occupancy_cso_t<FN_SPHERE>(L);
+    case FN_ACKLEY: return occupancy_cso_t<FN_ACKLEY>(L);
+    case FN_RASTRIGIN: return occupancy_cso_t<FN_RASTRIGIN>(L);
+    case FN_GRIEWANK: return occupancy_cso_t<FN_GRIEWANK>(L);
+    case FN_ROSENBROCK: return occupancy_cso_t<FN_ROSENBROCK>(L);
+    case FN_SCHWEFEL: return occupancy_cso_t<FN_SCHWEFEL>(L);
+    default: return 0;
+    }
 }
 
 }  // namespace evox

@@ -24,26 +24,40 @@ enum { FN_SPHERE = 0, FN_ACKLEY, FN_RASTRIGIN, FN_GRIEWANK, FN_ROSENBROCK, FN_SC
 // Random-stream ids (fourth Philox counter word).
 enum { STREAM_INIT_X = 0, STREAM_INIT_V = 1, STREAM_PSO = 2, STREAM_CSO = 3, STREAM_PERM = 4 };
 
-constexpr int kBlock = 256;     // threads per block when a row takes <= 256 lanes
-constexpr int kGridCap = 2048;  // blocks per launch at most (8 per CU on 256 CUs)
+constexpr int kBlock = 256;              // threads per block when a row takes <= 256 lanes
+constexpr int kGridCap = 2048;           // blocks of the grid-stride kernels (8 per CU on 256 CUs)
+constexpr int64_t kMaxGrid = 1 << 20;    // blocks of the row kernels at most (grid-stride beyond)
+constexpr int kSlots = 2048;             // selection slots (atomicMin targets)
 constexpr int kMaxG = 1024;
 
 __host__ __device__ constexpr int block_for(int G) { return G > kBlock ? G : kBlock; }
-__host__ __device__ constexpr int maxit_for(int G) { return G == kMaxG ? 8 : 4; }
 
-// Threads per row and chunks per thread for dimension D: the smallest G that
-// needs at most 4 chunks per lane (8 at G = 1024).  Returns false when D is
-// beyond what one row group holds in registers.
-inline bool row_layout(int64_t D, int *G_out, int *nit_out)
+// Row layout: G lanes per row, MAXIT float4 chunk registers per lane, nit of
+// them used.  Two families:
+//   wide    at most 4 chunks per lane (8 at G = 1024): the PSO and the
+//           evaluation kernels, which stream whole rows and want few lanes
+//           per row reduction;
+//   narrow  one chunk per lane up to D = 4096 (then G = 1024, up to 8): the
+//           CSO kernels, whose random row gathers want a row in one load
+//           instruction and few registers per lane.
+// The layout depends only on (D, family), so every kernel of a state reduces
+// a row in the same order and produces bit-identical fitness.
+enum { LAYOUT_WIDE = 4, LAYOUT_NARROW = 1 };
+
+struct Layout {
+    int G, maxit, nit;
+};
+
+inline bool row_layout(int64_t D, int family, Layout *L)
 {
     if (D < 1) return false;
     const int64_t c4 = (D + 3) / 4;
     int G = 4;
-    while (G < kMaxG && (c4 + G - 1) / G > 4) G *= 2;
+    while (G < kMaxG && (c4 + G - 1) / G > family) G *= 2;
     const int64_t nit = (c4 + G - 1) / G;
-    if (nit > maxit_for(G)) return false;
-    *G_out = G;
-    *nit_out = (int)nit;
+    const int maxit = G == kMaxG ? 8 : family;
+    if (nit > maxit) return false;
+    *L = Layout{G, maxit, (int)nit};
     return true;
 }
 
@@ -283,55 +297,78 @@ __device__ __forceinline__ float row_fitness(const float4 (&xr)[MAXIT], int g, i
 
 // ---------------------------------------------------------------------------
 // Selection order: smaller value, then lower index; -0 == +0; NaN after all
-// numbers.  A total order, so any reduction tree gives the same winner.
+// numbers.  A total order, so any reduction tree gives the same winner.  It
+// is encoded as one 64-bit key, (order-preserving value bits << 32) | index,
+// so the order is an unsigned integer min and a block's candidate is folded
+// into a slot with one atomicMin.
 // ---------------------------------------------------------------------------
-__device__ __forceinline__ bool cand_better(float a, int64_t ia, float b, int64_t ib)
+__device__ __forceinline__ uint64_t sel_key(float v, int64_t i)
 {
-    const bool na = a != a, nb = b != b;
-    if (na || nb) return (na && nb) ? ia < ib : nb;
-    if (a < b) return true;
-    if (b < a) return false;
-    return ia < ib;
+    uint32_t o;
+    if (v != v) {
+        o = 0xFFFFFFFFu;
+    } else {
+        uint32_t b = __float_as_uint(v);
+        if ((b << 1) == 0) b = 0;  // -0 -> +0
+        o = (b & 0x80000000u) ? ~b : (b | 0x80000000u);
+    }
+    return ((uint64_t)o << 32) | (uint32_t)i;
 }
 
-__device__ __forceinline__ int64_t shfl_xor_i64(int64_t v, int m)
+__device__ __forceinline__ float key_value(uint64_t k)
+{
+    const uint32_t o = (uint32_t)(k >> 32);
+    if (o == 0xFFFFFFFFu) return __builtin_nanf("");
+    return __uint_as_float((o & 0x80000000u) ? (o & 0x7FFFFFFFu) : ~o);
+}
+
+__device__ __forceinline__ int64_t key_index(uint64_t k) { return (int64_t)(uint32_t)k; }
+
+constexpr uint64_t kNoKey = ~(uint64_t)0;
+
+__device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t v, int m)
 {
     const int lo = __shfl_xor((int)(uint32_t)v, m, 64);
-    const int hi = __shfl_xor((int)(uint32_t)((uint64_t)v >> 32), m, 64);
-    return (int64_t)(((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo);
+    const int hi = __shfl_xor((int)(uint32_t)(v >> 32), m, 64);
+    return ((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo;
 }
 
-// Block-wide argmin (and a count sum) of per-thread candidates; thread 0
-// gets the result.  sv/si/sc: LDS of blockDim/64 entries each.
-__device__ __forceinline__ void block_argmin(float &v, int64_t &i, uint32_t &cnt, float *sv,
-                                             int64_t *si, uint32_t *sc)
+// Block-wide min of per-thread keys and sum of counts; thread 0 gets them.
+// sk / sc: LDS of blockDim/64 entries each.  Reached by every thread.
+__device__ __forceinline__ void block_min_key(uint64_t &k, uint32_t &cnt, uint64_t *sk, uint32_t *sc)
 {
 #pragma unroll
     for (int m = 32; m >= 1; m >>= 1) {
-        const float ov = __shfl_xor(v, m, 64);
-        const int64_t oi = shfl_xor_i64(i, m);
+        const uint64_t o = shfl_xor_u64(k, m);
+        k = o < k ? o : k;
         cnt += (uint32_t)__shfl_xor((int)cnt, m, 64);
-        if (cand_better(ov, oi, v, i)) {
-            v = ov;
-            i = oi;
-        }
     }
     const int wave = threadIdx.x / 64, nw = blockDim.x / 64;
     if ((threadIdx.x & 63) == 0) {
-        sv[wave] = v;
-        si[wave] = i;
+        sk[wave] = k;
         sc[wave] = cnt;
     }
     __syncthreads();
-    if (threadIdx.x == 0) {
+    if (threadIdx.x == 0)
         for (int q = 1; q < nw; ++q) {
+            k = sk[q] < k ? sk[q] : k;
             cnt += sc[q];
-            if (cand_better(sv[q], si[q], v, i)) {
-                v = sv[q];
-                i = si[q];
-            }
         }
-    }
+}
+
+// Selection slots in device scratch: every block of a row kernel folds its
+// candidate into key[blockIdx mod kSlots] (and its improved-row count into
+// cnt); k_select reduces the slots and resets them.
+struct SelSlots {
+    uint64_t key[kSlots];
+    uint32_t cnt[kSlots];
+};
+
+__device__ __forceinline__ void slot_commit(SelSlots *sl, uint64_t k, uint32_t cnt)
+{
+    const int s = blockIdx.x & (kSlots - 1);
+    if (k != kNoKey) atomicMin((unsigned long long *)&sl->key[s], (unsigned long long)k);
+    if (cnt) atomicAdd(&sl->cnt[s], cnt);
 }
 
 // Result of a selection, kept in device scratch.

@@ -27,25 +27,24 @@
 namespace evox {
 
 // ---------------------------------------------------------------------------
-// The PSO generation kernel (modes above).  Grid-stride over groups of
-// block_for(G) / G rows; the loop bound is uniform over the block, so the
-// barriers inside row_fitness are reached by every thread.
+// The PSO generation kernel (modes above).  One group of block_for(G) / G
+// rows per block (grid-stride only beyond kMaxGrid blocks); the loop bound is
+// uniform over the block, so the barriers inside row_fitness are reached by
+// every thread.  Each block folds its best (pfit, row) into a selection slot.
 // ---------------------------------------------------------------------------
-template <int FN, int G, int MODE>
+template <int FN, int G, int MAXIT, int MODE>
 __global__ __launch_bounds__(block_for(G)) void k_pso(PsoArgs a)
 {
-    constexpr int B = block_for(G), RPB = B / G, MAXIT = maxit_for(G);
+    constexpr int B = block_for(G), RPB = B / G;
     constexpr bool MOVE = MODE != PSO_EVAL, EVAL = MODE != PSO_MOVE;
     __shared__ float nbr[(FN == FN_ROSENBROCK && G > 64) ? B * MAXIT : 1];
     __shared__ float red[2 * (B / 64)];
-    __shared__ float sv[B / 64];
-    __shared__ int64_t si[B / 64];
+    __shared__ uint64_t sk[B / 64];
     __shared__ uint32_t sc[B / 64];
 
     const int tid = threadIdx.x, g = tid % G, slot = tid / G;
     const int64_t C4 = (a.D + 3) >> 2;
-    float bv = __builtin_nanf("");
-    int64_t bi = INT64_MAX;
+    uint64_t best = kNoKey;
     uint32_t nimp = 0;
 
     for (int64_t rb = (int64_t)blockIdx.x * RPB; rb < a.N; rb += (int64_t)gridDim.x * RPB) {
@@ -104,45 +103,37 @@ __global__ __launch_bounds__(block_for(G)) void k_pso(PsoArgs a)
                 if (g == 0) {
                     if (imp) a.pf[row] = f;
                     if (a.fit) a.fit[row] = f;
-                    const float nf = imp ? f : pold;
-                    if (cand_better(nf, row, bv, bi)) {
-                        bv = nf;
-                        bi = row;
-                    }
+                    const uint64_t k = sel_key(imp ? f : pold, row);
+                    best = k < best ? k : best;
                     nimp += imp ? 1u : 0u;
                 }
             }
         }
     }
     if constexpr (EVAL) {
-        block_argmin(bv, bi, nimp, sv, si, sc);
-        if (tid == 0) {
-            a.pval[blockIdx.x] = bv;
-            a.pidx[blockIdx.x] = bi;
-            a.pcnt[blockIdx.x] = nimp;
-        }
+        block_min_key(best, nimp, sk, sc);
+        if (tid == 0) slot_commit(a.slots, best, nimp);
     }
 }
 
 // ---------------------------------------------------------------------------
-// Problem.evaluate over any row pitch / alignment; optional block partials
-// of the selection.  VEC: 16-byte aligned rows, float4 loads.
+// Problem.evaluate over any row pitch / alignment; optionally folds each
+// block's best (fitness, row) into a selection slot.  VEC: 16-byte aligned
+// rows, float4 loads.
 // ---------------------------------------------------------------------------
-template <int FN, int G, bool VEC>
+template <int FN, int G, int MAXIT, bool VEC>
 __global__ __launch_bounds__(block_for(G)) void k_eval(EvalArgs a)
 {
-    constexpr int B = block_for(G), RPB = B / G, MAXIT = maxit_for(G);
+    constexpr int B = block_for(G), RPB = B / G;
     __shared__ float nbr[(FN == FN_ROSENBROCK && G > 64) ? B * MAXIT : 1];
     __shared__ float red[2 * (B / 64)];
-    __shared__ float sv[B / 64];
-    __shared__ int64_t si[B / 64];
+    __shared__ uint64_t sk[B / 64];
     __shared__ uint32_t sc[B / 64];
 
     const int tid = threadIdx.x, g = tid % G, slot = tid / G;
     const int64_t C4 = (a.D + 3) >> 2;
-    float bv = __builtin_nanf("");
-    int64_t bi = INT64_MAX;
-    uint32_t dummy = 0;
+    uint64_t best = kNoKey;
+    uint32_t none = 0;
 
     for (int64_t rb = (int64_t)blockIdx.x * RPB; rb < a.N; rb += (int64_t)gridDim.x * RPB) {
         const int64_t row = rb + slot;
@@ -169,82 +160,95 @@ __global__ __launch_bounds__(block_for(G)) void k_eval(EvalArgs a)
         const float f = row_fitness<FN, G, MAXIT>(xr, g, a.D, nbr, red);
         if (active && g == 0) {
             a.out[row] = f;
-            if (cand_better(f, row, bv, bi)) {
-                bv = f;
-                bi = row;
-            }
+            const uint64_t k = sel_key(f, row);
+            best = k < best ? k : best;
         }
     }
-    if (a.pval) {
-        block_argmin(bv, bi, dummy, sv, si, sc);
-        if (tid == 0) {
-            a.pval[blockIdx.x] = bv;
-            a.pidx[blockIdx.x] = bi;
-        }
+    if (a.slots) {
+        block_min_key(best, none, sk, sc);
+        if (tid == 0) slot_commit(a.slots, best, 0);
     }
 }
 
 // ---------------------------------------------------------------------------
-// Column sums of a block's rows: per-thread fp64 sums cs[it][e] of column
-// 4 (g + G it) + e over the rows the thread handled are reduced over the
-// block's row slots in slot order and written to xsum[blockIdx][*].
-// lds: block_for(G) * 4 doubles when G < 256.
+// Column sums of a block's rows for the swarm mean.  Each thread accumulates
+// fp64 sums of its columns 4 (g + G it) + e over the rows it handles (in LDS
+// when a block holds several row slots, in registers otherwise); at the end
+// the slots are combined in slot order and written to xsum[blockIdx][*].
+// The order of every addition is fixed, so the result is reproducible.
 // ---------------------------------------------------------------------------
 template <int G, int MAXIT>
-__device__ __forceinline__ void block_colsum_write(const double (&cs)[MAXIT][4], int64_t D,
-                                                  int64_t ldx, double *xsum, double *lds)
-{
-    constexpr int B = block_for(G), RPB = B / G;
-    const int tid = threadIdx.x, g = tid % G, slot = tid / G;
-    double *dst = xsum + (int64_t)blockIdx.x * ldx;
-    if constexpr (RPB == 1) {
+struct ColAcc {
+    static constexpr int B = block_for(G), RPB = B / G;
+    static constexpr bool kLds = RPB > 1;
+    double *lds;                            // [4 MAXIT][B] when kLds
+    double reg[kLds ? 1 : MAXIT][4];
+
+    __device__ explicit ColAcc(double *l) : lds(l)
+    {
 #pragma unroll
         for (int it = 0; it < MAXIT; ++it)
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
+                if constexpr (kLds)
+                    lds[(it * 4 + e) * B + threadIdx.x] = 0.0;
+                else
+                    reg[it][e] = 0.0;
+            }
+    }
+    __device__ void add(int it, int e, double v)
+    {
+        if constexpr (kLds)
+            lds[(it * 4 + e) * B + threadIdx.x] += v;
+        else
+            reg[it][e] += v;
+    }
+    // Reached by every thread of the block.
+    __device__ void write(int64_t D, int64_t ldx, double *xsum)
+    {
+        const int tid = threadIdx.x;
+        double *dst = xsum + (int64_t)blockIdx.x * ldx;
+        if constexpr (kLds) {
+            __syncthreads();
+            for (int q = tid; q < 4 * G * MAXIT; q += B) {
+                const int it = q / (4 * G), r = q - it * 4 * G, g = r / 4, e = r % 4;
                 const int64_t j = 4 * ((int64_t)g + (int64_t)G * it) + e;
-                if (j < D) dst[j] = cs[it][e];
+                if (j < D) {
+                    const double *col = lds + (it * 4 + e) * B + g;
+                    double t = col[0];
+                    for (int sl = 1; sl < RPB; ++sl) t += col[sl * G];
+                    dst[j] = t;
+                }
             }
-    } else {
+        } else {
+            const int g = tid;  // one row slot: lane g of the row
 #pragma unroll
-        for (int it = 0; it < MAXIT; ++it) {
-            if (4 * (int64_t)G * it >= D) break;  // uniform
+            for (int it = 0; it < MAXIT; ++it)
 #pragma unroll
-            for (int e = 0; e < 4; ++e) lds[slot * 4 * G + 4 * g + e] = cs[it][e];
-            __syncthreads();
-            for (int q = tid; q < 4 * G; q += B) {
-                double s = lds[q];
-                for (int r = 1; r < RPB; ++r) s += lds[r * 4 * G + q];
-                const int64_t j = 4 * (int64_t)G * it + q;
-                if (j < D) dst[j] = s;
-            }
-            __syncthreads();
+                for (int e = 0; e < 4; ++e) {
+                    const int64_t j = 4 * ((int64_t)g + (int64_t)G * it) + e;
+                    if (j < D) dst[j] = reg[it][e];
+                }
         }
     }
-}
+};
 
-template <int FN, int G>
+template <int FN, int G, int MAXIT>
 __global__ __launch_bounds__(block_for(G)) void k_cso(CsoArgs a)
 {
-    constexpr int B = block_for(G), RPB = B / G, MAXIT = maxit_for(G);
+    constexpr int B = block_for(G), RPB = B / G;
     __shared__ float nbr[(FN == FN_ROSENBROCK && G > 64) ? B * MAXIT : 1];
     __shared__ float red[2 * (B / 64)];
-    __shared__ float sv[B / 64];
-    __shared__ int64_t si[B / 64];
+    __shared__ uint64_t sk[B / 64];
     __shared__ uint32_t sc[B / 64];
-    __shared__ double lds[RPB > 1 ? B * 4 : 1];
+    __shared__ double acc_lds[RPB > 1 ? 4 * MAXIT * B : 1];
 
     const int tid = threadIdx.x, g = tid % G, slot = tid / G;
     const int64_t C4 = (a.D + 3) >> 2;
     const int64_t NP = a.N / 2, NG = NP + (a.N & 1);  // pair groups (+ the unpaired one)
-    float bv = __builtin_nanf("");
-    int64_t bi = INT64_MAX;
-    uint32_t dummy = 0;
-    double cs[MAXIT][4];
-#pragma unroll
-    for (int it = 0; it < MAXIT; ++it)
-#pragma unroll
-        for (int e = 0; e < 4; ++e) cs[it][e] = 0.0;
+    uint64_t best = kNoKey;
+    uint32_t none = 0;
+    ColAcc<G, MAXIT> acc(acc_lds);
 
     for (int64_t kb = (int64_t)blockIdx.x * RPB; kb < NG; kb += (int64_t)gridDim.x * RPB) {
         const int64_t k = kb + slot;
@@ -299,51 +303,37 @@ __global__ __launch_bounds__(block_for(G)) void k_cso(CsoArgs a)
                     *reinterpret_cast<float4 *>(a.v + off) = make_float4(vo[0], vo[1], vo[2], vo[3]);
                 }
 #pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    cs[it][e] += (double)comp(xw, e);
-                    if (paired) cs[it][e] += (double)comp(xn, e);
-                }
+                for (int e = 0; e < 4; ++e)
+                    acc.add(it, e, paired ? (double)comp(xw, e) + (double)comp(xn, e) : (double)comp(xw, e));
             }
             xr[it] = xn;
         }
         const float f = row_fitness<FN, G, MAXIT>(xr, g, a.D, nbr, red);
         if (active && g == 0) {
-            if (cand_better(fw, w, bv, bi)) {
-                bv = fw;
-                bi = w;
-            }
+            const uint64_t kw = sel_key(fw, w);
+            best = kw < best ? kw : best;
             if (paired) {
                 a.fit[l] = f;
-                if (cand_better(f, l, bv, bi)) {
-                    bv = f;
-                    bi = l;
-                }
+                const uint64_t kl = sel_key(f, l);
+                best = kl < best ? kl : best;
             }
         }
     }
-    block_argmin(bv, bi, dummy, sv, si, sc);
-    if (tid == 0) {
-        a.pval[blockIdx.x] = bv;
-        a.pidx[blockIdx.x] = bi;
-    }
-    __syncthreads();
-    block_colsum_write<G, MAXIT>(cs, a.D, a.ldx, a.xsum, lds);
+    block_min_key(best, none, sk, sc);
+    if (tid == 0) slot_commit(a.slots, best, 0);
+    acc.write(a.D, a.ldx, a.xsum);
 }
 
 // Column sums of all rows of x (the swarm mean at creation / refresh).
-template <int G>
+template <int G, int MAXIT>
 __global__ __launch_bounds__(block_for(G)) void k_colsum(const float *x, int64_t N, int64_t D,
                                                         int64_t ldx, double *xsum)
 {
-    constexpr int B = block_for(G), RPB = B / G, MAXIT = maxit_for(G);
-    __shared__ double lds[RPB > 1 ? B * 4 : 1];
+    constexpr int B = block_for(G), RPB = B / G;
+    __shared__ double acc_lds[RPB > 1 ? 4 * MAXIT * B : 1];
     const int tid = threadIdx.x, g = tid % G, slot = tid / G;
     const int64_t C4 = (D + 3) >> 2;
-    double cs[MAXIT][4];
-#pragma unroll
-    for (int it = 0; it < MAXIT; ++it)
-#pragma unroll
-        for (int e = 0; e < 4; ++e) cs[it][e] = 0.0;
+    ColAcc<G, MAXIT> acc(acc_lds);
     for (int64_t rb = (int64_t)blockIdx.x * RPB; rb < N; rb += (int64_t)gridDim.x * RPB) {
         const int64_t row = rb + slot;
         if (row >= N) continue;
@@ -353,63 +343,98 @@ __global__ __launch_bounds__(block_for(G)) void k_colsum(const float *x, int64_t
             if (c < C4) {
                 const float4 xv = *reinterpret_cast<const float4 *>(x + row * ldx + 4 * c);
 #pragma unroll
-                for (int e = 0; e < 4; ++e) cs[it][e] += (double)comp(xv, e);
+                for (int e = 0; e < 4; ++e) acc.add(it, e, (double)comp(xv, e));
             }
         }
     }
-    block_colsum_write<G, MAXIT>(cs, D, ldx, xsum, lds);
+    acc.write(D, ldx, xsum);
 }
 
-#define EVOX_G_CASES(M, ...)                                                                      \
-    switch (G) {                                                                                  \
-    case 4: M(4, __VA_ARGS__); break;                                                             \
-    case 8: M(8, __VA_ARGS__); break;                                                             \
-    case 16: M(16, __VA_ARGS__); break;                                                           \
-    case 32: M(32, __VA_ARGS__); break;                                                           \
-    case 64: M(64, __VA_ARGS__); break;                                                           \
-    case 128: M(128, __VA_ARGS__); break;                                                         \
-    case 256: M(256, __VA_ARGS__); break;                                                         \
-    case 512: M(512, __VA_ARGS__); break;                                                         \
-    case 1024: M(1024, __VA_ARGS__); break;                                                       \
-    default: return hipErrorInvalidValue;                                                         \
-    }
+// Dispatch on the row layout (G, MAXIT) of a family.
+#define EVOX_WIDE_CASES(M, ...)                                                                   \
+    case 4 * 16 + 4: M(4, 4, __VA_ARGS__); break;                                                 \
+    case 8 * 16 + 4: M(8, 4, __VA_ARGS__); break;                                                 \
+    case 16 * 16 + 4: M(16, 4, __VA_ARGS__); break;                                               \
+    case 32 * 16 + 4: M(32, 4, __VA_ARGS__); break;                                               \
+    case 64 * 16 + 4: M(64, 4, __VA_ARGS__); break;                                               \
+    case 128 * 16 + 4: M(128, 4, __VA_ARGS__); break;                                             \
+    case 256 * 16 + 4: M(256, 4, __VA_ARGS__); break;                                             \
+    case 512 * 16 + 4: M(512, 4, __VA_ARGS__); break;                                             \
+    case 1024 * 16 + 8: M(1024, 8, __VA_ARGS__); break;
+#define EVOX_NARROW_CASES(M, ...)                                                                 \
+    case 4 * 16 + 1: M(4, 1, __VA_ARGS__); break;                                                 \
+    case 8 * 16 + 1: M(8, 1, __VA_ARGS__); break;                                                 \
+    case 16 * 16 + 1: M(16, 1, __VA_ARGS__); break;                                               \
+    case 32 * 16 + 1: M(32, 1, __VA_ARGS__); break;                                               \
+    case 64 * 16 + 1: M(64, 1, __VA_ARGS__); break;                                               \
+    case 128 * 16 + 1: M(128, 1, __VA_ARGS__); break;                                             \
+    case 256 * 16 + 1: M(256, 1, __VA_ARGS__); break;                                             \
+    case 512 * 16 + 1: M(512, 1, __VA_ARGS__); break;                                             \
+    case 1024 * 16 + 8: M(1024, 8, __VA_ARGS__); break;
+#define EVOX_ALL_CASES(M, ...)                                                                    \
+    EVOX_NARROW_CASES(M, __VA_ARGS__)                                                             \
+    case 4 * 16 + 4: M(4, 4, __VA_ARGS__); break;                                                 \
+    case 8 * 16 + 4: M(8, 4, __VA_ARGS__); break;                                                 \
+    case 16 * 16 + 4: M(16, 4, __VA_ARGS__); break;                                               \
+    case 32 * 16 + 4: M(32, 4, __VA_ARGS__); break;                                               \
+    case 64 * 16 + 4: M(64, 4, __VA_ARGS__); break;                                               \
+    case 128 * 16 + 4: M(128, 4, __VA_ARGS__); break;                                             \
+    case 256 * 16 + 4: M(256, 4, __VA_ARGS__); break;                                             \
+    case 512 * 16 + 4: M(512, 4, __VA_ARGS__); break;
 
-#define EVOX_LAUNCH_PSO(GG, MODEE) \
-    hipLaunchKernelGGL((k_pso<FN, GG, MODEE>), dim3(grid), dim3(block_for(GG)), 0, s, a)
-#define EVOX_LAUNCH_EVAL(GG, VECC) \
-    hipLaunchKernelGGL((k_eval<FN, GG, VECC>), dim3(grid), dim3(block_for(GG)), 0, s, a)
-#define EVOX_LAUNCH_CSO(GG, UNUSED) \
-    hipLaunchKernelGGL((k_cso<FN, GG>), dim3(grid), dim3(block_for(GG)), 0, s, a)
+#define EVOX_LAUNCH_PSO(GG, MM, MODEE) \
+    hipLaunchKernelGGL((k_pso<FN, GG, MM, MODEE>), dim3(grid), dim3(block_for(GG)), 0, s, a)
+#define EVOX_LAUNCH_EVAL(GG, MM, VECC) \
+    hipLaunchKernelGGL((k_eval<FN, GG, MM, VECC>), dim3(grid), dim3(block_for(GG)), 0, s, a)
+#define EVOX_LAUNCH_CSO(GG, MM, UNUSED) \
+    hipLaunchKernelGGL((k_cso<FN, GG, MM>), dim3(grid), dim3(block_for(GG)), 0, s, a)
 
 template <int FN>
-hipError_t launch_pso_t(int G, int mode, const PsoArgs &a, int grid, hipStream_t s)
+hipError_t launch_pso_t(Layout L, int mode, const PsoArgs &a, int grid, hipStream_t s)
 {
+    const int key = L.G * 16 + L.maxit;
     if (mode == PSO_EVAL) {
-        EVOX_G_CASES(EVOX_LAUNCH_PSO, PSO_EVAL)
+        switch (key) { EVOX_WIDE_CASES(EVOX_LAUNCH_PSO, PSO_EVAL) default: return hipErrorInvalidValue; }
     } else if (mode == PSO_FUSED) {
-        EVOX_G_CASES(EVOX_LAUNCH_PSO, PSO_FUSED)
+        switch (key) { EVOX_WIDE_CASES(EVOX_LAUNCH_PSO, PSO_FUSED) default: return hipErrorInvalidValue; }
     } else {
-        EVOX_G_CASES(EVOX_LAUNCH_PSO, PSO_MOVE)
+        if constexpr (FN != FN_SPHERE) {
+            return hipErrorInvalidValue;  // the move does not evaluate: instantiated once
+        } else {
+            switch (key) { EVOX_WIDE_CASES(EVOX_LAUNCH_PSO, PSO_MOVE) default: return hipErrorInvalidValue; }
+        }
     }
     return hipGetLastError();
 }
 
 template <int FN>
-hipError_t launch_eval_t(int G, bool vec, const EvalArgs &a, int grid, hipStream_t s)
+hipError_t launch_eval_t(Layout L, bool vec, const EvalArgs &a, int grid, hipStream_t s)
 {
+    const int key = L.G * 16 + L.maxit;
     if (vec) {
-        EVOX_G_CASES(EVOX_LAUNCH_EVAL, true)
+        switch (key) { EVOX_ALL_CASES(EVOX_LAUNCH_EVAL, true) default: return hipErrorInvalidValue; }
     } else {
-        EVOX_G_CASES(EVOX_LAUNCH_EVAL, false)
+        switch (key) { EVOX_ALL_CASES(EVOX_LAUNCH_EVAL, false) default: return hipErrorInvalidValue; }
     }
     return hipGetLastError();
 }
 
 template <int FN>
-hipError_t launch_cso_t(int G, const CsoArgs &a, int grid, hipStream_t s)
+hipError_t launch_cso_t(Layout L, const CsoArgs &a, int grid, hipStream_t s)
 {
-    EVOX_G_CASES(EVOX_LAUNCH_CSO, 0)
+    switch (L.G * 16 + L.maxit) { EVOX_NARROW_CASES(EVOX_LAUNCH_CSO, 0) default: return hipErrorInvalidValue; }
     return hipGetLastError();
+}
+
+template <int FN>
+int occupancy_cso_t(Layout L)
+{
+    int n = 0;
+#define EVOX_OCC_CSO(GG, MM, UNUSED) \
+    (void)hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k_cso<FN, GG, MM>, block_for(GG), 0)
+    switch (L.G * 16 + L.maxit) { EVOX_NARROW_CASES(EVOX_OCC_CSO, 0) default: return 0; }
+#undef EVOX_OCC_CSO
+    return n;
 }
 
 }  // namespace evox

@@ -21,17 +21,14 @@ struct PsoArgs {
     int32_t vclamp, xclamp;
     uint32_t k0, k1;
     uint32_t t;  // generation whose move this launch performs
-    float *pval;
-    int64_t *pidx;
-    uint32_t *pcnt;
+    SelSlots *slots;
 };
 
 struct EvalArgs {
     const float *X;
     int64_t N, D, ldx;
     float *out;
-    float *pval;  // nullable: no selection partials
-    int64_t *pidx;
+    SelSlots *slots;  // nullable: no selection
 };
 
 struct InitArgs {
@@ -50,22 +47,26 @@ struct CsoArgs {
     float phi, lb, ub;
     int32_t xclamp;
     uint32_t k0, k1, t;
-    float *pval;
-    int64_t *pidx;
+    SelSlots *slots;
     double *xsum;  // [grid][ldx] column partial sums of the new positions
 };
 
-hipError_t launch_pso(int fn, int G, int mode, const PsoArgs &a, int grid, hipStream_t s);
+hipError_t launch_pso(int fn, Layout L, int mode, const PsoArgs &a, int grid, hipStream_t s);
 template <int FN>
-hipError_t launch_pso_t(int G, int mode, const PsoArgs &a, int grid, hipStream_t s);
+hipError_t launch_pso_t(Layout L, int mode, const PsoArgs &a, int grid, hipStream_t s);
 template <int FN>
-hipError_t launch_eval_t(int G, bool vec, const EvalArgs &a, int grid, hipStream_t s);
+hipError_t launch_eval_t(Layout L, bool vec, const EvalArgs &a, int grid, hipStream_t s);
 template <int FN>
-hipError_t launch_cso_t(int G, const CsoArgs &a, int grid, hipStream_t s);
-hipError_t launch_eval(int fn, int G, bool vec, const EvalArgs &a, int grid, hipStream_t s);
-hipError_t launch_select(const float *pval, const int64_t *pidx, const uint32_t *pcnt, int nparts,
-                         const float *rows, int64_t ldx, float *row_out, DevBest *best,
-                         float *best_f_out, int64_t *best_i_out, hipStream_t s);
+hipError_t launch_cso_t(Layout L, const CsoArgs &a, int grid, hipStream_t s);
+template <int FN>
+int occupancy_cso_t(Layout L);  // resident blocks per CU of k_cso
+hipError_t launch_eval(int fn, Layout L, bool vec, const EvalArgs &a, int grid, hipStream_t s);
+// Second pass of the selection: reduce and reset the slots, store the result
+// (best and/or the two outputs, each nullable) and copy the selected row of
+// `rows` (ldx floats) to row_out (nullable).
+hipError_t launch_select(SelSlots *slots, const float *rows, int64_t ldx, float *row_out,
+                         DevBest *best, float *best_f_out, int64_t *best_i_out, hipStream_t s);
+hipError_t launch_slots_init(SelSlots *slots, hipStream_t s);
 hipError_t launch_init(const InitArgs &a, hipStream_t s);
 hipError_t launch_philox_fill(uint32_t k0, uint32_t k1, uint32_t c1, uint32_t c2, uint32_t c3,
                               int64_t n, uint32_t *out, hipStream_t s);
@@ -73,24 +74,36 @@ hipError_t launch_copy_row(const float *src, float *dst, int64_t ldx, hipStream_
 hipError_t launch_fill(float *dst, int64_t n, float value, hipStream_t s);
 hipError_t launch_best_init(DevBest *best, float f, int64_t i, hipStream_t s);
 hipError_t launch_zero_u32(uint32_t *dst, int64_t n, hipStream_t s);
-// Selection partials over a fitness array (first pass of the argmin).
-int argmin_partials_grid(int64_t N);
-hipError_t launch_argmin_partials(const float *f, int64_t N, float *pval, int64_t *pidx, int grid,
-                                  hipStream_t s);
+// First pass of the selection over a stored fitness array.
+hipError_t launch_argmin_slots(const float *f, int64_t N, SelSlots *slots, hipStream_t s);
 
-// CSO pairing: bucket sort of the stream-4 keys by (key, index).
+// CSO pairing: superbucket sort of the stream-4 keys by (key, index).
+constexpr int kPermChunk = 4096;        // individuals per block of the count / place passes
+constexpr int kPermMaxBits = 13;        // superbuckets <= 8192
+constexpr int kPermMaxBuckets = 1 << kPermMaxBits;
+constexpr int kPermSortCap = 4096;      // LDS capacity of one superbucket sort (mean <= 2048)
+constexpr int64_t kCsoMaxN = (int64_t)1 << 24;
 struct PermArgs {
     int64_t N;
-    int bits;  // buckets = 2^bits
+    int bits;  // superbuckets = 2^bits
     uint32_t k0, k1, t;
     uint32_t *hist, *offs, *cursor, *tkey, *tidx, *perm;
 };
 hipError_t launch_perm(const PermArgs &a, hipStream_t s);
-hipError_t launch_cso(int fn, int G, const CsoArgs &a, int grid, hipStream_t s);
-hipError_t launch_colsum(int G, const float *x, int64_t N, int64_t D, int64_t ldx, double *xsum,
+hipError_t launch_cso(int fn, Layout L, const CsoArgs &a, int grid, hipStream_t s);
+int occupancy_cso(int fn, Layout L);
+hipError_t launch_colsum(Layout L, const float *x, int64_t N, int64_t D, int64_t ldx, double *xsum,
                          int grid, hipStream_t s);
-// xbar = (sum of the partial rows, in order) / N, rounded once to fp32.
-hipError_t launch_cso_mean(const double *xsum, int nparts, int64_t N, int64_t D, int64_t ldx,
-                           float *xbar, hipStream_t s);
+
+// Swarm mean from per-block fp64 column sums.
+constexpr int kMeanStages = 128;
+struct MeanArgs {
+    const double *xsum;  // [nparts][ldx]
+    int64_t nparts, N, D, ldx;
+    float *xbar;         // [ldx]
+    double *s1;          // [kMeanStages][ldx] stage sums
+    uint32_t *ticket;    // [ceil(ldx / 64)], zero between launches
+};
+hipError_t launch_cso_mean(const MeanArgs &m, hipStream_t s);
 
 }  // namespace evox

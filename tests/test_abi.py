@@ -56,6 +56,12 @@ def test_row_layout_policy(evox):
         assert G == 4 or (G // 2) * (8 if G // 2 == 1024 else 4) * 4 < D or nit > 1
     with pytest.raises(evox.EvoxError):
         evox.row_layout(32769)
+    # CSO: one chunk per lane while it fits
+    assert evox.row_layout(100, evox.CSO) == (32, 1)
+    assert evox.row_layout(10, evox.CSO) == (4, 1)
+    assert evox.row_layout(4096, evox.CSO) == (1024, 1)
+    assert evox.row_layout(4100, evox.CSO) == (1024, 2)
+    assert evox.row_layout(32768, evox.CSO) == (1024, 8)
 
 
 def test_scratch_bytes(evox):
@@ -68,10 +74,11 @@ def test_scratch_bytes(evox):
     assert evox.evox_scratch_bytes(bad) == 0
 
 
-@pytest.mark.parametrize("field,value", [("N", 0), ("D", 0), ("D", 40000), ("ldx", 6),
-                                         ("fn_id", 6), ("algo", 3)])
-def test_create_rejects_bad_params(evox, field, value):
-    p = evox.make_params(evox.PSO, evox.SPHERE, 8, 5, -1, 1)
+@pytest.mark.parametrize("algo,field,value", [(0, "N", 0), (0, "D", 0), (0, "D", 40000),
+                                              (0, "ldx", 6), (0, "fn_id", 6), (0, "algo", 3),
+                                              (1, "N", 1), (1, "N", 2**24 + 1)])
+def test_create_rejects_bad_params(evox, algo, field, value):
+    p = evox.make_params(algo, evox.SPHERE, 8, 5, -1, 1)
     setattr(p, field, value)
     b = evox.Buffers()
     h = ctypes.c_void_p()
