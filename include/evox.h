@@ -186,11 +186,14 @@ int evox_best(evox_state *state, float *best_fit, int64_t *best_idx, float *best
 /* Generations completed so far. */
 int64_t evox_generation(const evox_state *state);
 
-/* Layout the kernels of algorithm `algo` use for dimension D: threads per
- * row and float4 chunks per thread (for tests and reports).  PSO (and
- * evox_eval) use up to 4 chunks per thread, CSO one chunk per thread up to
- * D = 4096; both reach 1024 threads x 8 chunks at D = EVOX_MAX_D. */
-int evox_row_layout(int32_t algo, int64_t D, int32_t *threads_per_row, int32_t *chunks_per_thread);
+/* Kernel families for evox_row_layout. */
+enum evox_layout { EVOX_LAYOUT_PSO = 0, EVOX_LAYOUT_CSO = 1, EVOX_LAYOUT_EVAL = 2 };
+
+/* Row layout the kernels of a family use for dimension D: threads per row
+ * and float4 chunks per thread (for tests and reports).  The threads per row
+ * are the fewest (a power of two, 4..1024) that hold the row in at most 2
+ * (PSO), 1 (CSO) or 4 (evox_eval) chunks per thread, and 8 at 1024 threads. */
+int evox_row_layout(int32_t kernels, int64_t D, int32_t *threads_per_row, int32_t *chunks_per_thread);
 
 /* Diagnostic: out[4 k + m] = word m of Philox(seed, (k, c1, c2, c3)) for
  * k < n_ctr, computed by the device Philox the kernels use (device out). */

@@ -109,9 +109,13 @@ def _ptr(t):
     return ctypes.c_void_p(t.data_ptr()) if t is not None else None
 
 
-def row_layout(D, algo=PSO):
+LAYOUT_PSO, LAYOUT_CSO, LAYOUT_EVAL = 0, 1, 2
+
+
+def row_layout(D, kernels=LAYOUT_PSO):
+    """(threads per row, float4 chunks per thread) of a kernel family at dimension D."""
     g, n = ctypes.c_int32(0), ctypes.c_int32(0)
-    _check(lib().evox_row_layout(algo, D, ctypes.byref(g), ctypes.byref(n)))
+    _check(lib().evox_row_layout(kernels, D, ctypes.byref(g), ctypes.byref(n)))
     return g.value, n.value
 
 

@@ -68,7 +68,7 @@ struct Plan {
     Layout L{0, 0, 0};
     int grid = 0, cso_grid = 0, colsum_grid = 0, bits = 0;
     size_t best = 0, slots = 0;
-    size_t hist = 0, offs = 0, cursor = 0, tkey = 0, tidx = 0, perm = 0, xsum = 0, s1 = 0, ticket = 0;
+    size_t hist = 0, offs = 0, cursor = 0, tkey = 0, tidx = 0, perm = 0, pw = 0, xsum = 0, s1 = 0, ticket = 0;
     int64_t xsum_rows = 0;
     size_t total = 0;
 };
@@ -88,7 +88,7 @@ int make_plan(const evox_params *P, Plan *pl)
     if (P->ldx < P->D || (P->ldx & 3))
         return fail(EVOX_EINVAL, "ldx = %lld must be >= D and a multiple of 4", (long long)P->ldx);
     Plan p;
-    const int family = P->algo == EVOX_CSO ? LAYOUT_NARROW : LAYOUT_WIDE;
+    const int family = P->algo == EVOX_CSO ? LAYOUT_CSO : LAYOUT_PSO;
     if (!row_layout(P->D, family, &p.L)) return fail(EVOX_EINVAL, "no row layout for D = %lld", (long long)P->D);
     p.grid = grid_for(P->N, p.L.G, kMaxGrid);
     size_t off = 0;
@@ -111,6 +111,7 @@ int make_plan(const evox_params *P, Plan *pl)
         p.tkey = take(4 * (size_t)P->N);
         p.tidx = take(4 * (size_t)P->N);
         p.perm = take(4 * (size_t)P->N);
+        p.pw = take(8 * (size_t)(P->N / 2 + 1));
         p.xsum_rows = cap;
         p.xsum = take(sizeof(double) * (size_t)cap * (size_t)P->ldx);
         p.s1 = take(sizeof(double) * (size_t)kMeanStages * (size_t)P->ldx);
@@ -133,6 +134,7 @@ struct evox_state {
     DevBest *best;
     SelSlots *slots;
     uint32_t *hist, *offs, *cursor, *tkey, *tidx, *perm, *ticket;
+    uint64_t *pw;
     double *xsum, *s1;
     // profiling of the fused generation kernel
     bool prof;
@@ -197,6 +199,7 @@ PsoArgs pso_args(evox_state *s)
     a.k1 = s->k1;
     a.t = 0;
     a.slots = s->slots;
+    a.nt = 20 * P.N * P.D > kStreamBytes;
     return a;
 }
 
@@ -212,7 +215,7 @@ int cso_refresh(evox_state *s, bool refit)
     const Plan &pl = s->pl;
     hipError_t e;
     if (refit) {
-        EvalArgs ea{s->B.x, P.N, P.D, P.ldx, s->B.fit, nullptr};
+        EvalArgs ea{s->B.x, P.N, P.D, P.ldx, s->B.fit, nullptr, 4 * P.N * P.ldx > kStreamBytes};
         if ((e = launch_eval(P.fn_id, pl.L, true, ea, pl.grid, s->stream)) != hipSuccess)
             return hip_fail(e, "evaluate");
     }
@@ -271,6 +274,7 @@ int evox_state_create(const evox_params *params, const evox_buffers *b, void *hi
     s->slots = at<SelSlots>(b->scratch, pl.slots);
     s->hist = s->offs = s->cursor = s->tkey = s->tidx = s->perm = nullptr;
     s->xsum = s->s1 = nullptr;
+    s->pw = nullptr;
     s->ticket = nullptr;
     if (P.algo == EVOX_CSO) {
         s->hist = at<uint32_t>(b->scratch, pl.hist);
@@ -279,6 +283,7 @@ int evox_state_create(const evox_params *params, const evox_buffers *b, void *hi
         s->tkey = at<uint32_t>(b->scratch, pl.tkey);
         s->tidx = at<uint32_t>(b->scratch, pl.tidx);
         s->perm = at<uint32_t>(b->scratch, pl.perm);
+        s->pw = at<uint64_t>(b->scratch, pl.pw);
         s->xsum = at<double>(b->scratch, pl.xsum);
         s->s1 = at<double>(b->scratch, pl.s1);
         s->ticket = at<uint32_t>(b->scratch, pl.ticket);
@@ -354,11 +359,11 @@ static int eval_common(int fn_id, const float *X, int64_t N, int64_t D, int64_t 
     if (ldx < D) return fail(EVOX_EINVAL, "ldx = %lld < D", (long long)ldx);
     if (N > 0 && (!X || !out)) return fail(EVOX_EINVAL, "X and out are required");
     Layout L;
-    if (!row_layout(D, LAYOUT_WIDE, &L)) return fail(EVOX_EINVAL, "no row layout for D = %lld", (long long)D);
+    if (!row_layout(D, LAYOUT_EVAL, &L)) return fail(EVOX_EINVAL, "no row layout for D = %lld", (long long)D);
     const int grid = grid_for(N, L.G, kMaxGrid);
     if (N == 0) return EVOX_OK;
     const bool vec = (ldx & 3) == 0 && aligned16(X);
-    EvalArgs a{X, N, D, ldx, out, slots};
+    EvalArgs a{X, N, D, ldx, out, slots, 4 * N * ldx > kStreamBytes};
     hipError_t e = launch_eval(fn_id, L, vec, a, grid, st);
     if (e != hipSuccess) return hip_fail(e, "evaluate");
     return EVOX_OK;
@@ -446,9 +451,10 @@ int evox_cso_step(evox_state *s, int64_t n_gens)
     hipError_t e;
     for (int64_t k = 0; k < n_gens; ++k) {
         const uint32_t t = (uint32_t)(s->t + k);
-        PermArgs pa{P.N, pl.bits, s->k0, s->k1, t, s->hist, s->offs, s->cursor, s->tkey, s->tidx, s->perm};
+        PermArgs pa{P.N, pl.bits, s->k0, s->k1, t, s->hist, s->offs, s->cursor, s->tkey, s->tidx, s->perm,
+                    s->B.fit, s->pw};
         if ((e = launch_perm(pa, s->stream)) != hipSuccess) return hip_fail(e, "pairing");
-        CsoArgs ca{s->B.x, s->B.v, s->B.fit, s->B.xbar, s->perm, P.N, P.D, P.ldx, P.phi, P.lb, P.ub,
+        CsoArgs ca{s->B.x, s->B.v, s->B.fit, s->B.xbar, s->perm, s->pw, P.N, P.D, P.ldx, P.phi, P.lb, P.ub,
                    P.clamp_x != 0, s->k0, s->k1, t, s->slots, s->xsum};
         e = timed(s, [&] { return launch_cso(P.fn_id, pl.L, ca, pl.cso_grid, s->stream); });
         if (e != hipSuccess) return hip_fail(e, "cso generation");
@@ -489,11 +495,13 @@ int evox_best(evox_state *s, float *best_fit, int64_t *best_idx, float *best_x_h
 
 int64_t evox_generation(const evox_state *s) { return s ? s->t : -1; }
 
-int evox_row_layout(int32_t algo, int64_t D, int32_t *threads_per_row, int32_t *chunks_per_thread)
+int evox_row_layout(int32_t kernels, int64_t D, int32_t *threads_per_row, int32_t *chunks_per_thread)
 {
-    if (algo != EVOX_PSO && algo != EVOX_CSO) return fail(EVOX_EINVAL, "unknown algo %d", algo);
+    static const int family[3] = {LAYOUT_PSO, LAYOUT_CSO, LAYOUT_EVAL};
+    if (kernels < EVOX_LAYOUT_PSO || kernels > EVOX_LAYOUT_EVAL)
+        return fail(EVOX_EINVAL, "unknown kernel family %d", kernels);
     Layout L;
-    if (D > EVOX_MAX_D || !row_layout(D, algo == EVOX_CSO ? LAYOUT_NARROW : LAYOUT_WIDE, &L))
+    if (D > EVOX_MAX_D || !row_layout(D, family[kernels], &L))
         return fail(EVOX_EINVAL, "no row layout for D = %lld", (long long)D);
     if (threads_per_row) *threads_per_row = L.G;
     if (chunks_per_thread) *chunks_per_thread = L.nit;

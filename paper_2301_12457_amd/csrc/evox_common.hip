@@ -12,7 +12,8 @@
 //                 placement of (key, index) into the superbucket ranges
 //   k_perm_sort   one block per superbucket (~1000 entries): counting sort on
 //                 the next 8 key bits in LDS, then ranks inside sub-buckets,
-//                 written as the permutation
+//                 written as the permutation, and the winner / loser of every
+//                 pair inside the superbucket
 #include "evox_kernels.hpp"
 
 namespace evox {
@@ -316,19 +317,32 @@ __global__ __launch_bounds__(256) void k_perm_place(PermArgs a)
     });
 }
 
-// Pass 3: one block per superbucket orders its entries by (key, index):
-// a counting sort on the next 8 key bits (256 sub-buckets of ~4 entries) in
-// LDS, then each entry's rank inside its sub-bucket by comparison, written
-// as the permutation.  The bucket's count and cursor are then cleared for
-// the next generation.  A bucket larger than the LDS capacity (not expected
-// for uniform keys) is ranked directly in global memory instead.
+// Pass 3: one block per superbucket orders its entries by (key, index): a
+// counting sort on the next 8 key bits (256 sub-buckets of ~4 entries) in
+// LDS, then each entry's rank inside its sub-bucket by comparison.  The
+// ordered indices are written as the permutation, and every pair
+// (perm[2k], perm[2k+1]) that lies inside the superbucket is decided here:
+// pw[k] = winner | loser << 32 (the second wins when its fitness is strictly
+// lower, or the first's is NaN and its own is not).  A pair that straddles two
+// superbuckets gets kPairUnknown and is decided by the generation kernel.
+// The bucket's count and cursor are then cleared for the next generation.  A
+// bucket larger than the LDS capacity (not expected for uniform keys) is
+// ranked directly in global memory and all its pairs are left undecided.
+__device__ __forceinline__ uint64_t decide_pair(const float *fit, uint32_t a, uint32_t b)
+{
+    const float fa = fit[a], fb = fit[b];
+    const bool second = fb < fa || (fa != fa && fb == fb);
+    return second ? ((uint64_t)a << 32) | b : ((uint64_t)b << 32) | a;
+}
+
 __global__ __launch_bounds__(256) void k_perm_sort(PermArgs a)
 {
-    __shared__ uint32_t K[kPermSortCap], I[kPermSortCap];
+    __shared__ uint32_t K[kPermSortCap], I[kPermSortCap], S[kPermSortCap];
     __shared__ uint32_t cnt[256], start[256], cur[256];
     const int b = blockIdx.x;
     const uint32_t lo = a.offs[b], n = a.hist[b];
     const int shift = 24 - a.bits;  // the 8 key bits below the superbucket bits
+    const uint32_t np = (uint32_t)(a.N / 2);
     if (n <= (uint32_t)kPermSortCap) {
         cnt[threadIdx.x] = 0;
         __syncthreads();
@@ -343,7 +357,7 @@ __global__ __launch_bounds__(256) void k_perm_sort(PermArgs a)
                 const uint32_t o = __shfl_up(inc, d, 64);
                 if (l >= d) inc += o;
             }
-            uint32_t ex = inc - tot;
+            const uint32_t ex = inc - tot;
             start[4 * l] = ex;
             start[4 * l + 1] = ex + c0;
             start[4 * l + 2] = ex + c0 + c1;
@@ -364,7 +378,16 @@ __global__ __launch_bounds__(256) void k_perm_sort(PermArgs a)
             const uint32_t s0 = start[sb], s1 = s0 + cnt[sb];
             uint32_t rank = 0;
             for (uint32_t r = s0; r < s1; ++r) rank += (K[r] < key || (K[r] == key && I[r] < idx)) ? 1u : 0u;
-            a.perm[lo + s0 + rank] = idx;
+            S[s0 + rank] = idx;
+        }
+        __syncthreads();
+        for (uint32_t q = threadIdx.x; q < n; q += 256) {
+            a.perm[lo + q] = S[q];
+            const uint32_t p = lo + q;
+            if ((p & 1u) == 0 && p / 2 < np)
+                a.pw[p / 2] = q + 1 < n ? decide_pair(a.fit, S[q], S[q + 1]) : kPairUnknown;
+            else if ((p & 1u) == 1 && q == 0)
+                a.pw[p / 2] = kPairUnknown;
         }
     } else {
         for (uint32_t p = threadIdx.x; p < n; p += 256) {
@@ -375,6 +398,7 @@ __global__ __launch_bounds__(256) void k_perm_sort(PermArgs a)
                 rank += (kq < key || (kq == key && iq < idx)) ? 1u : 0u;
             }
             a.perm[lo + rank] = idx;
+            if ((lo + p) / 2 < np) a.pw[(lo + p) / 2] = kPairUnknown;
         }
     }
     __syncthreads();
@@ -429,9 +453,10 @@ __global__ __launch_bounds__(256) void k_cso_mean(MeanArgs m)
     if (j < m.D) s = strided_sum(m.xsum + j, rg + (int64_t)kMeanStages * lane, 4 * kMeanStages, m.nparts, m.ldx);
     part[lane][col] = s;
     __syncthreads();
-    if (lane == 0 && j < m.D)
-        m.s1[rg * m.ldx + j] = ((part[0][col] + part[1][col]) + part[2][col]) + part[3][col];
-    __threadfence();
+    if (lane == 0) {  // wave 0 writes this block's stage sums and releases them
+        if (j < m.D) m.s1[rg * m.ldx + j] = ((part[0][col] + part[1][col]) + part[2][col]) + part[3][col];
+        __threadfence();
+    }
     __syncthreads();
     if (threadIdx.x == 0) last = atomicAdd(&m.ticket[tile], 1u) == (uint32_t)(kMeanStages - 1);
     __syncthreads();
@@ -462,7 +487,11 @@ hipError_t launch_cso_mean(const MeanArgs &m, hipStream_t s)
 hipError_t launch_colsum(Layout L, const float *x, int64_t N, int64_t D, int64_t ldx, double *xsum,
                          int grid, hipStream_t s)
 {
-    switch (L.G * 16 + L.maxit) { EVOX_NARROW_CASES(EVOX_LAUNCH_COLSUM, 0) default: return hipErrorInvalidValue; }
+    switch (L.G * 16 + L.maxit) {
+        EVOX_FAMILY_CASES(EVOX_LAUNCH_COLSUM, LAYOUT_CSO, 0)
+        EVOX_BIG_CASE(EVOX_LAUNCH_COLSUM, 0)
+        default: return hipErrorInvalidValue;
+    }
     return hipGetLastError();
 }
 

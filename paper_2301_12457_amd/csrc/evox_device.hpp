@@ -33,16 +33,18 @@ constexpr int kMaxG = 1024;
 __host__ __device__ constexpr int block_for(int G) { return G > kBlock ? G : kBlock; }
 
 // Row layout: G lanes per row, MAXIT float4 chunk registers per lane, nit of
-// them used.  Two families:
-//   wide    at most 4 chunks per lane (8 at G = 1024): the PSO and the
-//           evaluation kernels, which stream whole rows and want few lanes
-//           per row reduction;
-//   narrow  one chunk per lane up to D = 4096 (then G = 1024, up to 8): the
-//           CSO kernels, whose random row gathers want a row in one load
-//           instruction and few registers per lane.
+// them used; G is the fewest lanes (a power of two) that hold the row in at
+// most `family` chunks per lane (8 at G = 1024).  Three families, chosen by
+// measurement on gfx950:
+//   LAYOUT_EVAL   4 chunks per lane: evox_eval (one wave per row at D = 1000,
+//                 no LDS step in the row reduction);
+//   LAYOUT_PSO    2 chunks per lane: the PSO generation kernels (fewer
+//                 registers per lane, more waves in flight);
+//   LAYOUT_CSO    1 chunk per lane up to D = 4096: the CSO kernels, whose
+//                 random row gathers want a row in one load instruction.
 // The layout depends only on (D, family), so every kernel of a state reduces
 // a row in the same order and produces bit-identical fitness.
-enum { LAYOUT_WIDE = 4, LAYOUT_NARROW = 1 };
+enum { LAYOUT_CSO = 1, LAYOUT_PSO = 2, LAYOUT_EVAL = 4 };
 
 struct Layout {
     int G, maxit, nit;
@@ -91,6 +93,43 @@ __device__ __forceinline__ U4 philox(uint32_t c0, uint32_t c1, uint32_t c2, uint
 
 // Top 24 bits times 2^-24: exact, in [0, 1).
 __device__ __forceinline__ float u01(uint32_t w) { return (float)(w >> 8) * 0x1p-24f; }
+
+// Streaming (nontemporal) 128-bit row accesses: population rows are touched
+// once per generation, so they are loaded and stored with the nontemporal
+// hint, which on gfx950 keeps them from displacing reused data in the caches
+// and lets HBM run mixed read/write streams closer to peak.
+typedef float v4f_t __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ float4 ld_stream(const float *p)
+{
+    const v4f_t t = __builtin_nontemporal_load(reinterpret_cast<const v4f_t *>(p));
+    return make_float4(t.x, t.y, t.z, t.w);
+}
+
+__device__ __forceinline__ void st_stream(float *p, float4 v)
+{
+    const v4f_t t = {v.x, v.y, v.z, v.w};
+    __builtin_nontemporal_store(t, reinterpret_cast<v4f_t *>(p));
+}
+
+// Row access with the streaming hint only when `nt` (wave-uniform): a state
+// that fits in the 256 MB last-level cache is better served by normal
+// accesses, a larger one by streaming ones.
+__device__ __forceinline__ float4 ld_row(const float *p, bool nt)
+{
+    return nt ? ld_stream(p) : *reinterpret_cast<const float4 *>(p);
+}
+
+__device__ __forceinline__ void st_row(float *p, float4 v, bool nt)
+{
+    if (nt)
+        st_stream(p, v);
+    else
+        *reinterpret_cast<float4 *>(p) = v;
+}
+
+// Streamed bytes of one pass above which the streaming hint is used.
+constexpr int64_t kStreamBytes = (int64_t)512 << 20;
 
 __device__ __forceinline__ float comp(const float4 &v, int e)
 {

@@ -57,10 +57,10 @@ __global__ __launch_bounds__(block_for(G)) void k_pso(PsoArgs a)
             float4 xn = make_float4(0.f, 0.f, 0.f, 0.f);
             if (active && c < C4) {
                 const int64_t off = row * a.ldx + 4 * c;
-                const float4 xv = *reinterpret_cast<const float4 *>(a.x + off);
+                const float4 xv = ld_row(a.x + off, a.nt);
                 if constexpr (MOVE) {
-                    const float4 vv = *reinterpret_cast<const float4 *>(a.v + off);
-                    const float4 pv = *reinterpret_cast<const float4 *>(a.p + off);
+                    const float4 vv = ld_row(a.v + off, a.nt);
+                    const float4 pv = ld_row(a.p + off, a.nt);
                     const float4 gv = *reinterpret_cast<const float4 *>(a.gbest + 4 * c);
                     const U4 r1 = philox((uint32_t)(2 * c), (uint32_t)row, a.t, STREAM_PSO, a.k0, a.k1);
                     const U4 r2 =
@@ -80,8 +80,8 @@ __global__ __launch_bounds__(block_for(G)) void k_pso(PsoArgs a)
                         vo[e] = in ? nv : 0.0f;
                     }
                     xn = make_float4(xo[0], xo[1], xo[2], xo[3]);
-                    *reinterpret_cast<float4 *>(a.x + off) = xn;
-                    *reinterpret_cast<float4 *>(a.v + off) = make_float4(vo[0], vo[1], vo[2], vo[3]);
+                    st_row(a.x + off, xn, a.nt);
+                    st_row(a.v + off, make_float4(vo[0], vo[1], vo[2], vo[3]), a.nt);
                 } else {
                     xn = xv;
                 }
@@ -97,7 +97,7 @@ __global__ __launch_bounds__(block_for(G)) void k_pso(PsoArgs a)
 #pragma unroll
                     for (int it = 0; it < MAXIT; ++it) {
                         const int64_t c = g + (int64_t)G * it;
-                        if (c < C4) *reinterpret_cast<float4 *>(a.p + row * a.ldx + 4 * c) = xr[it];
+                        if (c < C4) st_row(a.p + row * a.ldx + 4 * c, xr[it], a.nt);
                     }
                 }
                 if (g == 0) {
@@ -146,7 +146,7 @@ __global__ __launch_bounds__(block_for(G)) void k_eval(EvalArgs a)
             if (active && c < C4) {
                 const float *src = a.X + row * a.ldx + 4 * c;
                 if constexpr (VEC) {
-                    xv = *reinterpret_cast<const float4 *>(src);
+                    xv = ld_row(src, a.nt);
                 } else {
                     const int64_t left = a.D - 4 * c;
                     xv.x = src[0];
@@ -250,24 +250,35 @@ __global__ __launch_bounds__(block_for(G)) void k_cso(CsoArgs a)
     uint32_t none = 0;
     ColAcc<G, MAXIT> acc(acc_lds);
 
-    for (int64_t kb = (int64_t)blockIdx.x * RPB; kb < NG; kb += (int64_t)gridDim.x * RPB) {
+    // pairs come decided from the pairing sort; the next iteration's pair is
+    // loaded one iteration ahead so the row gathers do not wait for it
+    const int64_t stride = (int64_t)gridDim.x * RPB;
+    int64_t kb = (int64_t)blockIdx.x * RPB;
+    uint64_t u_next = kb + slot < NP ? a.pw[kb + slot] : kPairUnknown;
+    for (; kb < NG; kb += stride) {
         const int64_t k = kb + slot;
         const bool active = k < NG;
         const bool paired = k < NP;
+        const uint64_t u = u_next;
+        u_next = k + stride < NP ? a.pw[k + stride] : kPairUnknown;
         int64_t w = 0, l = 0;
         float fw = 0.0f;
         if (active) {
             if (paired) {
-                const int64_t p0 = a.perm[2 * k], p1 = a.perm[2 * k + 1];
-                const float f0 = a.fit[p0], f1 = a.fit[p1];
-                const bool second = f1 < f0 || (f0 != f0 && f1 == f1);
-                w = second ? p1 : p0;
-                l = second ? p0 : p1;
-                fw = second ? f1 : f0;
+                if (u != kPairUnknown) {
+                    w = (int64_t)(uint32_t)u;
+                    l = (int64_t)(u >> 32);
+                } else {  // pair across two superbuckets
+                    const int64_t p0 = a.perm[2 * k], p1 = a.perm[2 * k + 1];
+                    const float f0 = a.fit[p0], f1 = a.fit[p1];
+                    const bool second = f1 < f0 || (f0 != f0 && f1 == f1);
+                    w = second ? p1 : p0;
+                    l = second ? p0 : p1;
+                }
             } else {
                 w = a.perm[a.N - 1];
-                fw = a.fit[w];
             }
+            fw = a.fit[w];
         }
         float4 xr[MAXIT];
 #pragma unroll
@@ -278,8 +289,8 @@ __global__ __launch_bounds__(block_for(G)) void k_cso(CsoArgs a)
                 const float4 xw = *reinterpret_cast<const float4 *>(a.x + w * a.ldx + 4 * c);
                 if (paired) {
                     const int64_t off = l * a.ldx + 4 * c;
-                    const float4 xl = *reinterpret_cast<const float4 *>(a.x + off);
-                    const float4 vl = *reinterpret_cast<const float4 *>(a.v + off);
+                    const float4 xl = ld_stream(a.x + off);
+                    const float4 vl = ld_stream(a.v + off);
                     const float4 xb = *reinterpret_cast<const float4 *>(a.xbar + 4 * c);
                     const U4 R1 = philox((uint32_t)(3 * c), (uint32_t)l, a.t, STREAM_CSO, a.k0, a.k1);
                     const U4 R2 = philox((uint32_t)(3 * c + 1), (uint32_t)l, a.t, STREAM_CSO, a.k0, a.k1);
@@ -299,8 +310,8 @@ __global__ __launch_bounds__(block_for(G)) void k_cso(CsoArgs a)
                         vo[e] = in ? nv : 0.0f;
                     }
                     xn = make_float4(xo[0], xo[1], xo[2], xo[3]);
-                    *reinterpret_cast<float4 *>(a.x + off) = xn;
-                    *reinterpret_cast<float4 *>(a.v + off) = make_float4(vo[0], vo[1], vo[2], vo[3]);
+                    st_stream(a.x + off, xn);
+                    st_stream(a.v + off, make_float4(vo[0], vo[1], vo[2], vo[3]));
                 }
 #pragma unroll
                 for (int e = 0; e < 4; ++e)
@@ -341,7 +352,7 @@ __global__ __launch_bounds__(block_for(G)) void k_colsum(const float *x, int64_t
         for (int it = 0; it < MAXIT; ++it) {
             const int64_t c = g + (int64_t)G * it;
             if (c < C4) {
-                const float4 xv = *reinterpret_cast<const float4 *>(x + row * ldx + 4 * c);
+                const float4 xv = ld_stream(x + row * ldx + 4 * c);
 #pragma unroll
                 for (int e = 0; e < 4; ++e) acc.add(it, e, (double)comp(xv, e));
             }
@@ -351,36 +362,16 @@ __global__ __launch_bounds__(block_for(G)) void k_colsum(const float *x, int64_t
 }
 
 // Dispatch on the row layout (G, MAXIT) of a family.
-#define EVOX_WIDE_CASES(M, ...)                                                                   \
-    case 4 * 16 + 4: M(4, 4, __VA_ARGS__); break;                                                 \
-    case 8 * 16 + 4: M(8, 4, __VA_ARGS__); break;                                                 \
-    case 16 * 16 + 4: M(16, 4, __VA_ARGS__); break;                                               \
-    case 32 * 16 + 4: M(32, 4, __VA_ARGS__); break;                                               \
-    case 64 * 16 + 4: M(64, 4, __VA_ARGS__); break;                                               \
-    case 128 * 16 + 4: M(128, 4, __VA_ARGS__); break;                                             \
-    case 256 * 16 + 4: M(256, 4, __VA_ARGS__); break;                                             \
-    case 512 * 16 + 4: M(512, 4, __VA_ARGS__); break;                                             \
-    case 1024 * 16 + 8: M(1024, 8, __VA_ARGS__); break;
-#define EVOX_NARROW_CASES(M, ...)                                                                 \
-    case 4 * 16 + 1: M(4, 1, __VA_ARGS__); break;                                                 \
-    case 8 * 16 + 1: M(8, 1, __VA_ARGS__); break;                                                 \
-    case 16 * 16 + 1: M(16, 1, __VA_ARGS__); break;                                               \
-    case 32 * 16 + 1: M(32, 1, __VA_ARGS__); break;                                               \
-    case 64 * 16 + 1: M(64, 1, __VA_ARGS__); break;                                               \
-    case 128 * 16 + 1: M(128, 1, __VA_ARGS__); break;                                             \
-    case 256 * 16 + 1: M(256, 1, __VA_ARGS__); break;                                             \
-    case 512 * 16 + 1: M(512, 1, __VA_ARGS__); break;                                             \
-    case 1024 * 16 + 8: M(1024, 8, __VA_ARGS__); break;
-#define EVOX_ALL_CASES(M, ...)                                                                    \
-    EVOX_NARROW_CASES(M, __VA_ARGS__)                                                             \
-    case 4 * 16 + 4: M(4, 4, __VA_ARGS__); break;                                                 \
-    case 8 * 16 + 4: M(8, 4, __VA_ARGS__); break;                                                 \
-    case 16 * 16 + 4: M(16, 4, __VA_ARGS__); break;                                               \
-    case 32 * 16 + 4: M(32, 4, __VA_ARGS__); break;                                               \
-    case 64 * 16 + 4: M(64, 4, __VA_ARGS__); break;                                               \
-    case 128 * 16 + 4: M(128, 4, __VA_ARGS__); break;                                             \
-    case 256 * 16 + 4: M(256, 4, __VA_ARGS__); break;                                             \
-    case 512 * 16 + 4: M(512, 4, __VA_ARGS__); break;
+#define EVOX_FAMILY_CASES(M, F, ...)                                                              \
+    case 4 * 16 + F: M(4, F, __VA_ARGS__); break;                                                 \
+    case 8 * 16 + F: M(8, F, __VA_ARGS__); break;                                                 \
+    case 16 * 16 + F: M(16, F, __VA_ARGS__); break;                                               \
+    case 32 * 16 + F: M(32, F, __VA_ARGS__); break;                                               \
+    case 64 * 16 + F: M(64, F, __VA_ARGS__); break;                                               \
+    case 128 * 16 + F: M(128, F, __VA_ARGS__); break;                                             \
+    case 256 * 16 + F: M(256, F, __VA_ARGS__); break;                                             \
+    case 512 * 16 + F: M(512, F, __VA_ARGS__); break;
+#define EVOX_BIG_CASE(M, ...) case 1024 * 16 + 8: M(1024, 8, __VA_ARGS__); break;
 
 #define EVOX_LAUNCH_PSO(GG, MM, MODEE) \
     hipLaunchKernelGGL((k_pso<FN, GG, MM, MODEE>), dim3(grid), dim3(block_for(GG)), 0, s, a)
@@ -394,14 +385,26 @@ hipError_t launch_pso_t(Layout L, int mode, const PsoArgs &a, int grid, hipStrea
 {
     const int key = L.G * 16 + L.maxit;
     if (mode == PSO_EVAL) {
-        switch (key) { EVOX_WIDE_CASES(EVOX_LAUNCH_PSO, PSO_EVAL) default: return hipErrorInvalidValue; }
+        switch (key) {
+            EVOX_FAMILY_CASES(EVOX_LAUNCH_PSO, LAYOUT_PSO, PSO_EVAL)
+            EVOX_BIG_CASE(EVOX_LAUNCH_PSO, PSO_EVAL)
+            default: return hipErrorInvalidValue;
+        }
     } else if (mode == PSO_FUSED) {
-        switch (key) { EVOX_WIDE_CASES(EVOX_LAUNCH_PSO, PSO_FUSED) default: return hipErrorInvalidValue; }
+        switch (key) {
+            EVOX_FAMILY_CASES(EVOX_LAUNCH_PSO, LAYOUT_PSO, PSO_FUSED)
+            EVOX_BIG_CASE(EVOX_LAUNCH_PSO, PSO_FUSED)
+            default: return hipErrorInvalidValue;
+        }
     } else {
         if constexpr (FN != FN_SPHERE) {
             return hipErrorInvalidValue;  // the move does not evaluate: instantiated once
         } else {
-            switch (key) { EVOX_WIDE_CASES(EVOX_LAUNCH_PSO, PSO_MOVE) default: return hipErrorInvalidValue; }
+            switch (key) {
+                EVOX_FAMILY_CASES(EVOX_LAUNCH_PSO, LAYOUT_PSO, PSO_MOVE)
+                EVOX_BIG_CASE(EVOX_LAUNCH_PSO, PSO_MOVE)
+                default: return hipErrorInvalidValue;
+            }
         }
     }
     return hipGetLastError();
@@ -412,9 +415,19 @@ hipError_t launch_eval_t(Layout L, bool vec, const EvalArgs &a, int grid, hipStr
 {
     const int key = L.G * 16 + L.maxit;
     if (vec) {
-        switch (key) { EVOX_ALL_CASES(EVOX_LAUNCH_EVAL, true) default: return hipErrorInvalidValue; }
+        switch (key) {
+            EVOX_FAMILY_CASES(EVOX_LAUNCH_EVAL, LAYOUT_EVAL, true)
+            EVOX_FAMILY_CASES(EVOX_LAUNCH_EVAL, LAYOUT_CSO, true)
+            EVOX_BIG_CASE(EVOX_LAUNCH_EVAL, true)
+            default: return hipErrorInvalidValue;
+        }
     } else {
-        switch (key) { EVOX_ALL_CASES(EVOX_LAUNCH_EVAL, false) default: return hipErrorInvalidValue; }
+        switch (key) {
+            EVOX_FAMILY_CASES(EVOX_LAUNCH_EVAL, LAYOUT_EVAL, false)
+            EVOX_FAMILY_CASES(EVOX_LAUNCH_EVAL, LAYOUT_CSO, false)
+            EVOX_BIG_CASE(EVOX_LAUNCH_EVAL, false)
+            default: return hipErrorInvalidValue;
+        }
     }
     return hipGetLastError();
 }
@@ -422,7 +435,11 @@ hipError_t launch_eval_t(Layout L, bool vec, const EvalArgs &a, int grid, hipStr
 template <int FN>
 hipError_t launch_cso_t(Layout L, const CsoArgs &a, int grid, hipStream_t s)
 {
-    switch (L.G * 16 + L.maxit) { EVOX_NARROW_CASES(EVOX_LAUNCH_CSO, 0) default: return hipErrorInvalidValue; }
+    switch (L.G * 16 + L.maxit) {
+        EVOX_FAMILY_CASES(EVOX_LAUNCH_CSO, LAYOUT_CSO, 0)
+        EVOX_BIG_CASE(EVOX_LAUNCH_CSO, 0)
+        default: return hipErrorInvalidValue;
+    }
     return hipGetLastError();
 }
 
@@ -432,7 +449,11 @@ int occupancy_cso_t(Layout L)
     int n = 0;
 #define EVOX_OCC_CSO(GG, MM, UNUSED) \
     (void)hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k_cso<FN, GG, MM>, block_for(GG), 0)
-    switch (L.G * 16 + L.maxit) { EVOX_NARROW_CASES(EVOX_OCC_CSO, 0) default: return 0; }
+    switch (L.G * 16 + L.maxit) {
+        EVOX_FAMILY_CASES(EVOX_OCC_CSO, LAYOUT_CSO, 0)
+        EVOX_BIG_CASE(EVOX_OCC_CSO, 0)
+        default: return 0;
+    }
 #undef EVOX_OCC_CSO
     return n;
 }

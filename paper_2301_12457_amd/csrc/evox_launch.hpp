@@ -22,6 +22,7 @@ struct PsoArgs {
     uint32_t k0, k1;
     uint32_t t;  // generation whose move this launch performs
     SelSlots *slots;
+    bool nt;     // streaming hint on row accesses
 };
 
 struct EvalArgs {
@@ -29,6 +30,7 @@ struct EvalArgs {
     int64_t N, D, ldx;
     float *out;
     SelSlots *slots;  // nullable: no selection
+    bool nt;          // streaming hint on row accesses
 };
 
 struct InitArgs {
@@ -43,6 +45,7 @@ struct CsoArgs {
     float *x, *v, *fit;
     const float *xbar;
     const uint32_t *perm;
+    const uint64_t *pw;
     int64_t N, D, ldx;
     float phi, lb, ub;
     int32_t xclamp;
@@ -83,11 +86,14 @@ constexpr int kPermMaxBits = 13;        // superbuckets <= 8192
 constexpr int kPermMaxBuckets = 1 << kPermMaxBits;
 constexpr int kPermSortCap = 4096;      // LDS capacity of one superbucket sort (mean <= 2048)
 constexpr int64_t kCsoMaxN = (int64_t)1 << 24;
+constexpr uint64_t kPairUnknown = ~(uint64_t)0;  // pw entry decided by the generation kernel
 struct PermArgs {
     int64_t N;
     int bits;  // superbuckets = 2^bits
     uint32_t k0, k1, t;
     uint32_t *hist, *offs, *cursor, *tkey, *tidx, *perm;
+    const float *fit;  // current fitness (pair decisions)
+    uint64_t *pw;      // [N / 2] winner | loser << 32, or kPairUnknown
 };
 hipError_t launch_perm(const PermArgs &a, hipStream_t s);
 hipError_t launch_cso(int fn, Layout L, const CsoArgs &a, int grid, hipStream_t s);

@@ -44,24 +44,35 @@ def test_struct_layouts_match_header(evox):
 
 
 def test_row_layout_policy(evox):
+    # PSO / evaluation: the fewest lanes that hold a row in <= 2 float4 per lane
     assert evox.row_layout(1) == (4, 1)
     assert evox.row_layout(10) == (4, 1)
-    assert evox.row_layout(100) == (8, 4)
-    assert evox.row_layout(1000) == (64, 4)
-    assert evox.row_layout(1001) == (64, 4)
+    assert evox.row_layout(100) == (16, 2)
+    assert evox.row_layout(1000) == (128, 2)
+    assert evox.row_layout(1001) == (128, 2)
     assert evox.row_layout(32768) == (1024, 8)
+    cap = lambda G: 8 if G == 1024 else 2
     for D in list(range(1, 300)) + [1023, 1024, 1025, 4096, 4097, 16385, 32767]:
         G, nit = evox.row_layout(D)
-        assert G * nit * 4 >= D and nit <= (8 if G == 1024 else 4)
-        assert G == 4 or (G // 2) * (8 if G // 2 == 1024 else 4) * 4 < D or nit > 1
+        c4 = (D + 3) // 4
+        assert G * nit >= c4 and nit <= cap(G)
+        assert G == 4 or (G // 2) * cap(G // 2) < c4      # no smaller group holds the row
     with pytest.raises(evox.EvoxError):
         evox.row_layout(32769)
     # CSO: one chunk per lane while it fits
-    assert evox.row_layout(100, evox.CSO) == (32, 1)
-    assert evox.row_layout(10, evox.CSO) == (4, 1)
-    assert evox.row_layout(4096, evox.CSO) == (1024, 1)
-    assert evox.row_layout(4100, evox.CSO) == (1024, 2)
-    assert evox.row_layout(32768, evox.CSO) == (1024, 8)
+    C = evox.LAYOUT_CSO
+    assert evox.row_layout(100, C) == (32, 1)
+    assert evox.row_layout(10, C) == (4, 1)
+    assert evox.row_layout(4096, C) == (1024, 1)
+    assert evox.row_layout(4100, C) == (1024, 2)
+    assert evox.row_layout(32768, C) == (1024, 8)
+    # evox_eval: up to 4 chunks per lane (one wave per row at D = 1000)
+    E = evox.LAYOUT_EVAL
+    assert evox.row_layout(1000, E) == (64, 4)
+    assert evox.row_layout(100, E) == (8, 4)
+    assert evox.row_layout(32768, E) == (1024, 8)
+    with pytest.raises(evox.EvoxError):
+        evox.row_layout(100, 3)
 
 
 def test_scratch_bytes(evox):
