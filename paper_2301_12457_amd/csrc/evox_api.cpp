@@ -68,8 +68,9 @@ struct Plan {
     Layout L{0, 0, 0};
     int grid = 0, cso_grid = 0, colsum_grid = 0, bits = 0;
     size_t best = 0, slots = 0;
-    size_t hist = 0, offs = 0, cursor = 0, tkey = 0, tidx = 0, perm = 0, pw = 0, xsum = 0, s1 = 0, ticket = 0;
+    size_t hist = 0, offs = 0, cursor = 0, tkey = 0, tidx = 0, perm = 0, xsum = 0, s1 = 0, ticket = 0;
     int64_t xsum_rows = 0;
+    int perm_batch = 0;
     size_t total = 0;
 };
 
@@ -104,14 +105,16 @@ int make_plan(const evox_params *P, Plan *pl)
         p.cso_grid = grid_for(P->N / 2 + (P->N & 1), p.L.G, cap);
         p.colsum_grid = grid_for(P->N, p.L.G, cap);
         p.bits = perm_bits(P->N);
-        const size_t nb = (size_t)1 << p.bits;
-        p.hist = take(4 * nb);
-        p.offs = take(4 * (nb + 1));
-        p.cursor = take(4 * nb);
-        p.tkey = take(4 * (size_t)P->N);
-        p.tidx = take(4 * (size_t)P->N);
-        p.perm = take(4 * (size_t)P->N);
-        p.pw = take(8 * (size_t)(P->N / 2 + 1));
+        // permutations sorted kPermBatch generations at a time, within 256 MB
+        int64_t batch = ((int64_t)256 << 20) / (12 * P->N);
+        p.perm_batch = (int)(batch < 1 ? 1 : batch > kPermBatch ? kPermBatch : batch);
+        const size_t B = (size_t)p.perm_batch, nb = (size_t)1 << p.bits;
+        p.hist = take(4 * nb * B);
+        p.offs = take(4 * (nb + 1) * B);
+        p.cursor = take(4 * nb * B);
+        p.tkey = take(4 * (size_t)P->N * B);
+        p.tidx = take(4 * (size_t)P->N * B);
+        p.perm = take(4 * (size_t)P->N * B);
         p.xsum_rows = cap;
         p.xsum = take(sizeof(double) * (size_t)cap * (size_t)P->ldx);
         p.s1 = take(sizeof(double) * (size_t)kMeanStages * (size_t)P->ldx);
@@ -134,7 +137,7 @@ struct evox_state {
     DevBest *best;
     SelSlots *slots;
     uint32_t *hist, *offs, *cursor, *tkey, *tidx, *perm, *ticket;
-    uint64_t *pw;
+    int64_t perm_t0;  // first generation of the stored permutation batch (-1: none)
     double *xsum, *s1;
     // profiling of the fused generation kernel
     bool prof;
@@ -203,9 +206,10 @@ PsoArgs pso_args(evox_state *s)
     return a;
 }
 
+// Swarm mean from nparts partial rows; also the selection from the slots.
 MeanArgs mean_args(evox_state *s, int nparts)
 {
-    return MeanArgs{s->xsum, nparts, s->P.N, s->P.D, s->P.ldx, s->B.xbar, s->s1, s->ticket};
+    return MeanArgs{s->xsum, nparts, s->P.N, s->P.D, s->P.ldx, s->B.xbar, s->s1, s->ticket, s->slots, s->best};
 }
 
 // CSO: fit (optional), swarm mean and best of the current positions.
@@ -221,12 +225,10 @@ int cso_refresh(evox_state *s, bool refit)
     }
     if ((e = launch_colsum(pl.L, s->B.x, P.N, P.D, P.ldx, s->xsum, pl.colsum_grid, s->stream)) != hipSuccess)
         return hip_fail(e, "column sums");
-    if ((e = launch_cso_mean(mean_args(s, pl.colsum_grid), s->stream)) != hipSuccess)
-        return hip_fail(e, "swarm mean");
     if ((e = launch_argmin_slots(s->B.fit, P.N, s->slots, s->stream)) != hipSuccess)
         return hip_fail(e, "select");
-    if ((e = launch_select(s->slots, nullptr, 0, nullptr, s->best, nullptr, nullptr, s->stream)) != hipSuccess)
-        return hip_fail(e, "select");
+    if ((e = launch_cso_mean(mean_args(s, pl.colsum_grid), s->stream)) != hipSuccess)
+        return hip_fail(e, "swarm mean");
     return EVOX_OK;
 }
 
@@ -274,7 +276,7 @@ int evox_state_create(const evox_params *params, const evox_buffers *b, void *hi
     s->slots = at<SelSlots>(b->scratch, pl.slots);
     s->hist = s->offs = s->cursor = s->tkey = s->tidx = s->perm = nullptr;
     s->xsum = s->s1 = nullptr;
-    s->pw = nullptr;
+    s->perm_t0 = -1;
     s->ticket = nullptr;
     if (P.algo == EVOX_CSO) {
         s->hist = at<uint32_t>(b->scratch, pl.hist);
@@ -283,7 +285,6 @@ int evox_state_create(const evox_params *params, const evox_buffers *b, void *hi
         s->tkey = at<uint32_t>(b->scratch, pl.tkey);
         s->tidx = at<uint32_t>(b->scratch, pl.tidx);
         s->perm = at<uint32_t>(b->scratch, pl.perm);
-        s->pw = at<uint64_t>(b->scratch, pl.pw);
         s->xsum = at<double>(b->scratch, pl.xsum);
         s->s1 = at<double>(b->scratch, pl.s1);
         s->ticket = at<uint32_t>(b->scratch, pl.ticket);
@@ -321,7 +322,7 @@ int evox_state_create(const evox_params *params, const evox_buffers *b, void *hi
             return hip_fail(e, "init");
         }
     } else {
-        const size_t nb = (size_t)1 << pl.bits;
+        const size_t nb = ((size_t)1 << pl.bits) * (size_t)pl.perm_batch;
         if ((e = launch_zero_u32(s->hist, (int64_t)nb, s->stream)) != hipSuccess ||
             (e = launch_zero_u32(s->cursor, (int64_t)nb, s->stream)) != hipSuccess ||
             (e = launch_zero_u32(s->ticket, (P.ldx + 63) / 64, s->stream)) != hipSuccess ||
@@ -450,19 +451,20 @@ int evox_cso_step(evox_state *s, int64_t n_gens)
     const Plan &pl = s->pl;
     hipError_t e;
     for (int64_t k = 0; k < n_gens; ++k) {
-        const uint32_t t = (uint32_t)(s->t + k);
-        PermArgs pa{P.N, pl.bits, s->k0, s->k1, t, s->hist, s->offs, s->cursor, s->tkey, s->tidx, s->perm,
-                    s->B.fit, s->pw};
-        if ((e = launch_perm(pa, s->stream)) != hipSuccess) return hip_fail(e, "pairing");
-        CsoArgs ca{s->B.x, s->B.v, s->B.fit, s->B.xbar, s->perm, s->pw, P.N, P.D, P.ldx, P.phi, P.lb, P.ub,
-                   P.clamp_x != 0, s->k0, s->k1, t, s->slots, s->xsum};
+        const int64_t t = s->t + k;
+        if (s->perm_t0 < 0 || t < s->perm_t0 || t >= s->perm_t0 + pl.perm_batch) {
+            PermArgs pa{P.N, pl.bits, s->k0, s->k1, (uint32_t)t, (uint32_t)pl.perm_batch, s->hist, s->offs,
+                        s->cursor, s->tkey, s->tidx, s->perm};
+            if ((e = launch_perm(pa, s->stream)) != hipSuccess) return hip_fail(e, "pairing");
+            s->perm_t0 = t;
+        }
+        const uint32_t *perm = s->perm + (t - s->perm_t0) * P.N;
+        CsoArgs ca{s->B.x, s->B.v, s->B.fit, s->B.xbar, perm, P.N, P.D, P.ldx, P.phi, P.lb, P.ub,
+                   P.clamp_x != 0, s->k0, s->k1, (uint32_t)t, s->slots, s->xsum};
         e = timed(s, [&] { return launch_cso(P.fn_id, pl.L, ca, pl.cso_grid, s->stream); });
         if (e != hipSuccess) return hip_fail(e, "cso generation");
         if ((e = launch_cso_mean(mean_args(s, pl.cso_grid), s->stream)) != hipSuccess)
             return hip_fail(e, "swarm mean");
-        if ((e = launch_select(s->slots, nullptr, 0, nullptr, s->best, nullptr, nullptr, s->stream)) !=
-            hipSuccess)
-            return hip_fail(e, "select");
     }
     s->t += n_gens;
     return EVOX_OK;

@@ -12,8 +12,10 @@
 //                 placement of (key, index) into the superbucket ranges
 //   k_perm_sort   one block per superbucket (~1000 entries): counting sort on
 //                 the next 8 key bits in LDS, then ranks inside sub-buckets,
-//                 written as the permutation, and the winner / loser of every
-//                 pair inside the superbucket
+//                 written as the permutation
+// The permutation depends only on (seed, t), so a batch of generations is
+// sorted at once (grid dimension y), which fills the GPU far better than one
+// generation of these latency-bound passes.
 #include "evox_kernels.hpp"
 
 namespace evox {
@@ -232,17 +234,32 @@ __device__ __forceinline__ uint32_t bucket_of(uint32_t key, int bits)
     return bits ? key >> (32 - bits) : 0u;
 }
 
-// Keys of the 16 individuals 4 * (4 * (blockIdx * 256) + r * 256 + tid) + e,
+// A batch of permutations covers generations t0 .. t0 + gridDim.y - 1; block
+// row blockIdx.y works on generation t0 + blockIdx.y and its slice of each
+// array (counts nb, offsets nb + 1, keys / indices / permutation N).
+struct PermSlice {
+    uint32_t t;
+    uint32_t *hist, *offs, *cursor, *tkey, *tidx, *perm;
+};
+
+__device__ __forceinline__ PermSlice perm_slice(const PermArgs &a)
+{
+    const int64_t b = blockIdx.y, nb = (int64_t)1 << a.bits;
+    return PermSlice{a.t0 + (uint32_t)b, a.hist + b * nb, a.offs + b * (nb + 1), a.cursor + b * nb,
+                     a.tkey + b * a.N, a.tidx + b * a.N, a.perm + b * a.N};
+}
+
+// Keys of the 16 individuals 4 * (blockIdx.x * 1024 + r * 256 + tid) + e,
 // r, e < 4, handled by one thread of a perm block (4096 per block).
 template <typename F>
-__device__ __forceinline__ void for_block_keys(const PermArgs &a, F &&f)
+__device__ __forceinline__ void for_block_keys(const PermArgs &a, uint32_t t, F &&f)
 {
     const int64_t q0 = (int64_t)blockIdx.x * (kPermChunk / 4);
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
         const int64_t q = q0 + r * 256 + threadIdx.x;
         if (4 * q < a.N) {
-            const U4 w = philox((uint32_t)q, 0u, a.t, STREAM_PERM, a.k0, a.k1);
+            const U4 w = philox((uint32_t)q, 0u, t, STREAM_PERM, a.k0, a.k1);
             const uint32_t k4[4] = {w.x, w.y, w.z, w.w};
 #pragma unroll
             for (int e = 0; e < 4; ++e)
@@ -256,13 +273,14 @@ __device__ __forceinline__ void for_block_keys(const PermArgs &a, F &&f)
 __global__ __launch_bounds__(256) void k_perm_count(PermArgs a)
 {
     __shared__ uint32_t h[kPermMaxBuckets];
+    const PermSlice sl = perm_slice(a);
     const int nb = 1 << a.bits;
     for (int b = threadIdx.x; b < nb; b += 256) h[b] = 0;
     __syncthreads();
-    for_block_keys(a, [&](uint32_t key, int64_t) { atomicAdd(&h[bucket_of(key, a.bits)], 1u); });
+    for_block_keys(a, sl.t, [&](uint32_t key, int64_t) { atomicAdd(&h[bucket_of(key, a.bits)], 1u); });
     __syncthreads();
     for (int b = threadIdx.x; b < nb; b += 256)
-        if (h[b]) atomicAdd(&a.hist[b], h[b]);
+        if (h[b]) atomicAdd(&sl.hist[b], h[b]);
 }
 
 // Exclusive scan of n <= kPermMaxBuckets counts into off (LDS), 256 threads.
@@ -295,59 +313,48 @@ __global__ __launch_bounds__(256) void k_perm_place(PermArgs a)
 {
     __shared__ uint32_t cnt[kPermMaxBuckets];
     __shared__ uint32_t off[kPermMaxBuckets];
+    const PermSlice sl = perm_slice(a);
     const int nb = 1 << a.bits;
-    for (int b = threadIdx.x; b < nb; b += 256) cnt[b] = a.hist[b];
+    for (int b = threadIdx.x; b < nb; b += 256) cnt[b] = sl.hist[b];
     __syncthreads();
     lds_exclusive_scan(cnt, nb, off);
     if (blockIdx.x == 0) {
-        for (int b = threadIdx.x; b < nb; b += 256) a.offs[b] = off[b];
-        if (threadIdx.x == 0) a.offs[nb] = (uint32_t)a.N;
+        for (int b = threadIdx.x; b < nb; b += 256) sl.offs[b] = off[b];
+        if (threadIdx.x == 0) sl.offs[nb] = (uint32_t)a.N;
     }
     for (int b = threadIdx.x; b < nb; b += 256) cnt[b] = 0;
     __syncthreads();
-    for_block_keys(a, [&](uint32_t key, int64_t) { atomicAdd(&cnt[bucket_of(key, a.bits)], 1u); });
+    for_block_keys(a, sl.t, [&](uint32_t key, int64_t) { atomicAdd(&cnt[bucket_of(key, a.bits)], 1u); });
     __syncthreads();
     for (int b = threadIdx.x; b < nb; b += 256)
-        if (cnt[b]) off[b] += atomicAdd(&a.cursor[b], cnt[b]);
+        if (cnt[b]) off[b] += atomicAdd(&sl.cursor[b], cnt[b]);
     __syncthreads();
-    for_block_keys(a, [&](uint32_t key, int64_t i) {
+    for_block_keys(a, sl.t, [&](uint32_t key, int64_t i) {
         const uint32_t pos = atomicAdd(&off[bucket_of(key, a.bits)], 1u);
-        a.tkey[pos] = key;
-        a.tidx[pos] = (uint32_t)i;
+        sl.tkey[pos] = key;
+        sl.tidx[pos] = (uint32_t)i;
     });
 }
 
 // Pass 3: one block per superbucket orders its entries by (key, index): a
 // counting sort on the next 8 key bits (256 sub-buckets of ~4 entries) in
-// LDS, then each entry's rank inside its sub-bucket by comparison.  The
-// ordered indices are written as the permutation, and every pair
-// (perm[2k], perm[2k+1]) that lies inside the superbucket is decided here:
-// pw[k] = winner | loser << 32 (the second wins when its fitness is strictly
-// lower, or the first's is NaN and its own is not).  A pair that straddles two
-// superbuckets gets kPairUnknown and is decided by the generation kernel.
-// The bucket's count and cursor are then cleared for the next generation.  A
-// bucket larger than the LDS capacity (not expected for uniform keys) is
-// ranked directly in global memory and all its pairs are left undecided.
-__device__ __forceinline__ uint64_t decide_pair(const float *fit, uint32_t a, uint32_t b)
-{
-    const float fa = fit[a], fb = fit[b];
-    const bool second = fb < fa || (fa != fa && fb == fb);
-    return second ? ((uint64_t)a << 32) | b : ((uint64_t)b << 32) | a;
-}
-
+// LDS, then each entry's rank inside its sub-bucket by comparison; the
+// ordered indices are written as the permutation.  The bucket's count and
+// cursor are then cleared for the next batch.  A bucket larger than the LDS
+// capacity (not expected for uniform keys) is ranked in global memory.
 __global__ __launch_bounds__(256) void k_perm_sort(PermArgs a)
 {
     __shared__ uint32_t K[kPermSortCap], I[kPermSortCap], S[kPermSortCap];
     __shared__ uint32_t cnt[256], start[256], cur[256];
+    const PermSlice sl = perm_slice(a);
     const int b = blockIdx.x;
-    const uint32_t lo = a.offs[b], n = a.hist[b];
+    const uint32_t lo = sl.offs[b], n = sl.hist[b];
     const int shift = 24 - a.bits;  // the 8 key bits below the superbucket bits
-    const uint32_t np = (uint32_t)(a.N / 2);
     if (n <= (uint32_t)kPermSortCap) {
         cnt[threadIdx.x] = 0;
         __syncthreads();
         for (uint32_t q = threadIdx.x; q < n; q += 256)
-            atomicAdd(&cnt[(a.tkey[lo + q] >> shift) & 255u], 1u);
+            atomicAdd(&cnt[(sl.tkey[lo + q] >> shift) & 255u], 1u);
         __syncthreads();
         if (threadIdx.x < 64) {  // exclusive scan of 256 counts by one wave, 4 per lane
             const int l = threadIdx.x;
@@ -367,10 +374,10 @@ __global__ __launch_bounds__(256) void k_perm_sort(PermArgs a)
         cur[threadIdx.x] = start[threadIdx.x];
         __syncthreads();
         for (uint32_t q = threadIdx.x; q < n; q += 256) {
-            const uint32_t key = a.tkey[lo + q];
+            const uint32_t key = sl.tkey[lo + q];
             const uint32_t pos = atomicAdd(&cur[(key >> shift) & 255u], 1u);
             K[pos] = key;
-            I[pos] = a.tidx[lo + q];
+            I[pos] = sl.tidx[lo + q];
         }
         __syncthreads();
         for (uint32_t q = threadIdx.x; q < n; q += 256) {
@@ -381,30 +388,22 @@ __global__ __launch_bounds__(256) void k_perm_sort(PermArgs a)
             S[s0 + rank] = idx;
         }
         __syncthreads();
-        for (uint32_t q = threadIdx.x; q < n; q += 256) {
-            a.perm[lo + q] = S[q];
-            const uint32_t p = lo + q;
-            if ((p & 1u) == 0 && p / 2 < np)
-                a.pw[p / 2] = q + 1 < n ? decide_pair(a.fit, S[q], S[q + 1]) : kPairUnknown;
-            else if ((p & 1u) == 1 && q == 0)
-                a.pw[p / 2] = kPairUnknown;
-        }
+        for (uint32_t q = threadIdx.x; q < n; q += 256) sl.perm[lo + q] = S[q];
     } else {
         for (uint32_t p = threadIdx.x; p < n; p += 256) {
-            const uint32_t key = a.tkey[lo + p], idx = a.tidx[lo + p];
+            const uint32_t key = sl.tkey[lo + p], idx = sl.tidx[lo + p];
             uint32_t rank = 0;
             for (uint32_t q = 0; q < n; ++q) {
-                const uint32_t kq = a.tkey[lo + q], iq = a.tidx[lo + q];
+                const uint32_t kq = sl.tkey[lo + q], iq = sl.tidx[lo + q];
                 rank += (kq < key || (kq == key && iq < idx)) ? 1u : 0u;
             }
-            a.perm[lo + rank] = idx;
-            if ((lo + p) / 2 < np) a.pw[(lo + p) / 2] = kPairUnknown;
+            sl.perm[lo + rank] = idx;
         }
     }
     __syncthreads();
     if (threadIdx.x == 0) {
-        a.hist[b] = 0;
-        a.cursor[b] = 0;
+        sl.hist[b] = 0;
+        sl.cursor[b] = 0;
     }
 }
 
@@ -412,12 +411,13 @@ hipError_t launch_perm(const PermArgs &a, hipStream_t s)
 {
     const unsigned chunks = (unsigned)((a.N + kPermChunk - 1) / kPermChunk);
     const unsigned nb = 1u << a.bits;
-    hipLaunchKernelGGL(k_perm_count, dim3(chunks), dim3(256), 0, s, a);
-    hipLaunchKernelGGL(k_perm_place, dim3(chunks), dim3(256), 0, s, a);
-    hipLaunchKernelGGL(k_perm_sort, dim3(nb), dim3(256), 0, s, a);
+    hipLaunchKernelGGL(k_perm_count, dim3(chunks, a.batch), dim3(256), 0, s, a);
+    hipLaunchKernelGGL(k_perm_place, dim3(chunks, a.batch), dim3(256), 0, s, a);
+    hipLaunchKernelGGL(k_perm_sort, dim3(nb, a.batch), dim3(256), 0, s, a);
     return hipGetLastError();
 }
 
+// Block (0, 0) also finishes the selection (slots -> best) when asked.
 // xbar = (sum of the per-block partial rows) / N, rounded once, in two
 // stages.  Block (tile, rg) of 64 columns x 4 lanes: lane l sums partial rows
 // rg + S (l + 4 u), u = 0, 1, ... (S = kMeanStages) in that order, the four
@@ -446,6 +446,24 @@ __global__ __launch_bounds__(256) void k_cso_mean(MeanArgs m)
 {
     __shared__ double part[4][64];
     __shared__ int last;
+    if (m.slots && blockIdx.x == 0 && blockIdx.y == 0) {
+        // second pass of the selection over the generation kernel's slots
+        __shared__ uint64_t sk[4];
+        __shared__ uint32_t sc[4];
+        uint64_t k = kNoKey;
+        uint32_t none = 0;
+        for (int q = threadIdx.x; q < kSlots; q += 256) {
+            const uint64_t kq = m.slots->key[q];
+            k = kq < k ? kq : k;
+            m.slots->key[q] = kNoKey;
+            m.slots->cnt[q] = 0;
+        }
+        block_min_key(k, none, sk, sc);
+        if (threadIdx.x == 0) {
+            m.best->f = key_value(k);
+            m.best->i = k == kNoKey ? 0 : key_index(k);
+        }
+    }
     const int col = threadIdx.x & 63, lane = threadIdx.x >> 6;
     const int64_t tile = blockIdx.x, rg = blockIdx.y;
     const int64_t j = tile * 64 + col;

@@ -250,35 +250,24 @@ __global__ __launch_bounds__(block_for(G)) void k_cso(CsoArgs a)
     uint32_t none = 0;
     ColAcc<G, MAXIT> acc(acc_lds);
 
-    // pairs come decided from the pairing sort; the next iteration's pair is
-    // loaded one iteration ahead so the row gathers do not wait for it
-    const int64_t stride = (int64_t)gridDim.x * RPB;
-    int64_t kb = (int64_t)blockIdx.x * RPB;
-    uint64_t u_next = kb + slot < NP ? a.pw[kb + slot] : kPairUnknown;
-    for (; kb < NG; kb += stride) {
+    for (int64_t kb = (int64_t)blockIdx.x * RPB; kb < NG; kb += (int64_t)gridDim.x * RPB) {
         const int64_t k = kb + slot;
         const bool active = k < NG;
         const bool paired = k < NP;
-        const uint64_t u = u_next;
-        u_next = k + stride < NP ? a.pw[k + stride] : kPairUnknown;
         int64_t w = 0, l = 0;
         float fw = 0.0f;
         if (active) {
             if (paired) {
-                if (u != kPairUnknown) {
-                    w = (int64_t)(uint32_t)u;
-                    l = (int64_t)(u >> 32);
-                } else {  // pair across two superbuckets
-                    const int64_t p0 = a.perm[2 * k], p1 = a.perm[2 * k + 1];
-                    const float f0 = a.fit[p0], f1 = a.fit[p1];
-                    const bool second = f1 < f0 || (f0 != f0 && f1 == f1);
-                    w = second ? p1 : p0;
-                    l = second ? p0 : p1;
-                }
+                const int64_t p0 = a.perm[2 * k], p1 = a.perm[2 * k + 1];
+                const float f0 = a.fit[p0], f1 = a.fit[p1];
+                const bool second = f1 < f0 || (f0 != f0 && f1 == f1);
+                w = second ? p1 : p0;
+                l = second ? p0 : p1;
+                fw = second ? f1 : f0;
             } else {
                 w = a.perm[a.N - 1];
+                fw = a.fit[w];
             }
-            fw = a.fit[w];
         }
         float4 xr[MAXIT];
 #pragma unroll

@@ -44,8 +44,7 @@ struct InitArgs {
 struct CsoArgs {
     float *x, *v, *fit;
     const float *xbar;
-    const uint32_t *perm;
-    const uint64_t *pw;
+    const uint32_t *perm;  // this generation's permutation
     int64_t N, D, ldx;
     float phi, lb, ub;
     int32_t xclamp;
@@ -86,14 +85,14 @@ constexpr int kPermMaxBits = 13;        // superbuckets <= 8192
 constexpr int kPermMaxBuckets = 1 << kPermMaxBits;
 constexpr int kPermSortCap = 4096;      // LDS capacity of one superbucket sort (mean <= 2048)
 constexpr int64_t kCsoMaxN = (int64_t)1 << 24;
-constexpr uint64_t kPairUnknown = ~(uint64_t)0;  // pw entry decided by the generation kernel
+constexpr int kPermBatch = 8;           // generations per permutation batch at most
 struct PermArgs {
     int64_t N;
-    int bits;  // superbuckets = 2^bits
-    uint32_t k0, k1, t;
-    uint32_t *hist, *offs, *cursor, *tkey, *tidx, *perm;
-    const float *fit;  // current fitness (pair decisions)
-    uint64_t *pw;      // [N / 2] winner | loser << 32, or kPairUnknown
+    int bits;           // superbuckets = 2^bits
+    uint32_t k0, k1;
+    uint32_t t0;        // first generation of the batch
+    uint32_t batch;     // generations in the batch
+    uint32_t *hist, *offs, *cursor, *tkey, *tidx, *perm;  // [batch][...] slices
 };
 hipError_t launch_perm(const PermArgs &a, hipStream_t s);
 hipError_t launch_cso(int fn, Layout L, const CsoArgs &a, int grid, hipStream_t s);
@@ -109,6 +108,8 @@ struct MeanArgs {
     float *xbar;         // [ldx]
     double *s1;          // [kMeanStages][ldx] stage sums
     uint32_t *ticket;    // [ceil(ldx / 64)], zero between launches
+    SelSlots *slots;     // nullable: also reduce these selection slots into best
+    DevBest *best;
 };
 hipError_t launch_cso_mean(const MeanArgs &m, hipStream_t s);
 
