@@ -44,6 +44,10 @@ __global__ __launch_bounds__(block_for(G)) void k_pso(PsoArgs a)
 
     const int tid = threadIdx.x, g = tid % G, slot = tid / G;
     const int64_t C4 = (a.D + 3) >> 2;
+    // chunks written per row: the padding up to the row pitch is rewritten
+    // (with zeros) where the lanes cover it, so that rows of a 128-byte-
+    // aligned pitch are written as whole cache lines
+    const int64_t CW = a.ldx / 4 < (int64_t)G * MAXIT ? a.ldx / 4 : (int64_t)G * MAXIT;
     uint64_t best = kNoKey;
     uint32_t nimp = 0;
 
@@ -85,6 +89,10 @@ __global__ __launch_bounds__(block_for(G)) void k_pso(PsoArgs a)
                 } else {
                     xn = xv;
                 }
+            } else if (MOVE && active && c < CW) {
+                const int64_t off = row * a.ldx + 4 * c;
+                st_row(a.x + off, xn, a.nt);
+                st_row(a.v + off, xn, a.nt);
             }
             xr[it] = xn;
         }
@@ -97,7 +105,7 @@ __global__ __launch_bounds__(block_for(G)) void k_pso(PsoArgs a)
 #pragma unroll
                     for (int it = 0; it < MAXIT; ++it) {
                         const int64_t c = g + (int64_t)G * it;
-                        if (c < C4) st_row(a.p + row * a.ldx + 4 * c, xr[it], a.nt);
+                        if (c < CW) st_row(a.p + row * a.ldx + 4 * c, xr[it], a.nt);
                     }
                 }
                 if (g == 0) {

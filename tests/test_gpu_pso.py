@@ -117,3 +117,18 @@ def test_single_particle(evox_gpu, ref):
         g.step(1)
         r.step(1)
         compare_state(g, r, 2, f"generation {t}")
+
+
+@pytest.mark.parametrize("D,ldx", [(1001, 1024), (10, 64), (37, 40), (1000, 1000)])
+def test_padding_columns_stay_zero(evox_gpu, ref, D, ldx):
+    N = 9
+    g = evox_gpu.Swarm(evox_gpu.make_params(evox_gpu.PSO, 2, N, D, -5.12, 5.12, seed=4, ldx=ldx))
+    r = ref.PSO(ref.make_params(2, N, D, -5.12, 5.12, seed=4))
+    for _ in range(3):
+        g.step(2)
+        r.step(2)
+        for name in ("x", "v", "pbest"):
+            t = getattr(g, name).cpu().numpy()
+            assert np.all(t[:, D:] == 0), name
+        assert np.all(g.gbest[D:].cpu().numpy() == 0)
+        compare_state(g, r, 2, f"D {D} ldx {ldx}")
