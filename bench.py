@@ -34,9 +34,11 @@ def kernel_hash():
     return h.hexdigest()[:16]
 
 
-def traffic_from_profile(name, launches_bytes_unit):
-    """HBM bytes per launch of the dominant kernel from the committed PMC
-    summary, if it was taken on the current kernel sources."""
+def traffic_from_profile(name):
+    """HBM bytes per launch of the dominant kernel from the committed
+    rocprofv3 FETCH_SIZE / WRITE_SIZE summary (KiB per dispatch, each scaled
+    by what the counter reads for a device copy of known size), if it was
+    taken on the current kernel sources; None otherwise."""
     path = os.path.join(ROOT, "profiles", f"{name}_traffic.json")
     if not os.path.exists(path):
         return None
@@ -44,7 +46,8 @@ def traffic_from_profile(name, launches_bytes_unit):
         t = json.load(f)
     if t.get("kernel_sha") != kernel_hash():
         return None
-    return (t["fetch_kib_per_dispatch"] + t["write_kib_per_dispatch"]) * 1024.0 * t["copy_scale"]
+    return 1024.0 * (t["fetch_kib_per_dispatch"] * t["fetch_scale"] +
+                     t["write_kib_per_dispatch"] * t["write_scale"])
 
 
 def pso_bytes_per_launch(w, launches, improved_rows):
@@ -173,7 +176,7 @@ def main():
                          else cso_bytes_per_launch(w))
             achieved = bytes_per / (avg_ms / 1e3) / 1e9
             kname = "k_pso_fused" if w.algo == "pso" else "k_cso"
-            traffic = traffic_from_profile(w.name, bytes_per)
+            traffic = traffic_from_profile(w.name)
             roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                         "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                         "traffic": traffic, "kernel": kname,
@@ -184,7 +187,7 @@ def main():
         achieved = bytes_per / (ms / 1e3) / 1e9
         roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
-                    "traffic": traffic_from_profile(w.name, bytes_per), "kernel": "k_eval",
+                    "traffic": traffic_from_profile(w.name), "kernel": "k_eval",
                     "avg_launch_us": round(ms * 1e3, 2), "launches": args.steps,
                     "algorithmic_bytes_per_launch": bytes_per}
 
