@@ -195,6 +195,15 @@ enum evox_layout { EVOX_LAYOUT_PSO = 0, EVOX_LAYOUT_CSO = 1, EVOX_LAYOUT_EVAL = 
  * (PSO), 1 (CSO) or 4 (evox_eval) chunks per thread, and 8 at 1024 threads. */
 int evox_row_layout(int32_t kernels, int64_t D, int32_t *threads_per_row, int32_t *chunks_per_thread);
 
+/* Recommended row pitch (ldx, in floats) of an algo's state of dimension D:
+ * a multiple of 32 floats (rows start on 128-byte cache lines) where that
+ * pays, else a multiple of 4.  PSO (rows streamed in order; its kernels also
+ * write the padding so that row ends are whole lines): 32-multiples for
+ * D >= 512, where the padding is at most ~6 %.  CSO (rows gathered and
+ * written at random; padding never touched): 32-multiples for D >= 64.
+ * Returns the pitch, or 0 for an unknown algo or D outside [1, EVOX_MAX_D]. */
+int64_t evox_default_ldx(int32_t algo, int64_t D);
+
 /* Diagnostic: out[4 k + m] = word m of Philox(seed, (k, c1, c2, c3)) for
  * k < n_ctr, computed by the device Philox the kernels use (device out). */
 int evox_philox_fill(uint64_t seed, uint32_t c1, uint32_t c2, uint32_t c3, int64_t n_ctr,

@@ -23,7 +23,8 @@ MAX_D = 32768
 EXPORTS = (
     "evox_scratch_bytes", "evox_state_create", "evox_state_destroy", "evox_eval", "evox_eval_ld",
     "evox_eval_argmin_scratch_bytes", "evox_eval_argmin", "evox_pso_step", "evox_cso_step",
-    "evox_cso_refresh", "evox_best", "evox_generation", "evox_row_layout", "evox_philox_fill",
+    "evox_cso_refresh", "evox_best", "evox_generation", "evox_row_layout", "evox_default_ldx",
+    "evox_philox_fill",
     "evox_profile", "evox_profile_read", "evox_strerror", "evox_last_error",
 )
 
@@ -79,6 +80,7 @@ def lib():
             "evox_best": ([P, P, P, P], i32),
             "evox_generation": ([P], i64),
             "evox_row_layout": ([i32, i64, P, P], i32),
+            "evox_default_ldx": ([i32, i64], i64),
             "evox_philox_fill": ([u64, u32, u32, u32, i64, P, P], i32),
             "evox_profile": ([P, i32], i32),
             "evox_profile_read": ([P, P, P, P], i32),
@@ -148,16 +150,18 @@ def evox_philox_fill(seed, c1, c2, c3, n_ctr, out, stream=None):
     return out
 
 
-def pitch(D):
-    """Default row pitch in floats: a multiple of 32 (128-byte rows, whole
-    cache lines) when that costs at most ~6 % padding (D >= 512), else a
-    multiple of 4 (16-byte rows)."""
-    return (D + 31) // 32 * 32 if D >= 512 else (D + 3) // 4 * 4
+def pitch(D, algo=PSO):
+    """Recommended row pitch in floats for an algo's state (evox_default_ldx:
+    128-byte-aligned rows where that pays, else 16-byte)."""
+    ldx = lib().evox_default_ldx(algo, D)
+    if ldx <= 0:
+        raise EvoxError(EINVAL, f"no row pitch for algo {algo}, D = {D}")
+    return ldx
 
 
 def make_params(algo, fn_id, N, D, lb, ub, v_lo=0.0, v_hi=0.0, w=0.6, c1=1.5, c2=1.5, phi=0.1,
                 vmax=0.0, clamp_x=0, seed=0, ldx=None):
-    return Params(algo=algo, fn_id=fn_id, N=N, D=D, ldx=pitch(D) if ldx is None else ldx,
+    return Params(algo=algo, fn_id=fn_id, N=N, D=D, ldx=pitch(D, algo) if ldx is None else ldx,
                   lb=lb, ub=ub, v_lo=v_lo, v_hi=v_hi, w=w, c1=c1, c2=c2, phi=phi, vmax=vmax,
                   clamp_x=clamp_x, seed=seed)
 

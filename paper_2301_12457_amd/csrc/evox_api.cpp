@@ -510,6 +510,15 @@ int evox_row_layout(int32_t kernels, int64_t D, int32_t *threads_per_row, int32_
     return EVOX_OK;
 }
 
+int64_t evox_default_ldx(int32_t algo, int64_t D)
+{
+    if (D < 1 || D > EVOX_MAX_D) return 0;
+    const int64_t line = (D + 31) / 32 * 32, quad = (D + 3) / 4 * 4;
+    if (algo == EVOX_PSO) return D >= 512 ? line : quad;
+    if (algo == EVOX_CSO) return D >= 64 ? line : quad;
+    return 0;
+}
+
 int evox_philox_fill(uint64_t seed, uint32_t c1, uint32_t c2, uint32_t c3, int64_t n_ctr,
                      uint32_t *out_dev, void *hip_stream)
 {

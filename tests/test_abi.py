@@ -75,6 +75,22 @@ def test_row_layout_policy(evox):
         evox.row_layout(100, 3)
 
 
+def test_default_pitch_policy(evox):
+    L = evox.lib()
+    P, C = evox.PSO, evox.CSO
+    for D, want in [(1, 4), (10, 12), (100, 100), (511, 512), (512, 512), (1000, 1024), (1025, 1056),
+                    (32768, 32768)]:
+        assert L.evox_default_ldx(P, D) == want, (D, want)
+    for D, want in [(1, 4), (10, 12), (63, 64), (64, 64), (65, 96), (100, 128), (1000, 1024)]:
+        assert L.evox_default_ldx(C, D) == want, (D, want)
+    for algo, D in [(P, 0), (C, 32769), (2, 10)]:
+        assert L.evox_default_ldx(algo, D) == 0
+    assert evox.make_params(C, evox.GRIEWANK, 10, 100, -1, 1).ldx == 128
+    assert evox.make_params(P, evox.GRIEWANK, 10, 100, -1, 1).ldx == 100
+    with pytest.raises(evox.EvoxError):
+        evox.pitch(0)
+
+
 def test_scratch_bytes(evox):
     p = evox.make_params(evox.PSO, evox.SPHERE, 100, 10, -1, 1)
     assert evox.evox_scratch_bytes(p) > 0

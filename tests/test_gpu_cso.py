@@ -131,3 +131,30 @@ def test_refresh_after_external_edit(evox_gpu, ref):
     r.fit[:] = ref.evaluate(2, X)
     assert_fitness(2, X, g.fit.cpu().numpy(), r.fit, "refit")
     assert ulp_diff(host(g.xbar, 16), ref.colmean(X)).max() <= 1
+
+
+@pytest.mark.parametrize("D,ldx", [(100, 100), (100, 128), (37, 40), (70, 96), (257, 288), (64, 64)])
+def test_pitched_states_match_oracle(evox_gpu, ref, D, ldx):
+    """Any 4-multiple pitch gives the same generations; padding stays zero."""
+    N, fn, gens = 301, 3, 6
+    print(f"cso pitched D={D} ldx={ldx}", flush=True)
+    g = evox_gpu.Swarm(evox_gpu.make_params(evox_gpu.CSO, fn, N, D, -600.0, 600.0, seed=9, ldx=ldx))
+    r = ref.CSO(ref.make_params(fn, N, D, -600.0, 600.0, seed=9))
+    assert g.P.ldx == ldx and g.x.shape[1] == ldx
+    for t in range(gens):
+        xbar_ref = ref.colmean(r.x)
+        strict = np.array_equal(host(g.xbar, D), xbar_ref)
+        g.step(1)
+        r.step(1)
+        compare(g, r, fn, f"generation {t}", strict=strict)
+        for name in ("x", "v", "xbar"):
+            pad = getattr(g, name)[..., D:]
+            assert int((pad != 0).sum()) == 0, f"{name} padding written at generation {t}"
+        if not strict:
+            break
+
+
+def test_default_pitch_is_line_aligned(evox_gpu, ref):
+    g = evox_gpu.Swarm(evox_gpu.make_params(evox_gpu.CSO, 3, 64, 100, -600.0, 600.0, seed=3))
+    assert g.P.ldx == 128
+    assert g.x.data_ptr() % 128 == 0 and (g.P.ldx * 4) % 128 == 0
