@@ -23,7 +23,9 @@ class RefParams(ctypes.Structure):
         ("lb", ctypes.c_float), ("ub", ctypes.c_float),
         ("v_lo", ctypes.c_float), ("v_hi", ctypes.c_float),
         ("w", ctypes.c_float), ("c1", ctypes.c_float), ("c2", ctypes.c_float),
-        ("phi", ctypes.c_float), ("vmax", ctypes.c_float), ("pad_", ctypes.c_float),
+        ("phi", ctypes.c_float), ("vmax", ctypes.c_float),
+        ("x_init", ctypes.c_int32), ("x_mu", ctypes.c_float), ("x_sigma", ctypes.c_float),
+        ("pad_", ctypes.c_float),
         ("seed", ctypes.c_uint64),
     ]
 
@@ -52,6 +54,9 @@ def lib():
         L.evox_ref_argmin.argtypes = [P, i64]
         L.evox_ref_argmin.restype = i64
         L.evox_ref_init_uniform.argtypes = [u64, ctypes.c_int, i64, i64, f32, f32, P]
+        L.evox_ref_normal01.argtypes = [u64, i64, i64]
+        L.evox_ref_normal01.restype = ctypes.c_double
+        L.evox_ref_init_normal.argtypes = [u64, i64, i64, f32, f32, P]
         L.evox_ref_pso_init.argtypes = [P, P, P, P, P, P, P, P]
         L.evox_ref_pso_step.argtypes = [P, i64, i64, P, P, P, P, P, P, P]
         L.evox_ref_colmean.argtypes = [P, i64, i64, P]
@@ -122,10 +127,22 @@ def init_uniform(seed, stream, N, D, lo, hi):
     return out
 
 
+def normal01(seed, i, j):
+    """The fp64 standard normal deviate of element (i, j) (stream 5)."""
+    return lib().evox_ref_normal01(seed, i, j)
+
+
+def init_normal(seed, N, D, mu, sigma):
+    out = np.zeros((N, D), dtype=np.float32)
+    lib().evox_ref_init_normal(seed, N, D, mu, sigma, _ptr(out))
+    return out
+
+
 def make_params(fn, N, D, lb, ub, v_lo=0.0, v_hi=0.0, w=0.6, c1=1.5, c2=1.5, phi=0.1,
-                vmax=0.0, clamp_x=0, seed=0):
+                vmax=0.0, clamp_x=0, seed=0, x_init=0, x_mu=0.0, x_sigma=1.0):
     return RefParams(fn=fn, clamp_x=clamp_x, N=N, D=D, lb=lb, ub=ub, v_lo=v_lo, v_hi=v_hi,
-                     w=w, c1=c1, c2=c2, phi=phi, vmax=vmax, pad_=0.0, seed=seed)
+                     w=w, c1=c1, c2=c2, phi=phi, vmax=vmax, x_init=x_init, x_mu=x_mu,
+                     x_sigma=x_sigma, pad_=0.0, seed=seed)
 
 
 class PSO:

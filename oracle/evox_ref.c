@@ -93,7 +93,7 @@ void evox_ref_u01_array(const uint32_t *w, int64_t n, float *out)
 
 /* Random-stream identifiers (the counter's fourth word). */
 enum { STREAM_INIT_X = 0, STREAM_INIT_V = 1, STREAM_PSO = 2, STREAM_CSO = 3,
-       STREAM_PERM = 4 };
+       STREAM_PERM = 4, STREAM_INIT_NORMAL = 5 };
 
 /* Draw k of K for element (i, j) at generation t in stream s:
  * word (j mod 4) of Philox(seed, (K*floor(j/4) + k, i, t, s)). */
@@ -246,6 +246,8 @@ typedef struct {
     float w, c1, c2;    /* PSO inertia and acceleration coefficients */
     float phi;          /* CSO social factor */
     float vmax;         /* PSO velocity clamp; <= 0 means none */
+    int32_t x_init;     /* 0: x ~ U[lb, ub); 1: x ~ N(x_mu, x_sigma^2) */
+    float x_mu, x_sigma;
     float pad_;
     uint64_t seed;      /* Philox key */
 } evox_ref_params;
@@ -265,9 +267,41 @@ void evox_ref_init_uniform(uint64_t seed, int stream, int64_t N, int64_t D, floa
             out[i * D + j] = uniform_in(draw(seed, i, j, 1, 0, 0, stream), lo, hi);
 }
 
+/* Standard normal deviate for element (i, j) of the normal initial
+ * population, by the Box-Muller transform (Box & Muller, Ann. Math. Statist.
+ * 29, 1958): one Philox call per four elements, Philox(seed, (floor(j/4), i,
+ * 0, 5)); elements 4c, 4c+1 use words (0, 1) and elements 4c+2, 4c+3 words
+ * (2, 3).  Of a word pair (a, b), u1 = ((a >> 8) + 1) 2^-24 lies in (0, 1]
+ * (never 0, so the logarithm is finite) and u2 = (b >> 8) 2^-24 in [0, 1);
+ * with radius r = sqrt(-2 ln u1) and angle 2 pi u2, the even element of the
+ * pair is r cos(angle) and the odd one r sin(angle).  fp64 throughout. */
+double evox_ref_normal01(uint64_t seed, int64_t i, int64_t j)
+{
+    const uint32_t c0 = (uint32_t)(j / 4);
+    const int q = (int)(j % 4) / 2;
+    const uint32_t a = evox_ref_philox_word(seed, c0, (uint32_t)i, 0u, STREAM_INIT_NORMAL, 2 * q);
+    const uint32_t b = evox_ref_philox_word(seed, c0, (uint32_t)i, 0u, STREAM_INIT_NORMAL, 2 * q + 1);
+    const double u1 = ((double)(a >> 8) + 1.0) * 0x1p-24;
+    const double u2 = (double)(b >> 8) * 0x1p-24;
+    const double r = sqrt(-2.0 * log(u1));
+    const double angle = 2.0 * kPi * u2;
+    return (j % 2 == 0) ? r * cos(angle) : r * sin(angle);
+}
+
+/* x_ij = mu + sigma z_ij with z from evox_ref_normal01, rounded once. */
+void evox_ref_init_normal(uint64_t seed, int64_t N, int64_t D, float mu, float sigma, float *out)
+{
+    for (int64_t i = 0; i < N; ++i)
+        for (int64_t j = 0; j < D; ++j)
+            out[i * D + j] = (float)((double)mu + (double)sigma * evox_ref_normal01(seed, i, j));
+}
+
 static void init_xv(const evox_ref_params *P, float *x, float *v)
 {
-    evox_ref_init_uniform(P->seed, STREAM_INIT_X, P->N, P->D, P->lb, P->ub, x);
+    if (P->x_init == 1)
+        evox_ref_init_normal(P->seed, P->N, P->D, P->x_mu, P->x_sigma, x);
+    else
+        evox_ref_init_uniform(P->seed, STREAM_INIT_X, P->N, P->D, P->lb, P->ub, x);
     if (P->v_lo == 0.0f && P->v_hi == 0.0f)
         memset(v, 0, sizeof(float) * (size_t)(P->N * P->D));
     else
