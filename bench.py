@@ -16,7 +16,7 @@ import time
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
-from paper_2301_12457_amd.workloads import WORKLOADS, normal_matrix_torch  # noqa: E402
+from paper_2301_12457_amd.workloads import WORKLOADS  # noqa: E402
 
 METRIC = "individual·dim updates/sec per fused generation; % of HBM peak GB/s"
 UNIT = "individual·dim updates/s"
@@ -71,10 +71,8 @@ def cpu_baseline(w, budget_s=12.0):
     fn = {"sphere": 0, "ackley": 1, "rastrigin": 2, "griewank": 3, "rosenbrock": 4,
           "schwefel": 5}[w.fn]
     if w.algo == "eval":
-        import numpy as np
-        from paper_2301_12457_amd.workloads import normal_matrix_np
         rows = 20_000
-        X = normal_matrix_np(rows, w.D, w.x_mu, w.x_sigma, w.seed)
+        X = oracle.init_normal(w.seed, rows, w.D, w.x_mu, w.x_sigma)
         t0 = time.perf_counter()
         n = 0
         while time.perf_counter() - t0 < budget_s:
@@ -124,7 +122,8 @@ def main():
     fn = evox.FN_IDS[w.fn]
 
     if w.algo == "eval":
-        X = normal_matrix_torch(w.N, w.D, w.x_mu, w.x_sigma, w.seed)
+        X = torch.empty((w.N, w.D), dtype=torch.float32, device="cuda")
+        evox.evox_fill_normal(w.seed, w.N, w.D, w.D, w.x_mu, w.x_sigma, X)
         out = torch.empty(w.N, dtype=torch.float32, device="cuda")
         bf = torch.empty(1, dtype=torch.float32, device="cuda")
         bi = torch.empty(1, dtype=torch.int64, device="cuda")

@@ -83,12 +83,16 @@ typedef struct evox_params {
     int64_t N;        /* population size: PSO 1 .. 2^31 - 1, CSO 2 .. 2^24 */
     int64_t D;        /* dimension, 1 .. EVOX_MAX_D */
     int64_t ldx;      /* row pitch of x, v, pbest in floats: ldx >= D, ldx % 4 == 0 */
-    float lb, ub;     /* initial positions ~ U[lb, ub): x = fma(u, ub - lb, lb) */
+    float lb, ub;     /* x_init 0: initial positions ~ U[lb, ub): x = fma(u, ub - lb, lb);
+                         also the clamp box of clamp_x */
     float v_lo, v_hi; /* initial velocities ~ U[v_lo, v_hi); both 0 gives v = 0 */
     float w, c1, c2;  /* PSO inertia and acceleration coefficients */
     float phi;        /* CSO social factor */
     float vmax;       /* PSO velocity clamp to [-vmax, vmax]; <= 0: none */
     int32_t clamp_x;  /* nonzero: positions clamped to [lb, ub] after each move */
+    int32_t x_init;   /* 0: uniform in [lb, ub); 1: normal, as evox_fill_normal(seed, x_mu,
+                         x_sigma) */
+    float x_mu, x_sigma;
     uint64_t seed;    /* Philox key */
 } evox_params;
 
@@ -194,6 +198,21 @@ enum evox_layout { EVOX_LAYOUT_PSO = 0, EVOX_LAYOUT_CSO = 1, EVOX_LAYOUT_EVAL = 
  * are the fewest (a power of two, 4..1024) that hold the row in at most 2
  * (PSO), 1 (CSO) or 4 (evox_eval) chunks per thread, and 8 at 1024 threads. */
 int evox_row_layout(int32_t kernels, int64_t D, int32_t *threads_per_row, int32_t *chunks_per_thread);
+
+/* Normal synthetic population: X[i][j] = mu + sigma z_ij for i < N, j < D
+ * (device X, [N][ldx] floats, 16-byte aligned, ldx % 4 == 0, ldx >= D;
+ * columns D..ldx-1 set to 0).  z_ij is a standard normal deviate by the
+ * Box-Muller transform (Box & Muller, 1958) of Philox stream 5: one call
+ * Philox(seed, (floor(j/4), i, 0, 5)) per four elements; of its word pairs
+ * (0, 1) and (2, 3), a pair (a, b) gives u1 = ((a >> 8) + 1) 2^-24 in (0, 1],
+ * u2 = (b >> 8) 2^-24, r = sqrt(-2 ln u1), and elements r cos(2 pi u2) (even
+ * j) and r sin(2 pi u2) (odd j).  Computed in fp32 with the device logf, a
+ * correctly rounded sqrt and the hardware cosine / sine of the exactly
+ * reduced angle, so within sigma 1e-6 max(1, |z|) + 1 ulp of the exact value.
+ * The initial population of an x_init = 1 state is the same matrix.  N = 0
+ * does nothing. */
+int evox_fill_normal(uint64_t seed, int64_t N, int64_t D, int64_t ldx, float mu, float sigma,
+                     float *X, void *hip_stream);
 
 /* Recommended row pitch (ldx, in floats) of an algo's state of dimension D:
  * a multiple of 32 floats (rows start on 128-byte cache lines) where that

@@ -24,7 +24,7 @@ EXPORTS = (
     "evox_scratch_bytes", "evox_state_create", "evox_state_destroy", "evox_eval", "evox_eval_ld",
     "evox_eval_argmin_scratch_bytes", "evox_eval_argmin", "evox_pso_step", "evox_cso_step",
     "evox_cso_refresh", "evox_best", "evox_generation", "evox_row_layout", "evox_default_ldx",
-    "evox_philox_fill",
+    "evox_fill_normal", "evox_philox_fill",
     "evox_profile", "evox_profile_read", "evox_strerror", "evox_last_error",
 )
 
@@ -44,6 +44,7 @@ class Params(ctypes.Structure):
         ("w", ctypes.c_float), ("c1", ctypes.c_float), ("c2", ctypes.c_float),
         ("phi", ctypes.c_float), ("vmax", ctypes.c_float),
         ("clamp_x", ctypes.c_int32),
+        ("x_init", ctypes.c_int32), ("x_mu", ctypes.c_float), ("x_sigma", ctypes.c_float),
         ("seed", ctypes.c_uint64),
     ]
 
@@ -81,6 +82,7 @@ def lib():
             "evox_generation": ([P], i64),
             "evox_row_layout": ([i32, i64, P, P], i32),
             "evox_default_ldx": ([i32, i64], i64),
+            "evox_fill_normal": ([u64, i64, i64, i64, ctypes.c_float, ctypes.c_float, P, P], i32),
             "evox_philox_fill": ([u64, u32, u32, u32, i64, P, P], i32),
             "evox_profile": ([P, i32], i32),
             "evox_profile_read": ([P, P, P, P], i32),
@@ -150,6 +152,12 @@ def evox_philox_fill(seed, c1, c2, c3, n_ctr, out, stream=None):
     return out
 
 
+def evox_fill_normal(seed, N, D, ldx, mu, sigma, X, stream=None):
+    """X[:N, :D] = mu + sigma z (Philox stream 5, Box-Muller); padding set to 0."""
+    _check(lib().evox_fill_normal(seed, N, D, ldx, mu, sigma, _ptr(X), _stream(stream)))
+    return X
+
+
 def pitch(D, algo=PSO):
     """Recommended row pitch in floats for an algo's state (evox_default_ldx:
     128-byte-aligned rows where that pays, else 16-byte)."""
@@ -160,10 +168,10 @@ def pitch(D, algo=PSO):
 
 
 def make_params(algo, fn_id, N, D, lb, ub, v_lo=0.0, v_hi=0.0, w=0.6, c1=1.5, c2=1.5, phi=0.1,
-                vmax=0.0, clamp_x=0, seed=0, ldx=None):
+                vmax=0.0, clamp_x=0, seed=0, ldx=None, x_init=0, x_mu=0.0, x_sigma=1.0):
     return Params(algo=algo, fn_id=fn_id, N=N, D=D, ldx=pitch(D, algo) if ldx is None else ldx,
                   lb=lb, ub=ub, v_lo=v_lo, v_hi=v_hi, w=w, c1=c1, c2=c2, phi=phi, vmax=vmax,
-                  clamp_x=clamp_x, seed=seed)
+                  clamp_x=clamp_x, x_init=x_init, x_mu=x_mu, x_sigma=x_sigma, seed=seed)
 
 
 def evox_scratch_bytes(params):

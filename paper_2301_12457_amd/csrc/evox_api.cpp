@@ -88,6 +88,7 @@ int make_plan(const evox_params *P, Plan *pl)
         return fail(EVOX_EINVAL, "CSO N = %lld above %lld", (long long)P->N, (long long)kCsoMaxN);
     if (P->ldx < P->D || (P->ldx & 3))
         return fail(EVOX_EINVAL, "ldx = %lld must be >= D and a multiple of 4", (long long)P->ldx);
+    if (P->x_init != 0 && P->x_init != 1) return fail(EVOX_EINVAL, "unknown x_init %d", P->x_init);
     Plan p;
     const int family = P->algo == EVOX_CSO ? LAYOUT_CSO : LAYOUT_PSO;
     if (!row_layout(P->D, family, &p.L)) return fail(EVOX_EINVAL, "no row layout for D = %lld", (long long)P->D);
@@ -305,7 +306,8 @@ int evox_state_create(const evox_params *params, const evox_buffers *b, void *hi
 
     hipError_t e;
     InitArgs ia{b->x, b->v, P.algo == EVOX_PSO ? b->pbest : nullptr, P.N, P.D, P.ldx, P.lb, P.ub,
-                P.v_lo, P.v_hi, P.v_lo == 0.0f && P.v_hi == 0.0f, s->k0, s->k1};
+                P.v_lo, P.v_hi, P.v_lo == 0.0f && P.v_hi == 0.0f, P.x_init == 1, P.x_mu, P.x_sigma,
+                s->k0, s->k1};
     if ((e = launch_init(ia, s->stream)) != hipSuccess) {
         delete s;
         return hip_fail(e, "init");
@@ -517,6 +519,23 @@ int64_t evox_default_ldx(int32_t algo, int64_t D)
     if (algo == EVOX_PSO) return D >= 512 ? line : quad;
     if (algo == EVOX_CSO) return D >= 64 ? line : quad;
     return 0;
+}
+
+int evox_fill_normal(uint64_t seed, int64_t N, int64_t D, int64_t ldx, float mu, float sigma,
+                     float *X, void *hip_stream)
+{
+    if (N < 0 || N >= ((int64_t)1 << 31)) return fail(EVOX_EINVAL, "N = %lld out of range [0, 2^31)", (long long)N);
+    if (D < 1 || ldx < D || (ldx & 3) || ldx / 4 >= ((int64_t)1 << 32))
+        return fail(EVOX_EINVAL, "D = %lld, ldx = %lld: need 1 <= D <= ldx, ldx %% 4 == 0", (long long)D,
+                    (long long)ldx);
+    if (N == 0) return EVOX_OK;
+    if (!X) return fail(EVOX_EINVAL, "X is null");
+    if (!aligned16(X)) return fail(EVOX_EALIGN, "X is not 16-byte aligned");
+    InitArgs ia{X, nullptr, nullptr, N, D, ldx, 0.0f, 0.0f, 0.0f, 0.0f, 1, 1, mu, sigma,
+                (uint32_t)seed, (uint32_t)(seed >> 32)};
+    hipError_t e = launch_init(ia, (hipStream_t)hip_stream);
+    if (e != hipSuccess) return hip_fail(e, "fill normal");
+    return EVOX_OK;
 }
 
 int evox_philox_fill(uint64_t seed, uint32_t c1, uint32_t c2, uint32_t c3, int64_t n_ctr,

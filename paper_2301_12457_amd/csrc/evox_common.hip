@@ -34,21 +34,27 @@ __global__ __launch_bounds__(256) void k_init(InitArgs a)
         const int64_t row = q / L4, c = q - row * L4;
         float xo[4] = {0.f, 0.f, 0.f, 0.f}, vo[4] = {0.f, 0.f, 0.f, 0.f};
         if (c < C4) {
-            const U4 rx = philox((uint32_t)c, (uint32_t)row, 0u, STREAM_INIT_X, a.k0, a.k1);
-            U4 rv{0, 0, 0, 0};
-            if (!a.v_zero) rv = philox((uint32_t)c, (uint32_t)row, 0u, STREAM_INIT_V, a.k0, a.k1);
+            if (a.x_normal) {
+                const float4 z = normal4((uint32_t)c, (uint32_t)row, a.k0, a.k1);
 #pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                if (4 * c + e < a.D) {
-                    xo[e] = fmaf(wcomp(rx, e), xr, a.lb);
-                    vo[e] = a.v_zero ? 0.0f : fmaf(wcomp(rv, e), vr, a.v_lo);
-                }
+                for (int e = 0; e < 4; ++e)
+                    if (4 * c + e < a.D) xo[e] = fmaf(a.sigma, comp(z, e), a.mu);
+            } else {
+                const U4 rx = philox((uint32_t)c, (uint32_t)row, 0u, STREAM_INIT_X, a.k0, a.k1);
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    if (4 * c + e < a.D) xo[e] = fmaf(wcomp(rx, e), xr, a.lb);
+            }
+            if (a.v && !a.v_zero) {
+                const U4 rv = philox((uint32_t)c, (uint32_t)row, 0u, STREAM_INIT_V, a.k0, a.k1);
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    if (4 * c + e < a.D) vo[e] = fmaf(wcomp(rv, e), vr, a.v_lo);
             }
         }
         const float4 X = make_float4(xo[0], xo[1], xo[2], xo[3]);
-        const float4 V = make_float4(vo[0], vo[1], vo[2], vo[3]);
         reinterpret_cast<float4 *>(a.x)[q] = X;
-        reinterpret_cast<float4 *>(a.v)[q] = V;
+        if (a.v) reinterpret_cast<float4 *>(a.v)[q] = make_float4(vo[0], vo[1], vo[2], vo[3]);
         if (a.p) reinterpret_cast<float4 *>(a.p)[q] = X;
     }
 }

@@ -34,10 +34,12 @@ struct EvalArgs {
 };
 
 struct InitArgs {
-    float *x, *v, *p;  // p nullable
+    float *x, *v, *p;  // v, p nullable
     int64_t N, D, ldx;
     float lb, ub, v_lo, v_hi;
     int32_t v_zero;
+    int32_t x_normal;  // x = mu + sigma z (stream 5) instead of U[lb, ub)
+    float mu, sigma;
     uint32_t k0, k1;
 };
 

@@ -4,7 +4,10 @@ Holds none of the method's arithmetic: only the sizes and hyperparameters of
 each workload and seeded generators of input matrices, shared by the tests
 and the benchmark.  The populations of the PSO / CSO workloads are drawn by
 the method itself (Philox streams 0 and 1 at creation); the evaluation-only
-workload reads a matrix generated here.
+workload's population is the library's normal population (Philox stream 5,
+evox_fill_normal) in the benchmark, and a matrix of the same distribution
+generated here wherever the oracle must see the very same input (the oracle
+never reads what the GPU path produced).
 
 The shapes stand in for the paper's large-scale numerical experiments
 (Sec. VII-A-1: population and dimension scaling on Sphere, populations up to

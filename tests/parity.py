@@ -75,3 +75,16 @@ def ulp_diff(a, b):
     ai = np.where(ai < 0, -(ai & 0x7FFFFFFF), ai)
     bi = np.where(bi < 0, -(bi & 0x7FFFFFFF), bi)
     return np.abs(ai - bi)
+
+
+def normal_tol(x_ref, mu, sigma):
+    """Tolerance of the device normal deviates (Box-Muller in fp32 against
+    the fp64 oracle): logf within 1 ulp and a correctly rounded sqrt put the
+    radius r within 2^-23 relative, the hardware cosine / sine of the exactly
+    reduced angle is within 1.25e-7 absolute, so |z_gpu - z| <= 1.25e-7 r +
+    1.8e-7 |z| <= 1e-6 max(1, |z|) for r <= sqrt(2 ln 2^24) = 5.77; the final
+    fma adds at most one rounding of x."""
+    x_ref = np.asarray(x_ref, dtype=np.float64)
+    z = np.abs(x_ref - mu) / sigma if sigma else np.zeros_like(x_ref)
+    ulp = np.spacing(np.abs(x_ref).astype(np.float32)).astype(np.float64)
+    return abs(sigma) * 1e-6 * np.maximum(1.0, z) + ulp

@@ -37,9 +37,10 @@ def test_exports_every_declared_symbol(evox):
 
 
 def test_struct_layouts_match_header(evox):
-    # evox_params: 2 x int32, 3 x int64, 9 floats, int32, (pad), uint64
-    assert ctypes.sizeof(evox.Params) == 80
-    assert evox.Params.seed.offset == 72
+    # evox_params: 2 x int32, 3 x int64, 9 floats, 2 x int32, 2 floats, (pad), uint64
+    assert ctypes.sizeof(evox.Params) == 96
+    assert evox.Params.x_init.offset == 72
+    assert evox.Params.seed.offset == 88
     assert ctypes.sizeof(evox.Buffers) == 9 * 8
 
 
@@ -103,7 +104,8 @@ def test_scratch_bytes(evox):
 
 @pytest.mark.parametrize("algo,field,value", [(0, "N", 0), (0, "D", 0), (0, "D", 40000),
                                               (0, "ldx", 6), (0, "fn_id", 6), (0, "algo", 3),
-                                              (1, "N", 1), (1, "N", 2**24 + 1)])
+                                              (1, "N", 1), (1, "N", 2**24 + 1), (0, "x_init", 2),
+                                              (1, "x_init", -1)])
 def test_create_rejects_bad_params(evox, algo, field, value):
     p = evox.make_params(algo, evox.SPHERE, 8, 5, -1, 1)
     setattr(p, field, value)
@@ -140,6 +142,12 @@ def test_eval_rejects_bad_args(evox):
     assert L.evox_eval(0, None, 0, 3, None, None) == evox.OK     # empty: nothing to do
     assert L.evox_eval_ld(0, None, 0, 8, 4, None, None) == evox.EINVAL
     assert L.evox_eval_argmin(0, None, 0, 3, 3, None, None, None, None, 0, None) == evox.EINVAL
+    assert L.evox_fill_normal(1, 0, 3, 4, 0.0, 1.0, None, None) == evox.OK     # empty
+    assert L.evox_fill_normal(1, 5, 3, 4, 0.0, 1.0, None, None) == evox.EINVAL
+    assert L.evox_fill_normal(1, 5, 5, 4, 0.0, 1.0, 0x1000, None) == evox.EINVAL
+    assert L.evox_fill_normal(1, 5, 3, 6, 0.0, 1.0, 0x1000, None) == evox.EINVAL
+    assert L.evox_fill_normal(1, -1, 3, 4, 0.0, 1.0, 0x1000, None) == evox.EINVAL
+    assert L.evox_fill_normal(1, 5, 3, 4, 0.0, 1.0, 0x1004, None) == evox.EALIGN
 
 
 def test_null_state_is_rejected(evox):
