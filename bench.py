@@ -65,8 +65,34 @@ def cso_bytes_per_launch(w):
     return 20.0 * pairs * w.D + pairs * (4 * 2 + 4 * 2 + 4)
 
 
+def host_cpu():
+    """Model name of the host CPU and the number of cores this process may use."""
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return model, len(os.sched_getaffinity(0))
+
+
 def cpu_baseline(w, budget_s=12.0):
-    """The oracle, single-threaded, on a bounded sample of the workload."""
+    """The oracle, single-threaded and pinned to one core, on a bounded sample
+    of the workload."""
+    allowed = os.sched_getaffinity(0)
+    os.sched_setaffinity(0, {min(allowed)})
+    try:
+        out = _cpu_baseline(w, budget_s)
+    finally:
+        os.sched_setaffinity(0, allowed)
+    out["host_cpu"], out["host_cores_available"] = host_cpu()
+    return out
+
+
+def _cpu_baseline(w, budget_s):
     import oracle
     fn = {"sphere": 0, "ackley": 1, "rastrigin": 2, "griewank": 3, "rosenbrock": 4,
           "schwefel": 5}[w.fn]
@@ -94,6 +120,25 @@ def cpu_baseline(w, budget_s=12.0):
     dt = time.perf_counter() - t0
     return {"value": rows * w.D * gens / dt, "unit": UNIT, "cores": 1, "kind": "oracle",
             "sample": f"{rows} of {w.N} individuals x D={w.D}, {gens} generations, {dt:.1f} s"}
+
+
+def copy_bandwidth(torch, evox, mib=1024, reps=5):
+    """GB/s (read + write bytes) of the library's streaming 1 GiB device copy
+    on this GPU, measured in the same run as a reference for the achieved
+    bandwidth."""
+    n = mib * (1 << 20) // 4
+    a = torch.ones(n, dtype=torch.float32, device="cuda")
+    b = torch.empty_like(a)
+    evox.evox_copy(a, b, n)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        evox.evox_copy(a, b, n)
+    e1.record()
+    torch.cuda.synchronize()
+    sec = e0.elapsed_time(e1) / 1e3 / reps
+    del a, b
+    return 2.0 * n * 4 / sec / 1e9
 
 
 def main():
@@ -197,6 +242,11 @@ def main():
         for _ in range(3):
             b.copy_(a)
         torch.cuda.synchronize()
+        del a, b
+    if roofline is not None:
+        copy = copy_bandwidth(torch, evox)
+        roofline["copy_gbs"] = round(copy, 1)
+        roofline["frac_of_copy"] = round(roofline["achieved"] / copy, 4)
 
     base = None
     if not args.no_cpu_baseline:

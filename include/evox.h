@@ -223,6 +223,11 @@ int evox_fill_normal(uint64_t seed, int64_t N, int64_t D, int64_t ldx, float mu,
  * Returns the pitch, or 0 for an unknown algo or D outside [1, EVOX_MAX_D]. */
 int64_t evox_default_ldx(int32_t algo, int64_t D);
 
+/* Diagnostic, the bandwidth reference of the benchmark: dst[i] = src[i] for
+ * i < n (device pointers, 16-byte aligned, not overlapping), streamed with
+ * nontemporal 16-byte loads and stores.  n = 0 does nothing. */
+int evox_copy(const float *src, float *dst, int64_t n, void *hip_stream);
+
 /* Diagnostic: out[4 k + m] = word m of Philox(seed, (k, c1, c2, c3)) for
  * k < n_ctr, computed by the device Philox the kernels use (device out). */
 int evox_philox_fill(uint64_t seed, uint32_t c1, uint32_t c2, uint32_t c3, int64_t n_ctr,

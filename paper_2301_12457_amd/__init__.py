@@ -24,7 +24,7 @@ EXPORTS = (
     "evox_scratch_bytes", "evox_state_create", "evox_state_destroy", "evox_eval", "evox_eval_ld",
     "evox_eval_argmin_scratch_bytes", "evox_eval_argmin", "evox_pso_step", "evox_cso_step",
     "evox_cso_refresh", "evox_best", "evox_generation", "evox_row_layout", "evox_default_ldx",
-    "evox_fill_normal", "evox_philox_fill",
+    "evox_fill_normal", "evox_copy", "evox_philox_fill",
     "evox_profile", "evox_profile_read", "evox_strerror", "evox_last_error",
 )
 
@@ -83,6 +83,7 @@ def lib():
             "evox_row_layout": ([i32, i64, P, P], i32),
             "evox_default_ldx": ([i32, i64], i64),
             "evox_fill_normal": ([u64, i64, i64, i64, ctypes.c_float, ctypes.c_float, P, P], i32),
+            "evox_copy": ([P, P, i64, P], i32),
             "evox_philox_fill": ([u64, u32, u32, u32, i64, P, P], i32),
             "evox_profile": ([P, i32], i32),
             "evox_profile_read": ([P, P, P, P], i32),
@@ -156,6 +157,12 @@ def evox_fill_normal(seed, N, D, ldx, mu, sigma, X, stream=None):
     """X[:N, :D] = mu + sigma z (Philox stream 5, Box-Muller); padding set to 0."""
     _check(lib().evox_fill_normal(seed, N, D, ldx, mu, sigma, _ptr(X), _stream(stream)))
     return X
+
+
+def evox_copy(src, dst, n, stream=None):
+    """dst[:n] = src[:n] by the library's streaming copy (bandwidth reference)."""
+    _check(lib().evox_copy(_ptr(src), _ptr(dst), n, _stream(stream)))
+    return dst
 
 
 def pitch(D, algo=PSO):

@@ -538,6 +538,17 @@ int evox_fill_normal(uint64_t seed, int64_t N, int64_t D, int64_t ldx, float mu,
     return EVOX_OK;
 }
 
+int evox_copy(const float *src, float *dst, int64_t n, void *hip_stream)
+{
+    if (n < 0) return fail(EVOX_EINVAL, "n = %lld < 0", (long long)n);
+    if (n == 0) return EVOX_OK;
+    if (!src || !dst) return fail(EVOX_EINVAL, "src and dst are required");
+    if (!aligned16(src) || !aligned16(dst)) return fail(EVOX_EALIGN, "src or dst is not 16-byte aligned");
+    hipError_t e = launch_stream_copy(src, dst, n, (hipStream_t)hip_stream);
+    if (e != hipSuccess) return hip_fail(e, "copy");
+    return EVOX_OK;
+}
+
 int evox_philox_fill(uint64_t seed, uint32_t c1, uint32_t c2, uint32_t c3, int64_t n_ctr,
                      uint32_t *out_dev, void *hip_stream)
 {

@@ -74,6 +74,7 @@ hipError_t launch_slots_init(SelSlots *slots, hipStream_t s);
 hipError_t launch_init(const InitArgs &a, hipStream_t s);
 hipError_t launch_philox_fill(uint32_t k0, uint32_t k1, uint32_t c1, uint32_t c2, uint32_t c3,
                               int64_t n, uint32_t *out, hipStream_t s);
+hipError_t launch_stream_copy(const float *src, float *dst, int64_t n, hipStream_t s);
 hipError_t launch_copy_row(const float *src, float *dst, int64_t ldx, hipStream_t s);
 hipError_t launch_fill(float *dst, int64_t n, float value, hipStream_t s);
 hipError_t launch_best_init(DevBest *best, float f, int64_t i, hipStream_t s);

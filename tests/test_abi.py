@@ -142,6 +142,10 @@ def test_eval_rejects_bad_args(evox):
     assert L.evox_eval(0, None, 0, 3, None, None) == evox.OK     # empty: nothing to do
     assert L.evox_eval_ld(0, None, 0, 8, 4, None, None) == evox.EINVAL
     assert L.evox_eval_argmin(0, None, 0, 3, 3, None, None, None, None, 0, None) == evox.EINVAL
+    assert L.evox_copy(None, None, 0, None) == evox.OK
+    assert L.evox_copy(None, None, 5, None) == evox.EINVAL
+    assert L.evox_copy(0x1000, 0x2000, -1, None) == evox.EINVAL
+    assert L.evox_copy(0x1004, 0x2000, 5, None) == evox.EALIGN
     assert L.evox_fill_normal(1, 0, 3, 4, 0.0, 1.0, None, None) == evox.OK     # empty
     assert L.evox_fill_normal(1, 5, 3, 4, 0.0, 1.0, None, None) == evox.EINVAL
     assert L.evox_fill_normal(1, 5, 5, 4, 0.0, 1.0, 0x1000, None) == evox.EINVAL

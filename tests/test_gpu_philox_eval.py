@@ -101,3 +101,11 @@ def test_eval_empty_population(evox_gpu):
     X = torch.empty((0, 5), dtype=torch.float32, device="cuda")
     evox_gpu.evox_eval(0, X, out)
     torch.cuda.synchronize()
+
+
+@pytest.mark.parametrize("n", [1, 3, 4, 1027, 4096 * 1024 + 5])
+def test_stream_copy(evox_gpu, n):
+    src = torch.randn(n + 8, device="cuda")
+    dst = torch.zeros(n + 8, device="cuda")
+    evox_gpu.evox_copy(src, dst, n)
+    assert torch.equal(dst[:n], src[:n]) and torch.all(dst[n:] == 0)
