@@ -214,6 +214,28 @@ int evox_row_layout(int32_t kernels, int64_t D, int32_t *threads_per_row, int32_
 int evox_fill_normal(uint64_t seed, int64_t N, int64_t D, int64_t ldx, float mu, float sigma,
                      float *X, void *hip_stream);
 
+/* The pairing permutations of CSO generations t0 .. t0 + n_gens - 1 for a
+ * swarm of N individuals (1 <= N <= 2^24): perm_out[g][k] (device, uint32,
+ * [n_gens][N]) is the k-th individual in the order of (key_i, i), key_i =
+ * word (i mod 4) of Philox(seed, (floor(i/4), 0, t0 + g, 4)).  This is the
+ * permutation an evox_cso_step of that generation pairs by ((perm[2k],
+ * perm[2k+1]), Table II).  scratch (device, 256-byte aligned) holds at least
+ * evox_permutation_scratch_bytes(N, 1) bytes; with room for a batch of up to
+ * 8 generations, that many are sorted per launch.  Returns EVOX_ENOSPC if the
+ * scratch is too small. */
+size_t evox_permutation_scratch_bytes(int64_t N, int64_t batch);
+int evox_permutation(uint64_t seed, int64_t t0, int64_t n_gens, int64_t N, uint32_t *perm_out,
+                     void *scratch, size_t scratch_bytes, void *hip_stream);
+
+/* The same sort on caller keys (device, uint32, N <= EVOX_ARGSORT_MAX_N):
+ * perm_out[k] = the k-th index in the order of (keys[i], i), a stable
+ * argsort.  Keys that share their top bits in groups of more than 4096 are
+ * ranked by a quadratic pass, which is why N is bounded here.  scratch as for
+ * evox_permutation(N, 1 generation). */
+#define EVOX_ARGSORT_MAX_N 65536
+int evox_argsort_u32(const uint32_t *keys, int64_t N, uint32_t *perm_out, void *scratch,
+                     size_t scratch_bytes, void *hip_stream);
+
 /* Recommended row pitch (ldx, in floats) of an algo's state of dimension D:
  * a multiple of 32 floats (rows start on 128-byte cache lines) where that
  * pays, else a multiple of 4.  PSO (rows streamed in order; its kernels also

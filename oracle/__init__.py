@@ -61,6 +61,7 @@ def lib():
         L.evox_ref_pso_step.argtypes = [P, i64, i64, P, P, P, P, P, P, P]
         L.evox_ref_colmean.argtypes = [P, i64, i64, P]
         L.evox_ref_perm.argtypes = [u64, i64, i64, P]
+        L.evox_ref_argsort_u32.argtypes = [P, i64, P]
         L.evox_ref_cso_init.argtypes = [P, P, P, P]
         L.evox_ref_cso_step.argtypes = [P, i64, i64, P, P, P, P, P, P]
         _lib = L
@@ -189,6 +190,13 @@ def colmean(X):
     N, D = X.shape
     out = np.zeros(D, np.float32)
     lib().evox_ref_colmean(_ptr(X), N, D, _ptr(out))
+    return out
+
+
+def argsort_u32(keys):
+    keys = np.ascontiguousarray(keys, dtype=np.uint32)
+    out = np.zeros(keys.size, np.int64)
+    lib().evox_ref_argsort_u32(_ptr(keys), keys.size, _ptr(out))
     return out
 
 

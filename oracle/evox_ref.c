@@ -401,19 +401,29 @@ static int keyed_cmp(const void *pa, const void *pb)
     return (a->idx > b->idx) - (a->idx < b->idx);
 }
 
-/* Random permutation of 0..N-1 at generation t: sort the individuals by the
- * key (Philox word from stream 4), lower index first among equal keys. */
-void evox_ref_perm(uint64_t seed, int64_t t, int64_t N, int64_t *perm)
+/* The indices 0..N-1 in the order of (keys[i], i): a stable argsort. */
+void evox_ref_argsort_u32(const uint32_t *keys, int64_t N, int64_t *perm)
 {
     keyed *kv = (keyed *)malloc(sizeof(keyed) * (size_t)(N > 0 ? N : 1));
     for (int64_t i = 0; i < N; ++i) {
-        kv[i].key = evox_ref_philox_word(seed, (uint32_t)(i / 4), 0u, (uint32_t)t,
-                                         STREAM_PERM, (int)(i % 4));
+        kv[i].key = keys[i];
         kv[i].idx = i;
     }
     qsort(kv, (size_t)N, sizeof(keyed), keyed_cmp);
     for (int64_t i = 0; i < N; ++i) perm[i] = kv[i].idx;
     free(kv);
+}
+
+/* Random permutation of 0..N-1 at generation t: sort the individuals by the
+ * key (Philox word from stream 4), lower index first among equal keys. */
+void evox_ref_perm(uint64_t seed, int64_t t, int64_t N, int64_t *perm)
+{
+    uint32_t *keys = (uint32_t *)malloc(sizeof(uint32_t) * (size_t)(N > 0 ? N : 1));
+    for (int64_t i = 0; i < N; ++i)
+        keys[i] = evox_ref_philox_word(seed, (uint32_t)(i / 4), 0u, (uint32_t)t, STREAM_PERM,
+                                       (int)(i % 4));
+    evox_ref_argsort_u32(keys, N, perm);
+    free(keys);
 }
 
 /* Pair (a, b): b wins when its fitness is strictly lower, or when a's is

@@ -24,7 +24,8 @@ EXPORTS = (
     "evox_scratch_bytes", "evox_state_create", "evox_state_destroy", "evox_eval", "evox_eval_ld",
     "evox_eval_argmin_scratch_bytes", "evox_eval_argmin", "evox_pso_step", "evox_cso_step",
     "evox_cso_refresh", "evox_best", "evox_generation", "evox_row_layout", "evox_default_ldx",
-    "evox_fill_normal", "evox_copy", "evox_philox_fill",
+    "evox_fill_normal", "evox_copy", "evox_philox_fill", "evox_permutation_scratch_bytes",
+    "evox_permutation", "evox_argsort_u32",
     "evox_profile", "evox_profile_read", "evox_strerror", "evox_last_error",
 )
 
@@ -84,6 +85,9 @@ def lib():
             "evox_default_ldx": ([i32, i64], i64),
             "evox_fill_normal": ([u64, i64, i64, i64, ctypes.c_float, ctypes.c_float, P, P], i32),
             "evox_copy": ([P, P, i64, P], i32),
+            "evox_permutation_scratch_bytes": ([i64, i64], sz),
+            "evox_permutation": ([u64, i64, i64, i64, P, P, sz, P], i32),
+            "evox_argsort_u32": ([P, i64, P, P, sz, P], i32),
             "evox_philox_fill": ([u64, u32, u32, u32, i64, P, P], i32),
             "evox_profile": ([P, i32], i32),
             "evox_profile_read": ([P, P, P, P], i32),
@@ -163,6 +167,20 @@ def evox_copy(src, dst, n, stream=None):
     """dst[:n] = src[:n] by the library's streaming copy (bandwidth reference)."""
     _check(lib().evox_copy(_ptr(src), _ptr(dst), n, _stream(stream)))
     return dst
+
+
+def evox_permutation(seed, t0, n_gens, N, perm_out, scratch, stream=None):
+    """perm_out[g] = the CSO pairing permutation of generation t0 + g."""
+    _check(lib().evox_permutation(seed, t0, n_gens, N, _ptr(perm_out), _ptr(scratch),
+                                  scratch.numel() * scratch.element_size(), _stream(stream)))
+    return perm_out
+
+
+def evox_argsort_u32(keys, N, perm_out, scratch, stream=None):
+    """perm_out[:N] = stable argsort of the uint32 keys[:N] (as int32 tensors)."""
+    _check(lib().evox_argsort_u32(_ptr(keys), N, _ptr(perm_out), _ptr(scratch),
+                                  scratch.numel() * scratch.element_size(), _stream(stream)))
+    return perm_out
 
 
 def pitch(D, algo=PSO):

@@ -456,7 +456,7 @@ int evox_cso_step(evox_state *s, int64_t n_gens)
         const int64_t t = s->t + k;
         if (s->perm_t0 < 0 || t < s->perm_t0 || t >= s->perm_t0 + pl.perm_batch) {
             PermArgs pa{P.N, pl.bits, s->k0, s->k1, (uint32_t)t, (uint32_t)pl.perm_batch, s->hist, s->offs,
-                        s->cursor, s->tkey, s->tidx, s->perm};
+                        s->cursor, s->tkey, s->tidx, s->perm, nullptr};
             if ((e = launch_perm(pa, s->stream)) != hipSuccess) return hip_fail(e, "pairing");
             s->perm_t0 = t;
         }
@@ -519,6 +519,96 @@ int64_t evox_default_ldx(int32_t algo, int64_t D)
     if (algo == EVOX_PSO) return D >= 512 ? line : quad;
     if (algo == EVOX_CSO) return D >= 64 ? line : quad;
     return 0;
+}
+
+namespace {
+
+// Scratch of the pairing sort for `batch` generations of N individuals:
+// counts, offsets and cursors per superbucket, keys and indices per entry.
+size_t perm_scratch(int64_t N, int64_t batch, size_t *hist, size_t *offs, size_t *cursor, size_t *tkey,
+                    size_t *tidx)
+{
+    const size_t B = (size_t)batch, nb = (size_t)1 << perm_bits(N);
+    size_t off = 0;
+    auto take = [&](size_t bytes) {
+        const size_t at = off;
+        off = round256(off + bytes);
+        return at;
+    };
+    *hist = take(4 * nb * B);
+    *offs = take(4 * (nb + 1) * B);
+    *cursor = take(4 * nb * B);
+    *tkey = take(4 * (size_t)N * B);
+    *tidx = take(4 * (size_t)N * B);
+    return off;
+}
+
+size_t perm_scratch_total(int64_t N, int64_t batch)
+{
+    size_t a, b, c, d, e;
+    return perm_scratch(N, batch, &a, &b, &c, &d, &e);
+}
+
+// n_gens sorts of N keys into perm_out[n_gens][N], as many per launch as the
+// scratch holds (at most kPermBatch); keys (caller keys, n_gens 1) or null.
+int sort_batches(uint64_t seed, int64_t t0, int64_t n_gens, int64_t N, const uint32_t *keys,
+                 uint32_t *perm_out, void *scratch, size_t scratch_bytes, hipStream_t st)
+{
+    int64_t B = n_gens < kPermBatch ? n_gens : kPermBatch;
+    while (B > 1 && perm_scratch_total(N, B) > scratch_bytes) --B;
+    if (perm_scratch_total(N, B) > scratch_bytes)
+        return fail(EVOX_ENOSPC, "scratch has %zu bytes, needs %zu", scratch_bytes, perm_scratch_total(N, 1));
+    size_t oh, oo, oc, ok, oi;
+    perm_scratch(N, B, &oh, &oo, &oc, &ok, &oi);
+    uint32_t *hist = at<uint32_t>(scratch, oh), *cursor = at<uint32_t>(scratch, oc);
+    const int bits = perm_bits(N);
+    hipError_t e;
+    if ((e = launch_zero_u32(hist, ((int64_t)1 << bits) * B, st)) != hipSuccess ||
+        (e = launch_zero_u32(cursor, ((int64_t)1 << bits) * B, st)) != hipSuccess)
+        return hip_fail(e, "sort");
+    for (int64_t g = 0; g < n_gens; g += B) {
+        const int64_t b = n_gens - g < B ? n_gens - g : B;
+        PermArgs pa{N, bits, (uint32_t)seed, (uint32_t)(seed >> 32), (uint32_t)(t0 + g), (uint32_t)b, hist,
+                    at<uint32_t>(scratch, oo), cursor, at<uint32_t>(scratch, ok), at<uint32_t>(scratch, oi),
+                    perm_out + g * N, keys};
+        if ((e = launch_perm(pa, st)) != hipSuccess) return hip_fail(e, "sort");
+    }
+    return EVOX_OK;
+}
+
+}  // namespace
+
+size_t evox_permutation_scratch_bytes(int64_t N, int64_t batch)
+{
+    if (N < 1 || N > kCsoMaxN || batch < 1 || batch > kPermBatch) return 0;
+    return perm_scratch_total(N, batch);
+}
+
+int evox_permutation(uint64_t seed, int64_t t0, int64_t n_gens, int64_t N, uint32_t *perm_out, void *scratch,
+                     size_t scratch_bytes, void *hip_stream)
+{
+    if (N < 1 || N > kCsoMaxN) return fail(EVOX_EINVAL, "N = %lld out of range [1, 2^24]", (long long)N);
+    if (t0 < 0 || n_gens < 0 || t0 + n_gens > ((int64_t)1 << 32))
+        return fail(EVOX_EINVAL, "generations [%lld, %lld) outside [0, 2^32)", (long long)t0,
+                    (long long)(t0 + n_gens));
+    if (n_gens == 0) return EVOX_OK;
+    if (!perm_out || !scratch) return fail(EVOX_EINVAL, "perm_out and scratch are required");
+    if (((uintptr_t)perm_out & 3u) != 0) return fail(EVOX_EALIGN, "perm_out is not 4-byte aligned");
+    if (((uintptr_t)scratch & 255u) != 0) return fail(EVOX_EALIGN, "scratch is not 256-byte aligned");
+    return sort_batches(seed, t0, n_gens, N, nullptr, perm_out, scratch, scratch_bytes, (hipStream_t)hip_stream);
+}
+
+int evox_argsort_u32(const uint32_t *keys, int64_t N, uint32_t *perm_out, void *scratch, size_t scratch_bytes,
+                     void *hip_stream)
+{
+    if (N < 0 || N > EVOX_ARGSORT_MAX_N)
+        return fail(EVOX_EINVAL, "N = %lld out of range [0, %d]", (long long)N, EVOX_ARGSORT_MAX_N);
+    if (N == 0) return EVOX_OK;
+    if (!keys || !perm_out || !scratch) return fail(EVOX_EINVAL, "keys, perm_out and scratch are required");
+    if (((uintptr_t)keys & 3u) != 0 || ((uintptr_t)perm_out & 3u) != 0)
+        return fail(EVOX_EALIGN, "keys or perm_out is not 4-byte aligned");
+    if (((uintptr_t)scratch & 255u) != 0) return fail(EVOX_EALIGN, "scratch is not 256-byte aligned");
+    return sort_batches(0, 0, 1, N, keys, perm_out, scratch, scratch_bytes, (hipStream_t)hip_stream);
 }
 
 int evox_fill_normal(uint64_t seed, int64_t N, int64_t D, int64_t ldx, float mu, float sigma,

@@ -276,7 +276,8 @@ __device__ __forceinline__ PermSlice perm_slice(const PermArgs &a)
 }
 
 // Keys of the 16 individuals 4 * (blockIdx.x * 1024 + r * 256 + tid) + e,
-// r, e < 4, handled by one thread of a perm block (4096 per block).
+// r, e < 4, handled by one thread of a perm block (4096 per block): words of
+// Philox stream 4, or the caller's keys.
 template <typename F>
 __device__ __forceinline__ void for_block_keys(const PermArgs &a, uint32_t t, F &&f)
 {
@@ -285,8 +286,17 @@ __device__ __forceinline__ void for_block_keys(const PermArgs &a, uint32_t t, F 
     for (int r = 0; r < 4; ++r) {
         const int64_t q = q0 + r * 256 + threadIdx.x;
         if (4 * q < a.N) {
-            const U4 w = philox((uint32_t)q, 0u, t, STREAM_PERM, a.k0, a.k1);
-            const uint32_t k4[4] = {w.x, w.y, w.z, w.w};
+            uint32_t k4[4];
+            if (a.keys) {
+#pragma unroll
+                for (int e = 0; e < 4; ++e) k4[e] = 4 * q + e < a.N ? a.keys[4 * q + e] : 0u;
+            } else {
+                const U4 w = philox((uint32_t)q, 0u, t, STREAM_PERM, a.k0, a.k1);
+                k4[0] = w.x;
+                k4[1] = w.y;
+                k4[2] = w.z;
+                k4[3] = w.w;
+            }
 #pragma unroll
             for (int e = 0; e < 4; ++e)
                 if (4 * q + e < a.N) f(k4[e], 4 * q + e);

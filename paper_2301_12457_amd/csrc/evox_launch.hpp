@@ -96,6 +96,7 @@ struct PermArgs {
     uint32_t t0;        // first generation of the batch
     uint32_t batch;     // generations in the batch
     uint32_t *hist, *offs, *cursor, *tkey, *tidx, *perm;  // [batch][...] slices
+    const uint32_t *keys;  // caller keys (batch 1), or null: Philox stream-4 keys
 };
 hipError_t launch_perm(const PermArgs &a, hipStream_t s);
 hipError_t launch_cso(int fn, Layout L, const CsoArgs &a, int grid, hipStream_t s);

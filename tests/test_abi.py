@@ -92,6 +92,15 @@ def test_default_pitch_policy(evox):
         evox.pitch(0)
 
 
+def test_permutation_scratch(evox):
+    L = evox.lib()
+    assert L.evox_permutation_scratch_bytes(0, 1) == 0
+    assert L.evox_permutation_scratch_bytes(2**24 + 1, 1) == 0
+    assert L.evox_permutation_scratch_bytes(100, 9) == 0
+    one, eight = L.evox_permutation_scratch_bytes(10**6, 1), L.evox_permutation_scratch_bytes(10**6, 8)
+    assert one >= 8 * 10**6 and eight >= 8 * one - 8 * 4096
+
+
 def test_scratch_bytes(evox):
     p = evox.make_params(evox.PSO, evox.SPHERE, 100, 10, -1, 1)
     assert evox.evox_scratch_bytes(p) > 0

@@ -148,3 +148,14 @@ def test_resume_is_bit_exact(ref):
     for name in ("x", "v", "fit"):
         assert np.array_equal(getattr(a, name), getattr(b, name)), name
     assert (a.best_fit, a.best_idx, a.t) == (b.best_fit, b.best_idx, b.t)
+
+
+def test_argsort_is_a_stable_sort(ref):
+    """The sort under the pairing, pinned to numpy's stable argsort, on keys
+    with heavy ties, all-equal keys, extremes and random words."""
+    rng = np.random.default_rng(77)
+    cases = [rng.integers(0, 16, size=5000), np.full(3000, 7), np.array([2**32 - 1, 0, 2**32 - 1, 0, 5]),
+             rng.integers(0, 2**32, size=20000, dtype=np.uint64), np.arange(100)[::-1], np.zeros(0)]
+    for keys in cases:
+        keys = np.asarray(keys, dtype=np.uint32)
+        assert np.array_equal(ref.argsort_u32(keys), np.argsort(keys, kind="stable"))
