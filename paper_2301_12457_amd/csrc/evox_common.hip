@@ -275,15 +275,15 @@ __device__ __forceinline__ PermSlice perm_slice(const PermArgs &a)
                      a.tkey + b * a.N, a.tidx + b * a.N, a.perm + b * a.N};
 }
 
-// Keys of the 16 individuals 4 * (blockIdx.x * 1024 + r * 256 + tid) + e,
-// r, e < 4, handled by one thread of a perm block (4096 per block): words of
-// Philox stream 4, or the caller's keys.
+// Keys of the individuals 4 * (blockIdx.x * kPermChunk / 4 + r * 256 + tid)
+// + e, r < kPermChunk / 1024, e < 4, handled by one thread of a perm block
+// (kPermChunk per block): words of Philox stream 4, or the caller's keys.
 template <typename F>
 __device__ __forceinline__ void for_block_keys(const PermArgs &a, uint32_t t, F &&f)
 {
     const int64_t q0 = (int64_t)blockIdx.x * (kPermChunk / 4);
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
+    for (int r = 0; r < kPermChunk / 1024; ++r) {
         const int64_t q = q0 + r * 256 + threadIdx.x;
         if (4 * q < a.N) {
             uint32_t k4[4];
