@@ -25,7 +25,7 @@ class RefParams(ctypes.Structure):
         ("w", ctypes.c_float), ("c1", ctypes.c_float), ("c2", ctypes.c_float),
         ("phi", ctypes.c_float), ("vmax", ctypes.c_float),
         ("x_init", ctypes.c_int32), ("x_mu", ctypes.c_float), ("x_sigma", ctypes.c_float),
-        ("pad_", ctypes.c_float),
+        ("de_f", ctypes.c_float), ("de_cr", ctypes.c_float), ("pad_", ctypes.c_float),
         ("seed", ctypes.c_uint64),
     ]
 
@@ -62,6 +62,9 @@ def lib():
         L.evox_ref_colmean.argtypes = [P, i64, i64, P]
         L.evox_ref_perm.argtypes = [u64, i64, i64, P]
         L.evox_ref_argsort_u32.argtypes = [P, i64, P]
+        L.evox_ref_de_choices.argtypes = [u64, i64, i64, i64, i64, P]
+        L.evox_ref_de_init.argtypes = [P, P, P]
+        L.evox_ref_de_step.argtypes = [P, i64, i64, P, P, P, P, P]
         L.evox_ref_cso_init.argtypes = [P, P, P, P]
         L.evox_ref_cso_step.argtypes = [P, i64, i64, P, P, P, P, P, P]
         _lib = L
@@ -140,10 +143,10 @@ def init_normal(seed, N, D, mu, sigma):
 
 
 def make_params(fn, N, D, lb, ub, v_lo=0.0, v_hi=0.0, w=0.6, c1=1.5, c2=1.5, phi=0.1,
-                vmax=0.0, clamp_x=0, seed=0, x_init=0, x_mu=0.0, x_sigma=1.0):
+                vmax=0.0, clamp_x=0, seed=0, x_init=0, x_mu=0.0, x_sigma=1.0, de_f=0.5, de_cr=0.9):
     return RefParams(fn=fn, clamp_x=clamp_x, N=N, D=D, lb=lb, ub=ub, v_lo=v_lo, v_hi=v_hi,
                      w=w, c1=c1, c2=c2, phi=phi, vmax=vmax, x_init=x_init, x_mu=x_mu,
-                     x_sigma=x_sigma, pad_=0.0, seed=seed)
+                     x_sigma=x_sigma, de_f=de_f, de_cr=de_cr, pad_=0.0, seed=seed)
 
 
 class PSO:
@@ -232,5 +235,43 @@ class CSO:
                                      ctypes.byref(bi), _ptr(self.loser))
         if rc != 0:
             raise ValueError(f"evox_ref_cso_step rc={rc}")
+        self.best_fit, self.best_idx = bf.value, bi.value
+        self.t += n_gens
+
+
+def de_choices(seed, t, i, N, D):
+    """(r1, r2, r3, j_rand) of target i at generation t."""
+    out = np.zeros(4, np.int64)
+    lib().evox_ref_de_choices(seed, t, i, N, D, _ptr(out))
+    return tuple(int(v) for v in out)
+
+
+class DE:
+    """Oracle DE/rand/1/bin state: x, fit and the generation counter t."""
+
+    def __init__(self, params: RefParams):
+        self.P = params
+        N, D = params.N, params.D
+        self.x = np.zeros((N, D), np.float32)
+        self.fit = np.zeros(N, np.float32)
+        self.accepted = np.zeros(N, np.uint8)
+        self.best_fit = float("nan")
+        self.best_idx = -1
+        self.t = 0
+        rc = lib().evox_ref_de_init(ctypes.byref(self.P), _ptr(self.x), _ptr(self.fit))
+        if rc != 0:
+            raise ValueError(f"evox_ref_de_init rc={rc}")
+        self.best_idx = argmin(self.fit)
+        self.best_fit = float(self.fit[self.best_idx])
+
+    def step(self, n_gens):
+        for a in (self.x, self.fit):
+            assert a.flags.c_contiguous and a.dtype == np.float32
+        bf = ctypes.c_float(0.0)
+        bi = ctypes.c_int64(0)
+        rc = lib().evox_ref_de_step(ctypes.byref(self.P), self.t, n_gens, _ptr(self.x), _ptr(self.fit),
+                                    ctypes.byref(bf), ctypes.byref(bi), _ptr(self.accepted))
+        if rc != 0:
+            raise ValueError(f"evox_ref_de_step rc={rc}")
         self.best_fit, self.best_idx = bf.value, bi.value
         self.t += n_gens

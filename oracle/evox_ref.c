@@ -93,7 +93,7 @@ void evox_ref_u01_array(const uint32_t *w, int64_t n, float *out)
 
 /* Random-stream identifiers (the counter's fourth word). */
 enum { STREAM_INIT_X = 0, STREAM_INIT_V = 1, STREAM_PSO = 2, STREAM_CSO = 3,
-       STREAM_PERM = 4, STREAM_INIT_NORMAL = 5 };
+       STREAM_PERM = 4, STREAM_INIT_NORMAL = 5, STREAM_DE = 6 };
 
 /* Draw k of K for element (i, j) at generation t in stream s:
  * word (j mod 4) of Philox(seed, (K*floor(j/4) + k, i, t, s)). */
@@ -248,6 +248,7 @@ typedef struct {
     float vmax;         /* PSO velocity clamp; <= 0 means none */
     int32_t x_init;     /* 0: x ~ U[lb, ub); 1: x ~ N(x_mu, x_sigma^2) */
     float x_mu, x_sigma;
+    float de_f, de_cr;  /* DE differential weight F and crossover rate CR */
     float pad_;
     uint64_t seed;      /* Philox key */
 } evox_ref_params;
@@ -489,5 +490,107 @@ int evox_ref_cso_step(const evox_ref_params *P, int64_t t0, int64_t n_gens, floa
     free(xbar);
     free(perm);
     free(is_loser);
+    return 0;
+}
+
+/* ------------------------------------------------------------------------ */
+/* DE: DE/rand/1/bin (Storn & Price, J. Global Optim. 11, 1997), the vanilla */
+/* DE of the single-objective experiment (Sec. VII-A-1).                     */
+/* State: x, fit (fitness of x).                                             */
+/* ------------------------------------------------------------------------ */
+
+/* floor(w m / 2^32): a 32-bit word mapped to [0, m). */
+static int64_t below(uint32_t w, int64_t m)
+{
+    return (int64_t)(((uint64_t)w * (uint64_t)m) >> 32);
+}
+
+/* The random choices of target i at generation t: three partners r1, r2,
+ * r3, mutually distinct and distinct from i, and the crossover position
+ * j_rand in [0, D).  Words 0..3 of Philox(seed, (0, i, t, 6)) give a_k in
+ * [0, N - 1 - k) for k = 0, 1, 2 and j_rand in [0, D); r_k is the a_k-th
+ * (from 0) of the indices 0..N-1 not yet taken (i, r_1, ..., r_{k-1}),
+ * found by stepping a_k past the taken ones in increasing order.  Needs
+ * N >= 4.  out = (r1, r2, r3, j_rand). */
+void evox_ref_de_choices(uint64_t seed, int64_t t, int64_t i, int64_t N, int64_t D, int64_t out[4])
+{
+    uint32_t w[4];
+    for (int k = 0; k < 4; ++k)
+        w[k] = evox_ref_philox_word(seed, 0u, (uint32_t)i, (uint32_t)t, STREAM_DE, k);
+    int64_t taken[4] = {i, 0, 0, 0};
+    int n_taken = 1;
+    for (int k = 0; k < 3; ++k) {
+        int64_t r = below(w[k], N - 1 - k);
+        for (int e = 0; e < n_taken; ++e)  /* taken[] is in increasing order */
+            if (r >= taken[e]) ++r;
+        out[k] = r;
+        int pos = n_taken;  /* insert r, keeping taken[] sorted */
+        while (pos > 0 && taken[pos - 1] > r) {
+            taken[pos] = taken[pos - 1];
+            --pos;
+        }
+        taken[pos] = r;
+        ++n_taken;
+    }
+    out[3] = below(w[3], D);
+}
+
+int evox_ref_de_init(const evox_ref_params *P, float *x, float *fit)
+{
+    if (P->N < 4 || P->D < 1 || P->fn < 0 || P->fn >= FN_COUNT) return -1;
+    if (P->x_init == 1)
+        evox_ref_init_normal(P->seed, P->N, P->D, P->x_mu, P->x_sigma, x);
+    else
+        evox_ref_init_uniform(P->seed, STREAM_INIT_X, P->N, P->D, P->lb, P->ub, x);
+    return evox_ref_eval(P->fn, x, P->N, P->D, P->D, fit);
+}
+
+/* n_gens DE generations from generation t0.  For every target i, on the
+ * population of the previous generation: mutant v = x_r1 + F (x_r2 - x_r3)
+ * (fp32: fma(F, x_r2 - x_r3, x_r1)); binomial crossover u_j = v_j when the
+ * crossover draw of element j is <= CR or j = j_rand, else x_ij (the draw of
+ * element j is word j mod 4 of Philox(seed, (1 + floor(j/4), i, t, 6)));
+ * the trial replaces the target when its fitness is strictly lower (so NaN
+ * never replaces).  Afterwards (best_fit, best_idx) is the best of the
+ * population.  accepted (nullable, N bytes) receives 1 for the targets the
+ * last generation replaced. */
+int evox_ref_de_step(const evox_ref_params *P, int64_t t0, int64_t n_gens, float *x, float *fit,
+                     float *best_fit, int64_t *best_idx, uint8_t *accepted)
+{
+    const int64_t N = P->N, D = P->D;
+    if (N < 4 || D < 1 || n_gens < 0 || P->fn < 0 || P->fn >= FN_COUNT) return -1;
+    float *xn = (float *)malloc(sizeof(float) * (size_t)(N * D));
+    float *fn = (float *)malloc(sizeof(float) * (size_t)N);
+    float *u = (float *)malloc(sizeof(float) * (size_t)D);
+    if (!xn || !fn || !u) {
+        free(xn);
+        free(fn);
+        free(u);
+        return -1;
+    }
+    for (int64_t t = t0; t < t0 + n_gens; ++t) {
+        for (int64_t i = 0; i < N; ++i) {
+            int64_t c[4];
+            evox_ref_de_choices(P->seed, t, i, N, D, c);
+            const float *xi = x + i * D, *x1 = x + c[0] * D, *x2 = x + c[1] * D, *x3 = x + c[2] * D;
+            for (int64_t j = 0; j < D; ++j) {
+                const float mutant = fmaf(P->de_f, x2[j] - x3[j], x1[j]);
+                const float cr = draw(P->seed, i, j, 1, 1, t, STREAM_DE);
+                u[j] = (cr <= P->de_cr || j == c[3]) ? mutant : xi[j];
+            }
+            const float fu = (float)evox_ref_eval_row_f64(P->fn, u, D);
+            const int take = fu < fit[i];
+            memcpy(xn + i * D, take ? u : xi, sizeof(float) * (size_t)D);
+            fn[i] = take ? fu : fit[i];
+            if (accepted && t == t0 + n_gens - 1) accepted[i] = (uint8_t)take;
+        }
+        memcpy(x, xn, sizeof(float) * (size_t)(N * D));
+        memcpy(fit, fn, sizeof(float) * (size_t)N);
+    }
+    free(xn);
+    free(fn);
+    free(u);
+    *best_idx = evox_ref_argmin(fit, N);
+    *best_fit = fit[*best_idx];
     return 0;
 }
