@@ -57,6 +57,12 @@ def pso_bytes_per_launch(w, launches, improved_rows):
     return 20.0 * w.N * w.D + 4.0 * w.N + (4.0 * w.D + 4.0) * imp
 
 
+def de_bytes_per_launch(w):
+    # per target element: read the target, gather three partners, write the
+    # next population (20 B); per target: read and write its fitness
+    return 20.0 * w.N * w.D + 8.0 * w.N
+
+
 def cso_bytes_per_launch(w):
     # per pair: read winner row, loser x and v, write loser x and v
     # (20 B per pair element = 10 B per individual element); fitness of both
@@ -107,10 +113,11 @@ def _cpu_baseline(w, budget_s):
         dt = time.perf_counter() - t0
         return {"value": rows * w.D * n / dt, "unit": UNIT, "cores": 1, "kind": "oracle",
                 "sample": f"{rows} of {w.N} rows x D={w.D}, {n} evaluation passes, {dt:.1f} s"}
-    rows = min(w.N, 2000 if w.algo == "pso" else 20_000)
+    rows = min(w.N, 20_000 if w.algo == "cso" else 2000)
     P = oracle.make_params(fn, rows, w.D, w.lb, w.ub, v_lo=w.v_lo, v_hi=w.v_hi, w=w.w, c1=w.c1,
-                           c2=w.c2, phi=w.phi, vmax=w.vmax, seed=w.seed)
-    s = oracle.PSO(P) if w.algo == "pso" else oracle.CSO(P)
+                           c2=w.c2, phi=w.phi, vmax=w.vmax, seed=w.seed, de_f=w.de_f,
+                           de_cr=w.de_cr)
+    s = {"pso": oracle.PSO, "cso": oracle.CSO, "de": oracle.DE}[w.algo](P)
     s.step(1)
     t0 = time.perf_counter()
     gens = 0
@@ -179,10 +186,10 @@ def main():
             evox.evox_eval_argmin(fn, X, w.N, w.D, w.D, out, bf, bi, scratch)
         swarm = None
     else:
-        algo = evox.PSO if w.algo == "pso" else evox.CSO
+        algo = {"pso": evox.PSO, "cso": evox.CSO, "de": evox.DE}[w.algo]
         P = evox.make_params(algo, fn, w.N, w.D, w.lb, w.ub, v_lo=w.v_lo, v_hi=w.v_hi, w=w.w,
                              c1=w.c1, c2=w.c2, phi=w.phi, vmax=w.vmax, seed=w.seed,
-                             ldx=args.ldx or None)
+                             ldx=args.ldx or None, de_f=w.de_f, de_cr=w.de_cr)
         swarm = evox.Swarm(P)
 
         def step():
@@ -216,10 +223,11 @@ def main():
         swarm.profile(False)
         if launches > 0:
             avg_ms = fused_ms / launches
-            bytes_per = (pso_bytes_per_launch(w, launches, improved) if w.algo == "pso"
-                         else cso_bytes_per_launch(w))
+            bytes_per = {"pso": lambda: pso_bytes_per_launch(w, launches, improved),
+                         "cso": lambda: cso_bytes_per_launch(w),
+                         "de": lambda: de_bytes_per_launch(w)}[w.algo]()
             achieved = bytes_per / (avg_ms / 1e3) / 1e9
-            kname = "k_pso_fused" if w.algo == "pso" else "k_cso"
+            kname = {"pso": "k_pso_fused", "cso": "k_cso", "de": "k_de"}[w.algo]
             traffic = traffic_from_profile(w.name)
             roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                         "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),

@@ -63,7 +63,7 @@ enum evox_fn {
     EVOX_SCHWEFEL = 5
 };
 
-enum evox_algo { EVOX_PSO = 0, EVOX_CSO = 1 };
+enum evox_algo { EVOX_PSO = 0, EVOX_CSO = 1, EVOX_DE = 2 };
 
 enum evox_status {
     EVOX_OK = 0,
@@ -78,9 +78,9 @@ enum evox_status {
 
 /* Immutable hyperparameters (theta of Sec. IV-B), fixed at creation. */
 typedef struct evox_params {
-    int32_t algo;     /* EVOX_PSO or EVOX_CSO */
+    int32_t algo;     /* EVOX_PSO, EVOX_CSO or EVOX_DE */
     int32_t fn_id;    /* enum evox_fn */
-    int64_t N;        /* population size: PSO 1 .. 2^31 - 1, CSO 2 .. 2^24 */
+    int64_t N;        /* population size: PSO 1 .. 2^31 - 1, CSO 2 .. 2^24, DE 4 .. 2^31 - 1 */
     int64_t D;        /* dimension, 1 .. EVOX_MAX_D */
     int64_t ldx;      /* row pitch of x, v, pbest in floats: ldx >= D, ldx % 4 == 0 */
     float lb, ub;     /* x_init 0: initial positions ~ U[lb, ub): x = fma(u, ub - lb, lb);
@@ -93,6 +93,8 @@ typedef struct evox_params {
     int32_t x_init;   /* 0: uniform in [lb, ub); 1: normal, as evox_fill_normal(seed, x_mu,
                          x_sigma) */
     float x_mu, x_sigma;
+    float de_f;       /* DE differential weight F */
+    float de_cr;      /* DE crossover rate CR */
     uint64_t seed;    /* Philox key */
 } evox_params;
 
@@ -102,6 +104,8 @@ typedef struct evox_params {
  *        fitness of the last evaluated positions); xbar unused.
  *   CSO: x, v [N][ldx]; fit [N]; xbar [ldx] (swarm mean of x); pbest, pfit,
  *        gbest unused.
+ *   DE:  x [N][ldx]; fit [N] (the fitness of x); v, pbest, pfit, gbest, xbar
+ *        unused (the second population buffer is part of the scratch).
  * Every array pointer must be 16-byte aligned.  scratch must hold
  * evox_scratch_bytes(params) bytes, 256-byte aligned, and must not be used by
  * anything else while the state exists. */
@@ -176,6 +180,25 @@ int evox_pso_step(evox_state *state, int64_t n_gens);
  * then refreshed from the new positions. */
 int evox_cso_step(evox_state *state, int64_t n_gens);
 
+/* n_gens generations of DE/rand/1/bin (Storn & Price, J. Global Optim. 11,
+ * 1997; the vanilla DE of Sec. VII-A-1) on a DE state.  Generation t, for
+ * every target i, on the population of generation t:
+ *   - partners r1, r2, r3, mutually distinct and distinct from i, and a
+ *     crossover position j_rand, from words 0..3 of Philox(seed, (0, i, t,
+ *     6)): a_k = floor(w_k (N - 1 - k) / 2^32) for k = 0, 1, 2, and r_k is
+ *     the a_k-th (from 0) index not yet taken (i, r1, ...); j_rand =
+ *     floor(w_3 D / 2^32);
+ *   - mutant v = fma(de_f, x_r2 - x_r3, x_r1) (fp32);
+ *   - binomial crossover u_j = v_j if u01(word j mod 4 of Philox(seed,
+ *     (1 + floor(j/4), i, t, 6))) <= de_cr or j = j_rand, else x_ij;
+ *   - the trial replaces the target when F(u) < fit_i (strictly: ties and
+ *     NaN keep the target).
+ * All targets of a generation see the same population (the next one is
+ * written to the other buffer); when the call returns, x and fit hold the
+ * population and fitness after n_gens generations, and evox_best reports the
+ * best of them. */
+int evox_de_step(evox_state *state, int64_t n_gens);
+
 /* If the caller has changed x (or fit) of a CSO state, recompute xbar from x
  * and, when refit is nonzero, fit = F(x). */
 int evox_cso_refresh(evox_state *state, int refit);
@@ -240,7 +263,8 @@ int evox_argsort_u32(const uint32_t *keys, int64_t N, uint32_t *perm_out, void *
  * a multiple of 32 floats (rows start on 128-byte cache lines) where that
  * pays, else a multiple of 4.  PSO (rows streamed in order; its kernels also
  * write the padding so that row ends are whole lines): 32-multiples for
- * D >= 512, where the padding is at most ~6 %.  CSO (rows gathered and
+ * D >= 512, where the padding is at most ~6 %; DE, whose target rows are
+ * streamed the same way, likewise.  CSO (rows gathered and
  * written at random; padding never touched): 32-multiples for D >= 64.
  * Returns the pitch, or 0 for an unknown algo or D outside [1, EVOX_MAX_D]. */
 int64_t evox_default_ldx(int32_t algo, int64_t D);

@@ -71,15 +71,17 @@ struct Plan {
     size_t hist = 0, offs = 0, cursor = 0, tkey = 0, tidx = 0, perm = 0, xsum = 0, s1 = 0, ticket = 0;
     int64_t xsum_rows = 0;
     int perm_batch = 0;
+    size_t x2 = 0, fit2 = 0;  // DE: the other population buffer and its fitness
     size_t total = 0;
 };
 
 int make_plan(const evox_params *P, Plan *pl)
 {
     if (!P) return fail(EVOX_EINVAL, "params is null");
-    if (P->algo != EVOX_PSO && P->algo != EVOX_CSO) return fail(EVOX_EINVAL, "unknown algo %d", P->algo);
+    if (P->algo != EVOX_PSO && P->algo != EVOX_CSO && P->algo != EVOX_DE)
+        return fail(EVOX_EINVAL, "unknown algo %d", P->algo);
     if (P->fn_id < 0 || P->fn_id >= FN_COUNT) return fail(EVOX_EINVAL, "unknown fn_id %d", P->fn_id);
-    const int64_t nmin = P->algo == EVOX_CSO ? 2 : 1;
+    const int64_t nmin = P->algo == EVOX_CSO ? 2 : P->algo == EVOX_DE ? 4 : 1;
     if (P->N < nmin || P->N >= ((int64_t)1 << 31))
         return fail(EVOX_EINVAL, "N = %lld out of range [%lld, 2^31)", (long long)P->N, (long long)nmin);
     if (P->D < 1 || P->D > EVOX_MAX_D)
@@ -121,6 +123,10 @@ int make_plan(const evox_params *P, Plan *pl)
         p.s1 = take(sizeof(double) * (size_t)kMeanStages * (size_t)P->ldx);
         p.ticket = take(sizeof(uint32_t) * (size_t)((P->ldx + 63) / 64));
     }
+    if (P->algo == EVOX_DE) {
+        p.x2 = take(sizeof(float) * (size_t)P->N * (size_t)P->ldx);
+        p.fit2 = take(sizeof(float) * (size_t)P->N);
+    }
     p.total = off;
     *pl = p;
     return EVOX_OK;
@@ -140,6 +146,7 @@ struct evox_state {
     uint32_t *hist, *offs, *cursor, *tkey, *tidx, *perm, *ticket;
     int64_t perm_t0;  // first generation of the stored permutation batch (-1: none)
     double *xsum, *s1;
+    float *x2, *fit2;  // DE: the other population buffer
     // profiling of the fused generation kernel
     bool prof;
     std::vector<std::pair<hipEvent_t, hipEvent_t>> ev;
@@ -254,7 +261,9 @@ int evox_state_create(const evox_params *params, const evox_buffers *b, void *hi
     if (rc != EVOX_OK) return rc;
     const evox_params &P = *params;
     if (!b) return fail(EVOX_EINVAL, "buffers is null");
-    if (!b->x || !b->v || !b->scratch) return fail(EVOX_EINVAL, "x, v and scratch are required");
+    if (!b->x || !b->scratch) return fail(EVOX_EINVAL, "x and scratch are required");
+    if (P.algo != EVOX_DE && !b->v) return fail(EVOX_EINVAL, "PSO and CSO need v");
+    if (P.algo == EVOX_DE && !b->fit) return fail(EVOX_EINVAL, "DE needs fit");
     if (P.algo == EVOX_PSO && (!b->pbest || !b->pfit || !b->gbest))
         return fail(EVOX_EINVAL, "PSO needs pbest, pfit and gbest");
     if (P.algo == EVOX_CSO && (!b->fit || !b->xbar)) return fail(EVOX_EINVAL, "CSO needs fit and xbar");
@@ -279,6 +288,11 @@ int evox_state_create(const evox_params *params, const evox_buffers *b, void *hi
     s->xsum = s->s1 = nullptr;
     s->perm_t0 = -1;
     s->ticket = nullptr;
+    s->x2 = s->fit2 = nullptr;
+    if (P.algo == EVOX_DE) {
+        s->x2 = at<float>(b->scratch, pl.x2);
+        s->fit2 = at<float>(b->scratch, pl.fit2);
+    }
     if (P.algo == EVOX_CSO) {
         s->hist = at<uint32_t>(b->scratch, pl.hist);
         s->offs = at<uint32_t>(b->scratch, pl.offs);
@@ -305,7 +319,8 @@ int evox_state_create(const evox_params *params, const evox_buffers *b, void *hi
     }
 
     hipError_t e;
-    InitArgs ia{b->x, b->v, P.algo == EVOX_PSO ? b->pbest : nullptr, P.N, P.D, P.ldx, P.lb, P.ub,
+    InitArgs ia{b->x, P.algo == EVOX_DE ? nullptr : b->v, P.algo == EVOX_PSO ? b->pbest : nullptr, P.N, P.D,
+                P.ldx, P.lb, P.ub,
                 P.v_lo, P.v_hi, P.v_lo == 0.0f && P.v_hi == 0.0f, P.x_init == 1, P.x_mu, P.x_sigma,
                 s->k0, s->k1};
     if ((e = launch_init(ia, s->stream)) != hipSuccess) {
@@ -320,6 +335,17 @@ int evox_state_create(const evox_params *params, const evox_buffers *b, void *hi
         if ((e = best_init(s, std::numeric_limits<float>::infinity(), 0)) != hipSuccess ||
             (e = launch_fill(b->pfit, P.N, std::numeric_limits<float>::infinity(), s->stream)) != hipSuccess ||
             (e = launch_copy_row(b->pbest, b->gbest, P.ldx, s->stream)) != hipSuccess) {
+            delete s;
+            return hip_fail(e, "init");
+        }
+    } else if (P.algo == EVOX_DE) {
+        // the other buffer starts zero, so padding columns the kernels do
+        // not reach stay zero in both; then fit = F(x) and the first best
+        EvalArgs ea{b->x, P.N, P.D, P.ldx, b->fit, s->slots, 4 * P.N * P.ldx > kStreamBytes};
+        if ((e = launch_fill(s->x2, P.N * P.ldx, 0.0f, s->stream)) != hipSuccess ||
+            (e = best_init(s, std::numeric_limits<float>::infinity(), 0)) != hipSuccess ||
+            (e = launch_eval(P.fn_id, pl.L, true, ea, pl.grid, s->stream)) != hipSuccess ||
+            (e = launch_select(s->slots, nullptr, 0, nullptr, s->best, nullptr, nullptr, s->stream)) != hipSuccess) {
             delete s;
             return hip_fail(e, "init");
         }
@@ -472,6 +498,36 @@ int evox_cso_step(evox_state *s, int64_t n_gens)
     return EVOX_OK;
 }
 
+int evox_de_step(evox_state *s, int64_t n_gens)
+{
+    if (!s) return fail(EVOX_EINVAL, "state is null");
+    if (s->P.algo != EVOX_DE) return fail(EVOX_EINVAL, "evox_de_step on a PSO or CSO state");
+    if (n_gens < 0) return fail(EVOX_EINVAL, "n_gens = %lld < 0", (long long)n_gens);
+    if (s->t + n_gens >= ((int64_t)1 << 32)) return fail(EVOX_EINVAL, "generation counter would pass 2^32");
+    if (n_gens == 0) return EVOX_OK;
+    const evox_params &P = s->P;
+    const Plan &pl = s->pl;
+    hipError_t e;
+    for (int64_t k = 0; k < n_gens; ++k) {
+        // generation k reads one buffer and writes the other
+        const bool even = (k & 1) == 0;
+        DeArgs a{even ? s->B.x : s->x2, even ? s->B.fit : s->fit2, even ? s->x2 : s->B.x,
+                 even ? s->fit2 : s->B.fit, P.N, P.D, P.ldx, P.de_f, P.de_cr, s->k0, s->k1,
+                 (uint32_t)(s->t + k), k == n_gens - 1 ? s->slots : nullptr, 20 * P.N * P.D > kStreamBytes};
+        e = timed(s, [&] { return launch_de(P.fn_id, pl.L, a, pl.grid, s->stream); });
+        if (e != hipSuccess) return hip_fail(e, "de generation");
+    }
+    if ((e = launch_select(s->slots, nullptr, 0, nullptr, s->best, nullptr, nullptr, s->stream)) != hipSuccess)
+        return hip_fail(e, "select");
+    if (n_gens & 1) {  // the population ended in the other buffer: bring it home
+        if ((e = launch_stream_copy(s->x2, s->B.x, P.N * P.ldx, s->stream)) != hipSuccess ||
+            (e = launch_stream_copy(s->fit2, s->B.fit, P.N, s->stream)) != hipSuccess)
+            return hip_fail(e, "de copy");
+    }
+    s->t += n_gens;
+    return EVOX_OK;
+}
+
 int evox_cso_refresh(evox_state *s, int refit)
 {
     if (!s) return fail(EVOX_EINVAL, "state is null");
@@ -516,7 +572,7 @@ int64_t evox_default_ldx(int32_t algo, int64_t D)
 {
     if (D < 1 || D > EVOX_MAX_D) return 0;
     const int64_t line = (D + 31) / 32 * 32, quad = (D + 3) / 4 * 4;
-    if (algo == EVOX_PSO) return D >= 512 ? line : quad;
+    if (algo == EVOX_PSO || algo == EVOX_DE) return D >= 512 ? line : quad;
     if (algo == EVOX_CSO) return D >= 64 ? line : quad;
     return 0;
 }

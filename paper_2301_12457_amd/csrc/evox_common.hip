@@ -579,6 +579,12 @@ hipError_t launch_cso(int fn, Layout L, const CsoArgs &a, int grid, hipStream_t 
     EVOX_FN_SWITCH(EVOX_CALL_CSO)
 }
 
+hipError_t launch_de(int fn, Layout L, const DeArgs &a, int grid, hipStream_t s)
+{
+#define EVOX_CALL_DE(F) launch_de_t<F>(L, a, grid, s)
+    EVOX_FN_SWITCH(EVOX_CALL_DE)
+}
+
 int occupancy_cso(int fn, Layout L)
 {
     switch (fn) {

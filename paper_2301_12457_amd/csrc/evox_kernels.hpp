@@ -332,6 +332,115 @@ __global__ __launch_bounds__(block_for(G)) void k_cso(CsoArgs a)
     acc.write(a.D, a.ldx, a.xsum);
 }
 
+// ---------------------------------------------------------------------------
+// DE/rand/1/bin generation (Storn & Price, 1997), one target row per row
+// group: the target's three partners and crossover position from one Philox
+// call (stream 6, counter (0, i, t)); partners mutually distinct and distinct
+// from the target by stepping a draw in [0, N - 1 - k) past the indices
+// already taken, in increasing order (no rejection loop); per float4 chunk
+// the target row (streamed) and the three partner rows (gathered), the
+// crossover draws of Philox (1 + c, i, t, 6), mutant fma(F, x_r2 - x_r3,
+// x_r1), the trial evaluated from registers and kept when strictly better.
+// Every target writes its next row (trial or copy) to the other buffer, so
+// all targets of a generation see the same population.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ int64_t below(uint32_t w, int64_t m)
+{
+    return (int64_t)(((uint64_t)w * (uint64_t)m) >> 32);
+}
+
+template <int FN, int G, int MAXIT>
+__global__ __launch_bounds__(block_for(G)) void k_de(DeArgs a)
+{
+    constexpr int B = block_for(G), RPB = B / G;
+    __shared__ float nbr[(FN == FN_ROSENBROCK && G > 64) ? B * MAXIT : 1];
+    __shared__ float red[2 * (B / 64)];
+    __shared__ uint64_t sk[B / 64];
+    __shared__ uint32_t sc[B / 64];
+
+    const int tid = threadIdx.x, g = tid % G, slot = tid / G;
+    const int64_t C4 = (a.D + 3) >> 2;
+    const int64_t CW = a.ldx / 4 < (int64_t)G * MAXIT ? a.ldx / 4 : (int64_t)G * MAXIT;
+    uint64_t best = kNoKey;
+    uint32_t nacc = 0;
+
+    for (int64_t rb = (int64_t)blockIdx.x * RPB; rb < a.N; rb += (int64_t)gridDim.x * RPB) {
+        const int64_t row = rb + slot;
+        const bool active = row < a.N;
+        int64_t r[3] = {0, 0, 0}, jr = 0;
+        if (active) {
+            const U4 w = philox(0u, (uint32_t)row, a.t, STREAM_DE, a.k0, a.k1);
+            const uint32_t wk[3] = {w.x, w.y, w.z};
+            int64_t taken[3] = {row, 0, 0};
+#pragma unroll
+            for (int k = 0; k < 3; ++k) {
+                int64_t v = below(wk[k], a.N - 1 - k);
+#pragma unroll
+                for (int e = 0; e <= k; ++e)  // taken[0..k] in increasing order
+                    if (v >= taken[e]) ++v;
+                r[k] = v;
+                if (k < 2) {  // insert v into taken[0..k]
+                    int pos = k + 1;
+#pragma unroll
+                    for (int e = k; e >= 0; --e)
+                        if (taken[e] > v) {
+                            taken[e + 1] = taken[e];
+                            pos = e;
+                        }
+                    taken[pos] = v;
+                }
+            }
+            jr = below(w.w, a.D);
+        }
+        float4 xi[MAXIT], ur[MAXIT];
+#pragma unroll
+        for (int it = 0; it < MAXIT; ++it) {
+            const int64_t c = g + (int64_t)G * it;
+            float4 xv = make_float4(0.f, 0.f, 0.f, 0.f), uv = xv;
+            if (active && c < C4) {
+                const int64_t off = 4 * c;
+                xv = ld_row(a.x + row * a.ldx + off, a.nt);
+                const float4 v1 = *reinterpret_cast<const float4 *>(a.x + r[0] * a.ldx + off);
+                const float4 v2 = *reinterpret_cast<const float4 *>(a.x + r[1] * a.ldx + off);
+                const float4 v3 = *reinterpret_cast<const float4 *>(a.x + r[2] * a.ldx + off);
+                const U4 cw = philox((uint32_t)(1 + c), (uint32_t)row, a.t, STREAM_DE, a.k0, a.k1);
+                float uo[4];
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const int64_t j = 4 * c + e;
+                    const float mutant = fmaf(a.F, comp(v2, e) - comp(v3, e), comp(v1, e));
+                    const bool take = wcomp(cw, e) <= a.CR || j == jr;
+                    uo[e] = j < a.D ? (take ? mutant : comp(xv, e)) : 0.0f;
+                }
+                uv = make_float4(uo[0], uo[1], uo[2], uo[3]);
+            }
+            xi[it] = xv;
+            ur[it] = uv;
+        }
+        const float fu = row_fitness<FN, G, MAXIT>(ur, g, a.D, nbr, red);
+        if (active) {
+            const float fi = a.fit[row];
+            const bool acc = fu < fi;
+#pragma unroll
+            for (int it = 0; it < MAXIT; ++it) {
+                const int64_t c = g + (int64_t)G * it;
+                if (c < CW) st_row(a.xn + row * a.ldx + 4 * c, acc ? ur[it] : xi[it], a.nt);
+            }
+            if (g == 0) {
+                const float fn = acc ? fu : fi;
+                a.fitn[row] = fn;
+                const uint64_t k = sel_key(fn, row);
+                best = k < best ? k : best;
+                nacc += acc ? 1u : 0u;
+            }
+        }
+    }
+    if (a.slots) {
+        block_min_key(best, nacc, sk, sc);
+        if (tid == 0) slot_commit(a.slots, best, nacc);
+    }
+}
+
 // Column sums of all rows of x (the swarm mean at creation / refresh).
 template <int G, int MAXIT>
 __global__ __launch_bounds__(block_for(G)) void k_colsum(const float *x, int64_t N, int64_t D,
@@ -376,6 +485,8 @@ __global__ __launch_bounds__(block_for(G)) void k_colsum(const float *x, int64_t
     hipLaunchKernelGGL((k_eval<FN, GG, MM, VECC>), dim3(grid), dim3(block_for(GG)), 0, s, a)
 #define EVOX_LAUNCH_CSO(GG, MM, UNUSED) \
     hipLaunchKernelGGL((k_cso<FN, GG, MM>), dim3(grid), dim3(block_for(GG)), 0, s, a)
+#define EVOX_LAUNCH_DE(GG, MM, UNUSED) \
+    hipLaunchKernelGGL((k_de<FN, GG, MM>), dim3(grid), dim3(block_for(GG)), 0, s, a)
 
 template <int FN>
 hipError_t launch_pso_t(Layout L, int mode, const PsoArgs &a, int grid, hipStream_t s)
@@ -415,6 +526,7 @@ hipError_t launch_eval_t(Layout L, bool vec, const EvalArgs &a, int grid, hipStr
         switch (key) {
             EVOX_FAMILY_CASES(EVOX_LAUNCH_EVAL, LAYOUT_EVAL, true)
             EVOX_FAMILY_CASES(EVOX_LAUNCH_EVAL, LAYOUT_CSO, true)
+            EVOX_FAMILY_CASES(EVOX_LAUNCH_EVAL, LAYOUT_PSO, true)
             EVOX_BIG_CASE(EVOX_LAUNCH_EVAL, true)
             default: return hipErrorInvalidValue;
         }
@@ -435,6 +547,17 @@ hipError_t launch_cso_t(Layout L, const CsoArgs &a, int grid, hipStream_t s)
     switch (L.G * 16 + L.maxit) {
         EVOX_FAMILY_CASES(EVOX_LAUNCH_CSO, LAYOUT_CSO, 0)
         EVOX_BIG_CASE(EVOX_LAUNCH_CSO, 0)
+        default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
+
+template <int FN>
+hipError_t launch_de_t(Layout L, const DeArgs &a, int grid, hipStream_t s)
+{
+    switch (L.G * 16 + L.maxit) {
+        EVOX_FAMILY_CASES(EVOX_LAUNCH_DE, LAYOUT_PSO, 0)
+        EVOX_BIG_CASE(EVOX_LAUNCH_DE, 0)
         default: return hipErrorInvalidValue;
     }
     return hipGetLastError();

@@ -25,6 +25,17 @@ struct PsoArgs {
     bool nt;     // streaming hint on row accesses
 };
 
+struct DeArgs {
+    const float *x, *fit;  // generation t population and fitness
+    float *xn, *fitn;      // generation t + 1
+    int64_t N, D, ldx;
+    float F, CR;
+    uint32_t k0, k1;
+    uint32_t t;
+    SelSlots *slots;       // nullable: no selection in this launch
+    bool nt;               // streaming hint on the target rows
+};
+
 struct EvalArgs {
     const float *X;
     int64_t N, D, ldx;
@@ -63,6 +74,8 @@ hipError_t launch_eval_t(Layout L, bool vec, const EvalArgs &a, int grid, hipStr
 template <int FN>
 hipError_t launch_cso_t(Layout L, const CsoArgs &a, int grid, hipStream_t s);
 template <int FN>
+hipError_t launch_de_t(Layout L, const DeArgs &a, int grid, hipStream_t s);
+template <int FN>
 int occupancy_cso_t(Layout L);  // resident blocks per CU of k_cso
 hipError_t launch_eval(int fn, Layout L, bool vec, const EvalArgs &a, int grid, hipStream_t s);
 // Second pass of the selection: reduce and reset the slots, store the result
@@ -100,6 +113,7 @@ struct PermArgs {
 };
 hipError_t launch_perm(const PermArgs &a, hipStream_t s);
 hipError_t launch_cso(int fn, Layout L, const CsoArgs &a, int grid, hipStream_t s);
+hipError_t launch_de(int fn, Layout L, const DeArgs &a, int grid, hipStream_t s);
 int occupancy_cso(int fn, Layout L);
 hipError_t launch_colsum(Layout L, const float *x, int64_t N, int64_t D, int64_t ldx, double *xsum,
                          int grid, hipStream_t s);

@@ -16,7 +16,7 @@ about a million): synthetic, seeded, no dataset.
 import math
 from dataclasses import dataclass, field
 
-PSO, CSO, EVAL = "pso", "cso", "eval"
+PSO, CSO, DE, EVAL = "pso", "cso", "de", "eval"
 
 
 @dataclass(frozen=True)
@@ -39,6 +39,8 @@ class Workload:
     vmax: float = 0.0
     x_mu: float = 0.0      # evaluation-only input: x ~ N(x_mu, x_sigma^2)
     x_sigma: float = 0.0
+    de_f: float = 0.5      # DE differential weight and crossover rate
+    de_cr: float = 0.9
 
 
 WORKLOADS = {
@@ -50,6 +52,8 @@ WORKLOADS = {
                                       200, 2, lb=-5.12, ub=5.12, vmax=0.2 * 10.24),
     "cso_griewank_1e6x100": Workload("cso_griewank_1e6x100", CSO, "griewank", 1_000_000, 100, 200,
                                      3, lb=-600.0, ub=600.0, phi=0.1),
+    "de_sphere_1e5x1e3": Workload("de_sphere_1e5x1e3", DE, "sphere", 100_000, 1_000, 200, 5,
+                                  lb=-32.0, ub=32.0),
     "eval_rosenbrock_1m_x1e3": Workload("eval_rosenbrock_1m_x1e3", EVAL, "rosenbrock", 1_048_576,
                                         1_000, 1, 4, x_mu=1.0, x_sigma=0.5),
 }

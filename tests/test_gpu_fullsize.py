@@ -19,12 +19,12 @@ pytestmark = pytest.mark.gpu
 
 
 def swarm_pair(evox, ref, w):
-    algo = evox.PSO if w.algo == "pso" else evox.CSO
+    algo = {"pso": evox.PSO, "cso": evox.CSO, "de": evox.DE}[w.algo]
     fn = evox.FN_IDS[w.fn]
     kw = dict(v_lo=w.v_lo, v_hi=w.v_hi, w=w.w, c1=w.c1, c2=w.c2, phi=w.phi, vmax=w.vmax,
-              seed=w.seed)
+              seed=w.seed, de_f=w.de_f, de_cr=w.de_cr)
     g = evox.Swarm(evox.make_params(algo, fn, w.N, w.D, w.lb, w.ub, **kw))
-    Ref = ref.PSO if w.algo == "pso" else ref.CSO
+    Ref = {"pso": ref.PSO, "cso": ref.CSO, "de": ref.DE}[w.algo]
     r = Ref(ref.make_params(fn, w.N, w.D, w.lb, w.ub, **kw))
     return g, r, fn
 
@@ -68,6 +68,19 @@ def test_cso_workload_first_generations(evox_gpu, ref):
         assert index_ok(fn, r.x, r.fit, bi, r.best_idx)
         if not exact_mean:   # a 1-ulp mean difference moves the losers slightly: stop here
             break
+
+
+def test_de_workload_first_generations(evox_gpu, ref):
+    w = WORKLOADS["de_sphere_1e5x1e3"]
+    g, r, fn = swarm_pair(evox_gpu, ref, w)
+    D = w.D
+    assert np.array_equal(g.x[:, :D].cpu().numpy(), r.x)
+    g.step(2)
+    r.step(2)
+    assert np.array_equal(g.x[:, :D].cpu().numpy(), r.x)
+    assert_fitness(fn, r.x, g.fit.cpu().numpy(), r.fit, "de fit")
+    bf, bi = g.best()
+    assert index_ok(fn, r.x, r.fit, bi, r.best_idx) and bi == r.best_idx
 
 
 def test_eval_workload_every_row(evox_gpu, ref):
