@@ -93,7 +93,7 @@ void evox_ref_u01_array(const uint32_t *w, int64_t n, float *out)
 
 /* Random-stream identifiers (the counter's fourth word). */
 enum { STREAM_INIT_X = 0, STREAM_INIT_V = 1, STREAM_PSO = 2, STREAM_CSO = 3,
-       STREAM_PERM = 4, STREAM_INIT_NORMAL = 5, STREAM_DE = 6 };
+       STREAM_PERM = 4, STREAM_INIT_NORMAL = 5, STREAM_DE = 6, STREAM_ES = 7 };
 
 /* Draw k of K for element (i, j) at generation t in stream s:
  * word (j mod 4) of Philox(seed, (K*floor(j/4) + k, i, t, s)). */
@@ -249,6 +249,8 @@ typedef struct {
     int32_t x_init;     /* 0: x ~ U[lb, ub); 1: x ~ N(x_mu, x_sigma^2) */
     float x_mu, x_sigma;
     float de_f, de_cr;  /* DE differential weight F and crossover rate CR */
+    float es_sigma;     /* OpenES perturbation scale */
+    float es_lr;        /* OpenES learning rate */
     float pad_;
     uint64_t seed;      /* Philox key */
 } evox_ref_params;
@@ -269,24 +271,30 @@ void evox_ref_init_uniform(uint64_t seed, int stream, int64_t N, int64_t D, floa
 }
 
 /* Standard normal deviate for element (i, j) of the normal initial
- * population, by the Box-Muller transform (Box & Muller, Ann. Math. Statist.
+ * population (stream 5, generation 0; box_muller also serves other streams
+ * with the generation in the counter's third word), by the Box-Muller transform (Box & Muller, Ann. Math. Statist.
  * 29, 1958): one Philox call per four elements, Philox(seed, (floor(j/4), i,
  * 0, 5)); elements 4c, 4c+1 use words (0, 1) and elements 4c+2, 4c+3 words
  * (2, 3).  Of a word pair (a, b), u1 = ((a >> 8) + 1) 2^-24 lies in (0, 1]
  * (never 0, so the logarithm is finite) and u2 = (b >> 8) 2^-24 in [0, 1);
  * with radius r = sqrt(-2 ln u1) and angle 2 pi u2, the even element of the
  * pair is r cos(angle) and the odd one r sin(angle).  fp64 throughout. */
-double evox_ref_normal01(uint64_t seed, int64_t i, int64_t j)
+static double box_muller(uint64_t seed, int64_t i, int64_t j, int64_t t, int stream)
 {
     const uint32_t c0 = (uint32_t)(j / 4);
     const int q = (int)(j % 4) / 2;
-    const uint32_t a = evox_ref_philox_word(seed, c0, (uint32_t)i, 0u, STREAM_INIT_NORMAL, 2 * q);
-    const uint32_t b = evox_ref_philox_word(seed, c0, (uint32_t)i, 0u, STREAM_INIT_NORMAL, 2 * q + 1);
+    const uint32_t a = evox_ref_philox_word(seed, c0, (uint32_t)i, (uint32_t)t, (uint32_t)stream, 2 * q);
+    const uint32_t b = evox_ref_philox_word(seed, c0, (uint32_t)i, (uint32_t)t, (uint32_t)stream, 2 * q + 1);
     const double u1 = ((double)(a >> 8) + 1.0) * 0x1p-24;
     const double u2 = (double)(b >> 8) * 0x1p-24;
     const double r = sqrt(-2.0 * log(u1));
     const double angle = 2.0 * kPi * u2;
     return (j % 2 == 0) ? r * cos(angle) : r * sin(angle);
+}
+
+double evox_ref_normal01(uint64_t seed, int64_t i, int64_t j)
+{
+    return box_muller(seed, i, j, 0, STREAM_INIT_NORMAL);
 }
 
 /* x_ij = mu + sigma z_ij with z from evox_ref_normal01, rounded once. */
@@ -592,5 +600,91 @@ int evox_ref_de_step(const evox_ref_params *P, int64_t t0, int64_t n_gens, float
     free(u);
     *best_idx = evox_ref_argmin(fit, N);
     *best_fit = fit[*best_idx];
+    return 0;
+}
+
+/* ------------------------------------------------------------------------ */
+/* OpenES (Salimans, Ho, Chen, Sidor, Sutskever, arXiv 1703.03864, 2017; one */
+/* of the ES of Table II): antithetic Gaussian perturbations of a center,   */
+/* centered-rank fitness shaping, one gradient step.                         */
+/* State: theta (the center, fp32 [D]).                                      */
+/* ------------------------------------------------------------------------ */
+
+/* The perturbation eps_kj of antithetic pair k at generation t: the
+ * Box-Muller deviate of Philox(seed, (floor(j/4), k, t, 7)), the word layout
+ * of the normal initial population. */
+double evox_ref_es_eps(uint64_t seed, int64_t t, int64_t k, int64_t j)
+{
+    return box_muller(seed, k, j, t, STREAM_ES);
+}
+
+/* Initial center: theta_j = lb + u (ub - lb), u from row 0 of stream 0. */
+int evox_ref_es_init(const evox_ref_params *P, float *theta)
+{
+    if (P->N < 2 || (P->N & 1) || P->D < 1 || P->fn < 0 || P->fn >= FN_COUNT) return -1;
+    evox_ref_init_uniform(P->seed, STREAM_INIT_X, 1, P->D, P->lb, P->ub, theta);
+    return 0;
+}
+
+/* n_gens OpenES generations from generation t0.  Each: samples x_{2k} =
+ * theta + sigma eps_k and x_{2k+1} = theta - sigma eps_k (fp32:
+ * fma(+-sigma, eps, theta) with eps rounded to fp32), fitness f = F(x);
+ * centered ranks u_i = rank_i / (N - 1) - 1/2, rank_i the position of i in
+ * the order of (f_i, i) (NaN last, the argmin order); the gradient estimate
+ * g_j = sum_k (u_{2k} - u_{2k+1}) eps_kj / (N sigma) in fp64 (a descent
+ * direction for minimization: u grows with f); theta_j <- fma(-lr, g_j,
+ * theta_j) with g_j rounded to fp32.  fit (nullable, N floats) receives the
+ * last generation's fitness, rank (nullable) its ranks; (best_fit,
+ * best_idx) is the best sample of the last generation. */
+int evox_ref_es_step(const evox_ref_params *P, int64_t t0, int64_t n_gens, float *theta,
+                     float *fit_out, int64_t *rank_out, float *best_fit, int64_t *best_idx)
+{
+    const int64_t N = P->N, D = P->D, H = N / 2;
+    if (N < 2 || (N & 1) || D < 1 || n_gens < 0 || P->fn < 0 || P->fn >= FN_COUNT) return -1;
+    float *x = (float *)malloc(sizeof(float) * (size_t)D);
+    float *f = (float *)malloc(sizeof(float) * (size_t)N);
+    int64_t *order = (int64_t *)malloc(sizeof(int64_t) * (size_t)N);
+    int64_t *rank = (int64_t *)malloc(sizeof(int64_t) * (size_t)N);
+    double *g = (double *)malloc(sizeof(double) * (size_t)D);
+    if (!x || !f || !order || !rank || !g) {
+        free(x); free(f); free(order); free(rank); free(g);
+        return -1;
+    }
+    for (int64_t t = t0; t < t0 + n_gens; ++t) {
+        for (int64_t i = 0; i < N; ++i) {
+            const int64_t k = i / 2;
+            const float s = (i & 1) ? -P->es_sigma : P->es_sigma;
+            for (int64_t j = 0; j < D; ++j)
+                x[j] = fmaf(s, (float)evox_ref_es_eps(P->seed, t, k, j), theta[j]);
+            f[i] = (float)evox_ref_eval_row_f64(P->fn, x, D);
+        }
+        /* ranks: sort the indices in the argmin order, by insertion */
+        for (int64_t i = 0; i < N; ++i) {
+            int64_t p = i;
+            while (p > 0 && better(f[i], i, f[order[p - 1]], order[p - 1])) {
+                order[p] = order[p - 1];
+                --p;
+            }
+            order[p] = i;
+        }
+        for (int64_t p = 0; p < N; ++p) rank[order[p]] = p;
+        for (int64_t j = 0; j < D; ++j) g[j] = 0.0;
+        for (int64_t k = 0; k < H; ++k) {
+            const double u0 = (double)rank[2 * k] / (double)(N - 1) - 0.5;
+            const double u1 = (double)rank[2 * k + 1] / (double)(N - 1) - 0.5;
+            for (int64_t j = 0; j < D; ++j) g[j] += (u0 - u1) * evox_ref_es_eps(P->seed, t, k, j);
+        }
+        for (int64_t j = 0; j < D; ++j) {
+            const float gj = (float)(g[j] / ((double)N * (double)P->es_sigma));
+            theta[j] = fmaf(-P->es_lr, gj, theta[j]);
+        }
+        if (t == t0 + n_gens - 1) {
+            if (fit_out) memcpy(fit_out, f, sizeof(float) * (size_t)N);
+            if (rank_out) memcpy(rank_out, rank, sizeof(int64_t) * (size_t)N);
+            *best_idx = order[0];
+            *best_fit = f[order[0]];
+        }
+    }
+    free(x); free(f); free(order); free(rank); free(g);
     return 0;
 }
