@@ -63,7 +63,7 @@ enum evox_fn {
     EVOX_SCHWEFEL = 5
 };
 
-enum evox_algo { EVOX_PSO = 0, EVOX_CSO = 1, EVOX_DE = 2 };
+enum evox_algo { EVOX_PSO = 0, EVOX_CSO = 1, EVOX_DE = 2, EVOX_ES = 3 };
 
 enum evox_status {
     EVOX_OK = 0,
@@ -78,9 +78,10 @@ enum evox_status {
 
 /* Immutable hyperparameters (theta of Sec. IV-B), fixed at creation. */
 typedef struct evox_params {
-    int32_t algo;     /* EVOX_PSO, EVOX_CSO or EVOX_DE */
+    int32_t algo;     /* EVOX_PSO, EVOX_CSO, EVOX_DE or EVOX_ES (OpenES) */
     int32_t fn_id;    /* enum evox_fn */
-    int64_t N;        /* population size: PSO 1 .. 2^31 - 1, CSO 2 .. 2^24, DE 4 .. 2^31 - 1 */
+    int64_t N;        /* population size: PSO 1 .. 2^31 - 1, CSO 2 .. 2^24, DE 4 .. 2^31 - 1,
+                         ES even, 2 .. 16384 (N / 2 antithetic pairs) */
     int64_t D;        /* dimension, 1 .. EVOX_MAX_D */
     int64_t ldx;      /* row pitch of x, v, pbest in floats: ldx >= D, ldx % 4 == 0 */
     float lb, ub;     /* x_init 0: initial positions ~ U[lb, ub): x = fma(u, ub - lb, lb);
@@ -95,6 +96,8 @@ typedef struct evox_params {
     float x_mu, x_sigma;
     float de_f;       /* DE differential weight F */
     float de_cr;      /* DE crossover rate CR */
+    float es_sigma;   /* ES perturbation scale sigma */
+    float es_lr;      /* ES learning rate */
     uint64_t seed;    /* Philox key */
 } evox_params;
 
@@ -106,6 +109,9 @@ typedef struct evox_params {
  *        gbest unused.
  *   DE:  x [N][ldx]; fit [N] (the fitness of x); v, pbest, pfit, gbest, xbar
  *        unused (the second population buffer is part of the scratch).
+ *   ES:  x [ldx] = the center theta (one row; x_init / lb / ub / seed give
+ *        its first value, row 0 of the initial population); fit [N] = the
+ *        fitness of the last generation's samples; the rest unused.
  * Every array pointer must be 16-byte aligned.  scratch must hold
  * evox_scratch_bytes(params) bytes, 256-byte aligned, and must not be used by
  * anything else while the state exists. */
@@ -199,6 +205,22 @@ int evox_cso_step(evox_state *state, int64_t n_gens);
  * best of them. */
 int evox_de_step(evox_state *state, int64_t n_gens);
 
+/* n_gens OpenES generations (Salimans et al., arXiv 1703.03864, 2017; an ES
+ * of Table II) on an ES state.  Generation t:
+ *   - perturbations eps_kj, pair k < N/2, element j: the Box-Muller deviates
+ *     of Philox(seed, (floor(j/4), k, t, 7)) with the word layout of
+ *     evox_fill_normal;
+ *   - samples x_{2k} = fma(sigma, eps_k, theta), x_{2k+1} = fma(-sigma,
+ *     eps_k, theta), fit_i = F(x_i) (the samples exist only in registers);
+ *   - centered ranks u_i = rank_i / (N - 1) - 1/2, rank_i the position of
+ *     sample i in the order of (fit_i, i) (NaN last);
+ *   - g_j = sum_k (u_{2k} - u_{2k+1}) eps_kj / (N sigma) (fp64), the
+ *     perturbations regenerated from Philox;
+ *   - theta_j <- fma(-lr, g_j, theta_j), g_j rounded to fp32.
+ * evox_best reports the best sample of the last generation (fitness, index)
+ * and, as the solution, the current center theta. */
+int evox_es_step(evox_state *state, int64_t n_gens);
+
 /* If the caller has changed x (or fit) of a CSO state, recompute xbar from x
  * and, when refit is nonzero, fit = F(x). */
 int evox_cso_refresh(evox_state *state, int refit);
@@ -264,7 +286,7 @@ int evox_argsort_u32(const uint32_t *keys, int64_t N, uint32_t *perm_out, void *
  * pays, else a multiple of 4.  PSO (rows streamed in order; its kernels also
  * write the padding so that row ends are whole lines): 32-multiples for
  * D >= 512, where the padding is at most ~6 %; DE, whose target rows are
- * streamed the same way, likewise.  CSO (rows gathered and
+ * streamed the same way, and ES likewise.  CSO (rows gathered and
  * written at random; padding never touched): 32-multiples for D >= 64.
  * Returns the pitch, or 0 for an unknown algo or D outside [1, EVOX_MAX_D]. */
 int64_t evox_default_ldx(int32_t algo, int64_t D);

@@ -72,13 +72,14 @@ struct Plan {
     int64_t xsum_rows = 0;
     int perm_batch = 0;
     size_t x2 = 0, fit2 = 0;  // DE: the other population buffer and its fitness
+    size_t esw = 0, espart = 0;  // ES: pair weights, gradient partial sums
     size_t total = 0;
 };
 
 int make_plan(const evox_params *P, Plan *pl)
 {
     if (!P) return fail(EVOX_EINVAL, "params is null");
-    if (P->algo != EVOX_PSO && P->algo != EVOX_CSO && P->algo != EVOX_DE)
+    if (P->algo != EVOX_PSO && P->algo != EVOX_CSO && P->algo != EVOX_DE && P->algo != EVOX_ES)
         return fail(EVOX_EINVAL, "unknown algo %d", P->algo);
     if (P->fn_id < 0 || P->fn_id >= FN_COUNT) return fail(EVOX_EINVAL, "unknown fn_id %d", P->fn_id);
     const int64_t nmin = P->algo == EVOX_CSO ? 2 : P->algo == EVOX_DE ? 4 : 1;
@@ -88,13 +89,15 @@ int make_plan(const evox_params *P, Plan *pl)
         return fail(EVOX_EINVAL, "D = %lld out of range [1, %d]", (long long)P->D, EVOX_MAX_D);
     if (P->algo == EVOX_CSO && P->N > kCsoMaxN)
         return fail(EVOX_EINVAL, "CSO N = %lld above %lld", (long long)P->N, (long long)kCsoMaxN);
+    if (P->algo == EVOX_ES && (P->N < 2 || (P->N & 1) || P->N > kEsMaxN))
+        return fail(EVOX_EINVAL, "ES N = %lld must be even, in [2, %d]", (long long)P->N, kEsMaxN);
     if (P->ldx < P->D || (P->ldx & 3))
         return fail(EVOX_EINVAL, "ldx = %lld must be >= D and a multiple of 4", (long long)P->ldx);
     if (P->x_init != 0 && P->x_init != 1) return fail(EVOX_EINVAL, "unknown x_init %d", P->x_init);
     Plan p;
     const int family = P->algo == EVOX_CSO ? LAYOUT_CSO : LAYOUT_PSO;
     if (!row_layout(P->D, family, &p.L)) return fail(EVOX_EINVAL, "no row layout for D = %lld", (long long)P->D);
-    p.grid = grid_for(P->N, p.L.G, kMaxGrid);
+    p.grid = grid_for(P->algo == EVOX_ES ? P->N / 2 : P->N, p.L.G, kMaxGrid);
     size_t off = 0;
     auto take = [&](size_t bytes) {
         const size_t at = off;
@@ -127,6 +130,11 @@ int make_plan(const evox_params *P, Plan *pl)
         p.x2 = take(sizeof(float) * (size_t)P->N * (size_t)P->ldx);
         p.fit2 = take(sizeof(float) * (size_t)P->N);
     }
+    if (P->algo == EVOX_ES) {
+        const size_t H = (size_t)P->N / 2, chunks = (H + kEsPairChunk - 1) / kEsPairChunk;
+        p.esw = take(sizeof(double) * H);
+        p.espart = take(sizeof(double) * chunks * 4 * (size_t)((P->D + 3) / 4));
+    }
     p.total = off;
     *pl = p;
     return EVOX_OK;
@@ -147,6 +155,7 @@ struct evox_state {
     int64_t perm_t0;  // first generation of the stored permutation batch (-1: none)
     double *xsum, *s1;
     float *x2, *fit2;  // DE: the other population buffer
+    double *esw, *espart;  // ES: pair weights, gradient partial sums
     // profiling of the fused generation kernel
     bool prof;
     std::vector<std::pair<hipEvent_t, hipEvent_t>> ev;
@@ -262,8 +271,8 @@ int evox_state_create(const evox_params *params, const evox_buffers *b, void *hi
     const evox_params &P = *params;
     if (!b) return fail(EVOX_EINVAL, "buffers is null");
     if (!b->x || !b->scratch) return fail(EVOX_EINVAL, "x and scratch are required");
-    if (P.algo != EVOX_DE && !b->v) return fail(EVOX_EINVAL, "PSO and CSO need v");
-    if (P.algo == EVOX_DE && !b->fit) return fail(EVOX_EINVAL, "DE needs fit");
+    if ((P.algo == EVOX_PSO || P.algo == EVOX_CSO) && !b->v) return fail(EVOX_EINVAL, "PSO and CSO need v");
+    if ((P.algo == EVOX_DE || P.algo == EVOX_ES) && !b->fit) return fail(EVOX_EINVAL, "DE and ES need fit");
     if (P.algo == EVOX_PSO && (!b->pbest || !b->pfit || !b->gbest))
         return fail(EVOX_EINVAL, "PSO needs pbest, pfit and gbest");
     if (P.algo == EVOX_CSO && (!b->fit || !b->xbar)) return fail(EVOX_EINVAL, "CSO needs fit and xbar");
@@ -289,6 +298,11 @@ int evox_state_create(const evox_params *params, const evox_buffers *b, void *hi
     s->perm_t0 = -1;
     s->ticket = nullptr;
     s->x2 = s->fit2 = nullptr;
+    s->esw = s->espart = nullptr;
+    if (P.algo == EVOX_ES) {
+        s->esw = at<double>(b->scratch, pl.esw);
+        s->espart = at<double>(b->scratch, pl.espart);
+    }
     if (P.algo == EVOX_DE) {
         s->x2 = at<float>(b->scratch, pl.x2);
         s->fit2 = at<float>(b->scratch, pl.fit2);
@@ -319,8 +333,10 @@ int evox_state_create(const evox_params *params, const evox_buffers *b, void *hi
     }
 
     hipError_t e;
-    InitArgs ia{b->x, P.algo == EVOX_DE ? nullptr : b->v, P.algo == EVOX_PSO ? b->pbest : nullptr, P.N, P.D,
-                P.ldx, P.lb, P.ub,
+    // ES: x is the center theta, one row
+    const bool own_v = P.algo == EVOX_PSO || P.algo == EVOX_CSO;
+    InitArgs ia{b->x, own_v ? b->v : nullptr, P.algo == EVOX_PSO ? b->pbest : nullptr,
+                P.algo == EVOX_ES ? 1 : P.N, P.D, P.ldx, P.lb, P.ub,
                 P.v_lo, P.v_hi, P.v_lo == 0.0f && P.v_hi == 0.0f, P.x_init == 1, P.x_mu, P.x_sigma,
                 s->k0, s->k1};
     if ((e = launch_init(ia, s->stream)) != hipSuccess) {
@@ -335,6 +351,11 @@ int evox_state_create(const evox_params *params, const evox_buffers *b, void *hi
         if ((e = best_init(s, std::numeric_limits<float>::infinity(), 0)) != hipSuccess ||
             (e = launch_fill(b->pfit, P.N, std::numeric_limits<float>::infinity(), s->stream)) != hipSuccess ||
             (e = launch_copy_row(b->pbest, b->gbest, P.ldx, s->stream)) != hipSuccess) {
+            delete s;
+            return hip_fail(e, "init");
+        }
+    } else if (P.algo == EVOX_ES) {
+        if ((e = best_init(s, std::numeric_limits<float>::infinity(), 0)) != hipSuccess) {
             delete s;
             return hip_fail(e, "init");
         }
@@ -528,6 +549,32 @@ int evox_de_step(evox_state *s, int64_t n_gens)
     return EVOX_OK;
 }
 
+int evox_es_step(evox_state *s, int64_t n_gens)
+{
+    if (!s) return fail(EVOX_EINVAL, "state is null");
+    if (s->P.algo != EVOX_ES) return fail(EVOX_EINVAL, "evox_es_step on a state of another algorithm");
+    if (n_gens < 0) return fail(EVOX_EINVAL, "n_gens = %lld < 0", (long long)n_gens);
+    if (s->t + n_gens >= ((int64_t)1 << 32)) return fail(EVOX_EINVAL, "generation counter would pass 2^32");
+    if (n_gens == 0) return EVOX_OK;
+    const evox_params &P = s->P;
+    const Plan &pl = s->pl;
+    hipError_t e;
+    for (int64_t k = 0; k < n_gens; ++k) {
+        const uint32_t t = (uint32_t)(s->t + k);
+        EsArgs a{s->B.x, s->B.fit, P.N, P.D, P.es_sigma, s->k0, s->k1, t, k == n_gens - 1 ? s->slots : nullptr};
+        e = timed(s, [&] { return launch_es_eval(P.fn_id, pl.L, a, pl.grid, s->stream); });
+        if (e != hipSuccess) return hip_fail(e, "es samples");
+        if ((e = launch_es_rank(s->B.fit, P.N, P.es_sigma, s->esw, s->stream)) != hipSuccess)
+            return hip_fail(e, "es ranks");
+        EsGradArgs ga{s->esw, s->espart, s->B.x, P.N / 2, P.D, P.es_lr, s->k0, s->k1, t};
+        if ((e = launch_es_grad(ga, s->stream)) != hipSuccess) return hip_fail(e, "es gradient");
+    }
+    if ((e = launch_select(s->slots, nullptr, 0, nullptr, s->best, nullptr, nullptr, s->stream)) != hipSuccess)
+        return hip_fail(e, "select");
+    s->t += n_gens;
+    return EVOX_OK;
+}
+
 int evox_cso_refresh(evox_state *s, int refit)
 {
     if (!s) return fail(EVOX_EINVAL, "state is null");
@@ -545,7 +592,9 @@ int evox_best(evox_state *s, float *best_fit, int64_t *best_idx, float *best_x_h
     if (best_fit) *best_fit = h.f;
     if (best_idx) *best_idx = h.i;
     if (best_x_host) {
-        const float *src = s->P.algo == EVOX_PSO ? s->B.gbest : s->B.x + h.i * s->P.ldx;
+        const float *src = s->P.algo == EVOX_PSO ? s->B.gbest
+                           : s->P.algo == EVOX_ES ? s->B.x
+                                                  : s->B.x + h.i * s->P.ldx;
         e = hipMemcpyAsync(best_x_host, src, sizeof(float) * (size_t)s->P.D, hipMemcpyDeviceToHost, s->stream);
         if (e == hipSuccess) e = hipStreamSynchronize(s->stream);
         if (e != hipSuccess) return hip_fail(e, "read best row");
@@ -572,7 +621,7 @@ int64_t evox_default_ldx(int32_t algo, int64_t D)
 {
     if (D < 1 || D > EVOX_MAX_D) return 0;
     const int64_t line = (D + 31) / 32 * 32, quad = (D + 3) / 4 * 4;
-    if (algo == EVOX_PSO || algo == EVOX_DE) return D >= 512 ? line : quad;
+    if (algo == EVOX_PSO || algo == EVOX_DE || algo == EVOX_ES) return D >= 512 ? line : quad;
     if (algo == EVOX_CSO) return D >= 64 ? line : quad;
     return 0;
 }

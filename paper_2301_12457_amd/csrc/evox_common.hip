@@ -35,7 +35,7 @@ __global__ __launch_bounds__(256) void k_init(InitArgs a)
         float xo[4] = {0.f, 0.f, 0.f, 0.f}, vo[4] = {0.f, 0.f, 0.f, 0.f};
         if (c < C4) {
             if (a.x_normal) {
-                const float4 z = normal4((uint32_t)c, (uint32_t)row, a.k0, a.k1);
+                const float4 z = normal4((uint32_t)c, (uint32_t)row, 0u, STREAM_INIT_NORMAL, a.k0, a.k1);
 #pragma unroll
                 for (int e = 0; e < 4; ++e)
                     if (4 * c + e < a.D) xo[e] = fmaf(a.sigma, comp(z, e), a.mu);
@@ -583,6 +583,111 @@ hipError_t launch_de(int fn, Layout L, const DeArgs &a, int grid, hipStream_t s)
 {
 #define EVOX_CALL_DE(F) launch_de_t<F>(L, a, grid, s)
     EVOX_FN_SWITCH(EVOX_CALL_DE)
+}
+
+hipError_t launch_es_eval(int fn, Layout L, const EsArgs &a, int grid, hipStream_t s)
+{
+#define EVOX_CALL_ES(F) launch_es_eval_t<F>(L, a, grid, s)
+    EVOX_FN_SWITCH(EVOX_CALL_ES)
+}
+
+// ---------------------------------------------------------------------------
+// OpenES centered ranks: one block of 1024 sorts the N (<= kEsMaxN) keys
+// (orderable fitness, index) -- the argmin order -- with a bitonic network in
+// LDS, so key position p is sample i's rank; then each pair's weight
+// w_k = (rank_{2k} - rank_{2k+1}) / (N - 1) / (N sigma) (the difference of
+// the centered ranks rank / (N - 1) - 1/2, scaled by the estimate's 1 / (N
+// sigma)).
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(1024) void k_es_rank(const float *fit, int64_t N, float sigma, double *w)
+{
+    __shared__ uint64_t key[kEsMaxN];
+    uint32_t *rank_of = reinterpret_cast<uint32_t *>(key);  // reused once the order is known
+    int n2 = 1;
+    while (n2 < N) n2 <<= 1;
+    for (int i = threadIdx.x; i < n2; i += 1024) key[i] = i < N ? sel_key(fit[i], i) : kNoKey;
+    __syncthreads();
+    for (int size = 2; size <= n2; size <<= 1)
+        for (int stride = size >> 1; stride > 0; stride >>= 1) {
+            for (int q = threadIdx.x; q < n2 / 2; q += 1024) {
+                const int lo = 2 * q - (q & (stride - 1)), hi = lo + stride;
+                const bool up = (lo & size) == 0;
+                const uint64_t a = key[lo], b = key[hi];
+                if ((a > b) == up) {
+                    key[lo] = b;
+                    key[hi] = a;
+                }
+            }
+            __syncthreads();
+        }
+    constexpr int kPer = kEsMaxN / 1024;
+    uint32_t who[kPer];
+#pragma unroll
+    for (int r = 0; r < kPer; ++r) {
+        const int p = threadIdx.x + 1024 * r;
+        who[r] = p < N ? (uint32_t)key_index(key[p]) : 0u;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int r = 0; r < kPer; ++r) {
+        const int p = threadIdx.x + 1024 * r;
+        if (p < N) rank_of[who[r]] = (uint32_t)p;
+    }
+    __syncthreads();
+    const double scale = 1.0 / ((double)(N - 1) * (double)N * (double)sigma);
+    for (int k = threadIdx.x; k < N / 2; k += 1024)
+        w[k] = ((double)rank_of[2 * k] - (double)rank_of[2 * k + 1]) * scale;
+}
+
+hipError_t launch_es_rank(const float *fit, int64_t N, float sigma, double *w, hipStream_t s)
+{
+    hipLaunchKernelGGL(k_es_rank, dim3(1), dim3(1024), 0, s, fit, N, sigma, w);
+    return hipGetLastError();
+}
+
+// OpenES gradient, pass 1: thread (pair chunk b, column chunk c) sums
+// w_k eps_k over its kEsPairChunk pairs for four columns in fp64, the
+// perturbations regenerated from Philox exactly as the samples drew them.
+__global__ __launch_bounds__(256) void k_es_grad(EsGradArgs a)
+{
+    const int64_t C4 = (a.D + 3) / 4;
+    const int64_t c = (int64_t)blockIdx.x * 256 + threadIdx.x, b = blockIdx.y;
+    if (c >= C4) return;
+    const int64_t k0 = b * kEsPairChunk, k1 = k0 + kEsPairChunk < a.H ? k0 + kEsPairChunk : a.H;
+    double s0 = 0.0, s1 = 0.0, s2 = 0.0, s3 = 0.0;
+    for (int64_t k = k0; k < k1; ++k) {
+        const float4 z = normal4((uint32_t)c, (uint32_t)k, a.t, STREAM_ES, a.k0, a.k1);
+        const double wk = a.w[k];
+        s0 = fma(wk, (double)z.x, s0);
+        s1 = fma(wk, (double)z.y, s1);
+        s2 = fma(wk, (double)z.z, s2);
+        s3 = fma(wk, (double)z.w, s3);
+    }
+    double *dst = a.part + b * 4 * C4 + 4 * c;
+    dst[0] = s0;
+    dst[1] = s1;
+    dst[2] = s2;
+    dst[3] = s3;
+}
+
+// Pass 2: per column, the chunks' partial sums in chunk order, then the step
+// theta_j <- fma(-lr, g_j, theta_j) with g_j rounded to fp32 once.
+__global__ __launch_bounds__(256) void k_es_update(EsGradArgs a, int64_t chunks)
+{
+    const int64_t C4 = (a.D + 3) / 4;
+    const int64_t j = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (j >= a.D) return;
+    double g = 0.0;
+    for (int64_t b = 0; b < chunks; ++b) g += a.part[b * 4 * C4 + j];
+    a.theta[j] = fmaf(-a.lr, (float)g, a.theta[j]);
+}
+
+hipError_t launch_es_grad(const EsGradArgs &a, hipStream_t s)
+{
+    const int64_t C4 = (a.D + 3) / 4, chunks = (a.H + kEsPairChunk - 1) / kEsPairChunk;
+    hipLaunchKernelGGL(k_es_grad, dim3((unsigned)((C4 + 255) / 256), (unsigned)chunks), dim3(256), 0, s, a);
+    hipLaunchKernelGGL(k_es_update, dim3((unsigned)((a.D + 255) / 256)), dim3(256), 0, s, a, chunks);
+    return hipGetLastError();
 }
 
 int occupancy_cso(int fn, Layout L)

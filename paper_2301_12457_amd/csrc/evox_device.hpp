@@ -23,7 +23,7 @@ enum { FN_SPHERE = 0, FN_ACKLEY, FN_RASTRIGIN, FN_GRIEWANK, FN_ROSENBROCK, FN_SC
 
 // Random-stream ids (fourth Philox counter word).
 enum { STREAM_INIT_X = 0, STREAM_INIT_V = 1, STREAM_PSO = 2, STREAM_CSO = 3, STREAM_PERM = 4,
-       STREAM_INIT_NORMAL = 5, STREAM_DE = 6 };
+       STREAM_INIT_NORMAL = 5, STREAM_DE = 6, STREAM_ES = 7 };
 
 constexpr int kBlock = 256;              // threads per block when a row takes <= 256 lanes
 constexpr int kGridCap = 2048;           // blocks of the grid-stride kernels (8 per CU on 256 CUs)
@@ -155,13 +155,16 @@ __device__ __forceinline__ float sin_rev(float r)
     return __builtin_amdgcn_sinf(r - __builtin_rintf(r));
 }
 
-// Four standard normal deviates of float4 chunk c of row `row` (stream 5):
-// the Box-Muller transform of the word pairs (0, 1) and (2, 3) of one Philox
-// call, u1 = ((a >> 8) + 1) 2^-24 in (0, 1], u2 = (b >> 8) 2^-24; the even
-// element gets r cos(2 pi u2), the odd one r sin(2 pi u2), r = sqrt(-2 ln u1).
-__device__ __forceinline__ float4 normal4(uint32_t c, uint32_t row, uint32_t k0, uint32_t k1)
+// Four standard normal deviates of float4 chunk c of row `row` at generation
+// t of a stream: the Box-Muller transform of the word pairs (0, 1) and (2, 3)
+// of one Philox call, u1 = ((a >> 8) + 1) 2^-24 in (0, 1], u2 = (b >> 8)
+// 2^-24; the even element gets r cos(2 pi u2), the odd one r sin(2 pi u2),
+// r = sqrt(-2 ln u1).  Stream 5 at generation 0 is the normal initial
+// population, stream 7 the ES perturbations.
+__device__ __forceinline__ float4 normal4(uint32_t c, uint32_t row, uint32_t t, uint32_t stream, uint32_t k0,
+                                          uint32_t k1)
 {
-    const U4 w = philox(c, row, 0u, STREAM_INIT_NORMAL, k0, k1);
+    const U4 w = philox(c, row, t, stream, k0, k1);
     const float r0 = __builtin_sqrtf(-2.0f * logf((float)((w.x >> 8) + 1u) * 0x1p-24f));
     const float r1 = __builtin_sqrtf(-2.0f * logf((float)((w.z >> 8) + 1u) * 0x1p-24f));
     const float a0 = u01(w.y), a1 = u01(w.w);

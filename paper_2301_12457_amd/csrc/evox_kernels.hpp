@@ -441,6 +441,63 @@ __global__ __launch_bounds__(block_for(G)) void k_de(DeArgs a)
     }
 }
 
+// ---------------------------------------------------------------------------
+// OpenES samples and fitness: one row group per antithetic pair k; the
+// perturbation chunk eps_k (Philox stream 7, generation t, Box-Muller) and
+// both samples fma(+-sigma, eps, theta) live in registers only, and both rows
+// are reduced to their fitness.  theta (D floats) is read by every pair from
+// the caches.
+// ---------------------------------------------------------------------------
+template <int FN, int G, int MAXIT>
+__global__ __launch_bounds__(block_for(G)) void k_es_eval(EsArgs a)
+{
+    constexpr int B = block_for(G), RPB = B / G;
+    __shared__ float nbr[(FN == FN_ROSENBROCK && G > 64) ? B * MAXIT : 1];
+    __shared__ float red[2 * (B / 64)];
+    __shared__ uint64_t sk[B / 64];
+    __shared__ uint32_t sc[B / 64];
+
+    const int tid = threadIdx.x, g = tid % G, slot = tid / G;
+    const int64_t C4 = (a.D + 3) >> 2, H = a.N / 2;
+    uint64_t best = kNoKey;
+    for (int64_t kb = (int64_t)blockIdx.x * RPB; kb < H; kb += (int64_t)gridDim.x * RPB) {
+        const int64_t k = kb + slot;
+        const bool active = k < H;
+        float4 xp[MAXIT], xm[MAXIT];
+#pragma unroll
+        for (int it = 0; it < MAXIT; ++it) {
+            const int64_t c = g + (int64_t)G * it;
+            float po[4] = {0.f, 0.f, 0.f, 0.f}, mo[4] = {0.f, 0.f, 0.f, 0.f};
+            if (active && c < C4) {
+                const float4 th = *reinterpret_cast<const float4 *>(a.theta + 4 * c);
+                const float4 z = normal4((uint32_t)c, (uint32_t)k, a.t, STREAM_ES, a.k0, a.k1);
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    if (4 * c + e < a.D) {
+                        po[e] = fmaf(a.sigma, comp(z, e), comp(th, e));
+                        mo[e] = fmaf(-a.sigma, comp(z, e), comp(th, e));
+                    }
+            }
+            xp[it] = make_float4(po[0], po[1], po[2], po[3]);
+            xm[it] = make_float4(mo[0], mo[1], mo[2], mo[3]);
+        }
+        const float fp = row_fitness<FN, G, MAXIT>(xp, g, a.D, nbr, red);
+        const float fm = row_fitness<FN, G, MAXIT>(xm, g, a.D, nbr, red);
+        if (active && g == 0) {
+            a.fit[2 * k] = fp;
+            a.fit[2 * k + 1] = fm;
+            const uint64_t kp = sel_key(fp, 2 * k), km = sel_key(fm, 2 * k + 1);
+            best = kp < best ? kp : best;
+            best = km < best ? km : best;
+        }
+    }
+    if (a.slots) {
+        uint32_t none = 0;
+        block_min_key(best, none, sk, sc);
+        if (tid == 0) slot_commit(a.slots, best, 0);
+    }
+}
+
 // Column sums of all rows of x (the swarm mean at creation / refresh).
 template <int G, int MAXIT>
 __global__ __launch_bounds__(block_for(G)) void k_colsum(const float *x, int64_t N, int64_t D,
@@ -487,6 +544,8 @@ __global__ __launch_bounds__(block_for(G)) void k_colsum(const float *x, int64_t
     hipLaunchKernelGGL((k_cso<FN, GG, MM>), dim3(grid), dim3(block_for(GG)), 0, s, a)
 #define EVOX_LAUNCH_DE(GG, MM, UNUSED) \
     hipLaunchKernelGGL((k_de<FN, GG, MM>), dim3(grid), dim3(block_for(GG)), 0, s, a)
+#define EVOX_LAUNCH_ES(GG, MM, UNUSED) \
+    hipLaunchKernelGGL((k_es_eval<FN, GG, MM>), dim3(grid), dim3(block_for(GG)), 0, s, a)
 
 template <int FN>
 hipError_t launch_pso_t(Layout L, int mode, const PsoArgs &a, int grid, hipStream_t s)
@@ -558,6 +617,17 @@ hipError_t launch_de_t(Layout L, const DeArgs &a, int grid, hipStream_t s)
     switch (L.G * 16 + L.maxit) {
         EVOX_FAMILY_CASES(EVOX_LAUNCH_DE, LAYOUT_PSO, 0)
         EVOX_BIG_CASE(EVOX_LAUNCH_DE, 0)
+        default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
+
+template <int FN>
+hipError_t launch_es_eval_t(Layout L, const EsArgs &a, int grid, hipStream_t s)
+{
+    switch (L.G * 16 + L.maxit) {
+        EVOX_FAMILY_CASES(EVOX_LAUNCH_ES, LAYOUT_PSO, 0)
+        EVOX_BIG_CASE(EVOX_LAUNCH_ES, 0)
         default: return hipErrorInvalidValue;
     }
     return hipGetLastError();

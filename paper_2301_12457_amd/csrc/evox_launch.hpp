@@ -36,6 +36,29 @@ struct DeArgs {
     bool nt;               // streaming hint on the target rows
 };
 
+// OpenES.  k_es_eval: both samples theta +- sigma eps_k of each antithetic
+// pair from registers; k_es_rank: centered ranks in LDS (N <= kEsMaxN) and
+// the pair weights; k_es_grad / k_es_update: the gradient estimate with the
+// perturbations regenerated from Philox (never stored) and the step.
+constexpr int kEsMaxN = 16384;
+constexpr int kEsPairChunk = 64;  // pairs per thread of the gradient pass
+struct EsArgs {
+    const float *theta;
+    float *fit;            // [N] sample fitness
+    int64_t N, D;
+    float sigma;
+    uint32_t k0, k1, t;
+    SelSlots *slots;       // nullable
+};
+struct EsGradArgs {
+    const double *w;       // [N/2] pair weights (u_{2k} - u_{2k+1}) / (N sigma)
+    double *part;          // [ceil(H / kEsPairChunk)][4 * ceil(D / 4)] partial sums
+    float *theta;
+    int64_t H, D;
+    float lr;
+    uint32_t k0, k1, t;
+};
+
 struct EvalArgs {
     const float *X;
     int64_t N, D, ldx;
@@ -76,6 +99,8 @@ hipError_t launch_cso_t(Layout L, const CsoArgs &a, int grid, hipStream_t s);
 template <int FN>
 hipError_t launch_de_t(Layout L, const DeArgs &a, int grid, hipStream_t s);
 template <int FN>
+hipError_t launch_es_eval_t(Layout L, const EsArgs &a, int grid, hipStream_t s);
+template <int FN>
 int occupancy_cso_t(Layout L);  // resident blocks per CU of k_cso
 hipError_t launch_eval(int fn, Layout L, bool vec, const EvalArgs &a, int grid, hipStream_t s);
 // Second pass of the selection: reduce and reset the slots, store the result
@@ -114,6 +139,9 @@ struct PermArgs {
 hipError_t launch_perm(const PermArgs &a, hipStream_t s);
 hipError_t launch_cso(int fn, Layout L, const CsoArgs &a, int grid, hipStream_t s);
 hipError_t launch_de(int fn, Layout L, const DeArgs &a, int grid, hipStream_t s);
+hipError_t launch_es_eval(int fn, Layout L, const EsArgs &a, int grid, hipStream_t s);
+hipError_t launch_es_rank(const float *fit, int64_t N, float sigma, double *w, hipStream_t s);
+hipError_t launch_es_grad(const EsGradArgs &a, hipStream_t s);
 int occupancy_cso(int fn, Layout L);
 hipError_t launch_colsum(Layout L, const float *x, int64_t N, int64_t D, int64_t ldx, double *xsum,
                          int grid, hipStream_t s);
