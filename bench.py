@@ -63,6 +63,16 @@ def de_bytes_per_launch(w):
     return 20.0 * w.N * w.D + 8.0 * w.N
 
 
+# OpenES is bound by vector-ALU work (the perturbations are regenerated, not
+# stored): lane-ops per perturbation element and generation, counted from
+# the computation as written -- Philox4x32-10 is 10 rounds of two 32x32->64
+# products (4 ops) and 4 xors per 4 elements (20), Box-Muller 16 ops per 2
+# elements (8), the two samples and their Sphere terms (4); the gradient
+# pass regenerates the perturbation (28) and adds its weighted value (1).
+ES_OPS_PER_ELEMENT = 20 + 8 + 4 + 28 + 1
+ALU_PEAK_TOPS = 256 * 64 * 2.4e9 / 1e12   # 256 CUs x 64 lanes x 2.4 GHz, 32-bit lane-ops
+
+
 def cso_bytes_per_launch(w):
     # per pair: read winner row, loser x and v, write loser x and v
     # (20 B per pair element = 10 B per individual element); fitness of both
@@ -113,11 +123,11 @@ def _cpu_baseline(w, budget_s):
         dt = time.perf_counter() - t0
         return {"value": rows * w.D * n / dt, "unit": UNIT, "cores": 1, "kind": "oracle",
                 "sample": f"{rows} of {w.N} rows x D={w.D}, {n} evaluation passes, {dt:.1f} s"}
-    rows = min(w.N, 20_000 if w.algo == "cso" else 2000)
+    rows = min(w.N, 20_000 if w.algo == "cso" else 200 if w.algo == "es" else 2000)
     P = oracle.make_params(fn, rows, w.D, w.lb, w.ub, v_lo=w.v_lo, v_hi=w.v_hi, w=w.w, c1=w.c1,
                            c2=w.c2, phi=w.phi, vmax=w.vmax, seed=w.seed, de_f=w.de_f,
-                           de_cr=w.de_cr)
-    s = {"pso": oracle.PSO, "cso": oracle.CSO, "de": oracle.DE}[w.algo](P)
+                           de_cr=w.de_cr, es_sigma=w.es_sigma, es_lr=w.es_lr)
+    s = {"pso": oracle.PSO, "cso": oracle.CSO, "de": oracle.DE, "es": oracle.ES}[w.algo](P)
     s.step(1)
     t0 = time.perf_counter()
     gens = 0
@@ -186,10 +196,11 @@ def main():
             evox.evox_eval_argmin(fn, X, w.N, w.D, w.D, out, bf, bi, scratch)
         swarm = None
     else:
-        algo = {"pso": evox.PSO, "cso": evox.CSO, "de": evox.DE}[w.algo]
+        algo = {"pso": evox.PSO, "cso": evox.CSO, "de": evox.DE, "es": evox.ES}[w.algo]
         P = evox.make_params(algo, fn, w.N, w.D, w.lb, w.ub, v_lo=w.v_lo, v_hi=w.v_hi, w=w.w,
                              c1=w.c1, c2=w.c2, phi=w.phi, vmax=w.vmax, seed=w.seed,
-                             ldx=args.ldx or None, de_f=w.de_f, de_cr=w.de_cr)
+                             ldx=args.ldx or None, de_f=w.de_f, de_cr=w.de_cr,
+                             es_sigma=w.es_sigma, es_lr=w.es_lr)
         swarm = evox.Swarm(P)
 
         def step():
@@ -221,7 +232,19 @@ def main():
     if swarm is not None:
         fused_ms, launches, improved = swarm.profile_read()
         swarm.profile(False)
-        if launches > 0:
+        if launches > 0 and w.algo == "es":
+            # the ALU roofline of the whole generation (samples, ranks,
+            # gradient, step), timed over the step
+            gen_s = ms / 1e3 / w.gens
+            ops = ES_OPS_PER_ELEMENT * (w.N // 2) * w.D
+            achieved = ops / gen_s / 1e12
+            roofline = {"bound": "alu", "achieved": round(achieved, 2), "peak": ALU_PEAK_TOPS,
+                        "unit": "Tops/s", "frac": round(achieved / ALU_PEAK_TOPS, 4),
+                        "traffic": None, "kernel": "k_es_eval + k_es_grad",
+                        "sample_kernel_avg_us": round(fused_ms / launches * 1e3, 2),
+                        "generation_us": round(gen_s * 1e6, 2), "launches": launches,
+                        "algorithmic_ops_per_generation": ops}
+        elif launches > 0:
             avg_ms = fused_ms / launches
             bytes_per = {"pso": lambda: pso_bytes_per_launch(w, launches, improved),
                          "cso": lambda: cso_bytes_per_launch(w),
@@ -251,7 +274,7 @@ def main():
             b.copy_(a)
         torch.cuda.synchronize()
         del a, b
-    if roofline is not None:
+    if roofline is not None and roofline["bound"] == "hbm":
         copy = copy_bandwidth(torch, evox)
         roofline["copy_gbs"] = round(copy, 1)
         roofline["frac_of_copy"] = round(roofline["achieved"] / copy, 4)

@@ -72,7 +72,7 @@ struct Plan {
     int64_t xsum_rows = 0;
     int perm_batch = 0;
     size_t x2 = 0, fit2 = 0;  // DE: the other population buffer and its fitness
-    size_t esw = 0, espart = 0;  // ES: pair weights, gradient partial sums
+    size_t esrank = 0, espart = 0;  // ES: sample ranks, gradient partial sums
     size_t total = 0;
 };
 
@@ -132,7 +132,7 @@ int make_plan(const evox_params *P, Plan *pl)
     }
     if (P->algo == EVOX_ES) {
         const size_t H = (size_t)P->N / 2, chunks = (H + kEsPairChunk - 1) / kEsPairChunk;
-        p.esw = take(sizeof(double) * H);
+        p.esrank = take(sizeof(uint32_t) * 2 * H);
         p.espart = take(sizeof(double) * chunks * 4 * (size_t)((P->D + 3) / 4));
     }
     p.total = off;
@@ -155,7 +155,8 @@ struct evox_state {
     int64_t perm_t0;  // first generation of the stored permutation batch (-1: none)
     double *xsum, *s1;
     float *x2, *fit2;  // DE: the other population buffer
-    double *esw, *espart;  // ES: pair weights, gradient partial sums
+    uint32_t *esrank;  // ES: sample ranks
+    double *espart;    // ES: gradient partial sums
     // profiling of the fused generation kernel
     bool prof;
     std::vector<std::pair<hipEvent_t, hipEvent_t>> ev;
@@ -298,9 +299,10 @@ int evox_state_create(const evox_params *params, const evox_buffers *b, void *hi
     s->perm_t0 = -1;
     s->ticket = nullptr;
     s->x2 = s->fit2 = nullptr;
-    s->esw = s->espart = nullptr;
+    s->esrank = nullptr;
+    s->espart = nullptr;
     if (P.algo == EVOX_ES) {
-        s->esw = at<double>(b->scratch, pl.esw);
+        s->esrank = at<uint32_t>(b->scratch, pl.esrank);
         s->espart = at<double>(b->scratch, pl.espart);
     }
     if (P.algo == EVOX_DE) {
@@ -561,12 +563,13 @@ int evox_es_step(evox_state *s, int64_t n_gens)
     hipError_t e;
     for (int64_t k = 0; k < n_gens; ++k) {
         const uint32_t t = (uint32_t)(s->t + k);
-        EsArgs a{s->B.x, s->B.fit, P.N, P.D, P.es_sigma, s->k0, s->k1, t, k == n_gens - 1 ? s->slots : nullptr};
+        EsArgs a{s->B.x, s->B.fit, s->esrank, P.N, P.D, P.es_sigma, s->k0, s->k1, t,
+                 k == n_gens - 1 ? s->slots : nullptr};
         e = timed(s, [&] { return launch_es_eval(P.fn_id, pl.L, a, pl.grid, s->stream); });
         if (e != hipSuccess) return hip_fail(e, "es samples");
-        if ((e = launch_es_rank(s->B.fit, P.N, P.es_sigma, s->esw, s->stream)) != hipSuccess)
+        if ((e = launch_es_rank(s->B.fit, P.N, s->esrank, s->stream)) != hipSuccess)
             return hip_fail(e, "es ranks");
-        EsGradArgs ga{s->esw, s->espart, s->B.x, P.N / 2, P.D, P.es_lr, s->k0, s->k1, t};
+        EsGradArgs ga{s->esrank, s->espart, s->B.x, P.N / 2, P.D, P.es_sigma, P.es_lr, s->k0, s->k1, t};
         if ((e = launch_es_grad(ga, s->stream)) != hipSuccess) return hip_fail(e, "es gradient");
     }
     if ((e = launch_select(s->slots, nullptr, 0, nullptr, s->best, nullptr, nullptr, s->stream)) != hipSuccess)

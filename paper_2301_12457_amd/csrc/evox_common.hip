@@ -543,7 +543,7 @@ hipError_t launch_colsum(Layout L, const float *x, int64_t N, int64_t D, int64_t
 {
     switch (L.G * 16 + L.maxit) {
         EVOX_FAMILY_CASES(EVOX_LAUNCH_COLSUM, LAYOUT_CSO, 0)
-        EVOX_BIG_CASE(EVOX_LAUNCH_COLSUM, 0)
+        EVOX_BIG_CASES(EVOX_LAUNCH_COLSUM, LAYOUT_CSO, 0)
         default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
@@ -592,72 +592,53 @@ hipError_t launch_es_eval(int fn, Layout L, const EsArgs &a, int grid, hipStream
 }
 
 // ---------------------------------------------------------------------------
-// OpenES centered ranks: one block of 1024 sorts the N (<= kEsMaxN) keys
-// (orderable fitness, index) -- the argmin order -- with a bitonic network in
-// LDS, so key position p is sample i's rank; then each pair's weight
-// w_k = (rank_{2k} - rank_{2k+1}) / (N - 1) / (N sigma) (the difference of
-// the centered ranks rank / (N - 1) - 1/2, scaled by the estimate's 1 / (N
-// sigma)).
+// OpenES centered ranks: rank_i = #{j : key_j < key_i} with key = (orderable
+// fitness, index), the argmin order, so the ranks are a permutation and NaN
+// ranks last.  Block (tile of 256 samples i, range of kEsRankSpan samples j)
+// stages its j-keys in LDS, counts, and adds its count to rank_i with one
+// integer atomic per i (exact, so the result does not depend on the order of
+// the additions).  rank is zeroed by k_es_eval of the same generation.
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(1024) void k_es_rank(const float *fit, int64_t N, float sigma, double *w)
+constexpr int kEsRankSpan = 512;
+
+__global__ __launch_bounds__(256) void k_es_rank(const float *fit, int64_t N, uint32_t *rank)
 {
-    __shared__ uint64_t key[kEsMaxN];
-    uint32_t *rank_of = reinterpret_cast<uint32_t *>(key);  // reused once the order is known
-    int n2 = 1;
-    while (n2 < N) n2 <<= 1;
-    for (int i = threadIdx.x; i < n2; i += 1024) key[i] = i < N ? sel_key(fit[i], i) : kNoKey;
+    __shared__ uint64_t kj[kEsRankSpan];
+    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    const int64_t j0 = (int64_t)blockIdx.y * kEsRankSpan;
+    const int64_t nj = N - j0 < kEsRankSpan ? N - j0 : kEsRankSpan;
+    for (int q = threadIdx.x; q < nj; q += 256) kj[q] = sel_key(fit[j0 + q], j0 + q);
     __syncthreads();
-    for (int size = 2; size <= n2; size <<= 1)
-        for (int stride = size >> 1; stride > 0; stride >>= 1) {
-            for (int q = threadIdx.x; q < n2 / 2; q += 1024) {
-                const int lo = 2 * q - (q & (stride - 1)), hi = lo + stride;
-                const bool up = (lo & size) == 0;
-                const uint64_t a = key[lo], b = key[hi];
-                if ((a > b) == up) {
-                    key[lo] = b;
-                    key[hi] = a;
-                }
-            }
-            __syncthreads();
-        }
-    constexpr int kPer = kEsMaxN / 1024;
-    uint32_t who[kPer];
-#pragma unroll
-    for (int r = 0; r < kPer; ++r) {
-        const int p = threadIdx.x + 1024 * r;
-        who[r] = p < N ? (uint32_t)key_index(key[p]) : 0u;
-    }
-    __syncthreads();
-#pragma unroll
-    for (int r = 0; r < kPer; ++r) {
-        const int p = threadIdx.x + 1024 * r;
-        if (p < N) rank_of[who[r]] = (uint32_t)p;
-    }
-    __syncthreads();
-    const double scale = 1.0 / ((double)(N - 1) * (double)N * (double)sigma);
-    for (int k = threadIdx.x; k < N / 2; k += 1024)
-        w[k] = ((double)rank_of[2 * k] - (double)rank_of[2 * k + 1]) * scale;
+    if (i >= N) return;
+    const uint64_t ki = sel_key(fit[i], i);
+    uint32_t below_i = 0;
+    for (int q = 0; q < nj; ++q) below_i += kj[q] < ki ? 1u : 0u;
+    if (below_i) atomicAdd(&rank[i], below_i);
 }
 
-hipError_t launch_es_rank(const float *fit, int64_t N, float sigma, double *w, hipStream_t s)
+hipError_t launch_es_rank(const float *fit, int64_t N, uint32_t *rank, hipStream_t s)
 {
-    hipLaunchKernelGGL(k_es_rank, dim3(1), dim3(1024), 0, s, fit, N, sigma, w);
+    const unsigned tiles = (unsigned)((N + 255) / 256), spans = (unsigned)((N + kEsRankSpan - 1) / kEsRankSpan);
+    hipLaunchKernelGGL(k_es_rank, dim3(tiles, spans), dim3(256), 0, s, fit, N, rank);
     return hipGetLastError();
 }
 
 // OpenES gradient, pass 1: thread (pair chunk b, column chunk c) sums
-// w_k eps_k over its kEsPairChunk pairs for four columns in fp64, the
-// perturbations regenerated from Philox exactly as the samples drew them.
+// w_k eps_k over its kEsPairChunk pairs for four columns in fp64, with the
+// pair weight w_k = (rank_{2k} - rank_{2k+1}) / ((N - 1) N sigma) (the
+// difference of the centered ranks rank / (N - 1) - 1/2 over N sigma) and
+// the perturbations regenerated from Philox exactly as the samples drew them.
 __global__ __launch_bounds__(256) void k_es_grad(EsGradArgs a)
 {
     const int64_t C4 = (a.D + 3) / 4;
     const int64_t c = (int64_t)blockIdx.x * 256 + threadIdx.x, b = blockIdx.y;
     if (c >= C4) return;
     const int64_t k0 = b * kEsPairChunk, k1 = k0 + kEsPairChunk < a.H ? k0 + kEsPairChunk : a.H;
+    const double scale = 1.0 / ((double)(2 * a.H - 1) * (double)(2 * a.H) * (double)a.sigma);
     double s0 = 0.0, s1 = 0.0, s2 = 0.0, s3 = 0.0;
     for (int64_t k = k0; k < k1; ++k) {
         const float4 z = normal4((uint32_t)c, (uint32_t)k, a.t, STREAM_ES, a.k0, a.k1);
-        const double wk = a.w[k];
+        const double wk = ((double)a.rank[2 * k] - (double)a.rank[2 * k + 1]) * scale;
         s0 = fma(wk, (double)z.x, s0);
         s1 = fma(wk, (double)z.y, s1);
         s2 = fma(wk, (double)z.z, s2);
@@ -670,23 +651,33 @@ __global__ __launch_bounds__(256) void k_es_grad(EsGradArgs a)
     dst[3] = s3;
 }
 
-// Pass 2: per column, the chunks' partial sums in chunk order, then the step
-// theta_j <- fma(-lr, g_j, theta_j) with g_j rounded to fp32 once.
+// Pass 2: per column, the chunks' partial sums -- four quarter-sums in chunk
+// order, combined in a fixed order in LDS -- then the step
+// theta_j <- fma(-lr, g_j, theta_j) with g_j rounded to fp32 once.  Block:
+// 64 columns x 4 quarters.
 __global__ __launch_bounds__(256) void k_es_update(EsGradArgs a, int64_t chunks)
 {
+    __shared__ double q4[4][64];
     const int64_t C4 = (a.D + 3) / 4;
-    const int64_t j = (int64_t)blockIdx.x * 256 + threadIdx.x;
-    if (j >= a.D) return;
+    const int col = threadIdx.x & 63, qt = threadIdx.x >> 6;
+    const int64_t j = (int64_t)blockIdx.x * 64 + col;
+    const int64_t per = (chunks + 3) / 4, b0 = qt * per, b1 = b0 + per < chunks ? b0 + per : chunks;
     double g = 0.0;
-    for (int64_t b = 0; b < chunks; ++b) g += a.part[b * 4 * C4 + j];
-    a.theta[j] = fmaf(-a.lr, (float)g, a.theta[j]);
+    if (j < a.D)
+        for (int64_t b = b0; b < b1; ++b) g += a.part[b * 4 * C4 + j];
+    q4[qt][col] = g;
+    __syncthreads();
+    if (qt == 0 && j < a.D) {
+        const double gj = ((q4[0][col] + q4[1][col]) + q4[2][col]) + q4[3][col];
+        a.theta[j] = fmaf(-a.lr, (float)gj, a.theta[j]);
+    }
 }
 
 hipError_t launch_es_grad(const EsGradArgs &a, hipStream_t s)
 {
     const int64_t C4 = (a.D + 3) / 4, chunks = (a.H + kEsPairChunk - 1) / kEsPairChunk;
     hipLaunchKernelGGL(k_es_grad, dim3((unsigned)((C4 + 255) / 256), (unsigned)chunks), dim3(256), 0, s, a);
-    hipLaunchKernelGGL(k_es_update, dim3((unsigned)((a.D + 255) / 256)), dim3(256), 0, s, a, chunks);
+    hipLaunchKernelGGL(k_es_update, dim3((unsigned)((a.D + 63) / 64)), dim3(256), 0, s, a, chunks);
     return hipGetLastError();
 }
 

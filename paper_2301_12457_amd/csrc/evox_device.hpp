@@ -58,7 +58,10 @@ inline bool row_layout(int64_t D, int family, Layout *L)
     int G = 4;
     while (G < kMaxG && (c4 + G - 1) / G > family) G *= 2;
     const int64_t nit = (c4 + G - 1) / G;
-    const int maxit = G == kMaxG ? 8 : family;
+    // the kernels' compile-time chunk count: the family's, and at 1024 lanes
+    // the smallest of (family, 4, 8) that holds the row (fewer registers for
+    // rows that need only a few chunks per lane)
+    const int maxit = G < kMaxG || nit <= family ? family : nit <= 4 ? 4 : 8;
     if (nit > maxit) return false;
     *L = Layout{G, maxit, (int)nit};
     return true;

@@ -486,6 +486,8 @@ __global__ __launch_bounds__(block_for(G)) void k_es_eval(EsArgs a)
         if (active && g == 0) {
             a.fit[2 * k] = fp;
             a.fit[2 * k + 1] = fm;
+            a.rank[2 * k] = 0u;
+            a.rank[2 * k + 1] = 0u;
             const uint64_t kp = sel_key(fp, 2 * k), km = sel_key(fm, 2 * k + 1);
             best = kp < best ? kp : best;
             best = km < best ? km : best;
@@ -534,7 +536,14 @@ __global__ __launch_bounds__(block_for(G)) void k_colsum(const float *x, int64_t
     case 128 * 16 + F: M(128, F, __VA_ARGS__); break;                                             \
     case 256 * 16 + F: M(256, F, __VA_ARGS__); break;                                             \
     case 512 * 16 + F: M(512, F, __VA_ARGS__); break;
-#define EVOX_BIG_CASE(M, ...) case 1024 * 16 + 8: M(1024, 8, __VA_ARGS__); break;
+// 1024 lanes per row: the family's own chunk count while it holds the row,
+// else the smallest of 4 and 8 chunks that does (row_layout's maxit)
+#define EVOX_BIG_4_8(M, ...)                                                                      \
+    case 1024 * 16 + 4: M(1024, 4, __VA_ARGS__); break;                                           \
+    case 1024 * 16 + 8: M(1024, 8, __VA_ARGS__); break;
+#define EVOX_BIG_CASES(M, F, ...)                                                                 \
+    case 1024 * 16 + F: M(1024, F, __VA_ARGS__); break;                                           \
+    EVOX_BIG_4_8(M, __VA_ARGS__)
 
 #define EVOX_LAUNCH_PSO(GG, MM, MODEE) \
     hipLaunchKernelGGL((k_pso<FN, GG, MM, MODEE>), dim3(grid), dim3(block_for(GG)), 0, s, a)
@@ -554,13 +563,13 @@ hipError_t launch_pso_t(Layout L, int mode, const PsoArgs &a, int grid, hipStrea
     if (mode == PSO_EVAL) {
         switch (key) {
             EVOX_FAMILY_CASES(EVOX_LAUNCH_PSO, LAYOUT_PSO, PSO_EVAL)
-            EVOX_BIG_CASE(EVOX_LAUNCH_PSO, PSO_EVAL)
+            EVOX_BIG_CASES(EVOX_LAUNCH_PSO, LAYOUT_PSO, PSO_EVAL)
             default: return hipErrorInvalidValue;
         }
     } else if (mode == PSO_FUSED) {
         switch (key) {
             EVOX_FAMILY_CASES(EVOX_LAUNCH_PSO, LAYOUT_PSO, PSO_FUSED)
-            EVOX_BIG_CASE(EVOX_LAUNCH_PSO, PSO_FUSED)
+            EVOX_BIG_CASES(EVOX_LAUNCH_PSO, LAYOUT_PSO, PSO_FUSED)
             default: return hipErrorInvalidValue;
         }
     } else {
@@ -569,7 +578,7 @@ hipError_t launch_pso_t(Layout L, int mode, const PsoArgs &a, int grid, hipStrea
         } else {
             switch (key) {
                 EVOX_FAMILY_CASES(EVOX_LAUNCH_PSO, LAYOUT_PSO, PSO_MOVE)
-                EVOX_BIG_CASE(EVOX_LAUNCH_PSO, PSO_MOVE)
+                EVOX_BIG_CASES(EVOX_LAUNCH_PSO, LAYOUT_PSO, PSO_MOVE)
                 default: return hipErrorInvalidValue;
             }
         }
@@ -586,14 +595,18 @@ hipError_t launch_eval_t(Layout L, bool vec, const EvalArgs &a, int grid, hipStr
             EVOX_FAMILY_CASES(EVOX_LAUNCH_EVAL, LAYOUT_EVAL, true)
             EVOX_FAMILY_CASES(EVOX_LAUNCH_EVAL, LAYOUT_CSO, true)
             EVOX_FAMILY_CASES(EVOX_LAUNCH_EVAL, LAYOUT_PSO, true)
-            EVOX_BIG_CASE(EVOX_LAUNCH_EVAL, true)
+            case 1024 * 16 + 1: EVOX_LAUNCH_EVAL(1024, 1, true); break;
+            case 1024 * 16 + 2: EVOX_LAUNCH_EVAL(1024, 2, true); break;
+            EVOX_BIG_4_8(EVOX_LAUNCH_EVAL, true)
             default: return hipErrorInvalidValue;
         }
     } else {
         switch (key) {
             EVOX_FAMILY_CASES(EVOX_LAUNCH_EVAL, LAYOUT_EVAL, false)
             EVOX_FAMILY_CASES(EVOX_LAUNCH_EVAL, LAYOUT_CSO, false)
-            EVOX_BIG_CASE(EVOX_LAUNCH_EVAL, false)
+            case 1024 * 16 + 1: EVOX_LAUNCH_EVAL(1024, 1, false); break;
+            case 1024 * 16 + 2: EVOX_LAUNCH_EVAL(1024, 2, false); break;
+            EVOX_BIG_4_8(EVOX_LAUNCH_EVAL, false)
             default: return hipErrorInvalidValue;
         }
     }
@@ -605,7 +618,7 @@ hipError_t launch_cso_t(Layout L, const CsoArgs &a, int grid, hipStream_t s)
 {
     switch (L.G * 16 + L.maxit) {
         EVOX_FAMILY_CASES(EVOX_LAUNCH_CSO, LAYOUT_CSO, 0)
-        EVOX_BIG_CASE(EVOX_LAUNCH_CSO, 0)
+        EVOX_BIG_CASES(EVOX_LAUNCH_CSO, LAYOUT_CSO, 0)
         default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
@@ -616,7 +629,7 @@ hipError_t launch_de_t(Layout L, const DeArgs &a, int grid, hipStream_t s)
 {
     switch (L.G * 16 + L.maxit) {
         EVOX_FAMILY_CASES(EVOX_LAUNCH_DE, LAYOUT_PSO, 0)
-        EVOX_BIG_CASE(EVOX_LAUNCH_DE, 0)
+        EVOX_BIG_CASES(EVOX_LAUNCH_DE, LAYOUT_PSO, 0)
         default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
@@ -627,7 +640,7 @@ hipError_t launch_es_eval_t(Layout L, const EsArgs &a, int grid, hipStream_t s)
 {
     switch (L.G * 16 + L.maxit) {
         EVOX_FAMILY_CASES(EVOX_LAUNCH_ES, LAYOUT_PSO, 0)
-        EVOX_BIG_CASE(EVOX_LAUNCH_ES, 0)
+        EVOX_BIG_CASES(EVOX_LAUNCH_ES, LAYOUT_PSO, 0)
         default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
@@ -641,7 +654,7 @@ int occupancy_cso_t(Layout L)
     (void)hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k_cso<FN, GG, MM>, block_for(GG), 0)
     switch (L.G * 16 + L.maxit) {
         EVOX_FAMILY_CASES(EVOX_OCC_CSO, LAYOUT_CSO, 0)
-        EVOX_BIG_CASE(EVOX_OCC_CSO, 0)
+        EVOX_BIG_CASES(EVOX_OCC_CSO, LAYOUT_CSO, 0)
         default: return 0;
     }
 #undef EVOX_OCC_CSO

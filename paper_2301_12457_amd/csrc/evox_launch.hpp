@@ -37,25 +37,26 @@ struct DeArgs {
 };
 
 // OpenES.  k_es_eval: both samples theta +- sigma eps_k of each antithetic
-// pair from registers; k_es_rank: centered ranks in LDS (N <= kEsMaxN) and
-// the pair weights; k_es_grad / k_es_update: the gradient estimate with the
-// perturbations regenerated from Philox (never stored) and the step.
+// pair from registers; k_es_rank: the ranks by counting (N <= kEsMaxN);
+// k_es_grad / k_es_update: the gradient estimate with the perturbations
+// regenerated from Philox (never stored) and the step.
 constexpr int kEsMaxN = 16384;
 constexpr int kEsPairChunk = 64;  // pairs per thread of the gradient pass
 struct EsArgs {
     const float *theta;
     float *fit;            // [N] sample fitness
+    uint32_t *rank;        // [N] zeroed here for k_es_rank
     int64_t N, D;
     float sigma;
     uint32_t k0, k1, t;
     SelSlots *slots;       // nullable
 };
 struct EsGradArgs {
-    const double *w;       // [N/2] pair weights (u_{2k} - u_{2k+1}) / (N sigma)
+    const uint32_t *rank;  // [N] sample ranks
     double *part;          // [ceil(H / kEsPairChunk)][4 * ceil(D / 4)] partial sums
     float *theta;
     int64_t H, D;
-    float lr;
+    float sigma, lr;
     uint32_t k0, k1, t;
 };
 
@@ -140,7 +141,7 @@ hipError_t launch_perm(const PermArgs &a, hipStream_t s);
 hipError_t launch_cso(int fn, Layout L, const CsoArgs &a, int grid, hipStream_t s);
 hipError_t launch_de(int fn, Layout L, const DeArgs &a, int grid, hipStream_t s);
 hipError_t launch_es_eval(int fn, Layout L, const EsArgs &a, int grid, hipStream_t s);
-hipError_t launch_es_rank(const float *fit, int64_t N, float sigma, double *w, hipStream_t s);
+hipError_t launch_es_rank(const float *fit, int64_t N, uint32_t *rank, hipStream_t s);
 hipError_t launch_es_grad(const EsGradArgs &a, hipStream_t s);
 int occupancy_cso(int fn, Layout L);
 hipError_t launch_colsum(Layout L, const float *x, int64_t N, int64_t D, int64_t ldx, double *xsum,

@@ -16,7 +16,7 @@ about a million): synthetic, seeded, no dataset.
 import math
 from dataclasses import dataclass, field
 
-PSO, CSO, DE, EVAL = "pso", "cso", "de", "eval"
+PSO, CSO, DE, ES, EVAL = "pso", "cso", "de", "es", "eval"
 
 
 @dataclass(frozen=True)
@@ -41,6 +41,8 @@ class Workload:
     x_sigma: float = 0.0
     de_f: float = 0.5      # DE differential weight and crossover rate
     de_cr: float = 0.9
+    es_sigma: float = 0.1  # OpenES perturbation scale and learning rate
+    es_lr: float = 0.01
 
 
 WORKLOADS = {
@@ -54,6 +56,8 @@ WORKLOADS = {
                                      3, lb=-600.0, ub=600.0, phi=0.1),
     "de_sphere_1e5x1e3": Workload("de_sphere_1e5x1e3", DE, "sphere", 100_000, 1_000, 200, 5,
                                   lb=-32.0, ub=32.0),
+    "es_sphere_1e4x1e4": Workload("es_sphere_1e4x1e4", ES, "sphere", 10_000, 10_000, 100, 6,
+                                  lb=-5.0, ub=5.0, es_sigma=0.1, es_lr=0.05),
     "eval_rosenbrock_1m_x1e3": Workload("eval_rosenbrock_1m_x1e3", EVAL, "rosenbrock", 1_048_576,
                                         1_000, 1, 4, x_mu=1.0, x_sigma=0.5),
 }
