@@ -251,9 +251,9 @@ int evox_row_layout(int32_t kernels, int64_t D, int32_t *threads_per_row, int32_
  * Philox(seed, (floor(j/4), i, 0, 5)) per four elements; of its word pairs
  * (0, 1) and (2, 3), a pair (a, b) gives u1 = ((a >> 8) + 1) 2^-24 in (0, 1],
  * u2 = (b >> 8) 2^-24, r = sqrt(-2 ln u1), and elements r cos(2 pi u2) (even
- * j) and r sin(2 pi u2) (odd j).  Computed in fp32 with the device logf, a
- * correctly rounded sqrt and the hardware cosine / sine of the exactly
- * reduced angle, so within sigma 1e-6 max(1, |z|) + 1 ulp of the exact value.
+ * j) and r sin(2 pi u2) (odd j).  Computed in fp32 with the hardware log2
+ * (times -2 ln 2), square root, and cosine / sine of the exactly reduced
+ * angle, so within sigma 1e-6 max(1, |z|) + 1 ulp of the exact value.
  * The initial population of an x_init = 1 state is the same matrix.  N = 0
  * does nothing. */
 int evox_fill_normal(uint64_t seed, int64_t N, int64_t D, int64_t ldx, float mu, float sigma,

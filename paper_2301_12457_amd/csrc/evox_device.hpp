@@ -168,8 +168,11 @@ __device__ __forceinline__ float4 normal4(uint32_t c, uint32_t row, uint32_t t, 
                                           uint32_t k1)
 {
     const U4 w = philox(c, row, t, stream, k0, k1);
-    const float r0 = __builtin_sqrtf(-2.0f * logf((float)((w.x >> 8) + 1u) * 0x1p-24f));
-    const float r1 = __builtin_sqrtf(-2.0f * logf((float)((w.z >> 8) + 1u) * 0x1p-24f));
+    // -2 ln u1 = -(2 ln 2) log2 u1 with the hardware log2 and square root
+    // (u1 >= 2^-24 is never denormal; both within one ulp)
+    constexpr float kTwoLn2 = 0x1.62e430p+0f;  // 2 ln 2 rounded to fp32
+    const float r0 = __builtin_amdgcn_sqrtf(-kTwoLn2 * __builtin_amdgcn_logf((float)((w.x >> 8) + 1u) * 0x1p-24f));
+    const float r1 = __builtin_amdgcn_sqrtf(-kTwoLn2 * __builtin_amdgcn_logf((float)((w.z >> 8) + 1u) * 0x1p-24f));
     const float a0 = u01(w.y), a1 = u01(w.w);
     return make_float4(r0 * cos_rev(a0), r0 * sin_rev(a0), r1 * cos_rev(a1), r1 * sin_rev(a1));
 }

@@ -79,8 +79,9 @@ def ulp_diff(a, b):
 
 def normal_tol(x_ref, mu, sigma):
     """Tolerance of the device normal deviates (Box-Muller in fp32 against
-    the fp64 oracle): logf within 1 ulp and a correctly rounded sqrt put the
-    radius r within 2^-23 relative, the hardware cosine / sine of the exactly
+    the fp64 oracle): the hardware log2 and square root, each within one
+    ulp, and the rounded 2 ln 2 put the radius r within 2^-23 relative (1.75
+    ulp), the hardware cosine / sine of the exactly
     reduced angle is within 1.25e-7 absolute, so |z_gpu - z| <= 1.25e-7 r +
     1.8e-7 |z| <= 1e-6 max(1, |z|) for r <= sqrt(2 ln 2^24) = 5.77; the final
     fma adds at most one rounding of x."""
