@@ -26,7 +26,8 @@ class RefParams(ctypes.Structure):
         ("phi", ctypes.c_float), ("vmax", ctypes.c_float),
         ("x_init", ctypes.c_int32), ("x_mu", ctypes.c_float), ("x_sigma", ctypes.c_float),
         ("de_f", ctypes.c_float), ("de_cr", ctypes.c_float),
-        ("es_sigma", ctypes.c_float), ("es_lr", ctypes.c_float), ("pad_", ctypes.c_float),
+        ("es_sigma", ctypes.c_float), ("es_lr", ctypes.c_float),
+        ("pgpe_sigma_lr", ctypes.c_float), ("pgpe_max_change", ctypes.c_float),
         ("seed", ctypes.c_uint64),
     ]
 
@@ -68,6 +69,10 @@ def lib():
         L.evox_ref_es_eps.restype = ctypes.c_double
         L.evox_ref_es_init.argtypes = [P, P]
         L.evox_ref_es_step.argtypes = [P, i64, i64, P, P, P, P, P]
+        L.evox_ref_pgpe_z.argtypes = [u64, i64, i64, i64]
+        L.evox_ref_pgpe_z.restype = ctypes.c_double
+        L.evox_ref_pgpe_init.argtypes = [P, P, P]
+        L.evox_ref_pgpe_step.argtypes = [P, i64, i64, P, P, P, P, P, P]
         L.evox_ref_de_init.argtypes = [P, P, P]
         L.evox_ref_de_step.argtypes = [P, i64, i64, P, P, P, P, P]
         L.evox_ref_cso_init.argtypes = [P, P, P, P]
@@ -149,11 +154,11 @@ def init_normal(seed, N, D, mu, sigma):
 
 def make_params(fn, N, D, lb, ub, v_lo=0.0, v_hi=0.0, w=0.6, c1=1.5, c2=1.5, phi=0.1,
                 vmax=0.0, clamp_x=0, seed=0, x_init=0, x_mu=0.0, x_sigma=1.0, de_f=0.5, de_cr=0.9,
-                es_sigma=0.1, es_lr=0.01):
+                es_sigma=0.1, es_lr=0.01, pgpe_sigma_lr=0.01, pgpe_max_change=0.2):
     return RefParams(fn=fn, clamp_x=clamp_x, N=N, D=D, lb=lb, ub=ub, v_lo=v_lo, v_hi=v_hi,
                      w=w, c1=c1, c2=c2, phi=phi, vmax=vmax, x_init=x_init, x_mu=x_mu,
                      x_sigma=x_sigma, de_f=de_f, de_cr=de_cr, es_sigma=es_sigma, es_lr=es_lr,
-                     pad_=0.0, seed=seed)
+                     pgpe_sigma_lr=pgpe_sigma_lr, pgpe_max_change=pgpe_max_change, seed=seed)
 
 
 class PSO:
@@ -311,6 +316,40 @@ class ES:
                                     _ptr(self.fit), _ptr(self.rank), ctypes.byref(bf), ctypes.byref(bi))
         if rc != 0:
             raise ValueError(f"evox_ref_es_step rc={rc}")
+        if n_gens > 0:
+            self.best_fit, self.best_idx = bf.value, bi.value
+        self.t += n_gens
+
+
+def pgpe_z(seed, t, k, j):
+    """The fp64 standard deviate z_kj of PGPE pair k at generation t."""
+    return lib().evox_ref_pgpe_z(seed, t, k, j)
+
+
+class PGPE:
+    """Oracle PGPE state: center mu, standard deviations sigma, generation t."""
+
+    def __init__(self, params: RefParams):
+        self.P = params
+        self.mu = np.zeros(params.D, np.float32)
+        self.sigma = np.zeros(params.D, np.float32)
+        self.fit = np.zeros(params.N, np.float32)
+        self.rank = np.zeros(params.N, np.int64)
+        self.best_fit = float("nan")
+        self.best_idx = -1
+        self.t = 0
+        if lib().evox_ref_pgpe_init(ctypes.byref(self.P), _ptr(self.mu), _ptr(self.sigma)) != 0:
+            raise ValueError("evox_ref_pgpe_init failed")
+
+    def step(self, n_gens):
+        for a in (self.mu, self.sigma):
+            assert a.flags.c_contiguous and a.dtype == np.float32
+        bf = ctypes.c_float(0.0)
+        bi = ctypes.c_int64(0)
+        rc = lib().evox_ref_pgpe_step(ctypes.byref(self.P), self.t, n_gens, _ptr(self.mu), _ptr(self.sigma),
+                                      _ptr(self.fit), _ptr(self.rank), ctypes.byref(bf), ctypes.byref(bi))
+        if rc != 0:
+            raise ValueError(f"evox_ref_pgpe_step rc={rc}")
         if n_gens > 0:
             self.best_fit, self.best_idx = bf.value, bi.value
         self.t += n_gens

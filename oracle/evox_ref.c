@@ -93,7 +93,7 @@ void evox_ref_u01_array(const uint32_t *w, int64_t n, float *out)
 
 /* Random-stream identifiers (the counter's fourth word). */
 enum { STREAM_INIT_X = 0, STREAM_INIT_V = 1, STREAM_PSO = 2, STREAM_CSO = 3,
-       STREAM_PERM = 4, STREAM_INIT_NORMAL = 5, STREAM_DE = 6, STREAM_ES = 7 };
+       STREAM_PERM = 4, STREAM_INIT_NORMAL = 5, STREAM_DE = 6, STREAM_ES = 7, STREAM_PGPE = 8 };
 
 /* Draw k of K for element (i, j) at generation t in stream s:
  * word (j mod 4) of Philox(seed, (K*floor(j/4) + k, i, t, s)). */
@@ -249,9 +249,10 @@ typedef struct {
     int32_t x_init;     /* 0: x ~ U[lb, ub); 1: x ~ N(x_mu, x_sigma^2) */
     float x_mu, x_sigma;
     float de_f, de_cr;  /* DE differential weight F and crossover rate CR */
-    float es_sigma;     /* OpenES perturbation scale */
-    float es_lr;        /* OpenES learning rate */
-    float pad_;
+    float es_sigma;     /* OpenES perturbation scale; PGPE initial standard deviation */
+    float es_lr;        /* OpenES / PGPE center learning rate */
+    float pgpe_sigma_lr;     /* PGPE standard-deviation learning rate */
+    float pgpe_max_change;   /* PGPE bound on the relative change of a standard deviation */
     uint64_t seed;      /* Philox key */
 } evox_ref_params;
 
@@ -686,5 +687,104 @@ int evox_ref_es_step(const evox_ref_params *P, int64_t t0, int64_t n_gens, float
         }
     }
     free(x); free(f); free(order); free(rank); free(g);
+    return 0;
+}
+
+/* ------------------------------------------------------------------------ */
+/* PGPE with symmetric sampling (Sehnke, Osendorfer, Rueckstiess, Graves,    */
+/* Peters, Schmidhuber, Neural Networks 23, 2010; the ES the paper runs in   */
+/* its neuroevolution and EvoTorch comparisons).                             */
+/* State: mu (center) and sigma (per-dimension standard deviation), fp32.    */
+/* ------------------------------------------------------------------------ */
+
+/* z_kj of pair k at generation t: the Box-Muller deviate of Philox(seed,
+ * (floor(j/4), k, t, 8)); the perturbation is sigma_j z_kj. */
+double evox_ref_pgpe_z(uint64_t seed, int64_t t, int64_t k, int64_t j)
+{
+    return box_muller(seed, k, j, t, STREAM_PGPE);
+}
+
+/* First center: row 0 of the uniform population; sigma_j = es_sigma. */
+int evox_ref_pgpe_init(const evox_ref_params *P, float *mu, float *sigma)
+{
+    if (P->N < 2 || (P->N & 1) || P->D < 1 || P->fn < 0 || P->fn >= FN_COUNT) return -1;
+    evox_ref_init_uniform(P->seed, STREAM_INIT_X, 1, P->D, P->lb, P->ub, mu);
+    for (int64_t j = 0; j < P->D; ++j) sigma[j] = P->es_sigma;
+    return 0;
+}
+
+/* n_gens PGPE generations from generation t0.  Each: perturbations
+ * eps_kj = sigma_j z_kj (fp32 product) for pairs k < N/2; samples
+ * x_{2k} = mu + eps_k, x_{2k+1} = mu - eps_k (fp32: fma(+-sigma_j, z_kj,
+ * mu_j)); fitness f = F(x); centered ranks u_i = rank_i / (N - 1) - 1/2 in
+ * the argmin order (the utilities, higher is worse); with H = N/2, in fp64:
+ *     g_mu_j    = (1/H) sum_k (u_{2k} - u_{2k+1}) / 2 * sigma_j z_kj
+ *     g_sigma_j = (1/H) sum_k (u_{2k} + u_{2k+1}) / 2 * sigma_j (z_kj^2 - 1)
+ * (the symmetric-sampling gradients of the expected utility, whose baseline
+ * -- the mean utility -- is zero); descent steps in fp32:
+ *     mu_j    <- fma(-lr, g_mu_j, mu_j)
+ *     d_j      = -sigma_lr g_sigma_j, clamped to [-c sigma_j, c sigma_j]
+ *                with c = pgpe_max_change (c sigma_j rounded once)
+ *     sigma_j <- sigma_j + d_j
+ * with the gradients rounded to fp32 once.  fit / rank (nullable) receive
+ * the last generation's; (best_fit, best_idx) its best sample. */
+int evox_ref_pgpe_step(const evox_ref_params *P, int64_t t0, int64_t n_gens, float *mu, float *sigma,
+                       float *fit_out, int64_t *rank_out, float *best_fit, int64_t *best_idx)
+{
+    const int64_t N = P->N, D = P->D, H = N / 2;
+    if (N < 2 || (N & 1) || D < 1 || n_gens < 0 || P->fn < 0 || P->fn >= FN_COUNT) return -1;
+    float *x = (float *)malloc(sizeof(float) * (size_t)D);
+    float *f = (float *)malloc(sizeof(float) * (size_t)N);
+    int64_t *order = (int64_t *)malloc(sizeof(int64_t) * (size_t)N);
+    int64_t *rank = (int64_t *)malloc(sizeof(int64_t) * (size_t)N);
+    double *gm = (double *)malloc(sizeof(double) * (size_t)D);
+    double *gs = (double *)malloc(sizeof(double) * (size_t)D);
+    if (!x || !f || !order || !rank || !gm || !gs) {
+        free(x); free(f); free(order); free(rank); free(gm); free(gs);
+        return -1;
+    }
+    for (int64_t t = t0; t < t0 + n_gens; ++t) {
+        for (int64_t i = 0; i < N; ++i) {
+            const int64_t k = i / 2;
+            for (int64_t j = 0; j < D; ++j) {
+                const float s = (i & 1) ? -sigma[j] : sigma[j];
+                x[j] = fmaf(s, (float)evox_ref_pgpe_z(P->seed, t, k, j), mu[j]);
+            }
+            f[i] = (float)evox_ref_eval_row_f64(P->fn, x, D);
+        }
+        for (int64_t i = 0; i < N; ++i) {
+            int64_t p = i;
+            while (p > 0 && better(f[i], i, f[order[p - 1]], order[p - 1])) {
+                order[p] = order[p - 1];
+                --p;
+            }
+            order[p] = i;
+        }
+        for (int64_t p = 0; p < N; ++p) rank[order[p]] = p;
+        for (int64_t j = 0; j < D; ++j) gm[j] = gs[j] = 0.0;
+        for (int64_t k = 0; k < H; ++k) {
+            const double u0 = (double)rank[2 * k] / (double)(N - 1) - 0.5;
+            const double u1 = (double)rank[2 * k + 1] / (double)(N - 1) - 0.5;
+            for (int64_t j = 0; j < D; ++j) {
+                const double z = (double)(float)evox_ref_pgpe_z(P->seed, t, k, j);
+                gm[j] += 0.5 * (u0 - u1) * (double)sigma[j] * z;
+                gs[j] += 0.5 * (u0 + u1) * (double)sigma[j] * (z * z - 1.0);
+            }
+        }
+        for (int64_t j = 0; j < D; ++j) {
+            const float gmj = (float)(gm[j] / (double)H), gsj = (float)(gs[j] / (double)H);
+            mu[j] = fmaf(-P->es_lr, gmj, mu[j]);
+            const float cap = P->pgpe_max_change * sigma[j];
+            const float d = fminf(fmaxf(-P->pgpe_sigma_lr * gsj, -cap), cap);
+            sigma[j] = sigma[j] + d;
+        }
+        if (t == t0 + n_gens - 1) {
+            if (fit_out) memcpy(fit_out, f, sizeof(float) * (size_t)N);
+            if (rank_out) memcpy(rank_out, rank, sizeof(int64_t) * (size_t)N);
+            *best_idx = order[0];
+            *best_fit = f[order[0]];
+        }
+    }
+    free(x); free(f); free(order); free(rank); free(gm); free(gs);
     return 0;
 }
