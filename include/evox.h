@@ -63,7 +63,7 @@ enum evox_fn {
     EVOX_SCHWEFEL = 5
 };
 
-enum evox_algo { EVOX_PSO = 0, EVOX_CSO = 1, EVOX_DE = 2, EVOX_ES = 3 };
+enum evox_algo { EVOX_PSO = 0, EVOX_CSO = 1, EVOX_DE = 2, EVOX_ES = 3, EVOX_PGPE = 4 };
 
 enum evox_status {
     EVOX_OK = 0,
@@ -78,10 +78,10 @@ enum evox_status {
 
 /* Immutable hyperparameters (theta of Sec. IV-B), fixed at creation. */
 typedef struct evox_params {
-    int32_t algo;     /* EVOX_PSO, EVOX_CSO, EVOX_DE or EVOX_ES (OpenES) */
+    int32_t algo;     /* EVOX_PSO, EVOX_CSO, EVOX_DE, EVOX_ES (OpenES) or EVOX_PGPE */
     int32_t fn_id;    /* enum evox_fn */
     int64_t N;        /* population size: PSO 1 .. 2^31 - 1, CSO 2 .. 2^24, DE 4 .. 2^31 - 1,
-                         ES even, 2 .. 16384 (N / 2 antithetic pairs) */
+                         ES / PGPE even, 2 .. 16384 (N / 2 antithetic pairs) */
     int64_t D;        /* dimension, 1 .. EVOX_MAX_D */
     int64_t ldx;      /* row pitch of x, v, pbest in floats: ldx >= D, ldx % 4 == 0 */
     float lb, ub;     /* x_init 0: initial positions ~ U[lb, ub): x = fma(u, ub - lb, lb);
@@ -96,8 +96,10 @@ typedef struct evox_params {
     float x_mu, x_sigma;
     float de_f;       /* DE differential weight F */
     float de_cr;      /* DE crossover rate CR */
-    float es_sigma;   /* ES perturbation scale sigma */
-    float es_lr;      /* ES learning rate */
+    float es_sigma;   /* ES perturbation scale sigma; PGPE initial deviation (every dimension) */
+    float es_lr;      /* ES / PGPE center learning rate */
+    float pgpe_sigma_lr;    /* PGPE deviation learning rate */
+    float pgpe_max_change;  /* PGPE bound on a deviation's relative change per generation */
     uint64_t seed;    /* Philox key */
 } evox_params;
 
@@ -112,6 +114,8 @@ typedef struct evox_params {
  *   ES:  x [ldx] = the center theta (one row; x_init / lb / ub / seed give
  *        its first value, row 0 of the initial population); fit [N] = the
  *        fitness of the last generation's samples; the rest unused.
+ *   PGPE: as ES, and v [ldx] = the per-dimension deviations sigma (es_sigma
+ *        at creation, padding 0).
  * Every array pointer must be 16-byte aligned.  scratch must hold
  * evox_scratch_bytes(params) bytes, 256-byte aligned, and must not be used by
  * anything else while the state exists. */
@@ -221,6 +225,23 @@ int evox_de_step(evox_state *state, int64_t n_gens);
  * and, as the solution, the current center theta. */
 int evox_es_step(evox_state *state, int64_t n_gens);
 
+/* n_gens PGPE generations with symmetric sampling (Sehnke et al., Neural
+ * Networks 23, 2010; the ES of the paper's neuroevolution experiment,
+ * Sec. VII) on a PGPE state.  Generation t, with H = N/2 pairs:
+ *   - deviates z_kj from Philox(seed, (floor(j/4), k, t, 8)) with the
+ *     Box-Muller layout of evox_fill_normal; samples x_{2k} = fma(sigma_j,
+ *     z_kj, mu_j), x_{2k+1} = fma(-sigma_j, z_kj, mu_j); fit = F(x);
+ *   - centered ranks u_i = rank_i / (N - 1) - 1/2 (the argmin order);
+ *   - g_mu_j = sigma_j sum_k (u_{2k} - u_{2k+1}) z_kj / (2H),
+ *     g_sigma_j = sigma_j sum_k (u_{2k} + u_{2k+1}) (z_kj^2 - 1) / (2H)
+ *     (fp64; the baseline, the mean utility, is zero);
+ *   - mu_j <- fma(-es_lr, g_mu_j, mu_j); sigma_j <- sigma_j + d_j with
+ *     d_j = -pgpe_sigma_lr g_sigma_j clamped to +-pgpe_max_change sigma_j
+ *     (gradients rounded to fp32 once).
+ * evox_best reports the best sample of the last generation and the center
+ * mu as the solution. */
+int evox_pgpe_step(evox_state *state, int64_t n_gens);
+
 /* If the caller has changed x (or fit) of a CSO state, recompute xbar from x
  * and, when refit is nonzero, fit = F(x). */
 int evox_cso_refresh(evox_state *state, int refit);
@@ -286,7 +307,7 @@ int evox_argsort_u32(const uint32_t *keys, int64_t N, uint32_t *perm_out, void *
  * pays, else a multiple of 4.  PSO (rows streamed in order; its kernels also
  * write the padding so that row ends are whole lines): 32-multiples for
  * D >= 512, where the padding is at most ~6 %; DE, whose target rows are
- * streamed the same way, and ES likewise.  CSO (rows gathered and
+ * streamed the same way, and ES / PGPE likewise.  CSO (rows gathered and
  * written at random; padding never touched): 32-multiples for D >= 64.
  * Returns the pitch, or 0 for an unknown algo or D outside [1, EVOX_MAX_D]. */
 int64_t evox_default_ldx(int32_t algo, int64_t D);

@@ -15,7 +15,7 @@ LIB_PATH = os.path.join(HERE, "libevox.so")
 SPHERE, ACKLEY, RASTRIGIN, GRIEWANK, ROSENBROCK, SCHWEFEL = range(6)
 FN_IDS = {"sphere": SPHERE, "ackley": ACKLEY, "rastrigin": RASTRIGIN, "griewank": GRIEWANK,
           "rosenbrock": ROSENBROCK, "schwefel": SCHWEFEL}
-PSO, CSO, DE, ES = 0, 1, 2, 3
+PSO, CSO, DE, ES, PGPE = 0, 1, 2, 3, 4
 OK, EINVAL, EHIP, ENOSPC, EALIGN = 0, -1, -2, -3, -4
 MAX_D = 32768
 
@@ -23,7 +23,7 @@ MAX_D = 32768
 EXPORTS = (
     "evox_scratch_bytes", "evox_state_create", "evox_state_destroy", "evox_eval", "evox_eval_ld",
     "evox_eval_argmin_scratch_bytes", "evox_eval_argmin", "evox_pso_step", "evox_cso_step",
-    "evox_de_step", "evox_es_step",
+    "evox_de_step", "evox_es_step", "evox_pgpe_step",
     "evox_cso_refresh", "evox_best", "evox_generation", "evox_row_layout", "evox_default_ldx",
     "evox_fill_normal", "evox_copy", "evox_philox_fill", "evox_permutation_scratch_bytes",
     "evox_permutation", "evox_argsort_u32",
@@ -49,6 +49,7 @@ class Params(ctypes.Structure):
         ("x_init", ctypes.c_int32), ("x_mu", ctypes.c_float), ("x_sigma", ctypes.c_float),
         ("de_f", ctypes.c_float), ("de_cr", ctypes.c_float),
         ("es_sigma", ctypes.c_float), ("es_lr", ctypes.c_float),
+        ("pgpe_sigma_lr", ctypes.c_float), ("pgpe_max_change", ctypes.c_float),
         ("seed", ctypes.c_uint64),
     ]
 
@@ -83,6 +84,7 @@ def lib():
             "evox_cso_step": ([P, i64], i32),
             "evox_de_step": ([P, i64], i32),
             "evox_es_step": ([P, i64], i32),
+            "evox_pgpe_step": ([P, i64], i32),
             "evox_cso_refresh": ([P, i32], i32),
             "evox_best": ([P, P, P, P], i32),
             "evox_generation": ([P], i64),
@@ -199,11 +201,12 @@ def pitch(D, algo=PSO):
 
 def make_params(algo, fn_id, N, D, lb, ub, v_lo=0.0, v_hi=0.0, w=0.6, c1=1.5, c2=1.5, phi=0.1,
                 vmax=0.0, clamp_x=0, seed=0, ldx=None, x_init=0, x_mu=0.0, x_sigma=1.0, de_f=0.5,
-                de_cr=0.9, es_sigma=0.1, es_lr=0.01):
+                de_cr=0.9, es_sigma=0.1, es_lr=0.01, pgpe_sigma_lr=0.01, pgpe_max_change=0.2):
     return Params(algo=algo, fn_id=fn_id, N=N, D=D, ldx=pitch(D, algo) if ldx is None else ldx,
                   lb=lb, ub=ub, v_lo=v_lo, v_hi=v_hi, w=w, c1=c1, c2=c2, phi=phi, vmax=vmax,
                   clamp_x=clamp_x, x_init=x_init, x_mu=x_mu, x_sigma=x_sigma, de_f=de_f,
-                  de_cr=de_cr, es_sigma=es_sigma, es_lr=es_lr, seed=seed)
+                  de_cr=de_cr, es_sigma=es_sigma, es_lr=es_lr, pgpe_sigma_lr=pgpe_sigma_lr,
+                  pgpe_max_change=pgpe_max_change, seed=seed)
 
 
 def evox_scratch_bytes(params):
@@ -211,12 +214,13 @@ def evox_scratch_bytes(params):
 
 
 class Swarm:
-    """A PSO, CSO, DE or ES state over torch-allocated device buffers.
+    """A PSO, CSO, DE, OpenES or PGPE state over torch-allocated device buffers.
 
     x, v (and pbest) are [N, ldx] float32 tensors whose first D columns are the
     population; pfit / fit are [N]; gbest / xbar are [ldx].  DE has x and fit
     only (its second population buffer lives in the scratch); ES has x = the
-    center theta [ldx] and fit = the last generation's sample fitness [N].
+    center theta [ldx] and fit = the last generation's sample fitness [N];
+    PGPE also v = the per-dimension deviations [ldx].
     """
 
     def __init__(self, params: Params, device="cuda", stream=None):
@@ -225,10 +229,12 @@ class Swarm:
         self.stream = stream if stream is not None else torch.cuda.current_stream(device)
         N, ldx = params.N, params.ldx
         f32 = dict(dtype=torch.float32, device=device)
-        # ES: x is the center theta (one row)
-        self.x = torch.empty((N, ldx) if params.algo != ES else (ldx,), **f32)
-        self.v = torch.empty((N, ldx), **f32) if params.algo in (PSO, CSO) else None
-        if params.algo in (DE, ES):
+        # ES / PGPE: x is the center (one row); PGPE: v the deviations (one row)
+        one_row = params.algo in (ES, PGPE)
+        self.x = torch.empty((ldx,) if one_row else (N, ldx), **f32)
+        self.v = (torch.empty((N, ldx), **f32) if params.algo in (PSO, CSO)
+                  else torch.empty((ldx,), **f32) if params.algo == PGPE else None)
+        if params.algo in (DE, ES, PGPE):
             self.pbest = self.pfit = self.gbest = self.xbar = None
             self.fit = torch.empty((N,), **f32)
         elif params.algo == PSO:
@@ -274,8 +280,10 @@ class Swarm:
             _check(lib().evox_cso_step(self.handle, n_gens))
         elif self.P.algo == DE:
             _check(lib().evox_de_step(self.handle, n_gens))
-        else:
+        elif self.P.algo == ES:
             _check(lib().evox_es_step(self.handle, n_gens))
+        else:
+            _check(lib().evox_pgpe_step(self.handle, n_gens))
 
     def refresh(self, refit=True):
         _check(lib().evox_cso_refresh(self.handle, 1 if refit else 0))

@@ -79,8 +79,10 @@ struct Plan {
 int make_plan(const evox_params *P, Plan *pl)
 {
     if (!P) return fail(EVOX_EINVAL, "params is null");
-    if (P->algo != EVOX_PSO && P->algo != EVOX_CSO && P->algo != EVOX_DE && P->algo != EVOX_ES)
+    if (P->algo != EVOX_PSO && P->algo != EVOX_CSO && P->algo != EVOX_DE && P->algo != EVOX_ES &&
+        P->algo != EVOX_PGPE)
         return fail(EVOX_EINVAL, "unknown algo %d", P->algo);
+    const bool es_like = P->algo == EVOX_ES || P->algo == EVOX_PGPE;
     if (P->fn_id < 0 || P->fn_id >= FN_COUNT) return fail(EVOX_EINVAL, "unknown fn_id %d", P->fn_id);
     const int64_t nmin = P->algo == EVOX_CSO ? 2 : P->algo == EVOX_DE ? 4 : 1;
     if (P->N < nmin || P->N >= ((int64_t)1 << 31))
@@ -89,15 +91,15 @@ int make_plan(const evox_params *P, Plan *pl)
         return fail(EVOX_EINVAL, "D = %lld out of range [1, %d]", (long long)P->D, EVOX_MAX_D);
     if (P->algo == EVOX_CSO && P->N > kCsoMaxN)
         return fail(EVOX_EINVAL, "CSO N = %lld above %lld", (long long)P->N, (long long)kCsoMaxN);
-    if (P->algo == EVOX_ES && (P->N < 2 || (P->N & 1) || P->N > kEsMaxN))
-        return fail(EVOX_EINVAL, "ES N = %lld must be even, in [2, %d]", (long long)P->N, kEsMaxN);
+    if (es_like && (P->N < 2 || (P->N & 1) || P->N > kEsMaxN))
+        return fail(EVOX_EINVAL, "ES / PGPE N = %lld must be even, in [2, %d]", (long long)P->N, kEsMaxN);
     if (P->ldx < P->D || (P->ldx & 3))
         return fail(EVOX_EINVAL, "ldx = %lld must be >= D and a multiple of 4", (long long)P->ldx);
     if (P->x_init != 0 && P->x_init != 1) return fail(EVOX_EINVAL, "unknown x_init %d", P->x_init);
     Plan p;
     const int family = P->algo == EVOX_CSO ? LAYOUT_CSO : LAYOUT_PSO;
     if (!row_layout(P->D, family, &p.L)) return fail(EVOX_EINVAL, "no row layout for D = %lld", (long long)P->D);
-    p.grid = grid_for(P->algo == EVOX_ES ? P->N / 2 : P->N, p.L.G, kMaxGrid);
+    p.grid = grid_for(es_like ? P->N / 2 : P->N, p.L.G, kMaxGrid);
     size_t off = 0;
     auto take = [&](size_t bytes) {
         const size_t at = off;
@@ -130,10 +132,11 @@ int make_plan(const evox_params *P, Plan *pl)
         p.x2 = take(sizeof(float) * (size_t)P->N * (size_t)P->ldx);
         p.fit2 = take(sizeof(float) * (size_t)P->N);
     }
-    if (P->algo == EVOX_ES) {
+    if (es_like) {
         const size_t H = (size_t)P->N / 2, chunks = (H + kEsPairChunk - 1) / kEsPairChunk;
+        const size_t sums = P->algo == EVOX_PGPE ? 2 : 1;  // PGPE: center and deviation gradients
         p.esrank = take(sizeof(uint32_t) * 2 * H);
-        p.espart = take(sizeof(double) * chunks * 4 * (size_t)((P->D + 3) / 4));
+        p.espart = take(sizeof(double) * sums * chunks * 4 * (size_t)((P->D + 3) / 4));
     }
     p.total = off;
     *pl = p;
@@ -273,7 +276,9 @@ int evox_state_create(const evox_params *params, const evox_buffers *b, void *hi
     if (!b) return fail(EVOX_EINVAL, "buffers is null");
     if (!b->x || !b->scratch) return fail(EVOX_EINVAL, "x and scratch are required");
     if ((P.algo == EVOX_PSO || P.algo == EVOX_CSO) && !b->v) return fail(EVOX_EINVAL, "PSO and CSO need v");
-    if ((P.algo == EVOX_DE || P.algo == EVOX_ES) && !b->fit) return fail(EVOX_EINVAL, "DE and ES need fit");
+    if ((P.algo == EVOX_DE || P.algo == EVOX_ES || P.algo == EVOX_PGPE) && !b->fit)
+        return fail(EVOX_EINVAL, "DE, ES and PGPE need fit");
+    if (P.algo == EVOX_PGPE && !b->v) return fail(EVOX_EINVAL, "PGPE needs v (the deviations)");
     if (P.algo == EVOX_PSO && (!b->pbest || !b->pfit || !b->gbest))
         return fail(EVOX_EINVAL, "PSO needs pbest, pfit and gbest");
     if (P.algo == EVOX_CSO && (!b->fit || !b->xbar)) return fail(EVOX_EINVAL, "CSO needs fit and xbar");
@@ -301,7 +306,7 @@ int evox_state_create(const evox_params *params, const evox_buffers *b, void *hi
     s->x2 = s->fit2 = nullptr;
     s->esrank = nullptr;
     s->espart = nullptr;
-    if (P.algo == EVOX_ES) {
+    if (P.algo == EVOX_ES || P.algo == EVOX_PGPE) {
         s->esrank = at<uint32_t>(b->scratch, pl.esrank);
         s->espart = at<double>(b->scratch, pl.espart);
     }
@@ -335,10 +340,11 @@ int evox_state_create(const evox_params *params, const evox_buffers *b, void *hi
     }
 
     hipError_t e;
-    // ES: x is the center theta, one row
+    // ES / PGPE: x is the center, one row
     const bool own_v = P.algo == EVOX_PSO || P.algo == EVOX_CSO;
+    const bool es_like = P.algo == EVOX_ES || P.algo == EVOX_PGPE;
     InitArgs ia{b->x, own_v ? b->v : nullptr, P.algo == EVOX_PSO ? b->pbest : nullptr,
-                P.algo == EVOX_ES ? 1 : P.N, P.D, P.ldx, P.lb, P.ub,
+                es_like ? 1 : P.N, P.D, P.ldx, P.lb, P.ub,
                 P.v_lo, P.v_hi, P.v_lo == 0.0f && P.v_hi == 0.0f, P.x_init == 1, P.x_mu, P.x_sigma,
                 s->k0, s->k1};
     if ((e = launch_init(ia, s->stream)) != hipSuccess) {
@@ -356,8 +362,11 @@ int evox_state_create(const evox_params *params, const evox_buffers *b, void *hi
             delete s;
             return hip_fail(e, "init");
         }
-    } else if (P.algo == EVOX_ES) {
-        if ((e = best_init(s, std::numeric_limits<float>::infinity(), 0)) != hipSuccess) {
+    } else if (es_like) {
+        // PGPE: v holds the deviations, es_sigma in every dimension (padding 0)
+        if ((e = best_init(s, std::numeric_limits<float>::infinity(), 0)) != hipSuccess ||
+            (P.algo == EVOX_PGPE && (e = launch_fill(b->v, P.ldx, 0.0f, s->stream)) != hipSuccess) ||
+            (P.algo == EVOX_PGPE && (e = launch_fill(b->v, P.D, P.es_sigma, s->stream)) != hipSuccess)) {
             delete s;
             return hip_fail(e, "init");
         }
@@ -551,31 +560,55 @@ int evox_de_step(evox_state *s, int64_t n_gens)
     return EVOX_OK;
 }
 
-int evox_es_step(evox_state *s, int64_t n_gens)
+}  // extern "C"
+
+namespace {
+
+// n_gens OpenES (pgpe false) or PGPE generations: samples and fitness,
+// ranks, gradients and steps per generation; the selection after the last.
+int es_generations(evox_state *s, int64_t n_gens, bool pgpe)
 {
-    if (!s) return fail(EVOX_EINVAL, "state is null");
-    if (s->P.algo != EVOX_ES) return fail(EVOX_EINVAL, "evox_es_step on a state of another algorithm");
     if (n_gens < 0) return fail(EVOX_EINVAL, "n_gens = %lld < 0", (long long)n_gens);
     if (s->t + n_gens >= ((int64_t)1 << 32)) return fail(EVOX_EINVAL, "generation counter would pass 2^32");
     if (n_gens == 0) return EVOX_OK;
     const evox_params &P = s->P;
     const Plan &pl = s->pl;
+    const uint32_t stream = pgpe ? STREAM_PGPE : STREAM_ES;
+    float *sig = pgpe ? s->B.v : nullptr;
     hipError_t e;
     for (int64_t k = 0; k < n_gens; ++k) {
         const uint32_t t = (uint32_t)(s->t + k);
-        EsArgs a{s->B.x, s->B.fit, s->esrank, P.N, P.D, P.es_sigma, s->k0, s->k1, t,
+        EsArgs a{s->B.x, sig, s->B.fit, s->esrank, P.N, P.D, P.es_sigma, s->k0, s->k1, t, stream,
                  k == n_gens - 1 ? s->slots : nullptr};
         e = timed(s, [&] { return launch_es_eval(P.fn_id, pl.L, a, pl.grid, s->stream); });
-        if (e != hipSuccess) return hip_fail(e, "es samples");
-        if ((e = launch_es_rank(s->B.fit, P.N, s->esrank, s->stream)) != hipSuccess)
-            return hip_fail(e, "es ranks");
-        EsGradArgs ga{s->esrank, s->espart, s->B.x, P.N / 2, P.D, P.es_sigma, P.es_lr, s->k0, s->k1, t};
-        if ((e = launch_es_grad(ga, s->stream)) != hipSuccess) return hip_fail(e, "es gradient");
+        if (e != hipSuccess) return hip_fail(e, "samples");
+        if ((e = launch_es_rank(s->B.fit, P.N, s->esrank, s->stream)) != hipSuccess) return hip_fail(e, "ranks");
+        EsGradArgs ga{s->esrank, s->espart, s->B.x, sig, P.N / 2, P.D, P.es_sigma, P.es_lr,
+                      P.pgpe_sigma_lr, P.pgpe_max_change, s->k0, s->k1, t, stream};
+        if ((e = launch_es_grad(ga, s->stream)) != hipSuccess) return hip_fail(e, "gradient");
     }
     if ((e = launch_select(s->slots, nullptr, 0, nullptr, s->best, nullptr, nullptr, s->stream)) != hipSuccess)
         return hip_fail(e, "select");
     s->t += n_gens;
     return EVOX_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int evox_es_step(evox_state *s, int64_t n_gens)
+{
+    if (!s) return fail(EVOX_EINVAL, "state is null");
+    if (s->P.algo != EVOX_ES) return fail(EVOX_EINVAL, "evox_es_step on a state of another algorithm");
+    return es_generations(s, n_gens, false);
+}
+
+int evox_pgpe_step(evox_state *s, int64_t n_gens)
+{
+    if (!s) return fail(EVOX_EINVAL, "state is null");
+    if (s->P.algo != EVOX_PGPE) return fail(EVOX_EINVAL, "evox_pgpe_step on a state of another algorithm");
+    return es_generations(s, n_gens, true);
 }
 
 int evox_cso_refresh(evox_state *s, int refit)
@@ -595,9 +628,9 @@ int evox_best(evox_state *s, float *best_fit, int64_t *best_idx, float *best_x_h
     if (best_fit) *best_fit = h.f;
     if (best_idx) *best_idx = h.i;
     if (best_x_host) {
-        const float *src = s->P.algo == EVOX_PSO ? s->B.gbest
-                           : s->P.algo == EVOX_ES ? s->B.x
-                                                  : s->B.x + h.i * s->P.ldx;
+        const float *src = s->P.algo == EVOX_PSO                                ? s->B.gbest
+                           : s->P.algo == EVOX_ES || s->P.algo == EVOX_PGPE ? s->B.x
+                                                                              : s->B.x + h.i * s->P.ldx;
         e = hipMemcpyAsync(best_x_host, src, sizeof(float) * (size_t)s->P.D, hipMemcpyDeviceToHost, s->stream);
         if (e == hipSuccess) e = hipStreamSynchronize(s->stream);
         if (e != hipSuccess) return hip_fail(e, "read best row");
@@ -624,7 +657,8 @@ int64_t evox_default_ldx(int32_t algo, int64_t D)
 {
     if (D < 1 || D > EVOX_MAX_D) return 0;
     const int64_t line = (D + 31) / 32 * 32, quad = (D + 3) / 4 * 4;
-    if (algo == EVOX_PSO || algo == EVOX_DE || algo == EVOX_ES) return D >= 512 ? line : quad;
+    if (algo == EVOX_PSO || algo == EVOX_DE || algo == EVOX_ES || algo == EVOX_PGPE)
+        return D >= 512 ? line : quad;
     if (algo == EVOX_CSO) return D >= 64 ? line : quad;
     return 0;
 }

@@ -623,61 +623,101 @@ hipError_t launch_es_rank(const float *fit, int64_t N, uint32_t *rank, hipStream
     return hipGetLastError();
 }
 
-// OpenES gradient, pass 1: thread (pair chunk b, column chunk c) sums
-// w_k eps_k over its kEsPairChunk pairs for four columns in fp64, with the
-// pair weight w_k = (rank_{2k} - rank_{2k+1}) / ((N - 1) N sigma) (the
-// difference of the centered ranks rank / (N - 1) - 1/2 over N sigma) and
-// the perturbations regenerated from Philox exactly as the samples drew them.
+// Gradient, pass 1: thread (pair chunk b, column chunk c) sums, over its
+// kEsPairChunk pairs and in fp64, the deviates z_k regenerated from Philox
+// exactly as the samples drew them, weighted by the pair's centered ranks
+// u = rank / (N - 1) - 1/2:
+//   OpenES  w_k z_k,               w_k = (u_{2k} - u_{2k+1}) / (N sigma)
+//   PGPE    m_k z_k and s_k (z_k^2 - 1),
+//           m_k = (u_{2k} - u_{2k+1}) / (2H), s_k = (u_{2k} + u_{2k+1}) / (2H)
+// (the per-dimension sigma_j factor of PGPE is applied in pass 2).
+template <bool PGPE>
 __global__ __launch_bounds__(256) void k_es_grad(EsGradArgs a)
 {
     const int64_t C4 = (a.D + 3) / 4;
     const int64_t c = (int64_t)blockIdx.x * 256 + threadIdx.x, b = blockIdx.y;
     if (c >= C4) return;
     const int64_t k0 = b * kEsPairChunk, k1 = k0 + kEsPairChunk < a.H ? k0 + kEsPairChunk : a.H;
-    const double scale = 1.0 / ((double)(2 * a.H - 1) * (double)(2 * a.H) * (double)a.sigma);
-    double s0 = 0.0, s1 = 0.0, s2 = 0.0, s3 = 0.0;
+    const double nm1 = (double)(2 * a.H - 1);
+    double s[4] = {0.0, 0.0, 0.0, 0.0}, q[4] = {0.0, 0.0, 0.0, 0.0};
     for (int64_t k = k0; k < k1; ++k) {
-        const float4 z = normal4((uint32_t)c, (uint32_t)k, a.t, STREAM_ES, a.k0, a.k1);
-        const double wk = ((double)a.rank[2 * k] - (double)a.rank[2 * k + 1]) * scale;
-        s0 = fma(wk, (double)z.x, s0);
-        s1 = fma(wk, (double)z.y, s1);
-        s2 = fma(wk, (double)z.z, s2);
-        s3 = fma(wk, (double)z.w, s3);
+        const float4 z = normal4((uint32_t)c, (uint32_t)k, a.t, a.stream, a.k0, a.k1);
+        const double u0 = (double)a.rank[2 * k] / nm1 - 0.5, u1 = (double)a.rank[2 * k + 1] / nm1 - 0.5;
+        const double zz[4] = {(double)z.x, (double)z.y, (double)z.z, (double)z.w};
+        if constexpr (PGPE) {
+            const double m = 0.5 * (u0 - u1) / (double)a.H, sw = 0.5 * (u0 + u1) / (double)a.H;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                s[e] = fma(m, zz[e], s[e]);
+                q[e] = fma(sw, zz[e] * zz[e] - 1.0, q[e]);
+            }
+        } else {
+            const double w = (u0 - u1) / ((double)(2 * a.H) * (double)a.sigma);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) s[e] = fma(w, zz[e], s[e]);
+        }
     }
+    const int64_t chunks = (a.H + kEsPairChunk - 1) / kEsPairChunk;
     double *dst = a.part + b * 4 * C4 + 4 * c;
-    dst[0] = s0;
-    dst[1] = s1;
-    dst[2] = s2;
-    dst[3] = s3;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) dst[e] = s[e];
+    if constexpr (PGPE) {
+        double *dq = dst + chunks * 4 * C4;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) dq[e] = q[e];
+    }
 }
 
 // Pass 2: per column, the chunks' partial sums -- four quarter-sums in chunk
-// order, combined in a fixed order in LDS -- then the step
-// theta_j <- fma(-lr, g_j, theta_j) with g_j rounded to fp32 once.  Block:
-// 64 columns x 4 quarters.
+// order, combined in a fixed order in LDS -- then the steps, each gradient
+// rounded to fp32 once:
+//   theta_j <- fma(-lr, g_j, theta_j)       (PGPE: g_j = sigma_j * sum)
+//   PGPE: d_j = -sig_lr * (sigma_j * sum'), clamped to +-max_change sigma_j,
+//         sigma_j <- sigma_j + d_j.
+// Block: 64 columns x 4 quarters.
+template <bool PGPE>
 __global__ __launch_bounds__(256) void k_es_update(EsGradArgs a, int64_t chunks)
 {
-    __shared__ double q4[4][64];
+    __shared__ double q4[2][4][64];
     const int64_t C4 = (a.D + 3) / 4;
     const int col = threadIdx.x & 63, qt = threadIdx.x >> 6;
     const int64_t j = (int64_t)blockIdx.x * 64 + col;
     const int64_t per = (chunks + 3) / 4, b0 = qt * per, b1 = b0 + per < chunks ? b0 + per : chunks;
-    double g = 0.0;
+    double g = 0.0, h = 0.0;
     if (j < a.D)
-        for (int64_t b = b0; b < b1; ++b) g += a.part[b * 4 * C4 + j];
-    q4[qt][col] = g;
+        for (int64_t b = b0; b < b1; ++b) {
+            g += a.part[b * 4 * C4 + j];
+            if constexpr (PGPE) h += a.part[(chunks + b) * 4 * C4 + j];
+        }
+    q4[0][qt][col] = g;
+    q4[1][qt][col] = h;
     __syncthreads();
     if (qt == 0 && j < a.D) {
-        const double gj = ((q4[0][col] + q4[1][col]) + q4[2][col]) + q4[3][col];
-        a.theta[j] = fmaf(-a.lr, (float)gj, a.theta[j]);
+        const double gj = ((q4[0][0][col] + q4[0][1][col]) + q4[0][2][col]) + q4[0][3][col];
+        if constexpr (PGPE) {
+            const double hj = ((q4[1][0][col] + q4[1][1][col]) + q4[1][2][col]) + q4[1][3][col];
+            const float sj = a.sig[j];
+            a.theta[j] = fmaf(-a.lr, (float)((double)sj * gj), a.theta[j]);
+            const float cap = a.max_change * sj;
+            const float d = fminf(fmaxf(-a.sig_lr * (float)((double)sj * hj), -cap), cap);
+            a.sig[j] = sj + d;
+        } else {
+            a.theta[j] = fmaf(-a.lr, (float)gj, a.theta[j]);
+        }
     }
 }
 
 hipError_t launch_es_grad(const EsGradArgs &a, hipStream_t s)
 {
     const int64_t C4 = (a.D + 3) / 4, chunks = (a.H + kEsPairChunk - 1) / kEsPairChunk;
-    hipLaunchKernelGGL(k_es_grad, dim3((unsigned)((C4 + 255) / 256), (unsigned)chunks), dim3(256), 0, s, a);
-    hipLaunchKernelGGL(k_es_update, dim3((unsigned)((a.D + 63) / 64)), dim3(256), 0, s, a, chunks);
+    const dim3 grid((unsigned)((C4 + 255) / 256), (unsigned)chunks), upd((unsigned)((a.D + 63) / 64));
+    if (a.sig) {
+        hipLaunchKernelGGL(k_es_grad<true>, grid, dim3(256), 0, s, a);
+        hipLaunchKernelGGL(k_es_update<true>, upd, dim3(256), 0, s, a, chunks);
+    } else {
+        hipLaunchKernelGGL(k_es_grad<false>, grid, dim3(256), 0, s, a);
+        hipLaunchKernelGGL(k_es_update<false>, upd, dim3(256), 0, s, a, chunks);
+    }
     return hipGetLastError();
 }
 

@@ -442,11 +442,11 @@ __global__ __launch_bounds__(block_for(G)) void k_de(DeArgs a)
 }
 
 // ---------------------------------------------------------------------------
-// OpenES samples and fitness: one row group per antithetic pair k; the
-// perturbation chunk eps_k (Philox stream 7, generation t, Box-Muller) and
-// both samples fma(+-sigma, eps, theta) live in registers only, and both rows
-// are reduced to their fitness.  theta (D floats) is read by every pair from
-// the caches.
+// OpenES / PGPE samples and fitness: one row group per antithetic pair k;
+// the deviate chunk z_k (Philox stream 7 or 8, generation t, Box-Muller) and
+// both samples fma(+-sigma, z, center) live in registers only, and both rows
+// are reduced to their fitness.  The center (and PGPE's sigma) are read by
+// every pair from the caches.
 // ---------------------------------------------------------------------------
 template <int FN, int G, int MAXIT>
 __global__ __launch_bounds__(block_for(G)) void k_es_eval(EsArgs a)
@@ -470,12 +470,14 @@ __global__ __launch_bounds__(block_for(G)) void k_es_eval(EsArgs a)
             float po[4] = {0.f, 0.f, 0.f, 0.f}, mo[4] = {0.f, 0.f, 0.f, 0.f};
             if (active && c < C4) {
                 const float4 th = *reinterpret_cast<const float4 *>(a.theta + 4 * c);
-                const float4 z = normal4((uint32_t)c, (uint32_t)k, a.t, STREAM_ES, a.k0, a.k1);
+                const float4 sg = a.sig ? *reinterpret_cast<const float4 *>(a.sig + 4 * c)
+                                        : make_float4(a.sigma, a.sigma, a.sigma, a.sigma);
+                const float4 z = normal4((uint32_t)c, (uint32_t)k, a.t, a.stream, a.k0, a.k1);
 #pragma unroll
                 for (int e = 0; e < 4; ++e)
                     if (4 * c + e < a.D) {
-                        po[e] = fmaf(a.sigma, comp(z, e), comp(th, e));
-                        mo[e] = fmaf(-a.sigma, comp(z, e), comp(th, e));
+                        po[e] = fmaf(comp(sg, e), comp(z, e), comp(th, e));
+                        mo[e] = fmaf(-comp(sg, e), comp(z, e), comp(th, e));
                     }
             }
             xp[it] = make_float4(po[0], po[1], po[2], po[3]);

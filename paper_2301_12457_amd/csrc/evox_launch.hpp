@@ -36,28 +36,31 @@ struct DeArgs {
     bool nt;               // streaming hint on the target rows
 };
 
-// OpenES.  k_es_eval: both samples theta +- sigma eps_k of each antithetic
-// pair from registers; k_es_rank: the ranks by counting (N <= kEsMaxN);
-// k_es_grad / k_es_update: the gradient estimate with the perturbations
-// regenerated from Philox (never stored) and the step.
+// OpenES and PGPE.  k_es_eval: both samples center +- sigma z_k of each
+// antithetic pair from registers (sigma a scalar, or per dimension for
+// PGPE); k_es_rank: the ranks by counting (N <= kEsMaxN); k_es_grad /
+// k_es_update: the gradient estimates with the deviates regenerated from
+// Philox (never stored) and the steps.
 constexpr int kEsMaxN = 16384;
 constexpr int kEsPairChunk = 64;  // pairs per thread of the gradient pass
 struct EsArgs {
     const float *theta;
+    const float *sig;      // PGPE: per-dimension deviations; null: the scalar sigma
     float *fit;            // [N] sample fitness
     uint32_t *rank;        // [N] zeroed here for k_es_rank
     int64_t N, D;
     float sigma;
-    uint32_t k0, k1, t;
+    uint32_t k0, k1, t, stream;
     SelSlots *slots;       // nullable
 };
 struct EsGradArgs {
     const uint32_t *rank;  // [N] sample ranks
-    double *part;          // [ceil(H / kEsPairChunk)][4 * ceil(D / 4)] partial sums
+    double *part;          // [1 or 2][ceil(H / kEsPairChunk)][4 * ceil(D / 4)] partial sums
     float *theta;
+    float *sig;            // PGPE: per-dimension deviations (updated); null for OpenES
     int64_t H, D;
-    float sigma, lr;
-    uint32_t k0, k1, t;
+    float sigma, lr, sig_lr, max_change;
+    uint32_t k0, k1, t, stream;
 };
 
 struct EvalArgs {

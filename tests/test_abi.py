@@ -37,12 +37,13 @@ def test_exports_every_declared_symbol(evox):
 
 
 def test_struct_layouts_match_header(evox):
-    # evox_params: 2 x int32, 3 x int64, 9 floats, 2 x int32, 6 floats, (pad), uint64
-    assert ctypes.sizeof(evox.Params) == 112
+    # evox_params: 2 x int32, 3 x int64, 9 floats, 2 x int32, 8 floats, (pad), uint64
+    assert ctypes.sizeof(evox.Params) == 120
     assert evox.Params.x_init.offset == 72
     assert evox.Params.de_f.offset == 84
     assert evox.Params.es_lr.offset == 96
-    assert evox.Params.seed.offset == 104
+    assert evox.Params.pgpe_max_change.offset == 104
+    assert evox.Params.seed.offset == 112
     assert ctypes.sizeof(evox.Buffers) == 9 * 8
 
 
@@ -88,7 +89,7 @@ def test_default_pitch_policy(evox):
         assert L.evox_default_ldx(C, D) == want, (D, want)
     for D in (10, 100, 1000):
         assert L.evox_default_ldx(evox.DE, D) == L.evox_default_ldx(P, D)
-    for algo, D in [(P, 0), (C, 32769), (4, 10)]:
+    for algo, D in [(P, 0), (C, 32769), (5, 10)]:
         assert L.evox_default_ldx(algo, D) == 0
     assert evox.make_params(C, evox.GRIEWANK, 10, 100, -1, 1).ldx == 128
     assert evox.make_params(P, evox.GRIEWANK, 10, 100, -1, 1).ldx == 100
@@ -116,10 +117,10 @@ def test_scratch_bytes(evox):
 
 
 @pytest.mark.parametrize("algo,field,value", [(0, "N", 0), (0, "D", 0), (0, "D", 40000),
-                                              (0, "ldx", 6), (0, "fn_id", 6), (0, "algo", 4),
+                                              (0, "ldx", 6), (0, "fn_id", 6), (0, "algo", 5),
                                               (1, "N", 1), (1, "N", 2**24 + 1), (0, "x_init", 2),
                                               (1, "x_init", -1), (2, "N", 3), (2, "D", 0),
-                                              (3, "N", 7), (3, "N", 16386), (3, "N", 0)])
+                                              (3, "N", 7), (3, "N", 16386), (3, "N", 0), (4, "N", 5)])
 def test_create_rejects_bad_params(evox, algo, field, value):
     p = evox.make_params(algo, evox.SPHERE, 8, 5, -1, 1)
     setattr(p, field, value)
@@ -174,6 +175,7 @@ def test_null_state_is_rejected(evox):
     assert L.evox_cso_step(None, 1) == evox.EINVAL
     assert L.evox_de_step(None, 1) == evox.EINVAL
     assert L.evox_es_step(None, 1) == evox.EINVAL
+    assert L.evox_pgpe_step(None, 1) == evox.EINVAL
     assert L.evox_best(None, None, None, None) == evox.EINVAL
     assert L.evox_generation(None) == -1
     assert L.evox_strerror(evox.ENOSPC).decode() == "scratch buffer too small"
