@@ -70,6 +70,8 @@ def de_bytes_per_launch(w):
 # elements (8), the two samples and their Sphere terms (4); the gradient
 # pass regenerates the perturbation (28) and adds its weighted value (1).
 ES_OPS_PER_ELEMENT = 20 + 8 + 4 + 28 + 1
+# PGPE: the same, with two weighted sums in the gradient pass (z and z^2 - 1)
+PGPE_OPS_PER_ELEMENT = 20 + 8 + 4 + 28 + 3
 ALU_PEAK_TOPS = 256 * 64 * 2.4e9 / 1e12   # 256 CUs x 64 lanes x 2.4 GHz, 32-bit lane-ops
 
 
@@ -123,11 +125,13 @@ def _cpu_baseline(w, budget_s):
         dt = time.perf_counter() - t0
         return {"value": rows * w.D * n / dt, "unit": UNIT, "cores": 1, "kind": "oracle",
                 "sample": f"{rows} of {w.N} rows x D={w.D}, {n} evaluation passes, {dt:.1f} s"}
-    rows = min(w.N, 20_000 if w.algo == "cso" else 200 if w.algo == "es" else 2000)
+    rows = min(w.N, 20_000 if w.algo == "cso" else 200 if w.algo in ("es", "pgpe") else 2000)
     P = oracle.make_params(fn, rows, w.D, w.lb, w.ub, v_lo=w.v_lo, v_hi=w.v_hi, w=w.w, c1=w.c1,
                            c2=w.c2, phi=w.phi, vmax=w.vmax, seed=w.seed, de_f=w.de_f,
-                           de_cr=w.de_cr, es_sigma=w.es_sigma, es_lr=w.es_lr)
-    s = {"pso": oracle.PSO, "cso": oracle.CSO, "de": oracle.DE, "es": oracle.ES}[w.algo](P)
+                           de_cr=w.de_cr, es_sigma=w.es_sigma, es_lr=w.es_lr,
+                           pgpe_sigma_lr=w.pgpe_sigma_lr, pgpe_max_change=w.pgpe_max_change)
+    s = {"pso": oracle.PSO, "cso": oracle.CSO, "de": oracle.DE, "es": oracle.ES,
+         "pgpe": oracle.PGPE}[w.algo](P)
     s.step(1)
     t0 = time.perf_counter()
     gens = 0
@@ -196,11 +200,13 @@ def main():
             evox.evox_eval_argmin(fn, X, w.N, w.D, w.D, out, bf, bi, scratch)
         swarm = None
     else:
-        algo = {"pso": evox.PSO, "cso": evox.CSO, "de": evox.DE, "es": evox.ES}[w.algo]
+        algo = {"pso": evox.PSO, "cso": evox.CSO, "de": evox.DE, "es": evox.ES,
+                "pgpe": evox.PGPE}[w.algo]
         P = evox.make_params(algo, fn, w.N, w.D, w.lb, w.ub, v_lo=w.v_lo, v_hi=w.v_hi, w=w.w,
                              c1=w.c1, c2=w.c2, phi=w.phi, vmax=w.vmax, seed=w.seed,
                              ldx=args.ldx or None, de_f=w.de_f, de_cr=w.de_cr,
-                             es_sigma=w.es_sigma, es_lr=w.es_lr)
+                             es_sigma=w.es_sigma, es_lr=w.es_lr, pgpe_sigma_lr=w.pgpe_sigma_lr,
+                             pgpe_max_change=w.pgpe_max_change)
         swarm = evox.Swarm(P)
 
         def step():
@@ -232,11 +238,11 @@ def main():
     if swarm is not None:
         fused_ms, launches, improved = swarm.profile_read()
         swarm.profile(False)
-        if launches > 0 and w.algo == "es":
+        if launches > 0 and w.algo in ("es", "pgpe"):
             # the ALU roofline of the whole generation (samples, ranks,
             # gradient, step), timed over the step
             gen_s = ms / 1e3 / w.gens
-            ops = ES_OPS_PER_ELEMENT * (w.N // 2) * w.D
+            ops = (ES_OPS_PER_ELEMENT if w.algo == "es" else PGPE_OPS_PER_ELEMENT) * (w.N // 2) * w.D
             achieved = ops / gen_s / 1e12
             roofline = {"bound": "alu", "achieved": round(achieved, 2), "peak": ALU_PEAK_TOPS,
                         "unit": "Tops/s", "frac": round(achieved / ALU_PEAK_TOPS, 4),

@@ -16,7 +16,7 @@ about a million): synthetic, seeded, no dataset.
 import math
 from dataclasses import dataclass, field
 
-PSO, CSO, DE, ES, EVAL = "pso", "cso", "de", "es", "eval"
+PSO, CSO, DE, ES, PGPE, EVAL = "pso", "cso", "de", "es", "pgpe", "eval"
 
 
 @dataclass(frozen=True)
@@ -41,8 +41,10 @@ class Workload:
     x_sigma: float = 0.0
     de_f: float = 0.5      # DE differential weight and crossover rate
     de_cr: float = 0.9
-    es_sigma: float = 0.1  # OpenES perturbation scale and learning rate
+    es_sigma: float = 0.1  # OpenES perturbation scale (PGPE: initial deviation) and learning rate
     es_lr: float = 0.01
+    pgpe_sigma_lr: float = 0.01
+    pgpe_max_change: float = 0.2
 
 
 WORKLOADS = {
@@ -58,6 +60,8 @@ WORKLOADS = {
                                   lb=-32.0, ub=32.0),
     "es_sphere_1e4x1e4": Workload("es_sphere_1e4x1e4", ES, "sphere", 10_000, 10_000, 100, 6,
                                   lb=-5.0, ub=5.0, es_sigma=0.1, es_lr=0.05),
+    "pgpe_sphere_1e4x1e4": Workload("pgpe_sphere_1e4x1e4", PGPE, "sphere", 10_000, 10_000, 100, 7,
+                                    lb=-5.0, ub=5.0, es_sigma=1.0, es_lr=0.5, pgpe_sigma_lr=0.1),
     "eval_rosenbrock_1m_x1e3": Workload("eval_rosenbrock_1m_x1e3", EVAL, "rosenbrock", 1_048_576,
                                         1_000, 1, 4, x_mu=1.0, x_sigma=0.5),
 }
