@@ -69,6 +69,7 @@ def lib():
         L.evox_ref_es_eps.restype = ctypes.c_double
         L.evox_ref_es_init.argtypes = [P, P]
         L.evox_ref_es_step.argtypes = [P, i64, i64, P, P, P, P, P]
+        L.evox_ref_gemm.argtypes = [ctypes.c_int, ctypes.c_int, i64, i64, i64, f32, P, i64, P, i64, f32, P, i64]
         L.evox_ref_pgpe_z.argtypes = [u64, i64, i64, i64]
         L.evox_ref_pgpe_z.restype = ctypes.c_double
         L.evox_ref_pgpe_init.argtypes = [P, P, P]
@@ -353,3 +354,16 @@ class PGPE:
         if n_gens > 0:
             self.best_fit, self.best_idx = bf.value, bi.value
         self.t += n_gens
+
+
+def gemm(A, B, ta=False, tb=False, alpha=1.0, beta=0.0, C=None):
+    """alpha op(A) op(B) + beta C in fp64 per output, rounded to fp32."""
+    A = np.ascontiguousarray(A, dtype=np.float32)
+    B = np.ascontiguousarray(B, dtype=np.float32)
+    M = A.shape[1] if ta else A.shape[0]
+    K = A.shape[0] if ta else A.shape[1]
+    N = B.shape[0] if tb else B.shape[1]
+    out = np.zeros((M, N), np.float32) if C is None else np.ascontiguousarray(C, dtype=np.float32).copy()
+    lib().evox_ref_gemm(int(ta), int(tb), M, N, K, alpha, _ptr(A), A.shape[1], _ptr(B), B.shape[1], beta,
+                        _ptr(out), N)
+    return out

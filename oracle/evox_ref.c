@@ -788,3 +788,25 @@ int evox_ref_pgpe_step(const evox_ref_params *P, int64_t t0, int64_t n_gens, flo
     free(x); free(f); free(order); free(rank); free(gm); free(gs);
     return 0;
 }
+
+/* ------------------------------------------------------------------------ */
+/* Dense matrix product (the contractions of the matrix-adaptation ES):      */
+/* C = alpha op(A) op(B) + beta C, op(A) [M x K], op(B) [K x N], row-major    */
+/* with leading dimensions; op(A) = A^T when ta (A stored K x M), likewise    */
+/* for B.  Each output in fp64 from the fp32 inputs, rounded once.            */
+/* ------------------------------------------------------------------------ */
+void evox_ref_gemm(int ta, int tb, int64_t M, int64_t N, int64_t K, float alpha, const float *A,
+                   int64_t lda, const float *B, int64_t ldb, float beta, float *C, int64_t ldc)
+{
+    for (int64_t i = 0; i < M; ++i)
+        for (int64_t j = 0; j < N; ++j) {
+            double acc = 0.0;
+            for (int64_t k = 0; k < K; ++k) {
+                const double a = ta ? A[k * lda + i] : A[i * lda + k];
+                const double b = tb ? B[j * ldb + k] : B[k * ldb + j];
+                acc += a * b;
+            }
+            const double c = beta != 0.0f ? (double)beta * (double)C[i * ldc + j] : 0.0;
+            C[i * ldc + j] = (float)((double)alpha * acc + c);
+        }
+}
