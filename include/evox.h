@@ -312,6 +312,17 @@ int evox_argsort_u32(const uint32_t *keys, int64_t N, uint32_t *perm_out, void *
  * Returns the pitch, or 0 for an unknown algo or D outside [1, EVOX_MAX_D]. */
 int64_t evox_default_ldx(int32_t algo, int64_t D);
 
+/* Dense fp32 product on the matrix cores, the contraction of the matrix-
+ * adaptation ES (evox_mae_step): C = alpha op(A) op(B) + beta C with op(A)
+ * M x K and op(B) K x N, row-major device matrices (op(X) = X^T when trans_x:
+ * A is then stored K x M, B N x K), leading dimensions multiples of 4 and at
+ * least the stored row lengths, 16-byte aligned pointers.  Accumulation in
+ * fp32 (v_mfma_f32_32x32x2f32) in a fixed order, so results are reproducible;
+ * beta = 0 ignores C's old contents.  M or N = 0 does nothing. */
+int evox_sgemm(int32_t trans_a, int32_t trans_b, int64_t M, int64_t N, int64_t K, float alpha,
+               const float *A, int64_t lda, const float *B, int64_t ldb, float beta, float *C,
+               int64_t ldc, void *hip_stream);
+
 /* Diagnostic, the bandwidth reference of the benchmark: dst[i] = src[i] for
  * i < n (device pointers, 16-byte aligned, not overlapping), streamed with
  * nontemporal 16-byte loads and stores.  n = 0 does nothing. */

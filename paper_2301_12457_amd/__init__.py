@@ -25,7 +25,7 @@ EXPORTS = (
     "evox_eval_argmin_scratch_bytes", "evox_eval_argmin", "evox_pso_step", "evox_cso_step",
     "evox_de_step", "evox_es_step", "evox_pgpe_step",
     "evox_cso_refresh", "evox_best", "evox_generation", "evox_row_layout", "evox_default_ldx",
-    "evox_fill_normal", "evox_copy", "evox_philox_fill", "evox_permutation_scratch_bytes",
+    "evox_fill_normal", "evox_sgemm", "evox_copy", "evox_philox_fill", "evox_permutation_scratch_bytes",
     "evox_permutation", "evox_argsort_u32",
     "evox_profile", "evox_profile_read", "evox_strerror", "evox_last_error",
 )
@@ -92,6 +92,8 @@ def lib():
             "evox_default_ldx": ([i32, i64], i64),
             "evox_fill_normal": ([u64, i64, i64, i64, ctypes.c_float, ctypes.c_float, P, P], i32),
             "evox_copy": ([P, P, i64, P], i32),
+            "evox_sgemm": ([i32, i32, i64, i64, i64, ctypes.c_float, P, i64, P, i64, ctypes.c_float, P, i64, P],
+                           i32),
             "evox_permutation_scratch_bytes": ([i64, i64], sz),
             "evox_permutation": ([u64, i64, i64, i64, P, P, sz, P], i32),
             "evox_argsort_u32": ([P, i64, P, P, sz, P], i32),
@@ -168,6 +170,17 @@ def evox_fill_normal(seed, N, D, ldx, mu, sigma, X, stream=None):
     """X[:N, :D] = mu + sigma z (Philox stream 5, Box-Muller); padding set to 0."""
     _check(lib().evox_fill_normal(seed, N, D, ldx, mu, sigma, _ptr(X), _stream(stream)))
     return X
+
+
+def evox_sgemm(A, B, C, trans_a=False, trans_b=False, alpha=1.0, beta=0.0, stream=None):
+    """C = alpha op(A) op(B) + beta C on the matrix cores (2-D fp32 tensors,
+    row strides multiples of 4)."""
+    M = A.shape[1] if trans_a else A.shape[0]
+    K = A.shape[0] if trans_a else A.shape[1]
+    N = B.shape[0] if trans_b else B.shape[1]
+    _check(lib().evox_sgemm(int(trans_a), int(trans_b), M, N, K, alpha, _ptr(A), A.stride(0), _ptr(B),
+                            B.stride(0), beta, _ptr(C), C.stride(0), _stream(stream)))
+    return C
 
 
 def evox_copy(src, dst, n, stream=None):

@@ -770,6 +770,24 @@ int evox_fill_normal(uint64_t seed, int64_t N, int64_t D, int64_t ldx, float mu,
     return EVOX_OK;
 }
 
+int evox_sgemm(int32_t trans_a, int32_t trans_b, int64_t M, int64_t N, int64_t K, float alpha, const float *A,
+               int64_t lda, const float *B, int64_t ldb, float beta, float *C, int64_t ldc, void *hip_stream)
+{
+    if (M < 0 || N < 0 || K < 0) return fail(EVOX_EINVAL, "negative size");
+    if (M == 0 || N == 0) return EVOX_OK;
+    const int64_t a_cols = trans_a ? M : K, b_cols = trans_b ? K : N;
+    if (lda < a_cols || ldb < b_cols || ldc < N) return fail(EVOX_EINVAL, "leading dimension below the row length");
+    if ((lda & 3) || (ldb & 3) || (ldc & 3)) return fail(EVOX_EALIGN, "leading dimensions must be multiples of 4");
+    if (!C || (K > 0 && (!A || !B))) return fail(EVOX_EINVAL, "null matrix");
+    if ((M + 127) / 128 > 65535 || (N + 127) / 128 > INT32_MAX) return fail(EVOX_EINVAL, "matrix too tall");
+    if ((A && !aligned16(A)) || (B && !aligned16(B)) || !aligned16(C))
+        return fail(EVOX_EALIGN, "matrices must be 16-byte aligned");
+    GemmArgs g{M, N, K, alpha, A, lda, B, ldb, beta, C, ldc};
+    hipError_t e = launch_gemm(trans_a != 0, trans_b != 0, g, (hipStream_t)hip_stream);
+    if (e != hipSuccess) return hip_fail(e, "gemm");
+    return EVOX_OK;
+}
+
 int evox_copy(const float *src, float *dst, int64_t n, void *hip_stream)
 {
     if (n < 0) return fail(EVOX_EINVAL, "n = %lld < 0", (long long)n);

@@ -63,6 +63,21 @@ struct EsGradArgs {
     uint32_t k0, k1, t, stream;
 };
 
+// C = alpha op(A) op(B) + beta C (row-major; op(A) is M x K, op(B) K x N;
+// leading dimensions and pointers 16-byte multiples for the vector loads).
+struct GemmArgs {
+    int64_t M, N, K;
+    float alpha;
+    const float *A;
+    int64_t lda;
+    const float *B;
+    int64_t ldb;
+    float beta;
+    float *C;
+    int64_t ldc;
+};
+hipError_t launch_gemm(bool ta, bool tb, const GemmArgs &g, hipStream_t s);
+
 struct EvalArgs {
     const float *X;
     int64_t N, D, ldx;
