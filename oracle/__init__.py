@@ -74,6 +74,12 @@ def lib():
         L.evox_ref_pgpe_z.restype = ctypes.c_double
         L.evox_ref_pgpe_init.argtypes = [P, P, P]
         L.evox_ref_pgpe_step.argtypes = [P, i64, i64, P, P, P, P, P, P]
+        L.evox_ref_maes_z.argtypes = [u64, i64, i64, i64]
+        L.evox_ref_maes_z.restype = ctypes.c_double
+        L.evox_ref_maes_consts.argtypes = [i64, i64, P, P]
+        L.evox_ref_maes_consts.restype = i64
+        L.evox_ref_maes_init.argtypes = [P, P, P, P, P]
+        L.evox_ref_maes_step.argtypes = [P, i64, i64, P, P, P, P, P, P, P, P, i64, P, P]
         L.evox_ref_de_init.argtypes = [P, P, P]
         L.evox_ref_de_step.argtypes = [P, i64, i64, P, P, P, P, P]
         L.evox_ref_cso_init.argtypes = [P, P, P, P]
@@ -83,7 +89,7 @@ def lib():
 
 
 def _ptr(a):
-    return a.ctypes.data_as(ctypes.c_void_p)
+    return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
 
 
 def _f32(a):
@@ -351,6 +357,62 @@ class PGPE:
                                       _ptr(self.fit), _ptr(self.rank), ctypes.byref(bf), ctypes.byref(bi))
         if rc != 0:
             raise ValueError(f"evox_ref_pgpe_step rc={rc}")
+        if n_gens > 0:
+            self.best_fit, self.best_idx = bf.value, bi.value
+        self.t += n_gens
+
+
+def maes_z(seed, t, k, j):
+    """The MA-ES deviate z_kj of sample k at generation t (fp64)."""
+    return lib().evox_ref_maes_z(seed, t, k, j)
+
+
+def maes_consts(N, D):
+    """(mu, weights[mu], dict of mu_eff, c_s, d_s, c_1, c_w, chi_D)."""
+    w = np.zeros(max(N // 2, 1), np.float64)
+    c = np.zeros(6, np.float64)
+    mu = lib().evox_ref_maes_consts(N, D, _ptr(w), _ptr(c))
+    if mu < 0:
+        raise ValueError("invalid MA-ES sizes")
+    return mu, w[:mu], dict(zip(("mu_eff", "c_s", "d_s", "c_1", "c_w", "chi"), c.tolist()))
+
+
+class MAES:
+    """Oracle MA-ES state: center y, step size sigma, transformation M [D, D],
+    evolution path s, generation t."""
+
+    def __init__(self, params: RefParams):
+        D = params.D
+        self.P = params
+        self.y = np.zeros(D, np.float32)
+        self.sigma = np.zeros(1, np.float32)
+        self.M = np.zeros((D, D), np.float32)
+        self.s = np.zeros(D, np.float32)
+        self.fit = np.zeros(params.N, np.float32)
+        self.rank = np.zeros(params.N, np.int64)
+        self.d = None
+        self.best_fit = float("nan")
+        self.best_idx = -1
+        self.t = 0
+        if lib().evox_ref_maes_init(ctypes.byref(self.P), _ptr(self.y), _ptr(self.sigma), _ptr(self.M),
+                                    _ptr(self.s)) != 0:
+            raise ValueError("evox_ref_maes_init failed")
+
+    def step(self, n_gens, rows=None, keep_d=False):
+        """n_gens generations; rows (one generation only) limits the update
+        of M to those rows; keep_d stores the last generation's d_k in .d."""
+        for a in (self.y, self.sigma, self.M, self.s):
+            assert a.flags.c_contiguous and a.dtype == np.float32
+        bf = ctypes.c_float(0.0)
+        bi = ctypes.c_int64(0)
+        r = None if rows is None else np.ascontiguousarray(rows, dtype=np.int64)
+        self.d = np.zeros((self.P.N, self.P.D), np.float32) if keep_d else None
+        rc = lib().evox_ref_maes_step(ctypes.byref(self.P), self.t, n_gens, _ptr(self.y), _ptr(self.sigma),
+                                      _ptr(self.M), _ptr(self.s), _ptr(self.fit), _ptr(self.rank),
+                                      ctypes.byref(bf), ctypes.byref(bi), 0 if r is None else r.size,
+                                      _ptr(r), _ptr(self.d))
+        if rc != 0:
+            raise ValueError(f"evox_ref_maes_step rc={rc}")
         if n_gens > 0:
             self.best_fit, self.best_idx = bf.value, bi.value
         self.t += n_gens

@@ -93,7 +93,8 @@ void evox_ref_u01_array(const uint32_t *w, int64_t n, float *out)
 
 /* Random-stream identifiers (the counter's fourth word). */
 enum { STREAM_INIT_X = 0, STREAM_INIT_V = 1, STREAM_PSO = 2, STREAM_CSO = 3,
-       STREAM_PERM = 4, STREAM_INIT_NORMAL = 5, STREAM_DE = 6, STREAM_ES = 7, STREAM_PGPE = 8 };
+       STREAM_PERM = 4, STREAM_INIT_NORMAL = 5, STREAM_DE = 6, STREAM_ES = 7, STREAM_PGPE = 8,
+       STREAM_MAES = 9 };
 
 /* Draw k of K for element (i, j) at generation t in stream s:
  * word (j mod 4) of Philox(seed, (K*floor(j/4) + k, i, t, s)). */
@@ -809,4 +810,189 @@ void evox_ref_gemm(int ta, int tb, int64_t M, int64_t N, int64_t K, float alpha,
             const double c = beta != 0.0f ? (double)beta * (double)C[i * ldc + j] : 0.0;
             C[i * ldc + j] = (float)((double)alpha * acc + c);
         }
+}
+
+/* ------------------------------------------------------------------------ */
+/* CMA-ES (Table II; the ES of the scaling experiment of Sec. V-A) in its    */
+/* matrix-adaptation form, MA-ES (Beyer and Sendhoff, IEEE TEVC 21(5),       */
+/* 2017): the transformation M with M M^T in the role of the covariance      */
+/* matrix is adapted directly, so sampling needs no eigendecomposition.      */
+/* State: center y [D], step size sigma, M [D x D] (identity at start),      */
+/* evolution path s [D] (zero at start), all fp32.                           */
+/* ------------------------------------------------------------------------ */
+
+/* z_kj of sample k at generation t: the Box-Muller deviate of
+ * Philox(seed, (floor(j/4), k, t, 9)). */
+double evox_ref_maes_z(uint64_t seed, int64_t t, int64_t k, int64_t j)
+{
+    return box_muller(seed, k, j, t, STREAM_MAES);
+}
+
+/* The default strategy constants for N = lambda samples in D dimensions
+ * (Hansen's CMA-ES defaults, which MA-ES keeps): mu = floor(lambda/2)
+ * parents; weights w_i proportional to ln(mu + 1/2) - ln i (i = 1..mu),
+ * summing to one; mu_eff = 1 / sum w_i^2;
+ *   c_s     = (mu_eff + 2) / (D + mu_eff + 5)
+ *   d_s     = 1 + c_s + 2 max(0, sqrt((mu_eff - 1) / (D + 1)) - 1)
+ *   c_1     = 2 / ((D + 1.3)^2 + mu_eff)
+ *   c_w     = min(1 - c_1, 2 (mu_eff - 2 + 1/mu_eff) / ((D + 2)^2 + mu_eff))
+ *   chi_D   = sqrt(D) (1 - 1/(4D) + 1/(21 D^2)), the expected length of a
+ *             standard normal vector in D dimensions.
+ * w (nullable) receives the mu weights; c the six numbers mu_eff, c_s, d_s,
+ * c_1, c_w, chi_D.  Returns mu, or -1 for N < 2 or D < 1. */
+int64_t evox_ref_maes_consts(int64_t N, int64_t D, double *w, double *c)
+{
+    if (N < 2 || D < 1) return -1;
+    const int64_t mu = N / 2;
+    double sw = 0.0, sw2 = 0.0;
+    for (int64_t i = 1; i <= mu; ++i) sw += log((double)mu + 0.5) - log((double)i);
+    for (int64_t i = 1; i <= mu; ++i) {
+        const double wi = (log((double)mu + 0.5) - log((double)i)) / sw;
+        if (w) w[i - 1] = wi;
+        sw2 += wi * wi;
+    }
+    const double n = (double)D, me = 1.0 / sw2;
+    const double cs = (me + 2.0) / (n + me + 5.0);
+    const double ds = 1.0 + cs + 2.0 * fmax(0.0, sqrt((me - 1.0) / (n + 1.0)) - 1.0);
+    const double c1 = 2.0 / ((n + 1.3) * (n + 1.3) + me);
+    const double cw = fmin(1.0 - c1, 2.0 * (me - 2.0 + 1.0 / me) / ((n + 2.0) * (n + 2.0) + me));
+    c[0] = me;
+    c[1] = cs;
+    c[2] = ds;
+    c[3] = c1;
+    c[4] = cw;
+    c[5] = sqrt(n) * (1.0 - 1.0 / (4.0 * n) + 1.0 / (21.0 * n * n));
+    return mu;
+}
+
+/* Initial state: y = row 0 of the uniform population (stream 0), sigma =
+ * es_sigma, M = I, s = 0. */
+int evox_ref_maes_init(const evox_ref_params *P, float *y, float *sigma, float *M, float *s)
+{
+    if (P->N < 2 || P->D < 1 || P->fn < 0 || P->fn >= FN_COUNT) return -1;
+    const int64_t D = P->D;
+    evox_ref_init_uniform(P->seed, STREAM_INIT_X, 1, D, P->lb, P->ub, y);
+    *sigma = P->es_sigma;
+    for (int64_t i = 0; i < D; ++i) {
+        s[i] = 0.0f;
+        for (int64_t j = 0; j < D; ++j) M[i * D + j] = i == j ? 1.0f : 0.0f;
+    }
+    return 0;
+}
+
+/* n_gens MA-ES generations from generation t0.  Each, with the constants of
+ * evox_ref_maes_consts:
+ *   z_k = (z_kj rounded to fp32), k < lambda
+ *   d_k = M z_k                      (fp64 sums, rounded to fp32)
+ *   x_k = y + sigma d_k              (fp32: fma(sigma, d_kj, y_j))
+ *   f_k = F(x_k); order the samples by (f_k, k) (NaN last, the argmin order)
+ *   <z>_w = sum_{i<mu} w_i z_{i:lambda},  <d>_w likewise   (fp64)
+ *   y  <- y + sigma <d>_w
+ *   s  <- (1 - c_s) s + sqrt(mu_eff c_s (2 - c_s)) <z>_w
+ *   M  <- M [I + c_1/2 (s s^T - I) + c_w/2 (sum_{i<mu} w_i z_{i:lambda}
+ *            z_{i:lambda}^T - I)]      (the new s; the bracket in fp64,
+ *                                      the product in fp64 per element)
+ *   sigma <- sigma exp(c_s/d_s (|s| / chi_D - 1))
+ * each new fp32 value rounded once from fp64.  M is row-major D x D.
+ * rows (nullable; n_gens must then be 1) restricts the update of M to the
+ * n_rows listed rows, the others keeping their old values.  fit, rank
+ * (nullable) receive the last generation's fitness and ranks, d_out
+ * (nullable, N x D) its d_k; (best_fit, best_idx) is its best sample. */
+int evox_ref_maes_step(const evox_ref_params *P, int64_t t0, int64_t n_gens, float *y, float *sigma,
+                       float *M, float *s, float *fit_out, int64_t *rank_out, float *best_fit,
+                       int64_t *best_idx, int64_t n_rows, const int64_t *rows, float *d_out)
+{
+    const int64_t N = P->N, D = P->D;
+    if (N < 2 || D < 1 || n_gens < 0 || P->fn < 0 || P->fn >= FN_COUNT) return -1;
+    if (rows && n_gens != 1) return -1;
+    double c[6];
+    double *w = (double *)malloc(sizeof(double) * (size_t)(N / 2));
+    const int64_t mu = evox_ref_maes_consts(N, D, w, c);
+    const double me = c[0], cs = c[1], ds = c[2], c1 = c[3], cw = c[4], chi = c[5];
+    float *z = (float *)malloc(sizeof(float) * (size_t)(N * D));
+    float *d = (float *)malloc(sizeof(float) * (size_t)(N * D));
+    float *x = (float *)malloc(sizeof(float) * (size_t)D);
+    float *f = (float *)malloc(sizeof(float) * (size_t)N);
+    int64_t *order = (int64_t *)malloc(sizeof(int64_t) * (size_t)N);
+    int64_t *rank = (int64_t *)malloc(sizeof(int64_t) * (size_t)N);
+    double *zw = (double *)malloc(sizeof(double) * (size_t)D);
+    double *dw = (double *)malloc(sizeof(double) * (size_t)D);
+    double *T = (double *)malloc(sizeof(double) * (size_t)(D * D));
+    double *row = (double *)malloc(sizeof(double) * (size_t)D);
+    if (!w || !z || !d || !x || !f || !order || !rank || !zw || !dw || !T || !row) {
+        free(w); free(z); free(d); free(x); free(f); free(order); free(rank); free(zw); free(dw);
+        free(T); free(row);
+        return -1;
+    }
+    for (int64_t t = t0; t < t0 + n_gens; ++t) {
+        /* sampling and evaluation */
+        for (int64_t k = 0; k < N; ++k)
+            for (int64_t j = 0; j < D; ++j) z[k * D + j] = (float)evox_ref_maes_z(P->seed, t, k, j);
+        for (int64_t k = 0; k < N; ++k) {
+            for (int64_t i = 0; i < D; ++i) {
+                double acc = 0.0;
+                for (int64_t j = 0; j < D; ++j) acc += (double)M[i * D + j] * (double)z[k * D + j];
+                d[k * D + i] = (float)acc;
+            }
+            for (int64_t i = 0; i < D; ++i) x[i] = fmaf(*sigma, d[k * D + i], y[i]);
+            f[k] = (float)evox_ref_eval_row_f64(P->fn, x, D);
+        }
+        for (int64_t i = 0; i < N; ++i) {
+            int64_t p = i;
+            while (p > 0 && better(f[i], i, f[order[p - 1]], order[p - 1])) {
+                order[p] = order[p - 1];
+                --p;
+            }
+            order[p] = i;
+        }
+        for (int64_t p = 0; p < N; ++p) rank[order[p]] = p;
+        /* recombination */
+        for (int64_t j = 0; j < D; ++j) {
+            zw[j] = dw[j] = 0.0;
+            for (int64_t r = 0; r < mu; ++r) {
+                zw[j] += w[r] * (double)z[order[r] * D + j];
+                dw[j] += w[r] * (double)d[order[r] * D + j];
+            }
+        }
+        const double sig = (double)*sigma;
+        const double cz = sqrt(me * cs * (2.0 - cs));
+        double s2 = 0.0;
+        for (int64_t j = 0; j < D; ++j) {
+            y[j] = (float)((double)y[j] + sig * dw[j]);
+            s[j] = (float)((1.0 - cs) * (double)s[j] + cz * zw[j]);
+            s2 += (double)s[j] * (double)s[j];
+        }
+        /* T = I + c_1/2 (s s^T - I) + c_w/2 (sum_r w_r z_r z_r^T - I) */
+        for (int64_t a = 0; a < D; ++a)
+            for (int64_t b = 0; b < D; ++b) {
+                double zz = 0.0;
+                for (int64_t r = 0; r < mu; ++r)
+                    zz += w[r] * (double)z[order[r] * D + a] * (double)z[order[r] * D + b];
+                const double id = a == b ? 1.0 : 0.0;
+                T[a * D + b] = id + 0.5 * c1 * ((double)s[a] * (double)s[b] - id) + 0.5 * cw * (zz - id);
+            }
+        /* M <- M T, row by row */
+        const int64_t nr = rows ? n_rows : D;
+        for (int64_t q = 0; q < nr; ++q) {
+            const int64_t i = rows ? rows[q] : q;
+            if (i < 0 || i >= D) continue;
+            for (int64_t b = 0; b < D; ++b) {
+                double acc = 0.0;
+                for (int64_t a = 0; a < D; ++a) acc += (double)M[i * D + a] * T[a * D + b];
+                row[b] = acc;
+            }
+            for (int64_t b = 0; b < D; ++b) M[i * D + b] = (float)row[b];
+        }
+        *sigma = (float)(sig * exp(cs / ds * (sqrt(s2) / chi - 1.0)));
+        if (t == t0 + n_gens - 1) {
+            if (fit_out) memcpy(fit_out, f, sizeof(float) * (size_t)N);
+            if (rank_out) memcpy(rank_out, rank, sizeof(int64_t) * (size_t)N);
+            if (d_out) memcpy(d_out, d, sizeof(float) * (size_t)(N * D));
+            *best_idx = order[0];
+            *best_fit = f[order[0]];
+        }
+    }
+    free(w); free(z); free(d); free(x); free(f); free(order); free(rank); free(zw); free(dw);
+    free(T); free(row);
+    return 0;
 }
