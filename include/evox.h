@@ -63,7 +63,7 @@ enum evox_fn {
     EVOX_SCHWEFEL = 5
 };
 
-enum evox_algo { EVOX_PSO = 0, EVOX_CSO = 1, EVOX_DE = 2, EVOX_ES = 3, EVOX_PGPE = 4 };
+enum evox_algo { EVOX_PSO = 0, EVOX_CSO = 1, EVOX_DE = 2, EVOX_ES = 3, EVOX_PGPE = 4, EVOX_MAES = 5 };
 
 enum evox_status {
     EVOX_OK = 0,
@@ -78,10 +78,11 @@ enum evox_status {
 
 /* Immutable hyperparameters (theta of Sec. IV-B), fixed at creation. */
 typedef struct evox_params {
-    int32_t algo;     /* EVOX_PSO, EVOX_CSO, EVOX_DE, EVOX_ES (OpenES) or EVOX_PGPE */
+    int32_t algo;     /* EVOX_PSO, EVOX_CSO, EVOX_DE, EVOX_ES (OpenES), EVOX_PGPE or EVOX_MAES
+                         (CMA-ES as matrix adaptation) */
     int32_t fn_id;    /* enum evox_fn */
     int64_t N;        /* population size: PSO 1 .. 2^31 - 1, CSO 2 .. 2^24, DE 4 .. 2^31 - 1,
-                         ES / PGPE even, 2 .. 16384 (N / 2 antithetic pairs) */
+                         ES / PGPE even, 2 .. 16384 (N / 2 antithetic pairs), MAES 2 .. 16384 */
     int64_t D;        /* dimension, 1 .. EVOX_MAX_D */
     int64_t ldx;      /* row pitch of x, v, pbest in floats: ldx >= D, ldx % 4 == 0 */
     float lb, ub;     /* x_init 0: initial positions ~ U[lb, ub): x = fma(u, ub - lb, lb);
@@ -96,7 +97,8 @@ typedef struct evox_params {
     float x_mu, x_sigma;
     float de_f;       /* DE differential weight F */
     float de_cr;      /* DE crossover rate CR */
-    float es_sigma;   /* ES perturbation scale sigma; PGPE initial deviation (every dimension) */
+    float es_sigma;   /* ES perturbation scale sigma; PGPE initial deviation (every dimension);
+                         MAES initial step size */
     float es_lr;      /* ES / PGPE center learning rate */
     float pgpe_sigma_lr;    /* PGPE deviation learning rate */
     float pgpe_max_change;  /* PGPE bound on a deviation's relative change per generation */
@@ -116,11 +118,17 @@ typedef struct evox_params {
  *        fitness of the last generation's samples; the rest unused.
  *   PGPE: as ES, and v [ldx] = the per-dimension deviations sigma (es_sigma
  *        at creation, padding 0).
+ *   MAES: x [ldx] = the center y (as ES), v [ldx] = the evolution path s
+ *        (zero at creation), mat [D][ldx] = the transformation matrix M
+ *        (identity at creation; M M^T plays the covariance matrix), sigma [1]
+ *        = the step size (es_sigma at creation), fit [N] = the last
+ *        generation's sample fitness; the rest unused.
  * Every array pointer must be 16-byte aligned.  scratch must hold
  * evox_scratch_bytes(params) bytes, 256-byte aligned, and must not be used by
  * anything else while the state exists. */
 typedef struct evox_buffers {
     float *x, *v, *pbest, *pfit, *fit, *gbest, *xbar;
+    float *mat, *sigma;  /* MAES only */
     void *scratch;
     size_t scratch_bytes;
 } evox_buffers;
@@ -241,6 +249,28 @@ int evox_es_step(evox_state *state, int64_t n_gens);
  * evox_best reports the best sample of the last generation and the center
  * mu as the solution. */
 int evox_pgpe_step(evox_state *state, int64_t n_gens);
+
+/* n_gens generations of CMA-ES (Table II; Sec. V-A runs it on Sphere up to
+ * D = 16384) in the matrix-adaptation form of Beyer and Sendhoff (IEEE TEVC
+ * 21(5), 2017), with Hansen's default constants: mu = floor(N/2) parents,
+ * weights w_i ~ ln(mu + 1/2) - ln i summing to one, mu_eff = 1 / sum w_i^2,
+ * c_s = (mu_eff + 2) / (D + mu_eff + 5), d_s = 1 + c_s + 2 max(0,
+ * sqrt((mu_eff - 1) / (D + 1)) - 1), c_1 = 2 / ((D + 1.3)^2 + mu_eff), c_w =
+ * min(1 - c_1, 2 (mu_eff - 2 + 1/mu_eff) / ((D + 2)^2 + mu_eff)), chi_D =
+ * sqrt(D) (1 - 1/(4D) + 1/(21 D^2)).  Generation t:
+ *   - deviates z_kj from Philox(seed, (floor(j/4), k, t, 9)) (the Box-Muller
+ *     layout of evox_fill_normal), steps d_k = M z_k (fp32 matrix-core
+ *     product), samples fma(sigma, d_kj, y_j), fit = F(samples);
+ *   - parents: the mu best in the argmin order;
+ *   - y <- y + sigma sum w_i d_i, s <- (1 - c_s) s + sqrt(mu_eff c_s (2 - c_s))
+ *     sum w_i z_i (fp64 sums, one rounding);
+ *   - M <- M [I + c_1/2 (s s^T - I) + c_w/2 (sum w_i z_i z_i^T - I)],
+ *     computed as (1 - (c_1 + c_w)/2) M + c_1/2 (M s) s^T + c_w/2 sum w_i d_i
+ *     z_i^T (fp32 matrix-core product over mu + 1 terms);
+ *   - sigma <- sigma exp(c_s/d_s (|s| / chi_D - 1)).
+ * evox_best reports the best sample of the last generation and the center y
+ * as the solution. */
+int evox_maes_step(evox_state *state, int64_t n_gens);
 
 /* If the caller has changed x (or fit) of a CSO state, recompute xbar from x
  * and, when refit is nonzero, fit = F(x). */

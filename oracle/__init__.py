@@ -76,6 +76,7 @@ def lib():
         L.evox_ref_pgpe_step.argtypes = [P, i64, i64, P, P, P, P, P, P]
         L.evox_ref_maes_z.argtypes = [u64, i64, i64, i64]
         L.evox_ref_maes_z.restype = ctypes.c_double
+        L.evox_ref_maes_deviates.argtypes = [u64, i64, i64, i64, P]
         L.evox_ref_maes_consts.argtypes = [i64, i64, P, P]
         L.evox_ref_maes_consts.restype = i64
         L.evox_ref_maes_init.argtypes = [P, P, P, P, P]
@@ -365,6 +366,13 @@ class PGPE:
 def maes_z(seed, t, k, j):
     """The MA-ES deviate z_kj of sample k at generation t (fp64)."""
     return lib().evox_ref_maes_z(seed, t, k, j)
+
+
+def maes_deviates(seed, t, N, D):
+    """The generation's deviates z [N, D], rounded to fp32 as the step uses them."""
+    z = np.zeros((N, D), np.float32)
+    lib().evox_ref_maes_deviates(seed, t, N, D, _ptr(z))
+    return z
 
 
 def maes_consts(N, D):

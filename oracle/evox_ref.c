@@ -828,6 +828,13 @@ double evox_ref_maes_z(uint64_t seed, int64_t t, int64_t k, int64_t j)
     return box_muller(seed, k, j, t, STREAM_MAES);
 }
 
+/* The deviates of one generation rounded to fp32, z[k * D + j] = z_kj. */
+void evox_ref_maes_deviates(uint64_t seed, int64_t t, int64_t N, int64_t D, float *z)
+{
+    for (int64_t k = 0; k < N; ++k)
+        for (int64_t j = 0; j < D; ++j) z[k * D + j] = (float)evox_ref_maes_z(seed, t, k, j);
+}
+
 /* The default strategy constants for N = lambda samples in D dimensions
  * (Hansen's CMA-ES defaults, which MA-ES keeps): mu = floor(lambda/2)
  * parents; weights w_i proportional to ln(mu + 1/2) - ln i (i = 1..mu),
@@ -926,8 +933,7 @@ int evox_ref_maes_step(const evox_ref_params *P, int64_t t0, int64_t n_gens, flo
     }
     for (int64_t t = t0; t < t0 + n_gens; ++t) {
         /* sampling and evaluation */
-        for (int64_t k = 0; k < N; ++k)
-            for (int64_t j = 0; j < D; ++j) z[k * D + j] = (float)evox_ref_maes_z(P->seed, t, k, j);
+        evox_ref_maes_deviates(P->seed, t, N, D, z);
         for (int64_t k = 0; k < N; ++k) {
             for (int64_t i = 0; i < D; ++i) {
                 double acc = 0.0;

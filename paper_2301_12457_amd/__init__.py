@@ -15,7 +15,7 @@ LIB_PATH = os.path.join(HERE, "libevox.so")
 SPHERE, ACKLEY, RASTRIGIN, GRIEWANK, ROSENBROCK, SCHWEFEL = range(6)
 FN_IDS = {"sphere": SPHERE, "ackley": ACKLEY, "rastrigin": RASTRIGIN, "griewank": GRIEWANK,
           "rosenbrock": ROSENBROCK, "schwefel": SCHWEFEL}
-PSO, CSO, DE, ES, PGPE = 0, 1, 2, 3, 4
+PSO, CSO, DE, ES, PGPE, MAES = 0, 1, 2, 3, 4, 5
 OK, EINVAL, EHIP, ENOSPC, EALIGN = 0, -1, -2, -3, -4
 MAX_D = 32768
 
@@ -23,7 +23,7 @@ MAX_D = 32768
 EXPORTS = (
     "evox_scratch_bytes", "evox_state_create", "evox_state_destroy", "evox_eval", "evox_eval_ld",
     "evox_eval_argmin_scratch_bytes", "evox_eval_argmin", "evox_pso_step", "evox_cso_step",
-    "evox_de_step", "evox_es_step", "evox_pgpe_step",
+    "evox_de_step", "evox_es_step", "evox_pgpe_step", "evox_maes_step",
     "evox_cso_refresh", "evox_best", "evox_generation", "evox_row_layout", "evox_default_ldx",
     "evox_fill_normal", "evox_sgemm", "evox_copy", "evox_philox_fill", "evox_permutation_scratch_bytes",
     "evox_permutation", "evox_argsort_u32",
@@ -55,7 +55,8 @@ class Params(ctypes.Structure):
 
 
 class Buffers(ctypes.Structure):
-    _fields_ = [(n, ctypes.c_void_p) for n in ("x", "v", "pbest", "pfit", "fit", "gbest", "xbar")] + [
+    _fields_ = [(n, ctypes.c_void_p) for n in ("x", "v", "pbest", "pfit", "fit", "gbest", "xbar", "mat",
+                                                "sigma")] + [
         ("scratch", ctypes.c_void_p), ("scratch_bytes", ctypes.c_size_t)]
 
 
@@ -85,6 +86,7 @@ def lib():
             "evox_de_step": ([P, i64], i32),
             "evox_es_step": ([P, i64], i32),
             "evox_pgpe_step": ([P, i64], i32),
+            "evox_maes_step": ([P, i64], i32),
             "evox_cso_refresh": ([P, i32], i32),
             "evox_best": ([P, P, P, P], i32),
             "evox_generation": ([P], i64),
@@ -227,13 +229,14 @@ def evox_scratch_bytes(params):
 
 
 class Swarm:
-    """A PSO, CSO, DE, OpenES or PGPE state over torch-allocated device buffers.
+    """A PSO, CSO, DE, OpenES, PGPE or MA-ES state over torch-allocated device buffers.
 
     x, v (and pbest) are [N, ldx] float32 tensors whose first D columns are the
     population; pfit / fit are [N]; gbest / xbar are [ldx].  DE has x and fit
     only (its second population buffer lives in the scratch); ES has x = the
     center theta [ldx] and fit = the last generation's sample fitness [N];
-    PGPE also v = the per-dimension deviations [ldx].
+    PGPE also v = the per-dimension deviations [ldx].  MA-ES has x = the center
+    y [ldx], v = the path s [ldx], mat = M [D, ldx], sigma [1] and fit [N].
     """
 
     def __init__(self, params: Params, device="cuda", stream=None):
@@ -243,11 +246,13 @@ class Swarm:
         N, ldx = params.N, params.ldx
         f32 = dict(dtype=torch.float32, device=device)
         # ES / PGPE: x is the center (one row); PGPE: v the deviations (one row)
-        one_row = params.algo in (ES, PGPE)
+        one_row = params.algo in (ES, PGPE, MAES)
         self.x = torch.empty((ldx,) if one_row else (N, ldx), **f32)
         self.v = (torch.empty((N, ldx), **f32) if params.algo in (PSO, CSO)
-                  else torch.empty((ldx,), **f32) if params.algo == PGPE else None)
-        if params.algo in (DE, ES, PGPE):
+                  else torch.empty((ldx,), **f32) if params.algo in (PGPE, MAES) else None)
+        self.mat = torch.empty((params.D, ldx), **f32) if params.algo == MAES else None
+        self.sigma = torch.empty((1,), **f32) if params.algo == MAES else None
+        if params.algo in (DE, ES, PGPE, MAES):
             self.pbest = self.pfit = self.gbest = self.xbar = None
             self.fit = torch.empty((N,), **f32)
         elif params.algo == PSO:
@@ -266,7 +271,8 @@ class Swarm:
         self.scratch = torch.empty((nbytes + 255) // 256 * 256 // 4, dtype=torch.int32, device=device)
         self.buffers = Buffers(x=_ptr(self.x), v=_ptr(self.v), pbest=_ptr(self.pbest),
                                pfit=_ptr(self.pfit), fit=_ptr(self.fit), gbest=_ptr(self.gbest),
-                               xbar=_ptr(self.xbar), scratch=_ptr(self.scratch),
+                               xbar=_ptr(self.xbar), mat=_ptr(self.mat), sigma=_ptr(self.sigma),
+                               scratch=_ptr(self.scratch),
                                scratch_bytes=self.scratch.numel() * 4)
         self.handle = ctypes.c_void_p()
         _check(lib().evox_state_create(ctypes.byref(self.P), ctypes.byref(self.buffers),
@@ -295,8 +301,10 @@ class Swarm:
             _check(lib().evox_de_step(self.handle, n_gens))
         elif self.P.algo == ES:
             _check(lib().evox_es_step(self.handle, n_gens))
-        else:
+        elif self.P.algo == PGPE:
             _check(lib().evox_pgpe_step(self.handle, n_gens))
+        else:
+            _check(lib().evox_maes_step(self.handle, n_gens))
 
     def refresh(self, refit=True):
         _check(lib().evox_cso_refresh(self.handle, 1 if refit else 0))

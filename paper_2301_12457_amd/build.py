@@ -37,6 +37,7 @@ def _units():
         units.append((os.path.join(CSRC, "evox_fn.hip"), f"evox_fn{fn}.o", [f"-DEVOX_FN={fn}"]))
     units.append((os.path.join(CSRC, "evox_common.hip"), "evox_common.o", []))
     units.append((os.path.join(CSRC, "evox_gemm.hip"), "evox_gemm.o", []))
+    units.append((os.path.join(CSRC, "evox_maes.hip"), "evox_maes.o", []))
     units.append((os.path.join(CSRC, "evox_api.cpp"), "evox_api.o", ["-x", "hip"]))
     return units
 

@@ -73,14 +73,33 @@ struct Plan {
     int perm_batch = 0;
     size_t x2 = 0, fit2 = 0;  // DE: the other population buffer and its fitness
     size_t esrank = 0, espart = 0;  // ES: sample ranks, gradient partial sums
+    // MA-ES: deviates, steps, split-K workspace, update factors, parents,
+    // weights, path-norm partial sums
+    size_t mae_z = 0, mae_d = 0, mae_work = 0, mae_at = 0, mae_bt = 0, mae_sel = 0, mae_w = 0, mae_part = 0;
+    int mae_splits = 1;
+    int64_t mae_mu = 0, mae_kp = 0;
     size_t total = 0;
 };
+
+// K-slices of the sampling product (N + 1) x D x D: enough blocks to fill the
+// chip (the 128-row tiles of a small population give few), each slice at
+// least 256 deep.
+int mae_splits(int64_t N, int64_t D)
+{
+    const int64_t rows = N + 1, bm = rows <= 64 ? 64 : 128, bn = rows <= 128 ? 64 : 128;
+    const int64_t tiles = ((D + bn - 1) / bn) * ((rows + bm - 1) / bm);
+    int64_t sp = (1024 + tiles - 1) / tiles;
+    const int64_t deep = D / 256 > 1 ? D / 256 : 1;
+    if (sp > deep) sp = deep;
+    if (sp > 16) sp = 16;
+    return (int)(sp < 1 ? 1 : sp);
+}
 
 int make_plan(const evox_params *P, Plan *pl)
 {
     if (!P) return fail(EVOX_EINVAL, "params is null");
     if (P->algo != EVOX_PSO && P->algo != EVOX_CSO && P->algo != EVOX_DE && P->algo != EVOX_ES &&
-        P->algo != EVOX_PGPE)
+        P->algo != EVOX_PGPE && P->algo != EVOX_MAES)
         return fail(EVOX_EINVAL, "unknown algo %d", P->algo);
     const bool es_like = P->algo == EVOX_ES || P->algo == EVOX_PGPE;
     if (P->fn_id < 0 || P->fn_id >= FN_COUNT) return fail(EVOX_EINVAL, "unknown fn_id %d", P->fn_id);
@@ -93,6 +112,8 @@ int make_plan(const evox_params *P, Plan *pl)
         return fail(EVOX_EINVAL, "CSO N = %lld above %lld", (long long)P->N, (long long)kCsoMaxN);
     if (es_like && (P->N < 2 || (P->N & 1) || P->N > kEsMaxN))
         return fail(EVOX_EINVAL, "ES / PGPE N = %lld must be even, in [2, %d]", (long long)P->N, kEsMaxN);
+    if (P->algo == EVOX_MAES && (P->N < 2 || P->N > kEsMaxN))
+        return fail(EVOX_EINVAL, "MAES N = %lld out of range [2, %d]", (long long)P->N, kEsMaxN);
     if (P->ldx < P->D || (P->ldx & 3))
         return fail(EVOX_EINVAL, "ldx = %lld must be >= D and a multiple of 4", (long long)P->ldx);
     if (P->x_init != 0 && P->x_init != 1) return fail(EVOX_EINVAL, "unknown x_init %d", P->x_init);
@@ -138,6 +159,21 @@ int make_plan(const evox_params *P, Plan *pl)
         p.esrank = take(sizeof(uint32_t) * 2 * H);
         p.espart = take(sizeof(double) * sums * chunks * 4 * (size_t)((P->D + 3) / 4));
     }
+    if (P->algo == EVOX_MAES) {
+        const size_t rows = (size_t)P->N + 1, D = (size_t)P->D;
+        p.mae_mu = P->N / 2;
+        p.mae_kp = (p.mae_mu + 1 + 3) / 4 * 4;
+        p.mae_splits = mae_splits(P->N, P->D);
+        p.mae_z = take(sizeof(float) * rows * (size_t)P->ldx);
+        p.mae_d = take(sizeof(float) * rows * (size_t)P->ldx);
+        p.mae_work = p.mae_splits > 1 ? take(sizeof(float) * (size_t)p.mae_splits * rows * D) : 0;
+        p.mae_at = take(sizeof(float) * D * (size_t)p.mae_kp);
+        p.mae_bt = take(sizeof(float) * D * (size_t)p.mae_kp);
+        p.esrank = take(sizeof(uint32_t) * (size_t)P->N);
+        p.mae_sel = take(sizeof(int32_t) * (size_t)p.mae_mu);
+        p.mae_w = take(sizeof(double) * (size_t)p.mae_mu);
+        p.mae_part = take(sizeof(double) * ((D + kMaeBlock - 1) / kMaeBlock));
+    }
     p.total = off;
     *pl = p;
     return EVOX_OK;
@@ -160,6 +196,10 @@ struct evox_state {
     float *x2, *fit2;  // DE: the other population buffer
     uint32_t *esrank;  // ES: sample ranks
     double *espart;    // ES: gradient partial sums
+    MaeArgs mae;       // MA-ES: the generation's buffers and constants (t set per generation)
+    float mae_beta;    // 1 - (c_1 + c_w) / 2
+    float *mae_work;
+    std::vector<double> mae_w;  // the weights, host copy of the device table
     // profiling of the fused generation kernel
     bool prof;
     std::vector<std::pair<hipEvent_t, hipEvent_t>> ev;
@@ -276,13 +316,15 @@ int evox_state_create(const evox_params *params, const evox_buffers *b, void *hi
     if (!b) return fail(EVOX_EINVAL, "buffers is null");
     if (!b->x || !b->scratch) return fail(EVOX_EINVAL, "x and scratch are required");
     if ((P.algo == EVOX_PSO || P.algo == EVOX_CSO) && !b->v) return fail(EVOX_EINVAL, "PSO and CSO need v");
-    if ((P.algo == EVOX_DE || P.algo == EVOX_ES || P.algo == EVOX_PGPE) && !b->fit)
-        return fail(EVOX_EINVAL, "DE, ES and PGPE need fit");
+    if ((P.algo == EVOX_DE || P.algo == EVOX_ES || P.algo == EVOX_PGPE || P.algo == EVOX_MAES) && !b->fit)
+        return fail(EVOX_EINVAL, "DE, ES, PGPE and MAES need fit");
+    if (P.algo == EVOX_MAES && (!b->v || !b->mat || !b->sigma))
+        return fail(EVOX_EINVAL, "MAES needs v (the path), mat and sigma");
     if (P.algo == EVOX_PGPE && !b->v) return fail(EVOX_EINVAL, "PGPE needs v (the deviations)");
     if (P.algo == EVOX_PSO && (!b->pbest || !b->pfit || !b->gbest))
         return fail(EVOX_EINVAL, "PSO needs pbest, pfit and gbest");
     if (P.algo == EVOX_CSO && (!b->fit || !b->xbar)) return fail(EVOX_EINVAL, "CSO needs fit and xbar");
-    const void *ptrs[] = {b->x, b->v, b->pbest, b->pfit, b->fit, b->gbest, b->xbar};
+    const void *ptrs[] = {b->x, b->v, b->pbest, b->pfit, b->fit, b->gbest, b->xbar, b->mat, b->sigma};
     for (const void *p : ptrs)
         if (p && !aligned16(p)) return fail(EVOX_EALIGN, "buffer %p is not 16-byte aligned", p);
     if (((uintptr_t)b->scratch & 255u) != 0) return fail(EVOX_EALIGN, "scratch is not 256-byte aligned");
@@ -314,6 +356,53 @@ int evox_state_create(const evox_params *params, const evox_buffers *b, void *hi
         s->x2 = at<float>(b->scratch, pl.x2);
         s->fit2 = at<float>(b->scratch, pl.fit2);
     }
+    s->mae = MaeArgs{};
+    s->mae_beta = 1.0f;
+    s->mae_work = nullptr;
+    if (P.algo == EVOX_MAES) {
+        // Hansen's default strategy constants for N samples in D dimensions
+        const int64_t mu = pl.mae_mu;
+        const double n = (double)P.D;
+        double sw = 0.0, sw2 = 0.0;
+        s->mae_w.resize((size_t)mu);
+        for (int64_t i = 0; i < mu; ++i) sw += std::log((double)mu + 0.5) - std::log((double)(i + 1));
+        for (int64_t i = 0; i < mu; ++i) {
+            s->mae_w[(size_t)i] = (std::log((double)mu + 0.5) - std::log((double)(i + 1))) / sw;
+            sw2 += s->mae_w[(size_t)i] * s->mae_w[(size_t)i];
+        }
+        const double me = 1.0 / sw2, cs = (me + 2.0) / (n + me + 5.0);
+        const double ds = 1.0 + cs + 2.0 * std::fmax(0.0, std::sqrt((me - 1.0) / (n + 1.0)) - 1.0);
+        const double c1 = 2.0 / ((n + 1.3) * (n + 1.3) + me);
+        const double cw = std::fmin(1.0 - c1, 2.0 * (me - 2.0 + 1.0 / me) / ((n + 2.0) * (n + 2.0) + me));
+        MaeArgs &m = s->mae;
+        m.Z = at<float>(b->scratch, pl.mae_z);
+        m.Dm = at<float>(b->scratch, pl.mae_d);
+        m.N = P.N;
+        m.D = P.D;
+        m.ldx = P.ldx;
+        m.mu = mu;
+        m.kp = pl.mae_kp;
+        s->esrank = at<uint32_t>(b->scratch, pl.esrank);
+        m.rank = s->esrank;
+        m.sel = at<int32_t>(b->scratch, pl.mae_sel);
+        m.w = at<double>(b->scratch, pl.mae_w);
+        m.y = b->x;
+        m.s = b->v;
+        m.sigma = b->sigma;
+        m.At = at<float>(b->scratch, pl.mae_at);
+        m.Bt = at<float>(b->scratch, pl.mae_bt);
+        m.part = at<double>(b->scratch, pl.mae_part);
+        m.cs = cs;
+        m.cz = std::sqrt(me * cs * (2.0 - cs));
+        m.hc1 = 0.5 * c1;
+        m.hcw = 0.5 * cw;
+        m.damp = cs / ds;
+        m.chi = std::sqrt(n) * (1.0 - 1.0 / (4.0 * n) + 1.0 / (21.0 * n * n));
+        m.k0 = s->k0;
+        m.k1 = s->k1;
+        s->mae_beta = (float)(1.0 - 0.5 * (c1 + cw));
+        if (pl.mae_splits > 1) s->mae_work = at<float>(b->scratch, pl.mae_work);
+    }
     if (P.algo == EVOX_CSO) {
         s->hist = at<uint32_t>(b->scratch, pl.hist);
         s->offs = at<uint32_t>(b->scratch, pl.offs);
@@ -342,7 +431,7 @@ int evox_state_create(const evox_params *params, const evox_buffers *b, void *hi
     hipError_t e;
     // ES / PGPE: x is the center, one row
     const bool own_v = P.algo == EVOX_PSO || P.algo == EVOX_CSO;
-    const bool es_like = P.algo == EVOX_ES || P.algo == EVOX_PGPE;
+    const bool es_like = P.algo == EVOX_ES || P.algo == EVOX_PGPE || P.algo == EVOX_MAES;
     InitArgs ia{b->x, own_v ? b->v : nullptr, P.algo == EVOX_PSO ? b->pbest : nullptr,
                 es_like ? 1 : P.N, P.D, P.ldx, P.lb, P.ub,
                 P.v_lo, P.v_hi, P.v_lo == 0.0f && P.v_hi == 0.0f, P.x_init == 1, P.x_mu, P.x_sigma,
@@ -367,6 +456,17 @@ int evox_state_create(const evox_params *params, const evox_buffers *b, void *hi
         if ((e = best_init(s, std::numeric_limits<float>::infinity(), 0)) != hipSuccess ||
             (P.algo == EVOX_PGPE && (e = launch_fill(b->v, P.ldx, 0.0f, s->stream)) != hipSuccess) ||
             (P.algo == EVOX_PGPE && (e = launch_fill(b->v, P.D, P.es_sigma, s->stream)) != hipSuccess)) {
+            delete s;
+            return hip_fail(e, "init");
+        }
+        // MA-ES: s = 0, M = I, sigma = es_sigma, the weight table
+        if (P.algo == EVOX_MAES &&
+            ((e = launch_fill(b->v, P.ldx, 0.0f, s->stream)) != hipSuccess ||
+             (e = launch_mae_identity(b->mat, P.D, P.ldx, s->stream)) != hipSuccess ||
+             (e = launch_fill(b->sigma, 1, P.es_sigma, s->stream)) != hipSuccess ||
+             (e = hipMemcpyAsync((void *)s->mae.w, s->mae_w.data(), sizeof(double) * s->mae_w.size(),
+                                 hipMemcpyHostToDevice, s->stream)) != hipSuccess ||
+             (e = hipStreamSynchronize(s->stream)) != hipSuccess)) {
             delete s;
             return hip_fail(e, "init");
         }
@@ -593,6 +693,40 @@ int es_generations(evox_state *s, int64_t n_gens, bool pgpe)
     return EVOX_OK;
 }
 
+int mae_generations(evox_state *s, int64_t n_gens)
+{
+    if (n_gens < 0) return fail(EVOX_EINVAL, "n_gens = %lld < 0", (long long)n_gens);
+    if (s->t + n_gens >= ((int64_t)1 << 32)) return fail(EVOX_EINVAL, "generation counter would pass 2^32");
+    if (n_gens == 0) return EVOX_OK;
+    const evox_params &P = s->P;
+    const Plan &pl = s->pl;
+    MaeArgs m = s->mae;
+    // the sampling product Dm = Z M^T ((N + 1) x D over K = D) and the update
+    // M <- beta M + At Bt^T (D x D over K = mu + 1)
+    const GemmArgs sample{P.N + 1, P.D, P.D, 1.0f, m.Z, P.ldx, s->B.mat, P.ldx, 0.0f, m.Dm, P.ldx};
+    const GemmArgs update{P.D, P.D, m.mu + 1, 1.0f, m.At, m.kp, m.Bt, m.kp, s->mae_beta, s->B.mat, P.ldx};
+    hipError_t e;
+    for (int64_t k = 0; k < n_gens; ++k) {
+        m.t = (uint32_t)(s->t + k);
+        MaeEvalArgs ea{s->B.x, m.Dm, P.ldx, s->B.sigma, s->B.fit, s->esrank, P.N, P.D,
+                       k == n_gens - 1 ? s->slots : nullptr};
+        if ((e = launch_mae_sample(m, s->stream)) != hipSuccess) return hip_fail(e, "deviates");
+        if ((e = timed(s, [&] { return launch_gemm_nt(sample, pl.mae_splits, s->mae_work, s->stream); })) !=
+            hipSuccess)
+            return hip_fail(e, "sampling product");
+        if ((e = launch_mae_eval(P.fn_id, pl.L, ea, pl.grid, s->stream)) != hipSuccess)
+            return hip_fail(e, "samples");
+        if ((e = launch_es_rank(s->B.fit, P.N, s->esrank, s->stream)) != hipSuccess) return hip_fail(e, "ranks");
+        if ((e = launch_mae_select(m, s->stream)) != hipSuccess) return hip_fail(e, "parents");
+        if ((e = launch_mae_recombine(m, s->stream)) != hipSuccess) return hip_fail(e, "recombination");
+        if ((e = launch_gemm_nt(update, 1, nullptr, s->stream)) != hipSuccess) return hip_fail(e, "matrix update");
+    }
+    if ((e = launch_select(s->slots, nullptr, 0, nullptr, s->best, nullptr, nullptr, s->stream)) != hipSuccess)
+        return hip_fail(e, "select");
+    s->t += n_gens;
+    return EVOX_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -609,6 +743,13 @@ int evox_pgpe_step(evox_state *s, int64_t n_gens)
     if (!s) return fail(EVOX_EINVAL, "state is null");
     if (s->P.algo != EVOX_PGPE) return fail(EVOX_EINVAL, "evox_pgpe_step on a state of another algorithm");
     return es_generations(s, n_gens, true);
+}
+
+int evox_maes_step(evox_state *s, int64_t n_gens)
+{
+    if (!s) return fail(EVOX_EINVAL, "state is null");
+    if (s->P.algo != EVOX_MAES) return fail(EVOX_EINVAL, "evox_maes_step on a state of another algorithm");
+    return mae_generations(s, n_gens);
 }
 
 int evox_cso_refresh(evox_state *s, int refit)
@@ -628,9 +769,8 @@ int evox_best(evox_state *s, float *best_fit, int64_t *best_idx, float *best_x_h
     if (best_fit) *best_fit = h.f;
     if (best_idx) *best_idx = h.i;
     if (best_x_host) {
-        const float *src = s->P.algo == EVOX_PSO                                ? s->B.gbest
-                           : s->P.algo == EVOX_ES || s->P.algo == EVOX_PGPE ? s->B.x
-                                                                              : s->B.x + h.i * s->P.ldx;
+        const bool center = s->P.algo == EVOX_ES || s->P.algo == EVOX_PGPE || s->P.algo == EVOX_MAES;
+        const float *src = s->P.algo == EVOX_PSO ? s->B.gbest : center ? s->B.x : s->B.x + h.i * s->P.ldx;
         e = hipMemcpyAsync(best_x_host, src, sizeof(float) * (size_t)s->P.D, hipMemcpyDeviceToHost, s->stream);
         if (e == hipSuccess) e = hipStreamSynchronize(s->stream);
         if (e != hipSuccess) return hip_fail(e, "read best row");
@@ -657,7 +797,7 @@ int64_t evox_default_ldx(int32_t algo, int64_t D)
 {
     if (D < 1 || D > EVOX_MAX_D) return 0;
     const int64_t line = (D + 31) / 32 * 32, quad = (D + 3) / 4 * 4;
-    if (algo == EVOX_PSO || algo == EVOX_DE || algo == EVOX_ES || algo == EVOX_PGPE)
+    if (algo == EVOX_PSO || algo == EVOX_DE || algo == EVOX_ES || algo == EVOX_PGPE || algo == EVOX_MAES)
         return D >= 512 ? line : quad;
     if (algo == EVOX_CSO) return D >= 64 ? line : quad;
     return 0;

@@ -591,6 +591,12 @@ hipError_t launch_es_eval(int fn, Layout L, const EsArgs &a, int grid, hipStream
     EVOX_FN_SWITCH(EVOX_CALL_ES)
 }
 
+hipError_t launch_mae_eval(int fn, Layout L, const MaeEvalArgs &a, int grid, hipStream_t s)
+{
+#define EVOX_CALL_MAE(F) launch_mae_eval_t<F>(L, a, grid, s)
+    EVOX_FN_SWITCH(EVOX_CALL_MAE)
+}
+
 // ---------------------------------------------------------------------------
 // OpenES centered ranks: rank_i = #{j : key_j < key_i} with key = (orderable
 // fitness, index), the argmin order, so the ranks are a permutation and NaN

@@ -121,11 +121,162 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs g)
             }
 }
 
+// ---------------------------------------------------------------------------
+// C = alpha A B^T + beta C with A [M x K] and B [N x K] both K-contiguous, the
+// layout of the two contractions of the matrix-adaptation ES (samples times
+// M^T, and the rank-mu update).  Block tile BM x BN (BM, BN in {64, 128}),
+// 2 x 2 waves of (BM/2) x (BN/2), each a grid of 32x32x2 MFMA accumulators;
+// K in tiles of 32, each staged in LDS row-major ([row][k], rows padded to 36
+// floats so that every row starts 16-byte aligned) after being prefetched
+// into registers while the previous tile is multiplied.  Within a tile, lane
+// half h = l / 32 takes k = 16 h + step (steps 0..15), so each lane reads its
+// operands as float4 runs along k; the order in which the products are summed
+// is fixed.
+// Split-K (gridDim.z = splits): block z sums k in [z kc, (z + 1) kc) and, with
+// a workspace, stores its raw partial tile there; k_splitk_reduce then adds
+// the partials in order z = 0, 1, ... and applies alpha and beta.  Without a
+// workspace (one split) the block applies alpha and beta itself.
+// ---------------------------------------------------------------------------
+constexpr int kNtBK = 32, kNtLD = kNtBK + 4;
+
+template <int BM, int BN>
+__global__ __launch_bounds__(256) void k_gemm_nt(GemmArgs g, float *work, int64_t kc)
+{
+    constexpr int TM = BM / 64, TN = BN / 64;            // 32x32 tiles per wave
+    constexpr int QA = BM * kNtBK / 4 / 256, QB = BN * kNtBK / 4 / 256;  // float4 per thread
+    __shared__ float As[BM * kNtLD];
+    __shared__ float Bs[BN * kNtLD];
+    const int tid = threadIdx.x, wave = tid / 64, lane = tid % 64, col = lane % 32, h = lane / 32;
+    const int wm = wave / 2, wn = wave % 2;
+    const int64_t i0 = (int64_t)blockIdx.y * BM, j0 = (int64_t)blockIdx.x * BN;
+    const int64_t kb = (int64_t)blockIdx.z * kc, ke = kb + kc < g.K ? kb + kc : g.K;
+    float4 ra[QA], rb[QB];
+    auto load = [&](int64_t k0) {
+#pragma unroll
+        for (int q = 0; q < QA; ++q) {
+            const int idx = tid + 256 * q, row = idx / 8, c4 = idx % 8;
+            ra[q] = quad_or_zero(g.A, g.lda, i0 + row, k0 + 4 * c4, g.M, ke);
+        }
+#pragma unroll
+        for (int q = 0; q < QB; ++q) {
+            const int idx = tid + 256 * q, row = idx / 8, c4 = idx % 8;
+            rb[q] = quad_or_zero(g.B, g.ldb, j0 + row, k0 + 4 * c4, g.N, ke);
+        }
+    };
+    auto store = [&]() {
+#pragma unroll
+        for (int q = 0; q < QA; ++q) {
+            const int idx = tid + 256 * q, row = idx / 8, c4 = idx % 8;
+            *reinterpret_cast<float4 *>(&As[row * kNtLD + 4 * c4]) = ra[q];
+        }
+#pragma unroll
+        for (int q = 0; q < QB; ++q) {
+            const int idx = tid + 256 * q, row = idx / 8, c4 = idx % 8;
+            *reinterpret_cast<float4 *>(&Bs[row * kNtLD + 4 * c4]) = rb[q];
+        }
+    };
+    f32x16 acc[TM][TN];
+#pragma unroll
+    for (int m = 0; m < TM; ++m)
+#pragma unroll
+        for (int n = 0; n < TN; ++n)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) acc[m][n][v] = 0.0f;
+
+    if (kb < ke) {
+        load(kb);
+        store();
+        __syncthreads();
+        for (int64_t k0 = kb; k0 < ke; k0 += kNtBK) {
+            const bool more = k0 + kNtBK < ke;
+            if (more) load(k0 + kNtBK);
+#pragma unroll
+            for (int c = 0; c < 4; ++c) {
+                float4 a4[TM], b4[TN];
+#pragma unroll
+                for (int m = 0; m < TM; ++m)
+                    a4[m] = *reinterpret_cast<const float4 *>(&As[(wm * TM * 32 + m * 32 + col) * kNtLD + h * 16 + 4 * c]);
+#pragma unroll
+                for (int n = 0; n < TN; ++n)
+                    b4[n] = *reinterpret_cast<const float4 *>(&Bs[(wn * TN * 32 + n * 32 + col) * kNtLD + h * 16 + 4 * c]);
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+#pragma unroll
+                    for (int m = 0; m < TM; ++m)
+#pragma unroll
+                        for (int n = 0; n < TN; ++n)
+                            acc[m][n] = __builtin_amdgcn_mfma_f32_32x32x2f32(comp(a4[m], e), comp(b4[n], e),
+                                                                             acc[m][n], 0, 0, 0);
+            }
+            __syncthreads();
+            if (more) {
+                store();
+                __syncthreads();
+            }
+        }
+    }
+#pragma unroll
+    for (int m = 0; m < TM; ++m)
+#pragma unroll
+        for (int n = 0; n < TN; ++n)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+                const int64_t i = i0 + wm * TM * 32 + m * 32 + (v / 4) * 8 + h * 4 + v % 4;
+                const int64_t j = j0 + wn * TN * 32 + n * 32 + col;
+                if (i < g.M && j < g.N) {
+                    if (work) {
+                        work[((int64_t)blockIdx.z * g.M + i) * g.N + j] = acc[m][n][v];
+                    } else {
+                        float *c = g.C + i * g.ldc + j;
+                        *c = g.beta != 0.0f ? fmaf(g.alpha, acc[m][n][v], g.beta * *c) : g.alpha * acc[m][n][v];
+                    }
+                }
+            }
+}
+
+__global__ __launch_bounds__(256) void k_splitk_reduce(GemmArgs g, const float *work, int splits)
+{
+    const int64_t n = g.M * g.N;
+    for (int64_t q = (int64_t)blockIdx.x * 256 + threadIdx.x; q < n; q += (int64_t)gridDim.x * 256) {
+        float acc = work[q];
+        for (int z = 1; z < splits; ++z) acc += work[(int64_t)z * n + q];
+        const int64_t i = q / g.N, j = q % g.N;
+        float *c = g.C + i * g.ldc + j;
+        *c = g.beta != 0.0f ? fmaf(g.alpha, acc, g.beta * *c) : g.alpha * acc;
+    }
+}
+
 }  // namespace
+
+int64_t gemm_nt_chunk(int64_t K, int splits)
+{
+    const int64_t per = (K + splits - 1) / splits;
+    return (per + kNtBK - 1) / kNtBK * kNtBK;
+}
+
+hipError_t launch_gemm_nt(const GemmArgs &g, int splits, float *work, hipStream_t s)
+{
+    if (g.M <= 0 || g.N <= 0) return hipSuccess;
+    if (splits < 1 || (splits > 1 && !work)) return hipErrorInvalidValue;
+    const int64_t kc = splits > 1 ? gemm_nt_chunk(g.K, splits) : (g.K > 0 ? g.K : 1);
+    const int bm = g.M <= 64 ? 64 : 128, bn = g.M <= 128 ? 64 : 128;
+    const dim3 grid((unsigned)((g.N + bn - 1) / bn), (unsigned)((g.M + bm - 1) / bm), (unsigned)splits);
+    float *w = splits > 1 ? work : nullptr;
+    if (bm == 64) hipLaunchKernelGGL((k_gemm_nt<64, 64>), grid, dim3(256), 0, s, g, w, kc);
+    else if (bn == 64) hipLaunchKernelGGL((k_gemm_nt<128, 64>), grid, dim3(256), 0, s, g, w, kc);
+    else hipLaunchKernelGGL((k_gemm_nt<128, 128>), grid, dim3(256), 0, s, g, w, kc);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || splits == 1) return e;
+    const int64_t n = g.M * g.N, blocks = (n + 255) / 256;
+    hipLaunchKernelGGL(k_splitk_reduce, dim3((unsigned)(blocks < 4096 ? blocks : 4096)), dim3(256), 0, s, g,
+                       (const float *)work, splits);
+    return hipGetLastError();
+}
 
 hipError_t launch_gemm(bool ta, bool tb, const GemmArgs &g, hipStream_t s)
 {
     if (g.M <= 0 || g.N <= 0) return hipSuccess;
+    if (!ta && tb) return launch_gemm_nt(g, 1, nullptr, s);
     const dim3 grid((unsigned)((g.N + kBN - 1) / kBN), (unsigned)((g.M + kBM - 1) / kBM));
     if (!ta && !tb) hipLaunchKernelGGL((k_gemm<false, false>), grid, dim3(256), 0, s, g);
     if (!ta && tb) hipLaunchKernelGGL((k_gemm<false, true>), grid, dim3(256), 0, s, g);

@@ -502,6 +502,57 @@ __global__ __launch_bounds__(block_for(G)) void k_es_eval(EsArgs a)
     }
 }
 
+// ---------------------------------------------------------------------------
+// MA-ES samples: row k < N of the steps d (pitch ldd, from the matrix product)
+// becomes x_k = fma(sigma, d_k, y) in registers and is reduced to its fitness;
+// the sample's rank counter is cleared for the counting pass, and the last
+// generation feeds the best-sample selection.
+// ---------------------------------------------------------------------------
+template <int FN, int G, int MAXIT>
+__global__ __launch_bounds__(block_for(G)) void k_mae_eval(MaeEvalArgs a)
+{
+    constexpr int B = block_for(G), RPB = B / G;
+    __shared__ float nbr[(FN == FN_ROSENBROCK && G > 64) ? B * MAXIT : 1];
+    __shared__ float red[2 * (B / 64)];
+    __shared__ uint64_t sk[B / 64];
+    __shared__ uint32_t sc[B / 64];
+
+    const int tid = threadIdx.x, g = tid % G, slot = tid / G;
+    const int64_t C4 = (a.D + 3) >> 2;
+    const float sg = *a.sigma;
+    uint64_t best = kNoKey;
+    for (int64_t kb = (int64_t)blockIdx.x * RPB; kb < a.N; kb += (int64_t)gridDim.x * RPB) {
+        const int64_t k = kb + slot;
+        const bool active = k < a.N;
+        float4 xr[MAXIT];
+#pragma unroll
+        for (int it = 0; it < MAXIT; ++it) {
+            const int64_t c = g + (int64_t)G * it;
+            float o[4] = {0.f, 0.f, 0.f, 0.f};
+            if (active && c < C4) {
+                const float4 y = *reinterpret_cast<const float4 *>(a.y + 4 * c);
+                const float4 d = *reinterpret_cast<const float4 *>(a.d + k * a.ldd + 4 * c);
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    if (4 * c + e < a.D) o[e] = fmaf(sg, comp(d, e), comp(y, e));
+            }
+            xr[it] = make_float4(o[0], o[1], o[2], o[3]);
+        }
+        const float f = row_fitness<FN, G, MAXIT>(xr, g, a.D, nbr, red);
+        if (active && g == 0) {
+            a.fit[k] = f;
+            a.rank[k] = 0u;
+            const uint64_t key = sel_key(f, k);
+            best = key < best ? key : best;
+        }
+    }
+    if (a.slots) {
+        uint32_t none = 0;
+        block_min_key(best, none, sk, sc);
+        if (tid == 0) slot_commit(a.slots, best, 0);
+    }
+}
+
 // Column sums of all rows of x (the swarm mean at creation / refresh).
 template <int G, int MAXIT>
 __global__ __launch_bounds__(block_for(G)) void k_colsum(const float *x, int64_t N, int64_t D,
@@ -557,6 +608,8 @@ __global__ __launch_bounds__(block_for(G)) void k_colsum(const float *x, int64_t
     hipLaunchKernelGGL((k_de<FN, GG, MM>), dim3(grid), dim3(block_for(GG)), 0, s, a)
 #define EVOX_LAUNCH_ES(GG, MM, UNUSED) \
     hipLaunchKernelGGL((k_es_eval<FN, GG, MM>), dim3(grid), dim3(block_for(GG)), 0, s, a)
+#define EVOX_LAUNCH_MAE(GG, MM, UNUSED) \
+    hipLaunchKernelGGL((k_mae_eval<FN, GG, MM>), dim3(grid), dim3(block_for(GG)), 0, s, a)
 
 template <int FN>
 hipError_t launch_pso_t(Layout L, int mode, const PsoArgs &a, int grid, hipStream_t s)
@@ -643,6 +696,17 @@ hipError_t launch_es_eval_t(Layout L, const EsArgs &a, int grid, hipStream_t s)
     switch (L.G * 16 + L.maxit) {
         EVOX_FAMILY_CASES(EVOX_LAUNCH_ES, LAYOUT_PSO, 0)
         EVOX_BIG_CASES(EVOX_LAUNCH_ES, LAYOUT_PSO, 0)
+        default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
+
+template <int FN>
+hipError_t launch_mae_eval_t(Layout L, const MaeEvalArgs &a, int grid, hipStream_t s)
+{
+    switch (L.G * 16 + L.maxit) {
+        EVOX_FAMILY_CASES(EVOX_LAUNCH_MAE, LAYOUT_PSO, 0)
+        EVOX_BIG_CASES(EVOX_LAUNCH_MAE, LAYOUT_PSO, 0)
         default: return hipErrorInvalidValue;
     }
     return hipGetLastError();

@@ -63,6 +63,40 @@ struct EsGradArgs {
     uint32_t k0, k1, t, stream;
 };
 
+// Matrix-adaptation ES.  One generation: k_mae_sample writes the deviates Z
+// [(N + 1) rows][ldx] (row N is the path s, so that the product also yields
+// M s); the product Dm = Z M^T gives the steps d_k = M z_k and M s; k_mae_eval
+// the fitness of y + sigma d_k; k_es_rank the ranks; k_mae_select the parents
+// in rank order; k_mae_recombine the new center and path and the two
+// K-contiguous factors of the matrix update; k_mae_sigma the step size; the
+// product M <- beta M + At Bt^T the new M.
+constexpr int kMaeBlock = 256;  // threads (columns) per block of the recombination
+struct MaeEvalArgs {
+    const float *y, *d;   // center [ldx]; steps [N][ldd]
+    int64_t ldd;
+    const float *sigma;   // step size (device scalar)
+    float *fit;           // [N]
+    uint32_t *rank;       // [N] zeroed here for k_es_rank
+    int64_t N, D;
+    SelSlots *slots;      // nullable
+};
+struct MaeArgs {
+    float *Z, *Dm;        // [(N + 1)][ldx]
+    int64_t N, D, ldx, mu, kp;  // kp: row pitch of At / Bt, >= mu + 1, a multiple of 4
+    const uint32_t *rank; // [N]
+    int32_t *sel;         // [mu] the parents' sample indices, best first
+    const double *w;      // [mu] recombination weights
+    float *y, *s, *sigma; // center [ldx], path [ldx], step size [1]
+    float *At, *Bt;       // [D][kp]
+    double *part;         // [ceil(D / kMaeBlock)] partial sums of |s|^2
+    double cs, cz, hc1, hcw, damp, chi;  // c_s, sqrt(mu_eff c_s (2 - c_s)), c_1 / 2, c_w / 2, c_s / d_s, chi_D
+    uint32_t k0, k1, t;
+};
+hipError_t launch_mae_sample(const MaeArgs &a, hipStream_t s);
+hipError_t launch_mae_select(const MaeArgs &a, hipStream_t s);
+hipError_t launch_mae_recombine(const MaeArgs &a, hipStream_t s);  // and the step size
+hipError_t launch_mae_identity(float *M, int64_t D, int64_t ldx, hipStream_t s);
+
 // C = alpha op(A) op(B) + beta C (row-major; op(A) is M x K, op(B) K x N;
 // leading dimensions and pointers 16-byte multiples for the vector loads).
 struct GemmArgs {
@@ -77,6 +111,11 @@ struct GemmArgs {
     int64_t ldc;
 };
 hipError_t launch_gemm(bool ta, bool tb, const GemmArgs &g, hipStream_t s);
+// The A B^T product (A [M x K], B [N x K]) with `splits` K-slices; splits > 1
+// needs a workspace of splits * M * N floats.  gemm_nt_chunk: the K extent of
+// one slice.
+hipError_t launch_gemm_nt(const GemmArgs &g, int splits, float *work, hipStream_t s);
+int64_t gemm_nt_chunk(int64_t K, int splits);
 
 struct EvalArgs {
     const float *X;
@@ -120,6 +159,8 @@ hipError_t launch_de_t(Layout L, const DeArgs &a, int grid, hipStream_t s);
 template <int FN>
 hipError_t launch_es_eval_t(Layout L, const EsArgs &a, int grid, hipStream_t s);
 template <int FN>
+hipError_t launch_mae_eval_t(Layout L, const MaeEvalArgs &a, int grid, hipStream_t s);
+template <int FN>
 int occupancy_cso_t(Layout L);  // resident blocks per CU of k_cso
 hipError_t launch_eval(int fn, Layout L, bool vec, const EvalArgs &a, int grid, hipStream_t s);
 // Second pass of the selection: reduce and reset the slots, store the result
@@ -160,6 +201,7 @@ hipError_t launch_cso(int fn, Layout L, const CsoArgs &a, int grid, hipStream_t 
 hipError_t launch_de(int fn, Layout L, const DeArgs &a, int grid, hipStream_t s);
 hipError_t launch_es_eval(int fn, Layout L, const EsArgs &a, int grid, hipStream_t s);
 hipError_t launch_es_rank(const float *fit, int64_t N, uint32_t *rank, hipStream_t s);
+hipError_t launch_mae_eval(int fn, Layout L, const MaeEvalArgs &a, int grid, hipStream_t s);
 hipError_t launch_es_grad(const EsGradArgs &a, hipStream_t s);
 int occupancy_cso(int fn, Layout L);
 hipError_t launch_colsum(Layout L, const float *x, int64_t N, int64_t D, int64_t ldx, double *xsum,

@@ -44,7 +44,7 @@ def test_struct_layouts_match_header(evox):
     assert evox.Params.es_lr.offset == 96
     assert evox.Params.pgpe_max_change.offset == 104
     assert evox.Params.seed.offset == 112
-    assert ctypes.sizeof(evox.Buffers) == 9 * 8
+    assert ctypes.sizeof(evox.Buffers) == 11 * 8
 
 
 def test_row_layout_policy(evox):
@@ -88,8 +88,9 @@ def test_default_pitch_policy(evox):
     for D, want in [(1, 4), (10, 12), (63, 64), (64, 64), (65, 96), (100, 128), (1000, 1024)]:
         assert L.evox_default_ldx(C, D) == want, (D, want)
     for D in (10, 100, 1000):
-        assert L.evox_default_ldx(evox.DE, D) == L.evox_default_ldx(P, D)
-    for algo, D in [(P, 0), (C, 32769), (5, 10)]:
+        for algo in (evox.DE, evox.ES, evox.PGPE, evox.MAES):
+            assert L.evox_default_ldx(algo, D) == L.evox_default_ldx(P, D)
+    for algo, D in [(P, 0), (C, 32769), (6, 10)]:
         assert L.evox_default_ldx(algo, D) == 0
     assert evox.make_params(C, evox.GRIEWANK, 10, 100, -1, 1).ldx == 128
     assert evox.make_params(P, evox.GRIEWANK, 10, 100, -1, 1).ldx == 100
