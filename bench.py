@@ -73,6 +73,14 @@ ES_OPS_PER_ELEMENT = 20 + 8 + 4 + 28 + 1
 # PGPE: the same, with two weighted sums in the gradient pass (z and z^2 - 1)
 PGPE_OPS_PER_ELEMENT = 20 + 8 + 4 + 28 + 3
 ALU_PEAK_TOPS = 256 * 64 * 2.4e9 / 1e12   # 256 CUs x 64 lanes x 2.4 GHz, 32-bit lane-ops
+MFMA_F32_PEAK_TFLOPS = 157.3              # dense fp32 matrix-core peak
+
+
+def maes_flops(w):
+    """Algorithmic flops of the MA-ES generation's two products: the steps
+    and M s, 2 (N + 1) D^2, and the rank-mu update, 2 (mu + 1) D^2."""
+    mu = w.N // 2
+    return 2.0 * (w.N + 1) * w.D ** 2, 2.0 * (mu + 1) * w.D ** 2
 
 
 def cso_bytes_per_launch(w):
@@ -126,12 +134,15 @@ def _cpu_baseline(w, budget_s):
         return {"value": rows * w.D * n / dt, "unit": UNIT, "cores": 1, "kind": "oracle",
                 "sample": f"{rows} of {w.N} rows x D={w.D}, {n} evaluation passes, {dt:.1f} s"}
     rows = min(w.N, 20_000 if w.algo == "cso" else 200 if w.algo in ("es", "pgpe") else 2000)
-    P = oracle.make_params(fn, rows, w.D, w.lb, w.ub, v_lo=w.v_lo, v_hi=w.v_hi, w=w.w, c1=w.c1,
+    # MA-ES: the oracle's matrix product costs D^3 per generation, so the
+    # sample keeps the population and shrinks the dimension
+    D = min(w.D, 1024) if w.algo == "maes" else w.D
+    P = oracle.make_params(fn, rows, D, w.lb, w.ub, v_lo=w.v_lo, v_hi=w.v_hi, w=w.w, c1=w.c1,
                            c2=w.c2, phi=w.phi, vmax=w.vmax, seed=w.seed, de_f=w.de_f,
                            de_cr=w.de_cr, es_sigma=w.es_sigma, es_lr=w.es_lr,
                            pgpe_sigma_lr=w.pgpe_sigma_lr, pgpe_max_change=w.pgpe_max_change)
     s = {"pso": oracle.PSO, "cso": oracle.CSO, "de": oracle.DE, "es": oracle.ES,
-         "pgpe": oracle.PGPE}[w.algo](P)
+         "pgpe": oracle.PGPE, "maes": oracle.MAES}[w.algo](P)
     s.step(1)
     t0 = time.perf_counter()
     gens = 0
@@ -139,8 +150,8 @@ def _cpu_baseline(w, budget_s):
         s.step(1)
         gens += 1
     dt = time.perf_counter() - t0
-    return {"value": rows * w.D * gens / dt, "unit": UNIT, "cores": 1, "kind": "oracle",
-            "sample": f"{rows} of {w.N} individuals x D={w.D}, {gens} generations, {dt:.1f} s"}
+    return {"value": rows * D * gens / dt, "unit": UNIT, "cores": 1, "kind": "oracle",
+            "sample": f"{rows} of {w.N} individuals x D={D} of {w.D}, {gens} generations, {dt:.1f} s"}
 
 
 def copy_bandwidth(torch, evox, mib=1024, reps=5):
@@ -201,7 +212,7 @@ def main():
         swarm = None
     else:
         algo = {"pso": evox.PSO, "cso": evox.CSO, "de": evox.DE, "es": evox.ES,
-                "pgpe": evox.PGPE}[w.algo]
+                "pgpe": evox.PGPE, "maes": evox.MAES}[w.algo]
         P = evox.make_params(algo, fn, w.N, w.D, w.lb, w.ub, v_lo=w.v_lo, v_hi=w.v_hi, w=w.w,
                              c1=w.c1, c2=w.c2, phi=w.phi, vmax=w.vmax, seed=w.seed,
                              ldx=args.ldx or None, de_f=w.de_f, de_cr=w.de_cr,
@@ -238,7 +249,21 @@ def main():
     if swarm is not None:
         fused_ms, launches, improved = swarm.profile_read()
         swarm.profile(False)
-        if launches > 0 and w.algo in ("es", "pgpe"):
+        if launches > 0 and w.algo == "maes":
+            # the matrix-core roofline of the sampling product (the timed
+            # launch: k_gemm_nt and its split-K reduction)
+            avg_ms = fused_ms / launches
+            f_sample, f_update = maes_flops(w)
+            achieved = f_sample / (avg_ms / 1e3) / 1e12
+            gen_s = ms / 1e3 / w.gens
+            roofline = {"bound": "mfma", "achieved": round(achieved, 2), "peak": MFMA_F32_PEAK_TFLOPS,
+                        "unit": "TFLOP/s", "frac": round(achieved / MFMA_F32_PEAK_TFLOPS, 4),
+                        "traffic": None, "kernel": "k_gemm_nt<128,64> + k_splitk_reduce (Z M^T)",
+                        "avg_launch_us": round(avg_ms * 1e3, 2), "launches": launches,
+                        "algorithmic_flops_per_launch": f_sample,
+                        "generation_us": round(gen_s * 1e6, 2),
+                        "generation_tflops": round((f_sample + f_update) / gen_s / 1e12, 2)}
+        elif launches > 0 and w.algo in ("es", "pgpe"):
             # the ALU roofline of the whole generation (samples, ranks,
             # gradient, step), timed over the step
             gen_s = ms / 1e3 / w.gens

@@ -266,7 +266,8 @@ int evox_pgpe_step(evox_state *state, int64_t n_gens);
  *     sum w_i z_i (fp64 sums, one rounding);
  *   - M <- M [I + c_1/2 (s s^T - I) + c_w/2 (sum w_i z_i z_i^T - I)],
  *     computed as (1 - (c_1 + c_w)/2) M + c_1/2 (M s) s^T + c_w/2 sum w_i d_i
- *     z_i^T (fp32 matrix-core product over mu + 1 terms);
+ *     z_i^T (the mu + 1 terms summed in fp32 on the matrix cores, then one
+ *     fused multiply-add with the rounded (1 - (c_1 + c_w)/2) M);
  *   - sigma <- sigma exp(c_s/d_s (|s| / chi_D - 1)).
  * evox_best reports the best sample of the last generation and the center y
  * as the solution. */

@@ -77,22 +77,35 @@ struct Plan {
     // weights, path-norm partial sums
     size_t mae_z = 0, mae_d = 0, mae_work = 0, mae_at = 0, mae_bt = 0, mae_sel = 0, mae_w = 0, mae_part = 0;
     int mae_splits = 1;
-    int64_t mae_mu = 0, mae_kp = 0;
+    int64_t mae_mu = 0, mae_kp = 0, mae_ldf = 0;
     size_t total = 0;
 };
 
-// K-slices of the sampling product (N + 1) x D x D: enough blocks to fill the
-// chip (the 128-row tiles of a small population give few), each slice at
-// least 256 deep.
-int mae_splits(int64_t N, int64_t D)
+// K-slices of the sampling product (N + 1) x D x D: a small population gives
+// few output tiles, so the product is split along K until the blocks fill
+// the chip -- a whole number of rounds of resident blocks when the occupancy
+// is known (a partial last round idles most of the chip), else about 1024
+// blocks -- with every slice at least 256 deep.
+int mae_splits(int64_t N, int64_t D, int64_t resident)
 {
     const int64_t rows = N + 1, bm = rows <= 64 ? 64 : 128, bn = rows <= 128 ? 64 : 128;
     const int64_t tiles = ((D + bn - 1) / bn) * ((rows + bm - 1) / bm);
-    int64_t sp = (1024 + tiles - 1) / tiles;
+    int64_t sp = resident > 0 ? resident / tiles : (1024 + tiles - 1) / tiles;
     const int64_t deep = D / 256 > 1 ? D / 256 : 1;
     if (sp > deep) sp = deep;
     if (sp > 16) sp = 16;
     return (int)(sp < 1 ? 1 : sp);
+}
+
+// Blocks of the sampling product's thin tile shape resident on the device at
+// once (0 if unknown).
+int64_t resident_thin_blocks()
+{
+    int dev = 0, cus = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+        return 0;
+    return (int64_t)cus * occupancy_gemm_nt_thin();
 }
 
 int make_plan(const evox_params *P, Plan *pl)
@@ -162,13 +175,17 @@ int make_plan(const evox_params *P, Plan *pl)
     if (P->algo == EVOX_MAES) {
         const size_t rows = (size_t)P->N + 1, D = (size_t)P->D;
         p.mae_mu = P->N / 2;
-        p.mae_kp = (p.mae_mu + 1 + 3) / 4 * 4;
-        p.mae_splits = mae_splits(P->N, P->D);
+        // factor terms: ceil((mu + 1) / 2) steps of two when an unrolled rank
+        // kernel exists for that count, else a multiple of 32 terms
+        const int64_t steps = (p.mae_mu + 2) / 2;
+        p.mae_kp = steps <= kMaeRankUnrolled ? 2 * steps : (p.mae_mu + 1 + 31) / 32 * 32;
+        p.mae_ldf = (P->D + 63) / 64 * 64;
+        p.mae_splits = mae_splits(P->N, P->D, resident_thin_blocks());
         p.mae_z = take(sizeof(float) * rows * (size_t)P->ldx);
         p.mae_d = take(sizeof(float) * rows * (size_t)P->ldx);
         p.mae_work = p.mae_splits > 1 ? take(sizeof(float) * (size_t)p.mae_splits * rows * D) : 0;
-        p.mae_at = take(sizeof(float) * D * (size_t)p.mae_kp);
-        p.mae_bt = take(sizeof(float) * D * (size_t)p.mae_kp);
+        p.mae_at = take(sizeof(float) * (size_t)p.mae_ldf * (size_t)p.mae_kp);
+        p.mae_bt = take(sizeof(float) * (size_t)p.mae_ldf * (size_t)p.mae_kp);
         p.esrank = take(sizeof(uint32_t) * (size_t)P->N);
         p.mae_sel = take(sizeof(int32_t) * (size_t)p.mae_mu);
         p.mae_w = take(sizeof(double) * (size_t)p.mae_mu);
@@ -382,6 +399,7 @@ int evox_state_create(const evox_params *params, const evox_buffers *b, void *hi
         m.ldx = P.ldx;
         m.mu = mu;
         m.kp = pl.mae_kp;
+        m.ldf = pl.mae_ldf;
         s->esrank = at<uint32_t>(b->scratch, pl.esrank);
         m.rank = s->esrank;
         m.sel = at<int32_t>(b->scratch, pl.mae_sel);
@@ -463,6 +481,8 @@ int evox_state_create(const evox_params *params, const evox_buffers *b, void *hi
         if (P.algo == EVOX_MAES &&
             ((e = launch_fill(b->v, P.ldx, 0.0f, s->stream)) != hipSuccess ||
              (e = launch_mae_identity(b->mat, P.D, P.ldx, s->stream)) != hipSuccess ||
+             (e = launch_fill(s->mae.At, s->mae.kp * s->mae.ldf, 0.0f, s->stream)) != hipSuccess ||
+             (e = launch_fill(s->mae.Bt, s->mae.kp * s->mae.ldf, 0.0f, s->stream)) != hipSuccess ||
              (e = launch_fill(b->sigma, 1, P.es_sigma, s->stream)) != hipSuccess ||
              (e = hipMemcpyAsync((void *)s->mae.w, s->mae_w.data(), sizeof(double) * s->mae_w.size(),
                                  hipMemcpyHostToDevice, s->stream)) != hipSuccess ||
@@ -701,10 +721,9 @@ int mae_generations(evox_state *s, int64_t n_gens)
     const evox_params &P = s->P;
     const Plan &pl = s->pl;
     MaeArgs m = s->mae;
-    // the sampling product Dm = Z M^T ((N + 1) x D over K = D) and the update
-    // M <- beta M + At Bt^T (D x D over K = mu + 1)
+    // the sampling product Dm = Z M^T ((N + 1) x D over K = D); the update
+    // M <- beta M + At^T Bt is the rank pass
     const GemmArgs sample{P.N + 1, P.D, P.D, 1.0f, m.Z, P.ldx, s->B.mat, P.ldx, 0.0f, m.Dm, P.ldx};
-    const GemmArgs update{P.D, P.D, m.mu + 1, 1.0f, m.At, m.kp, m.Bt, m.kp, s->mae_beta, s->B.mat, P.ldx};
     hipError_t e;
     for (int64_t k = 0; k < n_gens; ++k) {
         m.t = (uint32_t)(s->t + k);
@@ -719,7 +738,8 @@ int mae_generations(evox_state *s, int64_t n_gens)
         if ((e = launch_es_rank(s->B.fit, P.N, s->esrank, s->stream)) != hipSuccess) return hip_fail(e, "ranks");
         if ((e = launch_mae_select(m, s->stream)) != hipSuccess) return hip_fail(e, "parents");
         if ((e = launch_mae_recombine(m, s->stream)) != hipSuccess) return hip_fail(e, "recombination");
-        if ((e = launch_gemm_nt(update, 1, nullptr, s->stream)) != hipSuccess) return hip_fail(e, "matrix update");
+        if ((e = launch_mae_rank(m, s->B.mat, s->mae_beta, s->stream)) != hipSuccess)
+            return hip_fail(e, "matrix update");
     }
     if ((e = launch_select(s->slots, nullptr, 0, nullptr, s->best, nullptr, nullptr, s->stream)) != hipSuccess)
         return hip_fail(e, "select");

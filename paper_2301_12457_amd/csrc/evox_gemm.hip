@@ -248,6 +248,13 @@ __global__ __launch_bounds__(256) void k_splitk_reduce(GemmArgs g, const float *
 
 }  // namespace
 
+int occupancy_gemm_nt_thin()
+{
+    int n = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k_gemm_nt<128, 64>, 256, 0) != hipSuccess) return 0;
+    return n;
+}
+
 int64_t gemm_nt_chunk(int64_t K, int splits)
 {
     const int64_t per = (K + splits - 1) / splits;

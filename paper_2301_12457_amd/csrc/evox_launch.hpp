@@ -69,8 +69,9 @@ struct EsGradArgs {
 // the fitness of y + sigma d_k; k_es_rank the ranks; k_mae_select the parents
 // in rank order; k_mae_recombine the new center and path and the two
 // K-contiguous factors of the matrix update; k_mae_sigma the step size; the
-// product M <- beta M + At Bt^T the new M.
+// rank-(mu + 1) pass M <- beta M + At^T Bt the new M.
 constexpr int kMaeBlock = 256;  // threads (columns) per block of the recombination
+constexpr int kMaeRankUnrolled = 32;  // rank-pass step counts with an unrolled kernel of their own
 struct MaeEvalArgs {
     const float *y, *d;   // center [ldx]; steps [N][ldd]
     int64_t ldd;
@@ -82,12 +83,13 @@ struct MaeEvalArgs {
 };
 struct MaeArgs {
     float *Z, *Dm;        // [(N + 1)][ldx]
-    int64_t N, D, ldx, mu, kp;  // kp: row pitch of At / Bt, >= mu + 1, a multiple of 4
+    int64_t N, D, ldx, mu;
+    int64_t kp, ldf;      // factor terms (mu + 1 padded with zero terms) and their pitch
     const uint32_t *rank; // [N]
     int32_t *sel;         // [mu] the parents' sample indices, best first
     const double *w;      // [mu] recombination weights
     float *y, *s, *sigma; // center [ldx], path [ldx], step size [1]
-    float *At, *Bt;       // [D][kp]
+    float *At, *Bt;       // [kp][ldf], k-major, zero past term mu and column D
     double *part;         // [ceil(D / kMaeBlock)] partial sums of |s|^2
     double cs, cz, hc1, hcw, damp, chi;  // c_s, sqrt(mu_eff c_s (2 - c_s)), c_1 / 2, c_w / 2, c_s / d_s, chi_D
     uint32_t k0, k1, t;
@@ -95,7 +97,9 @@ struct MaeArgs {
 hipError_t launch_mae_sample(const MaeArgs &a, hipStream_t s);
 hipError_t launch_mae_select(const MaeArgs &a, hipStream_t s);
 hipError_t launch_mae_recombine(const MaeArgs &a, hipStream_t s);  // and the step size
+hipError_t launch_mae_rank(const MaeArgs &a, float *M, float beta, hipStream_t s);  // M <- beta M + At^T Bt
 hipError_t launch_mae_identity(float *M, int64_t D, int64_t ldx, hipStream_t s);
+int occupancy_gemm_nt_thin();  // resident blocks per CU of the sampling product's tile shape
 
 // C = alpha op(A) op(B) + beta C (row-major; op(A) is M x K, op(B) K x N;
 // leading dimensions and pointers 16-byte multiples for the vector loads).

@@ -6,14 +6,17 @@
 //     M [I + c_1/2 (s' s'^T - I) + c_w/2 (sum_i w_i z_i z_i^T - I)]
 //   = (1 - (c_1 + c_w)/2) M + (M s') (c_1/2 s')^T + sum_i d_i (c_w/2 w_i z_i)^T,
 // and M s' = (1 - c_s) M s + sqrt(mu_eff c_s (2 - c_s)) sum_i w_i d_i, so the
-// update is one product of two D x (mu + 1) factors whose columns this file
-// writes, and M s comes from the sampling product (the path rides along as
-// an extra deviate row).
+// update is one rank-(mu + 1) product of two factors that this file writes
+// k-major ([term][column], so that a wave's operand loads are coalesced) and
+// then applies to M in one streaming pass, and M s comes from the sampling
+// product (the path rides along as an extra deviate row).
 #include "evox_launch.hpp"
 
 namespace evox {
 
 namespace {
+
+typedef float f32x16 __attribute__((ext_vector_type(16)));
 
 // Deviates z_k (rows k < N, Philox stream 9 with the generation in the
 // counter) and the path s (row N); columns D..ldx-1 zero.
@@ -46,9 +49,11 @@ __global__ __launch_bounds__(256) void k_mae_select(MaeArgs a)
 }
 
 // One thread per column j: the weighted parent sums <z>_w and <d>_w in fp64,
-// y_j <- y_j + sigma <d>_w, s_j <- (1 - c_s) s_j + c_z <z>_w, the factor rows
-//     At[j] = (d_{1:N, j}, ..., d_{mu:N, j}, (M s')_j, 0 ...)
-//     Bt[j] = (c_w/2 w_1 z_{1:N, j}, ..., c_w/2 w_mu z_{mu:N, j}, c_1/2 s'_j, 0 ...)
+// y_j <- y_j + sigma <d>_w, s_j <- (1 - c_s) s_j + c_z <z>_w, column j of the
+// factors (term r at At[r][j], Bt[r][j]; the zero terms past mu and the zero
+// columns past D are set once at creation)
+//     At[., j] = (d_{1:N, j}, ..., d_{mu:N, j}, (M s')_j)
+//     Bt[., j] = (c_w/2 w_1 z_{1:N, j}, ..., c_w/2 w_mu z_{mu:N, j}, c_1/2 s'_j)
 // and the block's sum of s'_j^2 (fp64, fixed order).
 __global__ __launch_bounds__(kMaeBlock) void k_mae_recombine(MaeArgs a)
 {
@@ -57,21 +62,20 @@ __global__ __launch_bounds__(kMaeBlock) void k_mae_recombine(MaeArgs a)
     double sq = 0.0;
     if (j < a.D) {
         double zw = 0.0, dw = 0.0;
-        float *at = a.At + j * a.kp, *bt = a.Bt + j * a.kp;
+        float *at = a.At + j, *bt = a.Bt + j;
         for (int64_t r = 0; r < a.mu; ++r) {
             const int64_t k = a.sel[r];
             const double wr = a.w[r];
             const float z = a.Z[k * a.ldx + j], d = a.Dm[k * a.ldx + j];
             zw += wr * (double)z;
             dw += wr * (double)d;
-            at[r] = d;
-            bt[r] = (float)(a.hcw * wr * (double)z);
+            at[r * a.ldf] = d;
+            bt[r * a.ldf] = (float)(a.hcw * wr * (double)z);
         }
         const double sig = (double)*a.sigma, keep = 1.0 - a.cs;
         const float sn = (float)(keep * (double)a.s[j] + a.cz * zw);
-        at[a.mu] = (float)(keep * (double)a.Dm[a.N * a.ldx + j] + a.cz * dw);
-        bt[a.mu] = (float)(a.hc1 * (double)sn);
-        for (int64_t r = a.mu + 1; r < a.kp; ++r) at[r] = bt[r] = 0.0f;
+        at[a.mu * a.ldf] = (float)(keep * (double)a.Dm[a.N * a.ldx + j] + a.cz * dw);
+        bt[a.mu * a.ldf] = (float)(a.hc1 * (double)sn);
         a.y[j] = (float)((double)a.y[j] + sig * dw);
         a.s[j] = sn;
         sq = (double)sn * (double)sn;
@@ -99,6 +103,65 @@ __global__ __launch_bounds__(256) void k_mae_sigma(MaeArgs a, int64_t nparts)
         __syncthreads();
     }
     if (threadIdx.x == 0) *a.sigma = (float)((double)*a.sigma * exp(a.damp * (sqrt(red[0]) / a.chi - 1.0)));
+}
+
+// M <- beta M + At^T Bt over the factor terms (2 STEPS of them; the factors
+// hold zeros past the mu + 1 real terms and past column D, up to their
+// padded extents, so no operand load needs a guard): each wave owns a
+// 32 x 64 tile of M and accumulates two 32x32x2 MFMA tiles, loading the
+// operands directly from the k-major factors (lane l: row or column l % 32
+// of term 2 step + l / 32, one 128-byte line per half wave).  The tile of M
+// is loaded first; the operands of a fully unrolled block of steps are all
+// issued before its products, so that a wave waits for them once.  No LDS,
+// no barrier.  STEPS = 0: any number of steps (a.kp / 2, a multiple of 16),
+// 16 at a time.
+template <int STEPS>
+__global__ __launch_bounds__(256) void k_mae_rank(MaeArgs a, float *M, float beta)
+{
+    constexpr int CH = STEPS > 0 ? STEPS : 16;
+    const int lane = threadIdx.x % 64, col = lane % 32, h = lane / 32;
+    const int64_t tn = (a.D + 63) / 64;
+    const int64_t wave = (int64_t)blockIdx.x * 4 + threadIdx.x / 64;
+    const int64_t i0 = (wave / tn) * 32, j0 = (wave % tn) * 64;
+    if (i0 >= a.D) return;
+    float old[2][16];
+#pragma unroll
+    for (int n = 0; n < 2; ++n)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+            const int64_t i = i0 + (v / 4) * 8 + h * 4 + v % 4, j = j0 + 32 * n + col;
+            old[n][v] = (i < a.D && j < a.D) ? M[i * a.ldx + j] : 0.0f;
+        }
+    f32x16 acc[2];
+#pragma unroll
+    for (int n = 0; n < 2; ++n)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) acc[n][v] = 0.0f;
+    const float *pa = a.At + h * a.ldf + i0 + col;
+    const float *pb = a.Bt + h * a.ldf + j0 + col;
+    const int64_t steps = STEPS > 0 ? STEPS : a.kp / 2;
+    for (int64_t c0 = 0; c0 < steps; c0 += CH) {
+        float av[CH], b0[CH], b1[CH];
+#pragma unroll
+        for (int t = 0; t < CH; ++t) {
+            const int64_t off = 2 * (c0 + t) * a.ldf;
+            av[t] = pa[off];
+            b0[t] = pb[off];
+            b1[t] = pb[off + 32];
+        }
+#pragma unroll
+        for (int t = 0; t < CH; ++t) {
+            acc[0] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[t], b0[t], acc[0], 0, 0, 0);
+            acc[1] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[t], b1[t], acc[1], 0, 0, 0);
+        }
+    }
+#pragma unroll
+    for (int n = 0; n < 2; ++n)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+            const int64_t i = i0 + (v / 4) * 8 + h * 4 + v % 4, j = j0 + 32 * n + col;
+            if (i < a.D && j < a.D) M[i * a.ldx + j] = fmaf(1.0f, acc[n][v], beta * old[n][v]);
+        }
 }
 
 __global__ __launch_bounds__(256) void k_mae_identity(float *M, int64_t D, int64_t ldx)
@@ -135,6 +198,27 @@ hipError_t launch_mae_recombine(const MaeArgs &a, hipStream_t s)
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(k_mae_sigma, dim3(1), dim3(256), 0, s, a, nparts);
+    return hipGetLastError();
+}
+
+hipError_t launch_mae_rank(const MaeArgs &a, float *M, float beta, hipStream_t s)
+{
+    const int64_t waves = ((a.D + 31) / 32) * ((a.D + 63) / 64);
+    const dim3 grid((unsigned)((waves + 3) / 4)), block(256);
+    const int64_t steps = (a.mu + 2) / 2;  // ceil((mu + 1) / 2)
+    switch (steps > kMaeRankUnrolled ? 0 : steps) {
+#define EVOX_RANK_CASE(S) \
+    case S: hipLaunchKernelGGL((k_mae_rank<S>), grid, block, 0, s, a, M, beta); break;
+        EVOX_RANK_CASE(1) EVOX_RANK_CASE(2) EVOX_RANK_CASE(3) EVOX_RANK_CASE(4) EVOX_RANK_CASE(5)
+        EVOX_RANK_CASE(6) EVOX_RANK_CASE(7) EVOX_RANK_CASE(8) EVOX_RANK_CASE(9) EVOX_RANK_CASE(10)
+        EVOX_RANK_CASE(11) EVOX_RANK_CASE(12) EVOX_RANK_CASE(13) EVOX_RANK_CASE(14) EVOX_RANK_CASE(15)
+        EVOX_RANK_CASE(16) EVOX_RANK_CASE(17) EVOX_RANK_CASE(18) EVOX_RANK_CASE(19) EVOX_RANK_CASE(20)
+        EVOX_RANK_CASE(21) EVOX_RANK_CASE(22) EVOX_RANK_CASE(23) EVOX_RANK_CASE(24) EVOX_RANK_CASE(25)
+        EVOX_RANK_CASE(26) EVOX_RANK_CASE(27) EVOX_RANK_CASE(28) EVOX_RANK_CASE(29) EVOX_RANK_CASE(30)
+        EVOX_RANK_CASE(31) EVOX_RANK_CASE(32)
+#undef EVOX_RANK_CASE
+        default: hipLaunchKernelGGL((k_mae_rank<0>), grid, block, 0, s, a, M, beta); break;
+    }
     return hipGetLastError();
 }
 

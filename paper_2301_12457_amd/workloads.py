@@ -16,7 +16,7 @@ about a million): synthetic, seeded, no dataset.
 import math
 from dataclasses import dataclass, field
 
-PSO, CSO, DE, ES, PGPE, EVAL = "pso", "cso", "de", "es", "pgpe", "eval"
+PSO, CSO, DE, ES, PGPE, MAES, EVAL = "pso", "cso", "de", "es", "pgpe", "maes", "eval"
 
 
 @dataclass(frozen=True)
@@ -62,6 +62,8 @@ WORKLOADS = {
                                   lb=-5.0, ub=5.0, es_sigma=0.1, es_lr=0.05),
     "pgpe_sphere_1e4x1e4": Workload("pgpe_sphere_1e4x1e4", PGPE, "sphere", 10_000, 10_000, 100, 7,
                                     lb=-5.0, ub=5.0, es_sigma=1.0, es_lr=0.5, pgpe_sigma_lr=0.1),
+    "maes_sphere_100x16384": Workload("maes_sphere_100x16384", MAES, "sphere", 100, 16_384, 20, 10,
+                                      lb=-5.0, ub=5.0, es_sigma=1.0),
     "eval_rosenbrock_1m_x1e3": Workload("eval_rosenbrock_1m_x1e3", EVAL, "rosenbrock", 1_048_576,
                                         1_000, 1, 4, x_mu=1.0, x_sigma=0.5),
 }
