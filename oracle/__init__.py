@@ -81,6 +81,19 @@ def lib():
         L.evox_ref_maes_consts.restype = i64
         L.evox_ref_maes_init.argtypes = [P, P, P, P, P]
         L.evox_ref_maes_step.argtypes = [P, i64, i64, P, P, P, P, P, P, P, P, i64, P, P]
+        L.evox_ref_dtlz1.argtypes = [P, i64, ctypes.c_int32, P]
+        L.evox_ref_dtlz1_rows.argtypes = [P, i64, i64, ctypes.c_int32, P]
+        L.evox_ref_dominates.argtypes = [P, P, ctypes.c_int32]
+        L.evox_ref_dominates.restype = ctypes.c_int
+        L.evox_ref_nds.argtypes = [P, i64, ctypes.c_int32, P]
+        L.evox_ref_nds.restype = ctypes.c_int32
+        L.evox_ref_crowding.argtypes = [P, i64, ctypes.c_int32, P, P]
+        L.evox_ref_nsga2_parents.argtypes = [u64, i64, i64, i64, P, P, P, P]
+        L.evox_ref_poly_mutate.argtypes = [ctypes.c_double, ctypes.c_double, ctypes.c_double]
+        L.evox_ref_poly_mutate.restype = ctypes.c_double
+        L.evox_ref_nsga2_offspring.argtypes = [P, i64, i64, P, P, P, P]
+        L.evox_ref_nsga2_init.argtypes = [P, P, P, P, P]
+        L.evox_ref_nsga2_step.argtypes = [P, i64, i64, P, P, P, P]
         L.evox_ref_de_init.argtypes = [P, P, P]
         L.evox_ref_de_step.argtypes = [P, i64, i64, P, P, P, P, P]
         L.evox_ref_cso_init.argtypes = [P, P, P, P]
@@ -423,6 +436,96 @@ class MAES:
             raise ValueError(f"evox_ref_maes_step rc={rc}")
         if n_gens > 0:
             self.best_fit, self.best_idx = bf.value, bi.value
+        self.t += n_gens
+
+
+class NSGA2Params(ctypes.Structure):
+    _fields_ = [("N", ctypes.c_int64), ("D", ctypes.c_int64), ("M", ctypes.c_int32),
+                ("eta_c", ctypes.c_float), ("eta_m", ctypes.c_float), ("seed", ctypes.c_uint64)]
+
+
+def dtlz1(X, M):
+    """fp32 objectives [n, M] of the rows of X (fp64 inside, rounded once)."""
+    X = _f32(np.atleast_2d(X))
+    F = np.zeros((X.shape[0], M), np.float32)
+    lib().evox_ref_dtlz1_rows(_ptr(X), X.shape[0], X.shape[1], M, _ptr(F))
+    return F
+
+
+def dtlz1_f64(x, M):
+    x = _f32(np.asarray(x).reshape(1, -1))[0]
+    f = np.zeros(M, np.float64)
+    lib().evox_ref_dtlz1(_ptr(x), x.size, M, _ptr(f))
+    return f
+
+
+def dominates(a, b):
+    a, b = _f32(np.asarray(a).reshape(1, -1))[0], _f32(np.asarray(b).reshape(1, -1))[0]
+    return bool(lib().evox_ref_dominates(_ptr(a), _ptr(b), a.size))
+
+
+def nds(F):
+    """0-based front index of every row of F [n, M]."""
+    F = _f32(np.atleast_2d(F))
+    front = np.zeros(F.shape[0], np.int32)
+    lib().evox_ref_nds(_ptr(F), F.shape[0], F.shape[1], _ptr(front))
+    return front
+
+
+def crowding(F, front):
+    F = _f32(np.atleast_2d(F))
+    front = np.ascontiguousarray(front, dtype=np.int32)
+    crowd = np.zeros(F.shape[0], np.float64)
+    lib().evox_ref_crowding(_ptr(F), F.shape[0], F.shape[1], _ptr(front), _ptr(crowd))
+    return crowd
+
+
+def nsga2_params(N, D, M=3, eta_c=20.0, eta_m=20.0, seed=0):
+    return NSGA2Params(N=N, D=D, M=M, eta_c=eta_c, eta_m=eta_m, seed=seed)
+
+
+def poly_mutate(x, u, eta):
+    return lib().evox_ref_poly_mutate(x, u, eta)
+
+
+def nsga2_parents(seed, t, p, N, front, crowd):
+    front = np.ascontiguousarray(front, dtype=np.int32)
+    crowd = np.ascontiguousarray(crowd, dtype=np.float64)
+    a, b = ctypes.c_int64(0), ctypes.c_int64(0)
+    lib().evox_ref_nsga2_parents(seed, t, p, N, _ptr(front), _ptr(crowd), ctypes.byref(a), ctypes.byref(b))
+    return a.value, b.value
+
+
+def nsga2_offspring(P, t, p, a, b):
+    a, b = _f32(np.asarray(a).reshape(1, -1))[0], _f32(np.asarray(b).reshape(1, -1))[0]
+    c0, c1 = np.zeros(P.D, np.float32), np.zeros(P.D, np.float32)
+    lib().evox_ref_nsga2_offspring(ctypes.byref(P), t, p, _ptr(a), _ptr(b), _ptr(c0), _ptr(c1))
+    return c0, c1
+
+
+class NSGA2:
+    """Oracle NSGA-II state on DTLZ1: population X [N, D], objectives F [N, M],
+    fronts and crowding distances, generation t."""
+
+    def __init__(self, params: NSGA2Params):
+        self.P = params
+        N, D, M = params.N, params.D, params.M
+        self.X = np.zeros((N, D), np.float32)
+        self.F = np.zeros((N, M), np.float32)
+        self.front = np.zeros(N, np.int32)
+        self.crowd = np.zeros(N, np.float64)
+        self.t = 0
+        if lib().evox_ref_nsga2_init(ctypes.byref(self.P), _ptr(self.X), _ptr(self.F), _ptr(self.front),
+                                     _ptr(self.crowd)) != 0:
+            raise ValueError("evox_ref_nsga2_init failed")
+
+    def step(self, n_gens):
+        for a in (self.X, self.F, self.front, self.crowd):
+            assert a.flags.c_contiguous
+        rc = lib().evox_ref_nsga2_step(ctypes.byref(self.P), self.t, n_gens, _ptr(self.X), _ptr(self.F),
+                                       _ptr(self.front), _ptr(self.crowd))
+        if rc != 0:
+            raise ValueError(f"evox_ref_nsga2_step rc={rc}")
         self.t += n_gens
 
 

@@ -94,7 +94,7 @@ void evox_ref_u01_array(const uint32_t *w, int64_t n, float *out)
 /* Random-stream identifiers (the counter's fourth word). */
 enum { STREAM_INIT_X = 0, STREAM_INIT_V = 1, STREAM_PSO = 2, STREAM_CSO = 3,
        STREAM_PERM = 4, STREAM_INIT_NORMAL = 5, STREAM_DE = 6, STREAM_ES = 7, STREAM_PGPE = 8,
-       STREAM_MAES = 9 };
+       STREAM_MAES = 9, STREAM_NSGA_SEL = 10, STREAM_NSGA_VAR = 11, STREAM_NSGA_MUT = 12 };
 
 /* Draw k of K for element (i, j) at generation t in stream s:
  * word (j mod 4) of Philox(seed, (K*floor(j/4) + k, i, t, s)). */
@@ -1000,5 +1000,288 @@ int evox_ref_maes_step(const evox_ref_params *P, int64_t t0, int64_t n_gens, flo
     }
     free(w); free(z); free(d); free(x); free(f); free(order); free(rank); free(zw); free(dw);
     free(T); free(row);
+    return 0;
+}
+
+/* ------------------------------------------------------------------------ */
+/* NSGA-II (Table II; the multi-objective scaling experiment of Sec. V-A     */
+/* runs it on DTLZ1) following Deb, Pratap, Agarwal and Meyarivan, IEEE TEVC */
+/* 6(2), 2002: crowded binary tournaments, simulated binary crossover and    */
+/* polynomial mutation, non-dominated sorting of parents and offspring       */
+/* together, crowding distance, elitist truncation.                          */
+/* ------------------------------------------------------------------------ */
+
+typedef struct {
+    int64_t N, D;       /* population (even), decision variables (>= M) */
+    int32_t M;          /* objectives */
+    float eta_c, eta_m; /* distribution indices of the crossover and the mutation */
+    uint64_t seed;
+} evox_ref_nsga2_params;
+
+/* DTLZ1 (Deb, Thiele, Laumanns, Zitzler, 2002) on x in [0, 1]^D with M
+ * objectives, k = D - M + 1 distance variables:
+ *   g = 100 (k + sum_{i >= M-1} ((x_i - 1/2)^2 - cos(20 pi (x_i - 1/2))))
+ *   f_0 = (1 + g)/2 x_0 x_1 ... x_{M-2}
+ *   f_m = (1 + g)/2 x_0 ... x_{M-2-m} (1 - x_{M-1-m}),  m = 1 .. M-1
+ * in fp64; the Pareto-optimal front is sum_m f_m = 1/2 at g = 0. */
+void evox_ref_dtlz1(const float *x, int64_t D, int32_t M, double *f)
+{
+    const double pi = 3.14159265358979323846;
+    double g = 0.0;
+    for (int64_t i = M - 1; i < D; ++i) {
+        const double d = (double)x[i] - 0.5;
+        g += d * d - cos(20.0 * pi * d);
+    }
+    g = 100.0 * ((double)(D - M + 1) + g);
+    for (int32_t m = 0; m < M; ++m) {
+        double v = 0.5 * (1.0 + g);
+        for (int32_t i = 0; i < M - 1 - m; ++i) v *= (double)x[i];
+        if (m > 0) v *= 1.0 - (double)x[M - 1 - m];
+        f[m] = v;
+    }
+}
+
+/* Objectives of n rows (pitch D) rounded to fp32, F[i * M + m]. */
+void evox_ref_dtlz1_rows(const float *X, int64_t n, int64_t D, int32_t M, float *F)
+{
+    double f[64];
+    for (int64_t i = 0; i < n; ++i) {
+        evox_ref_dtlz1(X + i * D, D, M, f);
+        for (int32_t m = 0; m < M; ++m) F[i * M + m] = (float)f[m];
+    }
+}
+
+/* a dominates b (minimisation): no objective worse, at least one better. */
+int evox_ref_dominates(const float *a, const float *b, int32_t M)
+{
+    int strict = 0;
+    for (int32_t m = 0; m < M; ++m) {
+        if (a[m] > b[m]) return 0;
+        if (a[m] < b[m]) strict = 1;
+    }
+    return strict;
+}
+
+/* Non-dominated sorting by its definition: front 0 holds the points no
+ * point dominates; front k + 1 the points that only points of fronts <= k
+ * dominate.  front[i] receives the 0-based front index.  Returns the number
+ * of fronts. */
+int32_t evox_ref_nds(const float *F, int64_t n, int32_t M, int32_t *front)
+{
+    for (int64_t i = 0; i < n; ++i) front[i] = -1;
+    int64_t left = n;
+    int32_t k = 0;
+    while (left > 0) {
+        /* members of front k: unassigned and dominated by no unassigned point */
+        for (int64_t i = 0; i < n; ++i) {
+            if (front[i] != -1) continue;
+            int dominated = 0;
+            for (int64_t j = 0; j < n && !dominated; ++j)  /* j still unassigned (-1, or -2 below) */
+                if (front[j] < 0) dominated = evox_ref_dominates(F + j * M, F + i * M, M);
+            if (!dominated) front[i] = -2; /* front k, marked once every point is checked */
+        }
+        for (int64_t i = 0; i < n; ++i)
+            if (front[i] == -2) {
+                front[i] = k;
+                --left;
+            }
+        ++k;
+    }
+    return k;
+}
+
+/* Crowding distance within each front (Deb et al. 2002): per objective m
+ * (in the order m = 0 .. M-1), the front's members in the order of (f_m,
+ * index); the first and last get +inf, every other member adds
+ * (f_m[next] - f_m[prev]) / (f_m,max - f_m,min) in fp64 when the range is
+ * not zero.  A member of a front of one or two points gets +inf. */
+void evox_ref_crowding(const float *F, int64_t n, int32_t M, const int32_t *front, double *crowd)
+{
+    int64_t *idx = (int64_t *)malloc(sizeof(int64_t) * (size_t)(n > 0 ? n : 1));
+    int32_t nf = 0;
+    for (int64_t i = 0; i < n; ++i) {
+        crowd[i] = 0.0;
+        if (front[i] + 1 > nf) nf = front[i] + 1;
+    }
+    for (int32_t k = 0; k < nf; ++k) {
+        int64_t c = 0;
+        for (int64_t i = 0; i < n; ++i)
+            if (front[i] == k) idx[c++] = i;
+        for (int32_t m = 0; m < M; ++m) {
+            /* insertion sort by (f_m, index) */
+            for (int64_t a = 1; a < c; ++a) {
+                const int64_t v = idx[a];
+                int64_t b = a;
+                while (b > 0 && (F[idx[b - 1] * M + m] > F[v * M + m] ||
+                                 (F[idx[b - 1] * M + m] == F[v * M + m] && idx[b - 1] > v))) {
+                    idx[b] = idx[b - 1];
+                    --b;
+                }
+                idx[b] = v;
+            }
+            if (c == 0) continue;
+            crowd[idx[0]] = INFINITY;
+            crowd[idx[c - 1]] = INFINITY;
+            const double lo = (double)F[idx[0] * M + m], hi = (double)F[idx[c - 1] * M + m];
+            if (hi > lo)
+                for (int64_t a = 1; a + 1 < c; ++a)
+                    crowd[idx[a]] += ((double)F[idx[a + 1] * M + m] - (double)F[idx[a - 1] * M + m]) / (hi - lo);
+        }
+    }
+    free(idx);
+}
+
+/* The crowded comparison of a binary tournament: the lower front wins, then
+ * the larger crowding distance, then the lower index. */
+static int64_t crowded_winner(int64_t a, int64_t b, const int32_t *front, const double *crowd)
+{
+    if (front[a] != front[b]) return front[a] < front[b] ? a : b;
+    if (crowd[a] != crowd[b]) return crowd[a] > crowd[b] ? a : b;
+    return a < b ? a : b;
+}
+
+/* The two parents of offspring pair p at generation t: tournaments between
+ * the individuals floor(w_q N / 2^32) named by the four words w_0..w_3 of
+ * Philox(seed, (0, p, t, 10)): (w_0, w_1) and (w_2, w_3). */
+void evox_ref_nsga2_parents(uint64_t seed, int64_t t, int64_t p, int64_t N, const int32_t *front,
+                            const double *crowd, int64_t *p1, int64_t *p2)
+{
+    int64_t c[4];
+    for (int q = 0; q < 4; ++q)
+        c[q] = (int64_t)(((uint64_t)evox_ref_philox_word(seed, 0, (uint32_t)p, (uint32_t)t, STREAM_NSGA_SEL, q) *
+                          (uint64_t)N) >> 32);
+    *p1 = crowded_winner(c[0], c[1], front, crowd);
+    *p2 = crowded_winner(c[2], c[3], front, crowd);
+}
+
+/* Polynomial mutation of x in [0, 1] with distribution index eta and draw
+ * u in [0, 1) (Deb and Goyal, 1996, in its bounded form): u < 1/2 moves
+ * down by 1 - (2u + (1 - 2u)(1 - x)^(eta+1))^(1/(eta+1)), u >= 1/2 up by
+ * 1 - (2(1 - u) + 2(u - 1/2) x^(eta+1))^(1/(eta+1)); clipped to [0, 1]. */
+double evox_ref_poly_mutate(double x, double u, double eta)
+{
+    const double e1 = eta + 1.0, inv = 1.0 / e1;
+    double y;
+    if (u < 0.5)
+        y = x + (pow(2.0 * u + (1.0 - 2.0 * u) * pow(1.0 - x, e1), inv) - 1.0);
+    else
+        y = x + (1.0 - pow(2.0 * (1.0 - u) + 2.0 * (u - 0.5) * pow(x, e1), inv));
+    return y < 0.0 ? 0.0 : y > 1.0 ? 1.0 : y;
+}
+
+/* Offspring 2p and 2p + 1 from parents a and b (rows of D floats in [0,1]).
+ * Per variable j, with the words w of Philox(seed, (j, p, t, 11)) and v of
+ * Philox(seed, (j, p, t, 12)), u(w) = the top 24 bits times 2^-24:
+ *   simulated binary crossover (Deb and Agrawal, 1995; crossover
+ *   probability 1): spread beta = (2u)^(1/(eta_c+1)) for u = u(w_0) <= 1/2,
+ *   else (2 - 2u)^(-1/(eta_c+1)); negated when w_1 is odd; 1 (the variable
+ *   is not crossed) when u(w_1) >= 1/2; children (a + b)/2 +- beta (a - b)/2
+ *   clipped to [0, 1] and rounded to fp32;
+ *   polynomial mutation of child q (q = 0, 1) when u(w_{2+q}) < 1/D, with
+ *   draw u(v_q), rounded to fp32.
+ * Arithmetic in fp64. */
+void evox_ref_nsga2_offspring(const evox_ref_nsga2_params *P, int64_t t, int64_t p, const float *a,
+                              const float *b, float *c0, float *c1)
+{
+    const double ec = (double)P->eta_c, em = (double)P->eta_m, pm = 1.0 / (double)P->D;
+    for (int64_t j = 0; j < P->D; ++j) {
+        uint32_t w[4], v[2];
+        for (int q = 0; q < 4; ++q)
+            w[q] = evox_ref_philox_word(P->seed, (uint32_t)j, (uint32_t)p, (uint32_t)t, STREAM_NSGA_VAR, q);
+        for (int q = 0; q < 2; ++q)
+            v[q] = evox_ref_philox_word(P->seed, (uint32_t)j, (uint32_t)p, (uint32_t)t, STREAM_NSGA_MUT, q);
+        const double u = (double)evox_ref_u01(w[0]);
+        double beta = u <= 0.5 ? pow(2.0 * u, 1.0 / (ec + 1.0)) : pow(2.0 - 2.0 * u, -1.0 / (ec + 1.0));
+        if (w[1] & 1u) beta = -beta;
+        if ((double)evox_ref_u01(w[1]) >= 0.5) beta = 1.0;
+        const double xa = (double)a[j], xb = (double)b[j];
+        double y[2] = {0.5 * (xa + xb) + 0.5 * beta * (xa - xb), 0.5 * (xa + xb) - 0.5 * beta * (xa - xb)};
+        float out[2];
+        for (int q = 0; q < 2; ++q) {
+            const double yc = y[q] < 0.0 ? 0.0 : y[q] > 1.0 ? 1.0 : y[q];
+            out[q] = (float)yc;
+            if ((double)evox_ref_u01(w[2 + q]) < pm)
+                out[q] = (float)evox_ref_poly_mutate((double)out[q], (double)evox_ref_u01(v[q]), em);
+        }
+        c0[j] = out[0];
+        c1[j] = out[1];
+    }
+}
+
+/* Initial population: x ~ U[0, 1) from stream 0 (the uniform initial
+ * population with lb = 0, ub = 1), its objectives, fronts and crowding. */
+int evox_ref_nsga2_init(const evox_ref_nsga2_params *P, float *X, float *F, int32_t *front, double *crowd)
+{
+    if (P->N < 2 || (P->N & 1) || P->M < 2 || P->M > 64 || P->D < P->M) return -1;
+    evox_ref_init_uniform(P->seed, STREAM_INIT_X, P->N, P->D, 0.0f, 1.0f, X);
+    evox_ref_dtlz1_rows(X, P->N, P->D, P->M, F);
+    evox_ref_nds(F, P->N, P->M, front);
+    evox_ref_crowding(F, P->N, P->M, front, crowd);
+    return 0;
+}
+
+/* n_gens generations from generation t0: offspring Q (pairs p < N/2 from
+ * tournament parents), R = (P, Q) with P first, fronts and crowding of R,
+ * then the survivors: whole fronts in order while they fit, and from the
+ * first front that does not fit, its members of largest crowding distance
+ * (ties: lower index in R) up to N; the survivors keep their order in R and
+ * their fronts and crowding distances. */
+int evox_ref_nsga2_step(const evox_ref_nsga2_params *P, int64_t t0, int64_t n_gens, float *X, float *F,
+                        int32_t *front, double *crowd)
+{
+    const int64_t N = P->N, D = P->D, R = 2 * P->N;
+    const int32_t M = P->M;
+    if (N < 2 || (N & 1) || M < 2 || M > 64 || D < M || n_gens < 0) return -1;
+    float *XR = (float *)malloc(sizeof(float) * (size_t)(R * D));
+    float *FR = (float *)malloc(sizeof(float) * (size_t)(R * M));
+    int32_t *fr = (int32_t *)malloc(sizeof(int32_t) * (size_t)R);
+    double *cr = (double *)malloc(sizeof(double) * (size_t)R);
+    char *keep = (char *)malloc((size_t)R);
+    if (!XR || !FR || !fr || !cr || !keep) {
+        free(XR); free(FR); free(fr); free(cr); free(keep);
+        return -1;
+    }
+    for (int64_t t = t0; t < t0 + n_gens; ++t) {
+        memcpy(XR, X, sizeof(float) * (size_t)(N * D));
+        memcpy(FR, F, sizeof(float) * (size_t)(N * M));
+        for (int64_t p = 0; p < N / 2; ++p) {
+            int64_t a, b;
+            evox_ref_nsga2_parents(P->seed, t, p, N, front, crowd, &a, &b);
+            evox_ref_nsga2_offspring(P, t, p, X + a * D, X + b * D, XR + (N + 2 * p) * D, XR + (N + 2 * p + 1) * D);
+        }
+        evox_ref_dtlz1_rows(XR + N * D, N, D, M, FR + N * M);
+        const int32_t nf = evox_ref_nds(FR, R, M, fr);
+        evox_ref_crowding(FR, R, M, fr, cr);
+        int64_t taken = 0;
+        for (int64_t i = 0; i < R; ++i) keep[i] = 0;
+        for (int32_t k = 0; k < nf && taken < N; ++k) {
+            int64_t size = 0;
+            for (int64_t i = 0; i < R; ++i) size += fr[i] == k;
+            if (taken + size <= N) {
+                for (int64_t i = 0; i < R; ++i)
+                    if (fr[i] == k) keep[i] = 1;
+                taken += size;
+            } else {
+                /* members of front k by (crowding descending, index) */
+                while (taken < N) {
+                    int64_t best = -1;
+                    for (int64_t i = 0; i < R; ++i)
+                        if (fr[i] == k && !keep[i] && (best < 0 || cr[i] > cr[best])) best = i;
+                    keep[best] = 1;
+                    ++taken;
+                }
+            }
+        }
+        int64_t q = 0;
+        for (int64_t i = 0; i < R; ++i)
+            if (keep[i]) {
+                memcpy(X + q * D, XR + i * D, sizeof(float) * (size_t)D);
+                memcpy(F + q * M, FR + i * M, sizeof(float) * (size_t)M);
+                front[q] = fr[i];
+                crowd[q] = cr[i];
+                ++q;
+            }
+    }
+    free(XR); free(FR); free(fr); free(cr); free(keep);
     return 0;
 }

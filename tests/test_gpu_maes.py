@@ -197,3 +197,35 @@ def test_rejects_bad_sizes(evox_gpu):
     for N, D in ((1, 10), (16385, 10), (10, 0)):
         with pytest.raises(ev.EvoxError):
             ev.Swarm(ev.make_params(ev.MAES, SPHERE, N, D, -1.0, 1.0))
+
+
+def test_full_size_first_generation(evox_gpu, ref):
+    """The benchmark's size, N = 100, D = 16384, one generation from the
+    initial state.  With M = I the steps are the deviates exactly (every
+    product but one is zero), so each sample's fitness is checked against
+    F(fma(sigma, z_k, y)) from the oracle's deviates and evaluation; the
+    parents against the oracle order of those values; and the new M, which
+    is I T with T symmetric, for symmetry on sampled rows."""
+    N, D, seed, sigma = 100, 16384, 10, 1.0
+    g = evox_gpu.Swarm(evox_gpu.make_params(evox_gpu.MAES, SPHERE, N, D, -5.0, 5.0, seed=seed, es_sigma=sigma))
+    y0 = ref.init_uniform(seed, 0, 1, D, -5.0, 5.0)[0].astype(np.float64)
+    g.step(1)
+    z = ref.maes_deviates(seed, 0, N, D).astype(np.float64)
+    X = (np.float64(np.float32(sigma)) * z + y0).astype(np.float32)
+    f_ref = ref.evaluate(SPHERE, X).astype(np.float64)
+    f_gpu = g.fit.cpu().numpy().astype(np.float64)
+    ftol = 2 * (tol(SPHERE, X, f_ref) + (2 * np.abs(X.astype(np.float64)) * 2e-6 * np.maximum(1, np.abs(z))).sum(1))
+    bad = np.nonzero(np.abs(f_gpu - f_ref) > ftol)[0]
+    assert bad.size == 0, f"sample fitness off at {bad[:5]}"
+    order = np.lexsort((np.arange(N), f_ref))
+    gorder = np.lexsort((np.arange(N), f_gpu))
+    for p in np.nonzero(gorder != order)[0]:
+        a, b = gorder[p], order[p]
+        assert abs(f_ref[a] - f_ref[b]) <= ftol[a] + ftol[b], f"rank {p}: {a} vs {b}"
+    rows = np.random.default_rng(1).choice(D, 48, replace=False)
+    Mr = g.mat[torch.from_numpy(rows).cuda()][:, :D].cpu().numpy().astype(np.float64)
+    Mc = g.mat[:, torch.from_numpy(rows).cuda()].cpu().numpy().astype(np.float64).T
+    assert np.all(np.isfinite(Mr))
+    assert np.allclose(Mr, Mc, rtol=1e-5, atol=1e-7), np.abs(Mr - Mc).max()
+    sig = float(g.sigma.cpu()[0])
+    assert np.isfinite(sig) and 0 < sig
