@@ -63,7 +63,8 @@ enum evox_fn {
     EVOX_SCHWEFEL = 5
 };
 
-enum evox_algo { EVOX_PSO = 0, EVOX_CSO = 1, EVOX_DE = 2, EVOX_ES = 3, EVOX_PGPE = 4, EVOX_MAES = 5 };
+enum evox_algo { EVOX_PSO = 0, EVOX_CSO = 1, EVOX_DE = 2, EVOX_ES = 3, EVOX_PGPE = 4, EVOX_MAES = 5,
+                 EVOX_NSGA2 = 6 };
 
 enum evox_status {
     EVOX_OK = 0,
@@ -78,11 +79,12 @@ enum evox_status {
 
 /* Immutable hyperparameters (theta of Sec. IV-B), fixed at creation. */
 typedef struct evox_params {
-    int32_t algo;     /* EVOX_PSO, EVOX_CSO, EVOX_DE, EVOX_ES (OpenES), EVOX_PGPE or EVOX_MAES
-                         (CMA-ES as matrix adaptation) */
-    int32_t fn_id;    /* enum evox_fn */
+    int32_t algo;     /* EVOX_PSO, EVOX_CSO, EVOX_DE, EVOX_ES (OpenES), EVOX_PGPE, EVOX_MAES
+                         (CMA-ES as matrix adaptation) or EVOX_NSGA2 (on DTLZ1) */
+    int32_t fn_id;    /* enum evox_fn (NSGA2: ignored, the problem is DTLZ1) */
     int64_t N;        /* population size: PSO 1 .. 2^31 - 1, CSO 2 .. 2^24, DE 4 .. 2^31 - 1,
-                         ES / PGPE even, 2 .. 16384 (N / 2 antithetic pairs), MAES 2 .. 16384 */
+                         ES / PGPE even, 2 .. 16384 (N / 2 antithetic pairs), MAES 2 .. 16384,
+                         NSGA2 even, 4 .. 32768 */
     int64_t D;        /* dimension, 1 .. EVOX_MAX_D */
     int64_t ldx;      /* row pitch of x, v, pbest in floats: ldx >= D, ldx % 4 == 0 */
     float lb, ub;     /* x_init 0: initial positions ~ U[lb, ub): x = fma(u, ub - lb, lb);
@@ -103,6 +105,10 @@ typedef struct evox_params {
     float pgpe_sigma_lr;    /* PGPE deviation learning rate */
     float pgpe_max_change;  /* PGPE bound on a deviation's relative change per generation */
     uint64_t seed;    /* Philox key */
+    int32_t n_obj;    /* NSGA2: objectives of DTLZ1, 2 .. 8 (D >= n_obj) */
+    float sbx_eta;    /* NSGA2: distribution index of the simulated binary crossover */
+    float pm_eta;     /* NSGA2: distribution index of the polynomial mutation */
+    int32_t reserved; /* zero */
 } evox_params;
 
 /* Caller-owned device buffers, borrowed by the state (row-major, pitch ldx;
@@ -118,6 +124,11 @@ typedef struct evox_params {
  *        fitness of the last generation's samples; the rest unused.
  *   PGPE: as ES, and v [ldx] = the per-dimension deviations sigma (es_sigma
  *        at creation, padding 0).
+ *   NSGA2: x [N][ldx] = the population in [0, 1]^D (uniform at creation,
+ *        lb and ub ignored), obj [N][n_obj] = its DTLZ1 objectives, front [N]
+ *        = each individual's 0-based front and crowd [N] = its crowding
+ *        distance within that front (of the merged population it survived);
+ *        the rest unused.
  *   MAES: x [ldx] = the center y (as ES), v [ldx] = the evolution path s
  *        (zero at creation), mat [D][ldx] = the transformation matrix M
  *        (identity at creation; M M^T plays the covariance matrix), sigma [1]
@@ -129,6 +140,9 @@ typedef struct evox_params {
 typedef struct evox_buffers {
     float *x, *v, *pbest, *pfit, *fit, *gbest, *xbar;
     float *mat, *sigma;  /* MAES only */
+    float *obj;          /* NSGA2 only: objectives */
+    int32_t *front;      /* NSGA2 only */
+    double *crowd;       /* NSGA2 only */
     void *scratch;
     size_t scratch_bytes;
 } evox_buffers;
@@ -272,6 +286,41 @@ int evox_pgpe_step(evox_state *state, int64_t n_gens);
  * evox_best reports the best sample of the last generation and the center y
  * as the solution. */
 int evox_maes_step(evox_state *state, int64_t n_gens);
+
+/* n_gens generations of NSGA-II (Table II; Sec. V-A runs it on DTLZ1) after
+ * Deb, Pratap, Agarwal and Meyarivan (IEEE TEVC 6(2), 2002).  Generation t:
+ *   - offspring pair p < N/2 from two crowded binary tournaments (candidates
+ *     floor(w_q N / 2^32) for the words w_0..w_3 of Philox(seed, (0, p, t,
+ *     10)); the lower front wins, then the larger crowding distance, then
+ *     the lower index);
+ *   - per variable j, words w of Philox(seed, (j, p, t, 11)) and v of
+ *     (j, p, t, 12), u(w) = top 24 bits x 2^-24: simulated binary crossover
+ *     with spread (2u)^(1/(sbx_eta+1)) for u = u(w_0) <= 1/2, else
+ *     (2 - 2u)^(-1/(sbx_eta+1)), negated when w_1 is odd, 1 (no crossing)
+ *     when u(w_1) >= 1/2; children (a + b)/2 +- beta (a - b)/2 clipped to
+ *     [0, 1]; polynomial mutation (index pm_eta) of child q when u(w_{2+q})
+ *     < 1/D with draw u(v_q); fp64, each child rounded to fp32 once;
+ *   - DTLZ1 objectives of the offspring (fp64, rounded once);
+ *   - non-dominated fronts and crowding distances of parents and offspring
+ *     together (parents first), then the survivors: whole fronts while
+ *     they fit, and from the next front its members of largest crowding
+ *     distance (lower index on ties), kept in their merged order.
+ * Synchronizes the stream once per front sorted.  evox_best returns
+ * EVOX_EINVAL for this algorithm (there is no single best). */
+int evox_nsga2_step(evox_state *state, int64_t n_gens);
+
+/* Non-dominated sorting and crowding distances (the sorting step of
+ * NSGA-II) of n points with M objectives (minimised): F (device, fp32,
+ * [n][M], no NaN), front (device, int32 [n]) receives every point's 0-based
+ * front, crowd (device, fp64 [n]) its crowding distance within the front
+ * (per objective in order 0..M-1: +inf at either end of the front's order
+ * of (value, index), else + (next - previous) / (last - first) when that
+ * range is not zero).  1 <= n <= 65536, 2 <= M <= 8; scratch (device,
+ * 256-byte aligned) of evox_nsga2_sort_scratch_bytes(n, M) bytes.  Returns
+ * when the result is in place (the stream is synchronized once per front). */
+size_t evox_nsga2_sort_scratch_bytes(int64_t n, int32_t M);
+int evox_nsga2_sort(const float *F, int64_t n, int32_t M, int32_t *front, double *crowd, void *scratch,
+                    size_t scratch_bytes, void *hip_stream);
 
 /* If the caller has changed x (or fit) of a CSO state, recompute xbar from x
  * and, when refit is nonzero, fit = F(x). */

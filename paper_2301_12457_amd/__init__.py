@@ -15,7 +15,7 @@ LIB_PATH = os.path.join(HERE, "libevox.so")
 SPHERE, ACKLEY, RASTRIGIN, GRIEWANK, ROSENBROCK, SCHWEFEL = range(6)
 FN_IDS = {"sphere": SPHERE, "ackley": ACKLEY, "rastrigin": RASTRIGIN, "griewank": GRIEWANK,
           "rosenbrock": ROSENBROCK, "schwefel": SCHWEFEL}
-PSO, CSO, DE, ES, PGPE, MAES = 0, 1, 2, 3, 4, 5
+PSO, CSO, DE, ES, PGPE, MAES, NSGA2 = 0, 1, 2, 3, 4, 5, 6
 OK, EINVAL, EHIP, ENOSPC, EALIGN = 0, -1, -2, -3, -4
 MAX_D = 32768
 
@@ -23,7 +23,8 @@ MAX_D = 32768
 EXPORTS = (
     "evox_scratch_bytes", "evox_state_create", "evox_state_destroy", "evox_eval", "evox_eval_ld",
     "evox_eval_argmin_scratch_bytes", "evox_eval_argmin", "evox_pso_step", "evox_cso_step",
-    "evox_de_step", "evox_es_step", "evox_pgpe_step", "evox_maes_step",
+    "evox_de_step", "evox_es_step", "evox_pgpe_step", "evox_maes_step", "evox_nsga2_step",
+    "evox_nsga2_sort_scratch_bytes", "evox_nsga2_sort",
     "evox_cso_refresh", "evox_best", "evox_generation", "evox_row_layout", "evox_default_ldx",
     "evox_fill_normal", "evox_sgemm", "evox_copy", "evox_philox_fill", "evox_permutation_scratch_bytes",
     "evox_permutation", "evox_argsort_u32",
@@ -51,12 +52,14 @@ class Params(ctypes.Structure):
         ("es_sigma", ctypes.c_float), ("es_lr", ctypes.c_float),
         ("pgpe_sigma_lr", ctypes.c_float), ("pgpe_max_change", ctypes.c_float),
         ("seed", ctypes.c_uint64),
+        ("n_obj", ctypes.c_int32), ("sbx_eta", ctypes.c_float), ("pm_eta", ctypes.c_float),
+        ("reserved", ctypes.c_int32),
     ]
 
 
 class Buffers(ctypes.Structure):
     _fields_ = [(n, ctypes.c_void_p) for n in ("x", "v", "pbest", "pfit", "fit", "gbest", "xbar", "mat",
-                                                "sigma")] + [
+                                                "sigma", "obj", "front", "crowd")] + [
         ("scratch", ctypes.c_void_p), ("scratch_bytes", ctypes.c_size_t)]
 
 
@@ -87,6 +90,9 @@ def lib():
             "evox_es_step": ([P, i64], i32),
             "evox_pgpe_step": ([P, i64], i32),
             "evox_maes_step": ([P, i64], i32),
+            "evox_nsga2_step": ([P, i64], i32),
+            "evox_nsga2_sort_scratch_bytes": ([i64, i32], ctypes.c_size_t),
+            "evox_nsga2_sort": ([P, i64, i32, P, P, P, ctypes.c_size_t, P], i32),
             "evox_cso_refresh": ([P, i32], i32),
             "evox_best": ([P, P, P, P], i32),
             "evox_generation": ([P], i64),
@@ -185,6 +191,21 @@ def evox_sgemm(A, B, C, trans_a=False, trans_b=False, alpha=1.0, beta=0.0, strea
     return C
 
 
+def evox_nsga2_sort(F, front, crowd, scratch=None, stream=None):
+    """Fronts (int32) and crowding distances (float64) of the rows of F
+    [n, M] (fp32 device tensor), through the library's sort."""
+    import torch
+    n, M = F.shape
+    nbytes = int(lib().evox_nsga2_sort_scratch_bytes(n, M))
+    if nbytes == 0:
+        _check(EINVAL)
+    if scratch is None:
+        scratch = torch.empty((nbytes + 255) // 256 * 64, dtype=torch.int32, device=F.device)
+    _check(lib().evox_nsga2_sort(_ptr(F), n, M, _ptr(front), _ptr(crowd), _ptr(scratch), scratch.numel() * 4,
+                                 _stream(stream)))
+    return front, crowd
+
+
 def evox_copy(src, dst, n, stream=None):
     """dst[:n] = src[:n] by the library's streaming copy (bandwidth reference)."""
     _check(lib().evox_copy(_ptr(src), _ptr(dst), n, _stream(stream)))
@@ -216,12 +237,13 @@ def pitch(D, algo=PSO):
 
 def make_params(algo, fn_id, N, D, lb, ub, v_lo=0.0, v_hi=0.0, w=0.6, c1=1.5, c2=1.5, phi=0.1,
                 vmax=0.0, clamp_x=0, seed=0, ldx=None, x_init=0, x_mu=0.0, x_sigma=1.0, de_f=0.5,
-                de_cr=0.9, es_sigma=0.1, es_lr=0.01, pgpe_sigma_lr=0.01, pgpe_max_change=0.2):
+                de_cr=0.9, es_sigma=0.1, es_lr=0.01, pgpe_sigma_lr=0.01, pgpe_max_change=0.2, n_obj=3,
+                sbx_eta=20.0, pm_eta=20.0):
     return Params(algo=algo, fn_id=fn_id, N=N, D=D, ldx=pitch(D, algo) if ldx is None else ldx,
                   lb=lb, ub=ub, v_lo=v_lo, v_hi=v_hi, w=w, c1=c1, c2=c2, phi=phi, vmax=vmax,
                   clamp_x=clamp_x, x_init=x_init, x_mu=x_mu, x_sigma=x_sigma, de_f=de_f,
                   de_cr=de_cr, es_sigma=es_sigma, es_lr=es_lr, pgpe_sigma_lr=pgpe_sigma_lr,
-                  pgpe_max_change=pgpe_max_change, seed=seed)
+                  pgpe_max_change=pgpe_max_change, seed=seed, n_obj=n_obj, sbx_eta=sbx_eta, pm_eta=pm_eta)
 
 
 def evox_scratch_bytes(params):
@@ -229,7 +251,7 @@ def evox_scratch_bytes(params):
 
 
 class Swarm:
-    """A PSO, CSO, DE, OpenES, PGPE or MA-ES state over torch-allocated device buffers.
+    """A PSO, CSO, DE, OpenES, PGPE, MA-ES or NSGA-II state over torch-allocated device buffers.
 
     x, v (and pbest) are [N, ldx] float32 tensors whose first D columns are the
     population; pfit / fit are [N]; gbest / xbar are [ldx].  DE has x and fit
@@ -237,6 +259,8 @@ class Swarm:
     center theta [ldx] and fit = the last generation's sample fitness [N];
     PGPE also v = the per-dimension deviations [ldx].  MA-ES has x = the center
     y [ldx], v = the path s [ldx], mat = M [D, ldx], sigma [1] and fit [N].
+    NSGA-II has x [N, ldx], obj [N, n_obj] (DTLZ1), front [N] (int32) and
+    crowd [N] (float64).
     """
 
     def __init__(self, params: Params, device="cuda", stream=None):
@@ -252,7 +276,13 @@ class Swarm:
                   else torch.empty((ldx,), **f32) if params.algo in (PGPE, MAES) else None)
         self.mat = torch.empty((params.D, ldx), **f32) if params.algo == MAES else None
         self.sigma = torch.empty((1,), **f32) if params.algo == MAES else None
-        if params.algo in (DE, ES, PGPE, MAES):
+        nsga = params.algo == NSGA2
+        self.obj = torch.empty((N, params.n_obj), **f32) if nsga else None
+        self.front = torch.empty((N,), dtype=torch.int32, device=device) if nsga else None
+        self.crowd = torch.empty((N,), dtype=torch.float64, device=device) if nsga else None
+        if nsga:
+            self.pbest = self.pfit = self.gbest = self.xbar = self.fit = None
+        elif params.algo in (DE, ES, PGPE, MAES):
             self.pbest = self.pfit = self.gbest = self.xbar = None
             self.fit = torch.empty((N,), **f32)
         elif params.algo == PSO:
@@ -272,6 +302,7 @@ class Swarm:
         self.buffers = Buffers(x=_ptr(self.x), v=_ptr(self.v), pbest=_ptr(self.pbest),
                                pfit=_ptr(self.pfit), fit=_ptr(self.fit), gbest=_ptr(self.gbest),
                                xbar=_ptr(self.xbar), mat=_ptr(self.mat), sigma=_ptr(self.sigma),
+                               obj=_ptr(self.obj), front=_ptr(self.front), crowd=_ptr(self.crowd),
                                scratch=_ptr(self.scratch),
                                scratch_bytes=self.scratch.numel() * 4)
         self.handle = ctypes.c_void_p()
@@ -303,8 +334,10 @@ class Swarm:
             _check(lib().evox_es_step(self.handle, n_gens))
         elif self.P.algo == PGPE:
             _check(lib().evox_pgpe_step(self.handle, n_gens))
-        else:
+        elif self.P.algo == MAES:
             _check(lib().evox_maes_step(self.handle, n_gens))
+        else:
+            _check(lib().evox_nsga2_step(self.handle, n_gens))
 
     def refresh(self, refit=True):
         _check(lib().evox_cso_refresh(self.handle, 1 if refit else 0))

@@ -38,6 +38,7 @@ def _units():
     units.append((os.path.join(CSRC, "evox_common.hip"), "evox_common.o", []))
     units.append((os.path.join(CSRC, "evox_gemm.hip"), "evox_gemm.o", []))
     units.append((os.path.join(CSRC, "evox_maes.hip"), "evox_maes.o", []))
+    units.append((os.path.join(CSRC, "evox_nsga2.hip"), "evox_nsga2.o", []))
     units.append((os.path.join(CSRC, "evox_api.cpp"), "evox_api.o", ["-x", "hip"]))
     return units
 

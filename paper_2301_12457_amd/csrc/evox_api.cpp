@@ -64,6 +64,12 @@ int grid_for(int64_t groups, int G, int64_t cap)
     return (int)g;
 }
 
+template <typename T>
+T *at_off(void *base, size_t off)
+{
+    return reinterpret_cast<T *>(static_cast<char *>(base) + off);
+}
+
 struct Plan {
     Layout L{0, 0, 0};
     int grid = 0, cso_grid = 0, colsum_grid = 0, bits = 0;
@@ -78,8 +84,44 @@ struct Plan {
     size_t mae_z = 0, mae_d = 0, mae_work = 0, mae_at = 0, mae_bt = 0, mae_sel = 0, mae_w = 0, mae_part = 0;
     int mae_splits = 1;
     int64_t mae_mu = 0, mae_kp = 0, mae_ldf = 0;
+    // NSGA-II: offspring, survivors' rows, merged objectives / fronts /
+    // crowding, the sorting scratch, survivor flags and their prefix sums
+    size_t ns_q = 0, ns_x2 = 0, ns_fr = 0, ns_frontr = 0, ns_crowdr = 0, ns_keep = 0, ns_pre = 0;
+    size_t ns_cnt = 0, ns_list = 0, ns_foff = 0, ns_pos = 0, ns_sorted = 0, ns_len = 0;
     size_t total = 0;
 };
+
+// Scratch of the non-dominated sorting of n points with M objectives,
+// placed from `off` on: counts, the front-ordered list, front offsets, the
+// per-objective positions and orders, the list length.
+struct NsgaSortScratch {
+    size_t cnt, list, foff, pos, sorted, len, end;
+};
+NsgaSortScratch nsga_sort_layout(int64_t n, int32_t M, size_t off)
+{
+    NsgaSortScratch l{};
+    auto take = [&](size_t bytes) {
+        const size_t at = off;
+        off = round256(off + bytes);
+        return at;
+    };
+    l.cnt = take(4 * (size_t)n);
+    l.list = take(4 * (size_t)n);
+    l.foff = take(4 * ((size_t)n + 1));
+    l.pos = take(4 * (size_t)M * (size_t)n);
+    l.sorted = take(4 * (size_t)M * (size_t)n);
+    l.len = take(4);
+    l.end = off;
+    return l;
+}
+
+NsgaSortArgs nsga_sort_args(void *scratch, const NsgaSortScratch &l, const float *F, int64_t n, int32_t M,
+                            int32_t *front, double *crowd)
+{
+    return NsgaSortArgs{F, n, M, front, crowd, at_off<uint32_t>(scratch, l.cnt), at_off<int32_t>(scratch, l.list),
+                        at_off<int32_t>(scratch, l.foff), at_off<int32_t>(scratch, l.pos),
+                        at_off<int32_t>(scratch, l.sorted), n, at_off<uint32_t>(scratch, l.len)};
+}
 
 // K-slices of the sampling product (N + 1) x D x D: a small population gives
 // few output tiles, so the product is split along K until the blocks fill
@@ -112,7 +154,7 @@ int make_plan(const evox_params *P, Plan *pl)
 {
     if (!P) return fail(EVOX_EINVAL, "params is null");
     if (P->algo != EVOX_PSO && P->algo != EVOX_CSO && P->algo != EVOX_DE && P->algo != EVOX_ES &&
-        P->algo != EVOX_PGPE && P->algo != EVOX_MAES)
+        P->algo != EVOX_PGPE && P->algo != EVOX_MAES && P->algo != EVOX_NSGA2)
         return fail(EVOX_EINVAL, "unknown algo %d", P->algo);
     const bool es_like = P->algo == EVOX_ES || P->algo == EVOX_PGPE;
     if (P->fn_id < 0 || P->fn_id >= FN_COUNT) return fail(EVOX_EINVAL, "unknown fn_id %d", P->fn_id);
@@ -127,6 +169,15 @@ int make_plan(const evox_params *P, Plan *pl)
         return fail(EVOX_EINVAL, "ES / PGPE N = %lld must be even, in [2, %d]", (long long)P->N, kEsMaxN);
     if (P->algo == EVOX_MAES && (P->N < 2 || P->N > kEsMaxN))
         return fail(EVOX_EINVAL, "MAES N = %lld out of range [2, %d]", (long long)P->N, kEsMaxN);
+    if (P->algo == EVOX_NSGA2) {
+        if (P->N < 4 || (P->N & 1) || P->N > kNsgaMaxN)
+            return fail(EVOX_EINVAL, "NSGA2 N = %lld must be even, in [4, %lld]", (long long)P->N,
+                        (long long)kNsgaMaxN);
+        if (P->n_obj < 2 || P->n_obj > kNsgaMaxM || P->D < P->n_obj)
+            return fail(EVOX_EINVAL, "NSGA2 n_obj = %d must be in [2, %d] and <= D", P->n_obj, kNsgaMaxM);
+        if (!(P->sbx_eta >= 0.0f) || !(P->pm_eta >= 0.0f))
+            return fail(EVOX_EINVAL, "NSGA2 distribution indices must be >= 0");
+    }
     if (P->ldx < P->D || (P->ldx & 3))
         return fail(EVOX_EINVAL, "ldx = %lld must be >= D and a multiple of 4", (long long)P->ldx);
     if (P->x_init != 0 && P->x_init != 1) return fail(EVOX_EINVAL, "unknown x_init %d", P->x_init);
@@ -191,6 +242,24 @@ int make_plan(const evox_params *P, Plan *pl)
         p.mae_w = take(sizeof(double) * (size_t)p.mae_mu);
         p.mae_part = take(sizeof(double) * ((D + kMaeBlock - 1) / kMaeBlock));
     }
+    if (P->algo == EVOX_NSGA2) {
+        const size_t N = (size_t)P->N, R = 2 * N, M = (size_t)P->n_obj;
+        p.ns_q = take(sizeof(float) * N * (size_t)P->ldx);
+        p.ns_x2 = take(sizeof(float) * N * (size_t)P->ldx);
+        p.ns_fr = take(sizeof(float) * R * M);
+        p.ns_frontr = take(sizeof(int32_t) * R);
+        p.ns_crowdr = take(sizeof(double) * R);
+        p.ns_keep = take(sizeof(int32_t) * R);
+        p.ns_pre = take(sizeof(int32_t) * R);
+        const NsgaSortScratch l = nsga_sort_layout((int64_t)R, P->n_obj, off);
+        p.ns_cnt = l.cnt;
+        p.ns_list = l.list;
+        p.ns_foff = l.foff;
+        p.ns_pos = l.pos;
+        p.ns_sorted = l.sorted;
+        p.ns_len = l.len;
+        off = l.end;
+    }
     p.total = off;
     *pl = p;
     return EVOX_OK;
@@ -217,6 +286,8 @@ struct evox_state {
     float mae_beta;    // 1 - (c_1 + c_w) / 2
     float *mae_work;
     std::vector<double> mae_w;  // the weights, host copy of the device table
+    NsgaSortArgs ns_sort;       // NSGA-II: sorting of the merged population
+    NsgaSelArgs ns_sel;         // NSGA-II: survivor selection
     // profiling of the fused generation kernel
     bool prof;
     std::vector<std::pair<hipEvent_t, hipEvent_t>> ev;
@@ -337,11 +408,14 @@ int evox_state_create(const evox_params *params, const evox_buffers *b, void *hi
         return fail(EVOX_EINVAL, "DE, ES, PGPE and MAES need fit");
     if (P.algo == EVOX_MAES && (!b->v || !b->mat || !b->sigma))
         return fail(EVOX_EINVAL, "MAES needs v (the path), mat and sigma");
+    if (P.algo == EVOX_NSGA2 && (!b->obj || !b->front || !b->crowd))
+        return fail(EVOX_EINVAL, "NSGA2 needs obj, front and crowd");
     if (P.algo == EVOX_PGPE && !b->v) return fail(EVOX_EINVAL, "PGPE needs v (the deviations)");
     if (P.algo == EVOX_PSO && (!b->pbest || !b->pfit || !b->gbest))
         return fail(EVOX_EINVAL, "PSO needs pbest, pfit and gbest");
     if (P.algo == EVOX_CSO && (!b->fit || !b->xbar)) return fail(EVOX_EINVAL, "CSO needs fit and xbar");
-    const void *ptrs[] = {b->x, b->v, b->pbest, b->pfit, b->fit, b->gbest, b->xbar, b->mat, b->sigma};
+    const void *ptrs[] = {b->x, b->v, b->pbest, b->pfit, b->fit, b->gbest, b->xbar, b->mat, b->sigma, b->obj,
+                          b->front, b->crowd};
     for (const void *p : ptrs)
         if (p && !aligned16(p)) return fail(EVOX_EALIGN, "buffer %p is not 16-byte aligned", p);
     if (((uintptr_t)b->scratch & 255u) != 0) return fail(EVOX_EALIGN, "scratch is not 256-byte aligned");
@@ -421,6 +495,22 @@ int evox_state_create(const evox_params *params, const evox_buffers *b, void *hi
         s->mae_beta = (float)(1.0 - 0.5 * (c1 + cw));
         if (pl.mae_splits > 1) s->mae_work = at<float>(b->scratch, pl.mae_work);
     }
+    s->ns_sort = NsgaSortArgs{};
+    s->ns_sel = NsgaSelArgs{};
+    if (P.algo == EVOX_NSGA2) {
+        const int64_t R = 2 * P.N;
+        float *FR = at<float>(b->scratch, pl.ns_fr);
+        int32_t *frontR = at<int32_t>(b->scratch, pl.ns_frontr);
+        double *crowdR = at<double>(b->scratch, pl.ns_crowdr);
+        s->ns_sort = NsgaSortArgs{FR, R, P.n_obj, frontR, crowdR, at<uint32_t>(b->scratch, pl.ns_cnt),
+                                  at<int32_t>(b->scratch, pl.ns_list), at<int32_t>(b->scratch, pl.ns_foff),
+                                  at<int32_t>(b->scratch, pl.ns_pos), at<int32_t>(b->scratch, pl.ns_sorted), R,
+                                  at<uint32_t>(b->scratch, pl.ns_len)};
+        s->ns_sel = NsgaSelArgs{b->x, at<float>(b->scratch, pl.ns_q), P.N, P.ldx, P.n_obj, FR, frontR, crowdR,
+                                s->ns_sort.list, at<int32_t>(b->scratch, pl.ns_keep),
+                                at<int32_t>(b->scratch, pl.ns_pre), at<float>(b->scratch, pl.ns_x2), b->obj,
+                                b->front, b->crowd};
+    }
     if (P.algo == EVOX_CSO) {
         s->hist = at<uint32_t>(b->scratch, pl.hist);
         s->offs = at<uint32_t>(b->scratch, pl.offs);
@@ -450,8 +540,9 @@ int evox_state_create(const evox_params *params, const evox_buffers *b, void *hi
     // ES / PGPE: x is the center, one row
     const bool own_v = P.algo == EVOX_PSO || P.algo == EVOX_CSO;
     const bool es_like = P.algo == EVOX_ES || P.algo == EVOX_PGPE || P.algo == EVOX_MAES;
+    const bool unit_box = P.algo == EVOX_NSGA2;  // DTLZ1's domain
     InitArgs ia{b->x, own_v ? b->v : nullptr, P.algo == EVOX_PSO ? b->pbest : nullptr,
-                es_like ? 1 : P.N, P.D, P.ldx, P.lb, P.ub,
+                es_like ? 1 : P.N, P.D, P.ldx, unit_box ? 0.0f : P.lb, unit_box ? 1.0f : P.ub,
                 P.v_lo, P.v_hi, P.v_lo == 0.0f && P.v_hi == 0.0f, P.x_init == 1, P.x_mu, P.x_sigma,
                 s->k0, s->k1};
     if ((e = launch_init(ia, s->stream)) != hipSuccess) {
@@ -462,7 +553,22 @@ int evox_state_create(const evox_params *params, const evox_buffers *b, void *hi
         delete s;
         return hip_fail(e, "init");
     }
-    if (P.algo == EVOX_PSO) {
+    if (P.algo == EVOX_NSGA2) {
+        // the offspring rows' padding stays zero; objectives, fronts and
+        // crowding of the initial population
+        NsgaSortArgs init = s->ns_sort;
+        init.F = b->obj;
+        init.n = P.N;
+        init.front = b->front;
+        init.crowd = b->crowd;
+        NsgaSortResult r;
+        if ((e = launch_fill(at<float>(b->scratch, pl.ns_q), P.N * P.ldx, 0.0f, s->stream)) != hipSuccess ||
+            (e = launch_nsga_dtlz1(b->x, P.N, P.D, P.ldx, P.n_obj, b->obj, s->stream)) != hipSuccess ||
+            (e = nsga_sort(init, P.N, &r, s->stream)) != hipSuccess) {
+            delete s;
+            return hip_fail(e, "init");
+        }
+    } else if (P.algo == EVOX_PSO) {
         if ((e = best_init(s, std::numeric_limits<float>::infinity(), 0)) != hipSuccess ||
             (e = launch_fill(b->pfit, P.N, std::numeric_limits<float>::infinity(), s->stream)) != hipSuccess ||
             (e = launch_copy_row(b->pbest, b->gbest, P.ldx, s->stream)) != hipSuccess) {
@@ -713,6 +819,35 @@ int es_generations(evox_state *s, int64_t n_gens, bool pgpe)
     return EVOX_OK;
 }
 
+int nsga_generations(evox_state *s, int64_t n_gens)
+{
+    if (n_gens < 0) return fail(EVOX_EINVAL, "n_gens = %lld < 0", (long long)n_gens);
+    if (s->t + n_gens >= ((int64_t)1 << 32)) return fail(EVOX_EINVAL, "generation counter would pass 2^32");
+    const evox_params &P = s->P;
+    const int32_t M = P.n_obj;
+    hipError_t e;
+    for (int64_t k = 0; k < n_gens; ++k) {
+        const uint32_t t = (uint32_t)(s->t + k);
+        NsgaVarArgs va{s->B.x, P.N, P.D, P.ldx, s->B.front, s->B.crowd, at<float>(s->B.scratch, s->pl.ns_q),
+                       (double)P.sbx_eta,
+                       (double)P.pm_eta, s->k0, s->k1, t};
+        NsgaSortResult r;
+        if ((e = launch_nsga_var(va, s->stream)) != hipSuccess) return hip_fail(e, "variation");
+        if ((e = launch_stream_copy(s->B.obj, (float *)s->ns_sort.F, P.N * M, s->stream)) != hipSuccess)
+            return hip_fail(e, "merge");
+        if ((e = launch_nsga_dtlz1(s->ns_sel.Q, P.N, P.D, P.ldx, M, (float *)s->ns_sort.F + P.N * M, s->stream)) !=
+            hipSuccess)
+            return hip_fail(e, "objectives");
+        if ((e = timed(s, [&] { return nsga_sort(s->ns_sort, P.N, &r, s->stream); })) != hipSuccess)
+            return hip_fail(e, "non-dominated sorting");
+        if ((e = launch_nsga_select(s->ns_sel, r, s->stream)) != hipSuccess) return hip_fail(e, "selection");
+        if ((e = launch_stream_copy(s->ns_sel.X2, s->B.x, P.N * P.ldx, s->stream)) != hipSuccess)
+            return hip_fail(e, "survivors");
+    }
+    s->t += n_gens;
+    return EVOX_OK;
+}
+
 int mae_generations(evox_state *s, int64_t n_gens)
 {
     if (n_gens < 0) return fail(EVOX_EINVAL, "n_gens = %lld < 0", (long long)n_gens);
@@ -765,6 +900,37 @@ int evox_pgpe_step(evox_state *s, int64_t n_gens)
     return es_generations(s, n_gens, true);
 }
 
+int evox_nsga2_step(evox_state *s, int64_t n_gens)
+{
+    if (!s) return fail(EVOX_EINVAL, "state is null");
+    if (s->P.algo != EVOX_NSGA2) return fail(EVOX_EINVAL, "evox_nsga2_step on a state of another algorithm");
+    return nsga_generations(s, n_gens);
+}
+
+size_t evox_nsga2_sort_scratch_bytes(int64_t n, int32_t M)
+{
+    if (n < 1 || n > EVOX_ARGSORT_MAX_N || M < 2 || M > kNsgaMaxM) return 0;
+    return nsga_sort_layout(n, M, 0).end;
+}
+
+int evox_nsga2_sort(const float *F, int64_t n, int32_t M, int32_t *front, double *crowd, void *scratch,
+                    size_t scratch_bytes, void *hip_stream)
+{
+    if (n < 1 || n > EVOX_ARGSORT_MAX_N || M < 2 || M > kNsgaMaxM)
+        return fail(EVOX_EINVAL, "n = %lld, M = %d: need 1 <= n <= %d, 2 <= M <= %d", (long long)n, M,
+                    EVOX_ARGSORT_MAX_N, kNsgaMaxM);
+    if (!F || !front || !crowd || !scratch) return fail(EVOX_EINVAL, "F, front, crowd and scratch are required");
+    if (((uintptr_t)F & 3u) || ((uintptr_t)front & 3u) || ((uintptr_t)crowd & 7u))
+        return fail(EVOX_EALIGN, "F, front or crowd is misaligned");
+    if (((uintptr_t)scratch & 255u) != 0) return fail(EVOX_EALIGN, "scratch is not 256-byte aligned");
+    const NsgaSortScratch l = nsga_sort_layout(n, M, 0);
+    if (scratch_bytes < l.end) return fail(EVOX_ENOSPC, "scratch has %zu bytes, needs %zu", scratch_bytes, l.end);
+    NsgaSortResult r;
+    hipError_t e = nsga_sort(nsga_sort_args(scratch, l, F, n, M, front, crowd), n, &r, (hipStream_t)hip_stream);
+    if (e != hipSuccess) return hip_fail(e, "non-dominated sorting");
+    return EVOX_OK;
+}
+
 int evox_maes_step(evox_state *s, int64_t n_gens)
 {
     if (!s) return fail(EVOX_EINVAL, "state is null");
@@ -782,6 +948,7 @@ int evox_cso_refresh(evox_state *s, int refit)
 int evox_best(evox_state *s, float *best_fit, int64_t *best_idx, float *best_x_host)
 {
     if (!s) return fail(EVOX_EINVAL, "state is null");
+    if (s->P.algo == EVOX_NSGA2) return fail(EVOX_EINVAL, "NSGA-II has no single best (read front and obj)");
     DevBest h{};
     hipError_t e = hipMemcpyAsync(&h, s->best, sizeof h, hipMemcpyDeviceToHost, s->stream);
     if (e == hipSuccess) e = hipStreamSynchronize(s->stream);
@@ -817,7 +984,8 @@ int64_t evox_default_ldx(int32_t algo, int64_t D)
 {
     if (D < 1 || D > EVOX_MAX_D) return 0;
     const int64_t line = (D + 31) / 32 * 32, quad = (D + 3) / 4 * 4;
-    if (algo == EVOX_PSO || algo == EVOX_DE || algo == EVOX_ES || algo == EVOX_PGPE || algo == EVOX_MAES)
+    if (algo == EVOX_PSO || algo == EVOX_DE || algo == EVOX_ES || algo == EVOX_PGPE || algo == EVOX_MAES ||
+        algo == EVOX_NSGA2)
         return D >= 512 ? line : quad;
     if (algo == EVOX_CSO) return D >= 64 ? line : quad;
     return 0;

@@ -24,7 +24,7 @@ enum { FN_SPHERE = 0, FN_ACKLEY, FN_RASTRIGIN, FN_GRIEWANK, FN_ROSENBROCK, FN_SC
 // Random-stream ids (fourth Philox counter word).
 enum { STREAM_INIT_X = 0, STREAM_INIT_V = 1, STREAM_PSO = 2, STREAM_CSO = 3, STREAM_PERM = 4,
        STREAM_INIT_NORMAL = 5, STREAM_DE = 6, STREAM_ES = 7, STREAM_PGPE = 8,
-       STREAM_MAES = 9 };
+       STREAM_MAES = 9, STREAM_NSGA_SEL = 10, STREAM_NSGA_VAR = 11, STREAM_NSGA_MUT = 12 };
 
 constexpr int kBlock = 256;              // threads per block when a row takes <= 256 lanes
 constexpr int kGridCap = 2048;           // blocks of the grid-stride kernels (8 per CU on 256 CUs)

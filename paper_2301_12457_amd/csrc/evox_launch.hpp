@@ -101,6 +101,57 @@ hipError_t launch_mae_rank(const MaeArgs &a, float *M, float beta, hipStream_t s
 hipError_t launch_mae_identity(float *M, int64_t D, int64_t ldx, hipStream_t s);
 int occupancy_gemm_nt_thin();  // resident blocks per CU of the sampling product's tile shape
 
+// NSGA-II on DTLZ1.
+constexpr int kNsgaMaxM = 8;          // objectives
+constexpr int64_t kNsgaMaxN = 32768;  // population (the merged population is 2N)
+struct NsgaVarArgs {
+    const float *X;        // parents [N][ldx]
+    int64_t N, D, ldx;
+    const int32_t *front;  // [N]
+    const double *crowd;   // [N]
+    float *Q;              // offspring [N][ldx]
+    double eta_c, eta_m;
+    uint32_t k0, k1, t;
+};
+struct NsgaSortArgs {
+    const float *F;        // [n][M]
+    int64_t n;
+    int32_t M;
+    int32_t *front;        // [n] out: front index, -1 past the fronts needed
+    double *crowd;         // [n] out: crowding distance within the front
+    uint32_t *cnt;         // [n] dominator counts
+    int32_t *list;         // [n] points front by front
+    int32_t *foff;         // [n + 1] first list position of each front
+    int32_t *pos, *sorted; // [M][cap] order within the front per objective
+    int64_t cap;           // >= n
+    uint32_t *len;         // [1]
+};
+struct NsgaSortResult {
+    int32_t fronts;        // fronts assigned
+    int64_t assigned;      // points in them
+    int64_t last;          // points in the last one
+};
+struct NsgaSelArgs {
+    const float *X, *Q;    // parents, offspring [N][ldx]
+    int64_t N, ldx;
+    int32_t M;
+    const float *FR;       // [2N][M]
+    const int32_t *frontR; // [2N]
+    const double *crowdR;  // [2N]
+    const int32_t *list;   // [2N] from the sort
+    int32_t *keep, *pre;   // [2N]
+    float *X2;             // [N][ldx] survivors' rows
+    float *F;              // [N][M]
+    int32_t *front;        // [N]
+    double *crowd;         // [N]
+};
+hipError_t launch_nsga_var(const NsgaVarArgs &a, hipStream_t s);
+hipError_t launch_nsga_dtlz1(const float *X, int64_t n, int64_t D, int64_t ldx, int32_t M, float *F, hipStream_t s);
+// Fronts until at least `need` points are assigned, and the crowding
+// distances within them; synchronizes the stream once per front.
+hipError_t nsga_sort(const NsgaSortArgs &a, int64_t need, NsgaSortResult *res, hipStream_t s);
+hipError_t launch_nsga_select(const NsgaSelArgs &a, const NsgaSortResult &r, hipStream_t s);
+
 // C = alpha op(A) op(B) + beta C (row-major; op(A) is M x K, op(B) K x N;
 // leading dimensions and pointers 16-byte multiples for the vector loads).
 struct GemmArgs {

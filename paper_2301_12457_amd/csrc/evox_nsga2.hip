@@ -1,0 +1,381 @@
+// NSGA-II on DTLZ1 (Table II; the multi-objective scaling experiment of
+// Sec. V-A, whose speed-up the paper attributes to computing the dominance
+// relations in parallel).  Deb, Pratap, Agarwal, Meyarivan (2002):
+//   variation   crowded binary tournaments, simulated binary crossover and
+//               polynomial mutation (one thread per pair and variable, fp64);
+//   objectives  DTLZ1 (one wave per row, fp64: its g is a difference of
+//               numbers near 100 k that fp32 would not resolve near the front);
+//   sorting     dominator counts over all pairs (tiled through LDS, exact
+//               integer atomics), then fronts peeled one at a time: the
+//               unassigned points with no unassigned dominator form the next
+//               front, whose members are appended to a list (fronts stored
+//               contiguously) and their dominance subtracted from the rest;
+//   crowding    each front member's position in every objective's order of
+//               (value, index) by counting within its front, then the
+//               distance summed objective by objective in that order;
+//   selection   whole fronts, then the last front's members of largest
+//               crowding distance (lower index on ties) by counting, and a
+//               compaction that keeps the merged order.
+#include "evox_launch.hpp"
+
+#include <cmath>
+
+namespace evox {
+
+namespace {
+
+constexpr int kSpan = 512;  // points per LDS tile of the pair kernels
+constexpr double kPi = 3.14159265358979323846;
+
+// a dominates b: no objective worse and at least one better (comparisons
+// as written, so that any value compares as in the definition)
+__device__ __forceinline__ bool dominates(const float *a, const float *b, int M)
+{
+    bool worse = false, better = false;
+    for (int m = 0; m < M; ++m) {
+        worse |= a[m] > b[m];
+        better |= a[m] < b[m];
+    }
+    return !worse && better;
+}
+
+__device__ __forceinline__ int64_t crowded_winner(int64_t a, int64_t b, const int32_t *front, const double *crowd)
+{
+    if (front[a] != front[b]) return front[a] < front[b] ? a : b;
+    if (crowd[a] != crowd[b]) return crowd[a] > crowd[b] ? a : b;
+    return a < b ? a : b;
+}
+
+// Polynomial mutation of x in [0, 1] with draw u and index eta (the bounded
+// form of Deb and Goyal): u < 1/2 lowers x by 1 - (2u + (1 - 2u)(1 - x)^(eta+1))
+// ^(1/(eta+1)), u >= 1/2 raises it by 1 - (2(1 - u) + 2(u - 1/2) x^(eta+1))
+// ^(1/(eta+1)); clipped to [0, 1].
+__device__ double poly_mutate(double x, double u, double eta)
+{
+    const double e1 = eta + 1.0, inv = 1.0 / e1;
+    double y;
+    if (u < 0.5)
+        y = x + (pow(2.0 * u + (1.0 - 2.0 * u) * pow(1.0 - x, e1), inv) - 1.0);
+    else
+        y = x + (1.0 - pow(2.0 * (1.0 - u) + 2.0 * (u - 0.5) * pow(x, e1), inv));
+    return y < 0.0 ? 0.0 : y > 1.0 ? 1.0 : y;
+}
+
+// Offspring rows 2p and 2p + 1, variable j (one thread each): parents from
+// the tournaments (w of Philox(0, p, t, 10): candidates floor(w_q N / 2^32),
+// (w_0, w_1) and (w_2, w_3)); crossover and mutation draws from Philox(j, p,
+// t, 11) and (j, p, t, 12).
+__global__ __launch_bounds__(256) void k_nsga_var(NsgaVarArgs a)
+{
+    const int64_t q = (int64_t)blockIdx.x * 256 + threadIdx.x, H = a.N / 2;
+    if (q >= H * a.D) return;
+    const int64_t p = q / a.D, j = q % a.D;
+    const U4 ws = philox(0u, (uint32_t)p, a.t, STREAM_NSGA_SEL, a.k0, a.k1);
+    const uint64_t n = (uint64_t)a.N;
+    const int64_t c0 = (int64_t)(((uint64_t)ws.x * n) >> 32), c1 = (int64_t)(((uint64_t)ws.y * n) >> 32);
+    const int64_t c2 = (int64_t)(((uint64_t)ws.z * n) >> 32), c3 = (int64_t)(((uint64_t)ws.w * n) >> 32);
+    const int64_t pa = crowded_winner(c0, c1, a.front, a.crowd), pb = crowded_winner(c2, c3, a.front, a.crowd);
+    const U4 w = philox((uint32_t)j, (uint32_t)p, a.t, STREAM_NSGA_VAR, a.k0, a.k1);
+    const U4 v = philox((uint32_t)j, (uint32_t)p, a.t, STREAM_NSGA_MUT, a.k0, a.k1);
+    const double ec = a.eta_c, em = a.eta_m, pm = 1.0 / (double)a.D;
+    const double u = (double)u01(w.x);
+    double beta = u <= 0.5 ? pow(2.0 * u, 1.0 / (ec + 1.0)) : pow(2.0 - 2.0 * u, -1.0 / (ec + 1.0));
+    if (w.y & 1u) beta = -beta;
+    if ((double)u01(w.y) >= 0.5) beta = 1.0;
+    const double xa = (double)a.X[pa * a.ldx + j], xb = (double)a.X[pb * a.ldx + j];
+    const double y[2] = {0.5 * (xa + xb) + 0.5 * beta * (xa - xb), 0.5 * (xa + xb) - 0.5 * beta * (xa - xb)};
+    const uint32_t coin[2] = {w.z, w.w}, mu[2] = {v.x, v.y};
+    for (int c = 0; c < 2; ++c) {
+        const double yc = y[c] < 0.0 ? 0.0 : y[c] > 1.0 ? 1.0 : y[c];
+        float out = (float)yc;
+        if ((double)u01(coin[c]) < pm) out = (float)poly_mutate((double)out, (double)u01(mu[c]), em);
+        a.Q[(2 * p + c) * a.ldx + j] = out;
+    }
+}
+
+// DTLZ1 of row r (one wave): g = 100 (k + sum_{i >= M-1} ((x_i - 1/2)^2 -
+// cos(20 pi (x_i - 1/2)))), f_0 = (1 + g)/2 x_0 ... x_{M-2}, f_m = (1 + g)/2
+// x_0 ... x_{M-2-m} (1 - x_{M-1-m}); fp64, each objective rounded once.
+__global__ __launch_bounds__(256) void k_nsga_dtlz1(const float *X, int64_t n, int64_t D, int64_t ldx, int32_t M,
+                                                    float *F)
+{
+    const int64_t r = (int64_t)blockIdx.x * 4 + threadIdx.x / 64;
+    const int lane = threadIdx.x % 64;
+    if (r >= n) return;
+    const float *x = X + r * ldx;
+    double acc = 0.0;
+    for (int64_t i = M - 1 + lane; i < D; i += 64) {
+        const double d = (double)x[i] - 0.5;
+        acc += d * d - cos(20.0 * kPi * d);
+    }
+    for (int o = 32; o > 0; o /= 2) acc += __shfl_xor(acc, o);
+    if (lane < M) {
+        const int m = lane;
+        const double g = 100.0 * ((double)(D - M + 1) + acc);
+        double f = 0.5 * (1.0 + g);
+        for (int i = 0; i < M - 1 - m; ++i) f *= (double)x[i];
+        if (m > 0) f *= 1.0 - (double)x[M - 1 - m];
+        F[r * M + m] = (float)f;
+    }
+}
+
+// cnt[i] += #{j in this block's span : F_j dominates F_i}.
+__global__ __launch_bounds__(256) void k_nsga_count(const float *F, int64_t n, int32_t M, uint32_t *cnt)
+{
+    __shared__ float fj[kSpan * kNsgaMaxM];
+    const int64_t j0 = (int64_t)blockIdx.y * kSpan, nj = n - j0 < kSpan ? n - j0 : kSpan;
+    for (int64_t q = threadIdx.x; q < nj * M; q += 256) fj[q] = F[j0 * M + q];
+    __syncthreads();
+    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (i >= n) return;
+    float fi[kNsgaMaxM];
+    for (int m = 0; m < M; ++m) fi[m] = F[i * M + m];
+    uint32_t c = 0;
+    for (int64_t q = 0; q < nj; ++q) c += dominates(fj + q * M, fi, M);
+    if (c) atomicAdd(cnt + i, c);
+}
+
+// Front k: unassigned points with no unassigned dominator, appended to list.
+__global__ __launch_bounds__(256) void k_nsga_mark(int32_t *front, const uint32_t *cnt, int64_t n, int32_t k,
+                                                   int32_t *list, uint32_t *len)
+{
+    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (i >= n || front[i] != -1 || cnt[i] != 0) return;
+    front[i] = k;
+    list[atomicAdd(len, 1u)] = (int32_t)i;
+}
+
+// cnt[i] -= #{j in this block's span of the new front : F_j dominates F_i}
+// for the points still unassigned.
+__global__ __launch_bounds__(256) void k_nsga_peel(const float *F, int64_t n, int32_t M, const int32_t *list,
+                                                   int64_t size, const int32_t *front, uint32_t *cnt)
+{
+    __shared__ float fj[kSpan * kNsgaMaxM];
+    const int64_t q0 = (int64_t)blockIdx.y * kSpan, nq = size - q0 < kSpan ? size - q0 : kSpan;
+    for (int64_t q = threadIdx.x; q < nq * M; q += 256) fj[q] = F[(int64_t)list[q0 + q / M] * M + q % M];
+    __syncthreads();
+    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (i >= n || front[i] != -1) return;
+    float fi[kNsgaMaxM];
+    for (int m = 0; m < M; ++m) fi[m] = F[i * M + m];
+    uint32_t c = 0;
+    for (int64_t q = 0; q < nq; ++q) c += dominates(fj + q * M, fi, M);
+    if (c) atomicSub(cnt + i, c);
+}
+
+// foff[k] = first list position of front k; foff[K] = total.
+__global__ __launch_bounds__(256) void k_nsga_foff(const int32_t *list, int64_t total, const int32_t *front,
+                                                   int32_t *foff)
+{
+    const int64_t q = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (q >= total) return;
+    const int32_t k = front[list[q]];
+    if (q == 0 || front[list[q - 1]] != k) foff[k] = (int32_t)q;
+    if (q == total - 1) foff[k + 1] = (int32_t)total;
+}
+
+// Position of list entry q in each objective's order of (value, index)
+// within its front, and the inverse: sorted[m][foff[k] + pos] = the point.
+__global__ __launch_bounds__(256) void k_nsga_order(NsgaSortArgs a, int64_t total)
+{
+    const int64_t q = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (q >= total) return;
+    const int32_t i = a.list[q], k = a.front[i];
+    const int32_t b = a.foff[k], e = a.foff[k + 1];
+    float fi[kNsgaMaxM];
+    int32_t c[kNsgaMaxM];
+    for (int m = 0; m < a.M; ++m) {
+        fi[m] = a.F[(int64_t)i * a.M + m];
+        c[m] = 0;
+    }
+    for (int32_t r = b; r < e; ++r) {
+        const int32_t j = a.list[r];
+        for (int m = 0; m < a.M; ++m) {
+            const float fj = a.F[(int64_t)j * a.M + m];
+            c[m] += (fj < fi[m]) || (fj == fi[m] && j < i);
+        }
+    }
+    for (int m = 0; m < a.M; ++m) {
+        a.pos[m * a.cap + q] = c[m];
+        a.sorted[m * a.cap + b + c[m]] = i;
+    }
+}
+
+// Crowding distance of list entry q: per objective in order, +inf at either
+// end of the front's order, else + (next - previous) / (last - first) when
+// the range is not zero (fp64).
+__global__ __launch_bounds__(256) void k_nsga_crowd(NsgaSortArgs a, int64_t total)
+{
+    const int64_t q = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (q >= total) return;
+    const int32_t i = a.list[q], k = a.front[i];
+    const int32_t b = a.foff[k], e = a.foff[k + 1], size = e - b;
+    double d = 0.0;
+    for (int m = 0; m < a.M; ++m) {
+        const int32_t p = a.pos[m * a.cap + q];
+        const int32_t *srt = a.sorted + m * a.cap + b;
+        if (p == 0 || p == size - 1) {
+            d = INFINITY;
+        } else {
+            const double lo = (double)a.F[(int64_t)srt[0] * a.M + m];
+            const double hi = (double)a.F[(int64_t)srt[size - 1] * a.M + m];
+            if (hi > lo)
+                d += ((double)a.F[(int64_t)srt[p + 1] * a.M + m] - (double)a.F[(int64_t)srt[p - 1] * a.M + m]) /
+                     (hi - lo);
+        }
+    }
+    a.crowd[i] = d;
+}
+
+// keep[i] for the survivors: members of the fronts before the last, and the
+// last front's members ranked below `need` by (crowding descending, index).
+__global__ __launch_bounds__(256) void k_nsga_trunc(const int32_t *list, int64_t full, int64_t total, int64_t need,
+                                                    const double *crowd, int32_t *keep)
+{
+    const int64_t q = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (q >= total) return;
+    const int32_t i = list[q];
+    if (q < full) {
+        keep[i] = 1;
+        return;
+    }
+    const double ci = crowd[i];
+    int64_t r = 0;
+    for (int64_t s = full; s < total; ++s) {
+        const int32_t j = list[s];
+        r += crowd[j] > ci || (crowd[j] == ci && j < i);
+    }
+    if (r < need) keep[i] = 1;
+}
+
+// Exclusive prefix sums of keep[0 .. n) (one block; n <= 1024 * per-thread).
+__global__ __launch_bounds__(1024) void k_nsga_scan(const int32_t *keep, int64_t n, int32_t *pre)
+{
+    __shared__ int32_t part[1024];
+    const int64_t per = (n + 1023) / 1024, b = threadIdx.x * per, e = b + per < n ? b + per : n;
+    int32_t s = 0;
+    for (int64_t i = b; i < e; ++i) s += keep[i];
+    part[threadIdx.x] = s;
+    __syncthreads();
+    for (int o = 1; o < 1024; o *= 2) {
+        const int32_t v = threadIdx.x >= (unsigned)o ? part[threadIdx.x - o] : 0;
+        __syncthreads();
+        part[threadIdx.x] += v;
+        __syncthreads();
+    }
+    int32_t run = threadIdx.x ? part[threadIdx.x - 1] : 0;
+    for (int64_t i = b; i < e; ++i) {
+        pre[i] = run;
+        run += keep[i];
+    }
+}
+
+// Survivor i of the merged population (parents 0..N-1, offspring N..2N-1)
+// to row pre[i]: its row (float4 chunk c per thread), objectives, front and
+// crowding distance.
+__global__ __launch_bounds__(256) void k_nsga_compact(NsgaSelArgs a)
+{
+    const int64_t c4 = a.ldx / 4, q = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (q >= 2 * a.N * c4) return;
+    const int64_t i = q / c4, c = q % c4;
+    if (!a.keep[i]) return;
+    const int64_t r = a.pre[i];
+    const float *src = i < a.N ? a.X + i * a.ldx : a.Q + (i - a.N) * a.ldx;
+    *reinterpret_cast<float4 *>(a.X2 + r * a.ldx + 4 * c) = *reinterpret_cast<const float4 *>(src + 4 * c);
+    if (c == 0) {
+        for (int m = 0; m < a.M; ++m) a.F[r * a.M + m] = a.FR[i * a.M + m];
+        a.front[r] = a.frontR[i];
+        a.crowd[r] = a.crowdR[i];
+    }
+}
+
+__global__ __launch_bounds__(256) void k_fill_i32(int32_t *p, int64_t n, int32_t v)
+{
+    for (int64_t q = (int64_t)blockIdx.x * 256 + threadIdx.x; q < n; q += (int64_t)gridDim.x * 256) p[q] = v;
+}
+
+unsigned blocks(int64_t n, int64_t per) { return (unsigned)((n + per - 1) / per); }
+
+}  // namespace
+
+hipError_t launch_nsga_var(const NsgaVarArgs &a, hipStream_t s)
+{
+    const int64_t n = a.N / 2 * a.D;
+    if (n == 0) return hipSuccess;
+    hipLaunchKernelGGL(k_nsga_var, dim3(blocks(n, 256)), dim3(256), 0, s, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_nsga_dtlz1(const float *X, int64_t n, int64_t D, int64_t ldx, int32_t M, float *F, hipStream_t s)
+{
+    if (n == 0) return hipSuccess;
+    hipLaunchKernelGGL(k_nsga_dtlz1, dim3(blocks(n, 4)), dim3(256), 0, s, X, n, D, ldx, M, F);
+    return hipGetLastError();
+}
+
+hipError_t nsga_sort(const NsgaSortArgs &a, int64_t need, NsgaSortResult *res, hipStream_t s)
+{
+    const int64_t n = a.n;
+    *res = NsgaSortResult{0, 0, 0};
+    if (n == 0) return hipSuccess;
+    hipError_t e;
+    hipLaunchKernelGGL(k_fill_i32, dim3(blocks(n, 256) < 4096 ? blocks(n, 256) : 4096), dim3(256), 0, s, a.front,
+                       n, -1);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    if ((e = launch_zero_u32(a.cnt, n, s)) != hipSuccess) return e;
+    hipLaunchKernelGGL(k_nsga_count, dim3(blocks(n, 256), blocks(n, kSpan)), dim3(256), 0, s, a.F, n, a.M, a.cnt);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    // every slot of the per-objective orders holds a valid index even if the
+    // order kernel were handed values without a total order
+    hipLaunchKernelGGL(k_fill_i32, dim3(4096), dim3(256), 0, s, a.sorted, (int64_t)a.M * a.cap, 0);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    int64_t assigned = 0, last = 0;
+    int32_t k = 0;
+    while (assigned < need) {
+        if ((e = launch_zero_u32(a.len, 1, s)) != hipSuccess) return e;
+        hipLaunchKernelGGL(k_nsga_mark, dim3(blocks(n, 256)), dim3(256), 0, s, a.front, (const uint32_t *)a.cnt, n,
+                           k, a.list + assigned, a.len);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+        uint32_t size = 0;
+        if ((e = hipMemcpyAsync(&size, a.len, sizeof size, hipMemcpyDeviceToHost, s)) != hipSuccess ||
+            (e = hipStreamSynchronize(s)) != hipSuccess)
+            return e;
+        if (size == 0) return hipErrorUnknown;  // cannot happen: a finite set has a non-dominated point
+        last = size;
+        assigned += size;
+        ++k;
+        if (assigned < need) {
+            hipLaunchKernelGGL(k_nsga_peel, dim3(blocks(n, 256), blocks(size, kSpan)), dim3(256), 0, s, a.F, n, a.M,
+                               (const int32_t *)(a.list + assigned - size), (int64_t)size, (const int32_t *)a.front,
+                               a.cnt);
+            if ((e = hipGetLastError()) != hipSuccess) return e;
+        }
+    }
+    hipLaunchKernelGGL(k_nsga_foff, dim3(blocks(assigned, 256)), dim3(256), 0, s, (const int32_t *)a.list, assigned,
+                       (const int32_t *)a.front, a.foff);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL(k_nsga_order, dim3(blocks(assigned, 256)), dim3(256), 0, s, a, assigned);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL(k_nsga_crowd, dim3(blocks(assigned, 256)), dim3(256), 0, s, a, assigned);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    *res = NsgaSortResult{k, assigned, last};
+    return hipSuccess;
+}
+
+hipError_t launch_nsga_select(const NsgaSelArgs &a, const NsgaSortResult &r, hipStream_t s)
+{
+    const int64_t full = r.assigned - r.last, need = a.N - full;
+    hipError_t e;
+    hipLaunchKernelGGL(k_fill_i32, dim3(blocks(2 * a.N, 256) < 4096 ? blocks(2 * a.N, 256) : 4096), dim3(256), 0, s,
+                       a.keep, 2 * a.N, 0);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL(k_nsga_trunc, dim3(blocks(r.assigned, 256)), dim3(256), 0, s, a.list, full, r.assigned, need,
+                       a.crowdR, a.keep);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL(k_nsga_scan, dim3(1), dim3(1024), 0, s, (const int32_t *)a.keep, 2 * a.N, a.pre);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL(k_nsga_compact, dim3(blocks(2 * a.N * (a.ldx / 4), 256)), dim3(256), 0, s, a);
+    return hipGetLastError();
+}
+
+}  // namespace evox

@@ -38,13 +38,13 @@ def test_exports_every_declared_symbol(evox):
 
 def test_struct_layouts_match_header(evox):
     # evox_params: 2 x int32, 3 x int64, 9 floats, 2 x int32, 8 floats, (pad), uint64
-    assert ctypes.sizeof(evox.Params) == 120
+    assert ctypes.sizeof(evox.Params) == 136
     assert evox.Params.x_init.offset == 72
     assert evox.Params.de_f.offset == 84
     assert evox.Params.es_lr.offset == 96
     assert evox.Params.pgpe_max_change.offset == 104
     assert evox.Params.seed.offset == 112
-    assert ctypes.sizeof(evox.Buffers) == 11 * 8
+    assert ctypes.sizeof(evox.Buffers) == 14 * 8
 
 
 def test_row_layout_policy(evox):
@@ -88,9 +88,9 @@ def test_default_pitch_policy(evox):
     for D, want in [(1, 4), (10, 12), (63, 64), (64, 64), (65, 96), (100, 128), (1000, 1024)]:
         assert L.evox_default_ldx(C, D) == want, (D, want)
     for D in (10, 100, 1000):
-        for algo in (evox.DE, evox.ES, evox.PGPE, evox.MAES):
+        for algo in (evox.DE, evox.ES, evox.PGPE, evox.MAES, evox.NSGA2):
             assert L.evox_default_ldx(algo, D) == L.evox_default_ldx(P, D)
-    for algo, D in [(P, 0), (C, 32769), (6, 10)]:
+    for algo, D in [(P, 0), (C, 32769), (7, 10)]:
         assert L.evox_default_ldx(algo, D) == 0
     assert evox.make_params(C, evox.GRIEWANK, 10, 100, -1, 1).ldx == 128
     assert evox.make_params(P, evox.GRIEWANK, 10, 100, -1, 1).ldx == 100
