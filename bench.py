@@ -74,6 +74,10 @@ ES_OPS_PER_ELEMENT = 20 + 8 + 4 + 28 + 1
 PGPE_OPS_PER_ELEMENT = 20 + 8 + 4 + 28 + 3
 ALU_PEAK_TOPS = 256 * 64 * 2.4e9 / 1e12   # 256 CUs x 64 lanes x 2.4 GHz, 32-bit lane-ops
 MFMA_F32_PEAK_TFLOPS = 157.3              # dense fp32 matrix-core peak
+# NSGA-II's dominance pass: per ordered pair of the merged population, two
+# comparisons per objective, one combination of the two outcomes and one add
+def nsga2_count_ops(w):
+    return (2.0 * w.N) ** 2 * (2 * w.n_obj + 2)
 
 
 def maes_flops(w):
@@ -120,6 +124,18 @@ def cpu_baseline(w, budget_s=12.0):
 
 def _cpu_baseline(w, budget_s):
     import oracle
+    if w.algo == "nsga2":
+        # the oracle's sorting is quadratic per front: a population of 1000
+        rows = min(w.N, 1000)
+        s = oracle.NSGA2(oracle.nsga2_params(rows, w.D, w.n_obj, seed=w.seed))
+        t0 = time.perf_counter()
+        gens = 0
+        while time.perf_counter() - t0 < budget_s and gens < w.gens:
+            s.step(1)
+            gens += 1
+        dt = time.perf_counter() - t0
+        return {"value": rows * w.D * gens / dt, "unit": UNIT, "cores": 1, "kind": "oracle",
+                "sample": f"{rows} of {w.N} individuals x D={w.D}, {gens} generations, {dt:.1f} s"}
     fn = {"sphere": 0, "ackley": 1, "rastrigin": 2, "griewank": 3, "rosenbrock": 4,
           "schwefel": 5}[w.fn]
     if w.algo == "eval":
@@ -196,7 +212,7 @@ def main():
     w = WORKLOADS[args.workload]
     torch.cuda.set_device(0)
     stream = torch.cuda.current_stream()
-    fn = evox.FN_IDS[w.fn]
+    fn = evox.FN_IDS[w.fn] if w.algo != "nsga2" else 0   # NSGA-II: DTLZ1
 
     if w.algo == "eval":
         X = torch.empty((w.N, w.D), dtype=torch.float32, device="cuda")
@@ -212,12 +228,12 @@ def main():
         swarm = None
     else:
         algo = {"pso": evox.PSO, "cso": evox.CSO, "de": evox.DE, "es": evox.ES,
-                "pgpe": evox.PGPE, "maes": evox.MAES}[w.algo]
+                "pgpe": evox.PGPE, "maes": evox.MAES, "nsga2": evox.NSGA2}[w.algo]
         P = evox.make_params(algo, fn, w.N, w.D, w.lb, w.ub, v_lo=w.v_lo, v_hi=w.v_hi, w=w.w,
                              c1=w.c1, c2=w.c2, phi=w.phi, vmax=w.vmax, seed=w.seed,
                              ldx=args.ldx or None, de_f=w.de_f, de_cr=w.de_cr,
                              es_sigma=w.es_sigma, es_lr=w.es_lr, pgpe_sigma_lr=w.pgpe_sigma_lr,
-                             pgpe_max_change=w.pgpe_max_change)
+                             pgpe_max_change=w.pgpe_max_change, n_obj=w.n_obj)
         swarm = evox.Swarm(P)
 
         def step():
@@ -249,7 +265,18 @@ def main():
     if swarm is not None:
         fused_ms, launches, improved = swarm.profile_read()
         swarm.profile(False)
-        if launches > 0 and w.algo == "maes":
+        if launches > 0 and w.algo == "nsga2":
+            # the vector-ALU roofline of the all-pairs dominance count
+            avg_ms = fused_ms / launches
+            ops = nsga2_count_ops(w)
+            achieved = ops / (avg_ms / 1e3) / 1e12
+            roofline = {"bound": "alu", "achieved": round(achieved, 2), "peak": ALU_PEAK_TOPS,
+                        "unit": "Tops/s", "frac": round(achieved / ALU_PEAK_TOPS, 4), "traffic": None,
+                        "kernel": "k_nsga_count (dominators of 2N points)",
+                        "avg_launch_us": round(avg_ms * 1e3, 2), "launches": launches,
+                        "algorithmic_ops_per_launch": ops,
+                        "generation_us": round(ms / 1e3 / w.gens * 1e6, 2)}
+        elif launches > 0 and w.algo == "maes":
             # the matrix-core roofline of the sampling product (the timed
             # launch: k_gemm_nt and its split-K reduction)
             avg_ms = fused_ms / launches

@@ -838,7 +838,8 @@ int nsga_generations(evox_state *s, int64_t n_gens)
         if ((e = launch_nsga_dtlz1(s->ns_sel.Q, P.N, P.D, P.ldx, M, (float *)s->ns_sort.F + P.N * M, s->stream)) !=
             hipSuccess)
             return hip_fail(e, "objectives");
-        if ((e = timed(s, [&] { return nsga_sort(s->ns_sort, P.N, &r, s->stream); })) != hipSuccess)
+        if ((e = timed(s, [&] { return nsga_count(s->ns_sort, s->stream); })) != hipSuccess ||
+            (e = nsga_fronts(s->ns_sort, P.N, &r, s->stream)) != hipSuccess)
             return hip_fail(e, "non-dominated sorting");
         if ((e = launch_nsga_select(s->ns_sel, r, s->stream)) != hipSuccess) return hip_fail(e, "selection");
         if ((e = launch_stream_copy(s->ns_sel.X2, s->B.x, P.N * P.ldx, s->stream)) != hipSuccess)

@@ -148,8 +148,12 @@ struct NsgaSelArgs {
 hipError_t launch_nsga_var(const NsgaVarArgs &a, hipStream_t s);
 hipError_t launch_nsga_dtlz1(const float *X, int64_t n, int64_t D, int64_t ldx, int32_t M, float *F, hipStream_t s);
 // Fronts until at least `need` points are assigned, and the crowding
-// distances within them; synchronizes the stream once per front.
+// distances within them; synchronizes the stream once per front.  The same
+// in two parts: the dominator counts over all pairs, then the peeling and
+// the crowding distances.
 hipError_t nsga_sort(const NsgaSortArgs &a, int64_t need, NsgaSortResult *res, hipStream_t s);
+hipError_t nsga_count(const NsgaSortArgs &a, hipStream_t s);
+hipError_t nsga_fronts(const NsgaSortArgs &a, int64_t need, NsgaSortResult *res, hipStream_t s);
 hipError_t launch_nsga_select(const NsgaSelArgs &a, const NsgaSortResult &r, hipStream_t s);
 
 // C = alpha op(A) op(B) + beta C (row-major; op(A) is M x K, op(B) K x N;

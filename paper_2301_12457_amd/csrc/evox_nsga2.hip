@@ -313,10 +313,9 @@ hipError_t launch_nsga_dtlz1(const float *X, int64_t n, int64_t D, int64_t ldx, 
     return hipGetLastError();
 }
 
-hipError_t nsga_sort(const NsgaSortArgs &a, int64_t need, NsgaSortResult *res, hipStream_t s)
+hipError_t nsga_count(const NsgaSortArgs &a, hipStream_t s)
 {
     const int64_t n = a.n;
-    *res = NsgaSortResult{0, 0, 0};
     if (n == 0) return hipSuccess;
     hipError_t e;
     hipLaunchKernelGGL(k_fill_i32, dim3(blocks(n, 256) < 4096 ? blocks(n, 256) : 4096), dim3(256), 0, s, a.front,
@@ -324,7 +323,15 @@ hipError_t nsga_sort(const NsgaSortArgs &a, int64_t need, NsgaSortResult *res, h
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if ((e = launch_zero_u32(a.cnt, n, s)) != hipSuccess) return e;
     hipLaunchKernelGGL(k_nsga_count, dim3(blocks(n, 256), blocks(n, kSpan)), dim3(256), 0, s, a.F, n, a.M, a.cnt);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
+    return hipGetLastError();
+}
+
+hipError_t nsga_fronts(const NsgaSortArgs &a, int64_t need, NsgaSortResult *res, hipStream_t s)
+{
+    const int64_t n = a.n;
+    *res = NsgaSortResult{0, 0, 0};
+    if (n == 0) return hipSuccess;
+    hipError_t e;
     // every slot of the per-objective orders holds a valid index even if the
     // order kernel were handed values without a total order
     hipLaunchKernelGGL(k_fill_i32, dim3(4096), dim3(256), 0, s, a.sorted, (int64_t)a.M * a.cap, 0);
@@ -360,6 +367,12 @@ hipError_t nsga_sort(const NsgaSortArgs &a, int64_t need, NsgaSortResult *res, h
     if ((e = hipGetLastError()) != hipSuccess) return e;
     *res = NsgaSortResult{k, assigned, last};
     return hipSuccess;
+}
+
+hipError_t nsga_sort(const NsgaSortArgs &a, int64_t need, NsgaSortResult *res, hipStream_t s)
+{
+    hipError_t e = nsga_count(a, s);
+    return e != hipSuccess ? e : nsga_fronts(a, need, res, s);
 }
 
 hipError_t launch_nsga_select(const NsgaSelArgs &a, const NsgaSortResult &r, hipStream_t s)

@@ -16,7 +16,7 @@ about a million): synthetic, seeded, no dataset.
 import math
 from dataclasses import dataclass, field
 
-PSO, CSO, DE, ES, PGPE, MAES, EVAL = "pso", "cso", "de", "es", "pgpe", "maes", "eval"
+PSO, CSO, DE, ES, PGPE, MAES, NSGA2, EVAL = "pso", "cso", "de", "es", "pgpe", "maes", "nsga2", "eval"
 
 
 @dataclass(frozen=True)
@@ -45,6 +45,7 @@ class Workload:
     es_lr: float = 0.01
     pgpe_sigma_lr: float = 0.01
     pgpe_max_change: float = 0.2
+    n_obj: int = 3
 
 
 WORKLOADS = {
@@ -64,6 +65,8 @@ WORKLOADS = {
                                     lb=-5.0, ub=5.0, es_sigma=1.0, es_lr=0.5, pgpe_sigma_lr=0.1),
     "maes_sphere_100x16384": Workload("maes_sphere_100x16384", MAES, "sphere", 100, 16_384, 20, 10,
                                       lb=-5.0, ub=5.0, es_sigma=1.0),
+    "nsga2_dtlz1_16384x100": Workload("nsga2_dtlz1_16384x100", NSGA2, "dtlz1", 16_384, 100, 10, 11,
+                                      lb=0.0, ub=1.0, n_obj=3),
     "eval_rosenbrock_1m_x1e3": Workload("eval_rosenbrock_1m_x1e3", EVAL, "rosenbrock", 1_048_576,
                                         1_000, 1, 4, x_mu=1.0, x_sigma=0.5),
 }
