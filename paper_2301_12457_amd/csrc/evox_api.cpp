@@ -508,8 +508,8 @@ int evox_state_create(const evox_params *params, const evox_buffers *b, void *hi
                                   at<uint32_t>(b->scratch, pl.ns_len)};
         s->ns_sel = NsgaSelArgs{b->x, at<float>(b->scratch, pl.ns_q), P.N, P.ldx, P.n_obj, FR, frontR, crowdR,
                                 s->ns_sort.list, at<int32_t>(b->scratch, pl.ns_keep),
-                                at<int32_t>(b->scratch, pl.ns_pre), at<float>(b->scratch, pl.ns_x2), b->obj,
-                                b->front, b->crowd};
+                                at<int32_t>(b->scratch, pl.ns_pre), s->ns_sort.pos, at<float>(b->scratch, pl.ns_x2),
+                                b->obj, b->front, b->crowd};
     }
     if (P.algo == EVOX_CSO) {
         s->hist = at<uint32_t>(b->scratch, pl.hist);

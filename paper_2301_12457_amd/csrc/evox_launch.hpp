@@ -140,6 +140,7 @@ struct NsgaSelArgs {
     const double *crowdR;  // [2N]
     const int32_t *list;   // [2N] from the sort
     int32_t *keep, *pre;   // [2N]
+    int32_t *rank;         // [2N] last-front ranks (the sort's free per-objective positions)
     float *X2;             // [N][ldx] survivors' rows
     float *F;              // [N][M]
     int32_t *front;        // [N]

@@ -11,8 +11,9 @@
 //               front, whose members are appended to a list (fronts stored
 //               contiguously) and their dominance subtracted from the rest;
 //   crowding    each front member's position in every objective's order of
-//               (value, index) by counting within its front, then the
-//               distance summed objective by objective in that order;
+//               (value, index) by counting within its front (tiles of the
+//               front through LDS), then the distance summed objective by
+//               objective in that order;
 //   selection   whole fronts, then the last front's members of largest
 //               crowding distance (lower index on ties) by counting, and a
 //               compaction that keeps the merged order.
@@ -26,18 +27,6 @@ namespace {
 
 constexpr int kSpan = 512;  // points per LDS tile of the pair kernels
 constexpr double kPi = 3.14159265358979323846;
-
-// a dominates b: no objective worse and at least one better (comparisons
-// as written, so that any value compares as in the definition)
-__device__ __forceinline__ bool dominates(const float *a, const float *b, int M)
-{
-    bool worse = false, better = false;
-    for (int m = 0; m < M; ++m) {
-        worse |= a[m] > b[m];
-        better |= a[m] < b[m];
-    }
-    return !worse && better;
-}
 
 __device__ __forceinline__ int64_t crowded_winner(int64_t a, int64_t b, const int32_t *front, const double *crowd)
 {
@@ -119,19 +108,55 @@ __global__ __launch_bounds__(256) void k_nsga_dtlz1(const float *X, int64_t n, i
     }
 }
 
-// cnt[i] += #{j in this block's span : F_j dominates F_i}.
-__global__ __launch_bounds__(256) void k_nsga_count(const float *F, int64_t n, int32_t M, uint32_t *cnt)
+// Objectives of a point padded to P = 4 or 8 floats in LDS (read back as
+// float4 broadcasts: every lane of a wave reads the same point).
+template <int P>
+__device__ __forceinline__ void load_pad(float *dst, const float *F, int64_t row, int32_t M)
 {
-    __shared__ float fj[kSpan * kNsgaMaxM];
+#pragma unroll
+    for (int m = 0; m < P; ++m) dst[m] = m < M ? F[row * M + m] : 0.0f;
+}
+
+// Dominance of b by a for M objectives known at compile time (comparisons as
+// written: NaN neither dominates nor is dominated differently than in the
+// definition).
+template <int M>
+__device__ __forceinline__ bool dominates_t(const float *a, const float *b)
+{
+    bool worse = false, better = false;
+#pragma unroll
+    for (int m = 0; m < M; ++m) {
+        worse |= a[m] > b[m];
+        better |= a[m] < b[m];
+    }
+    return !worse && better;
+}
+
+// cnt[i] += #{j in this block's span : F_j dominates F_i}.
+template <int M>
+__global__ __launch_bounds__(256) void k_nsga_count(const float *F, int64_t n, uint32_t *cnt)
+{
+    constexpr int P = M <= 4 ? 4 : 8;
+    __shared__ __align__(16) float fj[kSpan * P];
     const int64_t j0 = (int64_t)blockIdx.y * kSpan, nj = n - j0 < kSpan ? n - j0 : kSpan;
-    for (int64_t q = threadIdx.x; q < nj * M; q += 256) fj[q] = F[j0 * M + q];
+    for (int64_t q = threadIdx.x; q < nj; q += 256) load_pad<P>(fj + q * P, F, j0 + q, M);
     __syncthreads();
     const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
     if (i >= n) return;
-    float fi[kNsgaMaxM];
+    float fi[M];
+#pragma unroll
     for (int m = 0; m < M; ++m) fi[m] = F[i * M + m];
     uint32_t c = 0;
-    for (int64_t q = 0; q < nj; ++q) c += dominates(fj + q * M, fi, M);
+#pragma unroll 4
+    for (int64_t q = 0; q < nj; ++q) {
+        float v[P];
+#pragma unroll
+        for (int h = 0; h < P / 4; ++h) {
+            const float4 t = *reinterpret_cast<const float4 *>(fj + q * P + 4 * h);
+            v[4 * h] = t.x, v[4 * h + 1] = t.y, v[4 * h + 2] = t.z, v[4 * h + 3] = t.w;
+        }
+        c += dominates_t<M>(v, fi);
+    }
     if (c) atomicAdd(cnt + i, c);
 }
 
@@ -147,19 +172,31 @@ __global__ __launch_bounds__(256) void k_nsga_mark(int32_t *front, const uint32_
 
 // cnt[i] -= #{j in this block's span of the new front : F_j dominates F_i}
 // for the points still unassigned.
-__global__ __launch_bounds__(256) void k_nsga_peel(const float *F, int64_t n, int32_t M, const int32_t *list,
-                                                   int64_t size, const int32_t *front, uint32_t *cnt)
+template <int M>
+__global__ __launch_bounds__(256) void k_nsga_peel(const float *F, int64_t n, const int32_t *list, int64_t size,
+                                                   const int32_t *front, uint32_t *cnt)
 {
-    __shared__ float fj[kSpan * kNsgaMaxM];
+    constexpr int P = M <= 4 ? 4 : 8;
+    __shared__ __align__(16) float fj[kSpan * P];
     const int64_t q0 = (int64_t)blockIdx.y * kSpan, nq = size - q0 < kSpan ? size - q0 : kSpan;
-    for (int64_t q = threadIdx.x; q < nq * M; q += 256) fj[q] = F[(int64_t)list[q0 + q / M] * M + q % M];
+    for (int64_t q = threadIdx.x; q < nq; q += 256) load_pad<P>(fj + q * P, F, list[q0 + q], M);
     __syncthreads();
     const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
     if (i >= n || front[i] != -1) return;
-    float fi[kNsgaMaxM];
+    float fi[M];
+#pragma unroll
     for (int m = 0; m < M; ++m) fi[m] = F[i * M + m];
     uint32_t c = 0;
-    for (int64_t q = 0; q < nq; ++q) c += dominates(fj + q * M, fi, M);
+#pragma unroll 4
+    for (int64_t q = 0; q < nq; ++q) {
+        float v[P];
+#pragma unroll
+        for (int h = 0; h < P / 4; ++h) {
+            const float4 t = *reinterpret_cast<const float4 *>(fj + q * P + 4 * h);
+            v[4 * h] = t.x, v[4 * h + 1] = t.y, v[4 * h + 2] = t.z, v[4 * h + 3] = t.w;
+        }
+        c += dominates_t<M>(v, fi);
+    }
     if (c) atomicSub(cnt + i, c);
 }
 
@@ -175,30 +212,62 @@ __global__ __launch_bounds__(256) void k_nsga_foff(const int32_t *list, int64_t 
 }
 
 // Position of list entry q in each objective's order of (value, index)
-// within its front, and the inverse: sorted[m][foff[k] + pos] = the point.
+// within its front: pos[m][q] += #{list entries r of the same front in this
+// block's span : (F_r,m, r's point) < (F_q,m, q's point)}.  Fronts are
+// contiguous in the list, so a block whose span lies outside its entries'
+// fronts exits at once; the work is the sum of the squared front sizes.
+template <int M>
 __global__ __launch_bounds__(256) void k_nsga_order(NsgaSortArgs a, int64_t total)
+{
+    constexpr int P = M <= 4 ? 4 : 8;
+    __shared__ __align__(16) float fj[kSpan * P];
+    __shared__ int32_t ij[kSpan], kj[kSpan];
+    const int64_t q0 = (int64_t)blockIdx.x * 256, r0 = (int64_t)blockIdx.y * kSpan;
+    const int64_t qlast = q0 + 255 < total ? q0 + 255 : total - 1;
+    const int32_t lo = a.foff[a.front[a.list[q0]]], hi = a.foff[a.front[a.list[qlast]] + 1];
+    const int64_t nr = total - r0 < kSpan ? total - r0 : kSpan;
+    if (r0 >= hi || r0 + nr <= lo) return;
+    for (int64_t r = threadIdx.x; r < nr; r += 256) {
+        const int32_t j = a.list[r0 + r];
+        ij[r] = j;
+        kj[r] = a.front[j];
+        load_pad<P>(fj + r * P, a.F, j, M);
+    }
+    __syncthreads();
+    const int64_t q = q0 + threadIdx.x;
+    if (q >= total) return;
+    const int32_t i = a.list[q], k = a.front[i];
+    float fi[M];
+    int32_t c[M];
+#pragma unroll
+    for (int m = 0; m < M; ++m) {
+        fi[m] = a.F[(int64_t)i * M + m];
+        c[m] = 0;
+    }
+    for (int64_t r = 0; r < nr; ++r) {
+        if (kj[r] != k) continue;
+        const int32_t j = ij[r];
+        float v[P];
+#pragma unroll
+        for (int h = 0; h < P / 4; ++h) {
+            const float4 t = *reinterpret_cast<const float4 *>(fj + r * P + 4 * h);
+            v[4 * h] = t.x, v[4 * h + 1] = t.y, v[4 * h + 2] = t.z, v[4 * h + 3] = t.w;
+        }
+#pragma unroll
+        for (int m = 0; m < M; ++m) c[m] += (v[m] < fi[m]) || (v[m] == fi[m] && j < i);
+    }
+#pragma unroll
+    for (int m = 0; m < M; ++m)
+        if (c[m]) atomicAdd(a.pos + m * a.cap + q, c[m]);
+}
+
+// sorted[m][foff[k] + pos[m][q]] = the point of list entry q.
+__global__ __launch_bounds__(256) void k_nsga_scatter(NsgaSortArgs a, int64_t total)
 {
     const int64_t q = (int64_t)blockIdx.x * 256 + threadIdx.x;
     if (q >= total) return;
-    const int32_t i = a.list[q], k = a.front[i];
-    const int32_t b = a.foff[k], e = a.foff[k + 1];
-    float fi[kNsgaMaxM];
-    int32_t c[kNsgaMaxM];
-    for (int m = 0; m < a.M; ++m) {
-        fi[m] = a.F[(int64_t)i * a.M + m];
-        c[m] = 0;
-    }
-    for (int32_t r = b; r < e; ++r) {
-        const int32_t j = a.list[r];
-        for (int m = 0; m < a.M; ++m) {
-            const float fj = a.F[(int64_t)j * a.M + m];
-            c[m] += (fj < fi[m]) || (fj == fi[m] && j < i);
-        }
-    }
-    for (int m = 0; m < a.M; ++m) {
-        a.pos[m * a.cap + q] = c[m];
-        a.sorted[m * a.cap + b + c[m]] = i;
-    }
+    const int32_t i = a.list[q], b = a.foff[a.front[i]];
+    for (int m = 0; m < a.M; ++m) a.sorted[m * a.cap + b + a.pos[m * a.cap + q]] = i;
 }
 
 // Crowding distance of list entry q: per objective in order, +inf at either
@@ -227,25 +296,39 @@ __global__ __launch_bounds__(256) void k_nsga_crowd(NsgaSortArgs a, int64_t tota
     a.crowd[i] = d;
 }
 
-// keep[i] for the survivors: members of the fronts before the last, and the
-// last front's members ranked below `need` by (crowding descending, index).
-__global__ __launch_bounds__(256) void k_nsga_trunc(const int32_t *list, int64_t full, int64_t total, int64_t need,
-                                                    const double *crowd, int32_t *keep)
+// Rank of the last front's entry q (list positions [full, total)) in the
+// order of (crowding descending, index): rank[q - full] += #{entries of this
+// block's span ahead of it}.
+__global__ __launch_bounds__(256) void k_nsga_trunc(const int32_t *list, int64_t full, int64_t total,
+                                                    const double *crowd, int32_t *rank)
+{
+    __shared__ double cj[kSpan];
+    __shared__ int32_t ij[kSpan];
+    const int64_t size = total - full, r0 = (int64_t)blockIdx.y * kSpan;
+    const int64_t nr = size - r0 < kSpan ? size - r0 : kSpan;
+    for (int64_t r = threadIdx.x; r < nr; r += 256) {
+        const int32_t j = list[full + r0 + r];
+        ij[r] = j;
+        cj[r] = crowd[j];
+    }
+    __syncthreads();
+    const int64_t q = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (q >= size) return;
+    const int32_t i = list[full + q];
+    const double ci = crowd[i];
+    int32_t c = 0;
+    for (int64_t r = 0; r < nr; ++r) c += cj[r] > ci || (cj[r] == ci && ij[r] < i);
+    if (c) atomicAdd(rank + q, c);
+}
+
+// keep[i] for the survivors: the members of the fronts before the last, and
+// the last front's entries ranked below `need`.
+__global__ __launch_bounds__(256) void k_nsga_keep(const int32_t *list, int64_t full, int64_t total, int64_t need,
+                                                   const int32_t *rank, int32_t *keep)
 {
     const int64_t q = (int64_t)blockIdx.x * 256 + threadIdx.x;
     if (q >= total) return;
-    const int32_t i = list[q];
-    if (q < full) {
-        keep[i] = 1;
-        return;
-    }
-    const double ci = crowd[i];
-    int64_t r = 0;
-    for (int64_t s = full; s < total; ++s) {
-        const int32_t j = list[s];
-        r += crowd[j] > ci || (crowd[j] == ci && j < i);
-    }
-    if (r < need) keep[i] = 1;
+    if (q < full || rank[q - full] < need) keep[list[q]] = 1;
 }
 
 // Exclusive prefix sums of keep[0 .. n) (one block; n <= 1024 * per-thread).
@@ -296,6 +379,18 @@ __global__ __launch_bounds__(256) void k_fill_i32(int32_t *p, int64_t n, int32_t
 
 unsigned blocks(int64_t n, int64_t per) { return (unsigned)((n + per - 1) / per); }
 
+#define EVOX_NSGA_M_SWITCH(M, CALL) \
+    switch (M) {                   \
+        case 2: CALL(2); break;    \
+        case 3: CALL(3); break;    \
+        case 4: CALL(4); break;    \
+        case 5: CALL(5); break;    \
+        case 6: CALL(6); break;    \
+        case 7: CALL(7); break;    \
+        case 8: CALL(8); break;    \
+        default: return hipErrorInvalidValue; \
+    }
+
 }  // namespace
 
 hipError_t launch_nsga_var(const NsgaVarArgs &a, hipStream_t s)
@@ -322,7 +417,10 @@ hipError_t nsga_count(const NsgaSortArgs &a, hipStream_t s)
                        n, -1);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if ((e = launch_zero_u32(a.cnt, n, s)) != hipSuccess) return e;
-    hipLaunchKernelGGL(k_nsga_count, dim3(blocks(n, 256), blocks(n, kSpan)), dim3(256), 0, s, a.F, n, a.M, a.cnt);
+    const dim3 grid(blocks(n, 256), blocks(n, kSpan));
+#define EVOX_COUNT(MM) hipLaunchKernelGGL((k_nsga_count<MM>), grid, dim3(256), 0, s, a.F, n, a.cnt)
+    EVOX_NSGA_M_SWITCH(a.M, EVOX_COUNT)
+#undef EVOX_COUNT
     return hipGetLastError();
 }
 
@@ -352,16 +450,27 @@ hipError_t nsga_fronts(const NsgaSortArgs &a, int64_t need, NsgaSortResult *res,
         assigned += size;
         ++k;
         if (assigned < need) {
-            hipLaunchKernelGGL(k_nsga_peel, dim3(blocks(n, 256), blocks(size, kSpan)), dim3(256), 0, s, a.F, n, a.M,
-                               (const int32_t *)(a.list + assigned - size), (int64_t)size, (const int32_t *)a.front,
-                               a.cnt);
+            const dim3 grid(blocks(n, 256), blocks(size, kSpan));
+            const int32_t *members = a.list + assigned - size;
+#define EVOX_PEEL(MM)                                                                                      \
+    hipLaunchKernelGGL((k_nsga_peel<MM>), grid, dim3(256), 0, s, a.F, n, members, (int64_t)size,           \
+                       (const int32_t *)a.front, a.cnt)
+            EVOX_NSGA_M_SWITCH(a.M, EVOX_PEEL)
+#undef EVOX_PEEL
             if ((e = hipGetLastError()) != hipSuccess) return e;
         }
     }
     hipLaunchKernelGGL(k_nsga_foff, dim3(blocks(assigned, 256)), dim3(256), 0, s, (const int32_t *)a.list, assigned,
                        (const int32_t *)a.front, a.foff);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    hipLaunchKernelGGL(k_nsga_order, dim3(blocks(assigned, 256)), dim3(256), 0, s, a, assigned);
+    hipLaunchKernelGGL(k_fill_i32, dim3(4096), dim3(256), 0, s, a.pos, (int64_t)a.M * a.cap, 0);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    const dim3 og(blocks(assigned, 256), blocks(assigned, kSpan));
+#define EVOX_ORDER(MM) hipLaunchKernelGGL((k_nsga_order<MM>), og, dim3(256), 0, s, a, assigned)
+    EVOX_NSGA_M_SWITCH(a.M, EVOX_ORDER)
+#undef EVOX_ORDER
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL(k_nsga_scatter, dim3(blocks(assigned, 256)), dim3(256), 0, s, a, assigned);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     hipLaunchKernelGGL(k_nsga_crowd, dim3(blocks(assigned, 256)), dim3(256), 0, s, a, assigned);
     if ((e = hipGetLastError()) != hipSuccess) return e;
@@ -382,8 +491,12 @@ hipError_t launch_nsga_select(const NsgaSelArgs &a, const NsgaSortResult &r, hip
     hipLaunchKernelGGL(k_fill_i32, dim3(blocks(2 * a.N, 256) < 4096 ? blocks(2 * a.N, 256) : 4096), dim3(256), 0, s,
                        a.keep, 2 * a.N, 0);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    hipLaunchKernelGGL(k_nsga_trunc, dim3(blocks(r.assigned, 256)), dim3(256), 0, s, a.list, full, r.assigned, need,
-                       a.crowdR, a.keep);
+    if ((e = launch_zero_u32((uint32_t *)a.rank, r.last, s)) != hipSuccess) return e;
+    hipLaunchKernelGGL(k_nsga_trunc, dim3(blocks(r.last, 256), blocks(r.last, kSpan)), dim3(256), 0, s, a.list, full,
+                       r.assigned, a.crowdR, a.rank);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL(k_nsga_keep, dim3(blocks(r.assigned, 256)), dim3(256), 0, s, a.list, full, r.assigned, need,
+                       (const int32_t *)a.rank, a.keep);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     hipLaunchKernelGGL(k_nsga_scan, dim3(1), dim3(1024), 0, s, (const int32_t *)a.keep, 2 * a.N, a.pre);
     if ((e = hipGetLastError()) != hipSuccess) return e;
