@@ -29,6 +29,7 @@ class RefParams(ctypes.Structure):
         ("es_sigma", ctypes.c_float), ("es_lr", ctypes.c_float),
         ("pgpe_sigma_lr", ctypes.c_float), ("pgpe_max_change", ctypes.c_float),
         ("seed", ctypes.c_uint64),
+        ("cso_local", ctypes.c_int32),
     ]
 
 
@@ -62,6 +63,7 @@ def lib():
         L.evox_ref_pso_init.argtypes = [P, P, P, P, P, P, P, P]
         L.evox_ref_pso_step.argtypes = [P, i64, i64, P, P, P, P, P, P, P]
         L.evox_ref_colmean.argtypes = [P, i64, i64, P]
+        L.evox_ref_ring_mean.argtypes = [P, i64, i64, P]
         L.evox_ref_perm.argtypes = [u64, i64, i64, P]
         L.evox_ref_argsort_u32.argtypes = [P, i64, P]
         L.evox_ref_de_choices.argtypes = [u64, i64, i64, i64, i64, P]
@@ -175,11 +177,12 @@ def init_normal(seed, N, D, mu, sigma):
 
 def make_params(fn, N, D, lb, ub, v_lo=0.0, v_hi=0.0, w=0.6, c1=1.5, c2=1.5, phi=0.1,
                 vmax=0.0, clamp_x=0, seed=0, x_init=0, x_mu=0.0, x_sigma=1.0, de_f=0.5, de_cr=0.9,
-                es_sigma=0.1, es_lr=0.01, pgpe_sigma_lr=0.01, pgpe_max_change=0.2):
+                es_sigma=0.1, es_lr=0.01, pgpe_sigma_lr=0.01, pgpe_max_change=0.2, cso_local=0):
     return RefParams(fn=fn, clamp_x=clamp_x, N=N, D=D, lb=lb, ub=ub, v_lo=v_lo, v_hi=v_hi,
                      w=w, c1=c1, c2=c2, phi=phi, vmax=vmax, x_init=x_init, x_mu=x_mu,
                      x_sigma=x_sigma, de_f=de_f, de_cr=de_cr, es_sigma=es_sigma, es_lr=es_lr,
-                     pgpe_sigma_lr=pgpe_sigma_lr, pgpe_max_change=pgpe_max_change, seed=seed)
+                     pgpe_sigma_lr=pgpe_sigma_lr, pgpe_max_change=pgpe_max_change, seed=seed,
+                     cso_local=cso_local)
 
 
 class PSO:
@@ -527,6 +530,14 @@ class NSGA2:
         if rc != 0:
             raise ValueError(f"evox_ref_nsga2_step rc={rc}")
         self.t += n_gens
+
+
+def ring_mean(X):
+    """Each row's ring-neighbourhood mean (rows i - 1, i, i + 1 modulo N)."""
+    X = _f32(np.atleast_2d(X))
+    out = np.zeros_like(X)
+    lib().evox_ref_ring_mean(_ptr(X), X.shape[0], X.shape[1], _ptr(out))
+    return out
 
 
 def gemm(A, B, ta=False, tb=False, alpha=1.0, beta=0.0, C=None):

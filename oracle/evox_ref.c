@@ -255,6 +255,7 @@ typedef struct {
     float pgpe_sigma_lr;     /* PGPE standard-deviation learning rate */
     float pgpe_max_change;   /* PGPE bound on the relative change of a standard deviation */
     uint64_t seed;      /* Philox key */
+    int32_t cso_local;  /* CSO: 0 = the swarm mean, 1 = the mean of the ring neighbourhood */
 } evox_ref_params;
 
 /* Algorithm.setup (Sec. IV-A): uniform initial population and velocity.
@@ -451,9 +452,23 @@ int evox_ref_cso_init(const evox_ref_params *P, float *x, float *v, float *fit)
     return evox_ref_eval(P->fn, x, P->N, P->D, P->D, fit);
 }
 
-/* n_gens CSO iterations from generation t0.  Each: swarm mean of the current
- * positions; random pairing; each loser l moves toward its winner w and the
- * mean,
+/* The ring-neighbourhood means of CSO's local version (Cheng and Jin, 2015,
+ * whose x-bar may be the mean of a predefined neighbourhood): individual i's
+ * neighbourhood is i - 1, i, i + 1 (indices modulo N), and its mean
+ * ((x_{i-1} + x_i) + x_{i+1}) / 3 is taken in fp64 and rounded once. */
+void evox_ref_ring_mean(const float *X, int64_t N, int64_t D, float *out)
+{
+    for (int64_t i = 0; i < N; ++i) {
+        const int64_t a = (i + N - 1) % N, b = (i + 1) % N;
+        for (int64_t j = 0; j < D; ++j)
+            out[i * D + j] = (float)((((double)X[a * D + j] + (double)X[i * D + j]) + (double)X[b * D + j]) / 3.0);
+    }
+}
+
+/* n_gens CSO iterations from generation t0.  Each: the mean xbar of the
+ * current positions -- the swarm's, or with cso_local each loser's ring
+ * neighbourhood mean, all taken before any loser moves; random pairing; each
+ * loser l moves toward its winner w and the mean,
  *     v_l <- R1 v_l + R2 (x_w - x_l) + phi R3 (xbar - x_l),  x_l <- x_l + v_l,
  * and only the losers are re-evaluated.  Afterwards (best_fit, best_idx) is
  * the best of the current swarm.  loser_flag (nullable, N bytes) receives 1
@@ -463,11 +478,14 @@ int evox_ref_cso_step(const evox_ref_params *P, int64_t t0, int64_t n_gens, floa
 {
     const int64_t N = P->N, D = P->D;
     if (N < 1 || D < 1 || n_gens < 0 || P->fn < 0 || P->fn >= FN_COUNT) return -1;
-    float *xbar = (float *)malloc(sizeof(float) * (size_t)D);
+    float *xbar = (float *)malloc(sizeof(float) * (size_t)(P->cso_local ? N * D : D));
     int64_t *perm = (int64_t *)malloc(sizeof(int64_t) * (size_t)N);
     uint8_t *is_loser = (uint8_t *)calloc((size_t)N, 1);
     for (int64_t t = t0; t < t0 + n_gens; ++t) {
-        evox_ref_colmean(x, N, D, xbar);
+        if (P->cso_local)
+            evox_ref_ring_mean(x, N, D, xbar);
+        else
+            evox_ref_colmean(x, N, D, xbar);
         evox_ref_perm(P->seed, t, N, perm);
         memset(is_loser, 0, (size_t)N);
         for (int64_t k = 0; k < N / 2; ++k) {
@@ -483,7 +501,7 @@ int evox_ref_cso_step(const evox_ref_params *P, int64_t t0, int64_t n_gens, floa
                 float t0v = R1 * vl;
                 float t1v = fmaf(R2, xw - xl, t0v);
                 float c = P->phi * R3;
-                float vn = fmaf(c, xbar[j] - xl, t1v);
+                float vn = fmaf(c, xbar[(P->cso_local ? l * D : 0) + j] - xl, t1v);
                 float xn = xl + vn;
                 if (P->clamp_x) xn = fminf(fmaxf(xn, P->lb), P->ub);
                 v[l * D + j] = vn;

@@ -159,3 +159,60 @@ def test_argsort_is_a_stable_sort(ref):
     for keys in cases:
         keys = np.asarray(keys, dtype=np.uint32)
         assert np.array_equal(ref.argsort_u32(keys), np.argsort(keys, kind="stable"))
+
+
+# ---- the neighbourhood version (the loser learns from its ring neighbourhood's mean) ----
+
+def test_ring_mean_hand_worked(ref):
+    X = np.array([[0.0], [3.0], [6.0], [9.0]], np.float32)
+    assert ref.ring_mean(X)[:, 0].tolist() == [4.0, 3.0, 6.0, 5.0]     # (9+0+3)/3, (0+3+6)/3, ...
+    Y = np.array([[1.0, 2.0], [2.0, 2.0], [4.0, -3.0]], np.float32)     # N = 3: every ring is the swarm
+    assert np.array_equal(ref.ring_mean(Y), np.repeat(ref.colmean(Y)[None], 3, axis=0))
+
+
+def test_three_individuals_local_equals_global(ref):
+    a = fresh(ref, 3, 9, seed=12, cso_local=0)
+    b = fresh(ref, 3, 9, seed=12, cso_local=1)
+    for _ in range(6):
+        a.step(1)
+        b.step(1)
+        assert np.array_equal(a.x, b.x) and np.array_equal(a.v, b.v) and np.array_equal(a.fit, b.fit)
+
+
+def test_loser_learns_from_its_ring_mean(ref, rocrand_philox):
+    """v = 0: v_l' = R2 (x_w - x_l) + phi R3 (m_l - x_l), so m_l is decoded from
+    the update with rocRAND's words and must be the mean of rows l - 1, l, l + 1
+    (wrapping), which here is far from the swarm mean."""
+    N, D, seed, phi = 10, 3, 13, 0.5
+    s = fresh(ref, N, D, seed=seed, phi=phi, cso_local=1)
+    x0 = (np.arange(N, dtype=np.float32)[:, None] ** 2 * np.array([1.0, -2.0, 0.5], np.float32)).astype(np.float32)
+    s.x[:] = x0
+    s.v[:] = 0.0
+    s.fit[:] = np.arange(N, dtype=np.float32)[::-1]
+    perm = ref.perm(seed, 0, N)
+    f0 = s.fit.copy()
+    s.step(1)
+    ring = (np.roll(x0, 1, 0).astype(np.float64) + x0 + np.roll(x0, -1, 0)) / 3
+    glob = x0.astype(np.float64).mean(0)
+    for k in range(N // 2):
+        a, b = perm[2 * k], perm[2 * k + 1]
+        w, l = (b, a) if f0[b] < f0[a] else (a, b)
+        words = rocrand_philox([(seed, 3 * (j // 4) + q, l, 0, 3) for j in range(D) for q in (1, 2)])
+        R2 = u01_exact([words[2 * j, j % 4] for j in range(D)]).astype(np.float64)
+        R3 = u01_exact([words[2 * j + 1, j % 4] for j in range(D)]).astype(np.float64)
+        xl, xw = x0[l].astype(np.float64), x0[w].astype(np.float64)
+        m = xl + (s.v[l].astype(np.float64) - R2 * (xw - xl)) / (np.float32(phi) * R3)
+        scale = np.abs(xl) + np.abs(xw) + np.abs(ring[l]) + 1
+        assert np.all(np.abs(m - ring[l]) <= 1e-5 * scale / (phi * R3)), (l, m, ring[l])
+        assert np.any(np.abs(m - glob) > 1e-2 * scale), l
+
+
+def test_local_version_converges_and_resumes(ref):
+    a = fresh(ref, 40, 10, seed=14, cso_local=1)
+    b = fresh(ref, 40, 10, seed=14, cso_local=1)
+    f0 = a.best_fit if a.t else float(a.fit.min())
+    a.step(200)
+    for n in (1, 99, 100):
+        b.step(n)
+    assert np.array_equal(a.x, b.x) and np.array_equal(a.fit, b.fit)
+    assert a.best_fit < 0.5 * f0
