@@ -90,9 +90,11 @@ def maes_flops(w):
 def cso_bytes_per_launch(w):
     # per pair: read winner row, loser x and v, write loser x and v
     # (20 B per pair element = 10 B per individual element); fitness of both
-    # and the permutation entries (4 B each), write loser fitness
+    # and the permutation entries (4 B each), write loser fitness; the
+    # neighbourhood version also reads the loser's mean row (4 B per pair
+    # element)
     pairs = w.N // 2
-    return 20.0 * pairs * w.D + pairs * (4 * 2 + 4 * 2 + 4)
+    return (24.0 if w.cso_local else 20.0) * pairs * w.D + pairs * (4 * 2 + 4 * 2 + 4)
 
 
 def host_cpu():
@@ -153,7 +155,7 @@ def _cpu_baseline(w, budget_s):
     # MA-ES: the oracle's matrix product costs D^3 per generation, so the
     # sample keeps the population and shrinks the dimension
     D = min(w.D, 1024) if w.algo == "maes" else w.D
-    P = oracle.make_params(fn, rows, D, w.lb, w.ub, v_lo=w.v_lo, v_hi=w.v_hi, w=w.w, c1=w.c1,
+    P = oracle.make_params(fn, rows, D, w.lb, w.ub, cso_local=w.cso_local, v_lo=w.v_lo, v_hi=w.v_hi, w=w.w, c1=w.c1,
                            c2=w.c2, phi=w.phi, vmax=w.vmax, seed=w.seed, de_f=w.de_f,
                            de_cr=w.de_cr, es_sigma=w.es_sigma, es_lr=w.es_lr,
                            pgpe_sigma_lr=w.pgpe_sigma_lr, pgpe_max_change=w.pgpe_max_change)
@@ -233,7 +235,7 @@ def main():
                              c1=w.c1, c2=w.c2, phi=w.phi, vmax=w.vmax, seed=w.seed,
                              ldx=args.ldx or None, de_f=w.de_f, de_cr=w.de_cr,
                              es_sigma=w.es_sigma, es_lr=w.es_lr, pgpe_sigma_lr=w.pgpe_sigma_lr,
-                             pgpe_max_change=w.pgpe_max_change, n_obj=w.n_obj)
+                             pgpe_max_change=w.pgpe_max_change, n_obj=w.n_obj, cso_local=w.cso_local)
         swarm = evox.Swarm(P)
 
         def step():

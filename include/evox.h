@@ -108,7 +108,9 @@ typedef struct evox_params {
     int32_t n_obj;    /* NSGA2: objectives of DTLZ1, 2 .. 8 (D >= n_obj) */
     float sbx_eta;    /* NSGA2: distribution index of the simulated binary crossover */
     float pm_eta;     /* NSGA2: distribution index of the polynomial mutation */
-    int32_t reserved; /* zero */
+    int32_t cso_local; /* CSO: 0 = losers learn from the swarm mean; 1 = from the mean of their
+                          ring neighbourhood (rows i-1, i, i+1 modulo N, taken before the
+                          generation moves anyone) */
 } evox_params;
 
 /* Caller-owned device buffers, borrowed by the state (row-major, pitch ldx;

@@ -53,7 +53,7 @@ class Params(ctypes.Structure):
         ("pgpe_sigma_lr", ctypes.c_float), ("pgpe_max_change", ctypes.c_float),
         ("seed", ctypes.c_uint64),
         ("n_obj", ctypes.c_int32), ("sbx_eta", ctypes.c_float), ("pm_eta", ctypes.c_float),
-        ("reserved", ctypes.c_int32),
+        ("cso_local", ctypes.c_int32),
     ]
 
 
@@ -238,12 +238,13 @@ def pitch(D, algo=PSO):
 def make_params(algo, fn_id, N, D, lb, ub, v_lo=0.0, v_hi=0.0, w=0.6, c1=1.5, c2=1.5, phi=0.1,
                 vmax=0.0, clamp_x=0, seed=0, ldx=None, x_init=0, x_mu=0.0, x_sigma=1.0, de_f=0.5,
                 de_cr=0.9, es_sigma=0.1, es_lr=0.01, pgpe_sigma_lr=0.01, pgpe_max_change=0.2, n_obj=3,
-                sbx_eta=20.0, pm_eta=20.0):
+                sbx_eta=20.0, pm_eta=20.0, cso_local=0):
     return Params(algo=algo, fn_id=fn_id, N=N, D=D, ldx=pitch(D, algo) if ldx is None else ldx,
                   lb=lb, ub=ub, v_lo=v_lo, v_hi=v_hi, w=w, c1=c1, c2=c2, phi=phi, vmax=vmax,
                   clamp_x=clamp_x, x_init=x_init, x_mu=x_mu, x_sigma=x_sigma, de_f=de_f,
                   de_cr=de_cr, es_sigma=es_sigma, es_lr=es_lr, pgpe_sigma_lr=pgpe_sigma_lr,
-                  pgpe_max_change=pgpe_max_change, seed=seed, n_obj=n_obj, sbx_eta=sbx_eta, pm_eta=pm_eta)
+                  pgpe_max_change=pgpe_max_change, seed=seed, n_obj=n_obj, sbx_eta=sbx_eta, pm_eta=pm_eta,
+                  cso_local=cso_local)
 
 
 def evox_scratch_bytes(params):

@@ -78,6 +78,7 @@ struct Plan {
     int64_t xsum_rows = 0;
     int perm_batch = 0;
     size_t x2 = 0, fit2 = 0;  // DE: the other population buffer and its fitness
+    size_t xloc = 0;          // CSO neighbourhood version: the losers' mean rows
     size_t esrank = 0, espart = 0;  // ES: sample ranks, gradient partial sums
     // MA-ES: deviates, steps, split-K workspace, update factors, parents,
     // weights, path-norm partial sums
@@ -181,6 +182,8 @@ int make_plan(const evox_params *P, Plan *pl)
     if (P->ldx < P->D || (P->ldx & 3))
         return fail(EVOX_EINVAL, "ldx = %lld must be >= D and a multiple of 4", (long long)P->ldx);
     if (P->x_init != 0 && P->x_init != 1) return fail(EVOX_EINVAL, "unknown x_init %d", P->x_init);
+    if (P->cso_local != 0 && (P->cso_local != 1 || P->algo != EVOX_CSO))
+        return fail(EVOX_EINVAL, "cso_local = %d: 0, or 1 for CSO", P->cso_local);
     Plan p;
     const int family = P->algo == EVOX_CSO ? LAYOUT_CSO : LAYOUT_PSO;
     if (!row_layout(P->D, family, &p.L)) return fail(EVOX_EINVAL, "no row layout for D = %lld", (long long)P->D);
@@ -212,6 +215,7 @@ int make_plan(const evox_params *P, Plan *pl)
         p.xsum = take(sizeof(double) * (size_t)cap * (size_t)P->ldx);
         p.s1 = take(sizeof(double) * (size_t)kMeanStages * (size_t)P->ldx);
         p.ticket = take(sizeof(uint32_t) * (size_t)((P->ldx + 63) / 64));
+        if (P->cso_local) p.xloc = take(sizeof(float) * (size_t)P->N * (size_t)P->ldx);
     }
     if (P->algo == EVOX_DE) {
         p.x2 = take(sizeof(float) * (size_t)P->N * (size_t)P->ldx);
@@ -745,8 +749,13 @@ int evox_cso_step(evox_state *s, int64_t n_gens)
             s->perm_t0 = t;
         }
         const uint32_t *perm = s->perm + (t - s->perm_t0) * P.N;
-        CsoArgs ca{s->B.x, s->B.v, s->B.fit, s->B.xbar, perm, P.N, P.D, P.ldx, P.phi, P.lb, P.ub,
-                   P.clamp_x != 0, s->k0, s->k1, (uint32_t)t, s->slots, s->xsum};
+        // the neighbourhood version's mean rows, from the positions before the
+        // generation moves anyone (the generation kernel updates in place)
+        float *xloc = P.cso_local ? at<float>(s->B.scratch, pl.xloc) : nullptr;
+        if (xloc && (e = launch_ring_mean(s->B.x, P.N, P.ldx, xloc, s->stream)) != hipSuccess)
+            return hip_fail(e, "neighbourhood means");
+        CsoArgs ca{s->B.x, s->B.v, s->B.fit, xloc ? xloc : s->B.xbar, perm, P.N, P.D, P.ldx, P.phi, P.lb, P.ub,
+                   P.clamp_x != 0, s->k0, s->k1, (uint32_t)t, s->slots, s->xsum, xloc ? P.ldx : 0};
         e = timed(s, [&] { return launch_cso(P.fn_id, pl.L, ca, pl.cso_grid, s->stream); });
         if (e != hipSuccess) return hip_fail(e, "cso generation");
         if ((e = launch_cso_mean(mean_args(s, pl.cso_grid), s->stream)) != hipSuccess)

@@ -288,7 +288,7 @@ __global__ __launch_bounds__(block_for(G)) void k_cso(CsoArgs a)
                     const int64_t off = l * a.ldx + 4 * c;
                     const float4 xl = ld_stream(a.x + off);
                     const float4 vl = ld_stream(a.v + off);
-                    const float4 xb = *reinterpret_cast<const float4 *>(a.xbar + 4 * c);
+                    const float4 xb = *reinterpret_cast<const float4 *>(a.xbar + l * a.xbar_ld + 4 * c);
                     const U4 R1 = philox((uint32_t)(3 * c), (uint32_t)l, a.t, STREAM_CSO, a.k0, a.k1);
                     const U4 R2 = philox((uint32_t)(3 * c + 1), (uint32_t)l, a.t, STREAM_CSO, a.k0, a.k1);
                     const U4 R3 = philox((uint32_t)(3 * c + 2), (uint32_t)l, a.t, STREAM_CSO, a.k0, a.k1);

@@ -205,6 +205,7 @@ struct CsoArgs {
     uint32_t k0, k1, t;
     SelSlots *slots;
     double *xsum;  // [grid][ldx] column partial sums of the new positions
+    int64_t xbar_ld;  // 0: one mean row for the swarm; ldx: loser l's mean is row l
 };
 
 hipError_t launch_pso(int fn, Layout L, int mode, const PsoArgs &a, int grid, hipStream_t s);
@@ -233,6 +234,9 @@ hipError_t launch_init(const InitArgs &a, hipStream_t s);
 hipError_t launch_philox_fill(uint32_t k0, uint32_t k1, uint32_t c1, uint32_t c2, uint32_t c3,
                               int64_t n, uint32_t *out, hipStream_t s);
 hipError_t launch_stream_copy(const float *src, float *dst, int64_t n, hipStream_t s);
+// CSO's neighbourhood version: out row i = ((x_{i-1} + x_i) + x_{i+1}) / 3
+// (indices modulo N) in fp64, rounded once; every column of the pitch.
+hipError_t launch_ring_mean(const float *x, int64_t N, int64_t ldx, float *out, hipStream_t s);
 hipError_t launch_copy_row(const float *src, float *dst, int64_t ldx, hipStream_t s);
 hipError_t launch_fill(float *dst, int64_t n, float value, hipStream_t s);
 hipError_t launch_best_init(DevBest *best, float f, int64_t i, hipStream_t s);

@@ -46,6 +46,7 @@ class Workload:
     pgpe_sigma_lr: float = 0.01
     pgpe_max_change: float = 0.2
     n_obj: int = 3
+    cso_local: int = 0
 
 
 WORKLOADS = {
@@ -57,6 +58,8 @@ WORKLOADS = {
                                       200, 2, lb=-5.12, ub=5.12, vmax=0.2 * 10.24),
     "cso_griewank_1e6x100": Workload("cso_griewank_1e6x100", CSO, "griewank", 1_000_000, 100, 200,
                                      3, lb=-600.0, ub=600.0, phi=0.1),
+    "cso_local_griewank_1e6x100": Workload("cso_local_griewank_1e6x100", CSO, "griewank", 1_000_000, 100,
+                                           200, 3, lb=-600.0, ub=600.0, phi=0.1, cso_local=1),
     "de_sphere_1e5x1e3": Workload("de_sphere_1e5x1e3", DE, "sphere", 100_000, 1_000, 200, 5,
                                   lb=-32.0, ub=32.0),
     "es_sphere_1e4x1e4": Workload("es_sphere_1e4x1e4", ES, "sphere", 10_000, 10_000, 100, 6,

@@ -158,3 +158,44 @@ def test_default_pitch_is_line_aligned(evox_gpu, ref):
     g = evox_gpu.Swarm(evox_gpu.make_params(evox_gpu.CSO, 3, 64, 100, -600.0, 600.0, seed=3))
     assert g.P.ldx == 128
     assert g.x.data_ptr() % 128 == 0 and (g.P.ldx * 4) % 128 == 0
+
+
+LOCAL_CASES = [
+    dict(fn=3, N=1000, D=100, seed=3, lb=-600.0, ub=600.0, gens=15),
+    dict(fn=1, N=64, D=37, seed=1, lb=-32.768, ub=32.768, v_lo=-1.0, v_hi=1.0, gens=15),
+    dict(fn=2, N=33, D=257, seed=2, lb=-5.12, ub=5.12, clamp_x=1, gens=10),
+    dict(fn=0, N=3, D=5, seed=7, lb=-1.0, ub=1.0, gens=10),
+    dict(fn=0, N=2, D=1, seed=8, lb=-1.0, ub=1.0, gens=10),
+]
+
+
+@pytest.mark.parametrize("case", LOCAL_CASES, ids=[f"fn{c['fn']}-{c['N']}x{c['D']}" for c in LOCAL_CASES])
+def test_neighbourhood_version_matches_oracle(evox_gpu, ref, case):
+    """The ring means are computed in the oracle's fp64 order, so rows and
+    velocities match bit for bit generation after generation."""
+    c = dict(case)
+    gens = c.pop("gens")
+    print(f"cso local {c} gens={gens}", flush=True)
+    g, r = pair(evox_gpu, ref, cso_local=1, **c)
+    for t in range(gens):
+        g.step(1)
+        r.step(1)
+        compare(g, r, c["fn"], f"generation {t}", strict=True)
+    assert g.t == r.t
+
+
+def test_neighbourhood_version_equals_swarm_version_at_three(evox_gpu, ref):
+    a, _ = pair(evox_gpu, ref, 0, 3, 9, 12, -5.0, 5.0)
+    b, _ = pair(evox_gpu, ref, 0, 3, 9, 12, -5.0, 5.0, cso_local=1)
+    a.step(8)
+    b.step(8)
+    for name in ("x", "v", "fit"):
+        assert torch.equal(getattr(a, name), getattr(b, name)), name
+
+
+def test_neighbourhood_flag_only_for_cso(evox_gpu):
+    import paper_2301_12457_amd as ev
+    with pytest.raises(ev.EvoxError):
+        ev.Swarm(ev.make_params(ev.PSO, 0, 10, 5, -1.0, 1.0, cso_local=1))
+    with pytest.raises(ev.EvoxError):
+        ev.Swarm(ev.make_params(ev.CSO, 0, 10, 5, -1.0, 1.0, cso_local=2))
