@@ -287,7 +287,8 @@ def main():
             gen_s = ms / 1e3 / w.gens
             roofline = {"bound": "mfma", "achieved": round(achieved, 2), "peak": MFMA_F32_PEAK_TFLOPS,
                         "unit": "TFLOP/s", "frac": round(achieved / MFMA_F32_PEAK_TFLOPS, 4),
-                        "traffic": None, "kernel": "k_gemm_nt<128,64> + k_splitk_reduce (Z M^T)",
+                        "traffic": None, "kernel": "k_gemm_nt<%d,%d> + k_splitk_reduce (Z M^T)" % (
+                            64 if w.N + 1 <= 64 else 128, 64 if w.N + 1 <= 128 else 128),
                         "avg_launch_us": round(avg_ms * 1e3, 2), "launches": launches,
                         "algorithmic_flops_per_launch": f_sample,
                         "generation_us": round(gen_s * 1e6, 2),

@@ -83,11 +83,12 @@ struct Plan {
     // MA-ES: deviates, steps, split-K workspace, update factors, parents,
     // weights, path-norm partial sums
     size_t mae_z = 0, mae_d = 0, mae_work = 0, mae_at = 0, mae_bt = 0, mae_sel = 0, mae_w = 0, mae_part = 0;
+    size_t mae_wpart = 0;
     int mae_splits = 1;
     int64_t mae_mu = 0, mae_kp = 0, mae_ldf = 0;
     // NSGA-II: offspring, survivors' rows, merged objectives / fronts /
     // crowding, the sorting scratch, survivor flags and their prefix sums
-    size_t ns_q = 0, ns_x2 = 0, ns_fr = 0, ns_frontr = 0, ns_crowdr = 0, ns_keep = 0, ns_pre = 0;
+    size_t ns_q = 0, ns_x2 = 0, ns_fr = 0, ns_frontr = 0, ns_crowdr = 0, ns_keep = 0, ns_pre = 0, ns_sums = 0;
     size_t ns_cnt = 0, ns_list = 0, ns_foff = 0, ns_pos = 0, ns_sorted = 0, ns_len = 0;
     size_t total = 0;
 };
@@ -245,6 +246,7 @@ int make_plan(const evox_params *P, Plan *pl)
         p.mae_sel = take(sizeof(int32_t) * (size_t)p.mae_mu);
         p.mae_w = take(sizeof(double) * (size_t)p.mae_mu);
         p.mae_part = take(sizeof(double) * ((D + kMaeBlock - 1) / kMaeBlock));
+        p.mae_wpart = take(sizeof(double) * 2 * D * (size_t)((p.mae_mu + kMaeChunk - 1) / kMaeChunk));
     }
     if (P->algo == EVOX_NSGA2) {
         const size_t N = (size_t)P->N, R = 2 * N, M = (size_t)P->n_obj;
@@ -255,6 +257,7 @@ int make_plan(const evox_params *P, Plan *pl)
         p.ns_crowdr = take(sizeof(double) * R);
         p.ns_keep = take(sizeof(int32_t) * R);
         p.ns_pre = take(sizeof(int32_t) * R);
+        p.ns_sums = take(sizeof(int32_t) * ((R + 1023) / 1024));
         const NsgaSortScratch l = nsga_sort_layout((int64_t)R, P->n_obj, off);
         p.ns_cnt = l.cnt;
         p.ns_list = l.list;
@@ -488,6 +491,7 @@ int evox_state_create(const evox_params *params, const evox_buffers *b, void *hi
         m.At = at<float>(b->scratch, pl.mae_at);
         m.Bt = at<float>(b->scratch, pl.mae_bt);
         m.part = at<double>(b->scratch, pl.mae_part);
+        m.wpart = at<double>(b->scratch, pl.mae_wpart);
         m.cs = cs;
         m.cz = std::sqrt(me * cs * (2.0 - cs));
         m.hc1 = 0.5 * c1;
@@ -512,8 +516,9 @@ int evox_state_create(const evox_params *params, const evox_buffers *b, void *hi
                                   at<uint32_t>(b->scratch, pl.ns_len)};
         s->ns_sel = NsgaSelArgs{b->x, at<float>(b->scratch, pl.ns_q), P.N, P.ldx, P.n_obj, FR, frontR, crowdR,
                                 s->ns_sort.list, at<int32_t>(b->scratch, pl.ns_keep),
-                                at<int32_t>(b->scratch, pl.ns_pre), s->ns_sort.pos, at<float>(b->scratch, pl.ns_x2),
-                                b->obj, b->front, b->crowd};
+                                at<int32_t>(b->scratch, pl.ns_pre), s->ns_sort.pos,
+                                at<int32_t>(b->scratch, pl.ns_sums), at<float>(b->scratch, pl.ns_x2), b->obj,
+                                b->front, b->crowd};
     }
     if (P.algo == EVOX_CSO) {
         s->hist = at<uint32_t>(b->scratch, pl.hist);

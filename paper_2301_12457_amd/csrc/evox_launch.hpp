@@ -71,6 +71,7 @@ struct EsGradArgs {
 // K-contiguous factors of the matrix update; k_mae_sigma the step size; the
 // rank-(mu + 1) pass M <- beta M + At^T Bt the new M.
 constexpr int kMaeBlock = 256;  // threads (columns) per block of the recombination
+constexpr int kMaeChunk = 64;   // parents per partial weighted sum
 constexpr int kMaeRankUnrolled = 32;  // rank-pass step counts with an unrolled kernel of their own
 struct MaeEvalArgs {
     const float *y, *d;   // center [ldx]; steps [N][ldd]
@@ -91,6 +92,7 @@ struct MaeArgs {
     float *y, *s, *sigma; // center [ldx], path [ldx], step size [1]
     float *At, *Bt;       // [kp][ldf], k-major, zero past term mu and column D
     double *part;         // [ceil(D / kMaeBlock)] partial sums of |s|^2
+    double *wpart;        // [ceil(mu / kMaeChunk)][2][D] weighted parent sums per chunk
     double cs, cz, hc1, hcw, damp, chi;  // c_s, sqrt(mu_eff c_s (2 - c_s)), c_1 / 2, c_w / 2, c_s / d_s, chi_D
     uint32_t k0, k1, t;
 };
@@ -141,6 +143,7 @@ struct NsgaSelArgs {
     const int32_t *list;   // [2N] from the sort
     int32_t *keep, *pre;   // [2N]
     int32_t *rank;         // [2N] last-front ranks (the sort's free per-objective positions)
+    int32_t *sums;         // [ceil(2N / 1024)] block sums of the survivor prefix sums
     float *X2;             // [N][ldx] survivors' rows
     float *F;              // [N][M]
     int32_t *front;        // [N]

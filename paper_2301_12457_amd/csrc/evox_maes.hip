@@ -48,34 +48,57 @@ __global__ __launch_bounds__(256) void k_mae_select(MaeArgs a)
     if (r < (uint32_t)a.mu) a.sel[r] = (int32_t)k;
 }
 
-// One thread per column j: the weighted parent sums <z>_w and <d>_w in fp64,
-// y_j <- y_j + sigma <d>_w, s_j <- (1 - c_s) s_j + c_z <z>_w, column j of the
-// factors (term r at At[r][j], Bt[r][j]; the zero terms past mu and the zero
-// columns past D are set once at creation)
-//     At[., j] = (d_{1:N, j}, ..., d_{mu:N, j}, (M s')_j)
-//     Bt[., j] = (c_w/2 w_1 z_{1:N, j}, ..., c_w/2 w_mu z_{mu:N, j}, c_1/2 s'_j)
-// and the block's sum of s'_j^2 (fp64, fixed order).
-__global__ __launch_bounds__(kMaeBlock) void k_mae_recombine(MaeArgs a)
+// Factor terms r < mu, one thread per (column j, term r): At[r][j] = d_{r:N, j}
+// and Bt[r][j] = c_w/2 w_r z_{r:N, j} (rounded once).
+__global__ __launch_bounds__(256) void k_mae_gather(MaeArgs a)
+{
+    const int64_t j = (int64_t)blockIdx.x * 256 + threadIdx.x, r = blockIdx.y;
+    if (j >= a.D) return;
+    const int64_t k = a.sel[r];
+    a.At[r * a.ldf + j] = a.Dm[k * a.ldx + j];
+    a.Bt[r * a.ldf + j] = (float)(a.hcw * a.w[r] * (double)a.Z[k * a.ldx + j]);
+}
+
+// Weighted parent sums over chunk c of kMaeChunk parents, one thread per
+// column: wpart[c][0][j] = sum w_r z_{r:N, j}, wpart[c][1][j] = sum w_r d_{r:N, j}
+// (fp64, parents in rank order).
+__global__ __launch_bounds__(256) void k_mae_wsum(MaeArgs a)
+{
+    const int64_t j = (int64_t)blockIdx.x * 256 + threadIdx.x, c = blockIdx.y;
+    if (j >= a.D) return;
+    const int64_t r0 = c * kMaeChunk, r1 = r0 + kMaeChunk < a.mu ? r0 + kMaeChunk : a.mu;
+    double zw = 0.0, dw = 0.0;
+    for (int64_t r = r0; r < r1; ++r) {
+        const int64_t k = a.sel[r];
+        const double wr = a.w[r];
+        zw += wr * (double)a.Z[k * a.ldx + j];
+        dw += wr * (double)a.Dm[k * a.ldx + j];
+    }
+    a.wpart[(2 * c) * a.D + j] = zw;
+    a.wpart[(2 * c + 1) * a.D + j] = dw;
+}
+
+// One thread per column j: <z>_w and <d>_w from the chunk sums (in chunk
+// order), y_j <- y_j + sigma <d>_w, s_j <- (1 - c_s) s_j + c_z <z>_w, the last
+// factor term (At[mu][j] = (M s')_j, Bt[mu][j] = c_1/2 s'_j; the terms past mu
+// and the columns past D are zero from creation), and the block's sum of
+// s'_j^2 (fp64, fixed order).  Term r < mu of the factors is
+//     At[r][j] = d_{r:N, j},  Bt[r][j] = c_w/2 w_r z_{r:N, j}  (k_mae_gather).
+__global__ __launch_bounds__(kMaeBlock) void k_mae_recombine(MaeArgs a, int64_t nchunks)
 {
     __shared__ double red[kMaeBlock];
     const int64_t j = (int64_t)blockIdx.x * kMaeBlock + threadIdx.x;
     double sq = 0.0;
     if (j < a.D) {
         double zw = 0.0, dw = 0.0;
-        float *at = a.At + j, *bt = a.Bt + j;
-        for (int64_t r = 0; r < a.mu; ++r) {
-            const int64_t k = a.sel[r];
-            const double wr = a.w[r];
-            const float z = a.Z[k * a.ldx + j], d = a.Dm[k * a.ldx + j];
-            zw += wr * (double)z;
-            dw += wr * (double)d;
-            at[r * a.ldf] = d;
-            bt[r * a.ldf] = (float)(a.hcw * wr * (double)z);
+        for (int64_t c = 0; c < nchunks; ++c) {
+            zw += a.wpart[(2 * c) * a.D + j];
+            dw += a.wpart[(2 * c + 1) * a.D + j];
         }
         const double sig = (double)*a.sigma, keep = 1.0 - a.cs;
         const float sn = (float)(keep * (double)a.s[j] + a.cz * zw);
-        at[a.mu * a.ldf] = (float)(keep * (double)a.Dm[a.N * a.ldx + j] + a.cz * dw);
-        bt[a.mu * a.ldf] = (float)(a.hc1 * (double)sn);
+        a.At[a.mu * a.ldf + j] = (float)(keep * (double)a.Dm[a.N * a.ldx + j] + a.cz * dw);
+        a.Bt[a.mu * a.ldf + j] = (float)(a.hc1 * (double)sn);
         a.y[j] = (float)((double)a.y[j] + sig * dw);
         a.s[j] = sn;
         sq = (double)sn * (double)sn;
@@ -139,20 +162,38 @@ __global__ __launch_bounds__(256) void k_mae_rank(MaeArgs a, float *M, float bet
         for (int v = 0; v < 16; ++v) acc[n][v] = 0.0f;
     const float *pa = a.At + h * a.ldf + i0 + col;
     const float *pb = a.Bt + h * a.ldf + j0 + col;
-    const int64_t steps = STEPS > 0 ? STEPS : a.kp / 2;
-    for (int64_t c0 = 0; c0 < steps; c0 += CH) {
-        float av[CH], b0[CH], b1[CH];
+    float av[2][CH], b0[2][CH], b1[2][CH];
+    auto load = [&](int buf, int64_t c0) {
 #pragma unroll
         for (int t = 0; t < CH; ++t) {
             const int64_t off = 2 * (c0 + t) * a.ldf;
-            av[t] = pa[off];
-            b0[t] = pb[off];
-            b1[t] = pb[off + 32];
+            av[buf][t] = pa[off];
+            b0[buf][t] = pb[off];
+            b1[buf][t] = pb[off + 32];
         }
+    };
+    auto products = [&](int buf) {
 #pragma unroll
         for (int t = 0; t < CH; ++t) {
-            acc[0] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[t], b0[t], acc[0], 0, 0, 0);
-            acc[1] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[t], b1[t], acc[1], 0, 0, 0);
+            acc[0] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[buf][t], b0[buf][t], acc[0], 0, 0, 0);
+            acc[1] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[buf][t], b1[buf][t], acc[1], 0, 0, 0);
+        }
+    };
+    if constexpr (STEPS > 0) {
+        load(0, 0);
+        products(0);
+    } else {
+        // any number of steps (a multiple of CH): the next block's operands
+        // are loaded while the current block's products run
+        const int64_t steps = a.kp / 2;
+        load(0, 0);
+        for (int64_t c0 = 0; c0 < steps; c0 += 2 * CH) {
+            if (c0 + CH < steps) load(1, c0 + CH);
+            products(0);
+            if (c0 + CH < steps) {
+                if (c0 + 2 * CH < steps) load(0, c0 + 2 * CH);
+                products(1);
+            }
         }
     }
 #pragma unroll
@@ -193,10 +234,15 @@ hipError_t launch_mae_select(const MaeArgs &a, hipStream_t s)
 
 hipError_t launch_mae_recombine(const MaeArgs &a, hipStream_t s)
 {
-    const int64_t nparts = (a.D + kMaeBlock - 1) / kMaeBlock;
-    hipLaunchKernelGGL(k_mae_recombine, dim3((unsigned)nparts), dim3(kMaeBlock), 0, s, a);
+    const int64_t nparts = (a.D + kMaeBlock - 1) / kMaeBlock, cols = (a.D + 255) / 256;
+    const int64_t nchunks = (a.mu + kMaeChunk - 1) / kMaeChunk;
+    hipLaunchKernelGGL(k_mae_gather, dim3((unsigned)cols, (unsigned)a.mu), dim3(256), 0, s, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(k_mae_wsum, dim3((unsigned)cols, (unsigned)nchunks), dim3(256), 0, s, a);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL(k_mae_recombine, dim3((unsigned)nparts), dim3(kMaeBlock), 0, s, a, nchunks);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
     hipLaunchKernelGGL(k_mae_sigma, dim3(1), dim3(256), 0, s, a, nparts);
     return hipGetLastError();
 }

@@ -331,26 +331,63 @@ __global__ __launch_bounds__(256) void k_nsga_keep(const int32_t *list, int64_t 
     if (q < full || rank[q - full] < need) keep[list[q]] = 1;
 }
 
-// Exclusive prefix sums of keep[0 .. n) (one block; n <= 1024 * per-thread).
-__global__ __launch_bounds__(1024) void k_nsga_scan(const int32_t *keep, int64_t n, int32_t *pre)
+// Exclusive prefix sums of keep[0 .. n) in three passes: each block of
+// kScanChunk entries sums its entries; one block turns the block sums into
+// exclusive offsets; each block scans its entries from its offset.
+constexpr int kScanChunk = 1024;
+
+__global__ __launch_bounds__(256) void k_nsga_scan_sums(const int32_t *keep, int64_t n, int32_t *sums)
 {
-    __shared__ int32_t part[1024];
-    const int64_t per = (n + 1023) / 1024, b = threadIdx.x * per, e = b + per < n ? b + per : n;
-    int32_t s = 0;
-    for (int64_t i = b; i < e; ++i) s += keep[i];
+    __shared__ int32_t part[256];
+    const int64_t b = (int64_t)blockIdx.x * kScanChunk;
+    int32_t v = 0;
+    for (int64_t i = b + threadIdx.x; i < b + kScanChunk && i < n; i += 256) v += keep[i];
+    part[threadIdx.x] = v;
+    __syncthreads();
+    for (int o = 128; o > 0; o /= 2) {
+        if (threadIdx.x < (unsigned)o) part[threadIdx.x] += part[threadIdx.x + o];
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) sums[blockIdx.x] = part[0];
+}
+
+__global__ __launch_bounds__(256) void k_nsga_scan_offsets(int32_t *sums, int64_t nb)
+{
+    if (threadIdx.x != 0) return;
+    int32_t run = 0;
+    for (int64_t q = 0; q < nb; ++q) {
+        const int32_t v = sums[q];
+        sums[q] = run;
+        run += v;
+    }
+}
+
+__global__ __launch_bounds__(256) void k_nsga_scan_local(const int32_t *keep, int64_t n, const int32_t *sums,
+                                                         int32_t *pre)
+{
+    __shared__ int32_t part[256];
+    const int64_t b = (int64_t)blockIdx.x * kScanChunk + 4 * threadIdx.x;
+    int32_t v[4], s = 0;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        v[e] = b + e < n ? keep[b + e] : 0;
+        s += v[e];
+    }
     part[threadIdx.x] = s;
     __syncthreads();
-    for (int o = 1; o < 1024; o *= 2) {
-        const int32_t v = threadIdx.x >= (unsigned)o ? part[threadIdx.x - o] : 0;
+    for (int o = 1; o < 256; o *= 2) {
+        const int32_t t = threadIdx.x >= (unsigned)o ? part[threadIdx.x - o] : 0;
         __syncthreads();
-        part[threadIdx.x] += v;
+        part[threadIdx.x] += t;
         __syncthreads();
     }
-    int32_t run = threadIdx.x ? part[threadIdx.x - 1] : 0;
-    for (int64_t i = b; i < e; ++i) {
-        pre[i] = run;
-        run += keep[i];
-    }
+    int32_t run = sums[blockIdx.x] + (threadIdx.x ? part[threadIdx.x - 1] : 0);
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+        if (b + e < n) {
+            pre[b + e] = run;
+            run += v[e];
+        }
 }
 
 // Survivor i of the merged population (parents 0..N-1, offspring N..2N-1)
@@ -498,7 +535,14 @@ hipError_t launch_nsga_select(const NsgaSelArgs &a, const NsgaSortResult &r, hip
     hipLaunchKernelGGL(k_nsga_keep, dim3(blocks(r.assigned, 256)), dim3(256), 0, s, a.list, full, r.assigned, need,
                        (const int32_t *)a.rank, a.keep);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    hipLaunchKernelGGL(k_nsga_scan, dim3(1), dim3(1024), 0, s, (const int32_t *)a.keep, 2 * a.N, a.pre);
+    const int64_t nb = (2 * a.N + kScanChunk - 1) / kScanChunk;
+    hipLaunchKernelGGL(k_nsga_scan_sums, dim3((unsigned)nb), dim3(256), 0, s, (const int32_t *)a.keep, 2 * a.N,
+                       a.sums);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL(k_nsga_scan_offsets, dim3(1), dim3(256), 0, s, a.sums, nb);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL(k_nsga_scan_local, dim3((unsigned)nb), dim3(256), 0, s, (const int32_t *)a.keep, 2 * a.N,
+                       (const int32_t *)a.sums, a.pre);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     hipLaunchKernelGGL(k_nsga_compact, dim3(blocks(2 * a.N * (a.ldx / 4), 256)), dim3(256), 0, s, a);
     return hipGetLastError();

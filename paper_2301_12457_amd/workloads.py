@@ -68,6 +68,8 @@ WORKLOADS = {
                                     lb=-5.0, ub=5.0, es_sigma=1.0, es_lr=0.5, pgpe_sigma_lr=0.1),
     "maes_sphere_100x16384": Workload("maes_sphere_100x16384", MAES, "sphere", 100, 16_384, 20, 10,
                                       lb=-5.0, ub=5.0, es_sigma=1.0),
+    "maes_sphere_4096x1830": Workload("maes_sphere_4096x1830", MAES, "sphere", 4096, 1830, 10, 12,
+                                      lb=-5.0, ub=5.0, es_sigma=1.0),
     "nsga2_dtlz1_16384x100": Workload("nsga2_dtlz1_16384x100", NSGA2, "dtlz1", 16_384, 100, 10, 11,
                                       lb=0.0, ub=1.0, n_obj=3),
     "eval_rosenbrock_1m_x1e3": Workload("eval_rosenbrock_1m_x1e3", EVAL, "rosenbrock", 1_048_576,
