@@ -5,7 +5,8 @@ The oracle is single-threaded (about 30 ns per element and generation), so
 the PSO / CSO workloads are compared over their first generations (every
 element, bit for bit: 40 of the Ackley 1e4 x 1e3 run, 4 of the Rastrigin
 1e5 x 1e3 run, 3 of the CSO 1e6 x 100 run) rather than the whole run; the
-evaluation-only workload is compared on every row.
+evaluation-only workload is compared on every row.  The CSO neighbourhood
+version is compared over 3 generations of its 1e6 x 100 run.
 """
 import numpy as np
 import pytest
@@ -22,7 +23,7 @@ def swarm_pair(evox, ref, w):
     algo = {"pso": evox.PSO, "cso": evox.CSO, "de": evox.DE}[w.algo]
     fn = evox.FN_IDS[w.fn]
     kw = dict(v_lo=w.v_lo, v_hi=w.v_hi, w=w.w, c1=w.c1, c2=w.c2, phi=w.phi, vmax=w.vmax,
-              seed=w.seed, de_f=w.de_f, de_cr=w.de_cr)
+              seed=w.seed, de_f=w.de_f, de_cr=w.de_cr, cso_local=w.cso_local)
     g = evox.Swarm(evox.make_params(algo, fn, w.N, w.D, w.lb, w.ub, **kw))
     Ref = {"pso": ref.PSO, "cso": ref.CSO, "de": ref.DE}[w.algo]
     r = Ref(ref.make_params(fn, w.N, w.D, w.lb, w.ub, **kw))
@@ -68,6 +69,22 @@ def test_cso_workload_first_generations(evox_gpu, ref):
         assert index_ok(fn, r.x, r.fit, bi, r.best_idx)
         if not exact_mean:   # a 1-ulp mean difference moves the losers slightly: stop here
             break
+
+
+def test_cso_neighbourhood_workload_first_generations(evox_gpu, ref):
+    """The neighbourhood version at its benchmark size: the ring means are
+    computed in the oracle's order, so rows and velocities match bit for bit."""
+    w = WORKLOADS["cso_local_griewank_1e6x100"]
+    g, r, fn = swarm_pair(evox_gpu, ref, w)
+    D = w.D
+    for t in range(3):
+        g.step(1)
+        r.step(1)
+        assert np.array_equal(g.x[:, :D].cpu().numpy(), r.x), f"generation {t}: x"
+        assert np.array_equal(g.v[:, :D].cpu().numpy(), r.v), f"generation {t}: v"
+        assert_fitness(fn, r.x, g.fit.cpu().numpy(), r.fit, f"generation {t}: fit")
+        bf, bi = g.best()
+        assert index_ok(fn, r.x, r.fit, bi, r.best_idx)
 
 
 def test_de_workload_first_generations(evox_gpu, ref):
