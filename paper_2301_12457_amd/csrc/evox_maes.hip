@@ -137,9 +137,13 @@ __global__ __launch_bounds__(256) void k_mae_sigma(MaeArgs a, int64_t nparts)
 // is loaded first; the operands of a fully unrolled block of steps are all
 // issued before its products, so that a wave waits for them once.  No LDS,
 // no barrier.  STEPS = 0: any number of steps (a.kp / 2, a multiple of 16),
-// 16 at a time.
+// 16 at a time, double-buffered: the next block's loads are in flight while
+// the current block's products run.  The unrolled kernels are compiled for
+// 4 waves per SIMD (124 registers); the general one holds two blocks of
+// operands at one wave per SIMD, which measured faster than 2 or 3 waves
+// with 8-step blocks.
 template <int STEPS>
-__global__ __launch_bounds__(256) void k_mae_rank(MaeArgs a, float *M, float beta)
+__device__ __forceinline__ void rank_body(const MaeArgs &a, float *M, float beta)
 {
     constexpr int CH = STEPS > 0 ? STEPS : 16;
     const int lane = threadIdx.x % 64, col = lane % 32, h = lane / 32;
@@ -205,6 +209,18 @@ __global__ __launch_bounds__(256) void k_mae_rank(MaeArgs a, float *M, float bet
         }
 }
 
+template <int STEPS>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void k_mae_rank(MaeArgs a, float *M,
+                                                                                           float beta)
+{
+    rank_body<STEPS>(a, M, beta);
+}
+
+__global__ __launch_bounds__(256) void k_mae_rank_any(MaeArgs a, float *M, float beta)
+{
+    rank_body<0>(a, M, beta);
+}
+
 __global__ __launch_bounds__(256) void k_mae_identity(float *M, int64_t D, int64_t ldx)
 {
     const int64_t total = D * ldx;
@@ -263,7 +279,7 @@ hipError_t launch_mae_rank(const MaeArgs &a, float *M, float beta, hipStream_t s
         EVOX_RANK_CASE(26) EVOX_RANK_CASE(27) EVOX_RANK_CASE(28) EVOX_RANK_CASE(29) EVOX_RANK_CASE(30)
         EVOX_RANK_CASE(31) EVOX_RANK_CASE(32)
 #undef EVOX_RANK_CASE
-        default: hipLaunchKernelGGL((k_mae_rank<0>), grid, block, 0, s, a, M, beta); break;
+        default: hipLaunchKernelGGL(k_mae_rank_any, grid, block, 0, s, a, M, beta); break;
     }
     return hipGetLastError();
 }
