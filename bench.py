@@ -66,12 +66,13 @@ def de_bytes_per_launch(w):
 # OpenES is bound by vector-ALU work (the perturbations are regenerated, not
 # stored): lane-ops per perturbation element and generation, counted from
 # the computation as written -- Philox4x32-10 is 10 rounds of two 32x32->64
-# products (4 ops) and 4 xors per 4 elements (20), Box-Muller 16 ops per 2
-# elements (8), the two samples and their Sphere terms (4); the gradient
-# pass regenerates the perturbation (28) and adds its weighted value (1).
-ES_OPS_PER_ELEMENT = 20 + 8 + 4 + 28 + 1
+# products (4 ops) and two three-input xors (one instruction each on gfx950)
+# per 4 elements (15), Box-Muller 16 ops per 2 elements (8), the two samples
+# and their Sphere terms (4); the gradient pass regenerates the perturbation
+# (23) and adds its weighted value (1).
+ES_OPS_PER_ELEMENT = 15 + 8 + 4 + 23 + 1
 # PGPE: the same, with two weighted sums in the gradient pass (z and z^2 - 1)
-PGPE_OPS_PER_ELEMENT = 20 + 8 + 4 + 28 + 3
+PGPE_OPS_PER_ELEMENT = 15 + 8 + 4 + 23 + 3
 ALU_PEAK_TOPS = 256 * 64 * 2.4e9 / 1e12   # 256 CUs x 64 lanes x 2.4 GHz, 32-bit lane-ops
 MFMA_F32_PEAK_TFLOPS = 157.3              # dense fp32 matrix-core peak
 # NSGA-II's dominance pass: per ordered pair of the merged population, two

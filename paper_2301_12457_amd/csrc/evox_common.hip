@@ -665,25 +665,39 @@ hipError_t launch_es_rank(const float *fit, int64_t N, uint32_t *rank, hipStream
 template <bool PGPE>
 __global__ __launch_bounds__(256) void k_es_grad(EsGradArgs a)
 {
+    // the chunk's pair weights, computed once per block (three fp64
+    // divisions per pair) and read from LDS by every column
+    __shared__ double wts[PGPE ? 2 : 1][kEsPairChunk];
+    static_assert(kEsPairChunk <= 256, "one thread per pair of the chunk");
     const int64_t C4 = (a.D + 3) / 4;
     const int64_t c = (int64_t)blockIdx.x * 256 + threadIdx.x, b = blockIdx.y;
-    if (c >= C4) return;
     const int64_t k0 = b * kEsPairChunk, k1 = k0 + kEsPairChunk < a.H ? k0 + kEsPairChunk : a.H;
-    const double nm1 = (double)(2 * a.H - 1);
+    if (threadIdx.x < k1 - k0) {
+        const int64_t k = k0 + threadIdx.x;
+        const double nm1 = (double)(2 * a.H - 1);
+        const double u0 = (double)a.rank[2 * k] / nm1 - 0.5, u1 = (double)a.rank[2 * k + 1] / nm1 - 0.5;
+        if constexpr (PGPE) {
+            wts[0][threadIdx.x] = 0.5 * (u0 - u1) / (double)a.H;
+            wts[1][threadIdx.x] = 0.5 * (u0 + u1) / (double)a.H;
+        } else {
+            wts[0][threadIdx.x] = (u0 - u1) / ((double)(2 * a.H) * (double)a.sigma);
+        }
+    }
+    __syncthreads();
+    if (c >= C4) return;
     double s[4] = {0.0, 0.0, 0.0, 0.0}, q[4] = {0.0, 0.0, 0.0, 0.0};
     for (int64_t k = k0; k < k1; ++k) {
         const float4 z = normal4((uint32_t)c, (uint32_t)k, a.t, a.stream, a.k0, a.k1);
-        const double u0 = (double)a.rank[2 * k] / nm1 - 0.5, u1 = (double)a.rank[2 * k + 1] / nm1 - 0.5;
         const double zz[4] = {(double)z.x, (double)z.y, (double)z.z, (double)z.w};
         if constexpr (PGPE) {
-            const double m = 0.5 * (u0 - u1) / (double)a.H, sw = 0.5 * (u0 + u1) / (double)a.H;
+            const double m = wts[0][k - k0], sw = wts[1][k - k0];
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
                 s[e] = fma(m, zz[e], s[e]);
                 q[e] = fma(sw, zz[e] * zz[e] - 1.0, q[e]);
             }
         } else {
-            const double w = (u0 - u1) / ((double)(2 * a.H) * (double)a.sigma);
+            const double w = wts[0][k - k0];
 #pragma unroll
             for (int e = 0; e < 4; ++e) s[e] = fma(w, zz[e], s[e]);
         }

@@ -71,12 +71,17 @@ inline bool row_layout(int64_t D, int family, Layout *L)
 // ---------------------------------------------------------------------------
 // Philox4x32-10 (Salmon, Moraes, Dror, Shaw, SC'11): ten rounds of two
 // 32x32->64 multiplies and key xors, Weyl-incremented key.  Everything stays
-// in registers; the key is wave-uniform (SGPRs).
+// in registers; the key is wave-uniform (SGPRs).  Each round's two
+// three-input exclusive ors are single v_bitop3_b32 instructions (truth
+// table 0x96, odd parity of the three input bits) when kXor3: 40 instead of
+// 60 vector instructions per call.  kXor3 = false keeps the two-input form
+// for kernels where the denser schedule costs occupancy (same words).
 // ---------------------------------------------------------------------------
 struct U4 {
     uint32_t x, y, z, w;
 };
 
+template <bool kXor3 = true>
 __device__ __forceinline__ U4 philox(uint32_t c0, uint32_t c1, uint32_t c2, uint32_t c3,
                                      uint32_t k0, uint32_t k1)
 {
@@ -84,8 +89,14 @@ __device__ __forceinline__ U4 philox(uint32_t c0, uint32_t c1, uint32_t c2, uint
     for (int r = 0; r < 10; ++r) {
         const uint64_t m0 = (uint64_t)0xD2511F53u * (uint64_t)c0;
         const uint64_t m1 = (uint64_t)0xCD9E8D57u * (uint64_t)c2;
-        const uint32_t n0 = (uint32_t)(m1 >> 32) ^ c1 ^ k0;
-        const uint32_t n2 = (uint32_t)(m0 >> 32) ^ c3 ^ k1;
+        uint32_t n0, n2;
+        if constexpr (kXor3) {
+            n0 = __builtin_amdgcn_bitop3_b32((uint32_t)(m1 >> 32), c1, k0, 0x96);
+            n2 = __builtin_amdgcn_bitop3_b32((uint32_t)(m0 >> 32), c3, k1, 0x96);
+        } else {
+            n0 = (uint32_t)(m1 >> 32) ^ c1 ^ k0;
+            n2 = (uint32_t)(m0 >> 32) ^ c3 ^ k1;
+        }
         c1 = (uint32_t)m1;
         c3 = (uint32_t)m0;
         c0 = n0;
@@ -284,6 +295,38 @@ __device__ __forceinline__ float shfl_xor_g(float v, int m)
     return __shfl_xor(v, m, G < 64 ? G : 64);
 }
 
+// Combines the partials of a G-lane row group: butterfly inside the wave,
+// then (G > 64) across the group's waves through red (LDS of
+// block_for(G)/64 * 2 floats).  Every lane returns the combined partial.
+// Must be reached by every thread of the block (barriers when G > 64).
+template <int FN, int G>
+__device__ __forceinline__ Acc group_reduce(Acc s, float *red)
+{
+    using F = Fn<FN>;
+#pragma unroll
+    for (int m = (G < 64 ? G : 64) / 2; m >= 1; m >>= 1) {
+        Acc o{shfl_xor_g<G>(s.a, m), shfl_xor_g<G>(s.b, m)};
+        s = F::combine(s, o);
+    }
+    if constexpr (G > 64) {
+        const int tid = threadIdx.x;
+        constexpr int W = G / 64;  // waves per row
+        const int wave = tid / 64;
+        if ((tid & 63) == 0) {
+            red[2 * wave] = s.a;
+            red[2 * wave + 1] = s.b;
+        }
+        __syncthreads();
+        const int w0 = (wave / W) * W;
+        Acc t{red[2 * w0], red[2 * w0 + 1]};
+#pragma unroll
+        for (int q = 1; q < W; ++q) t = F::combine(t, Acc{red[2 * (w0 + q)], red[2 * (w0 + q) + 1]});
+        __syncthreads();
+        s = t;
+    }
+    return s;
+}
+
 template <int FN, int G, int MAXIT>
 __device__ __forceinline__ float row_fitness(const float4 (&xr)[MAXIT], int g, int64_t D,
                                              float *nbr, float *red)
@@ -334,28 +377,7 @@ __device__ __forceinline__ float row_fitness(const float4 (&xr)[MAXIT], int g, i
                 if (j0 + e < lim) F::elem(s, comp(v, e), n4[e], j0 + e);
         }
     }
-    // butterfly over the lanes of the row inside one wave
-#pragma unroll
-    for (int m = (G < 64 ? G : 64) / 2; m >= 1; m >>= 1) {
-        Acc o{shfl_xor_g<G>(s.a, m), shfl_xor_g<G>(s.b, m)};
-        s = F::combine(s, o);
-    }
-    if constexpr (G > 64) {
-        constexpr int W = G / 64;  // waves per row
-        const int wave = tid / 64;
-        if ((tid & 63) == 0) {
-            red[2 * wave] = s.a;
-            red[2 * wave + 1] = s.b;
-        }
-        __syncthreads();
-        const int w0 = (wave / W) * W;
-        Acc t{red[2 * w0], red[2 * w0 + 1]};
-#pragma unroll
-        for (int q = 1; q < W; ++q) t = F::combine(t, Acc{red[2 * (w0 + q)], red[2 * (w0 + q) + 1]});
-        __syncthreads();
-        s = t;
-    }
-    return F::finish(s, D);
+    return F::finish(group_reduce<FN, G>(s, red), D);
 }
 
 // ---------------------------------------------------------------------------

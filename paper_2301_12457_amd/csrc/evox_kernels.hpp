@@ -341,6 +341,8 @@ __global__ __launch_bounds__(block_for(G)) void k_cso(CsoArgs a)
 // the target row (streamed) and the three partner rows (gathered), the
 // crossover draws of Philox (1 + c, i, t, 6), mutant fma(F, x_r2 - x_r3,
 // x_r1), the trial evaluated from registers and kept when strictly better.
+// Philox in its two-input xor form here: the three-input form schedules the
+// kernel past 96 registers (4 instead of 5 waves per SIMD, 5 % slower).
 // Every target writes its next row (trial or copy) to the other buffer, so
 // all targets of a generation see the same population.
 // ---------------------------------------------------------------------------
@@ -369,7 +371,7 @@ __global__ __launch_bounds__(block_for(G)) void k_de(DeArgs a)
         const bool active = row < a.N;
         int64_t r[3] = {0, 0, 0}, jr = 0;
         if (active) {
-            const U4 w = philox(0u, (uint32_t)row, a.t, STREAM_DE, a.k0, a.k1);
+            const U4 w = philox<false>(0u, (uint32_t)row, a.t, STREAM_DE, a.k0, a.k1);
             const uint32_t wk[3] = {w.x, w.y, w.z};
             int64_t taken[3] = {row, 0, 0};
 #pragma unroll
@@ -403,7 +405,7 @@ __global__ __launch_bounds__(block_for(G)) void k_de(DeArgs a)
                 const float4 v1 = *reinterpret_cast<const float4 *>(a.x + r[0] * a.ldx + off);
                 const float4 v2 = *reinterpret_cast<const float4 *>(a.x + r[1] * a.ldx + off);
                 const float4 v3 = *reinterpret_cast<const float4 *>(a.x + r[2] * a.ldx + off);
-                const U4 cw = philox((uint32_t)(1 + c), (uint32_t)row, a.t, STREAM_DE, a.k0, a.k1);
+                const U4 cw = philox<false>((uint32_t)(1 + c), (uint32_t)row, a.t, STREAM_DE, a.k0, a.k1);
                 float uo[4];
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
@@ -447,7 +449,67 @@ __global__ __launch_bounds__(block_for(G)) void k_de(DeArgs a)
 // both samples fma(+-sigma, z, center) live in registers only, and both rows
 // are reduced to their fitness.  The center (and PGPE's sigma) are read by
 // every pair from the caches.
+//
+// k_es_eval_s (functions without neighbour coupling): each lane folds its
+// chunks into the two fitness partials as it generates them, so a lane can
+// take many chunks (kEsChunksPerLane) and the per-pair reductions and
+// barriers are spread over more deviates; k_es_eval (Rosenbrock) holds the
+// rows in registers for the neighbour term.
 // ---------------------------------------------------------------------------
+constexpr int kEsChunksPerLane = 16;
+
+template <int FN, int G>
+__global__ __launch_bounds__(block_for(G)) void k_es_eval_s(EsArgs a)
+{
+    using F = Fn<FN>;
+    static_assert(!F::kNeighbour, "neighbour-coupled functions use k_es_eval");
+    constexpr int B = block_for(G), RPB = B / G;
+    __shared__ float red[2 * (B / 64)];
+    __shared__ uint64_t sk[B / 64];
+    __shared__ uint32_t sc[B / 64];
+
+    const int tid = threadIdx.x, g = tid % G, slot = tid / G;
+    const int64_t C4 = (a.D + 3) >> 2, H = a.N / 2;
+    uint64_t best = kNoKey;
+    for (int64_t kb = (int64_t)blockIdx.x * RPB; kb < H; kb += (int64_t)gridDim.x * RPB) {
+        const int64_t k = kb + slot;
+        const bool active = k < H;
+        Acc sp = F::init(), sm = F::init();
+        if (active) {
+            for (int64_t c = g; c < C4; c += G) {
+                const float4 th = *reinterpret_cast<const float4 *>(a.theta + 4 * c);
+                const float4 sg = a.sig ? *reinterpret_cast<const float4 *>(a.sig + 4 * c)
+                                        : make_float4(a.sigma, a.sigma, a.sigma, a.sigma);
+                const float4 z = normal4((uint32_t)c, (uint32_t)k, a.t, a.stream, a.k0, a.k1);
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const int64_t j = 4 * c + e;
+                    if (j < a.D) {
+                        F::elem(sp, fmaf(comp(sg, e), comp(z, e), comp(th, e)), 0.0f, j);
+                        F::elem(sm, fmaf(-comp(sg, e), comp(z, e), comp(th, e)), 0.0f, j);
+                    }
+                }
+            }
+        }
+        const float fp = F::finish(group_reduce<FN, G>(sp, red), a.D);
+        const float fm = F::finish(group_reduce<FN, G>(sm, red), a.D);
+        if (active && g == 0) {
+            a.fit[2 * k] = fp;
+            a.fit[2 * k + 1] = fm;
+            a.rank[2 * k] = 0u;
+            a.rank[2 * k + 1] = 0u;
+            const uint64_t kp = sel_key(fp, 2 * k), km = sel_key(fm, 2 * k + 1);
+            best = kp < best ? kp : best;
+            best = km < best ? km : best;
+        }
+    }
+    if (a.slots) {
+        uint32_t none = 0;
+        block_min_key(best, none, sk, sc);
+        if (tid == 0) slot_commit(a.slots, best, 0);
+    }
+}
+
 template <int FN, int G, int MAXIT>
 __global__ __launch_bounds__(block_for(G)) void k_es_eval(EsArgs a)
 {
@@ -693,10 +755,35 @@ hipError_t launch_de_t(Layout L, const DeArgs &a, int grid, hipStream_t s)
 template <int FN>
 hipError_t launch_es_eval_t(Layout L, const EsArgs &a, int grid, hipStream_t s)
 {
-    switch (L.G * 16 + L.maxit) {
-        EVOX_FAMILY_CASES(EVOX_LAUNCH_ES, LAYOUT_PSO, 0)
-        EVOX_BIG_CASES(EVOX_LAUNCH_ES, LAYOUT_PSO, 0)
-        default: return hipErrorInvalidValue;
+    if constexpr (Fn<FN>::kNeighbour) {
+        switch (L.G * 16 + L.maxit) {
+            EVOX_FAMILY_CASES(EVOX_LAUNCH_ES, LAYOUT_PSO, 0)
+            EVOX_BIG_CASES(EVOX_LAUNCH_ES, LAYOUT_PSO, 0)
+            default: return hipErrorInvalidValue;
+        }
+    } else {
+        // the fewest lanes (a power of two, 4..1024) that hold the row in at
+        // most kEsChunksPerLane chunks per lane
+        const int64_t c4 = (a.D + 3) / 4;
+        int G = 4;
+        while (G < kMaxG && (c4 + G - 1) / G > kEsChunksPerLane) G *= 2;
+        const int64_t rpb = block_for(G) / G, H = a.N / 2;
+        int64_t nb = (H + rpb - 1) / rpb;
+        nb = nb < 1 ? 1 : nb > kMaxGrid ? kMaxGrid : nb;
+        const dim3 gs((unsigned)nb), bs((unsigned)block_for(G));
+        (void)grid;
+        switch (G) {
+            case 4: hipLaunchKernelGGL((k_es_eval_s<FN, 4>), gs, bs, 0, s, a); break;
+            case 8: hipLaunchKernelGGL((k_es_eval_s<FN, 8>), gs, bs, 0, s, a); break;
+            case 16: hipLaunchKernelGGL((k_es_eval_s<FN, 16>), gs, bs, 0, s, a); break;
+            case 32: hipLaunchKernelGGL((k_es_eval_s<FN, 32>), gs, bs, 0, s, a); break;
+            case 64: hipLaunchKernelGGL((k_es_eval_s<FN, 64>), gs, bs, 0, s, a); break;
+            case 128: hipLaunchKernelGGL((k_es_eval_s<FN, 128>), gs, bs, 0, s, a); break;
+            case 256: hipLaunchKernelGGL((k_es_eval_s<FN, 256>), gs, bs, 0, s, a); break;
+            case 512: hipLaunchKernelGGL((k_es_eval_s<FN, 512>), gs, bs, 0, s, a); break;
+            case 1024: hipLaunchKernelGGL((k_es_eval_s<FN, 1024>), gs, bs, 0, s, a); break;
+            default: return hipErrorInvalidValue;
+        }
     }
     return hipGetLastError();
 }
