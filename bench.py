@@ -302,7 +302,7 @@ def main():
             achieved = ops / gen_s / 1e12
             roofline = {"bound": "alu", "achieved": round(achieved, 2), "peak": ALU_PEAK_TOPS,
                         "unit": "Tops/s", "frac": round(achieved / ALU_PEAK_TOPS, 4),
-                        "traffic": None, "kernel": "k_es_eval + k_es_rank + k_es_grad + k_es_update",
+                        "traffic": None, "kernel": "k_es_eval_s + k_es_rank + k_es_grad + k_es_update",
                         "sample_kernel_avg_us": round(fused_ms / launches * 1e3, 2),
                         "generation_us": round(gen_s * 1e6, 2), "launches": launches,
                         "algorithmic_ops_per_generation": ops}

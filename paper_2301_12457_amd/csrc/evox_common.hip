@@ -713,40 +713,48 @@ __global__ __launch_bounds__(256) void k_es_grad(EsGradArgs a)
     }
 }
 
-// Pass 2: per column, the chunks' partial sums -- four quarter-sums in chunk
-// order, combined in a fixed order in LDS -- then the steps, each gradient
+// Pass 2: per column, the chunks' partial sums -- kEsUpdSlices slice sums in
+// chunk order, combined in a fixed order in LDS -- then the steps, each gradient
 // rounded to fp32 once:
 //   theta_j <- fma(-lr, g_j, theta_j)       (PGPE: g_j = sigma_j * sum)
 //   PGPE: d_j = -sig_lr * (sigma_j * sum'), clamped to +-max_change sigma_j,
 //         sigma_j <- sigma_j + d_j.
-// Block: 64 columns x 4 quarters.
+// Block: 64 columns x kEsUpdSlices slices.
+constexpr int kEsUpdSlices = 16;  // chunk-row slices summed in parallel per column
+
 template <bool PGPE>
-__global__ __launch_bounds__(256) void k_es_update(EsGradArgs a, int64_t chunks)
+__global__ __launch_bounds__(64 * kEsUpdSlices) void k_es_update(EsGradArgs a, int64_t chunks)
 {
-    __shared__ double q4[2][4][64];
+    __shared__ double qs[2][kEsUpdSlices][64];
     const int64_t C4 = (a.D + 3) / 4;
     const int col = threadIdx.x & 63, qt = threadIdx.x >> 6;
     const int64_t j = (int64_t)blockIdx.x * 64 + col;
-    const int64_t per = (chunks + 3) / 4, b0 = qt * per, b1 = b0 + per < chunks ? b0 + per : chunks;
+    const int64_t per = (chunks + kEsUpdSlices - 1) / kEsUpdSlices, b0 = qt * per,
+                  b1 = b0 + per < chunks ? b0 + per : chunks;
     double g = 0.0, h = 0.0;
     if (j < a.D)
         for (int64_t b = b0; b < b1; ++b) {
             g += a.part[b * 4 * C4 + j];
             if constexpr (PGPE) h += a.part[(chunks + b) * 4 * C4 + j];
         }
-    q4[0][qt][col] = g;
-    q4[1][qt][col] = h;
+    qs[0][qt][col] = g;
+    qs[1][qt][col] = h;
     __syncthreads();
     if (qt == 0 && j < a.D) {
-        const double gj = ((q4[0][0][col] + q4[0][1][col]) + q4[0][2][col]) + q4[0][3][col];
+        double gj = qs[0][0][col], hj = qs[1][0][col];
+#pragma unroll
+        for (int r = 1; r < kEsUpdSlices; ++r) {
+            gj += qs[0][r][col];
+            hj += qs[1][r][col];
+        }
         if constexpr (PGPE) {
-            const double hj = ((q4[1][0][col] + q4[1][1][col]) + q4[1][2][col]) + q4[1][3][col];
             const float sj = a.sig[j];
             a.theta[j] = fmaf(-a.lr, (float)((double)sj * gj), a.theta[j]);
             const float cap = a.max_change * sj;
             const float d = fminf(fmaxf(-a.sig_lr * (float)((double)sj * hj), -cap), cap);
             a.sig[j] = sj + d;
         } else {
+            (void)hj;
             a.theta[j] = fmaf(-a.lr, (float)gj, a.theta[j]);
         }
     }
@@ -758,10 +766,10 @@ hipError_t launch_es_grad(const EsGradArgs &a, hipStream_t s)
     const dim3 grid((unsigned)((C4 + 255) / 256), (unsigned)chunks), upd((unsigned)((a.D + 63) / 64));
     if (a.sig) {
         hipLaunchKernelGGL(k_es_grad<true>, grid, dim3(256), 0, s, a);
-        hipLaunchKernelGGL(k_es_update<true>, upd, dim3(256), 0, s, a, chunks);
+        hipLaunchKernelGGL(k_es_update<true>, upd, dim3(64 * kEsUpdSlices), 0, s, a, chunks);
     } else {
         hipLaunchKernelGGL(k_es_grad<false>, grid, dim3(256), 0, s, a);
-        hipLaunchKernelGGL(k_es_update<false>, upd, dim3(256), 0, s, a, chunks);
+        hipLaunchKernelGGL(k_es_update<false>, upd, dim3(64 * kEsUpdSlices), 0, s, a, chunks);
     }
     return hipGetLastError();
 }

@@ -36,9 +36,9 @@ struct DeArgs {
     bool nt;               // streaming hint on the target rows
 };
 
-// OpenES and PGPE.  k_es_eval: both samples center +- sigma z_k of each
-// antithetic pair from registers (sigma a scalar, or per dimension for
-// PGPE); k_es_rank: the ranks by counting (N <= kEsMaxN); k_es_grad /
+// OpenES and PGPE.  k_es_eval_s / k_es_eval: both samples center +-
+// sigma z_k of each antithetic pair from registers (sigma a scalar, or per
+// dimension for PGPE) and their fitness; k_es_rank: the ranks by counting (N <= kEsMaxN); k_es_grad /
 // k_es_update: the gradient estimates with the deviates regenerated from
 // Philox (never stored) and the steps.
 constexpr int kEsMaxN = 16384;
