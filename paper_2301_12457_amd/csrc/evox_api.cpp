@@ -112,7 +112,7 @@ NsgaSortScratch nsga_sort_layout(int64_t n, int32_t M, size_t off)
     l.foff = take(4 * ((size_t)n + 1));
     l.pos = take(4 * (size_t)M * (size_t)n);
     l.sorted = take(4 * (size_t)M * (size_t)n);
-    l.len = take(4);
+    l.len = take(4 * (size_t)kNsgaPeelBatch);
     l.end = off;
     return l;
 }

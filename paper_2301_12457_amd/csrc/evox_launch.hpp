@@ -106,6 +106,7 @@ int occupancy_gemm_nt_thin();  // resident blocks per CU of the sampling product
 // NSGA-II on DTLZ1.
 constexpr int kNsgaMaxM = 8;          // objectives
 constexpr int64_t kNsgaMaxN = 32768;  // population (the merged population is 2N)
+constexpr int kNsgaPeelBatch = 8;     // fronts peeled per host round trip
 struct NsgaVarArgs {
     const float *X;        // parents [N][ldx]
     int64_t N, D, ldx;
@@ -126,7 +127,7 @@ struct NsgaSortArgs {
     int32_t *foff;         // [n + 1] first list position of each front
     int32_t *pos, *sorted; // [M][cap] order within the front per objective
     int64_t cap;           // >= n
-    uint32_t *len;         // [1]
+    uint32_t *len;         // [kNsgaPeelBatch] sizes of the fronts of a peeling batch
 };
 struct NsgaSortResult {
     int32_t fronts;        // fronts assigned

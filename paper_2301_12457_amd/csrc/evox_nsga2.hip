@@ -161,24 +161,46 @@ __global__ __launch_bounds__(256) void k_nsga_count(const float *F, int64_t n, u
 }
 
 // Front k: unassigned points with no unassigned dominator, appended to list.
-__global__ __launch_bounds__(256) void k_nsga_mark(int32_t *front, const uint32_t *cnt, int64_t n, int32_t k,
-                                                   int32_t *list, uint32_t *len)
+// Fronts are peeled kNsgaPeelBatch at a time without a host round trip:
+// lens[kb] counts front (k0 + kb) of the batch, the fronts before the batch
+// hold `assigned0` points, and a front is only marked (peeled) while the
+// points assigned before it (with it) are fewer than `need`.
+__device__ __forceinline__ int64_t batch_base(const uint32_t *lens, int32_t kb, int64_t assigned0)
 {
+    int64_t base = assigned0;
+    for (int32_t r = 0; r < kb; ++r) base += lens[r];
+    return base;
+}
+
+__global__ __launch_bounds__(256) void k_nsga_mark(int32_t *front, const uint32_t *cnt, int64_t n, int32_t k,
+                                                   int32_t kb, int64_t assigned0, int64_t need, int32_t *list,
+                                                   uint32_t *lens)
+{
+    const int64_t base = batch_base(lens, kb, assigned0);
+    if (base >= need) return;  // the fronts needed are complete
     const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
     if (i >= n || front[i] != -1 || cnt[i] != 0) return;
     front[i] = k;
-    list[atomicAdd(len, 1u)] = (int32_t)i;
+    list[base + atomicAdd(lens + kb, 1u)] = (int32_t)i;
 }
 
 // cnt[i] -= #{j in this block's span of the new front : F_j dominates F_i}
 // for the points still unassigned.
 template <int M>
-__global__ __launch_bounds__(256) void k_nsga_peel(const float *F, int64_t n, const int32_t *list, int64_t size,
-                                                   const int32_t *front, uint32_t *cnt)
+__global__ __launch_bounds__(256) void k_nsga_peel(const float *F, int64_t n, const int32_t *list_all,
+                                                   const uint32_t *lens, int32_t kb, int64_t assigned0,
+                                                   int64_t need, const int32_t *front, uint32_t *cnt)
 {
     constexpr int P = M <= 4 ? 4 : 8;
     __shared__ __align__(16) float fj[kSpan * P];
-    const int64_t q0 = (int64_t)blockIdx.y * kSpan, nq = size - q0 < kSpan ? size - q0 : kSpan;
+    const int64_t base = batch_base(lens, kb, assigned0), size = lens[kb];
+    const int64_t q0 = (int64_t)blockIdx.y * kSpan;
+    // the grid covers the largest possible front; spans past this one's
+    // size, and every span once no later front is needed, exit at once
+    // (uniform over the block, before the barrier)
+    if (base + size >= need || q0 >= size) return;
+    const int32_t *list = list_all + base;
+    const int64_t nq = size - q0 < kSpan ? size - q0 : kSpan;
     for (int64_t q = threadIdx.x; q < nq; q += 256) load_pad<P>(fj + q * P, F, list[q0 + q], M);
     __syncthreads();
     const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
@@ -473,28 +495,29 @@ hipError_t nsga_fronts(const NsgaSortArgs &a, int64_t need, NsgaSortResult *res,
     if ((e = hipGetLastError()) != hipSuccess) return e;
     int64_t assigned = 0, last = 0;
     int32_t k = 0;
+    uint32_t lens[kNsgaPeelBatch];
     while (assigned < need) {
-        if ((e = launch_zero_u32(a.len, 1, s)) != hipSuccess) return e;
-        hipLaunchKernelGGL(k_nsga_mark, dim3(blocks(n, 256)), dim3(256), 0, s, a.front, (const uint32_t *)a.cnt, n,
-                           k, a.list + assigned, a.len);
-        if ((e = hipGetLastError()) != hipSuccess) return e;
-        uint32_t size = 0;
-        if ((e = hipMemcpyAsync(&size, a.len, sizeof size, hipMemcpyDeviceToHost, s)) != hipSuccess ||
-            (e = hipStreamSynchronize(s)) != hipSuccess)
-            return e;
-        if (size == 0) return hipErrorUnknown;  // cannot happen: a finite set has a non-dominated point
-        last = size;
-        assigned += size;
-        ++k;
-        if (assigned < need) {
-            const dim3 grid(blocks(n, 256), blocks(size, kSpan));
-            const int32_t *members = a.list + assigned - size;
+        if ((e = launch_zero_u32(a.len, kNsgaPeelBatch, s)) != hipSuccess) return e;
+        const dim3 grid(blocks(n, 256), blocks(n - assigned, kSpan));
+        for (int32_t kb = 0; kb < kNsgaPeelBatch; ++kb) {
+            hipLaunchKernelGGL(k_nsga_mark, dim3(blocks(n, 256)), dim3(256), 0, s, a.front,
+                               (const uint32_t *)a.cnt, n, k + kb, kb, assigned, need, a.list, a.len);
+            if ((e = hipGetLastError()) != hipSuccess) return e;
 #define EVOX_PEEL(MM)                                                                                      \
-    hipLaunchKernelGGL((k_nsga_peel<MM>), grid, dim3(256), 0, s, a.F, n, members, (int64_t)size,           \
-                       (const int32_t *)a.front, a.cnt)
+    hipLaunchKernelGGL((k_nsga_peel<MM>), grid, dim3(256), 0, s, a.F, n, (const int32_t *)a.list,          \
+                       (const uint32_t *)a.len, kb, assigned, need, (const int32_t *)a.front, a.cnt)
             EVOX_NSGA_M_SWITCH(a.M, EVOX_PEEL)
 #undef EVOX_PEEL
             if ((e = hipGetLastError()) != hipSuccess) return e;
+        }
+        if ((e = hipMemcpyAsync(lens, a.len, sizeof lens, hipMemcpyDeviceToHost, s)) != hipSuccess ||
+            (e = hipStreamSynchronize(s)) != hipSuccess)
+            return e;
+        for (int32_t kb = 0; kb < kNsgaPeelBatch && assigned < need; ++kb) {
+            if (lens[kb] == 0) return hipErrorUnknown;  // cannot happen: a finite set has a non-dominated point
+            last = lens[kb];
+            assigned += last;
+            ++k;
         }
     }
     hipLaunchKernelGGL(k_nsga_foff, dim3(blocks(assigned, 256)), dim3(256), 0, s, (const int32_t *)a.list, assigned,
