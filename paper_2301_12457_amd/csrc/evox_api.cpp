@@ -74,7 +74,7 @@ struct Plan {
     Layout L{0, 0, 0};
     int grid = 0, cso_grid = 0, colsum_grid = 0, bits = 0;
     size_t best = 0, slots = 0;
-    size_t hist = 0, offs = 0, cursor = 0, tkey = 0, tidx = 0, perm = 0, xsum = 0, s1 = 0, ticket = 0;
+    size_t hist = 0, offs = 0, cursor = 0, tkv = 0, perm = 0, xsum = 0, s1 = 0, ticket = 0;
     int64_t xsum_rows = 0;
     int perm_batch = 0;
     size_t x2 = 0, fit2 = 0;  // DE: the other population buffer and its fitness
@@ -209,8 +209,7 @@ int make_plan(const evox_params *P, Plan *pl)
         p.hist = take(4 * nb * B);
         p.offs = take(4 * (nb + 1) * B);
         p.cursor = take(4 * nb * B);
-        p.tkey = take(4 * (size_t)P->N * B);
-        p.tidx = take(4 * (size_t)P->N * B);
+        p.tkv = take(8 * (size_t)P->N * B);
         p.perm = take(4 * (size_t)P->N * B);
         p.xsum_rows = cap;
         p.xsum = take(sizeof(double) * (size_t)cap * (size_t)P->ldx);
@@ -283,7 +282,8 @@ struct evox_state {
     uint32_t k0, k1;
     DevBest *best;
     SelSlots *slots;
-    uint32_t *hist, *offs, *cursor, *tkey, *tidx, *perm, *ticket;
+    uint32_t *hist, *offs, *cursor, *perm, *ticket;
+    uint2 *tkv;
     int64_t perm_t0;  // first generation of the stored permutation batch (-1: none)
     double *xsum, *s1;
     float *x2, *fit2;  // DE: the other population buffer
@@ -363,9 +363,15 @@ PsoArgs pso_args(evox_state *s)
 }
 
 // Swarm mean from nparts partial rows; also the selection from the slots.
+// First-stage blocks per column tile: a power of two near nparts / 32, so
+// that a first-stage lane sums about 8 partial rows (one batch of loads) and
+// the last block about as few stage sums (at most kMeanStages blocks).
 MeanArgs mean_args(evox_state *s, int nparts)
 {
-    return MeanArgs{s->xsum, nparts, s->P.N, s->P.D, s->P.ldx, s->B.xbar, s->s1, s->ticket, s->slots, s->best};
+    int stages = 4;
+    while (stages < kMeanStages && 32 * (int64_t)stages < nparts) stages *= 2;
+    return MeanArgs{s->xsum, nparts, s->P.N, s->P.D, s->P.ldx, s->B.xbar, s->s1, stages, s->ticket, s->slots,
+                    s->best};
 }
 
 // CSO: fit (optional), swarm mean and best of the current positions.
@@ -439,7 +445,8 @@ int evox_state_create(const evox_params *params, const evox_buffers *b, void *hi
     s->k1 = (uint32_t)(P.seed >> 32);
     s->best = at<DevBest>(b->scratch, pl.best);
     s->slots = at<SelSlots>(b->scratch, pl.slots);
-    s->hist = s->offs = s->cursor = s->tkey = s->tidx = s->perm = nullptr;
+    s->hist = s->offs = s->cursor = s->perm = nullptr;
+    s->tkv = nullptr;
     s->xsum = s->s1 = nullptr;
     s->perm_t0 = -1;
     s->ticket = nullptr;
@@ -524,8 +531,7 @@ int evox_state_create(const evox_params *params, const evox_buffers *b, void *hi
         s->hist = at<uint32_t>(b->scratch, pl.hist);
         s->offs = at<uint32_t>(b->scratch, pl.offs);
         s->cursor = at<uint32_t>(b->scratch, pl.cursor);
-        s->tkey = at<uint32_t>(b->scratch, pl.tkey);
-        s->tidx = at<uint32_t>(b->scratch, pl.tidx);
+        s->tkv = at<uint2>(b->scratch, pl.tkv);
         s->perm = at<uint32_t>(b->scratch, pl.perm);
         s->xsum = at<double>(b->scratch, pl.xsum);
         s->s1 = at<double>(b->scratch, pl.s1);
@@ -749,7 +755,7 @@ int evox_cso_step(evox_state *s, int64_t n_gens)
         const int64_t t = s->t + k;
         if (s->perm_t0 < 0 || t < s->perm_t0 || t >= s->perm_t0 + pl.perm_batch) {
             PermArgs pa{P.N, pl.bits, s->k0, s->k1, (uint32_t)t, (uint32_t)pl.perm_batch, s->hist, s->offs,
-                        s->cursor, s->tkey, s->tidx, s->perm, nullptr};
+                        s->cursor, s->tkv, s->perm, nullptr};
             if ((e = launch_perm(pa, s->stream)) != hipSuccess) return hip_fail(e, "pairing");
             s->perm_t0 = t;
         }
@@ -1009,9 +1015,8 @@ int64_t evox_default_ldx(int32_t algo, int64_t D)
 namespace {
 
 // Scratch of the pairing sort for `batch` generations of N individuals:
-// counts, offsets and cursors per superbucket, keys and indices per entry.
-size_t perm_scratch(int64_t N, int64_t batch, size_t *hist, size_t *offs, size_t *cursor, size_t *tkey,
-                    size_t *tidx)
+// counts, offsets and cursors per superbucket, (key, index) per entry.
+size_t perm_scratch(int64_t N, int64_t batch, size_t *hist, size_t *offs, size_t *cursor, size_t *tkv)
 {
     const size_t B = (size_t)batch, nb = (size_t)1 << perm_bits(N);
     size_t off = 0;
@@ -1023,15 +1028,14 @@ size_t perm_scratch(int64_t N, int64_t batch, size_t *hist, size_t *offs, size_t
     *hist = take(4 * nb * B);
     *offs = take(4 * (nb + 1) * B);
     *cursor = take(4 * nb * B);
-    *tkey = take(4 * (size_t)N * B);
-    *tidx = take(4 * (size_t)N * B);
+    *tkv = take(8 * (size_t)N * B);
     return off;
 }
 
 size_t perm_scratch_total(int64_t N, int64_t batch)
 {
-    size_t a, b, c, d, e;
-    return perm_scratch(N, batch, &a, &b, &c, &d, &e);
+    size_t a, b, c, d;
+    return perm_scratch(N, batch, &a, &b, &c, &d);
 }
 
 // n_gens sorts of N keys into perm_out[n_gens][N], as many per launch as the
@@ -1043,8 +1047,8 @@ int sort_batches(uint64_t seed, int64_t t0, int64_t n_gens, int64_t N, const uin
     while (B > 1 && perm_scratch_total(N, B) > scratch_bytes) --B;
     if (perm_scratch_total(N, B) > scratch_bytes)
         return fail(EVOX_ENOSPC, "scratch has %zu bytes, needs %zu", scratch_bytes, perm_scratch_total(N, 1));
-    size_t oh, oo, oc, ok, oi;
-    perm_scratch(N, B, &oh, &oo, &oc, &ok, &oi);
+    size_t oh, oo, oc, ok;
+    perm_scratch(N, B, &oh, &oo, &oc, &ok);
     uint32_t *hist = at<uint32_t>(scratch, oh), *cursor = at<uint32_t>(scratch, oc);
     const int bits = perm_bits(N);
     hipError_t e;
@@ -1054,8 +1058,7 @@ int sort_batches(uint64_t seed, int64_t t0, int64_t n_gens, int64_t N, const uin
     for (int64_t g = 0; g < n_gens; g += B) {
         const int64_t b = n_gens - g < B ? n_gens - g : B;
         PermArgs pa{N, bits, (uint32_t)seed, (uint32_t)(seed >> 32), (uint32_t)(t0 + g), (uint32_t)b, hist,
-                    at<uint32_t>(scratch, oo), cursor, at<uint32_t>(scratch, ok), at<uint32_t>(scratch, oi),
-                    perm_out + g * N, keys};
+                    at<uint32_t>(scratch, oo), cursor, at<uint2>(scratch, ok), perm_out + g * N, keys};
         if ((e = launch_perm(pa, st)) != hipSuccess) return hip_fail(e, "sort");
     }
     return EVOX_OK;

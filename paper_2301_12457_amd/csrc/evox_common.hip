@@ -5,11 +5,12 @@
 // Pairing (CSO).  The permutation is the order of the individuals by
 // (key, index), key_i = Philox stream-4 word of individual i at generation t.
 // Keys are uniform 32-bit numbers, so a superbucket sort does it in three
-// light passes over 4096-individual chunks:
+// light passes over 4096-individual chunks (kPermChunk):
 //   k_perm_count  per-superbucket counts (top `bits` key bits; LDS
 //                 histogram, one global atomic per nonempty bucket)
 //   k_perm_place  scan of the counts, per-block range reservation, and
-//                 placement of (key, index) into the superbucket ranges
+//                 placement of (key, index) into the superbucket ranges, as
+//                 one 8-byte entry so a block's run of a bucket is contiguous
 //   k_perm_sort   one block per superbucket (~1000 entries): counting sort on
 //                 the next 8 key bits in LDS, then ranks inside sub-buckets,
 //                 written as the permutation
@@ -290,14 +291,16 @@ __device__ __forceinline__ uint32_t bucket_of(uint32_t key, int bits)
 // array (counts nb, offsets nb + 1, keys / indices / permutation N).
 struct PermSlice {
     uint32_t t;
-    uint32_t *hist, *offs, *cursor, *tkey, *tidx, *perm;
+    uint32_t *hist, *offs, *cursor;
+    uint2 *tkv;
+    uint32_t *perm;
 };
 
 __device__ __forceinline__ PermSlice perm_slice(const PermArgs &a)
 {
     const int64_t b = blockIdx.y, nb = (int64_t)1 << a.bits;
     return PermSlice{a.t0 + (uint32_t)b, a.hist + b * nb, a.offs + b * (nb + 1), a.cursor + b * nb,
-                     a.tkey + b * a.N, a.tidx + b * a.N, a.perm + b * a.N};
+                     a.tkv + b * a.N, a.perm + b * a.N};
 }
 
 // Keys of the individuals 4 * (blockIdx.x * kPermChunk / 4 + r * 256 + tid)
@@ -392,8 +395,7 @@ __global__ __launch_bounds__(256) void k_perm_place(PermArgs a)
     __syncthreads();
     for_block_keys(a, sl.t, [&](uint32_t key, int64_t i) {
         const uint32_t pos = atomicAdd(&off[bucket_of(key, a.bits)], 1u);
-        sl.tkey[pos] = key;
-        sl.tidx[pos] = (uint32_t)i;
+        sl.tkv[pos] = make_uint2(key, (uint32_t)i);
     });
 }
 
@@ -415,7 +417,7 @@ __global__ __launch_bounds__(256) void k_perm_sort(PermArgs a)
         cnt[threadIdx.x] = 0;
         __syncthreads();
         for (uint32_t q = threadIdx.x; q < n; q += 256)
-            atomicAdd(&cnt[(sl.tkey[lo + q] >> shift) & 255u], 1u);
+            atomicAdd(&cnt[(sl.tkv[lo + q].x >> shift) & 255u], 1u);
         __syncthreads();
         if (threadIdx.x < 64) {  // exclusive scan of 256 counts by one wave, 4 per lane
             const int l = threadIdx.x;
@@ -435,10 +437,10 @@ __global__ __launch_bounds__(256) void k_perm_sort(PermArgs a)
         cur[threadIdx.x] = start[threadIdx.x];
         __syncthreads();
         for (uint32_t q = threadIdx.x; q < n; q += 256) {
-            const uint32_t key = sl.tkey[lo + q];
-            const uint32_t pos = atomicAdd(&cur[(key >> shift) & 255u], 1u);
-            K[pos] = key;
-            I[pos] = sl.tidx[lo + q];
+            const uint2 e = sl.tkv[lo + q];
+            const uint32_t pos = atomicAdd(&cur[(e.x >> shift) & 255u], 1u);
+            K[pos] = e.x;
+            I[pos] = e.y;
         }
         __syncthreads();
         for (uint32_t q = threadIdx.x; q < n; q += 256) {
@@ -452,10 +454,10 @@ __global__ __launch_bounds__(256) void k_perm_sort(PermArgs a)
         for (uint32_t q = threadIdx.x; q < n; q += 256) sl.perm[lo + q] = S[q];
     } else {
         for (uint32_t p = threadIdx.x; p < n; p += 256) {
-            const uint32_t key = sl.tkey[lo + p], idx = sl.tidx[lo + p];
+            const uint32_t key = sl.tkv[lo + p].x, idx = sl.tkv[lo + p].y;
             uint32_t rank = 0;
             for (uint32_t q = 0; q < n; ++q) {
-                const uint32_t kq = sl.tkey[lo + q], iq = sl.tidx[lo + q];
+                const uint32_t kq = sl.tkv[lo + q].x, iq = sl.tkv[lo + q].y;
                 rank += (kq < key || (kq == key && iq < idx)) ? 1u : 0u;
             }
             sl.perm[lo + rank] = idx;
@@ -481,7 +483,7 @@ hipError_t launch_perm(const PermArgs &a, hipStream_t s)
 // Block (0, 0) also finishes the selection (slots -> best) when asked.
 // xbar = (sum of the per-block partial rows) / N, rounded once, in two
 // stages.  Block (tile, rg) of 64 columns x 4 lanes: lane l sums partial rows
-// rg + S (l + 4 u), u = 0, 1, ... (S = kMeanStages) in that order, the four
+// rg + S (l + 4 u), u = 0, 1, ... (S = m.stages) in that order, the four
 // lanes are added in lane order into s1[rg].  The last block of a tile to
 // finish sums s1[0..S) the same way (lane l: stages l + 4 u) and writes the
 // mean.  Padding columns get 0.  Loads go out in batches of 8.
@@ -511,13 +513,20 @@ __global__ __launch_bounds__(256) void k_cso_mean(MeanArgs m)
         // second pass of the selection over the generation kernel's slots
         __shared__ uint64_t sk[4];
         __shared__ uint32_t sc[4];
+        // all of a thread's slot loads issued before any of the resets, so
+        // the pass costs one memory latency instead of one per slot row
+        constexpr int R = kSlots / 256;
+        static_assert(kSlots % 256 == 0, "whole slot rows per thread");
+        uint64_t kq[R];
+#pragma unroll
+        for (int u = 0; u < R; ++u) kq[u] = m.slots->key[threadIdx.x + 256 * u];
         uint64_t k = kNoKey;
         uint32_t none = 0;
-        for (int q = threadIdx.x; q < kSlots; q += 256) {
-            const uint64_t kq = m.slots->key[q];
-            k = kq < k ? kq : k;
-            m.slots->key[q] = kNoKey;
-            m.slots->cnt[q] = 0;
+#pragma unroll
+        for (int u = 0; u < R; ++u) {
+            k = kq[u] < k ? kq[u] : k;
+            m.slots->key[threadIdx.x + 256 * u] = kNoKey;
+            m.slots->cnt[threadIdx.x + 256 * u] = 0;
         }
         block_min_key(k, none, sk, sc);
         if (threadIdx.x == 0) {
@@ -529,7 +538,7 @@ __global__ __launch_bounds__(256) void k_cso_mean(MeanArgs m)
     const int64_t tile = blockIdx.x, rg = blockIdx.y;
     const int64_t j = tile * 64 + col;
     double s = 0.0;
-    if (j < m.D) s = strided_sum(m.xsum + j, rg + (int64_t)kMeanStages * lane, 4 * kMeanStages, m.nparts, m.ldx);
+    if (j < m.D) s = strided_sum(m.xsum + j, rg + (int64_t)m.stages * lane, 4 * (int64_t)m.stages, m.nparts, m.ldx);
     part[lane][col] = s;
     __syncthreads();
     if (lane == 0) {  // wave 0 writes this block's stage sums and releases them
@@ -537,12 +546,12 @@ __global__ __launch_bounds__(256) void k_cso_mean(MeanArgs m)
         __threadfence();
     }
     __syncthreads();
-    if (threadIdx.x == 0) last = atomicAdd(&m.ticket[tile], 1u) == (uint32_t)(kMeanStages - 1);
+    if (threadIdx.x == 0) last = atomicAdd(&m.ticket[tile], 1u) == (uint32_t)(m.stages - 1);
     __syncthreads();
     if (last) {
         __threadfence();
         double t = 0.0;
-        if (j < m.D) t = strided_sum(m.s1 + j, lane, 4, kMeanStages, m.ldx);
+        if (j < m.D) t = strided_sum(m.s1 + j, lane, 4, m.stages, m.ldx);
         part[lane][col] = t;
         __syncthreads();
         if (lane == 0 && j < m.ldx) {
@@ -556,7 +565,8 @@ __global__ __launch_bounds__(256) void k_cso_mean(MeanArgs m)
 hipError_t launch_cso_mean(const MeanArgs &m, hipStream_t s)
 {
     const unsigned tiles = (unsigned)((m.ldx + 63) / 64);
-    hipLaunchKernelGGL(k_cso_mean, dim3(tiles, kMeanStages), dim3(256), 0, s, m);
+    if (m.stages < 1 || m.stages > kMeanStages) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(k_cso_mean, dim3(tiles, (unsigned)m.stages), dim3(256), 0, s, m);
     return hipGetLastError();
 }
 

@@ -261,7 +261,9 @@ struct PermArgs {
     uint32_t k0, k1;
     uint32_t t0;        // first generation of the batch
     uint32_t batch;     // generations in the batch
-    uint32_t *hist, *offs, *cursor, *tkey, *tidx, *perm;  // [batch][...] slices
+    uint32_t *hist, *offs, *cursor;  // [batch][...] slices
+    uint2 *tkv;                      // [batch][N] (key, index) placed by superbucket
+    uint32_t *perm;                  // [batch][N]
     const uint32_t *keys;  // caller keys (batch 1), or null: Philox stream-4 keys
 };
 hipError_t launch_perm(const PermArgs &a, hipStream_t s);
@@ -276,12 +278,13 @@ hipError_t launch_colsum(Layout L, const float *x, int64_t N, int64_t D, int64_t
                          int grid, hipStream_t s);
 
 // Swarm mean from per-block fp64 column sums.
-constexpr int kMeanStages = 128;
+constexpr int kMeanStages = 128;  // first-stage blocks per column tile at most
 struct MeanArgs {
     const double *xsum;  // [nparts][ldx]
     int64_t nparts, N, D, ldx;
     float *xbar;         // [ldx]
     double *s1;          // [kMeanStages][ldx] stage sums
+    int32_t stages;      // first-stage blocks per column tile, 1..kMeanStages
     uint32_t *ticket;    // [ceil(ldx / 64)], zero between launches
     SelSlots *slots;     // nullable: also reduce these selection slots into best
     DevBest *best;
