@@ -138,8 +138,11 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs g)
 // workspace (one split) the block applies alpha and beta itself.
 // ---------------------------------------------------------------------------
 constexpr int kNtBK = 32, kNtLD = kNtBK + 4;
+// register stages of the operand prefetch for the thin tiles (M <= 128,
+// 64 output columns per block); the 128 x 128 tiles keep one stage
+constexpr int kNtThinDepth = 2;
 
-template <int BM, int BN>
+template <int BM, int BN, int DEPTH>
 __global__ __launch_bounds__(256) void k_gemm_nt(GemmArgs g, float *work, int64_t kc)
 {
     constexpr int TM = BM / 64, TN = BN / 64;            // 32x32 tiles per wave
@@ -150,29 +153,31 @@ __global__ __launch_bounds__(256) void k_gemm_nt(GemmArgs g, float *work, int64_
     const int wm = wave / 2, wn = wave % 2;
     const int64_t i0 = (int64_t)blockIdx.y * BM, j0 = (int64_t)blockIdx.x * BN;
     const int64_t kb = (int64_t)blockIdx.z * kc, ke = kb + kc < g.K ? kb + kc : g.K;
-    float4 ra[QA], rb[QB];
-    auto load = [&](int64_t k0) {
+    // DEPTH register stages of the next K tiles' operands (compile-time
+    // stage indices, so they stay in registers)
+    float4 ra[DEPTH][QA], rb[DEPTH][QB];
+    auto load = [&](int d, int64_t k0) {
 #pragma unroll
         for (int q = 0; q < QA; ++q) {
             const int idx = tid + 256 * q, row = idx / 8, c4 = idx % 8;
-            ra[q] = quad_or_zero(g.A, g.lda, i0 + row, k0 + 4 * c4, g.M, ke);
+            ra[d][q] = quad_or_zero(g.A, g.lda, i0 + row, k0 + 4 * c4, g.M, ke);
         }
 #pragma unroll
         for (int q = 0; q < QB; ++q) {
             const int idx = tid + 256 * q, row = idx / 8, c4 = idx % 8;
-            rb[q] = quad_or_zero(g.B, g.ldb, j0 + row, k0 + 4 * c4, g.N, ke);
+            rb[d][q] = quad_or_zero(g.B, g.ldb, j0 + row, k0 + 4 * c4, g.N, ke);
         }
     };
-    auto store = [&]() {
+    auto store = [&](int d) {
 #pragma unroll
         for (int q = 0; q < QA; ++q) {
             const int idx = tid + 256 * q, row = idx / 8, c4 = idx % 8;
-            *reinterpret_cast<float4 *>(&As[row * kNtLD + 4 * c4]) = ra[q];
+            *reinterpret_cast<float4 *>(&As[row * kNtLD + 4 * c4]) = ra[d][q];
         }
 #pragma unroll
         for (int q = 0; q < QB; ++q) {
             const int idx = tid + 256 * q, row = idx / 8, c4 = idx % 8;
-            *reinterpret_cast<float4 *>(&Bs[row * kNtLD + 4 * c4]) = rb[q];
+            *reinterpret_cast<float4 *>(&Bs[row * kNtLD + 4 * c4]) = rb[d][q];
         }
     };
     f32x16 acc[TM][TN];
@@ -183,35 +188,47 @@ __global__ __launch_bounds__(256) void k_gemm_nt(GemmArgs g, float *work, int64_
 #pragma unroll
             for (int v = 0; v < 16; ++v) acc[m][n][v] = 0.0f;
 
-    if (kb < ke) {
-        load(kb);
-        store();
-        __syncthreads();
-        for (int64_t k0 = kb; k0 < ke; k0 += kNtBK) {
-            const bool more = k0 + kNtBK < ke;
-            if (more) load(k0 + kNtBK);
+    auto compute = [&]() {
 #pragma unroll
-            for (int c = 0; c < 4; ++c) {
-                float4 a4[TM], b4[TN];
+        for (int c = 0; c < 4; ++c) {
+            float4 a4[TM], b4[TN];
+#pragma unroll
+            for (int m = 0; m < TM; ++m)
+                a4[m] = *reinterpret_cast<const float4 *>(&As[(wm * TM * 32 + m * 32 + col) * kNtLD + h * 16 + 4 * c]);
+#pragma unroll
+            for (int n = 0; n < TN; ++n)
+                b4[n] = *reinterpret_cast<const float4 *>(&Bs[(wn * TN * 32 + n * 32 + col) * kNtLD + h * 16 + 4 * c]);
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
 #pragma unroll
                 for (int m = 0; m < TM; ++m)
-                    a4[m] = *reinterpret_cast<const float4 *>(&As[(wm * TM * 32 + m * 32 + col) * kNtLD + h * 16 + 4 * c]);
 #pragma unroll
-                for (int n = 0; n < TN; ++n)
-                    b4[n] = *reinterpret_cast<const float4 *>(&Bs[(wn * TN * 32 + n * 32 + col) * kNtLD + h * 16 + 4 * c]);
+                    for (int n = 0; n < TN; ++n)
+                        acc[m][n] = __builtin_amdgcn_mfma_f32_32x32x2f32(comp(a4[m], e), comp(b4[n], e),
+                                                                         acc[m][n], 0, 0, 0);
+        }
+    };
+    if (kb < ke) {
+        // tile kb in LDS, tiles kb + d kNtBK (d < DEPTH) in register stage d
+        load(0, kb);
+        store(0);
+        __syncthreads();
 #pragma unroll
-                for (int e = 0; e < 4; ++e)
+        for (int d = 1; d < DEPTH; ++d)
+            if (kb + d * kNtBK < ke) load(d, kb + d * kNtBK);
+        for (int64_t k0 = kb; k0 < ke; k0 += DEPTH * kNtBK) {
 #pragma unroll
-                    for (int m = 0; m < TM; ++m)
-#pragma unroll
-                        for (int n = 0; n < TN; ++n)
-                            acc[m][n] = __builtin_amdgcn_mfma_f32_32x32x2f32(comp(a4[m], e), comp(b4[n], e),
-                                                                             acc[m][n], 0, 0, 0);
-            }
-            __syncthreads();
-            if (more) {
-                store();
+            for (int d = 0; d < DEPTH; ++d) {
+                const int64_t kt = k0 + d * kNtBK;  // the tile in LDS (uniform)
+                if (kt >= ke) break;
+                // stage d held tile kt (now in LDS): refill it DEPTH tiles ahead
+                if (kt + DEPTH * kNtBK < ke) load(d, kt + DEPTH * kNtBK);
+                compute();
                 __syncthreads();
+                if (kt + kNtBK < ke) {
+                    store((d + 1) % DEPTH);
+                    __syncthreads();
+                }
             }
         }
     }
@@ -251,7 +268,8 @@ __global__ __launch_bounds__(256) void k_splitk_reduce(GemmArgs g, const float *
 int occupancy_gemm_nt_thin()
 {
     int n = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k_gemm_nt<128, 64>, 256, 0) != hipSuccess) return 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k_gemm_nt<128, 64, kNtThinDepth>, 256, 0) != hipSuccess)
+        return 0;
     return n;
 }
 
@@ -269,9 +287,9 @@ hipError_t launch_gemm_nt(const GemmArgs &g, int splits, float *work, hipStream_
     const int bm = g.M <= 64 ? 64 : 128, bn = g.M <= 128 ? 64 : 128;
     const dim3 grid((unsigned)((g.N + bn - 1) / bn), (unsigned)((g.M + bm - 1) / bm), (unsigned)splits);
     float *w = splits > 1 ? work : nullptr;
-    if (bm == 64) hipLaunchKernelGGL((k_gemm_nt<64, 64>), grid, dim3(256), 0, s, g, w, kc);
-    else if (bn == 64) hipLaunchKernelGGL((k_gemm_nt<128, 64>), grid, dim3(256), 0, s, g, w, kc);
-    else hipLaunchKernelGGL((k_gemm_nt<128, 128>), grid, dim3(256), 0, s, g, w, kc);
+    if (bm == 64) hipLaunchKernelGGL((k_gemm_nt<64, 64, kNtThinDepth>), grid, dim3(256), 0, s, g, w, kc);
+    else if (bn == 64) hipLaunchKernelGGL((k_gemm_nt<128, 64, kNtThinDepth>), grid, dim3(256), 0, s, g, w, kc);
+    else hipLaunchKernelGGL((k_gemm_nt<128, 128, 1>), grid, dim3(256), 0, s, g, w, kc);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || splits == 1) return e;
     const int64_t n = g.M * g.N, blocks = (n + 255) / 256;
