@@ -132,7 +132,7 @@ NsgaSortArgs nsga_sort_args(void *scratch, const NsgaSortScratch &l, const float
 // blocks -- with every slice at least 256 deep.
 int mae_splits(int64_t N, int64_t D, int64_t resident)
 {
-    const int64_t rows = N + 1, bm = rows <= 64 ? 64 : 128, bn = rows <= 128 ? 64 : 128;
+    const int64_t rows = N + 1, bm = rows <= 64 ? 64 : rows <= 112 ? 112 : 128, bn = rows <= 128 ? 64 : 128;
     const int64_t tiles = ((D + bn - 1) / bn) * ((rows + bm - 1) / bm);
     int64_t sp = resident > 0 ? resident / tiles : (1024 + tiles - 1) / tiles;
     const int64_t deep = D / 256 > 1 ? D / 256 : 1;
@@ -143,13 +143,13 @@ int mae_splits(int64_t N, int64_t D, int64_t resident)
 
 // Blocks of the sampling product's thin tile shape resident on the device at
 // once (0 if unknown).
-int64_t resident_thin_blocks()
+int64_t resident_thin_blocks(int64_t M)
 {
     int dev = 0, cus = 0;
     if (hipGetDevice(&dev) != hipSuccess ||
         hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
         return 0;
-    return (int64_t)cus * occupancy_gemm_nt_thin();
+    return (int64_t)cus * occupancy_gemm_nt_thin(M);
 }
 
 int make_plan(const evox_params *P, Plan *pl)
@@ -235,7 +235,7 @@ int make_plan(const evox_params *P, Plan *pl)
         const int64_t steps = (p.mae_mu + 2) / 2;
         p.mae_kp = steps <= kMaeRankUnrolled ? 2 * steps : (p.mae_mu + 1 + 31) / 32 * 32;
         p.mae_ldf = (P->D + 63) / 64 * 64;
-        p.mae_splits = mae_splits(P->N, P->D, resident_thin_blocks());
+        p.mae_splits = mae_splits(P->N, P->D, resident_thin_blocks(P->N + 1));
         p.mae_z = take(sizeof(float) * rows * (size_t)P->ldx);
         p.mae_d = take(sizeof(float) * rows * (size_t)P->ldx);
         p.mae_work = p.mae_splits > 1 ? take(sizeof(float) * (size_t)p.mae_splits * rows * D) : 0;

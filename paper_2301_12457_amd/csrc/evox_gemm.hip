@@ -18,6 +18,7 @@ namespace evox {
 namespace {
 
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kBM = 128, kBN = 128, kBK = 16, kPad = 4;
 
@@ -251,6 +252,107 @@ __global__ __launch_bounds__(256) void k_gemm_nt(GemmArgs g, float *work, int64_
             }
 }
 
+// A B^T for at most 16 RB rows of A (the thin sampling products): 16 x 16
+// MFMA tiles (v_mfma_f32_16x16x4f32), so 101 rows pad to 112 instead of
+// 128.  Block: all 16 RB rows x 64 columns, K tile kNtBK; wave w owns the
+// 16-column block w and the RB row blocks.  Within a K tile, lane group
+// q = lane / 16 takes the 8 consecutive k 8q .. 8q + 7, one per MFMA step
+// (any split of k over the four k slots of the instruction is a valid
+// product, since A and B use the same one), so each lane reads its
+// operands as two float4 per row block.  Operand prefetch as in k_gemm_nt.
+template <int RB, int DEPTH>
+__global__ __launch_bounds__(256) void k_gemm_nt16(GemmArgs g, float *work, int64_t kc)
+{
+    constexpr int BM = 16 * RB, BN = 64;
+    constexpr int FA = BM * kNtBK / 4, FB = BN * kNtBK / 4;  // float4 per tile
+    constexpr int QA = (FA + 255) / 256, QB = FB / 256;      // float4 per thread
+    __shared__ float As[BM * kNtLD];
+    __shared__ float Bs[BN * kNtLD];
+    const int tid = threadIdx.x, wave = tid / 64, lane = tid % 64, r16 = lane % 16, q = lane / 16;
+    const int64_t i0 = (int64_t)blockIdx.y * BM, j0 = (int64_t)blockIdx.x * BN;
+    const int64_t kb = (int64_t)blockIdx.z * kc, ke = kb + kc < g.K ? kb + kc : g.K;
+    float4 ra[DEPTH][QA], rb[DEPTH][QB];
+    auto load = [&](int d, int64_t k0) {
+#pragma unroll
+        for (int u = 0; u < QA; ++u) {
+            const int idx = tid + 256 * u, row = idx / 8, c4 = idx % 8;
+            if (idx < FA) ra[d][u] = quad_or_zero(g.A, g.lda, i0 + row, k0 + 4 * c4, g.M, ke);
+        }
+#pragma unroll
+        for (int u = 0; u < QB; ++u) {
+            const int idx = tid + 256 * u, row = idx / 8, c4 = idx % 8;
+            rb[d][u] = quad_or_zero(g.B, g.ldb, j0 + row, k0 + 4 * c4, g.N, ke);
+        }
+    };
+    auto store = [&](int d) {
+#pragma unroll
+        for (int u = 0; u < QA; ++u) {
+            const int idx = tid + 256 * u, row = idx / 8, c4 = idx % 8;
+            if (idx < FA) *reinterpret_cast<float4 *>(&As[row * kNtLD + 4 * c4]) = ra[d][u];
+        }
+#pragma unroll
+        for (int u = 0; u < QB; ++u) {
+            const int idx = tid + 256 * u, row = idx / 8, c4 = idx % 8;
+            *reinterpret_cast<float4 *>(&Bs[row * kNtLD + 4 * c4]) = rb[d][u];
+        }
+    };
+    f32x4 acc[RB];
+#pragma unroll
+    for (int m = 0; m < RB; ++m)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) acc[m][v] = 0.0f;
+    auto compute = [&]() {
+#pragma unroll
+        for (int hf = 0; hf < 2; ++hf) {  // k 8q + 4hf .. 8q + 4hf + 3
+            const float4 b4 = *reinterpret_cast<const float4 *>(&Bs[(wave * 16 + r16) * kNtLD + 8 * q + 4 * hf]);
+#pragma unroll
+            for (int m = 0; m < RB; ++m) {
+                const float4 a4 = *reinterpret_cast<const float4 *>(&As[(m * 16 + r16) * kNtLD + 8 * q + 4 * hf]);
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    acc[m] = __builtin_amdgcn_mfma_f32_16x16x4f32(comp(a4, e), comp(b4, e), acc[m], 0, 0, 0);
+            }
+        }
+    };
+    if (kb < ke) {
+        load(0, kb);
+        store(0);
+        __syncthreads();
+#pragma unroll
+        for (int d = 1; d < DEPTH; ++d)
+            if (kb + d * kNtBK < ke) load(d, kb + d * kNtBK);
+        for (int64_t k0 = kb; k0 < ke; k0 += DEPTH * kNtBK) {
+#pragma unroll
+            for (int d = 0; d < DEPTH; ++d) {
+                const int64_t kt = k0 + d * kNtBK;
+                if (kt >= ke) break;
+                if (kt + DEPTH * kNtBK < ke) load(d, kt + DEPTH * kNtBK);
+                compute();
+                __syncthreads();
+                if (kt + kNtBK < ke) {
+                    store((d + 1) % DEPTH);
+                    __syncthreads();
+                }
+            }
+        }
+    }
+    // result v of row block m: row 16 m + 4 q + v, column 16 wave + r16
+#pragma unroll
+    for (int m = 0; m < RB; ++m)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+            const int64_t i = i0 + m * 16 + 4 * q + v, j = j0 + wave * 16 + r16;
+            if (i < g.M && j < g.N) {
+                if (work) {
+                    work[((int64_t)blockIdx.z * g.M + i) * g.N + j] = acc[m][v];
+                } else {
+                    float *c = g.C + i * g.ldc + j;
+                    *c = g.beta != 0.0f ? fmaf(g.alpha, acc[m][v], g.beta * *c) : g.alpha * acc[m][v];
+                }
+            }
+        }
+}
+
 __global__ __launch_bounds__(256) void k_splitk_reduce(GemmArgs g, const float *work, int splits)
 {
     const int64_t n = g.M * g.N;
@@ -265,12 +367,13 @@ __global__ __launch_bounds__(256) void k_splitk_reduce(GemmArgs g, const float *
 
 }  // namespace
 
-int occupancy_gemm_nt_thin()
+int occupancy_gemm_nt_thin(int64_t M)
 {
     int n = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k_gemm_nt<128, 64, kNtThinDepth>, 256, 0) != hipSuccess)
-        return 0;
-    return n;
+    const hipError_t e = M > 64 && M <= 112
+                             ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k_gemm_nt16<7, kNtThinDepth>, 256, 0)
+                             : hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k_gemm_nt<128, 64, kNtThinDepth>, 256, 0);
+    return e == hipSuccess ? n : 0;
 }
 
 int64_t gemm_nt_chunk(int64_t K, int splits)
@@ -284,10 +387,13 @@ hipError_t launch_gemm_nt(const GemmArgs &g, int splits, float *work, hipStream_
     if (g.M <= 0 || g.N <= 0) return hipSuccess;
     if (splits < 1 || (splits > 1 && !work)) return hipErrorInvalidValue;
     const int64_t kc = splits > 1 ? gemm_nt_chunk(g.K, splits) : (g.K > 0 ? g.K : 1);
-    const int bm = g.M <= 64 ? 64 : 128, bn = g.M <= 128 ? 64 : 128;
+    // 65..112 rows: 16 x 16 tiles (7 row blocks) instead of 128 padded rows
+    const bool rows112 = g.M > 64 && g.M <= 112;
+    const int bm = g.M <= 64 ? 64 : rows112 ? 112 : 128, bn = g.M <= 128 ? 64 : 128;
     const dim3 grid((unsigned)((g.N + bn - 1) / bn), (unsigned)((g.M + bm - 1) / bm), (unsigned)splits);
     float *w = splits > 1 ? work : nullptr;
-    if (bm == 64) hipLaunchKernelGGL((k_gemm_nt<64, 64, kNtThinDepth>), grid, dim3(256), 0, s, g, w, kc);
+    if (rows112) hipLaunchKernelGGL((k_gemm_nt16<7, kNtThinDepth>), grid, dim3(256), 0, s, g, w, kc);
+    else if (bm == 64) hipLaunchKernelGGL((k_gemm_nt<64, 64, kNtThinDepth>), grid, dim3(256), 0, s, g, w, kc);
     else if (bn == 64) hipLaunchKernelGGL((k_gemm_nt<128, 64, kNtThinDepth>), grid, dim3(256), 0, s, g, w, kc);
     else hipLaunchKernelGGL((k_gemm_nt<128, 128, 1>), grid, dim3(256), 0, s, g, w, kc);
     hipError_t e = hipGetLastError();

@@ -101,7 +101,7 @@ hipError_t launch_mae_select(const MaeArgs &a, hipStream_t s);
 hipError_t launch_mae_recombine(const MaeArgs &a, hipStream_t s);  // and the step size
 hipError_t launch_mae_rank(const MaeArgs &a, float *M, float beta, hipStream_t s);  // M <- beta M + At^T Bt
 hipError_t launch_mae_identity(float *M, int64_t D, int64_t ldx, hipStream_t s);
-int occupancy_gemm_nt_thin();  // resident blocks per CU of the sampling product's tile shape
+int occupancy_gemm_nt_thin(int64_t M);  // resident blocks per CU of the tile shape for M rows (M <= 128)
 
 // NSGA-II on DTLZ1.
 constexpr int kNsgaMaxM = 8;          // objectives

@@ -31,8 +31,11 @@ def limit(A, B, ta, tb, alpha, beta, C0, want):
         np.spacing(np.abs(want))
 
 
+# (65..112 rows take the 16 x 16-tile kernel: a full 112-row block, a ragged
+# one with ragged columns and K, and the 101 rows of the MA-ES sampling
+# product)
 SHAPES = [(1, 1, 1), (5, 7, 3), (128, 128, 16), (129, 130, 17), (300, 77, 1000), (64, 512, 2048),
-          (1000, 1000, 1000), (33, 100, 0)]
+          (1000, 1000, 1000), (33, 100, 0), (112, 64, 64), (65, 33, 129), (101, 300, 777)]
 
 
 @pytest.mark.parametrize("ta", [False, True])
