@@ -98,9 +98,11 @@ def maes_flops(w):
 def cso_bytes_per_launch(w):
     # per pair: read winner row, loser x and v, write loser x and v
     # (20 B per pair element = 10 B per individual element); fitness of both
-    # and the permutation entries (4 B each), write loser fitness; the
-    # neighbourhood version also reads the loser's mean row (4 B per pair
-    # element)
+    # and the permutation entries (4 B each), write loser fitness.  The
+    # neighbourhood version writes the next positions to the other buffer:
+    # it also writes the winner's row (4 B per pair element); every old row
+    # is counted once, so the loser's neighbours (rows of other pairs) add
+    # nothing
     pairs = w.N // 2
     return (24.0 if w.cso_local else 20.0) * pairs * w.D + pairs * (4 * 2 + 4 * 2 + 4)
 

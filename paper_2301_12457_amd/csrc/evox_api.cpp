@@ -78,7 +78,7 @@ struct Plan {
     int64_t xsum_rows = 0;
     int perm_batch = 0;
     size_t x2 = 0, fit2 = 0;  // DE: the other population buffer and its fitness
-    size_t xloc = 0;          // CSO neighbourhood version: the losers' mean rows
+    size_t xalt = 0;          // CSO neighbourhood version: the other population buffer
     size_t esrank = 0, espart = 0;  // ES: sample ranks, gradient partial sums
     // MA-ES: deviates, steps, split-K workspace, update factors, parents,
     // weights, path-norm partial sums
@@ -215,7 +215,7 @@ int make_plan(const evox_params *P, Plan *pl)
         p.xsum = take(sizeof(double) * (size_t)cap * (size_t)P->ldx);
         p.s1 = take(sizeof(double) * (size_t)kMeanStages * (size_t)P->ldx);
         p.ticket = take(sizeof(uint32_t) * (size_t)((P->ldx + 63) / 64));
-        if (P->cso_local) p.xloc = take(sizeof(float) * (size_t)P->N * (size_t)P->ldx);
+        if (P->cso_local) p.xalt = take(sizeof(float) * (size_t)P->N * (size_t)P->ldx);
     }
     if (P->algo == EVOX_DE) {
         p.x2 = take(sizeof(float) * (size_t)P->N * (size_t)P->ldx);
@@ -545,7 +545,7 @@ int evox_state_create(const evox_params *params, const evox_buffers *b, void *hi
         int dev = 0, cus = 0;
         if (hipGetDevice(&dev) == hipSuccess &&
             hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess) {
-            const int occ = occupancy_cso(P.fn_id, pl.L);
+            const int occ = occupancy_cso(P.fn_id, pl.L, P.cso_local != 0);
             const int64_t resident = (int64_t)cus * (occ > 0 ? occ : 1);
             if (resident < s->pl.cso_grid) s->pl.cso_grid = (int)resident;
         }
@@ -624,7 +624,11 @@ int evox_state_create(const evox_params *params, const evox_buffers *b, void *hi
         }
     } else {
         const size_t nb = ((size_t)1 << pl.bits) * (size_t)pl.perm_batch;
-        if ((e = launch_zero_u32(s->hist, (int64_t)nb, s->stream)) != hipSuccess ||
+        // the neighbourhood version's other population buffer starts zero,
+        // so the padding columns the kernels never write stay zero in both
+        if ((P.cso_local && (e = launch_fill(at<float>(b->scratch, pl.xalt), P.N * P.ldx, 0.0f, s->stream)) !=
+                                hipSuccess) ||
+            (e = launch_zero_u32(s->hist, (int64_t)nb, s->stream)) != hipSuccess ||
             (e = launch_zero_u32(s->cursor, (int64_t)nb, s->stream)) != hipSuccess ||
             (e = launch_zero_u32(s->ticket, (P.ldx + 63) / 64, s->stream)) != hipSuccess ||
             (e = best_init(s, std::numeric_limits<float>::infinity(), 0)) != hipSuccess) {
@@ -751,6 +755,7 @@ int evox_cso_step(evox_state *s, int64_t n_gens)
     const evox_params &P = s->P;
     const Plan &pl = s->pl;
     hipError_t e;
+    float *cur = s->B.x, *alt = P.cso_local ? at<float>(s->B.scratch, pl.xalt) : nullptr;
     for (int64_t k = 0; k < n_gens; ++k) {
         const int64_t t = s->t + k;
         if (s->perm_t0 < 0 || t < s->perm_t0 || t >= s->perm_t0 + pl.perm_batch) {
@@ -760,18 +765,21 @@ int evox_cso_step(evox_state *s, int64_t n_gens)
             s->perm_t0 = t;
         }
         const uint32_t *perm = s->perm + (t - s->perm_t0) * P.N;
-        // the neighbourhood version's mean rows, from the positions before the
-        // generation moves anyone (the generation kernel updates in place)
-        float *xloc = P.cso_local ? at<float>(s->B.scratch, pl.xloc) : nullptr;
-        if (xloc && (e = launch_ring_mean(s->B.x, P.N, P.ldx, xloc, s->stream)) != hipSuccess)
-            return hip_fail(e, "neighbourhood means");
-        CsoArgs ca{s->B.x, s->B.v, s->B.fit, xloc ? xloc : s->B.xbar, perm, P.N, P.D, P.ldx, P.phi, P.lb, P.ub,
-                   P.clamp_x != 0, s->k0, s->k1, (uint32_t)t, s->slots, s->xsum, xloc ? P.ldx : 0};
+        // the neighbourhood version reads the positions before the generation
+        // from one population buffer and writes the next into the other, so
+        // every loser's neighbours are still the old rows
+        float *src = cur, *dst = P.cso_local ? (cur == s->B.x ? alt : s->B.x) : s->B.x;
+        CsoArgs ca{dst, s->B.v, s->B.fit, s->B.xbar, perm, P.N, P.D, P.ldx, P.phi, P.lb, P.ub,
+                   P.clamp_x != 0, s->k0, s->k1, (uint32_t)t, s->slots, s->xsum, src};
         e = timed(s, [&] { return launch_cso(P.fn_id, pl.L, ca, pl.cso_grid, s->stream); });
         if (e != hipSuccess) return hip_fail(e, "cso generation");
         if ((e = launch_cso_mean(mean_args(s, pl.cso_grid), s->stream)) != hipSuccess)
             return hip_fail(e, "swarm mean");
+        cur = dst;
     }
+    // the caller's x holds the positions after the call
+    if (cur != s->B.x && (e = launch_stream_copy(cur, s->B.x, P.N * P.ldx, s->stream)) != hipSuccess)
+        return hip_fail(e, "positions");
     s->t += n_gens;
     return EVOX_OK;
 }

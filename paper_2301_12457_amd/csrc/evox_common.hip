@@ -247,31 +247,6 @@ __global__ __launch_bounds__(256) void k_stream_copy(const float *src, float *ds
     if (blockIdx.x == 0 && threadIdx.x < (n & 3)) dst[4 * n4 + threadIdx.x] = src[4 * n4 + threadIdx.x];
 }
 
-__global__ __launch_bounds__(256) void k_ring_mean(const float *x, int64_t N, int64_t ldx, float *out)
-{
-    const int64_t c4 = ldx / 4, total = N * c4;
-    for (int64_t q = (int64_t)blockIdx.x * 256 + threadIdx.x; q < total; q += (int64_t)gridDim.x * 256) {
-        const int64_t i = q / c4, c = q % c4, a = i == 0 ? N - 1 : i - 1, b = i == N - 1 ? 0 : i + 1;
-        const float4 xa = *reinterpret_cast<const float4 *>(x + a * ldx + 4 * c);
-        const float4 xi = *reinterpret_cast<const float4 *>(x + i * ldx + 4 * c);
-        const float4 xc = *reinterpret_cast<const float4 *>(x + b * ldx + 4 * c);
-        float o[4];
-#pragma unroll
-        for (int e = 0; e < 4; ++e)
-            o[e] = (float)((((double)comp(xa, e) + (double)comp(xi, e)) + (double)comp(xc, e)) / 3.0);
-        *reinterpret_cast<float4 *>(out + i * ldx + 4 * c) = make_float4(o[0], o[1], o[2], o[3]);
-    }
-}
-
-hipError_t launch_ring_mean(const float *x, int64_t N, int64_t ldx, float *out, hipStream_t s)
-{
-    int64_t grid = (N * (ldx / 4) + 255) / 256;
-    if (grid > kMaxGrid) grid = kMaxGrid;
-    if (grid < 1) grid = 1;
-    hipLaunchKernelGGL(k_ring_mean, dim3((unsigned)grid), dim3(256), 0, s, x, N, ldx, out);
-    return hipGetLastError();
-}
-
 hipError_t launch_stream_copy(const float *src, float *dst, int64_t n, hipStream_t s)
 {
     int64_t grid = (n / 4 + 255) / 256;
@@ -784,15 +759,15 @@ hipError_t launch_es_grad(const EsGradArgs &a, hipStream_t s)
     return hipGetLastError();
 }
 
-int occupancy_cso(int fn, Layout L)
+int occupancy_cso(int fn, Layout L, bool local)
 {
     switch (fn) {
-    case FN_SPHERE: return occupancy_cso_t<FN_SPHERE>(L);
-    case FN_ACKLEY: return occupancy_cso_t<FN_ACKLEY>(L);
-    case FN_RASTRIGIN: return occupancy_cso_t<FN_RASTRIGIN>(L);
-    case FN_GRIEWANK: return occupancy_cso_t<FN_GRIEWANK>(L);
-    case FN_ROSENBROCK: return occupancy_cso_t<FN_ROSENBROCK>(L);
-    case FN_SCHWEFEL: return occupancy_cso_t<FN_SCHWEFEL>(L);
+    case FN_SPHERE: return occupancy_cso_t<FN_SPHERE>(L, local);
+    case FN_ACKLEY: return occupancy_cso_t<FN_ACKLEY>(L, local);
+    case FN_RASTRIGIN: return occupancy_cso_t<FN_RASTRIGIN>(L, local);
+    case FN_GRIEWANK: return occupancy_cso_t<FN_GRIEWANK>(L, local);
+    case FN_ROSENBROCK: return occupancy_cso_t<FN_ROSENBROCK>(L, local);
+    case FN_SCHWEFEL: return occupancy_cso_t<FN_SCHWEFEL>(L, local);
     default: return 0;
     }
 }

@@ -14,6 +14,6 @@ template hipError_t launch_cso_t<EVOX_FN>(Layout, const CsoArgs &, int, hipStrea
 template hipError_t launch_de_t<EVOX_FN>(Layout, const DeArgs &, int, hipStream_t);
 template hipError_t launch_es_eval_t<EVOX_FN>(Layout, const EsArgs &, int, hipStream_t);
 template hipError_t launch_mae_eval_t<EVOX_FN>(Layout, const MaeEvalArgs &, int, hipStream_t);
-template int occupancy_cso_t<EVOX_FN>(Layout);
+template int occupancy_cso_t<EVOX_FN>(Layout, bool);
 
 }  // namespace evox

@@ -19,7 +19,10 @@
 // (a random gather), its own x and v, moves, writes x and v, is re-evaluated
 // from registers, and both rows' new values are accumulated into per-block
 // fp64 column sums for the next swarm mean: 20 B per pair element, i.e. 10 B
-// per individual element.
+// per individual element.  The neighbourhood version reads the positions
+// from the other population buffer (xs): the loser's neighbours l - 1 and
+// l + 1 besides its own row (three consecutive rows), and writes every row
+// of x (the winner's as a copy).
 #pragma once
 
 #include "evox_launch.hpp"
@@ -241,7 +244,7 @@ struct ColAcc {
     }
 };
 
-template <int FN, int G, int MAXIT>
+template <int FN, int G, int MAXIT, bool LOCAL>
 __global__ __launch_bounds__(block_for(G)) void k_cso(CsoArgs a)
 {
     constexpr int B = block_for(G), RPB = B / G;
@@ -283,12 +286,27 @@ __global__ __launch_bounds__(block_for(G)) void k_cso(CsoArgs a)
             const int64_t c = g + (int64_t)G * it;
             float4 xn = make_float4(0.f, 0.f, 0.f, 0.f);
             if (active && c < C4) {
-                const float4 xw = *reinterpret_cast<const float4 *>(a.x + w * a.ldx + 4 * c);
+                constexpr bool local = LOCAL;  // the neighbourhood version (a.xs is the other buffer)
+                const float4 xw = *reinterpret_cast<const float4 *>(a.xs + w * a.ldx + 4 * c);
                 if (paired) {
                     const int64_t off = l * a.ldx + 4 * c;
-                    const float4 xl = ld_stream(a.x + off);
+                    const float4 xl = ld_stream(a.xs + off);
                     const float4 vl = ld_stream(a.v + off);
-                    const float4 xb = *reinterpret_cast<const float4 *>(a.xbar + l * a.xbar_ld + 4 * c);
+                    float4 xb;
+                    if constexpr (local) {
+                        // ring mean of the rows before the generation: ((x_{l-1} + x_l) + x_{l+1}) / 3
+                        // in fp64, rounded once
+                        const int64_t lm = l == 0 ? a.N - 1 : l - 1, lp = l == a.N - 1 ? 0 : l + 1;
+                        const float4 xa = *reinterpret_cast<const float4 *>(a.xs + lm * a.ldx + 4 * c);
+                        const float4 xc = *reinterpret_cast<const float4 *>(a.xs + lp * a.ldx + 4 * c);
+                        float mo[4];
+#pragma unroll
+                        for (int e = 0; e < 4; ++e)
+                            mo[e] = (float)((((double)comp(xa, e) + (double)comp(xl, e)) + (double)comp(xc, e)) / 3.0);
+                        xb = make_float4(mo[0], mo[1], mo[2], mo[3]);
+                    } else {
+                        xb = *reinterpret_cast<const float4 *>(a.xbar + 4 * c);
+                    }
                     const U4 R1 = philox((uint32_t)(3 * c), (uint32_t)l, a.t, STREAM_CSO, a.k0, a.k1);
                     const U4 R2 = philox((uint32_t)(3 * c + 1), (uint32_t)l, a.t, STREAM_CSO, a.k0, a.k1);
                     const U4 R3 = philox((uint32_t)(3 * c + 2), (uint32_t)l, a.t, STREAM_CSO, a.k0, a.k1);
@@ -310,6 +328,7 @@ __global__ __launch_bounds__(block_for(G)) void k_cso(CsoArgs a)
                     st_stream(a.x + off, xn);
                     st_stream(a.v + off, make_float4(vo[0], vo[1], vo[2], vo[3]));
                 }
+                if constexpr (local) st_stream(a.x + w * a.ldx + 4 * c, xw);  // the winner's row, unchanged
 #pragma unroll
                 for (int e = 0; e < 4; ++e)
                     acc.add(it, e, paired ? (double)comp(xw, e) + (double)comp(xn, e) : (double)comp(xw, e));
@@ -664,8 +683,8 @@ __global__ __launch_bounds__(block_for(G)) void k_colsum(const float *x, int64_t
     hipLaunchKernelGGL((k_pso<FN, GG, MM, MODEE>), dim3(grid), dim3(block_for(GG)), 0, s, a)
 #define EVOX_LAUNCH_EVAL(GG, MM, VECC) \
     hipLaunchKernelGGL((k_eval<FN, GG, MM, VECC>), dim3(grid), dim3(block_for(GG)), 0, s, a)
-#define EVOX_LAUNCH_CSO(GG, MM, UNUSED) \
-    hipLaunchKernelGGL((k_cso<FN, GG, MM>), dim3(grid), dim3(block_for(GG)), 0, s, a)
+#define EVOX_LAUNCH_CSO(GG, MM, LOC) \
+    hipLaunchKernelGGL((k_cso<FN, GG, MM, LOC>), dim3(grid), dim3(block_for(GG)), 0, s, a)
 #define EVOX_LAUNCH_DE(GG, MM, UNUSED) \
     hipLaunchKernelGGL((k_de<FN, GG, MM>), dim3(grid), dim3(block_for(GG)), 0, s, a)
 #define EVOX_LAUNCH_ES(GG, MM, UNUSED) \
@@ -733,10 +752,18 @@ hipError_t launch_eval_t(Layout L, bool vec, const EvalArgs &a, int grid, hipStr
 template <int FN>
 hipError_t launch_cso_t(Layout L, const CsoArgs &a, int grid, hipStream_t s)
 {
-    switch (L.G * 16 + L.maxit) {
-        EVOX_FAMILY_CASES(EVOX_LAUNCH_CSO, LAYOUT_CSO, 0)
-        EVOX_BIG_CASES(EVOX_LAUNCH_CSO, LAYOUT_CSO, 0)
-        default: return hipErrorInvalidValue;
+    if (a.xs != a.x) {  // the neighbourhood version
+        switch (L.G * 16 + L.maxit) {
+            EVOX_FAMILY_CASES(EVOX_LAUNCH_CSO, LAYOUT_CSO, true)
+            EVOX_BIG_CASES(EVOX_LAUNCH_CSO, LAYOUT_CSO, true)
+            default: return hipErrorInvalidValue;
+        }
+    } else {
+        switch (L.G * 16 + L.maxit) {
+            EVOX_FAMILY_CASES(EVOX_LAUNCH_CSO, LAYOUT_CSO, false)
+            EVOX_BIG_CASES(EVOX_LAUNCH_CSO, LAYOUT_CSO, false)
+            default: return hipErrorInvalidValue;
+        }
     }
     return hipGetLastError();
 }
@@ -800,11 +827,12 @@ hipError_t launch_mae_eval_t(Layout L, const MaeEvalArgs &a, int grid, hipStream
 }
 
 template <int FN>
-int occupancy_cso_t(Layout L)
+int occupancy_cso_t(Layout L, bool local)
 {
     int n = 0;
-#define EVOX_OCC_CSO(GG, MM, UNUSED) \
-    (void)hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k_cso<FN, GG, MM>, block_for(GG), 0)
+#define EVOX_OCC_CSO(GG, MM, UNUSED)                                                                             \
+    (void)(local ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k_cso<FN, GG, MM, true>, block_for(GG), 0)  \
+                 : hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k_cso<FN, GG, MM, false>, block_for(GG), 0))
     switch (L.G * 16 + L.maxit) {
         EVOX_FAMILY_CASES(EVOX_OCC_CSO, LAYOUT_CSO, 0)
         EVOX_BIG_CASES(EVOX_OCC_CSO, LAYOUT_CSO, 0)

@@ -209,7 +209,11 @@ struct CsoArgs {
     uint32_t k0, k1, t;
     SelSlots *slots;
     double *xsum;  // [grid][ldx] column partial sums of the new positions
-    int64_t xbar_ld;  // 0: one mean row for the swarm; ldx: loser l's mean is row l
+    // positions before the generation: x itself (swarm mean: the losers are
+    // moved in place), or the other population buffer (neighbourhood
+    // version: every row of x is written, the losers' new rows and copies of
+    // the others, and loser l's mean is that of rows l - 1, l, l + 1 of xs)
+    const float *xs;
 };
 
 hipError_t launch_pso(int fn, Layout L, int mode, const PsoArgs &a, int grid, hipStream_t s);
@@ -226,7 +230,7 @@ hipError_t launch_es_eval_t(Layout L, const EsArgs &a, int grid, hipStream_t s);
 template <int FN>
 hipError_t launch_mae_eval_t(Layout L, const MaeEvalArgs &a, int grid, hipStream_t s);
 template <int FN>
-int occupancy_cso_t(Layout L);  // resident blocks per CU of k_cso
+int occupancy_cso_t(Layout L, bool local);  // resident blocks per CU of k_cso
 hipError_t launch_eval(int fn, Layout L, bool vec, const EvalArgs &a, int grid, hipStream_t s);
 // Second pass of the selection: reduce and reset the slots, store the result
 // (best and/or the two outputs, each nullable) and copy the selected row of
@@ -240,7 +244,6 @@ hipError_t launch_philox_fill(uint32_t k0, uint32_t k1, uint32_t c1, uint32_t c2
 hipError_t launch_stream_copy(const float *src, float *dst, int64_t n, hipStream_t s);
 // CSO's neighbourhood version: out row i = ((x_{i-1} + x_i) + x_{i+1}) / 3
 // (indices modulo N) in fp64, rounded once; every column of the pitch.
-hipError_t launch_ring_mean(const float *x, int64_t N, int64_t ldx, float *out, hipStream_t s);
 hipError_t launch_copy_row(const float *src, float *dst, int64_t ldx, hipStream_t s);
 hipError_t launch_fill(float *dst, int64_t n, float value, hipStream_t s);
 hipError_t launch_best_init(DevBest *best, float f, int64_t i, hipStream_t s);
@@ -273,7 +276,7 @@ hipError_t launch_es_eval(int fn, Layout L, const EsArgs &a, int grid, hipStream
 hipError_t launch_es_rank(const float *fit, int64_t N, uint32_t *rank, hipStream_t s);
 hipError_t launch_mae_eval(int fn, Layout L, const MaeEvalArgs &a, int grid, hipStream_t s);
 hipError_t launch_es_grad(const EsGradArgs &a, hipStream_t s);
-int occupancy_cso(int fn, Layout L);
+int occupancy_cso(int fn, Layout L, bool local);
 hipError_t launch_colsum(Layout L, const float *x, int64_t N, int64_t D, int64_t ldx, double *xsum,
                          int grid, hipStream_t s);
 
