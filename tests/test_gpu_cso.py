@@ -184,6 +184,20 @@ def test_neighbourhood_version_matches_oracle(evox_gpu, ref, case):
     assert g.t == r.t
 
 
+def test_neighbourhood_version_several_generations_per_call(evox_gpu, ref):
+    """Calls of 2, 3 and 4 generations: the positions alternate between the
+    caller's x and the second buffer inside a call, and an odd count ends
+    with the copy back into x; rows, velocities and padding must be exact."""
+    c = dict(fn=3, N=501, D=29, seed=5, lb=-600.0, ub=600.0)
+    print(f"cso local multi {c}", flush=True)
+    g, r = pair(evox_gpu, ref, cso_local=1, **c)
+    for n in (2, 3, 4):
+        g.step(n)
+        r.step(n)
+        compare(g, r, c["fn"], f"after a call of {n}", strict=True)
+        assert not g.x[:, c["D"]:].any(), "padding columns must stay zero"
+
+
 def test_neighbourhood_version_equals_swarm_version_at_three(evox_gpu, ref):
     a, _ = pair(evox_gpu, ref, 0, 3, 9, 12, -5.0, 5.0)
     b, _ = pair(evox_gpu, ref, 0, 3, 9, 12, -5.0, 5.0, cso_local=1)
