@@ -118,7 +118,9 @@ typedef struct evox_params {
  *   PSO: x, v, pbest [N][ldx]; pfit [N]; gbest [ldx]; fit [N] optional (the
  *        fitness of the last evaluated positions); xbar unused.
  *   CSO: x, v [N][ldx]; fit [N]; xbar [ldx] (swarm mean of x); pbest, pfit,
- *        gbest unused.
+ *        gbest unused.  The neighbourhood version (cso_local = 1) keeps a
+ *        second population buffer in the scratch and alternates between it
+ *        and x inside a call; x holds the positions whenever a call returns.
  *   DE:  x [N][ldx]; fit [N] (the fitness of x); v, pbest, pfit, gbest, xbar
  *        unused (the second population buffer is part of the scratch).
  *   ES:  x [ldx] = the center theta (one row; x_init / lb / ub / seed give
@@ -211,7 +213,9 @@ int evox_pso_step(evox_state *state, int64_t n_gens);
  *     x_l = x_l + vn (clamped if clamp_x)
  * with R1..R3 from stream 3 at generation t, and only the losers are
  * re-evaluated.  Winners and an unpaired individual are untouched.  xbar is
- * then refreshed from the new positions. */
+ * then refreshed from the new positions.  With cso_local = 1 the mean of a
+ * loser l is that of rows l - 1, l, l + 1 (modulo N) of the positions before
+ * the generation, in fp64 rounded once. */
 int evox_cso_step(evox_state *state, int64_t n_gens);
 
 /* n_gens generations of DE/rand/1/bin (Storn & Price, J. Global Optim. 11,
