@@ -42,7 +42,7 @@ struct DeArgs {
 // k_es_update: the gradient estimates with the deviates regenerated from
 // Philox (never stored) and the steps.
 constexpr int kEsMaxN = 16384;
-constexpr int kEsPairChunk = 64;  // pairs per thread of the gradient pass
+constexpr int kEsPairChunk = 32;  // pairs per thread of the gradient pass
 struct EsArgs {
     const float *theta;
     const float *sig;      // PGPE: per-dimension deviations; null: the scalar sigma
