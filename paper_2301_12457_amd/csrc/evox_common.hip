@@ -610,31 +610,47 @@ hipError_t launch_mae_eval(int fn, Layout L, const MaeEvalArgs &a, int grid, hip
 // ---------------------------------------------------------------------------
 // OpenES centered ranks: rank_i = #{j : key_j < key_i} with key = (orderable
 // fitness, index), the argmin order, so the ranks are a permutation and NaN
-// ranks last.  Block (tile of 256 samples i, range of kEsRankSpan samples j)
-// stages its j-keys in LDS, counts, and adds its count to rank_i with one
-// integer atomic per i (exact, so the result does not depend on the order of
-// the additions).  rank is zeroed by k_es_eval of the same generation.
+// ranks last.  Block (tile of 256 kEsRankPer samples i, kEsRankPer per
+// thread, range of kEsRankSpan samples j) stages its j-keys in LDS, counts
+// (each key read from LDS serves kEsRankPer comparisons), and adds each
+// count to rank_i with one integer atomic per i (exact, so the result does
+// not depend on the order of the additions).  rank is zeroed by k_es_eval
+// of the same generation.
 // ---------------------------------------------------------------------------
-constexpr int kEsRankSpan = 512;
+constexpr int kEsRankSpan = 128, kEsRankPer = 4;
 
 __global__ __launch_bounds__(256) void k_es_rank(const float *fit, int64_t N, uint32_t *rank)
 {
     __shared__ uint64_t kj[kEsRankSpan];
-    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    const int64_t i0 = (int64_t)blockIdx.x * (256 * kEsRankPer) + threadIdx.x;
     const int64_t j0 = (int64_t)blockIdx.y * kEsRankSpan;
     const int64_t nj = N - j0 < kEsRankSpan ? N - j0 : kEsRankSpan;
     for (int q = threadIdx.x; q < nj; q += 256) kj[q] = sel_key(fit[j0 + q], j0 + q);
     __syncthreads();
-    if (i >= N) return;
-    const uint64_t ki = sel_key(fit[i], i);
-    uint32_t below_i = 0;
-    for (int q = 0; q < nj; ++q) below_i += kj[q] < ki ? 1u : 0u;
-    if (below_i) atomicAdd(&rank[i], below_i);
+    uint64_t ki[kEsRankPer];
+    uint32_t below[kEsRankPer];
+#pragma unroll
+    for (int u = 0; u < kEsRankPer; ++u) {
+        const int64_t i = i0 + 256 * u;
+        ki[u] = i < N ? sel_key(fit[i], i) : 0;  // key 0 counts nothing below it
+        below[u] = 0;
+    }
+    for (int q = 0; q < nj; ++q) {
+        const uint64_t k = kj[q];
+#pragma unroll
+        for (int u = 0; u < kEsRankPer; ++u) below[u] += k < ki[u] ? 1u : 0u;
+    }
+#pragma unroll
+    for (int u = 0; u < kEsRankPer; ++u) {
+        const int64_t i = i0 + 256 * u;
+        if (i < N && below[u]) atomicAdd(&rank[i], below[u]);
+    }
 }
 
 hipError_t launch_es_rank(const float *fit, int64_t N, uint32_t *rank, hipStream_t s)
 {
-    const unsigned tiles = (unsigned)((N + 255) / 256), spans = (unsigned)((N + kEsRankSpan - 1) / kEsRankSpan);
+    const unsigned tiles = (unsigned)((N + 256 * kEsRankPer - 1) / (256 * kEsRankPer)),
+                   spans = (unsigned)((N + kEsRankSpan - 1) / kEsRankSpan);
     hipLaunchKernelGGL(k_es_rank, dim3(tiles, spans), dim3(256), 0, s, fit, N, rank);
     return hipGetLastError();
 }
