@@ -244,8 +244,12 @@ struct ColAcc {
     }
 };
 
+// pairs whose winner and loser a block decides in one phase (the fitness
+// gathers of 64 pairs in flight at once), before its row groups move them
+constexpr int kCsoDecide = 64;
+
 template <int FN, int G, int MAXIT, bool LOCAL>
-__global__ __launch_bounds__(block_for(G)) void k_cso(CsoArgs a)
+__device__ __forceinline__ void cso_body(const CsoArgs &a)
 {
     constexpr int B = block_for(G), RPB = B / G;
     __shared__ float nbr[(FN == FN_ROSENBROCK && G > 64) ? B * MAXIT : 1];
@@ -261,25 +265,41 @@ __global__ __launch_bounds__(block_for(G)) void k_cso(CsoArgs a)
     uint32_t none = 0;
     ColAcc<G, MAXIT> acc(acc_lds);
 
-    for (int64_t kb = (int64_t)blockIdx.x * RPB; kb < NG; kb += (int64_t)gridDim.x * RPB) {
-        const int64_t k = kb + slot;
-        const bool active = k < NG;
-        const bool paired = k < NP;
-        int64_t w = 0, l = 0;
-        float fw = 0.0f;
-        if (active) {
-            if (paired) {
+    // Each phase: the block's threads decide SB pairs (winner, loser, the
+    // winner's fitness) into LDS, then its row groups move them RPB at a
+    // time, so the row gathers wait on no fitness load.
+    constexpr int SB = kCsoDecide > RPB ? kCsoDecide : RPB;
+    static_assert(SB % RPB == 0 && SB <= B, "whole row-group rounds per phase");
+    __shared__ int32_t dw[SB], dl[SB];
+    __shared__ float dfw[SB];
+    for (int64_t sb = (int64_t)blockIdx.x * SB; sb < NG; sb += (int64_t)gridDim.x * SB) {
+        for (int t = tid; t < SB; t += B) {
+            const int64_t k = sb + t;
+            int64_t w = 0, l = 0;
+            float fw = 0.0f;
+            if (k < NP) {
                 const int64_t p0 = a.perm[2 * k], p1 = a.perm[2 * k + 1];
                 const float f0 = a.fit[p0], f1 = a.fit[p1];
                 const bool second = f1 < f0 || (f0 != f0 && f1 == f1);
                 w = second ? p1 : p0;
                 l = second ? p0 : p1;
                 fw = second ? f1 : f0;
-            } else {
+            } else if (k < NG) {
                 w = a.perm[a.N - 1];
                 fw = a.fit[w];
             }
+            dw[t] = (int32_t)w;
+            dl[t] = (int32_t)l;
+            dfw[t] = fw;
         }
+        __syncthreads();
+        for (int r = 0; r < SB / RPB; ++r) {  // uniform trip count: every thread reaches the barriers
+        const int q = r * RPB + slot;
+        const int64_t k = sb + q;
+        const bool active = k < NG;
+        const bool paired = k < NP;
+        const int64_t w = dw[q], l = dl[q];
+        const float fw = dfw[q];
         float4 xr[MAXIT];
 #pragma unroll
         for (int it = 0; it < MAXIT; ++it) {
@@ -345,10 +365,28 @@ __global__ __launch_bounds__(block_for(G)) void k_cso(CsoArgs a)
                 best = kl < best ? kl : best;
             }
         }
+        }
+        __syncthreads();  // the next phase overwrites the decisions
     }
     block_min_key(best, none, sk, sc);
     if (tid == 0) slot_commit(a.slots, best, 0);
     acc.write(a.D, a.ldx, a.xsum);
+}
+
+template <int FN, int G, int MAXIT, bool LOCAL>
+__global__ __launch_bounds__(block_for(G)) void k_cso(CsoArgs a)
+{
+    cso_body<FN, G, MAXIT, LOCAL>(a);
+}
+
+// The swarm-mean generation with one chunk per lane and at most 32 lanes per
+// row (D <= 128), compiled for 5 waves per SIMD (within 96 registers, no
+// spills for any of the six functions; at 64 lanes Griewank would spill):
+// the shape of the large-population, moderate-D workloads.
+template <int FN, int G>
+__global__ __launch_bounds__(block_for(G)) __attribute__((amdgpu_waves_per_eu(5))) void k_cso5(CsoArgs a)
+{
+    cso_body<FN, G, 1, false>(a);
 }
 
 // ---------------------------------------------------------------------------
@@ -752,7 +790,15 @@ hipError_t launch_eval_t(Layout L, bool vec, const EvalArgs &a, int grid, hipStr
 template <int FN>
 hipError_t launch_cso_t(Layout L, const CsoArgs &a, int grid, hipStream_t s)
 {
-    if (a.xs != a.x) {  // the neighbourhood version
+    if (a.xs == a.x && L.maxit == 1 && L.G <= 32) {  // swarm mean, one chunk per lane: 5 waves per SIMD
+        switch (L.G) {
+            case 4: hipLaunchKernelGGL((k_cso5<FN, 4>), dim3(grid), dim3(block_for(4)), 0, s, a); break;
+            case 8: hipLaunchKernelGGL((k_cso5<FN, 8>), dim3(grid), dim3(block_for(8)), 0, s, a); break;
+            case 16: hipLaunchKernelGGL((k_cso5<FN, 16>), dim3(grid), dim3(block_for(16)), 0, s, a); break;
+            case 32: hipLaunchKernelGGL((k_cso5<FN, 32>), dim3(grid), dim3(block_for(32)), 0, s, a); break;
+            default: return hipErrorInvalidValue;
+        }
+    } else if (a.xs != a.x) {  // the neighbourhood version
         switch (L.G * 16 + L.maxit) {
             EVOX_FAMILY_CASES(EVOX_LAUNCH_CSO, LAYOUT_CSO, true)
             EVOX_BIG_CASES(EVOX_LAUNCH_CSO, LAYOUT_CSO, true)
@@ -830,6 +876,16 @@ template <int FN>
 int occupancy_cso_t(Layout L, bool local)
 {
     int n = 0;
+    if (!local && L.maxit == 1 && L.G <= 32) {
+        switch (L.G) {
+            case 4: (void)hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k_cso5<FN, 4>, block_for(4), 0); break;
+            case 8: (void)hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k_cso5<FN, 8>, block_for(8), 0); break;
+            case 16: (void)hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k_cso5<FN, 16>, block_for(16), 0); break;
+            case 32: (void)hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k_cso5<FN, 32>, block_for(32), 0); break;
+            default: return 0;
+        }
+        return n;
+    }
 #define EVOX_OCC_CSO(GG, MM, UNUSED)                                                                             \
     (void)(local ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k_cso<FN, GG, MM, true>, block_for(GG), 0)  \
                  : hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k_cso<FN, GG, MM, false>, block_for(GG), 0))
