@@ -234,7 +234,7 @@ int make_plan(const evox_params *P, Plan *pl)
         // kernel exists for that count, else a multiple of 32 terms
         const int64_t steps = (p.mae_mu + 2) / 2;
         p.mae_kp = steps <= kMaeRankUnrolled ? 2 * steps : (p.mae_mu + 1 + 31) / 32 * 32;
-        p.mae_ldf = (P->D + 63) / 64 * 64;
+        p.mae_ldf = (P->D + 127) / 128 * 128;
         p.mae_splits = mae_splits(P->N, P->D, resident_thin_blocks(P->N + 1));
         p.mae_z = take(sizeof(float) * rows * (size_t)P->ldx);
         p.mae_d = take(sizeof(float) * rows * (size_t)P->ldx);

@@ -128,24 +128,121 @@ __global__ __launch_bounds__(256) void k_mae_sigma(MaeArgs a, int64_t nparts)
     if (threadIdx.x == 0) *a.sigma = (float)((double)*a.sigma * exp(a.damp * (sqrt(red[0]) / a.chi - 1.0)));
 }
 
-// M <- beta M + At^T Bt over the factor terms (2 STEPS of them; the factors
-// hold zeros past the mu + 1 real terms and past column D, up to their
-// padded extents, so no operand load needs a guard): each wave owns a
-// 32 x 64 tile of M and accumulates two 32x32x2 MFMA tiles, loading the
-// operands directly from the k-major factors (lane l: row or column l % 32
-// of term 2 step + l / 32, one 128-byte line per half wave).  The tile of M
-// is loaded first; the operands of a fully unrolled block of steps are all
-// issued before its products, so that a wave waits for them once.  No LDS,
-// no barrier.  STEPS = 0: any number of steps (a.kp / 2, a multiple of 16),
-// 16 at a time, double-buffered: the next block's loads are in flight while
-// the current block's products run.  The unrolled kernels are compiled for
-// 4 waves per SIMD (124 registers); the general one holds two blocks of
-// operands at one wave per SIMD, which measured faster than 2 or 3 waves
-// with 8-step blocks.
+// M <- beta M + At^T Bt over 2 STEPS factor terms (the factors hold zeros
+// past the mu + 1 real terms and past column D, up to their padded extents:
+// kp = 2 STEPS terms, a pitch ldf that is a multiple of 128, so no operand
+// load needs a guard).  A block of four waves owns a 128 x 64 tile of M, each
+// wave a 32 x 64 slice of it accumulated in two 32x32x2 MFMA tiles.  The
+// block first issues its operand loads (the 128 rows of At and 64 columns
+// of Bt over all terms, float4 from the k-major factors), then each wave
+// issues the 32 loads of its slice of M; the operands go to LDS as soon as
+// they arrive (loads complete in order, so the slice is still on its way
+// from HBM) and the products read them from LDS while the slice arrives.
+// LDS holds each term pair interleaved ([pair][row][term of the pair]) so
+// that lane l = col + 32 h reads float 2 col + h of a pair: 64 consecutive
+// floats, no bank conflicts.  The barrier fences LDS only, keeping the
+// slice's loads in flight.  Rows past D read as zero and are not stored.
+// Waves per SIMD the staged operands leave room for: four blocks of up to
+// 40 KB of LDS per CU, three past that.
 template <int STEPS>
-__device__ __forceinline__ void rank_body(const MaeArgs &a, float *M, float beta)
+constexpr int kMaeRankWaves = STEPS * 48 * 32 <= 160 * 1024 / 4 ? 4 : 3;
+
+template <int STEPS>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(kMaeRankWaves<STEPS>))) void k_mae_rank(MaeArgs a, float *M,
+                                                                                           float beta)
 {
-    constexpr int CH = STEPS > 0 ? STEPS : 16;
+    constexpr int NA = STEPS * 32, NI = STEPS * 48, PER = (NI + 255) / 256;  // float4 pairs of terms to stage
+    __shared__ float4 sA[STEPS * 64], sB[STEPS * 32];
+    const int tid = threadIdx.x, lane = tid % 64, col = lane % 32, h = lane / 32, w = tid / 64;
+    const int64_t tn = (a.D + 63) / 64, ldf = a.ldf, ld = a.ldx;
+    const int64_t I0 = ((int64_t)blockIdx.x / tn) * 128, j0 = ((int64_t)blockIdx.x % tn) * 64;
+    const int64_t i0 = I0 + 32 * w;
+    float4 lo[PER], hi[PER];
+#pragma unroll
+    for (int p = 0; p < PER; ++p) {
+        // the last round's spare threads load the last item again (no
+        // branch around the loads, which would wait for them)
+        const int it = tid + 256 * p < NI ? tid + 256 * p : NI - 1;
+        const bool isA = it < NA;
+        const int s = isA ? it / 32 : (it - NA) / 16, q = isA ? it % 32 : (it - NA) % 16;
+        const float *f = (isA ? a.At + I0 : a.Bt + j0) + 2 * s * ldf + 4 * q;
+        lo[p] = *reinterpret_cast<const float4 *>(f);
+        hi[p] = *reinterpret_cast<const float4 *>(f + ldf);
+    }
+    // The wave's slice of M through a buffer descriptor based at its first
+    // element and ending at the end of M: rows past D fall outside its range
+    // and read as zero (they are not stored).  The row offset sits in the
+    // lane offset because the range check ignores the scalar offset.
+    const int64_t wi0 = I0 + 32 * __builtin_amdgcn_readfirstlane(w);  // = i0, known to be wave-uniform
+    const int64_t left = wi0 < a.D ? ((a.D - wi0) * ld - j0) * 4 : 0;  // bytes from the slice to the end of M
+    const __amdgpu_buffer_rsrc_t mr = __builtin_amdgcn_make_buffer_rsrc(
+        M + (wi0 < a.D ? wi0 * ld + j0 : 0), 0, (int)(left < 0x7fffffffLL ? left : 0x7fffffffLL), 0x00020000);
+    float old[2][16];
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+        const int off = (((v / 4) * 8 + h * 4 + v % 4) * (int)ld + col) * 4;
+        old[0][v] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(mr, off, 0, 0));  // the load returns bits
+        old[1][v] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(mr, off + 128, 0, 0));
+    }
+#pragma unroll
+    for (int p = 0; p < PER; ++p) {
+        const int it = tid + 256 * p;
+        if (p + 1 < PER || it < NI) {
+            const bool isA = it < NA;
+            const int s = isA ? it / 32 : (it - NA) / 16, q = isA ? it % 32 : (it - NA) % 16;
+            float4 *d = isA ? sA + s * 64 + 2 * q : sB + s * 32 + 2 * q;
+            d[0] = make_float4(lo[p].x, hi[p].x, lo[p].y, hi[p].y);
+            d[1] = make_float4(lo[p].z, hi[p].z, lo[p].w, hi[p].w);
+        }
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+    if (i0 >= a.D) return;
+    const float *la = reinterpret_cast<const float *>(sA) + (32 * w + col) * 2 + h;
+    const float *lb = reinterpret_cast<const float *>(sB) + col * 2 + h;
+    f32x16 acc[2];
+#pragma unroll
+    for (int n = 0; n < 2; ++n)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) acc[n][v] = 0.0f;
+#pragma unroll
+    for (int s = 0; s < STEPS; ++s) {
+        const float av = la[s * 256], b0 = lb[s * 128], b1 = lb[s * 128 + 64];
+        acc[0] = __builtin_amdgcn_mfma_f32_32x32x2f32(av, b0, acc[0], 0, 0, 0);
+        acc[1] = __builtin_amdgcn_mfma_f32_32x32x2f32(av, b1, acc[1], 0, 0, 0);
+    }
+    if (j0 + 64 <= a.D) {
+        // every column is inside the matrix: store through the descriptor,
+        // which drops the rows past D
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+            const int off = (((v / 4) * 8 + h * 4 + v % 4) * (int)ld + col) * 4;
+            __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(fmaf(1.0f, acc[0][v], beta * old[0][v])), mr, off, 0, 0);
+            __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(fmaf(1.0f, acc[1][v], beta * old[1][v])), mr, off + 128,
+                                                  0, 0);
+        }
+        return;
+    }
+#pragma unroll
+    for (int n = 0; n < 2; ++n)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+            const int64_t i = i0 + (v / 4) * 8 + h * 4 + v % 4, j = j0 + 32 * n + col;
+            if (i < a.D && j < a.D) M[i * ld + j] = fmaf(1.0f, acc[n][v], beta * old[n][v]);
+        }
+}
+
+// The same update for any number of terms (a.kp, a multiple of 32): each
+// wave owns a 32 x 64 tile of M and loads its MFMA operands directly from the
+// k-major factors (lane l: row or column l % 32 of term 2 step + l / 32, one
+// 128-byte line per half wave), 16 steps at a time, double-buffered: the
+// next block's loads are in flight while the current block's products run.
+// The tile of M is loaded first.  It holds two blocks of operands at one
+// wave per SIMD, which measured faster than 2 or 3 waves with 8-step blocks.
+__global__ __launch_bounds__(256) void k_mae_rank_any(MaeArgs a, float *M, float beta)
+{
+    constexpr int CH = 16;
     const int lane = threadIdx.x % 64, col = lane % 32, h = lane / 32;
     const int64_t tn = (a.D + 63) / 64;
     const int64_t wave = (int64_t)blockIdx.x * 4 + threadIdx.x / 64;
@@ -183,21 +280,14 @@ __device__ __forceinline__ void rank_body(const MaeArgs &a, float *M, float beta
             acc[1] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[buf][t], b1[buf][t], acc[1], 0, 0, 0);
         }
     };
-    if constexpr (STEPS > 0) {
-        load(0, 0);
+    const int64_t steps = a.kp / 2;
+    load(0, 0);
+    for (int64_t c0 = 0; c0 < steps; c0 += 2 * CH) {
+        if (c0 + CH < steps) load(1, c0 + CH);
         products(0);
-    } else {
-        // any number of steps (a multiple of CH): the next block's operands
-        // are loaded while the current block's products run
-        const int64_t steps = a.kp / 2;
-        load(0, 0);
-        for (int64_t c0 = 0; c0 < steps; c0 += 2 * CH) {
-            if (c0 + CH < steps) load(1, c0 + CH);
-            products(0);
-            if (c0 + CH < steps) {
-                if (c0 + 2 * CH < steps) load(0, c0 + 2 * CH);
-                products(1);
-            }
+        if (c0 + CH < steps) {
+            if (c0 + 2 * CH < steps) load(0, c0 + 2 * CH);
+            products(1);
         }
     }
 #pragma unroll
@@ -207,18 +297,6 @@ __device__ __forceinline__ void rank_body(const MaeArgs &a, float *M, float beta
             const int64_t i = i0 + (v / 4) * 8 + h * 4 + v % 4, j = j0 + 32 * n + col;
             if (i < a.D && j < a.D) M[i * a.ldx + j] = fmaf(1.0f, acc[n][v], beta * old[n][v]);
         }
-}
-
-template <int STEPS>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void k_mae_rank(MaeArgs a, float *M,
-                                                                                           float beta)
-{
-    rank_body<STEPS>(a, M, beta);
-}
-
-__global__ __launch_bounds__(256) void k_mae_rank_any(MaeArgs a, float *M, float beta)
-{
-    rank_body<0>(a, M, beta);
 }
 
 __global__ __launch_bounds__(256) void k_mae_identity(float *M, int64_t D, int64_t ldx)
@@ -266,8 +344,10 @@ hipError_t launch_mae_recombine(const MaeArgs &a, hipStream_t s)
 hipError_t launch_mae_rank(const MaeArgs &a, float *M, float beta, hipStream_t s)
 {
     const int64_t waves = ((a.D + 31) / 32) * ((a.D + 63) / 64);
-    const dim3 grid((unsigned)((waves + 3) / 4)), block(256);
+    const dim3 grid_any((unsigned)((waves + 3) / 4)), block(256);
+    const dim3 grid((unsigned)(((a.D + 127) / 128) * ((a.D + 63) / 64)));
     const int64_t steps = (a.mu + 2) / 2;  // ceil((mu + 1) / 2)
+    if (a.ldf % 128 != 0 || (steps <= kMaeRankUnrolled && a.kp != 2 * steps)) return hipErrorInvalidValue;
     switch (steps > kMaeRankUnrolled ? 0 : steps) {
 #define EVOX_RANK_CASE(S) \
     case S: hipLaunchKernelGGL((k_mae_rank<S>), grid, block, 0, s, a, M, beta); break;
@@ -279,7 +359,7 @@ hipError_t launch_mae_rank(const MaeArgs &a, float *M, float beta, hipStream_t s
         EVOX_RANK_CASE(26) EVOX_RANK_CASE(27) EVOX_RANK_CASE(28) EVOX_RANK_CASE(29) EVOX_RANK_CASE(30)
         EVOX_RANK_CASE(31) EVOX_RANK_CASE(32)
 #undef EVOX_RANK_CASE
-        default: hipLaunchKernelGGL(k_mae_rank_any, grid, block, 0, s, a, M, beta); break;
+        default: hipLaunchKernelGGL(k_mae_rank_any, grid_any, block, 0, s, a, M, beta); break;
     }
     return hipGetLastError();
 }
