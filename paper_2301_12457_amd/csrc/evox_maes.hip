@@ -172,7 +172,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(kMaeRankWav
     // The wave's slice of M through a buffer descriptor based at its first
     // element and ending at the end of M: rows past D fall outside its range
     // and read as zero (they are not stored).  The row offset sits in the
-    // lane offset because the range check ignores the scalar offset.
+    // lane offset because the range check ignores the scalar offset.  M is
+    // read and written once per pass, with the non-temporal policy (aux 2),
+    // which keeps the staged factors in the L2.
     const int64_t wi0 = I0 + 32 * __builtin_amdgcn_readfirstlane(w);  // = i0, known to be wave-uniform
     const int64_t left = wi0 < a.D ? ((a.D - wi0) * ld - j0) * 4 : 0;  // bytes from the slice to the end of M
     const __amdgpu_buffer_rsrc_t mr = __builtin_amdgcn_make_buffer_rsrc(
@@ -181,8 +183,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(kMaeRankWav
 #pragma unroll
     for (int v = 0; v < 16; ++v) {
         const int off = (((v / 4) * 8 + h * 4 + v % 4) * (int)ld + col) * 4;
-        old[0][v] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(mr, off, 0, 0));  // the load returns bits
-        old[1][v] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(mr, off + 128, 0, 0));
+        old[0][v] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(mr, off, 0, 2));  // the load returns bits
+        old[1][v] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(mr, off + 128, 0, 2));
     }
 #pragma unroll
     for (int p = 0; p < PER; ++p) {
@@ -218,9 +220,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(kMaeRankWav
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
             const int off = (((v / 4) * 8 + h * 4 + v % 4) * (int)ld + col) * 4;
-            __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(fmaf(1.0f, acc[0][v], beta * old[0][v])), mr, off, 0, 0);
+            __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(fmaf(1.0f, acc[0][v], beta * old[0][v])), mr, off, 0, 2);
             __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(fmaf(1.0f, acc[1][v], beta * old[1][v])), mr, off + 128,
-                                                  0, 0);
+                                                  0, 2);
         }
         return;
     }
