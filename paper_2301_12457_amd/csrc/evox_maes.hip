@@ -68,6 +68,8 @@ __global__ __launch_bounds__(256) void k_mae_wsum(MaeArgs a)
     if (j >= a.D) return;
     const int64_t r0 = c * kMaeChunk, r1 = r0 + kMaeChunk < a.mu ? r0 + kMaeChunk : a.mu;
     double zw = 0.0, dw = 0.0;
+    // unrolled so that several parents' loads are in flight (same order)
+#pragma unroll 8
     for (int64_t r = r0; r < r1; ++r) {
         const int64_t k = a.sel[r];
         const double wr = a.w[r];
@@ -91,6 +93,7 @@ __global__ __launch_bounds__(kMaeBlock) void k_mae_recombine(MaeArgs a, int64_t 
     double sq = 0.0;
     if (j < a.D) {
         double zw = 0.0, dw = 0.0;
+#pragma unroll 8
         for (int64_t c = 0; c < nchunks; ++c) {
             zw += a.wpart[(2 * c) * a.D + j];
             dw += a.wpart[(2 * c + 1) * a.D + j];
