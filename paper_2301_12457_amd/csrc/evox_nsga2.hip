@@ -339,7 +339,9 @@ __global__ __launch_bounds__(256) void k_nsga_trunc(const int32_t *list, int64_t
     const int32_t i = list[full + q];
     const double ci = crowd[i];
     int32_t c = 0;
-    for (int64_t r = 0; r < nr; ++r) c += cj[r] > ci || (cj[r] == ci && ij[r] < i);
+    // bitwise, not short-circuit: no branch per entry, so the loop unrolls
+#pragma unroll 8
+    for (int64_t r = 0; r < nr; ++r) c += (int32_t)((cj[r] > ci) | ((cj[r] == ci) & (ij[r] < i)));
     if (c) atomicAdd(rank + q, c);
 }
 
