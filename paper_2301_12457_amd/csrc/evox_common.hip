@@ -422,7 +422,8 @@ __global__ __launch_bounds__(256) void k_perm_sort(PermArgs a)
             const uint32_t key = K[q], idx = I[q], sb = (key >> shift) & 255u;
             const uint32_t s0 = start[sb], s1 = s0 + cnt[sb];
             uint32_t rank = 0;
-            for (uint32_t r = s0; r < s1; ++r) rank += (K[r] < key || (K[r] == key && I[r] < idx)) ? 1u : 0u;
+            // bitwise, not short-circuit: no branch per entry
+            for (uint32_t r = s0; r < s1; ++r) rank += (uint32_t)((K[r] < key) | ((K[r] == key) & (I[r] < idx)));
             S[s0 + rank] = idx;
         }
         __syncthreads();
@@ -433,7 +434,7 @@ __global__ __launch_bounds__(256) void k_perm_sort(PermArgs a)
             uint32_t rank = 0;
             for (uint32_t q = 0; q < n; ++q) {
                 const uint32_t kq = sl.tkv[lo + q].x, iq = sl.tkv[lo + q].y;
-                rank += (kq < key || (kq == key && iq < idx)) ? 1u : 0u;
+                rank += (uint32_t)((kq < key) | ((kq == key) & (iq < idx)));
             }
             sl.perm[lo + rank] = idx;
         }
