@@ -342,6 +342,16 @@ int evox_best(evox_state *state, float *best_fit, int64_t *best_idx, float *best
 /* Generations completed so far. */
 int64_t evox_generation(const evox_state *state);
 
+/* Resume at generation t (0 <= t < 2^32): the next step performs generation
+ * t, drawing the random numbers of generation t (t is the generation index
+ * in every Philox counter).  Together with buffers the caller has written
+ * this restores a state saved at generation t (the state as a function of t
+ * and its buffers, Sec. IV-B): for PSO, x, v, pbest and pfit (the next step
+ * re-evaluates x and re-selects the global best from pfit); for CSO, x, v and
+ * fit followed by evox_cso_refresh (swarm mean and best).  Enqueues nothing;
+ * EVOX_EINVAL for a null state or t out of range. */
+int evox_set_generation(evox_state *state, int64_t t);
+
 /* Kernel families for evox_row_layout. */
 enum evox_layout { EVOX_LAYOUT_PSO = 0, EVOX_LAYOUT_CSO = 1, EVOX_LAYOUT_EVAL = 2 };
 

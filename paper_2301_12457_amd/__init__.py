@@ -25,7 +25,8 @@ EXPORTS = (
     "evox_eval_argmin_scratch_bytes", "evox_eval_argmin", "evox_pso_step", "evox_cso_step",
     "evox_de_step", "evox_es_step", "evox_pgpe_step", "evox_maes_step", "evox_nsga2_step",
     "evox_nsga2_sort_scratch_bytes", "evox_nsga2_sort",
-    "evox_cso_refresh", "evox_best", "evox_generation", "evox_row_layout", "evox_default_ldx",
+    "evox_cso_refresh", "evox_best", "evox_generation", "evox_set_generation", "evox_row_layout",
+    "evox_default_ldx",
     "evox_fill_normal", "evox_sgemm", "evox_copy", "evox_philox_fill", "evox_permutation_scratch_bytes",
     "evox_permutation", "evox_argsort_u32",
     "evox_profile", "evox_profile_read", "evox_strerror", "evox_last_error",
@@ -96,6 +97,7 @@ def lib():
             "evox_cso_refresh": ([P, i32], i32),
             "evox_best": ([P, P, P, P], i32),
             "evox_generation": ([P], i64),
+            "evox_set_generation": ([P, i64], i32),
             "evox_row_layout": ([i32, i64, P, P], i32),
             "evox_default_ldx": ([i32, i64], i64),
             "evox_fill_normal": ([u64, i64, i64, i64, ctypes.c_float, ctypes.c_float, P, P], i32),
@@ -323,6 +325,9 @@ class Swarm:
     @property
     def t(self):
         return int(lib().evox_generation(self.handle))
+
+    def set_generation(self, t):
+        _check(lib().evox_set_generation(self.handle, t))
 
     def step(self, n_gens=1):
         if self.P.algo == PSO:

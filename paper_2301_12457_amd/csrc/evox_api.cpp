@@ -996,6 +996,14 @@ int evox_best(evox_state *s, float *best_fit, int64_t *best_idx, float *best_x_h
 
 int64_t evox_generation(const evox_state *s) { return s ? s->t : -1; }
 
+int evox_set_generation(evox_state *s, int64_t t)
+{
+    if (!s) return fail(EVOX_EINVAL, "state is null");
+    if (t < 0 || t >= ((int64_t)1 << 32)) return fail(EVOX_EINVAL, "t = %lld out of range [0, 2^32)", (long long)t);
+    s->t = t;
+    return EVOX_OK;
+}
+
 int evox_row_layout(int32_t kernels, int64_t D, int32_t *threads_per_row, int32_t *chunks_per_thread)
 {
     static const int family[3] = {LAYOUT_PSO, LAYOUT_CSO, LAYOUT_EVAL};

@@ -98,3 +98,25 @@ def normal_matrix_np(N, D, mu, sigma, seed):
     import numpy as np
     rng = np.random.default_rng(seed)
     return rng.normal(mu, sigma, size=(N, D)).astype(np.float32)
+
+
+def swarm_state_np(N, D, lb, ub, seed, spread, chunk=16384):
+    """Seeded positions, velocities and personal bests shaped like a swarm
+    part-way through a run: every individual near one common point
+    c ~ U[lb, ub]^D, with s = spread * (ub - lb),
+        x = c + s e1,   p = x + (s / 2) e2,   v = (s / 10) e3,
+    e_k standard normal; float32 [N, D] each, drawn chunk by chunk so that
+    large populations need no float64 temporaries."""
+    import numpy as np
+    rng = np.random.default_rng(seed)
+    c = rng.uniform(lb, ub, size=D).astype(np.float32)
+    s = np.float32(spread * (ub - lb))
+    x = np.empty((N, D), np.float32)
+    p = np.empty((N, D), np.float32)
+    v = np.empty((N, D), np.float32)
+    for a in range(0, N, chunk):
+        b = min(N, a + chunk)
+        x[a:b] = c + s * rng.standard_normal((b - a, D), dtype=np.float32)
+        p[a:b] = x[a:b] + (s / 2) * rng.standard_normal((b - a, D), dtype=np.float32)
+        v[a:b] = (s / 10) * rng.standard_normal((b - a, D), dtype=np.float32)
+    return x, v, p

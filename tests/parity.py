@@ -89,3 +89,21 @@ def normal_tol(x_ref, mu, sigma):
     z = np.abs(x_ref - mu) / sigma if sigma else np.zeros_like(x_ref)
     ulp = np.spacing(np.abs(x_ref).astype(np.float32)).astype(np.float64)
     return abs(sigma) * 1e-6 * np.maximum(1.0, z) + ulp
+
+
+def cso_lockstep(ref, g, r, what):
+    """One CSO generation on both sides from the same swarm mean.
+
+    The GPU sums the mean in fp64 in another order than the oracle; both
+    round once to fp32, so the two agree within 1 ulp (checked here) and
+    almost always exactly.  So that every generation compares the loser
+    update bit for bit, the oracle's mean is then written into the GPU
+    state's xbar, which the generation kernel reads."""
+    import torch
+    D = r.P.D
+    xbar = ref.colmean(r.x)
+    own = g.xbar[:D].cpu().numpy()
+    assert ulp_diff(own, xbar).max() <= 1, f"{what}: the GPU's swarm mean is more than 1 ulp off"
+    g.xbar[:D] = torch.from_numpy(xbar).to(g.xbar.device)
+    g.step(1)
+    r.step(1)

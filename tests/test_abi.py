@@ -179,4 +179,5 @@ def test_null_state_is_rejected(evox):
     assert L.evox_pgpe_step(None, 1) == evox.EINVAL
     assert L.evox_best(None, None, None, None) == evox.EINVAL
     assert L.evox_generation(None) == -1
+    assert L.evox_set_generation(None, 5) == evox.EINVAL
     assert L.evox_strerror(evox.ENOSPC).decode() == "scratch buffer too small"

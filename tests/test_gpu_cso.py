@@ -2,14 +2,16 @@
 
 The pairing permutation is integer work and must match exactly; the loser
 update is bit-exact given the same swarm mean; the mean itself is an fp64 sum
-in a different order on each side and must agree to 1 ulp; fitness within
+in a different order on each side and must agree to 1 ulp; so that every
+generation is compared bit for bit, the single-generation tests give the
+GPU the oracle's mean before each step (parity.cso_lockstep); fitness within
 the fitness tolerance; the reported best index exactly.
 """
 import numpy as np
 import pytest
 import torch
 
-from parity import assert_fitness, index_ok, ulp_diff
+from parity import assert_fitness, cso_lockstep, index_ok, ulp_diff
 
 pytestmark = pytest.mark.gpu
 
@@ -24,13 +26,12 @@ def host(t, D):
     return t[..., :D].cpu().numpy()
 
 
-def compare(g, r, fn, what, strict=True):
+def compare(g, r, fn, what):
     D = r.P.D
     x, v, f = host(g.x, D), host(g.v, D), g.fit.cpu().numpy()
-    if strict:
-        bad = np.nonzero((x != r.x).any(1))[0]
-        assert bad.size == 0, f"{what}: x differs in rows {bad[:8]}"
-        assert np.array_equal(v, r.v), f"{what}: v differs"
+    bad = np.nonzero((x != r.x).any(1))[0]
+    assert bad.size == 0, f"{what}: x differs in rows {bad[:8]}"
+    assert np.array_equal(v, r.v), f"{what}: v differs"
     assert_fitness(fn, r.x, f, r.fit, f"{what}: fit")
     bf, bi = g.best()
     if r.t > 0:
@@ -68,15 +69,9 @@ def test_generations_match_oracle(evox_gpu, ref, case):
     print(f"cso {c} gens={gens}", flush=True)
     g, r = pair(evox_gpu, ref, **c)
     for t in range(gens):
-        xbar_ref = ref.colmean(r.x)
-        assert ulp_diff(host(g.xbar, c["D"]), xbar_ref).max() <= 1, f"generation {t}: mean"
-        strict = np.array_equal(host(g.xbar, c["D"]), xbar_ref)
-        g.step(1)
-        r.step(1)
-        compare(g, r, c["fn"], f"generation {t}", strict=strict)
-        if not strict:   # a 1-ulp mean difference moves the losers slightly: stop here
-            break
-    assert g.t == r.t
+        cso_lockstep(ref, g, r, f"generation {t}")
+        compare(g, r, c["fn"], f"generation {t}")
+    assert g.t == r.t == gens
 
 
 def test_winners_untouched_and_losers_counted(evox_gpu, ref):
@@ -142,16 +137,11 @@ def test_pitched_states_match_oracle(evox_gpu, ref, D, ldx):
     r = ref.CSO(ref.make_params(fn, N, D, -600.0, 600.0, seed=9))
     assert g.P.ldx == ldx and g.x.shape[1] == ldx
     for t in range(gens):
-        xbar_ref = ref.colmean(r.x)
-        strict = np.array_equal(host(g.xbar, D), xbar_ref)
-        g.step(1)
-        r.step(1)
-        compare(g, r, fn, f"generation {t}", strict=strict)
+        cso_lockstep(ref, g, r, f"generation {t}")
+        compare(g, r, fn, f"generation {t}")
         for name in ("x", "v", "xbar"):
             pad = getattr(g, name)[..., D:]
             assert int((pad != 0).sum()) == 0, f"{name} padding written at generation {t}"
-        if not strict:
-            break
 
 
 def test_default_pitch_is_line_aligned(evox_gpu, ref):
@@ -180,7 +170,7 @@ def test_neighbourhood_version_matches_oracle(evox_gpu, ref, case):
     for t in range(gens):
         g.step(1)
         r.step(1)
-        compare(g, r, c["fn"], f"generation {t}", strict=True)
+        compare(g, r, c["fn"], f"generation {t}")
     assert g.t == r.t
 
 
@@ -194,7 +184,7 @@ def test_neighbourhood_version_several_generations_per_call(evox_gpu, ref):
     for n in (2, 3, 4):
         g.step(n)
         r.step(n)
-        compare(g, r, c["fn"], f"after a call of {n}", strict=True)
+        compare(g, r, c["fn"], f"after a call of {n}")
         assert not g.x[:, c["D"]:].any(), "padding columns must stay zero"
 
 

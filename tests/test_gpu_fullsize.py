@@ -4,15 +4,17 @@ benchmark times (the same library calls, grid and row layout).
 The oracle is single-threaded (about 30 ns per element and generation), so
 the PSO / CSO workloads are compared over their first generations (every
 element, bit for bit: 40 of the Ackley 1e4 x 1e3 run, 4 of the Rastrigin
-1e5 x 1e3 run, 3 of the CSO 1e6 x 100 run) rather than the whole run; the
-evaluation-only workload is compared on every row.  The CSO neighbourhood
-version is compared over 3 generations of its 1e6 x 100 run.
+1e5 x 1e3 run, 3 of the CSO 1e6 x 100 run) rather than the whole run, and
+at middle and last generation indices from pushed states in
+test_gpu_late.py; the evaluation-only workload is compared on every row.
+The CSO neighbourhood version is compared over 3 generations of its
+1e6 x 100 run.
 """
 import numpy as np
 import pytest
 import torch
 
-from parity import assert_fitness, index_ok, ulp_diff
+from parity import assert_fitness, cso_lockstep, index_ok
 
 from paper_2301_12457_amd.workloads import WORKLOADS, normal_matrix_torch
 
@@ -37,8 +39,17 @@ def test_pso_workload_first_generations(evox_gpu, ref, name, gens):
     print(f"{name}: {gens} generations", flush=True)
     g, r, fn = swarm_pair(evox_gpu, ref, w)
     D = w.D
+    g.profile(True)
     g.step(gens)
-    r.step(gens)
+    improved = 0
+    for _ in range(gens):
+        pf0 = r.pf.copy()
+        r.step(1)
+        improved += int((r.pf < pf0).sum())
+    # the improved-row counter of the generation kernels, which the
+    # benchmark's byte count uses, in the benchmark's launch configuration
+    assert g.profile_read()[2] == improved
+    g.profile(False)
     assert np.array_equal(g.x[:, :D].cpu().numpy(), r.x)
     assert np.array_equal(g.v[:, :D].cpu().numpy(), r.v)
     assert np.array_equal(g.pbest[:, :D].cpu().numpy(), r.p)
@@ -48,27 +59,21 @@ def test_pso_workload_first_generations(evox_gpu, ref, name, gens):
 
 
 def test_cso_workload_first_generations(evox_gpu, ref):
+    """Every generation compared bit for bit (x, v) from the same swarm mean
+    (parity.cso_lockstep: the GPU's own mean within 1 ulp of the oracle's,
+    then the oracle's given to both sides)."""
     w = WORKLOADS["cso_griewank_1e6x100"]
     g, r, fn = swarm_pair(evox_gpu, ref, w)
     D = w.D
     assert np.array_equal(g.x[:, :D].cpu().numpy(), r.x)
     for t in range(3):
-        xbar = ref.colmean(r.x)
-        assert ulp_diff(g.xbar[:D].cpu().numpy(), xbar).max() <= 1, f"generation {t}: mean"
-        exact_mean = np.array_equal(g.xbar[:D].cpu().numpy(), xbar)
-        g.step(1)
-        r.step(1)
-        x = g.x[:, :D].cpu().numpy()
-        if exact_mean:
-            assert np.array_equal(x, r.x), f"generation {t}: x"
-            assert np.array_equal(g.v[:, :D].cpu().numpy(), r.v), f"generation {t}: v"
-        else:
-            assert np.allclose(x, r.x, rtol=1e-5, atol=1e-3)
+        cso_lockstep(ref, g, r, f"generation {t}")
+        assert np.array_equal(g.x[:, :D].cpu().numpy(), r.x), f"generation {t}: x"
+        assert np.array_equal(g.v[:, :D].cpu().numpy(), r.v), f"generation {t}: v"
         assert_fitness(fn, r.x, g.fit.cpu().numpy(), r.fit, f"generation {t}: fit")
         bf, bi = g.best()
         assert index_ok(fn, r.x, r.fit, bi, r.best_idx)
-        if not exact_mean:   # a 1-ulp mean difference moves the losers slightly: stop here
-            break
+        assert bi == r.best_idx, f"generation {t}: best index {bi} vs {r.best_idx} (tolerance tie)"
 
 
 def test_cso_neighbourhood_workload_first_generations(evox_gpu, ref):

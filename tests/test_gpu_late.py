@@ -1,0 +1,198 @@
+"""Lockstep at the full benchmark sizes and late generation indices.
+
+A run of hundreds of generations cannot be replayed by the single-threaded
+oracle, so the tests push one seeded state to both sides (positions,
+velocities and personal bests shaped like a swarm part-way through its run,
+from the shared input generator; personal-best fitness and CSO fitness from
+the oracle, so both sides see the same values), set the generation index to
+a middle or the last generation of the workload (every Philox counter carries
+it), run the same generations on both and compare (the parity protocol of
+the loop of Eq. (1)-(3): bit-exact rows wherever the decisions agree).
+
+The states are separated from fitness near-ties: a particle whose personal
+best is within 1e-4 relative of its current fitness gets a personal best
+further away (deterministically), so every improvement decision of the
+pushed generation has a margin far above the fp32 evaluation error and both
+sides must take the same one.  The PSO two-generation tests also run the
+fused kernel (move of t, evaluation of t + 1); the decisions of generation
+t + 1 are made on each side's own fitness, so a differing decision is
+accepted only as a tolerance tie and its row is excluded from the bit-exact
+comparison (the count is printed).
+"""
+import numpy as np
+import pytest
+import torch
+
+from parity import assert_fitness, index_ok, tol, ulp_diff
+
+from paper_2301_12457_amd.workloads import WORKLOADS, swarm_state_np
+
+pytestmark = pytest.mark.gpu
+
+MARGIN = 1e-4
+
+
+def params(evox, ref, w):
+    fn = evox.FN_IDS[w.fn]
+    kw = dict(v_lo=w.v_lo, v_hi=w.v_hi, w=w.w, c1=w.c1, c2=w.c2, phi=w.phi, vmax=w.vmax, seed=w.seed)
+    algo = {"pso": evox.PSO, "cso": evox.CSO}[w.algo]
+    return fn, evox.make_params(algo, fn, w.N, w.D, w.lb, w.ub, **kw), ref.make_params(fn, w.N, w.D, w.lb,
+                                                                                          w.ub, **kw)
+
+
+def separated_pso_state(ref, fn, w, seed, spread):
+    """x, v, p, pf with every |F(x) - pf| above MARGIN relative, and the best
+    of min(F(x), pf) apart from the second best by as much (a converged swarm
+    has many nearly equal candidates: the leader's personal best is moved
+    halfway to the origin, the optimum of the workloads' functions, until it
+    leads clearly)."""
+    x, v, p = swarm_state_np(w.N, w.D, w.lb, w.ub, seed, spread)
+    fx = ref.evaluate(fn, x).astype(np.float64)
+    pf = ref.evaluate(fn, p)
+    for _ in range(8):
+        gap = np.abs(fx - pf.astype(np.float64))
+        near = np.nonzero(gap <= MARGIN * np.maximum(np.abs(fx), np.abs(pf)))[0]
+        if near.size == 0:
+            break
+        # move the personal best twice as far from x along the same direction
+        p[near] = p[near] + (p[near] - x[near])
+        pf[near] = ref.evaluate(fn, p[near])
+    else:
+        raise AssertionError("could not separate the personal bests")
+    for _ in range(32):
+        cand = np.minimum(fx, pf.astype(np.float64))
+        a, b = np.argsort(cand, kind="stable")[:2]
+        if cand[b] - cand[a] > MARGIN * abs(cand[a]):
+            break
+        p[a] = p[a] * np.float32(0.5)
+        pf[a] = ref.evaluate(fn, p[a:a + 1])[0]
+    else:
+        raise AssertionError("no clear leader")
+    assert abs(fx[a] - pf[a]) > MARGIN * max(abs(fx[a]), abs(pf[a]))
+    return x, v, p, pf
+
+
+def push_pso(evox, g, r, t, x, v, p, pf):
+    D = x.shape[1]
+    g.x[:, :D] = torch.from_numpy(x).cuda()
+    g.v[:, :D] = torch.from_numpy(v).cuda()
+    g.pbest[:, :D] = torch.from_numpy(p).cuda()
+    g.pfit.copy_(torch.from_numpy(pf).cuda())
+    g.set_generation(t)
+    r.x[:] = x
+    r.v[:] = v
+    r.p[:] = p
+    r.pf[:] = pf
+    r.t = t
+
+
+LATE_PSO = [("pso_ackley_1e4x1e3", 500, 0.05), ("pso_ackley_1e4x1e3", 999, 0.005),
+            ("pso_rastrigin_1e5x1e3", 100, 0.05), ("pso_rastrigin_1e5x1e3", 199, 0.005)]
+
+
+@pytest.mark.parametrize("name,t,spread", LATE_PSO, ids=[f"{n}-t{t}" for n, t, _ in LATE_PSO])
+def test_pso_one_generation_late(evox_gpu, ref, name, t, spread):
+    """Generation t from a pushed state: evaluation, personal bests, global
+    best, move -- every row bit for bit."""
+    w = WORKLOADS[name]
+    print(f"{name}: generation {t} from a pushed state (spread {spread})", flush=True)
+    fn, gp, rp = params(evox_gpu, ref, w)
+    x, v, p, pf = separated_pso_state(ref, fn, w, 1000 + t, spread)
+    g, r = evox_gpu.Swarm(gp), ref.PSO(rp)
+    push_pso(evox_gpu, g, r, t, x, v, p, pf)
+    g.step(1)
+    r.step(1)
+    D = w.D
+    assert g.t == r.t == t + 1
+    assert np.array_equal(g.pbest[:, :D].cpu().numpy(), r.p), "pbest"
+    assert np.array_equal(g.x[:, :D].cpu().numpy(), r.x), "x"
+    assert np.array_equal(g.v[:, :D].cpu().numpy(), r.v), "v"
+    assert_fitness(fn, r.p, g.pfit.cpu().numpy(), r.pf, f"{name} t={t}: pfit")
+    gf, gi, gx = g.best(with_x=True)
+    assert gi == r.gi, f"global best {gi} vs {r.gi}"
+    assert np.array_equal(gx, r.g)
+
+
+@pytest.mark.parametrize("name,t,spread", LATE_PSO, ids=[f"{n}-t{t}" for n, t, _ in LATE_PSO])
+def test_pso_two_generations_late(evox_gpu, ref, name, t, spread):
+    """Generations t - 1 and t in one call (so the fused kernel moves t - 1
+    and evaluates t); rows whose generation-t decision differs between the
+    two sides must be tolerance ties and are left out of the bit-exact
+    comparison, every other row is compared bit for bit."""
+    w = WORKLOADS[name]
+    t0 = t - 1
+    print(f"{name}: generations {t0}, {t} from a pushed state (spread {spread})", flush=True)
+    fn, gp, rp = params(evox_gpu, ref, w)
+    x, v, p, pf = separated_pso_state(ref, fn, w, 2000 + t, spread)
+    g, r = evox_gpu.Swarm(gp), ref.PSO(rp)
+    push_pso(evox_gpu, g, r, t0, x, v, p, pf)
+    g.profile(True)
+    g.step(2)
+    r.step(1)
+    pf_mid, x_mid = r.pf.copy(), r.x.copy()
+    f_mid = ref.evaluate(fn, x_mid)        # the oracle's fitness of x_t
+    imp_mid_ref = int((f_mid < pf_mid).sum())
+    imp0_ref = int((pf_mid < pf).sum())
+    r.step(1)
+    D = w.D
+    pg = g.pbest[:, :D].cpu().numpy()
+    same = (pg == r.p).all(1)
+    diff = np.nonzero(~same)[0]
+    ties = np.abs(f_mid[diff].astype(np.float64) - pf_mid[diff]) <= tol(fn, x_mid[diff], pf_mid[diff])
+    assert ties.all(), f"rows {diff[~ties][:8]} decided differently without a tolerance tie"
+    print(f"{name} t={t}: {diff.size} tolerance ties in the personal-best decisions", flush=True)
+    _, _, improved = g.profile_read()
+    g.profile(False)
+    assert abs(improved - (imp0_ref + imp_mid_ref)) <= diff.size, "improved-row counter"
+    gf, gi, gx = g.best(with_x=True)
+    assert index_ok(fn, r.p, r.pf, gi, r.gi), f"global best {gi} vs {r.gi}"
+    assert_fitness(fn, r.p, g.pfit.cpu().numpy(), r.pf, f"{name} t={t}: pfit")
+    if gi == r.gi:
+        assert np.array_equal(gx, r.g)
+        xg, vg = g.x[:, :D].cpu().numpy(), g.v[:, :D].cpu().numpy()
+        assert np.array_equal(xg[same], r.x[same]), "x"
+        assert np.array_equal(vg[same], r.v[same]), "v"
+    else:
+        print(f"{name} t={t}: global best a tolerance tie ({gi} vs {r.gi})", flush=True)
+
+
+LATE_CSO = [(100, 0.05), (199, 0.005)]
+
+
+@pytest.mark.parametrize("t,spread", LATE_CSO, ids=[f"t{t}" for t, _ in LATE_CSO])
+def test_cso_one_generation_late(evox_gpu, ref, t, spread):
+    """CSO generation t of the 1e6 x 100 Griewank workload from a pushed
+    state (fitness from the oracle, so the pair decisions see identical
+    values): the pairing of generation t, every loser's move bit for bit
+    (with the oracle's swarm mean given to both sides; the GPU's own mean of
+    the pushed rows within 1 ulp of it), fitness within the tolerance, the
+    best index exactly."""
+    w = WORKLOADS["cso_griewank_1e6x100"]
+    print(f"{w.name}: generation {t} from a pushed state (spread {spread})", flush=True)
+    fn, gp, rp = params(evox_gpu, ref, w)
+    x, v, _ = swarm_state_np(w.N, w.D, w.lb, w.ub, 3000 + t, spread)
+    f = ref.evaluate(fn, x)
+    g, r = evox_gpu.Swarm(gp), ref.CSO(rp)
+    D = w.D
+    g.x[:, :D] = torch.from_numpy(x).cuda()
+    g.v[:, :D] = torch.from_numpy(v).cuda()
+    g.fit.copy_(torch.from_numpy(f).cuda())
+    g.set_generation(t)
+    g.refresh(refit=False)
+    r.x[:] = x
+    r.v[:] = v
+    r.fit[:] = f
+    r.t = t
+    xbar = ref.colmean(r.x)
+    assert ulp_diff(g.xbar[:D].cpu().numpy(), xbar).max() <= 1, "swarm mean"
+    g.xbar[:D] = torch.from_numpy(xbar).cuda()
+    g.step(1)
+    r.step(1)
+    assert g.t == r.t == t + 1
+    assert np.array_equal(g.x[:, :D].cpu().numpy(), r.x), "x"
+    assert np.array_equal(g.v[:, :D].cpu().numpy(), r.v), "v"
+    assert not g.x[:, D:].any() and not g.v[:, D:].any(), "padding"
+    assert_fitness(fn, r.x, g.fit.cpu().numpy(), r.fit, f"t={t}: fit")
+    bf, bi = g.best()
+    assert index_ok(fn, r.x, r.fit, bi, r.best_idx)
+    assert bi == r.best_idx, f"best index {bi} vs {r.best_idx} (tolerance tie)"

@@ -132,3 +132,31 @@ def test_padding_columns_stay_zero(evox_gpu, ref, D, ldx):
             assert np.all(t[:, D:] == 0), name
         assert np.all(g.gbest[D:].cpu().numpy() == 0)
         compare_state(g, r, 2, f"D {D} ldx {ldx}")
+
+
+COUNTER_CASES = [dict(fn=0, N=100, D=10, seed=0, lb=-32.0, ub=32.0, gens=100),
+                 dict(fn=2, N=257, D=100, seed=2, lb=-5.12, ub=5.12, vmax=2.048, gens=30),
+                 dict(fn=1, N=64, D=1000, seed=1, lb=-32.768, ub=32.768, v_lo=-1.0, v_hi=1.0, gens=12)]
+
+
+@pytest.mark.parametrize("case", COUNTER_CASES, ids=[f"fn{c['fn']}-{c['N']}x{c['D']}" for c in COUNTER_CASES])
+def test_improved_row_counter_matches_oracle(evox_gpu, ref, case):
+    """The generation kernels count the rows whose personal best improved
+    (the pbest rows rewritten, part of the bytes the benchmark reports); over
+    one call of `gens` generations the count equals the oracle's number of
+    rows whose pfit fell, generation by generation."""
+    c = dict(case)
+    gens = c.pop("gens")
+    g, r = pair(evox_gpu, ref, **c)
+    expected = []
+    for _ in range(gens):
+        pf0 = r.pf.copy()
+        r.step(1)
+        expected.append(int((r.pf < pf0).sum()))
+    g.profile(True)
+    g.step(gens)
+    ms, launches, improved = g.profile_read()
+    g.profile(False)
+    compare_state(g, r, c["fn"], f"after {gens}")
+    assert launches == gens - 1              # the fused launches timed
+    assert improved == sum(expected), (improved, sum(expected), expected[:5])

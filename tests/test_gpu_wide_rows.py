@@ -6,7 +6,7 @@ import numpy as np
 import pytest
 import torch
 
-from parity import assert_fitness, tol
+from parity import assert_fitness, cso_lockstep, tol
 
 pytestmark = pytest.mark.gpu
 
@@ -34,12 +34,9 @@ def test_cso_wide(evox_gpu, ref, D):
     g = evox_gpu.Swarm(evox_gpu.make_params(evox_gpu.CSO, 3, 9, D, -600.0, 600.0, seed=D))
     r = ref.CSO(ref.make_params(3, 9, D, -600.0, 600.0, seed=D))
     for t in range(3):
-        exact = np.array_equal(g.xbar[:D].cpu().numpy(), ref.colmean(r.x))
-        g.step(1)
-        r.step(1)
-        if not exact:
-            break
+        cso_lockstep(ref, g, r, f"cso D {D} generation {t}")
         assert np.array_equal(g.x[:, :D].cpu().numpy(), r.x), t
+        assert np.array_equal(g.v[:, :D].cpu().numpy(), r.v), t
         assert_fitness(3, r.x, g.fit.cpu().numpy(), r.fit, f"cso D {D}")
 
 
