@@ -193,6 +193,21 @@ int evox_eval_argmin(int fn_id, const float *X, int64_t N, int64_t D, int64_t ld
                      float *best_fit_dev, int64_t *best_idx_dev, void *scratch,
                      size_t scratch_bytes, void *hip_stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): evox_eval_argmin
+ * without a scratch argument.  Its selection slots live in a device array of
+ * the library (EVOX_NOALLOC_SCRATCH_BYTES, 32 KiB, one copy per device, held
+ * until the process ends); the call allocates nothing (no hipMalloc, hipFree
+ * or allocating library routine) and resets the slots it uses with a kernel
+ * before the evaluation.  Every call on a device shares that device's array:
+ * calls that overlap on one device (concurrent streams or threads) race and
+ * give wrong results.  The caller's current device must be the device of
+ * hip_stream (EVOX_EINVAL otherwise); N, D, ldx as evox_eval_argmin, which
+ * also gives the same results bit for bit. */
+#define EVOX_NOALLOC_SCRATCH_BYTES 32768
+int evox_eval_argmin_noalloc(int fn_id, const float *X, int64_t N, int64_t D, int64_t ldx, float *out,
+                             float *best_fit_dev, int64_t *best_idx_dev, void *hip_stream);
+
 /* Workflow.step x n_gens for PSO (Sec. IV-A, Table I; Eq. (1)-(3)).  One
  * generation t: evaluate x (fitness f); where f_i < pfit_i strictly, pbest_i =
  * x_i and pfit_i = f_i; the global best is the minimum of pfit in the argmin

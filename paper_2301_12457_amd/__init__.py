@@ -22,7 +22,8 @@ MAX_D = 32768
 # every symbol include/evox.h declares
 EXPORTS = (
     "evox_scratch_bytes", "evox_state_create", "evox_state_destroy", "evox_eval", "evox_eval_ld",
-    "evox_eval_argmin_scratch_bytes", "evox_eval_argmin", "evox_pso_step", "evox_cso_step",
+    "evox_eval_argmin_scratch_bytes", "evox_eval_argmin", "evox_eval_argmin_noalloc", "evox_pso_step",
+    "evox_cso_step",
     "evox_de_step", "evox_es_step", "evox_pgpe_step", "evox_maes_step", "evox_nsga2_step",
     "evox_nsga2_sort_scratch_bytes", "evox_nsga2_sort",
     "evox_cso_refresh", "evox_best", "evox_generation", "evox_set_generation", "evox_row_layout",
@@ -85,6 +86,7 @@ def lib():
             "evox_eval_ld": ([i32, P, i64, i64, i64, P, P], i32),
             "evox_eval_argmin_scratch_bytes": ([i64], sz),
             "evox_eval_argmin": ([i32, P, i64, i64, i64, P, P, P, P, sz, P], i32),
+            "evox_eval_argmin_noalloc": ([i32, P, i64, i64, i64, P, P, P, P], i32),
             "evox_pso_step": ([P, i64], i32),
             "evox_cso_step": ([P, i64], i32),
             "evox_de_step": ([P, i64], i32),
@@ -164,6 +166,13 @@ def evox_eval_argmin(fn_id, X, N, D, ldx, out, best_fit, best_idx, scratch, stre
     _check(lib().evox_eval_argmin(fn_id, _ptr(X), N, D, ldx, _ptr(out), _ptr(best_fit),
                                   _ptr(best_idx), _ptr(scratch), scratch.numel() * scratch.element_size(),
                                   _stream(stream)))
+    return out
+
+
+def evox_eval_argmin_noalloc(fn_id, X, N, D, ldx, out, best_fit, best_idx, stream=None):
+    """evox_eval_argmin with the library's static per-device scratch (no allocation)."""
+    _check(lib().evox_eval_argmin_noalloc(fn_id, _ptr(X), N, D, ldx, _ptr(out), _ptr(best_fit),
+                                          _ptr(best_idx), _stream(stream)))
     return out
 
 

@@ -9,6 +9,7 @@
 #include <cstdio>
 #include <cstring>
 #include <limits>
+#include <mutex>
 #include <utility>
 #include <vector>
 
@@ -713,6 +714,75 @@ int evox_eval_argmin(int fn_id, const float *X, int64_t N, int64_t D, int64_t ld
     if (rc != EVOX_OK) return rc;
     e = launch_select(slots, nullptr, 0, nullptr, nullptr, best_fit_dev, best_idx_dev, st);
     if (e != hipSuccess) return hip_fail(e, "select");
+    return EVOX_OK;
+}
+
+}  // extern "C"
+
+namespace {
+
+// Scratch of evox_eval_argmin_noalloc: the selection slots, one copy per
+// device.  Host code never uses this name as an address: the device's own
+// address comes from hipGetSymbolAddress, once per device.
+static __device__ __align__(256) unsigned char scratch[EVOX_NOALLOC_SCRATCH_BYTES];
+static_assert(sizeof(SelSlots) <= EVOX_NOALLOC_SCRATCH_BYTES, "selection slots fit the static scratch");
+
+constexpr int kMaxDevices = 64;
+std::mutex g_noalloc_mu;
+void *g_noalloc_ptr[kMaxDevices] = {};
+
+// The static scratch's address on device `dev` (the current device).
+int noalloc_scratch(int dev, void **out)
+{
+    if (dev < 0 || dev >= kMaxDevices) return fail(EVOX_EINVAL, "device %d beyond the %d supported", dev, kMaxDevices);
+    std::lock_guard<std::mutex> lock(g_noalloc_mu);
+    if (!g_noalloc_ptr[dev]) {
+        void *p = nullptr;
+        const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return hip_fail(e, "address of the static scratch");
+        if (!p) return fail(EVOX_EHIP, "address of the static scratch is null");
+        g_noalloc_ptr[dev] = p;
+    }
+    *out = g_noalloc_ptr[dev];
+    return EVOX_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int evox_eval_argmin_noalloc(int fn_id, const float *X, int64_t N, int64_t D, int64_t ldx, float *out,
+                             float *best_fit_dev, int64_t *best_idx_dev, void *hip_stream)
+{
+    if (N < 1 || N >= ((int64_t)1 << 31))
+        return fail(EVOX_EINVAL, "N = %lld out of range [1, 2^31) for a selection", (long long)N);
+    if (!best_fit_dev || !best_idx_dev) return fail(EVOX_EINVAL, "best outputs are required");
+    const size_t need = evox_eval_argmin_scratch_bytes(N);
+    if (need > EVOX_NOALLOC_SCRATCH_BYTES)
+        return fail(EVOX_ENOSPC, "N = %lld needs %zu scratch bytes, the static scratch holds %d", (long long)N, need,
+                    EVOX_NOALLOC_SCRATCH_BYTES);
+    hipStream_t st = (hipStream_t)hip_stream;
+    // validate before enqueueing anything
+    int rc = eval_common(fn_id, nullptr, 0, D, ldx, nullptr, nullptr, st);
+    if (rc != EVOX_OK) return rc;
+    if (!X || !out) return fail(EVOX_EINVAL, "X and out are required");
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_fail(e, "current device");
+    if (st) {
+        hipDevice_t sdev = -1;
+        if ((e = hipStreamGetDevice(st, &sdev)) != hipSuccess) return hip_fail(e, "device of the stream");
+        if ((int)sdev != dev)
+            return fail(EVOX_EINVAL, "the stream belongs to device %d, the current device is %d", (int)sdev, dev);
+    }
+    void *ptr = nullptr;
+    if ((rc = noalloc_scratch(dev, &ptr)) != EVOX_OK) return rc;
+    SelSlots *slots = static_cast<SelSlots *>(ptr);
+    if ((e = launch_slots_init(slots, st)) != hipSuccess) return hip_fail(e, "select init");
+    rc = eval_common(fn_id, X, N, D, ldx, out, slots, st);
+    if (rc != EVOX_OK) return rc;
+    if ((e = launch_select(slots, nullptr, 0, nullptr, nullptr, best_fit_dev, best_idx_dev, st)) != hipSuccess)
+        return hip_fail(e, "select");
     return EVOX_OK;
 }
 

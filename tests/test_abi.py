@@ -180,4 +180,15 @@ def test_null_state_is_rejected(evox):
     assert L.evox_best(None, None, None, None) == evox.EINVAL
     assert L.evox_generation(None) == -1
     assert L.evox_set_generation(None, 5) == evox.EINVAL
+
+
+def test_noalloc_entry_point_validates_before_any_gpu_call(evox):
+    L = evox.lib()
+    f = ctypes.c_void_p(0x1000)
+    assert L.evox_eval_argmin_noalloc(0, f, 0, 10, 10, f, f, f, None) == evox.EINVAL    # N < 1
+    assert L.evox_eval_argmin_noalloc(9, f, 5, 10, 10, f, f, f, None) == evox.EINVAL    # fn_id
+    assert L.evox_eval_argmin_noalloc(0, f, 5, 10, 8, f, f, f, None) == evox.EINVAL     # ldx < D
+    assert L.evox_eval_argmin_noalloc(0, f, 5, 10, 10, f, None, f, None) == evox.EINVAL  # outputs
+    assert L.evox_eval_argmin_noalloc(0, None, 5, 10, 10, f, f, f, None) == evox.EINVAL  # X
+    assert "X and out are required" in L.evox_last_error().decode()
     assert L.evox_strerror(evox.ENOSPC).decode() == "scratch buffer too small"
