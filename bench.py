@@ -201,6 +201,37 @@ def copy_bandwidth(torch, evox, mib=1024, reps=5):
     return 2.0 * n * 4 / sec / 1e9
 
 
+def cso_data_floor(torch, evox, w, ldx, reps=5):
+    """The data-movement floor of the CSO generation on this GPU: the row
+    traffic of one swarm-mean generation alone (evox_pair_move: the winner
+    gathers and the losers' x and v, read and written, in the generation
+    kernel's traversal, with the pairs of generation 0 of the workload's
+    pairing), timed like the generation kernel.  Returns its average launch
+    duration and the algorithmic bytes per launch."""
+    N, D = w.N, w.D
+    perm = torch.empty(N, dtype=torch.int32, device="cuda")
+    scratch = torch.empty(evox.lib().evox_permutation_scratch_bytes(N, 1) // 4 + 64, dtype=torch.int32, device="cuda")
+    evox.evox_permutation(w.seed, 0, 1, N, perm, scratch)
+    p = perm.long()
+    pairs = N // 2
+    winner_of = torch.full((N,), -1, dtype=torch.int32, device="cuda")
+    winner_of[p[1::2][:pairs]] = p[0::2][:pairs].int()
+    x = torch.zeros((N, ldx), dtype=torch.float32, device="cuda")
+    v = torch.zeros_like(x)
+    evox.evox_pair_move(x, v, N, D, ldx, winner_of)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        evox.evox_pair_move(x, v, N, D, ldx, winner_of)
+    e1.record()
+    torch.cuda.synchronize()
+    us = e0.elapsed_time(e1) / reps * 1e3
+    del x, v, winner_of, perm, scratch
+    torch.cuda.empty_cache()
+    # rows: gather x_w, read x_l and v_l, write x_l and v_l; winner_of: 4 B per individual
+    return us, 20.0 * pairs * D + 4.0 * N
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -348,6 +379,12 @@ def main():
         copy = copy_bandwidth(torch, evox)
         roofline["copy_gbs"] = round(copy, 1)
         roofline["frac_of_copy"] = round(roofline["achieved"] / copy, 4)
+    if roofline is not None and w.algo == "cso" and not w.cso_local:
+        f_us, f_bytes = cso_data_floor(torch, evox, w, swarm.P.ldx)
+        roofline["data_floor"] = {"kernel": "k_pair_move (evox_pair_move)", "avg_launch_us": round(f_us, 2),
+                                  "algorithmic_bytes_per_launch": f_bytes,
+                                  "frac": round(f_bytes / (f_us / 1e6) / 1e9 / HBM_PEAK_GBS, 4),
+                                  "kernel_over_floor": round(roofline["avg_launch_us"] / f_us, 4)}
 
     base = None
     if not args.no_cpu_baseline:

@@ -418,8 +418,10 @@ int evox_argsort_u32(const uint32_t *keys, int64_t N, uint32_t *perm_out, void *
  * pays, else a multiple of 4.  PSO (rows streamed in order; its kernels also
  * write the padding so that row ends are whole lines): 32-multiples for
  * D >= 512, where the padding is at most ~6 %; DE, whose target rows are
- * streamed the same way, and ES / PGPE likewise.  CSO (rows gathered and
- * written at random; padding never touched): 32-multiples for D >= 64.
+ * streamed the same way, and ES / PGPE likewise.  CSO: D rounded up to a
+ * multiple of 4 (dense rows: the generation writes a random half of the rows
+ * in index order, and on the MI355X dense rows move faster than rows padded
+ * to whole lines: 1e6 x 100 generation kernel 242 against 252 us).
  * Returns the pitch, or 0 for an unknown algo or D outside [1, EVOX_MAX_D]. */
 int64_t evox_default_ldx(int32_t algo, int64_t D);
 
@@ -438,6 +440,20 @@ int evox_sgemm(int32_t trans_a, int32_t trans_b, int64_t M, int64_t N, int64_t K
  * i < n (device pointers, 16-byte aligned, not overlapping), streamed with
  * nontemporal 16-byte loads and stores.  n = 0 does nothing. */
 int evox_copy(const float *src, float *dst, int64_t n, void *hip_stream);
+
+/* Diagnostic, the data-movement floor of the CSO generation: the row traffic
+ * of one swarm-mean generation (Table II's CSO as evox_cso_step runs it) and
+ * nothing else.  For every i < N with winner_of[i] >= 0 (a loser; winner_of
+ * device int32 [N], each winner index < N, every index the winner of at most
+ * one loser and no loser a winner), in the generation kernel's traversal (row
+ * groups of the CSO layout of D, losers in index order): the winner's row is
+ * gathered, the loser's x and v are read, and v_i = v_i + (x_w - x_i), x_i =
+ * x_i + v_i are written (device x, v [N][ldx], 16-byte aligned, ldx % 4 == 0,
+ * padding columns zero).  No random numbers, fitness or swarm mean.  With the
+ * pairs of a real generation it times the accesses the generation kernel
+ * cannot avoid. */
+int evox_pair_move(float *x, float *v, int64_t N, int64_t D, int64_t ldx, const int32_t *winner_of,
+                   void *hip_stream);
 
 /* Diagnostic: out[4 k + m] = word m of Philox(seed, (k, c1, c2, c3)) for
  * k < n_ctr, computed by the device Philox the kernels use (device out). */

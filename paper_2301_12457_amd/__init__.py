@@ -28,7 +28,8 @@ EXPORTS = (
     "evox_nsga2_sort_scratch_bytes", "evox_nsga2_sort",
     "evox_cso_refresh", "evox_best", "evox_generation", "evox_set_generation", "evox_row_layout",
     "evox_default_ldx",
-    "evox_fill_normal", "evox_sgemm", "evox_copy", "evox_philox_fill", "evox_permutation_scratch_bytes",
+    "evox_fill_normal", "evox_sgemm", "evox_copy", "evox_pair_move", "evox_philox_fill",
+    "evox_permutation_scratch_bytes",
     "evox_permutation", "evox_argsort_u32",
     "evox_profile", "evox_profile_read", "evox_strerror", "evox_last_error",
 )
@@ -104,6 +105,7 @@ def lib():
             "evox_default_ldx": ([i32, i64], i64),
             "evox_fill_normal": ([u64, i64, i64, i64, ctypes.c_float, ctypes.c_float, P, P], i32),
             "evox_copy": ([P, P, i64, P], i32),
+            "evox_pair_move": ([P, P, i64, i64, i64, P, P], i32),
             "evox_sgemm": ([i32, i32, i64, i64, i64, ctypes.c_float, P, i64, P, i64, ctypes.c_float, P, i64, P],
                            i32),
             "evox_permutation_scratch_bytes": ([i64, i64], sz),
@@ -221,6 +223,11 @@ def evox_copy(src, dst, n, stream=None):
     """dst[:n] = src[:n] by the library's streaming copy (bandwidth reference)."""
     _check(lib().evox_copy(_ptr(src), _ptr(dst), n, _stream(stream)))
     return dst
+
+
+def evox_pair_move(x, v, N, D, ldx, winner_of, stream=None):
+    """The data movement of one swarm-mean CSO generation (diagnostic)."""
+    _check(lib().evox_pair_move(_ptr(x), _ptr(v), N, D, ldx, _ptr(winner_of), _stream(stream)))
 
 
 def evox_permutation(seed, t0, n_gens, N, perm_out, scratch, stream=None):

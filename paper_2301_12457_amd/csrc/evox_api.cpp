@@ -80,6 +80,7 @@ struct Plan {
     int perm_batch = 0;
     size_t x2 = 0, fit2 = 0;  // DE: the other population buffer and its fitness
     size_t xalt = 0;          // CSO neighbourhood version: the other population buffer
+    size_t mate = 0, cfit2 = 0;  // CSO swarm version: mate arrays, the other fitness buffer
     size_t esrank = 0, espart = 0;  // ES: sample ranks, gradient partial sums
     // MA-ES: deviates, steps, split-K workspace, update factors, parents,
     // weights, path-norm partial sums
@@ -200,11 +201,19 @@ int make_plan(const evox_params *P, Plan *pl)
     p.slots = take(sizeof(SelSlots));
     if (P->algo == EVOX_CSO) {
         const int cap = cso_grid_cap(P->ldx);
-        p.cso_grid = grid_for(P->N / 2 + (P->N & 1), p.L.G, cap);
+        const bool sweep = P->cso_local == 0;  // the swarm version sweeps ranges of individuals
+        if (sweep) {
+            int64_t ranges = (P->N + kCsoSweep - 1) / kCsoSweep;
+            p.cso_grid = (int)(ranges > cap ? cap : ranges);
+        } else {
+            p.cso_grid = grid_for(P->N / 2 + (P->N & 1), p.L.G, cap);
+        }
         p.colsum_grid = grid_for(P->N, p.L.G, cap);
         p.bits = perm_bits(P->N);
-        // permutations sorted kPermBatch generations at a time, within 256 MB
-        int64_t batch = ((int64_t)256 << 20) / (12 * P->N);
+        // permutations (and the swarm version's mate arrays) sorted
+        // kPermBatch generations at a time, within 256 MB
+        const int64_t per = sweep ? 16 : 12;
+        int64_t batch = ((int64_t)256 << 20) / (per * P->N);
         p.perm_batch = (int)(batch < 1 ? 1 : batch > kPermBatch ? kPermBatch : batch);
         const size_t B = (size_t)p.perm_batch, nb = (size_t)1 << p.bits;
         p.hist = take(4 * nb * B);
@@ -212,6 +221,10 @@ int make_plan(const evox_params *P, Plan *pl)
         p.cursor = take(4 * nb * B);
         p.tkv = take(8 * (size_t)P->N * B);
         p.perm = take(4 * (size_t)P->N * B);
+        if (sweep) {
+            p.mate = take(4 * (size_t)P->N * B);
+            p.cfit2 = take(sizeof(float) * (size_t)P->N);
+        }
         p.xsum_rows = cap;
         p.xsum = take(sizeof(double) * (size_t)cap * (size_t)P->ldx);
         p.s1 = take(sizeof(double) * (size_t)kMeanStages * (size_t)P->ldx);
@@ -284,6 +297,8 @@ struct evox_state {
     DevBest *best;
     SelSlots *slots;
     uint32_t *hist, *offs, *cursor, *perm, *ticket;
+    uint32_t *mate;    // CSO swarm version: mate arrays of the permutation batch
+    float *cfit2;      // CSO swarm version: the other fitness buffer
     uint2 *tkv;
     int64_t perm_t0;  // first generation of the stored permutation batch (-1: none)
     double *xsum, *s1;
@@ -446,7 +461,8 @@ int evox_state_create(const evox_params *params, const evox_buffers *b, void *hi
     s->k1 = (uint32_t)(P.seed >> 32);
     s->best = at<DevBest>(b->scratch, pl.best);
     s->slots = at<SelSlots>(b->scratch, pl.slots);
-    s->hist = s->offs = s->cursor = s->perm = nullptr;
+    s->hist = s->offs = s->cursor = s->perm = s->mate = nullptr;
+    s->cfit2 = nullptr;
     s->tkv = nullptr;
     s->xsum = s->s1 = nullptr;
     s->perm_t0 = -1;
@@ -534,6 +550,8 @@ int evox_state_create(const evox_params *params, const evox_buffers *b, void *hi
         s->cursor = at<uint32_t>(b->scratch, pl.cursor);
         s->tkv = at<uint2>(b->scratch, pl.tkv);
         s->perm = at<uint32_t>(b->scratch, pl.perm);
+        s->mate = P.cso_local ? nullptr : at<uint32_t>(b->scratch, pl.mate);
+        s->cfit2 = P.cso_local ? nullptr : at<float>(b->scratch, pl.cfit2);
         s->xsum = at<double>(b->scratch, pl.xsum);
         s->s1 = at<double>(b->scratch, pl.s1);
         s->ticket = at<uint32_t>(b->scratch, pl.ticket);
@@ -632,6 +650,8 @@ int evox_state_create(const evox_params *params, const evox_buffers *b, void *hi
             (e = launch_zero_u32(s->hist, (int64_t)nb, s->stream)) != hipSuccess ||
             (e = launch_zero_u32(s->cursor, (int64_t)nb, s->stream)) != hipSuccess ||
             (e = launch_zero_u32(s->ticket, (P.ldx + 63) / 64, s->stream)) != hipSuccess ||
+            // every mate entry is an index below N or kUnpaired at all times
+            (s->mate && (e = launch_fill_u32(s->mate, P.N * pl.perm_batch, kUnpaired, s->stream)) != hipSuccess) ||
             (e = best_init(s, std::numeric_limits<float>::infinity(), 0)) != hipSuccess) {
             delete s;
             return hip_fail(e, "init");
@@ -824,32 +844,40 @@ int evox_cso_step(evox_state *s, int64_t n_gens)
     if (s->t + n_gens >= ((int64_t)1 << 32)) return fail(EVOX_EINVAL, "generation counter would pass 2^32");
     const evox_params &P = s->P;
     const Plan &pl = s->pl;
+    const bool local = P.cso_local != 0;
     hipError_t e;
-    float *cur = s->B.x, *alt = P.cso_local ? at<float>(s->B.scratch, pl.xalt) : nullptr;
+    // the neighbourhood version alternates the positions between x and a
+    // second buffer; the swarm version alternates the fitness between fit and
+    // a second buffer (a generation reads every individual's fitness before
+    // it and writes every one after it)
+    float *cur = s->B.x, *alt = local ? at<float>(s->B.scratch, pl.xalt) : nullptr;
+    float *fcur = s->B.fit;
     for (int64_t k = 0; k < n_gens; ++k) {
         const int64_t t = s->t + k;
         if (s->perm_t0 < 0 || t < s->perm_t0 || t >= s->perm_t0 + pl.perm_batch) {
             PermArgs pa{P.N, pl.bits, s->k0, s->k1, (uint32_t)t, (uint32_t)pl.perm_batch, s->hist, s->offs,
-                        s->cursor, s->tkv, s->perm, nullptr};
+                        s->cursor, s->tkv, s->perm, nullptr, s->mate};
             if ((e = launch_perm(pa, s->stream)) != hipSuccess) return hip_fail(e, "pairing");
             s->perm_t0 = t;
         }
-        const uint32_t *perm = s->perm + (t - s->perm_t0) * P.N;
-        // the neighbourhood version reads the positions before the generation
-        // from one population buffer and writes the next into the other, so
-        // every loser's neighbours are still the old rows
-        float *src = cur, *dst = P.cso_local ? (cur == s->B.x ? alt : s->B.x) : s->B.x;
-        CsoArgs ca{dst, s->B.v, s->B.fit, s->B.xbar, perm, P.N, P.D, P.ldx, P.phi, P.lb, P.ub,
-                   P.clamp_x != 0, s->k0, s->k1, (uint32_t)t, s->slots, s->xsum, src};
+        const int64_t slice = (t - s->perm_t0) * P.N;
+        float *dst = local ? (cur == s->B.x ? alt : s->B.x) : s->B.x;
+        float *fnext = local ? s->B.fit : (fcur == s->B.fit ? s->cfit2 : s->B.fit);
+        CsoArgs ca{dst, s->B.v, fnext, fcur, s->B.xbar, s->perm + slice, local ? nullptr : s->mate + slice,
+                   P.N, P.D, P.ldx, P.phi, P.lb, P.ub, P.clamp_x != 0, s->k0, s->k1, (uint32_t)t, s->slots,
+                   s->xsum, cur};
         e = timed(s, [&] { return launch_cso(P.fn_id, pl.L, ca, pl.cso_grid, s->stream); });
         if (e != hipSuccess) return hip_fail(e, "cso generation");
         if ((e = launch_cso_mean(mean_args(s, pl.cso_grid), s->stream)) != hipSuccess)
             return hip_fail(e, "swarm mean");
         cur = dst;
+        fcur = fnext;
     }
-    // the caller's x holds the positions after the call
+    // the caller's x and fit hold the state after the call
     if (cur != s->B.x && (e = launch_stream_copy(cur, s->B.x, P.N * P.ldx, s->stream)) != hipSuccess)
         return hip_fail(e, "positions");
+    if (fcur != s->B.fit && (e = launch_stream_copy(fcur, s->B.fit, P.N, s->stream)) != hipSuccess)
+        return hip_fail(e, "fitness");
     s->t += n_gens;
     return EVOX_OK;
 }
@@ -1094,7 +1122,7 @@ int64_t evox_default_ldx(int32_t algo, int64_t D)
     if (algo == EVOX_PSO || algo == EVOX_DE || algo == EVOX_ES || algo == EVOX_PGPE || algo == EVOX_MAES ||
         algo == EVOX_NSGA2)
         return D >= 512 ? line : quad;
-    if (algo == EVOX_CSO) return D >= 64 ? line : quad;
+    if (algo == EVOX_CSO) return quad;
     return 0;
 }
 
@@ -1228,6 +1256,21 @@ int evox_copy(const float *src, float *dst, int64_t n, void *hip_stream)
     if (!aligned16(src) || !aligned16(dst)) return fail(EVOX_EALIGN, "src or dst is not 16-byte aligned");
     hipError_t e = launch_stream_copy(src, dst, n, (hipStream_t)hip_stream);
     if (e != hipSuccess) return hip_fail(e, "copy");
+    return EVOX_OK;
+}
+
+int evox_pair_move(float *x, float *v, int64_t N, int64_t D, int64_t ldx, const int32_t *winner_of,
+                   void *hip_stream)
+{
+    if (N < 2 || N > kCsoMaxN) return fail(EVOX_EINVAL, "N = %lld out of range [2, 2^24]", (long long)N);
+    if (D < 1 || D > EVOX_MAX_D) return fail(EVOX_EINVAL, "D = %lld out of range [1, %d]", (long long)D, EVOX_MAX_D);
+    if (ldx < D || (ldx & 3)) return fail(EVOX_EINVAL, "ldx = %lld must be >= D and a multiple of 4", (long long)ldx);
+    if (!x || !v || !winner_of) return fail(EVOX_EINVAL, "x, v and winner_of are required");
+    if (!aligned16(x) || !aligned16(v)) return fail(EVOX_EALIGN, "x or v is not 16-byte aligned");
+    Layout L;
+    if (!row_layout(D, LAYOUT_CSO, &L)) return fail(EVOX_EINVAL, "no row layout for D = %lld", (long long)D);
+    hipError_t e = launch_pair_move(L.G, x, v, N, D, ldx, winner_of, (hipStream_t)hip_stream);
+    if (e != hipSuccess) return hip_fail(e, "pair move");
     return EVOX_OK;
 }
 

@@ -165,10 +165,10 @@ hipError_t launch_best_init(DevBest *best, float f, int64_t i, hipStream_t s)
     return hipGetLastError();
 }
 
-__global__ __launch_bounds__(256) void k_zero_u32(uint32_t *dst, int64_t n)
+__global__ __launch_bounds__(256) void k_fill_u32(uint32_t *dst, int64_t n, uint32_t value)
 {
     for (int64_t j = (int64_t)blockIdx.x * 256 + threadIdx.x; j < n; j += (int64_t)gridDim.x * 256)
-        dst[j] = 0u;
+        dst[j] = value;
 }
 
 static unsigned flat_grid(int64_t n)
@@ -185,11 +185,13 @@ hipError_t launch_fill(float *dst, int64_t n, float value, hipStream_t s)
     return hipGetLastError();
 }
 
-hipError_t launch_zero_u32(uint32_t *dst, int64_t n, hipStream_t s)
+hipError_t launch_fill_u32(uint32_t *dst, int64_t n, uint32_t value, hipStream_t s)
 {
-    hipLaunchKernelGGL(k_zero_u32, dim3(flat_grid(n)), dim3(256), 0, s, dst, n);
+    hipLaunchKernelGGL(k_fill_u32, dim3(flat_grid(n)), dim3(256), 0, s, dst, n, value);
     return hipGetLastError();
 }
+
+hipError_t launch_zero_u32(uint32_t *dst, int64_t n, hipStream_t s) { return launch_fill_u32(dst, n, 0u, s); }
 
 // First pass of the selection over a stored fitness array.
 __global__ __launch_bounds__(256) void k_argmin_slots(const float *f, int64_t n, SelSlots *sl)
@@ -269,13 +271,22 @@ struct PermSlice {
     uint32_t *hist, *offs, *cursor;
     uint2 *tkv;
     uint32_t *perm;
+    uint32_t *mate;  // null: no mate array
 };
 
 __device__ __forceinline__ PermSlice perm_slice(const PermArgs &a)
 {
     const int64_t b = blockIdx.y, nb = (int64_t)1 << a.bits;
     return PermSlice{a.t0 + (uint32_t)b, a.hist + b * nb, a.offs + b * (nb + 1), a.cursor + b * nb,
-                     a.tkv + b * a.N, a.perm + b * a.N};
+                     a.tkv + b * a.N, a.perm + b * a.N, a.mate ? a.mate + b * a.N : nullptr};
+}
+
+// Mate entry of the individual at permutation position pos whose partner,
+// at position pos ^ 1, is `other`: pairs are positions (2k, 2k + 1), the
+// first of a pair wins ties.
+__device__ __forceinline__ uint32_t mate_entry(uint32_t pos, uint32_t other)
+{
+    return other | ((pos & 1u) ? 0u : kMateFirst);
 }
 
 // Keys of the individuals 4 * (blockIdx.x * kPermChunk / 4 + r * 256 + tid)
@@ -428,6 +439,17 @@ __global__ __launch_bounds__(256) void k_perm_sort(PermArgs a)
         }
         __syncthreads();
         for (uint32_t q = threadIdx.x; q < n; q += 256) sl.perm[lo + q] = S[q];
+        if (sl.mate) {
+            // pairs inside this superbucket's range; a pair that straddles two
+            // ranges is written by k_perm_edges
+            for (uint32_t q = threadIdx.x; q < n; q += 256) {
+                const uint32_t pos = lo + q, other = pos ^ 1u;
+                if ((int64_t)other >= a.N)
+                    sl.mate[S[q]] = kUnpaired;
+                else if (other >= lo && other < lo + n)
+                    sl.mate[S[q]] = mate_entry(pos, S[other - lo]);
+            }
+        }
     } else {
         for (uint32_t p = threadIdx.x; p < n; p += 256) {
             const uint32_t key = sl.tkv[lo + p].x, idx = sl.tkv[lo + p].y;
@@ -438,12 +460,38 @@ __global__ __launch_bounds__(256) void k_perm_sort(PermArgs a)
             }
             sl.perm[lo + rank] = idx;
         }
+        if (sl.mate) {
+            __syncthreads();  // the block's permutation entries are written
+            for (uint32_t q = threadIdx.x; q < n; q += 256) {
+                const uint32_t pos = lo + q, other = pos ^ 1u;
+                if ((int64_t)other >= a.N)
+                    sl.mate[sl.perm[pos]] = kUnpaired;
+                else if (other >= lo && other < lo + n)
+                    sl.mate[sl.perm[pos]] = mate_entry(pos, sl.perm[other]);
+            }
+        }
     }
     __syncthreads();
     if (threadIdx.x == 0) {
         sl.hist[b] = 0;
         sl.cursor[b] = 0;
     }
+}
+
+// Pass 4 (mate arrays only): the pairs that straddle two superbucket ranges,
+// one thread per range start.  A range that starts at an odd position lo
+// splits the pair (lo - 1, lo); empty ranges share their start with the next
+// range and write the same two entries again.
+__global__ __launch_bounds__(256) void k_perm_edges(PermArgs a)
+{
+    const PermSlice sl = perm_slice(a);
+    const int b = blockIdx.x * 256 + threadIdx.x, nb = 1 << a.bits;
+    if (b < 1 || b >= nb) return;
+    const uint32_t lo = sl.offs[b];
+    if ((int64_t)lo >= a.N || (lo & 1u) == 0) return;
+    const uint32_t first = sl.perm[lo - 1], second = sl.perm[lo];
+    sl.mate[first] = second | kMateFirst;
+    sl.mate[second] = first;
 }
 
 hipError_t launch_perm(const PermArgs &a, hipStream_t s)
@@ -453,7 +501,95 @@ hipError_t launch_perm(const PermArgs &a, hipStream_t s)
     hipLaunchKernelGGL(k_perm_count, dim3(chunks, a.batch), dim3(256), 0, s, a);
     hipLaunchKernelGGL(k_perm_place, dim3(chunks, a.batch), dim3(256), 0, s, a);
     hipLaunchKernelGGL(k_perm_sort, dim3(nb, a.batch), dim3(256), 0, s, a);
+    if (a.mate) hipLaunchKernelGGL(k_perm_edges, dim3((nb + 255) / 256, a.batch), dim3(256), 0, s, a);
     return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Diagnostic: the data movement of one swarm-mean CSO generation alone, in
+// the generation kernel's traversal (ranges of kCsoSweep individuals, the
+// losers listed in index order, one row group per listed loser): gather the
+// winner's row, read the loser's x and v, write v + (x_w - x) and the moved
+// x.  No random numbers, no fitness, no column sums: the floor the
+// generation kernel's row traffic sets on this hardware.
+// ---------------------------------------------------------------------------
+template <int G>
+__global__ __launch_bounds__(block_for(G)) void k_pair_move(float *x, float *v, int64_t N, int64_t D, int64_t ldx,
+                                                            const int32_t *winner_of)
+{
+    constexpr int B = block_for(G), RPB = B / G, NW = B / 64, R = kCsoSweep;
+    static_assert(R <= B, "one individual per thread in the listing phase");
+    __shared__ int32_t lst_l[R], lst_w[R];
+    __shared__ int32_t wcnt[NW];
+    const int tid = threadIdx.x, g = tid % G, slot = tid / G, lane = tid & 63, wave = tid >> 6;
+    const int64_t C4 = (D + 3) >> 2;
+    for (int64_t base = (int64_t)blockIdx.x * R; base < N; base += (int64_t)gridDim.x * R) {
+        int32_t w = -1;
+        if (tid < R && base + tid < N) w = winner_of[base + tid];
+        const bool listed = w >= 0 && w < N;  // an index out of range is ignored
+        const uint64_t bal = __ballot(listed);
+        if (lane == 0) wcnt[wave] = __popcll(bal);
+        __syncthreads();
+        int off = 0, total = 0;
+#pragma unroll
+        for (int q = 0; q < NW; ++q) {
+            off += q < wave ? wcnt[q] : 0;
+            total += wcnt[q];
+        }
+        if (listed) {
+            const int at = off + __popcll(bal & ((1ull << lane) - 1ull));
+            lst_l[at] = (int32_t)(base + tid);
+            lst_w[at] = w;
+        }
+        __syncthreads();
+        for (int q = slot; q < total; q += RPB) {
+            const int64_t l = lst_l[q], wr = lst_w[q];
+            for (int64_t c = g; c < C4; c += G) {
+                const int64_t off_l = l * ldx + 4 * c;
+                const float4 xw = *reinterpret_cast<const float4 *>(x + wr * ldx + 4 * c);
+                const float4 xl = ld_stream(x + off_l);
+                const float4 vl = ld_stream(v + off_l);
+                const float4 vn = make_float4(vl.x + (xw.x - xl.x), vl.y + (xw.y - xl.y), vl.z + (xw.z - xl.z),
+                                              vl.w + (xw.w - xl.w));
+                st_stream(v + off_l, vn);
+                st_stream(x + off_l, make_float4(xl.x + vn.x, xl.y + vn.y, xl.z + vn.z, xl.w + vn.w));
+            }
+        }
+        __syncthreads();  // the next range overwrites the list
+    }
+}
+
+template <int G>
+static hipError_t launch_pair_move_g(float *x, float *v, int64_t N, int64_t D, int64_t ldx, const int32_t *winner_of,
+                                     hipStream_t s)
+{
+    int occ = 0, dev = 0, cus = 0;
+    (void)hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, k_pair_move<G>, block_for(G), 0);
+    if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) !=
+                                                 hipSuccess)
+        cus = 256;
+    int64_t grid = (N + kCsoSweep - 1) / kCsoSweep;
+    const int64_t resident = (int64_t)cus * (occ > 0 ? occ : 1);
+    if (grid > resident) grid = resident;
+    hipLaunchKernelGGL((k_pair_move<G>), dim3((unsigned)grid), dim3(block_for(G)), 0, s, x, v, N, D, ldx, winner_of);
+    return hipGetLastError();
+}
+
+hipError_t launch_pair_move(int G, float *x, float *v, int64_t N, int64_t D, int64_t ldx, const int32_t *winner_of,
+                            hipStream_t s)
+{
+    switch (G) {
+        case 4: return launch_pair_move_g<4>(x, v, N, D, ldx, winner_of, s);
+        case 8: return launch_pair_move_g<8>(x, v, N, D, ldx, winner_of, s);
+        case 16: return launch_pair_move_g<16>(x, v, N, D, ldx, winner_of, s);
+        case 32: return launch_pair_move_g<32>(x, v, N, D, ldx, winner_of, s);
+        case 64: return launch_pair_move_g<64>(x, v, N, D, ldx, winner_of, s);
+        case 128: return launch_pair_move_g<128>(x, v, N, D, ldx, winner_of, s);
+        case 256: return launch_pair_move_g<256>(x, v, N, D, ldx, winner_of, s);
+        case 512: return launch_pair_move_g<512>(x, v, N, D, ldx, winner_of, s);
+        case 1024: return launch_pair_move_g<1024>(x, v, N, D, ldx, winner_of, s);
+        default: return hipErrorInvalidValue;
+    }
 }
 
 // Block (0, 0) also finishes the selection (slots -> best) when asked.

@@ -14,15 +14,17 @@
 // one HBM pass of 20 B per element per generation (read x, v, p; write x, v)
 // plus 4 B per element of rows whose personal best improved.
 //
-// CSO.  k_cso: one row group per pair (perm[2k], perm[2k+1]) of the
-// competitive swarm optimizer (Table II); the loser reads its winner's row
-// (a random gather), its own x and v, moves, writes x and v, is re-evaluated
-// from registers, and both rows' new values are accumulated into per-block
-// fp64 column sums for the next swarm mean: 20 B per pair element, i.e. 10 B
-// per individual element.  The neighbourhood version reads the positions
-// from the other population buffer (xs): the loser's neighbours l - 1 and
-// l + 1 besides its own row (three consecutive rows), and writes every row
-// of x (the winner's as a copy).
+// CSO (the competitive swarm optimizer of Table II).  k_cso / k_cso5 sweep
+// the individuals in index order: each decides from its mate entry and the
+// two fitness values whether it lost its pair; a loser reads its winner's
+// row (a random gather), its own x and v (in address order), moves, writes x
+// and v, is re-evaluated from registers, and both rows' new values are
+// accumulated into per-block fp64 column sums for the next swarm mean: 20 B
+// per pair element, i.e. 10 B per individual element.  The neighbourhood
+// version walks the pairs in permutation order, reads the positions from
+// the other population buffer (xs): the loser's neighbours l - 1 and l + 1
+// besides its own row (three consecutive rows), and writes every row of x
+// (the winner's as a copy).
 #pragma once
 
 #include "evox_launch.hpp"
@@ -244,12 +246,156 @@ struct ColAcc {
     }
 };
 
-// pairs whose winner and loser a block decides in one phase (the fitness
-// gathers of 64 pairs in flight at once), before its row groups move them
+// ---------------------------------------------------------------------------
+// The swarm-mean generation, swept in individual order.  A block takes
+// ranges of kCsoSweep consecutive individuals: every individual of the range
+// reads its mate entry and both fitness values (before the generation) and
+// decides whether it lost its pair; winners (and the odd one out) copy their
+// fitness to the output buffer, losers are listed in LDS in index order (a
+// ballot per wave, waves in order, so the list and the order of the column
+// sums are deterministic).  The row groups then move the listed losers:
+// gather the winner's row, read the loser's x and v -- rows in increasing
+// address order, so the loser traffic is a forward sweep over the
+// population instead of random rows -- update, write x and v, re-evaluate
+// from registers, and accumulate winner + new loser rows into the fp64
+// column sums of the next swarm mean.  The odd individual's row is listed
+// too, for its column sums only.
+// ---------------------------------------------------------------------------
+template <int FN, int G, int MAXIT>
+__device__ __forceinline__ void cso_sweep_body(const CsoArgs &a)
+{
+    constexpr int B = block_for(G), RPB = B / G, NW = B / 64, R = kCsoSweep;
+    static_assert(R <= B, "one individual per thread in the decision phase");
+    __shared__ float nbr[(FN == FN_ROSENBROCK && G > 64) ? B * MAXIT : 1];
+    __shared__ float red[2 * (B / 64)];
+    __shared__ uint64_t sk[B / 64];
+    __shared__ uint32_t sc[B / 64];
+    __shared__ double acc_lds[RPB > 1 ? 4 * MAXIT * B : 1];
+    __shared__ int32_t lst_l[R], lst_w[R];  // listed individual, its winner (-1: the odd one out)
+    __shared__ int32_t wcnt[NW];
+
+    const int tid = threadIdx.x, g = tid % G, slot = tid / G, lane = tid & 63, wave = tid >> 6;
+    const int64_t C4 = (a.D + 3) >> 2;
+    uint64_t best = kNoKey;
+    uint32_t none = 0;
+    ColAcc<G, MAXIT> acc(acc_lds);
+
+    for (int64_t base = (int64_t)blockIdx.x * R; base < a.N; base += (int64_t)gridDim.x * R) {
+        bool listed = false;
+        int32_t me = 0, other = -1;
+        if (tid < R && base + tid < a.N) {
+            const int64_t i = base + tid;
+            const uint32_t m = a.mate[i];
+            const float fi = a.fit_in[i];
+            bool loser = false;
+            if (m != kUnpaired) {
+                const int64_t j = m & ~kMateFirst;
+                const float fj = a.fit_in[j];
+                const bool first = (m & kMateFirst) != 0;
+                const float f0 = first ? fi : fj, f1 = first ? fj : fi;
+                const bool second_wins = f1 < f0 || (f0 != f0 && f1 == f1);
+                loser = first ? second_wins : !second_wins;
+                other = (int32_t)j;
+            }
+            if (!loser) {
+                a.fit[i] = fi;
+                const uint64_t k = sel_key(fi, i);
+                best = k < best ? k : best;
+            }
+            listed = loser || m == kUnpaired;
+            me = (int32_t)i;
+        }
+        const uint64_t bal = __ballot(listed);
+        if (lane == 0) wcnt[wave] = __popcll(bal);
+        __syncthreads();
+        int off = 0, total = 0;
+#pragma unroll
+        for (int q = 0; q < NW; ++q) {
+            off += q < wave ? wcnt[q] : 0;
+            total += wcnt[q];
+        }
+        if (listed) {
+            const int at = off + __popcll(bal & ((1ull << lane) - 1ull));
+            lst_l[at] = me;
+            lst_w[at] = other;
+        }
+        __syncthreads();
+        const int rounds = (total + RPB - 1) / RPB;  // uniform: every thread reaches the barriers
+        for (int r = 0; r < rounds; ++r) {
+            const int q = r * RPB + slot;
+            const bool active = q < total;
+            const int64_t l = active ? lst_l[q] : 0;
+            const int64_t w = active ? lst_w[q] : -1;
+            const bool paired = w >= 0;
+            float4 xr[MAXIT];
+#pragma unroll
+            for (int it = 0; it < MAXIT; ++it) {
+                const int64_t c = g + (int64_t)G * it;
+                float4 xn = make_float4(0.f, 0.f, 0.f, 0.f);
+                if (active && c < C4) {
+                    const int64_t off_l = l * a.ldx + 4 * c;
+                    const float4 xl = ld_stream(a.x + off_l);
+                    if (paired) {
+                        const float4 xw = *reinterpret_cast<const float4 *>(a.x + w * a.ldx + 4 * c);
+                        const float4 vl = ld_stream(a.v + off_l);
+                        const float4 xb = *reinterpret_cast<const float4 *>(a.xbar + 4 * c);
+                        const U4 R1 = philox((uint32_t)(3 * c), (uint32_t)l, a.t, STREAM_CSO, a.k0, a.k1);
+                        const U4 R2 = philox((uint32_t)(3 * c + 1), (uint32_t)l, a.t, STREAM_CSO, a.k0, a.k1);
+                        const U4 R3 = philox((uint32_t)(3 * c + 2), (uint32_t)l, a.t, STREAM_CSO, a.k0, a.k1);
+                        float xo[4], vo[4];
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) {
+                            const float xle = comp(xl, e);
+                            const float t0 = wcomp(R1, e) * comp(vl, e);
+                            const float t1 = fmaf(wcomp(R2, e), comp(xw, e) - xle, t0);
+                            const float cc = a.phi * wcomp(R3, e);
+                            const float nv = fmaf(cc, comp(xb, e) - xle, t1);
+                            float nx = xle + nv;
+                            if (a.xclamp) nx = fminf(fmaxf(nx, a.lb), a.ub);
+                            const bool in = 4 * c + e < a.D;
+                            xo[e] = in ? nx : 0.0f;
+                            vo[e] = in ? nv : 0.0f;
+                        }
+                        xn = make_float4(xo[0], xo[1], xo[2], xo[3]);
+                        st_stream(a.x + off_l, xn);
+                        st_stream(a.v + off_l, make_float4(vo[0], vo[1], vo[2], vo[3]));
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) acc.add(it, e, (double)comp(xw, e) + (double)comp(xn, e));
+                    } else {
+                        xn = xl;  // the odd one out: unchanged, counted in the column sums
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) acc.add(it, e, (double)comp(xl, e));
+                    }
+                }
+                xr[it] = xn;
+            }
+            const float f = row_fitness<FN, G, MAXIT>(xr, g, a.D, nbr, red);
+            if (active && paired && g == 0) {
+                a.fit[l] = f;
+                const uint64_t k = sel_key(f, l);
+                best = k < best ? k : best;
+            }
+        }
+        __syncthreads();  // the next range overwrites the list
+    }
+    block_min_key(best, none, sk, sc);
+    if (tid == 0) slot_commit(a.slots, best, 0);
+    acc.write(a.D, a.ldx, a.xsum);
+}
+
+// pairs whose winner and loser a block of the neighbourhood version decides
+// in one phase (the fitness gathers of 64 pairs in flight at once), before
+// its row groups move them
 constexpr int kCsoDecide = 64;
 
-template <int FN, int G, int MAXIT, bool LOCAL>
-__device__ __forceinline__ void cso_body(const CsoArgs &a)
+// ---------------------------------------------------------------------------
+// The neighbourhood version's generation, in permutation order: every row of
+// the next population buffer x is written (the losers' new rows and copies
+// of the winners'), the old rows are read from xs, and loser l learns from
+// the fp64 mean of the old rows l - 1, l, l + 1 (modulo N).
+// ---------------------------------------------------------------------------
+template <int FN, int G, int MAXIT>
+__device__ __forceinline__ void cso_local_body(const CsoArgs &a)
 {
     constexpr int B = block_for(G), RPB = B / G;
     __shared__ float nbr[(FN == FN_ROSENBROCK && G > 64) ? B * MAXIT : 1];
@@ -306,27 +452,21 @@ __device__ __forceinline__ void cso_body(const CsoArgs &a)
             const int64_t c = g + (int64_t)G * it;
             float4 xn = make_float4(0.f, 0.f, 0.f, 0.f);
             if (active && c < C4) {
-                constexpr bool local = LOCAL;  // the neighbourhood version (a.xs is the other buffer)
                 const float4 xw = *reinterpret_cast<const float4 *>(a.xs + w * a.ldx + 4 * c);
                 if (paired) {
                     const int64_t off = l * a.ldx + 4 * c;
                     const float4 xl = ld_stream(a.xs + off);
                     const float4 vl = ld_stream(a.v + off);
-                    float4 xb;
-                    if constexpr (local) {
-                        // ring mean of the rows before the generation: ((x_{l-1} + x_l) + x_{l+1}) / 3
-                        // in fp64, rounded once
-                        const int64_t lm = l == 0 ? a.N - 1 : l - 1, lp = l == a.N - 1 ? 0 : l + 1;
-                        const float4 xa = *reinterpret_cast<const float4 *>(a.xs + lm * a.ldx + 4 * c);
-                        const float4 xc = *reinterpret_cast<const float4 *>(a.xs + lp * a.ldx + 4 * c);
-                        float mo[4];
+                    // ring mean of the rows before the generation: ((x_{l-1} + x_l) + x_{l+1}) / 3
+                    // in fp64, rounded once
+                    const int64_t lm = l == 0 ? a.N - 1 : l - 1, lp = l == a.N - 1 ? 0 : l + 1;
+                    const float4 xa = *reinterpret_cast<const float4 *>(a.xs + lm * a.ldx + 4 * c);
+                    const float4 xc = *reinterpret_cast<const float4 *>(a.xs + lp * a.ldx + 4 * c);
+                    float mo[4];
 #pragma unroll
-                        for (int e = 0; e < 4; ++e)
-                            mo[e] = (float)((((double)comp(xa, e) + (double)comp(xl, e)) + (double)comp(xc, e)) / 3.0);
-                        xb = make_float4(mo[0], mo[1], mo[2], mo[3]);
-                    } else {
-                        xb = *reinterpret_cast<const float4 *>(a.xbar + 4 * c);
-                    }
+                    for (int e = 0; e < 4; ++e)
+                        mo[e] = (float)((((double)comp(xa, e) + (double)comp(xl, e)) + (double)comp(xc, e)) / 3.0);
+                    const float4 xb = make_float4(mo[0], mo[1], mo[2], mo[3]);
                     const U4 R1 = philox((uint32_t)(3 * c), (uint32_t)l, a.t, STREAM_CSO, a.k0, a.k1);
                     const U4 R2 = philox((uint32_t)(3 * c + 1), (uint32_t)l, a.t, STREAM_CSO, a.k0, a.k1);
                     const U4 R3 = philox((uint32_t)(3 * c + 2), (uint32_t)l, a.t, STREAM_CSO, a.k0, a.k1);
@@ -348,7 +488,7 @@ __device__ __forceinline__ void cso_body(const CsoArgs &a)
                     st_stream(a.x + off, xn);
                     st_stream(a.v + off, make_float4(vo[0], vo[1], vo[2], vo[3]));
                 }
-                if constexpr (local) st_stream(a.x + w * a.ldx + 4 * c, xw);  // the winner's row, unchanged
+                st_stream(a.x + w * a.ldx + 4 * c, xw);  // the winner's row, unchanged
 #pragma unroll
                 for (int e = 0; e < 4; ++e)
                     acc.add(it, e, paired ? (double)comp(xw, e) + (double)comp(xn, e) : (double)comp(xw, e));
@@ -376,17 +516,19 @@ __device__ __forceinline__ void cso_body(const CsoArgs &a)
 template <int FN, int G, int MAXIT, bool LOCAL>
 __global__ __launch_bounds__(block_for(G)) void k_cso(CsoArgs a)
 {
-    cso_body<FN, G, MAXIT, LOCAL>(a);
+    if constexpr (LOCAL)
+        cso_local_body<FN, G, MAXIT>(a);
+    else
+        cso_sweep_body<FN, G, MAXIT>(a);
 }
 
 // The swarm-mean generation with one chunk per lane and at most 32 lanes per
-// row (D <= 128), compiled for 5 waves per SIMD (within 96 registers, no
-// spills for any of the six functions; at 64 lanes Griewank would spill):
-// the shape of the large-population, moderate-D workloads.
+// row (D <= 128), compiled for 5 waves per SIMD (within 96 registers): the
+// shape of the large-population, moderate-D workloads.
 template <int FN, int G>
 __global__ __launch_bounds__(block_for(G)) __attribute__((amdgpu_waves_per_eu(5))) void k_cso5(CsoArgs a)
 {
-    cso_body<FN, G, 1, false>(a);
+    cso_sweep_body<FN, G, 1>(a);
 }
 
 // ---------------------------------------------------------------------------

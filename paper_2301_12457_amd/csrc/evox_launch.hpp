@@ -199,10 +199,22 @@ struct InitArgs {
     uint32_t k0, k1;
 };
 
+// CSO pairing in individual order (the swarm-mean generation): entry i of a
+// generation's mate array is the index of i's partner, with kMateFirst set
+// when i is the first of its pair (the one that wins ties); kUnpaired marks
+// the individual left over when N is odd.
+constexpr uint32_t kMateFirst = 0x80000000u;
+constexpr uint32_t kUnpaired = 0xFFFFFFFFu;
+constexpr int kCsoSweep = 128;  // individuals per range of the swarm-mean generation kernel
+
 struct CsoArgs {
-    float *x, *v, *fit;
+    float *x, *v;
+    float *fit;            // fitness after the generation (the swarm version writes every entry; the
+                           // neighbourhood version updates the losers' entries in place)
+    const float *fit_in;   // swarm version: fitness before the generation (another buffer than fit)
     const float *xbar;
-    const uint32_t *perm;  // this generation's permutation
+    const uint32_t *perm;  // neighbourhood version: this generation's permutation
+    const uint32_t *mate;  // swarm version: this generation's mate array
     int64_t N, D, ldx;
     float phi, lb, ub;
     int32_t xclamp;
@@ -242,12 +254,17 @@ hipError_t launch_init(const InitArgs &a, hipStream_t s);
 hipError_t launch_philox_fill(uint32_t k0, uint32_t k1, uint32_t c1, uint32_t c2, uint32_t c3,
                               int64_t n, uint32_t *out, hipStream_t s);
 hipError_t launch_stream_copy(const float *src, float *dst, int64_t n, hipStream_t s);
+// The data movement of a swarm-mean CSO generation with G lanes per row
+// (diagnostic): loser i = every index with winner_of[i] >= 0.
+hipError_t launch_pair_move(int G, float *x, float *v, int64_t N, int64_t D, int64_t ldx, const int32_t *winner_of,
+                            hipStream_t s);
 // CSO's neighbourhood version: out row i = ((x_{i-1} + x_i) + x_{i+1}) / 3
 // (indices modulo N) in fp64, rounded once; every column of the pitch.
 hipError_t launch_copy_row(const float *src, float *dst, int64_t ldx, hipStream_t s);
 hipError_t launch_fill(float *dst, int64_t n, float value, hipStream_t s);
 hipError_t launch_best_init(DevBest *best, float f, int64_t i, hipStream_t s);
 hipError_t launch_zero_u32(uint32_t *dst, int64_t n, hipStream_t s);
+hipError_t launch_fill_u32(uint32_t *dst, int64_t n, uint32_t value, hipStream_t s);
 // First pass of the selection over a stored fitness array.
 hipError_t launch_argmin_slots(const float *f, int64_t N, SelSlots *slots, hipStream_t s);
 
@@ -268,6 +285,7 @@ struct PermArgs {
     uint2 *tkv;                      // [batch][N] (key, index) placed by superbucket
     uint32_t *perm;                  // [batch][N]
     const uint32_t *keys;  // caller keys (batch 1), or null: Philox stream-4 keys
+    uint32_t *mate;        // [batch][N] mate arrays of the permutations, or null: none
 };
 hipError_t launch_perm(const PermArgs &a, hipStream_t s);
 hipError_t launch_cso(int fn, Layout L, const CsoArgs &a, int grid, hipStream_t s);

@@ -85,14 +85,14 @@ def test_default_pitch_policy(evox):
     for D, want in [(1, 4), (10, 12), (100, 100), (511, 512), (512, 512), (1000, 1024), (1025, 1056),
                     (32768, 32768)]:
         assert L.evox_default_ldx(P, D) == want, (D, want)
-    for D, want in [(1, 4), (10, 12), (63, 64), (64, 64), (65, 96), (100, 128), (1000, 1024)]:
+    for D, want in [(1, 4), (10, 12), (63, 64), (64, 64), (65, 68), (100, 100), (1000, 1000), (1001, 1004)]:
         assert L.evox_default_ldx(C, D) == want, (D, want)
     for D in (10, 100, 1000):
         for algo in (evox.DE, evox.ES, evox.PGPE, evox.MAES, evox.NSGA2):
             assert L.evox_default_ldx(algo, D) == L.evox_default_ldx(P, D)
     for algo, D in [(P, 0), (C, 32769), (7, 10)]:
         assert L.evox_default_ldx(algo, D) == 0
-    assert evox.make_params(C, evox.GRIEWANK, 10, 100, -1, 1).ldx == 128
+    assert evox.make_params(C, evox.GRIEWANK, 10, 100, -1, 1).ldx == 100
     assert evox.make_params(P, evox.GRIEWANK, 10, 100, -1, 1).ldx == 100
     with pytest.raises(evox.EvoxError):
         evox.pitch(0)
@@ -180,6 +180,16 @@ def test_null_state_is_rejected(evox):
     assert L.evox_best(None, None, None, None) == evox.EINVAL
     assert L.evox_generation(None) == -1
     assert L.evox_set_generation(None, 5) == evox.EINVAL
+
+
+def test_pair_move_validates_before_any_gpu_call(evox):
+    L = evox.lib()
+    f = ctypes.c_void_p(0x1000)
+    assert L.evox_pair_move(f, f, 1, 10, 12, f, None) == evox.EINVAL               # N < 2
+    assert L.evox_pair_move(f, f, 10, 0, 12, f, None) == evox.EINVAL               # D < 1
+    assert L.evox_pair_move(f, f, 10, 10, 14, f, None) == evox.EINVAL              # ldx % 4
+    assert L.evox_pair_move(f, f, 10, 10, 12, None, None) == evox.EINVAL           # winner_of
+    assert L.evox_pair_move(ctypes.c_void_p(0x1004), f, 10, 10, 12, f, None) == evox.EALIGN
 
 
 def test_noalloc_entry_point_validates_before_any_gpu_call(evox):

@@ -59,6 +59,11 @@ CASES = [
     dict(fn=5, N=7, D=3, seed=5, lb=-500.0, ub=500.0, clamp_x=1, gens=30),
     dict(fn=4, N=5, D=2050, seed=6, lb=-2.0, ub=2.0, gens=6),
     dict(fn=0, N=2, D=1, seed=8, lb=-1.0, ub=1.0, gens=10),
+    # several superbuckets in the pairing sort (pairs that straddle two of
+    # them), odd and even populations
+    dict(fn=0, N=5001, D=4, seed=13, lb=-5.0, ub=5.0, gens=12),
+    dict(fn=3, N=70_001, D=20, seed=14, lb=-600.0, ub=600.0, gens=6),
+    dict(fn=2, N=131_072, D=8, seed=15, lb=-5.12, ub=5.12, gens=4),
 ]
 
 
@@ -144,10 +149,11 @@ def test_pitched_states_match_oracle(evox_gpu, ref, D, ldx):
             assert int((pad != 0).sum()) == 0, f"{name} padding written at generation {t}"
 
 
-def test_default_pitch_is_line_aligned(evox_gpu, ref):
+def test_default_pitch_is_dense(evox_gpu, ref):
     g = evox_gpu.Swarm(evox_gpu.make_params(evox_gpu.CSO, 3, 64, 100, -600.0, 600.0, seed=3))
-    assert g.P.ldx == 128
-    assert g.x.data_ptr() % 128 == 0 and (g.P.ldx * 4) % 128 == 0
+    assert g.P.ldx == 100
+    g = evox_gpu.Swarm(evox_gpu.make_params(evox_gpu.CSO, 3, 64, 37, -600.0, 600.0, seed=3))
+    assert g.P.ldx == 40
 
 
 LOCAL_CASES = [
