@@ -22,6 +22,11 @@ METRIC = "individual·dim updates/sec per fused generation; % of HBM peak GB/s"
 UNIT = "individual·dim updates/s"
 HBM_PEAK_GBS = 8000.0
 DEFAULT_WORKLOAD = "pso_rastrigin_1e5x1e3"
+# the benchmark set: PSO Sphere 100 x 10, PSO Ackley 1e4 x 1e3, PSO Rastrigin
+# 1e5 x 1e3 (the headline), CSO Griewank 1e6 x 100, evaluation + argmin of
+# Rosenbrock 1,048,576 x 1000; every bench.py run times all of them
+CONFIG_WORKLOADS = ("pso_sphere_100x10", "pso_ackley_1e4x1e3", "pso_rastrigin_1e5x1e3", "cso_griewank_1e6x100",
+                    "eval_rosenbrock_1m_x1e3")
 KERNEL_SOURCES = ("paper_2301_12457_amd/csrc/evox_device.hpp",
                   "paper_2301_12457_amd/csrc/evox_kernels.hpp")
 
@@ -123,7 +128,10 @@ def host_cpu():
 
 def cpu_baseline(w, budget_s=12.0):
     """The oracle, single-threaded and pinned to one core, on a bounded sample
-    of the workload."""
+    of the workload; and, for PSO, CSO and evaluation, the all-core leg: the
+    oracle's steps with their row loops split over every core this process
+    may use (oracle/evox_ref_mt.c, bit-identical results), the comparison the
+    paper's CPU runs make (all host threads)."""
     allowed = os.sched_getaffinity(0)
     os.sched_setaffinity(0, {min(allowed)})
     try:
@@ -131,7 +139,46 @@ def cpu_baseline(w, budget_s=12.0):
     finally:
         os.sched_setaffinity(0, allowed)
     out["host_cpu"], out["host_cores_available"] = host_cpu()
+    if w.algo in ("pso", "cso", "eval"):
+        # every core of this process's share: the affinity set, bounded by the
+        # OpenMP thread budget where the host sets one
+        threads = len(allowed)
+        if os.environ.get("OMP_NUM_THREADS", "").isdigit():
+            threads = max(1, min(threads, int(os.environ["OMP_NUM_THREADS"])))
+        out["all_cores"] = _cpu_all_cores(w, threads, budget_s)
     return out
+
+
+def _cpu_all_cores(w, threads, budget_s):
+    import oracle
+    fn = oracle.FN_NAMES.index(w.fn)
+    if w.algo == "eval":
+        from paper_2301_12457_amd.workloads import normal_matrix_np
+        rows = min(w.N, 10_000 * threads)
+        X = normal_matrix_np(rows, w.D, w.x_mu, w.x_sigma, w.seed)
+        t0 = time.perf_counter()
+        n = 0
+        while time.perf_counter() - t0 < budget_s:
+            oracle.mt_evaluate(fn, X, threads)
+            n += 1
+        dt = time.perf_counter() - t0
+        return {"value": rows * w.D * n / dt, "unit": UNIT, "cores": threads,
+                "kind": "oracle, rows split over all cores",
+                "sample": f"{rows} of {w.N} rows x D={w.D}, {n} evaluation passes, {dt:.1f} s"}
+    rows = min(w.N, (20_000 if w.algo == "cso" else 2000) * threads)
+    P = oracle.make_params(fn, rows, w.D, w.lb, w.ub, v_lo=w.v_lo, v_hi=w.v_hi, w=w.w, c1=w.c1, c2=w.c2,
+                           phi=w.phi, vmax=w.vmax, seed=w.seed, cso_local=w.cso_local)
+    s = (oracle.PSO if w.algo == "pso" else oracle.CSO)(P)
+    oracle.mt_step(s, 1, threads)
+    t0 = time.perf_counter()
+    gens = 0
+    while time.perf_counter() - t0 < budget_s and gens < w.gens:
+        oracle.mt_step(s, 1, threads)
+        gens += 1
+    dt = time.perf_counter() - t0
+    return {"value": rows * w.D * gens / dt, "unit": UNIT, "cores": threads,
+            "kind": "oracle, rows split over all cores",
+            "sample": f"{rows} of {w.N} individuals x D={w.D}, {gens} generations, {dt:.1f} s"}
 
 
 def _cpu_baseline(w, budget_s):
@@ -239,6 +286,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD, choices=sorted(WORKLOADS))
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-configs", action="store_true",
+                    help="time only the chosen workload, not the rest of the benchmark set")
     ap.add_argument("--ldx", type=int, default=0,
                     help="row pitch in floats (default: D rounded up to a multiple of 4)")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
@@ -252,8 +301,54 @@ def main():
     import torch
     import paper_2301_12457_amd as evox
 
-    w = WORKLOADS[args.workload]
     torch.cuda.set_device(0)
+    w = WORKLOADS[args.workload]
+    head = measure(torch, evox, w, args.steps, args.warmup, args.ldx or None)
+    ms, roofline = head["ms_per_step"], head["roofline"]
+
+    if args.calib_copy_mib:
+        n = args.calib_copy_mib * (1 << 20) // 4
+        a = torch.ones(n, dtype=torch.float32, device="cuda")
+        b = torch.empty_like(a)
+        for _ in range(3):
+            b.copy_(a)
+        torch.cuda.synchronize()
+        del a, b
+    copy = copy_bandwidth(torch, evox)
+    if roofline is not None and roofline["bound"] == "hbm":
+        roofline["copy_gbs"] = round(copy, 1)
+        roofline["frac_of_copy"] = round(roofline["achieved"] / copy, 4)
+
+    # the other workloads of the benchmark set, timed in the same run
+    configs = []
+    if not args.no_configs:
+        for name in CONFIG_WORKLOADS:
+            if name == w.name:
+                continue
+            wc = WORKLOADS[name]
+            r = measure(torch, evox, wc, 5 if wc.algo == "eval" else 2, 1, None)
+            if r["roofline"] is not None and r["roofline"]["bound"] == "hbm":
+                r["roofline"]["frac_of_copy"] = round(r["roofline"]["achieved"] / copy, 4)
+            configs.append(r)
+            print(f"[bench] {name}: {r['ms_per_step']:.3f} ms/step", file=sys.stderr, flush=True)
+
+    base = None
+    if not args.no_cpu_baseline:
+        base = cpu_baseline(w)
+        print(f"[bench] cpu baseline: {base}", file=sys.stderr, flush=True)
+
+    line = {
+        "metric": METRIC, "value": head["value"], "unit": UNIT, "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "config": head["config"], "roofline": roofline, "cpu_baseline": base, "configs": configs,
+    }
+    print(json.dumps(line), flush=True)
+
+
+def measure(torch, evox, w, steps, warmup, ldx):
+    """Time `steps` steps of workload w after `warmup` untimed ones; the
+    dominant kernel's roofline from HIP events around its launches."""
     stream = torch.cuda.current_stream()
     fn = evox.FN_IDS[w.fn] if w.algo != "nsga2" else 0   # NSGA-II: DTLZ1
 
@@ -274,7 +369,7 @@ def main():
                 "pgpe": evox.PGPE, "maes": evox.MAES, "nsga2": evox.NSGA2}[w.algo]
         P = evox.make_params(algo, fn, w.N, w.D, w.lb, w.ub, v_lo=w.v_lo, v_hi=w.v_hi, w=w.w,
                              c1=w.c1, c2=w.c2, phi=w.phi, vmax=w.vmax, seed=w.seed,
-                             ldx=args.ldx or None, de_f=w.de_f, de_cr=w.de_cr,
+                             ldx=ldx, de_f=w.de_f, de_cr=w.de_cr,
                              es_sigma=w.es_sigma, es_lr=w.es_lr, pgpe_sigma_lr=w.pgpe_sigma_lr,
                              pgpe_max_change=w.pgpe_max_change, n_obj=w.n_obj, cso_local=w.cso_local)
         swarm = evox.Swarm(P)
@@ -282,7 +377,7 @@ def main():
         def step():
             swarm.step(w.gens)
 
-    for _ in range(args.warmup):
+    for _ in range(warmup):
         step()
     torch.cuda.synchronize()
     print(f"[bench] {w.name}: warmup done", file=sys.stderr, flush=True)
@@ -293,13 +388,13 @@ def main():
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     ev0.record(stream)
-    for _ in range(args.steps):
+    for _ in range(steps):
         step()
     ev1.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    ms = ev0.elapsed_time(ev1) / args.steps
-    print(f"[bench] timed {args.steps} steps: {ms:.3f} ms/step (wall {wall:.3f} s)",
+    ms = ev0.elapsed_time(ev1) / steps
+    print(f"[bench] {w.name}: timed {steps} steps: {ms:.3f} ms/step (wall {wall:.3f} s)",
           file=sys.stderr, flush=True)
 
     gens = w.gens if w.algo != "eval" else 1
@@ -358,49 +453,33 @@ def main():
                         "traffic": traffic, "kernel": kname,
                         "avg_launch_us": round(avg_ms * 1e3, 2), "launches": launches,
                         "algorithmic_bytes_per_launch": bytes_per}
+            if w.algo == "pso":
+                # the 20 B per element floor alone (read x, v, pbest; write
+                # x, v), without the rows whose personal best improved
+                floor_bytes = 20.0 * w.N * w.D
+                roofline["frac_floor_20B"] = round(floor_bytes / (avg_ms / 1e3) / 1e9 / HBM_PEAK_GBS, 4)
+                roofline["improved_rows_per_launch"] = round(improved / launches, 1)
     else:
         bytes_per = 4.0 * w.N * w.D + 4.0 * w.N
         achieved = bytes_per / (ms / 1e3) / 1e9
         roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                     "traffic": traffic_from_profile(w.name), "kernel": "k_eval",
-                    "avg_launch_us": round(ms * 1e3, 2), "launches": args.steps,
+                    "avg_launch_us": round(ms * 1e3, 2), "launches": steps,
                     "algorithmic_bytes_per_launch": bytes_per}
-
-    if args.calib_copy_mib:
-        n = args.calib_copy_mib * (1 << 20) // 4
-        a = torch.ones(n, dtype=torch.float32, device="cuda")
-        b = torch.empty_like(a)
-        for _ in range(3):
-            b.copy_(a)
-        torch.cuda.synchronize()
-        del a, b
-    if roofline is not None and roofline["bound"] == "hbm":
-        copy = copy_bandwidth(torch, evox)
-        roofline["copy_gbs"] = round(copy, 1)
-        roofline["frac_of_copy"] = round(roofline["achieved"] / copy, 4)
     if roofline is not None and w.algo == "cso" and not w.cso_local:
         f_us, f_bytes = cso_data_floor(torch, evox, w, swarm.P.ldx)
         roofline["data_floor"] = {"kernel": "k_pair_move (evox_pair_move)", "avg_launch_us": round(f_us, 2),
                                   "algorithmic_bytes_per_launch": f_bytes,
                                   "frac": round(f_bytes / (f_us / 1e6) / 1e9 / HBM_PEAK_GBS, 4),
                                   "kernel_over_floor": round(roofline["avg_launch_us"] / f_us, 4)}
-
-    base = None
-    if not args.no_cpu_baseline:
-        base = cpu_baseline(w)
-        print(f"[bench] cpu baseline: {base}", file=sys.stderr, flush=True)
-
-    line = {
-        "metric": METRIC, "value": value, "unit": UNIT, "n_gpus": 1, "steps": args.steps,
-        "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
-        "vs_baseline": None, "dtype": "f32", "data": "synthetic",
-        "config": {"workload": w.name, "algo": w.algo, "fn": w.fn, "N": w.N, "D": w.D,
-                   "ldx": (swarm.P.ldx if swarm is not None else w.D),
-                   "generations_per_step": gens, "seed": w.seed},
-        "roofline": roofline, "cpu_baseline": base,
-    }
-    print(json.dumps(line), flush=True)
+    config = {"workload": w.name, "algo": w.algo, "fn": w.fn, "N": w.N, "D": w.D,
+              "ldx": (swarm.P.ldx if swarm is not None else w.D), "generations_per_step": gens, "seed": w.seed}
+    result = {"workload": w.name, "value": value, "unit": UNIT, "ms_per_step": ms, "steps": steps,
+              "warmup": warmup, "ms_per_generation": ms / gens, "config": config, "roofline": roofline}
+    del swarm
+    torch.cuda.empty_cache()
+    return result
 
 
 if __name__ == "__main__":

@@ -104,6 +104,54 @@ def lib():
     return _lib
 
 
+_mt = None
+MT_LIB_PATH = os.path.join(HERE, "libevox_ref_mt.so")
+
+
+def mt_lib():
+    """The all-core CPU baseline (oracle/evox_ref_mt.c): the oracle's steps
+    with their row loops split over threads, bit-identical results."""
+    global _mt
+    if _mt is None:
+        if not os.path.exists(MT_LIB_PATH):
+            from . import build as _b
+            _b.build()
+        L = ctypes.CDLL(MT_LIB_PATH)
+        i64, P, ci = ctypes.c_int64, ctypes.c_void_p, ctypes.c_int
+        L.evox_mt_eval.argtypes = [ci, P, i64, i64, i64, P, ci]
+        L.evox_mt_pso_step.argtypes = [P, i64, i64, P, P, P, P, P, P, P, ci]
+        L.evox_mt_cso_step.argtypes = [P, i64, i64, P, P, P, P, P, ci]
+        _mt = L
+    return _mt
+
+
+def mt_evaluate(fn, X, threads):
+    X = _f32(X)
+    N, D = X.shape
+    out = np.zeros(N, dtype=np.float32)
+    if mt_lib().evox_mt_eval(fn, _ptr(X), N, D, D, _ptr(out), threads) != 0:
+        raise ValueError("evox_mt_eval failed")
+    return out
+
+
+def mt_step(state, n_gens, threads):
+    """n_gens generations of an oracle PSO or CSO state on `threads` threads."""
+    if isinstance(state, PSO):
+        rc = mt_lib().evox_mt_pso_step(ctypes.byref(state.P), state.t, n_gens, _ptr(state.x), _ptr(state.v),
+                                       _ptr(state.p), _ptr(state.pf), _ptr(state.g), ctypes.byref(state._gf),
+                                       ctypes.byref(state._gi), threads)
+    elif isinstance(state, CSO):
+        bf, bi = ctypes.c_float(0.0), ctypes.c_int64(0)
+        rc = mt_lib().evox_mt_cso_step(ctypes.byref(state.P), state.t, n_gens, _ptr(state.x), _ptr(state.v),
+                                       _ptr(state.fit), ctypes.byref(bf), ctypes.byref(bi), threads)
+        state.best_fit, state.best_idx = bf.value, bi.value
+    else:
+        raise TypeError(type(state))
+    if rc != 0:
+        raise ValueError(f"all-core step rc={rc}")
+    state.t += n_gens
+
+
 def _ptr(a):
     return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
 

@@ -465,6 +465,28 @@ void evox_ref_ring_mean(const float *X, int64_t N, int64_t D, float *out)
     }
 }
 
+/* Loser l of generation t moves toward its winner w and the mean xb (D
+ * floats: the swarm mean, or l's ring-neighbourhood mean). */
+static void cso_move_loser(const evox_ref_params *P, int64_t t, int64_t l, int64_t w, float *x, float *v,
+                           const float *xb)
+{
+    const int64_t D = P->D;
+    for (int64_t j = 0; j < D; ++j) {
+        float R1 = draw(P->seed, l, j, 3, 0, t, STREAM_CSO);
+        float R2 = draw(P->seed, l, j, 3, 1, t, STREAM_CSO);
+        float R3 = draw(P->seed, l, j, 3, 2, t, STREAM_CSO);
+        float xl = x[l * D + j], xw = x[w * D + j], vl = v[l * D + j];
+        float t0v = R1 * vl;
+        float t1v = fmaf(R2, xw - xl, t0v);
+        float c = P->phi * R3;
+        float vn = fmaf(c, xb[j] - xl, t1v);
+        float xn = xl + vn;
+        if (P->clamp_x) xn = fminf(fmaxf(xn, P->lb), P->ub);
+        v[l * D + j] = vn;
+        x[l * D + j] = xn;
+    }
+}
+
 /* n_gens CSO iterations from generation t0.  Each: the mean xbar of the
  * current positions -- the swarm's, or with cso_local each loser's ring
  * neighbourhood mean, all taken before any loser moves; random pairing; each
@@ -493,20 +515,7 @@ int evox_ref_cso_step(const evox_ref_params *P, int64_t t0, int64_t n_gens, floa
             int64_t w = a, l = b;
             if (second_wins(fit[a], fit[b])) { w = b; l = a; }
             is_loser[l] = 1;
-            for (int64_t j = 0; j < D; ++j) {
-                float R1 = draw(P->seed, l, j, 3, 0, t, STREAM_CSO);
-                float R2 = draw(P->seed, l, j, 3, 1, t, STREAM_CSO);
-                float R3 = draw(P->seed, l, j, 3, 2, t, STREAM_CSO);
-                float xl = x[l * D + j], xw = x[w * D + j], vl = v[l * D + j];
-                float t0v = R1 * vl;
-                float t1v = fmaf(R2, xw - xl, t0v);
-                float c = P->phi * R3;
-                float vn = fmaf(c, xbar[(P->cso_local ? l * D : 0) + j] - xl, t1v);
-                float xn = xl + vn;
-                if (P->clamp_x) xn = fminf(fmaxf(xn, P->lb), P->ub);
-                v[l * D + j] = vn;
-                x[l * D + j] = xn;
-            }
+            cso_move_loser(P, t, l, w, x, v, xbar + (P->cso_local ? l * D : 0));
         }
         for (int64_t i = 0; i < N; ++i)
             if (is_loser[i]) fit[i] = (float)evox_ref_eval_row_f64(P->fn, x + i * D, D);
