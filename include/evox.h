@@ -50,7 +50,8 @@ extern "C" {
 /* Benchmark functions (Problem.evaluate).  F(x) for x in R^D:
  *   SPHERE      sum x_i^2
  *   ACKLEY      -20 exp(-0.2 sqrt(mean x_i^2)) - exp(mean cos(2 pi x_i)) + 20 + e
- *   RASTRIGIN   10 D + sum (x_i^2 - 10 cos(2 pi x_i))
+ *   RASTRIGIN   10 D + sum (x_i^2 - 10 cos(2 pi x_i)) = sum (x_i^2 + 20 sin^2(pi x_i)), evaluated
+ *               in the second form (non-negative terms: relative accuracy at every x)
  *   GRIEWANK    1 + sum x_i^2 / 4000 - prod cos(x_i / sqrt(i)),  i = 1..D
  *   ROSENBROCK  sum_{i<D} 100 (x_{i+1} - x_i^2)^2 + (1 - x_i)^2
  *   SCHWEFEL    418.9829 D - sum x_i sin(sqrt(|x_i|))                        */

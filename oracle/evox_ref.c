@@ -141,14 +141,18 @@ static double ackley(const float *x, int64_t D)
     return -a * exp(-b * sqrt(s1 / n)) - exp(s2 / n) + a + exp(1.0);
 }
 
-/* A D + sum_i (x_i^2 - A cos(2 pi x_i)), A = 10 */
+/* A D + sum_i (x_i^2 - A cos(2 pi x_i)), A = 10, written term by term as
+ * sum_i (x_i^2 + 2 A sin^2(pi x_i)) (1 - cos 2u = 2 sin^2 u): every term is
+ * non-negative, so the sum has no cancellation.  sin(pi x_i) is taken of the
+ * exactly reduced x_i - rint(x_i) (same square for any integer shift). */
 static double rastrigin(const float *x, int64_t D)
 {
     const double A = 10.0;
-    double s = A * (double)D;
+    double s = 0.0;
     for (int64_t i = 0; i < D; ++i) {
         double xi = x[i];
-        s += xi * xi - A * cos(2.0 * kPi * xi);
+        double si = sin(kPi * (xi - rint(xi)));
+        s += xi * xi + 2.0 * A * si * si;
     }
     return s;
 }

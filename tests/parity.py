@@ -4,9 +4,9 @@ Fitness tolerance (reading of "fp32 fitness within 1e-5 relative"):
     |F_gpu - F_ref| <= 1e-5 * max(|F_ref|, S(x))
 with S the magnitude of the terms the function sums, so that exact
 cancellation at an optimum does not demand unbounded relative accuracy:
-    Sphere, Rosenbrock  S = |F|              (non-negative terms)
+    Sphere, Rosenbrock, Rastrigin  S = |F|   (non-negative terms: Rastrigin as
+                                              sum x^2 + 20 sin^2(pi x))
     Ackley              S = 20 + e
-    Rastrigin           S = 20 D + sum x^2
     Griewank            S = 2 + sum x^2 / 4000
     Schwefel            S = 418.9829 D + sum |x|
 """
@@ -22,12 +22,10 @@ def scale(fn, X, f_ref):
     X = np.asarray(X, dtype=np.float64)
     D = X.shape[1]
     f = np.abs(np.asarray(f_ref, dtype=np.float64))
-    if fn in (SPHERE, ROSENBROCK):
+    if fn in (SPHERE, ROSENBROCK, RASTRIGIN):
         return f
     if fn == ACKLEY:
         return np.maximum(f, 20.0 + math.e)
-    if fn == RASTRIGIN:
-        return np.maximum(f, 20.0 * D + (X * X).sum(1))
     if fn == GRIEWANK:
         return np.maximum(f, 2.0 + (X * X).sum(1) / 4000.0)
     if fn == SCHWEFEL:

@@ -74,6 +74,31 @@ def test_rastrigin_closed_forms(ref):
     assert close(ev(ref, R, np.full((1, D), 0.5))[0], 20.25 * D)
 
 
+def test_rastrigin_equals_the_textbook_sum(ref):
+    """The oracle sums x^2 + 2A sin^2(pi x); the textbook form A D + sum(x^2 -
+    A cos 2 pi x), computed here in fp64 with numpy's cosine, is the same
+    function (it cancels, so compare within its own rounding scale)."""
+    rng = np.random.default_rng(7)
+    X = rng.uniform(-5.12, 5.12, size=(64, 301)).astype(np.float32)
+    x = X.astype(np.float64)
+    textbook = 10.0 * x.shape[1] + (x * x - 10.0 * np.cos(2.0 * np.pi * x)).sum(1)
+    got = np.array([ref.lib().evox_ref_eval_row_f64(R, ref._ptr(np.ascontiguousarray(X[i])), X.shape[1])
+                    for i in range(X.shape[0])])
+    assert np.all(np.abs(got - textbook) <= 1e-12 * (20.0 * x.shape[1] + (x * x).sum(1)))
+
+
+def test_rastrigin_near_the_optimum_is_relative_accurate(ref):
+    """Near x = 0 each term is x^2 + 2A (pi x)^2 (1 - (pi x)^2 / 3 + ...): the
+    fp32 value is within a few ulp of that expansion however small F is."""
+    x = (np.arange(1, 41, dtype=np.float64) * 1e-4 * np.array([1, -1] * 20)).astype(np.float32)
+    xd = x.astype(np.float64)
+    y = np.pi * xd
+    want = float((xd * xd + 20.0 * y * y * (1.0 - y * y / 3.0 + 2.0 * y ** 4 / 45.0)).sum())
+    got = float(ev(ref, R, x[None, :])[0])
+    assert abs(got - want) <= 2e-7 * want
+    assert got > 0.0
+
+
 # ---------------- Griewank ----------------
 
 def test_griewank_optimum(ref):
