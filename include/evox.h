@@ -6,11 +6,14 @@
  *     T_pop, S = ask(S);   T_fit, S = evaluate(S, T_pop);   S = tell(S, T_fit)
  * with the stateful signature (state, ...) -> (result, state) and the
  * Algorithm / Problem / Workflow modules of Table I (setup, ask, tell,
- * evaluate, init, step).  This library implements that loop for two swarm
- * algorithms over an fp32 population matrix X[N, D]:
+ * evaluate, init, step).  This library implements that loop over an fp32
+ * population matrix X[N, D] for:
  *   - PSO (global-best, inertia weight; the PSO of the single-objective
  *     experiment, Sec. VII-A-1),
- *   - CSO, the competitive swarm optimizer listed in Table II,
+ *   - CSO, the competitive swarm optimizer listed in Table II (with the
+ *     swarm mean, or the ring-neighbourhood mean),
+ *   - DE/rand/1/bin, OpenES, PGPE, CMA-ES in its matrix-adaptation form
+ *     (MA-ES) and NSGA-II on DTLZ1 (Table II; Sec. VII-A and VII-B),
  * on six benchmark functions (Sphere, the function of Sec. VII-A-1, and the
  * textbook Ackley, Rastrigin, Griewank, Rosenbrock and Schwefel).
  *
@@ -220,7 +223,9 @@ int evox_eval_argmin_noalloc(int fn_id, const float *X, int64_t N, int64_t D, in
  * n_gens.  step(a) then step(b) equals step(a + b) bit for bit. */
 int evox_pso_step(evox_state *state, int64_t n_gens);
 
-/* Workflow.step x n_gens for CSO.  One generation t: xbar is the mean of the
+/* Workflow.step x n_gens (Sec. IV-A, Table I; Eq. (1)-(3)) for CSO, the
+ * competitive swarm optimizer of Table II (after Cheng and Jin, whose update
+ * rule the paper does not print).  One generation t: xbar is the mean of the
  * current positions; individuals are paired by a random permutation (sort by
  * (stream-4 key, index)): pairs (perm[2k], perm[2k+1]), k < floor(N/2); the
  * second wins when its fitness is strictly lower (or the first's is NaN and
@@ -271,7 +276,7 @@ int evox_es_step(evox_state *state, int64_t n_gens);
 
 /* n_gens PGPE generations with symmetric sampling (Sehnke et al., Neural
  * Networks 23, 2010; the ES of the paper's neuroevolution experiment,
- * Sec. VII) on a PGPE state.  Generation t, with H = N/2 pairs:
+ * Sec. VII-B) on a PGPE state.  Generation t, with H = N/2 pairs:
  *   - deviates z_kj from Philox(seed, (floor(j/4), k, t, 8)) with the
  *     Box-Muller layout of evox_fill_normal; samples x_{2k} = fma(sigma_j,
  *     z_kj, mu_j), x_{2k+1} = fma(-sigma_j, z_kj, mu_j); fit = F(x);
@@ -286,7 +291,7 @@ int evox_es_step(evox_state *state, int64_t n_gens);
  * mu as the solution. */
 int evox_pgpe_step(evox_state *state, int64_t n_gens);
 
-/* n_gens generations of CMA-ES (Table II; Sec. V-A runs it on Sphere up to
+/* n_gens generations of CMA-ES (Table II; Sec. VII-A-1 runs it on Sphere up to
  * D = 16384) in the matrix-adaptation form of Beyer and Sendhoff (IEEE TEVC
  * 21(5), 2017), with Hansen's default constants: mu = floor(N/2) parents,
  * weights w_i ~ ln(mu + 1/2) - ln i summing to one, mu_eff = 1 / sum w_i^2,
@@ -309,7 +314,7 @@ int evox_pgpe_step(evox_state *state, int64_t n_gens);
  * as the solution. */
 int evox_maes_step(evox_state *state, int64_t n_gens);
 
-/* n_gens generations of NSGA-II (Table II; Sec. V-A runs it on DTLZ1) after
+/* n_gens generations of NSGA-II (Table II; Sec. VII-A-2 runs it on DTLZ1) after
  * Deb, Pratap, Agarwal and Meyarivan (IEEE TEVC 6(2), 2002).  Generation t:
  *   - offspring pair p < N/2 from two crowded binary tournaments (candidates
  *     floor(w_q N / 2^32) for the words w_0..w_3 of Philox(seed, (0, p, t,

@@ -844,7 +844,7 @@ void evox_ref_gemm(int ta, int tb, int64_t M, int64_t N, int64_t K, float alpha,
 }
 
 /* ------------------------------------------------------------------------ */
-/* CMA-ES (Table II; the ES of the scaling experiment of Sec. V-A) in its    */
+/* CMA-ES (Table II; an ES of the scaling experiment of Sec. VII-A-1) in its */
 /* matrix-adaptation form, MA-ES (Beyer and Sendhoff, IEEE TEVC 21(5),       */
 /* 2017): the transformation M with M M^T in the role of the covariance      */
 /* matrix is adapted directly, so sampling needs no eigendecomposition.      */
@@ -1035,7 +1035,7 @@ int evox_ref_maes_step(const evox_ref_params *P, int64_t t0, int64_t n_gens, flo
 }
 
 /* ------------------------------------------------------------------------ */
-/* NSGA-II (Table II; the multi-objective scaling experiment of Sec. V-A     */
+/* NSGA-II (Table II; the multi-objective experiment of Sec. VII-A-2         */
 /* runs it on DTLZ1) following Deb, Pratap, Agarwal and Meyarivan, IEEE TEVC */
 /* 6(2), 2002: crowded binary tournaments, simulated binary crossover and    */
 /* polynomial mutation, non-dominated sorting of parents and offspring       */

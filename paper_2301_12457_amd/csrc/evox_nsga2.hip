@@ -1,5 +1,5 @@
 // NSGA-II on DTLZ1 (Table II; the multi-objective scaling experiment of
-// Sec. V-A, whose speed-up the paper attributes to computing the dominance
+// Sec. VII-A-2, whose speed-up the paper attributes to computing the dominance
 // relations in parallel).  Deb, Pratap, Agarwal, Meyarivan (2002):
 //   variation   crowded binary tournaments, simulated binary crossover and
 //               polynomial mutation (one thread per pair and variable, fp64);

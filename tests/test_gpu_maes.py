@@ -229,3 +229,95 @@ def test_full_size_first_generation(evox_gpu, ref):
     assert np.allclose(Mr, Mc, rtol=1e-5, atol=1e-7), np.abs(Mr - Mc).max()
     sig = float(g.sigma.cpu()[0])
     assert np.isfinite(sig) and 0 < sig
+
+
+def test_full_size_dense_matrix(evox_gpu, ref):
+    """N = 100, D = 16384 (the benchmark shape) from a seeded dense,
+    non-identity M pushed to the GPU at generation 7.  A plain oracle
+    generation costs ~10^10 operations at this D, so the reference is
+    composed from the oracle's own pieces -- its deviates, its evaluation and
+    its constants -- and fp64 matrix products (BLAS) that follow the
+    generation's definition: d_k = M z_k, samples fma(sigma, d_k, y), parents
+    in the argmin order, y' = y + sigma sum w d, s' = (1 - c_s) s + sqrt(mu_eff
+    c_s (2 - c_s)) sum w z, sigma' by path length, and on 48 sampled rows
+    M' = M T in the rank-(mu + 1) form (equal to M T, an oracle pin).  The GPU
+    must match within the bounds of the lockstep test: every sample's
+    fitness, the parents, y', s', sigma' and the sampled rows of M' (so both
+    the split-K sampling product and the rank pass are compared element by
+    element at the benchmark shape).  At this D the default learning rates
+    are ~1e-7 (c_1, c_w ~ 2 / D^2), so one generation moves M by about one
+    fp32 ulp: the rows are checked to their bound, the steps (through every
+    sample's fitness, the center and the path) carry the product's test."""
+    from paper_2301_12457_amd.workloads import normal_matrix_np
+    N, D, seed, t, fn = 100, 16384, 10, 7, SPHERE
+    M = normal_matrix_np(D, D, 0.0, 0.5 / math.sqrt(D), 77)
+    M[np.arange(D), np.arange(D)] += np.float32(1.0)
+    y = normal_matrix_np(1, D, 0.0, 2.0, 78)[0]
+    s0 = normal_matrix_np(1, D, 0.0, 0.3, 79)[0]
+    sig0 = np.float32(0.7)
+    g = evox_gpu.Swarm(evox_gpu.make_params(evox_gpu.MAES, fn, N, D, -5.0, 5.0, seed=seed, es_sigma=1.0))
+    g.mat[:, :D] = torch.from_numpy(M).cuda()
+    g.x[:D] = torch.from_numpy(y).cuda()
+    g.v[:D] = torch.from_numpy(s0).cuda()
+    g.sigma[:] = float(sig0)
+    g.set_generation(t)
+    g.step(1)
+    torch.cuda.synchronize()
+    mu, w, c = ref.maes_consts(N, D)
+    z = ref.maes_deviates(seed, t, N, D).astype(np.float64)
+    M64 = M.astype(np.float64)
+    d = (z @ M64.T).astype(np.float32).astype(np.float64)          # d_k = M z_k, rounded once
+    X = (np.float64(sig0) * d + y.astype(np.float64)).astype(np.float32)
+    f_ref = ref.evaluate(fn, X).astype(np.float64)
+    # bounds (as in the lockstep test): deviates within 2e-6 max(1, |z|), the
+    # steps within (gamma_D + 2e-6) |M| max(1, |z|) + ulp
+    Mabs = np.abs(M64)
+    dz = 2e-6 * np.maximum(1.0, np.abs(z))
+    dd = (gamma(D) + 2e-6) * (np.maximum(1.0, np.abs(z)) @ Mabs.T) + ulp(d)
+    del Mabs
+    dx = float(sig0) * dd + ulp(X)
+    fb = (grad_bound(fn, np.abs(X.astype(np.float64)) + dx) * dx).sum(1)
+    ftol = 2 * (fb + tol(fn, np.abs(X.astype(np.float64)) + dx, f_ref))
+    f_gpu = g.fit.cpu().numpy().astype(np.float64)
+    bad = np.nonzero(np.abs(f_gpu - f_ref) > ftol)[0]
+    assert bad.size == 0, f"sample fitness off at {bad[:5]}"
+    order = np.lexsort((np.arange(N), f_ref))
+    gorder = np.lexsort((np.arange(N), f_gpu))
+    assert np.array_equal(gorder[:mu], order[:mu]), "parents differ (not expected at this state)"
+    par = order[:mu]
+    zp, dp, ddp, dzp = z[par], d[par], dd[par], dz[par]
+    zw, dw = w @ zp, w @ dp
+    y1 = (y.astype(np.float64) + float(sig0) * dw).astype(np.float32)
+    cz = math.sqrt(c["mu_eff"] * c["c_s"] * (2 - c["c_s"]))
+    s1 = ((1 - c["c_s"]) * s0.astype(np.float64) + cz * zw).astype(np.float32)
+    nrm = float(np.linalg.norm(s1.astype(np.float64)))
+    sig1 = float(sig0) * math.exp(c["c_s"] / c["d_s"] * (nrm / c["chi"] - 1.0))
+    y_gpu = g.x[:D].cpu().numpy().astype(np.float64)
+    yb = float(sig0) * (w @ ddp) + 2 * ulp(y1) + float(sig0) * gamma(mu) * (w @ np.abs(dp))
+    assert np.all(np.abs(y_gpu - y1) <= yb), "center"
+    s_gpu = g.v[:D].cpu().numpy().astype(np.float64)
+    sb = cz * (w @ dzp) + 2 * ulp(s1) + cz * gamma(mu) * (w @ np.abs(zp))
+    assert np.all(np.abs(s_gpu - s1) <= sb), "path"
+    dn = np.linalg.norm(sb) + gamma(D) * nrm
+    assert abs(float(g.sigma.cpu()[0]) - sig1) <= sig1 * (c["c_s"] / c["d_s"] / c["chi"] * dn + 8 * U), "sigma"
+    # M' on sampled rows, rank-(mu + 1) form: beta M + c_1/2 (M s') s'^T + c_w/2 sum w (M z) z^T
+    rows = np.sort(np.random.default_rng(5).choice(D, 48, replace=False))
+    hc1, hcw = c["c_1"] / 2, c["c_w"] / 2
+    beta = 1 - hc1 - hcw
+    s1d = s1.astype(np.float64)
+    Mr = M64[rows]
+    ms = Mr @ s1d
+    Mz = dp[:, rows]                                                  # (M z_r)_i = d_r,i
+    M1 = beta * Mr + hc1 * np.outer(ms, s1d) + hcw * (w[:, None] * Mz).T @ zp
+    # bound: the terms' errors (steps, path) plus gamma_{mu+2} of their magnitudes
+    W = hcw * w[:, None]
+    Mrabs = np.abs(Mr)
+    dms = (1 - c["c_s"]) * gamma(D) * (Mrabs @ np.abs(s0.astype(np.float64))) + cz * (w @ ddp[:, rows]) \
+        + Mrabs @ (sb + ulp(s1d)) + ulp(ms)
+    err = (W * ddp[:, rows]).T @ np.abs(zp) + (W * np.abs(dp[:, rows])).T @ dzp \
+        + hc1 * (np.outer(dms, np.abs(s1d)) + np.outer(np.abs(ms), sb))
+    mag = (W * np.abs(dp[:, rows])).T @ np.abs(zp) + hc1 * np.outer(np.abs(ms), np.abs(s1d)) + beta * Mrabs
+    Mb = err + gamma(mu + 2) * mag + 2 * U * mag + 2 * ulp(M1)
+    M_gpu = g.mat[torch.from_numpy(rows).cuda()][:, :D].cpu().numpy().astype(np.float64)
+    bad = np.argwhere(np.abs(M_gpu - M1) > Mb)
+    assert bad.size == 0, f"matrix off at {bad[:5].tolist()}"
