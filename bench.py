@@ -55,10 +55,11 @@ def traffic_from_profile(name):
                      t["write_kib_per_dispatch"] * t["write_scale"])
 
 
-def pso_bytes_per_launch(w, launches, improved_rows):
+def pso_bytes_per_generation(w, evaluations, improved_rows):
     # read x, v, pbest and write x, v (20 B per element); read pfit (4 B per
-    # row); write pbest row and pfit of each improved row
-    imp = improved_rows / max(launches, 1)
+    # row); write pbest row and pfit of each improved row (the kernels' count
+    # over `evaluations` generations)
+    imp = improved_rows / max(evaluations, 1)
     return 20.0 * w.N * w.D + 4.0 * w.N + (4.0 * w.D + 4.0) * imp
 
 
@@ -441,8 +442,10 @@ def measure(torch, evox, w, steps, warmup, ldx):
                         "generation_us": round(gen_s * 1e6, 2), "launches": launches,
                         "algorithmic_ops_per_generation": ops}
         elif launches > 0:
+            # per generation of the timed launches (a fused launch is one
+            # generation; a small swarm's one-block launch is a whole step)
             avg_ms = fused_ms / launches
-            bytes_per = {"pso": lambda: pso_bytes_per_launch(w, launches, improved),
+            bytes_per = {"pso": lambda: pso_bytes_per_generation(w, steps * w.gens, improved),
                          "cso": lambda: cso_bytes_per_launch(w),
                          "de": lambda: de_bytes_per_launch(w)}[w.algo]()
             achieved = bytes_per / (avg_ms / 1e3) / 1e9
@@ -458,7 +461,14 @@ def measure(torch, evox, w, steps, warmup, ldx):
                 # x, v), without the rows whose personal best improved
                 floor_bytes = 20.0 * w.N * w.D
                 roofline["frac_floor_20B"] = round(floor_bytes / (avg_ms / 1e3) / 1e9 / HBM_PEAK_GBS, 4)
-                roofline["improved_rows_per_launch"] = round(improved / launches, 1)
+                roofline["improved_rows_per_generation"] = round(improved / (steps * w.gens), 1)
+                if launches == steps * w.gens:
+                    # the one-block kernel: one launch per step, the figures
+                    # above are per generation
+                    roofline["kernel"] = "k_pso_small (one block, a whole step per launch)"
+                    roofline["avg_launch_us"] = round(fused_ms / steps * 1e3, 2)
+                    roofline["launches"] = steps
+                    roofline["generation_us"] = round(avg_ms * 1e3, 3)
     else:
         bytes_per = 4.0 * w.N * w.D + 4.0 * w.N
         achieved = bytes_per / (ms / 1e3) / 1e9

@@ -469,8 +469,10 @@ int evox_philox_fill(uint64_t seed, uint32_t c1, uint32_t c2, uint32_t c3, int64
 /* Timing of the generation kernels with HIP events on the state's stream.
  * evox_profile(state, 1) starts recording (clears the totals), 0 stops.
  * evox_profile_read waits for the stream and returns the summed duration of
- * the fused generation-kernel launches, their count, and the number of rows
- * whose personal best improved in those launches (PSO). */
+ * the timed generation-kernel launches, the number of generations those
+ * launches performed (one per fused launch; a small PSO swarm, N D <= 16384,
+ * runs a whole call in one launch), and the number of rows whose personal
+ * best improved in every evaluation since profiling started (PSO). */
 int evox_profile(evox_state *state, int enable);
 int evox_profile_read(evox_state *state, double *fused_ms, int64_t *fused_launches,
                       int64_t *improved_rows);

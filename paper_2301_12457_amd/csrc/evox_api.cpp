@@ -315,6 +315,7 @@ struct evox_state {
     bool prof;
     std::vector<std::pair<hipEvent_t, hipEvent_t>> ev;
     size_t ev_used;
+    int64_t prof_gens;  // generations performed by the timed launches
     uint64_t improved_base;
 };
 
@@ -326,11 +327,13 @@ T *at(void *base, size_t off)
     return reinterpret_cast<T *>(static_cast<char *>(base) + off);
 }
 
-// Enqueue `launch` bracketed by profiling events when enabled.
+// Enqueue `launch` bracketed by profiling events when enabled; the launch
+// performs `gens` generations.
 template <typename F>
-hipError_t timed(evox_state *s, F &&launch)
+hipError_t timed(evox_state *s, F &&launch, int64_t gens = 1)
 {
     if (!s->prof) return launch();
+    s->prof_gens += gens;
     if (s->ev_used == s->ev.size()) {
         hipEvent_t a, b;
         hipError_t e = hipEventCreate(&a);
@@ -558,6 +561,7 @@ int evox_state_create(const evox_params *params, const evox_buffers *b, void *hi
     }
     s->prof = false;
     s->ev_used = 0;
+    s->prof_gens = 0;
     s->improved_base = 0;
     if (P.algo == EVOX_CSO) {
         // persistent grid for the pair kernel: every block resident at once
@@ -817,6 +821,14 @@ int evox_pso_step(evox_state *s, int64_t n_gens)
     const int fn = s->P.fn_id;
     PsoArgs a = pso_args(s);
     hipError_t e;
+    if (pl.L.G <= 64 && s->P.N * s->P.D <= kPsoSmallElems && s->P.ldx <= kPsoSmallMaxLdx) {
+        // a small swarm: the whole call in one block, one launch
+        a.t = (uint32_t)s->t;
+        e = timed(s, [&] { return launch_pso_small(fn, pl.L, a, n_gens, s->B.gbest, s->best, s->stream); }, n_gens);
+        if (e != hipSuccess) return hip_fail(e, "pso generations");
+        s->t += n_gens;
+        return EVOX_OK;
+    }
     // generation t: evaluate x_t, personal and global bests
     if ((e = launch_pso(fn, pl.L, PSO_EVAL, a, pl.grid, s->stream)) != hipSuccess) return hip_fail(e, "pso eval");
     if ((e = launch_select(s->slots, s->B.pbest, s->P.ldx, s->B.gbest, s->best, nullptr, nullptr,
@@ -1292,6 +1304,7 @@ int evox_profile(evox_state *s, int enable)
     if (!s) return fail(EVOX_EINVAL, "state is null");
     if (enable) {
         s->ev_used = 0;
+        s->prof_gens = 0;
         DevBest h{};
         hipError_t e = hipMemcpyAsync(&h, s->best, sizeof h, hipMemcpyDeviceToHost, s->stream);
         if (e == hipSuccess) e = hipStreamSynchronize(s->stream);
@@ -1318,7 +1331,7 @@ int evox_profile_read(evox_state *s, double *fused_ms, int64_t *fused_launches, 
     e = hipMemcpy(&h, s->best, sizeof h, hipMemcpyDeviceToHost);
     if (e != hipSuccess) return hip_fail(e, "profile read");
     if (fused_ms) *fused_ms = ms;
-    if (fused_launches) *fused_launches = (int64_t)s->ev_used;
+    if (fused_launches) *fused_launches = s->prof_gens;
     if (improved_rows) *improved_rows = (int64_t)(h.improved - s->improved_base);
     return EVOX_OK;
 }

@@ -714,6 +714,13 @@ hipError_t launch_pso(int fn, Layout L, int mode, const PsoArgs &a, int grid, hi
     EVOX_FN_SWITCH(EVOX_CALL_PSO)
 }
 
+hipError_t launch_pso_small(int fn, Layout L, const PsoArgs &a, int64_t n_gens, float *gbest_out, DevBest *best,
+                            hipStream_t s)
+{
+#define EVOX_CALL_PSO_SMALL(F) launch_pso_small_t<F>(L, a, n_gens, gbest_out, best, s)
+    EVOX_FN_SWITCH(EVOX_CALL_PSO_SMALL)
+}
+
 hipError_t launch_eval(int fn, Layout L, bool vec, const EvalArgs &a, int grid, hipStream_t s)
 {
 #define EVOX_CALL_EVAL(F) launch_eval_t<F>(L, vec, a, grid, s)

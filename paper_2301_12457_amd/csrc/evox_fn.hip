@@ -9,6 +9,7 @@
 namespace evox {
 
 template hipError_t launch_pso_t<EVOX_FN>(Layout, int, const PsoArgs &, int, hipStream_t);
+template hipError_t launch_pso_small_t<EVOX_FN>(Layout, const PsoArgs &, int64_t, float *, DevBest *, hipStream_t);
 template hipError_t launch_eval_t<EVOX_FN>(Layout, bool, const EvalArgs &, int, hipStream_t);
 template hipError_t launch_cso_t<EVOX_FN>(Layout, const CsoArgs &, int, hipStream_t);
 template hipError_t launch_de_t<EVOX_FN>(Layout, const DeArgs &, int, hipStream_t);

@@ -32,6 +32,34 @@
 namespace evox {
 
 // ---------------------------------------------------------------------------
+// The PSO move of float4 chunk c of a row at generation a.t: r1, r2 from
+// Philox stream 2 (counters 2c and 2c + 1), vn = fma(c2 r2, g - x, fma(c1 r1,
+// p - x, w v)), optional clamps, x + vn; elements past D give zeros.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ void pso_move4(const PsoArgs &a, int64_t row, int64_t c, float4 xv, float4 vv,
+                                          float4 pv, float4 gv, float4 &xn, float4 &vn)
+{
+    const U4 r1 = philox((uint32_t)(2 * c), (uint32_t)row, a.t, STREAM_PSO, a.k0, a.k1);
+    const U4 r2 = philox((uint32_t)(2 * c + 1), (uint32_t)row, a.t, STREAM_PSO, a.k0, a.k1);
+    float xo[4], vo[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        const float xe = comp(xv, e);
+        const float A = a.c1 * wcomp(r1, e);
+        const float Bc = a.c2 * wcomp(r2, e);
+        float nv = fmaf(Bc, comp(gv, e) - xe, fmaf(A, comp(pv, e) - xe, a.w * comp(vv, e)));
+        if (a.vclamp) nv = fminf(fmaxf(nv, -a.vmax), a.vmax);
+        float nx = xe + nv;
+        if (a.xclamp) nx = fminf(fmaxf(nx, a.lb), a.ub);
+        const bool in = 4 * c + e < a.D;
+        xo[e] = in ? nx : 0.0f;
+        vo[e] = in ? nv : 0.0f;
+    }
+    xn = make_float4(xo[0], xo[1], xo[2], xo[3]);
+    vn = make_float4(vo[0], vo[1], vo[2], vo[3]);
+}
+
+// ---------------------------------------------------------------------------
 // The PSO generation kernel (modes above).  One group of block_for(G) / G
 // rows per block (grid-stride only beyond kMaxGrid blocks); the loop bound is
 // uniform over the block, so the barriers inside row_fitness are reached by
@@ -71,26 +99,10 @@ __global__ __launch_bounds__(block_for(G)) void k_pso(PsoArgs a)
                     const float4 vv = ld_row(a.v + off, a.nt);
                     const float4 pv = ld_row(a.p + off, a.nt);
                     const float4 gv = *reinterpret_cast<const float4 *>(a.gbest + 4 * c);
-                    const U4 r1 = philox((uint32_t)(2 * c), (uint32_t)row, a.t, STREAM_PSO, a.k0, a.k1);
-                    const U4 r2 =
-                        philox((uint32_t)(2 * c + 1), (uint32_t)row, a.t, STREAM_PSO, a.k0, a.k1);
-                    float xo[4], vo[4];
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        const float xe = comp(xv, e);
-                        const float A = a.c1 * wcomp(r1, e);
-                        const float Bc = a.c2 * wcomp(r2, e);
-                        float nv = fmaf(Bc, comp(gv, e) - xe, fmaf(A, comp(pv, e) - xe, a.w * comp(vv, e)));
-                        if (a.vclamp) nv = fminf(fmaxf(nv, -a.vmax), a.vmax);
-                        float nx = xe + nv;
-                        if (a.xclamp) nx = fminf(fmaxf(nx, a.lb), a.ub);
-                        const bool in = 4 * c + e < a.D;
-                        xo[e] = in ? nx : 0.0f;
-                        vo[e] = in ? nv : 0.0f;
-                    }
-                    xn = make_float4(xo[0], xo[1], xo[2], xo[3]);
+                    float4 vn;
+                    pso_move4(a, row, c, xv, vv, pv, gv, xn, vn);
                     st_row(a.x + off, xn, a.nt);
-                    st_row(a.v + off, make_float4(vo[0], vo[1], vo[2], vo[3]), a.nt);
+                    st_row(a.v + off, vn, a.nt);
                 } else {
                     xn = xv;
                 }
@@ -126,6 +138,107 @@ __global__ __launch_bounds__(block_for(G)) void k_pso(PsoArgs a)
     if constexpr (EVAL) {
         block_min_key(best, nimp, sk, sc);
         if (tid == 0) slot_commit(a.slots, best, nimp);
+    }
+}
+
+// ---------------------------------------------------------------------------
+// A whole n-generation PSO call in one block, for swarms that one CU
+// evaluates and moves in a few microseconds (N D <= kPsoSmallElems, a row in
+// at most one wave): the grid-wide step between evaluation and move (the
+// global best) becomes a block barrier, so the call is one launch instead of
+// 2 n + 1.  Per generation t: evaluation of x_t and personal bests with the
+// row layout and reduction of k_pso (the same fitness bits, hence the same
+// decisions), the lexicographic minimum of (pfit, row) over the block, the
+// gbest row copied from pbest (to LDS and to gbest_out), then the move.
+// ---------------------------------------------------------------------------
+template <int FN, int G, int MAXIT>
+__global__ __launch_bounds__(kPsoSmallBlock) void k_pso_small(PsoArgs a, int64_t n_gens, float *gbest_out,
+                                                              DevBest *best)
+{
+    static_assert(G <= 64, "a row within one wave");
+    constexpr int B = kPsoSmallBlock, RPB = B / G;
+    __shared__ __align__(16) float gb[kPsoSmallMaxLdx];
+    __shared__ uint64_t sk[B / 64];
+    __shared__ uint32_t sc[B / 64];
+    __shared__ int64_t sel;
+    const int tid = threadIdx.x, g = tid % G, slot = tid / G;
+    const int64_t C4 = (a.D + 3) >> 2;
+    const int64_t CW = a.ldx / 4 < (int64_t)G * MAXIT ? a.ldx / 4 : (int64_t)G * MAXIT;
+    const uint32_t t0 = a.t;
+    for (int64_t k = 0; k < n_gens; ++k) {
+        a.t = t0 + (uint32_t)k;
+        // evaluate x_t, personal bests
+        uint64_t bk = kNoKey;
+        uint32_t nimp = 0;
+        for (int64_t rb = 0; rb < a.N; rb += RPB) {  // uniform trip count
+            const int64_t row = rb + slot;
+            const bool active = row < a.N;
+            float4 xr[MAXIT];
+#pragma unroll
+            for (int it = 0; it < MAXIT; ++it) {
+                const int64_t c = g + (int64_t)G * it;
+                xr[it] = active && c < C4 ? *reinterpret_cast<const float4 *>(a.x + row * a.ldx + 4 * c)
+                                          : make_float4(0.f, 0.f, 0.f, 0.f);
+            }
+            const float f = row_fitness<FN, G, MAXIT>(xr, g, a.D, nullptr, nullptr);
+            if (active) {
+                const float pold = a.pf[row];
+                const bool imp = f < pold;
+                if (imp) {
+#pragma unroll
+                    for (int it = 0; it < MAXIT; ++it) {
+                        const int64_t c = g + (int64_t)G * it;
+                        if (c < CW) *reinterpret_cast<float4 *>(a.p + row * a.ldx + 4 * c) = xr[it];
+                    }
+                }
+                if (g == 0) {
+                    if (imp) a.pf[row] = f;
+                    if (a.fit) a.fit[row] = f;
+                    const uint64_t key = sel_key(imp ? f : pold, row);
+                    bk = key < bk ? key : bk;
+                    nimp += imp ? 1u : 0u;
+                }
+            }
+        }
+        block_min_key(bk, nimp, sk, sc);
+        if (tid == 0) {
+            const int64_t i = bk == kNoKey ? 0 : key_index(bk);
+            best->f = key_value(bk);
+            best->i = i;
+            best->improved += nimp;
+            sel = i;
+        }
+        __syncthreads();
+        for (int64_t j = tid; j < a.ldx; j += B) {
+            const float v = a.p[sel * a.ldx + j];
+            gb[j] = v;
+            gbest_out[j] = v;
+        }
+        __syncthreads();
+        // move of generation t
+        for (int64_t rb = 0; rb < a.N; rb += RPB) {
+            const int64_t row = rb + slot;
+            if (row >= a.N) continue;
+#pragma unroll
+            for (int it = 0; it < MAXIT; ++it) {
+                const int64_t c = g + (int64_t)G * it;
+                const int64_t off = row * a.ldx + 4 * c;
+                if (c < C4) {
+                    const float4 xv = *reinterpret_cast<const float4 *>(a.x + off);
+                    const float4 vv = *reinterpret_cast<const float4 *>(a.v + off);
+                    const float4 pv = *reinterpret_cast<const float4 *>(a.p + off);
+                    const float4 gv = *reinterpret_cast<const float4 *>(gb + 4 * c);
+                    float4 xn, vn;
+                    pso_move4(a, row, c, xv, vv, pv, gv, xn, vn);
+                    *reinterpret_cast<float4 *>(a.x + off) = xn;
+                    *reinterpret_cast<float4 *>(a.v + off) = vn;
+                } else if (c < CW) {
+                    *reinterpret_cast<float4 *>(a.x + off) = make_float4(0.f, 0.f, 0.f, 0.f);
+                    *reinterpret_cast<float4 *>(a.v + off) = make_float4(0.f, 0.f, 0.f, 0.f);
+                }
+            }
+        }
+        __syncthreads();  // the next generation reads every moved row
     }
 }
 
@@ -898,6 +1011,26 @@ hipError_t launch_pso_t(Layout L, int mode, const PsoArgs &a, int grid, hipStrea
                 default: return hipErrorInvalidValue;
             }
         }
+    }
+    return hipGetLastError();
+}
+
+template <int FN>
+hipError_t launch_pso_small_t(Layout L, const PsoArgs &a, int64_t n_gens, float *gbest_out, DevBest *best,
+                              hipStream_t s)
+{
+    if (L.maxit != LAYOUT_PSO) return hipErrorInvalidValue;
+    switch (L.G) {
+#define EVOX_SMALL(GG)                                                                                        \
+    case GG: hipLaunchKernelGGL((k_pso_small<FN, GG, LAYOUT_PSO>), dim3(1), dim3(kPsoSmallBlock), 0, s, a, \
+                                n_gens, gbest_out, best); break;
+        EVOX_SMALL(4)
+        EVOX_SMALL(8)
+        EVOX_SMALL(16)
+        EVOX_SMALL(32)
+        EVOX_SMALL(64)
+#undef EVOX_SMALL
+        default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
 }

@@ -229,6 +229,16 @@ struct CsoArgs {
 };
 
 hipError_t launch_pso(int fn, Layout L, int mode, const PsoArgs &a, int grid, hipStream_t s);
+// A whole n-generation PSO call in one block of kPsoSmallBlock threads, for
+// N D <= kPsoSmallElems, rows in at most 64 lanes and ldx <= kPsoSmallMaxLdx.
+constexpr int kPsoSmallBlock = 1024;
+constexpr int64_t kPsoSmallElems = 16384;
+constexpr int64_t kPsoSmallMaxLdx = 1024;
+hipError_t launch_pso_small(int fn, Layout L, const PsoArgs &a, int64_t n_gens, float *gbest_out, DevBest *best,
+                            hipStream_t s);
+template <int FN>
+hipError_t launch_pso_small_t(Layout L, const PsoArgs &a, int64_t n_gens, float *gbest_out, DevBest *best,
+                              hipStream_t s);
 template <int FN>
 hipError_t launch_pso_t(Layout L, int mode, const PsoArgs &a, int grid, hipStream_t s);
 template <int FN>
