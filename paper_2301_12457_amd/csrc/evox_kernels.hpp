@@ -149,7 +149,9 @@ __global__ __launch_bounds__(block_for(G)) void k_pso(PsoArgs a)
 // 2 n + 1.  Per generation t: evaluation of x_t and personal bests with the
 // row layout and reduction of k_pso (the same fitness bits, hence the same
 // decisions), the lexicographic minimum of (pfit, row) over the block, the
-// gbest row copied from pbest (to LDS and to gbest_out), then the move.
+// gbest row from pbest through LDS, then the move.  When every row fits in
+// one pass of the block the swarm stays in registers for the whole call;
+// otherwise the rows are walked in passes through global memory.
 // ---------------------------------------------------------------------------
 template <int FN, int G, int MAXIT>
 __global__ __launch_bounds__(kPsoSmallBlock) void k_pso_small(PsoArgs a, int64_t n_gens, float *gbest_out,
@@ -165,6 +167,84 @@ __global__ __launch_bounds__(kPsoSmallBlock) void k_pso_small(PsoArgs a, int64_t
     const int64_t C4 = (a.D + 3) >> 2;
     const int64_t CW = a.ldx / 4 < (int64_t)G * MAXIT ? a.ldx / 4 : (int64_t)G * MAXIT;
     const uint32_t t0 = a.t;
+    for (int64_t j = tid; j < a.ldx; j += B) gb[j] = 0.0f;  // padding past the lanes' reach
+    __syncthreads();
+    if (a.N <= RPB) {
+        // every row in one pass of the block: x, v, pbest and pfit stay in
+        // registers for the whole call, only the gbest row goes through LDS
+        const int64_t row = slot;
+        const bool active = row < a.N;
+        float4 xr[MAXIT], vr[MAXIT], pr[MAXIT];
+#pragma unroll
+        for (int it = 0; it < MAXIT; ++it) {
+            const int64_t c = g + (int64_t)G * it, off = row * a.ldx + 4 * c;
+            const bool in = active && c < C4;
+            const float4 z = make_float4(0.f, 0.f, 0.f, 0.f);
+            xr[it] = in ? *reinterpret_cast<const float4 *>(a.x + off) : z;
+            vr[it] = in ? *reinterpret_cast<const float4 *>(a.v + off) : z;
+            pr[it] = in ? *reinterpret_cast<const float4 *>(a.p + off) : z;
+        }
+        float pf = active ? a.pf[row] : 0.0f, f = 0.0f;
+        uint64_t bk = kNoKey;
+        uint32_t nimp = 0, total_imp = 0;
+        for (int64_t k = 0; k < n_gens; ++k) {
+            a.t = t0 + (uint32_t)k;
+            f = row_fitness<FN, G, MAXIT>(xr, g, a.D, nullptr, nullptr);
+            const bool imp = active && f < pf;
+            if (imp) {
+#pragma unroll
+                for (int it = 0; it < MAXIT; ++it) pr[it] = xr[it];
+                pf = f;
+            }
+            bk = active && g == 0 ? sel_key(pf, row) : kNoKey;
+            nimp = imp && g == 0 ? 1u : 0u;
+            block_min_key(bk, nimp, sk, sc);
+            if (tid == 0) {
+                sel = bk == kNoKey ? 0 : key_index(bk);
+                total_imp += nimp;
+            }
+            __syncthreads();
+            if (row == sel) {
+#pragma unroll
+                for (int it = 0; it < MAXIT; ++it) {
+                    const int64_t c = g + (int64_t)G * it;
+                    if (c < CW) *reinterpret_cast<float4 *>(gb + 4 * c) = pr[it];
+                }
+            }
+            __syncthreads();
+#pragma unroll
+            for (int it = 0; it < MAXIT; ++it) {
+                const int64_t c = g + (int64_t)G * it;
+                if (active && c < C4) {
+                    const float4 gv = *reinterpret_cast<const float4 *>(gb + 4 * c);
+                    pso_move4(a, row, c, xr[it], vr[it], pr[it], gv, xr[it], vr[it]);
+                }
+            }
+            // the next write of gb follows the barriers of the next block minimum
+        }
+        if (active) {
+#pragma unroll
+            for (int it = 0; it < MAXIT; ++it) {
+                const int64_t c = g + (int64_t)G * it, off = row * a.ldx + 4 * c;
+                if (c < CW) {
+                    *reinterpret_cast<float4 *>(a.x + off) = xr[it];
+                    *reinterpret_cast<float4 *>(a.v + off) = vr[it];
+                    *reinterpret_cast<float4 *>(a.p + off) = pr[it];
+                }
+            }
+            if (g == 0) {
+                a.pf[row] = pf;
+                if (a.fit) a.fit[row] = f;
+            }
+        }
+        for (int64_t j = tid; j < a.ldx; j += B) gbest_out[j] = gb[j];
+        if (tid == 0) {
+            best->f = key_value(bk);
+            best->i = sel;
+            best->improved += total_imp;
+        }
+        return;
+    }
     for (int64_t k = 0; k < n_gens; ++k) {
         a.t = t0 + (uint32_t)k;
         // evaluate x_t, personal bests
