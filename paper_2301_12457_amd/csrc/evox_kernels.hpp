@@ -114,9 +114,13 @@ __global__ __launch_bounds__(block_for(G)) void k_pso(PsoArgs a)
             xr[it] = xn;
         }
         if constexpr (EVAL) {
+            // the personal-best fitness is read before the evaluation's
+            // block barriers: when a row spans several waves, lane 0 of its
+            // first wave rewrites it below, and a wave that read it after
+            // that store would take the opposite decision for its chunks
+            const float pold = active ? a.pf[row] : 0.0f;
             const float f = row_fitness<FN, G, MAXIT>(xr, g, a.D, nbr, red);
             if (active) {
-                const float pold = a.pf[row];
                 const bool imp = f < pold;
                 if (imp) {
 #pragma unroll

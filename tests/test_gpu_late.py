@@ -129,7 +129,7 @@ def test_pso_two_generations_late(evox_gpu, ref, name, t, spread):
     g.profile(True)
     g.step(2)
     r.step(1)
-    pf_mid, x_mid = r.pf.copy(), r.x.copy()
+    pf_mid, x_mid, p_mid = r.pf.copy(), r.x.copy(), r.p.copy()
     f_mid = ref.evaluate(fn, x_mid)        # the oracle's fitness of x_t
     imp_mid_ref = int((f_mid < pf_mid).sum())
     imp0_ref = int((pf_mid < pf).sum())
@@ -139,6 +139,14 @@ def test_pso_two_generations_late(evox_gpu, ref, name, t, spread):
     same = (pg == r.p).all(1)
     diff = np.nonzero(~same)[0]
     ties = np.abs(f_mid[diff].astype(np.float64) - pf_mid[diff]) <= tol(fn, x_mid[diff], pf_mid[diff])
+    if not ties.all():
+        pfg = g.pfit.cpu().numpy()
+        for i in diff[~ties][:4]:
+            cols = np.nonzero(pg[i] != r.p[i])[0]
+            print(f"row {i}: {cols.size} columns differ (first {cols[:6]}); pfit {pfg[i]} vs {r.pf[i]}; "
+                  f"generation t: F {f_mid[i]}, pbest before {pf_mid[i]}; the GPU row equals the oracle's "
+                  f"x_t {np.array_equal(pg[i], x_mid[i])}, its pbest before t {np.array_equal(pg[i], p_mid[i])}",
+                  flush=True)
     assert ties.all(), f"rows {diff[~ties][:8]} decided differently without a tolerance tie"
     print(f"{name} t={t}: {diff.size} tolerance ties in the personal-best decisions", flush=True)
     _, _, improved = g.profile_read()
