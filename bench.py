@@ -11,6 +11,7 @@ import hashlib
 import json
 import os
 import sys
+import statistics
 import time
 
 ROOT = os.path.dirname(os.path.abspath(__file__))
@@ -327,7 +328,7 @@ def main():
             if name == w.name:
                 continue
             wc = WORKLOADS[name]
-            r = measure(torch, evox, wc, 5 if wc.algo == "eval" else 2, 1, None)
+            r = measure(torch, evox, wc, 5, 1, None)
             if r["roofline"] is not None and r["roofline"]["bound"] == "hbm":
                 r["roofline"]["frac_of_copy"] = round(r["roofline"]["achieved"] / copy, 4)
             configs.append(r)
@@ -340,7 +341,8 @@ def main():
 
     line = {
         "metric": METRIC, "value": head["value"], "unit": UNIT, "n_gpus": 1, "steps": args.steps,
-        "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
+        "warmup": args.warmup, "ms_per_step": ms, "ms_per_step_median": head["ms_per_step_median"],
+        "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "f32", "data": "synthetic",
         "config": head["config"], "roofline": roofline, "cpu_baseline": base, "configs": configs,
     }
@@ -385,16 +387,20 @@ def measure(torch, evox, w, steps, warmup, ldx):
 
     if swarm is not None:
         swarm.profile(True)
-    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    # one event per step boundary: the total over the K steps is the
+    # measurement, the per-step times give its median
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+    ev0, ev1 = evs[0], evs[-1]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     ev0.record(stream)
-    for _ in range(steps):
+    for k in range(steps):
         step()
-    ev1.record(stream)
+        evs[k + 1].record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     ms = ev0.elapsed_time(ev1) / steps
+    ms_median = statistics.median(evs[k].elapsed_time(evs[k + 1]) for k in range(steps))
     print(f"[bench] {w.name}: timed {steps} steps: {ms:.3f} ms/step (wall {wall:.3f} s)",
           file=sys.stderr, flush=True)
 
@@ -485,7 +491,8 @@ def measure(torch, evox, w, steps, warmup, ldx):
                                   "kernel_over_floor": round(roofline["avg_launch_us"] / f_us, 4)}
     config = {"workload": w.name, "algo": w.algo, "fn": w.fn, "N": w.N, "D": w.D,
               "ldx": (swarm.P.ldx if swarm is not None else w.D), "generations_per_step": gens, "seed": w.seed}
-    result = {"workload": w.name, "value": value, "unit": UNIT, "ms_per_step": ms, "steps": steps,
+    result = {"workload": w.name, "value": value, "unit": UNIT, "ms_per_step": ms, "ms_per_step_median": ms_median,
+              "steps": steps,
               "warmup": warmup, "ms_per_generation": ms / gens, "config": config, "roofline": roofline}
     del swarm
     torch.cuda.empty_cache()
