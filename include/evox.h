@@ -22,8 +22,10 @@
  * evox_profile_read, which synchronize that stream.
  *
  * Ownership: every device buffer is allocated by the caller and only borrowed
- * by the library.  The library allocates no device memory; evox_state_create
- * allocates one host-side handle, freed by evox_state_destroy.
+ * by the library.  The library allocates no device memory (its one device
+ * array, the 32 KiB slots of evox_eval_argmin_noalloc, is static);
+ * evox_state_create allocates one host-side handle, freed by
+ * evox_state_destroy.
  *
  * Errors: every int-returning call returns EVOX_OK (0) or a negative
  * evox_status.  A call that fails validation enqueues nothing and leaves the
