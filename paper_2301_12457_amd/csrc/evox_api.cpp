@@ -80,7 +80,7 @@ struct Plan {
     int perm_batch = 0;
     size_t x2 = 0, fit2 = 0;  // DE: the other population buffer and its fitness
     size_t xalt = 0;          // CSO neighbourhood version: the other population buffer
-    size_t mate = 0, cfit2 = 0;  // CSO swarm version: mate arrays, the other fitness buffer
+    size_t mate = 0, cfit2 = 0;  // CSO: mate arrays, the other fitness buffer
     size_t esrank = 0, espart = 0;  // ES: sample ranks, gradient partial sums
     // MA-ES: deviates, steps, split-K workspace, update factors, parents,
     // weights, path-norm partial sums
@@ -201,18 +201,14 @@ int make_plan(const evox_params *P, Plan *pl)
     p.slots = take(sizeof(SelSlots));
     if (P->algo == EVOX_CSO) {
         const int cap = cso_grid_cap(P->ldx);
-        const bool sweep = P->cso_local == 0;  // the swarm version sweeps ranges of individuals
-        if (sweep) {
-            int64_t ranges = (P->N + kCsoSweep - 1) / kCsoSweep;
-            p.cso_grid = (int)(ranges > cap ? cap : ranges);
-        } else {
-            p.cso_grid = grid_for(P->N / 2 + (P->N & 1), p.L.G, cap);
-        }
+        // both versions sweep ranges of individuals
+        int64_t ranges = (P->N + kCsoSweep - 1) / kCsoSweep;
+        p.cso_grid = (int)(ranges > cap ? cap : ranges);
         p.colsum_grid = grid_for(P->N, p.L.G, cap);
         p.bits = perm_bits(P->N);
-        // permutations (and the swarm version's mate arrays) sorted
-        // kPermBatch generations at a time, within 256 MB
-        const int64_t per = sweep ? 16 : 12;
+        // permutations and their mate arrays sorted kPermBatch generations
+        // at a time, within 256 MB
+        const int64_t per = 16;
         int64_t batch = ((int64_t)256 << 20) / (per * P->N);
         p.perm_batch = (int)(batch < 1 ? 1 : batch > kPermBatch ? kPermBatch : batch);
         const size_t B = (size_t)p.perm_batch, nb = (size_t)1 << p.bits;
@@ -221,10 +217,8 @@ int make_plan(const evox_params *P, Plan *pl)
         p.cursor = take(4 * nb * B);
         p.tkv = take(8 * (size_t)P->N * B);
         p.perm = take(4 * (size_t)P->N * B);
-        if (sweep) {
-            p.mate = take(4 * (size_t)P->N * B);
-            p.cfit2 = take(sizeof(float) * (size_t)P->N);
-        }
+        p.mate = take(4 * (size_t)P->N * B);
+        p.cfit2 = take(sizeof(float) * (size_t)P->N);
         p.xsum_rows = cap;
         p.xsum = take(sizeof(double) * (size_t)cap * (size_t)P->ldx);
         p.s1 = take(sizeof(double) * (size_t)kMeanStages * (size_t)P->ldx);
@@ -297,8 +291,8 @@ struct evox_state {
     DevBest *best;
     SelSlots *slots;
     uint32_t *hist, *offs, *cursor, *perm, *ticket;
-    uint32_t *mate;    // CSO swarm version: mate arrays of the permutation batch
-    float *cfit2;      // CSO swarm version: the other fitness buffer
+    uint32_t *mate;    // CSO: mate arrays of the permutation batch
+    float *cfit2;      // CSO: the other fitness buffer
     uint2 *tkv;
     int64_t perm_t0;  // first generation of the stored permutation batch (-1: none)
     double *xsum, *s1;
@@ -553,8 +547,8 @@ int evox_state_create(const evox_params *params, const evox_buffers *b, void *hi
         s->cursor = at<uint32_t>(b->scratch, pl.cursor);
         s->tkv = at<uint2>(b->scratch, pl.tkv);
         s->perm = at<uint32_t>(b->scratch, pl.perm);
-        s->mate = P.cso_local ? nullptr : at<uint32_t>(b->scratch, pl.mate);
-        s->cfit2 = P.cso_local ? nullptr : at<float>(b->scratch, pl.cfit2);
+        s->mate = at<uint32_t>(b->scratch, pl.mate);
+        s->cfit2 = at<float>(b->scratch, pl.cfit2);
         s->xsum = at<double>(b->scratch, pl.xsum);
         s->s1 = at<double>(b->scratch, pl.s1);
         s->ticket = at<uint32_t>(b->scratch, pl.ticket);
@@ -858,10 +852,11 @@ int evox_cso_step(evox_state *s, int64_t n_gens)
     const Plan &pl = s->pl;
     const bool local = P.cso_local != 0;
     hipError_t e;
-    // the neighbourhood version alternates the positions between x and a
-    // second buffer; the swarm version alternates the fitness between fit and
-    // a second buffer (a generation reads every individual's fitness before
-    // it and writes every one after it)
+    // both versions alternate the fitness between fit and a second buffer (a
+    // generation reads every individual's fitness before it and writes every
+    // one after it); the neighbourhood version also alternates the positions
+    // between x and a second buffer (a loser's mean reads its neighbours'
+    // rows as they were before the generation)
     float *cur = s->B.x, *alt = local ? at<float>(s->B.scratch, pl.xalt) : nullptr;
     float *fcur = s->B.fit;
     for (int64_t k = 0; k < n_gens; ++k) {
@@ -874,8 +869,8 @@ int evox_cso_step(evox_state *s, int64_t n_gens)
         }
         const int64_t slice = (t - s->perm_t0) * P.N;
         float *dst = local ? (cur == s->B.x ? alt : s->B.x) : s->B.x;
-        float *fnext = local ? s->B.fit : (fcur == s->B.fit ? s->cfit2 : s->B.fit);
-        CsoArgs ca{dst, s->B.v, fnext, fcur, s->B.xbar, s->perm + slice, local ? nullptr : s->mate + slice,
+        float *fnext = fcur == s->B.fit ? s->cfit2 : s->B.fit;
+        CsoArgs ca{dst, s->B.v, fnext, fcur, s->B.xbar, s->perm + slice, s->mate + slice,
                    P.N, P.D, P.ldx, P.phi, P.lb, P.ub, P.clamp_x != 0, s->k0, s->k1, (uint32_t)t, s->slots,
                    s->xsum, cur};
         e = timed(s, [&] { return launch_cso(P.fn_id, pl.L, ca, pl.cso_grid, s->stream); });

@@ -580,80 +580,118 @@ __device__ __forceinline__ void cso_sweep_body(const CsoArgs &a)
     acc.write(a.D, a.ldx, a.xsum);
 }
 
-// pairs whose winner and loser a block of the neighbourhood version decides
-// in one phase (the fitness gathers of 64 pairs in flight at once), before
-// its row groups move them
-constexpr int kCsoDecide = 64;
-
 // ---------------------------------------------------------------------------
-// The neighbourhood version's generation, in permutation order: every row of
-// the next population buffer x is written (the losers' new rows and copies
-// of the winners'), the old rows are read from xs, and loser l learns from
-// the fp64 mean of the old rows l - 1, l, l + 1 (modulo N).
+// The neighbourhood version's generation, swept in individual order like
+// the swarm version: the old positions are read from xs and every row of the
+// next population buffer x is written.  Per range of kCsoSweep individuals
+// each one decides from its mate entry and both fitness values (before the
+// generation) whether it lost; the others (winners and the odd one out) are
+// listed first and copied, x_i = xs_i, their fitness carried over; then the
+// losers, listed in index order, learn from their winner's row and from the
+// fp64 mean of the old rows l - 1, l, l + 1 (modulo N, neighbours that the
+// sweep reads around the same time), are written and re-evaluated.  Both
+// lists are in index order, so the column sums' order is deterministic.
 // ---------------------------------------------------------------------------
 template <int FN, int G, int MAXIT>
 __device__ __forceinline__ void cso_local_body(const CsoArgs &a)
 {
-    constexpr int B = block_for(G), RPB = B / G;
+    constexpr int B = block_for(G), RPB = B / G, NW = B / 64, R = kCsoSweep;
+    static_assert(R <= B, "one individual per thread in the decision phase");
     __shared__ float nbr[(FN == FN_ROSENBROCK && G > 64) ? B * MAXIT : 1];
     __shared__ float red[2 * (B / 64)];
     __shared__ uint64_t sk[B / 64];
     __shared__ uint32_t sc[B / 64];
     __shared__ double acc_lds[RPB > 1 ? 4 * MAXIT * B : 1];
+    __shared__ int32_t lst_c[R];            // copied individuals (winners, the odd one out)
+    __shared__ int32_t lst_l[R], lst_w[R];  // losers and their winners
+    __shared__ int32_t ccnt[NW], lcnt[NW];
 
-    const int tid = threadIdx.x, g = tid % G, slot = tid / G;
+    const int tid = threadIdx.x, g = tid % G, slot = tid / G, lane = tid & 63, wave = tid >> 6;
     const int64_t C4 = (a.D + 3) >> 2;
-    const int64_t NP = a.N / 2, NG = NP + (a.N & 1);  // pair groups (+ the unpaired one)
     uint64_t best = kNoKey;
     uint32_t none = 0;
     ColAcc<G, MAXIT> acc(acc_lds);
 
-    // Each phase: the block's threads decide SB pairs (winner, loser, the
-    // winner's fitness) into LDS, then its row groups move them RPB at a
-    // time, so the row gathers wait on no fitness load.
-    constexpr int SB = kCsoDecide > RPB ? kCsoDecide : RPB;
-    static_assert(SB % RPB == 0 && SB <= B, "whole row-group rounds per phase");
-    __shared__ int32_t dw[SB], dl[SB];
-    __shared__ float dfw[SB];
-    for (int64_t sb = (int64_t)blockIdx.x * SB; sb < NG; sb += (int64_t)gridDim.x * SB) {
-        for (int t = tid; t < SB; t += B) {
-            const int64_t k = sb + t;
-            int64_t w = 0, l = 0;
-            float fw = 0.0f;
-            if (k < NP) {
-                const int64_t p0 = a.perm[2 * k], p1 = a.perm[2 * k + 1];
-                const float f0 = a.fit[p0], f1 = a.fit[p1];
-                const bool second = f1 < f0 || (f0 != f0 && f1 == f1);
-                w = second ? p1 : p0;
-                l = second ? p0 : p1;
-                fw = second ? f1 : f0;
-            } else if (k < NG) {
-                w = a.perm[a.N - 1];
-                fw = a.fit[w];
+    for (int64_t base = (int64_t)blockIdx.x * R; base < a.N; base += (int64_t)gridDim.x * R) {
+        bool in = false, loser = false;
+        int32_t me = 0, other = -1;
+        if (tid < R && base + tid < a.N) {
+            const int64_t i = base + tid;
+            const uint32_t m = a.mate[i];
+            const float fi = a.fit_in[i];
+            if (m != kUnpaired) {
+                const int64_t j = m & ~kMateFirst;
+                const float fj = a.fit_in[j];
+                const bool first = (m & kMateFirst) != 0;
+                const float f0 = first ? fi : fj, f1 = first ? fj : fi;
+                const bool second_wins = f1 < f0 || (f0 != f0 && f1 == f1);
+                loser = first ? second_wins : !second_wins;
+                other = (int32_t)j;
             }
-            dw[t] = (int32_t)w;
-            dl[t] = (int32_t)l;
-            dfw[t] = fw;
+            if (!loser) {
+                a.fit[i] = fi;
+                const uint64_t k = sel_key(fi, i);
+                best = k < best ? k : best;
+            }
+            in = true;
+            me = (int32_t)i;
+        }
+        const uint64_t bl = __ballot(loser), bc = __ballot(in && !loser);
+        if (lane == 0) {
+            lcnt[wave] = __popcll(bl);
+            ccnt[wave] = __popcll(bc);
         }
         __syncthreads();
-        for (int r = 0; r < SB / RPB; ++r) {  // uniform trip count: every thread reaches the barriers
-        const int q = r * RPB + slot;
-        const int64_t k = sb + q;
-        const bool active = k < NG;
-        const bool paired = k < NP;
-        const int64_t w = dw[q], l = dl[q];
-        const float fw = dfw[q];
-        float4 xr[MAXIT];
+        int offl = 0, offc = 0, nl = 0, nc = 0;
 #pragma unroll
-        for (int it = 0; it < MAXIT; ++it) {
-            const int64_t c = g + (int64_t)G * it;
-            float4 xn = make_float4(0.f, 0.f, 0.f, 0.f);
-            if (active && c < C4) {
-                const float4 xw = *reinterpret_cast<const float4 *>(a.xs + w * a.ldx + 4 * c);
-                if (paired) {
+        for (int q = 0; q < NW; ++q) {
+            offl += q < wave ? lcnt[q] : 0;
+            offc += q < wave ? ccnt[q] : 0;
+            nl += lcnt[q];
+            nc += ccnt[q];
+        }
+        const uint64_t below = (1ull << lane) - 1ull;
+        if (loser) {
+            const int at = offl + __popcll(bl & below);
+            lst_l[at] = me;
+            lst_w[at] = other;
+        } else if (in) {
+            lst_c[offc + __popcll(bc & below)] = me;
+        }
+        __syncthreads();
+        // the copies: a whole row per row group, counted in the column sums
+        for (int r = 0; r < (nc + RPB - 1) / RPB; ++r) {
+            const int q = r * RPB + slot;
+            if (q < nc) {
+                const int64_t i = lst_c[q];
+#pragma unroll
+                for (int it = 0; it < MAXIT; ++it) {
+                    const int64_t c = g + (int64_t)G * it;
+                    if (c < C4) {
+                        const float4 xi = *reinterpret_cast<const float4 *>(a.xs + i * a.ldx + 4 * c);
+                        st_stream(a.x + i * a.ldx + 4 * c, xi);
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) acc.add(it, e, (double)comp(xi, e));
+                    }
+                }
+            }
+        }
+        // the losers (uniform trip count: every thread reaches the barriers)
+        for (int r = 0; r < (nl + RPB - 1) / RPB; ++r) {
+            const int q = r * RPB + slot;
+            const bool active = q < nl;
+            const int64_t l = active ? lst_l[q] : 0;
+            const int64_t w = active ? lst_w[q] : 0;
+            float4 xr[MAXIT];
+#pragma unroll
+            for (int it = 0; it < MAXIT; ++it) {
+                const int64_t c = g + (int64_t)G * it;
+                float4 xn = make_float4(0.f, 0.f, 0.f, 0.f);
+                if (active && c < C4) {
                     const int64_t off = l * a.ldx + 4 * c;
-                    const float4 xl = ld_stream(a.xs + off);
+                    const float4 xl = *reinterpret_cast<const float4 *>(a.xs + off);
                     const float4 vl = ld_stream(a.v + off);
+                    const float4 xw = *reinterpret_cast<const float4 *>(a.xs + w * a.ldx + 4 * c);
                     // ring mean of the rows before the generation: ((x_{l-1} + x_l) + x_{l+1}) / 3
                     // in fp64, rounded once
                     const int64_t lm = l == 0 ? a.N - 1 : l - 1, lp = l == a.N - 1 ? 0 : l + 1;
@@ -677,33 +715,26 @@ __device__ __forceinline__ void cso_local_body(const CsoArgs &a)
                         const float nv = fmaf(cc, comp(xb, e) - xle, t1);
                         float nx = xle + nv;
                         if (a.xclamp) nx = fminf(fmaxf(nx, a.lb), a.ub);
-                        const bool in = 4 * c + e < a.D;
-                        xo[e] = in ? nx : 0.0f;
-                        vo[e] = in ? nv : 0.0f;
+                        const bool inb = 4 * c + e < a.D;
+                        xo[e] = inb ? nx : 0.0f;
+                        vo[e] = inb ? nv : 0.0f;
                     }
                     xn = make_float4(xo[0], xo[1], xo[2], xo[3]);
                     st_stream(a.x + off, xn);
                     st_stream(a.v + off, make_float4(vo[0], vo[1], vo[2], vo[3]));
-                }
-                st_stream(a.x + w * a.ldx + 4 * c, xw);  // the winner's row, unchanged
 #pragma unroll
-                for (int e = 0; e < 4; ++e)
-                    acc.add(it, e, paired ? (double)comp(xw, e) + (double)comp(xn, e) : (double)comp(xw, e));
+                    for (int e = 0; e < 4; ++e) acc.add(it, e, (double)comp(xn, e));
+                }
+                xr[it] = xn;
             }
-            xr[it] = xn;
-        }
-        const float f = row_fitness<FN, G, MAXIT>(xr, g, a.D, nbr, red);
-        if (active && g == 0) {
-            const uint64_t kw = sel_key(fw, w);
-            best = kw < best ? kw : best;
-            if (paired) {
+            const float f = row_fitness<FN, G, MAXIT>(xr, g, a.D, nbr, red);
+            if (active && g == 0) {
                 a.fit[l] = f;
-                const uint64_t kl = sel_key(f, l);
-                best = kl < best ? kl : best;
+                const uint64_t k = sel_key(f, l);
+                best = k < best ? k : best;
             }
         }
-        }
-        __syncthreads();  // the next phase overwrites the decisions
+        __syncthreads();  // the next range overwrites the lists
     }
     block_min_key(best, none, sk, sc);
     if (tid == 0) slot_commit(a.slots, best, 0);

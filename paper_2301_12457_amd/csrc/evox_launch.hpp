@@ -209,12 +209,11 @@ constexpr int kCsoSweep = 128;  // individuals per range of the swarm-mean gener
 
 struct CsoArgs {
     float *x, *v;
-    float *fit;            // fitness after the generation (the swarm version writes every entry; the
-                           // neighbourhood version updates the losers' entries in place)
-    const float *fit_in;   // swarm version: fitness before the generation (another buffer than fit)
+    float *fit;            // fitness after the generation (every entry written)
+    const float *fit_in;   // fitness before the generation (another buffer than fit)
     const float *xbar;
-    const uint32_t *perm;  // neighbourhood version: this generation's permutation
-    const uint32_t *mate;  // swarm version: this generation's mate array
+    const uint32_t *perm;  // this generation's permutation (not read by the generation kernels)
+    const uint32_t *mate;  // this generation's mate array
     int64_t N, D, ldx;
     float phi, lb, ub;
     int32_t xclamp;
