@@ -21,10 +21,10 @@
 // and v, is re-evaluated from registers, and both rows' new values are
 // accumulated into per-block fp64 column sums for the next swarm mean: 20 B
 // per pair element, i.e. 10 B per individual element.  The neighbourhood
-// version walks the pairs in permutation order, reads the positions from
-// the other population buffer (xs): the loser's neighbours l - 1 and l + 1
-// besides its own row (three consecutive rows), and writes every row of x
-// (the winner's as a copy).
+// version sweeps the same way, reads the positions from the other
+// population buffer (xs): the loser's neighbours l - 1 and l + 1 besides its
+// own row (three consecutive rows), and writes every row of x (the others'
+// as copies).
 #pragma once
 
 #include "evox_launch.hpp"

@@ -267,8 +267,7 @@ hipError_t launch_stream_copy(const float *src, float *dst, int64_t n, hipStream
 // (diagnostic): loser i = every index with winner_of[i] >= 0.
 hipError_t launch_pair_move(int G, float *x, float *v, int64_t N, int64_t D, int64_t ldx, const int32_t *winner_of,
                             hipStream_t s);
-// CSO's neighbourhood version: out row i = ((x_{i-1} + x_i) + x_{i+1}) / 3
-// (indices modulo N) in fp64, rounded once; every column of the pitch.
+// dst[0 .. ldx) = src[0 .. ldx).
 hipError_t launch_copy_row(const float *src, float *dst, int64_t ldx, hipStream_t s);
 hipError_t launch_fill(float *dst, int64_t n, float value, hipStream_t s);
 hipError_t launch_best_init(DevBest *best, float f, int64_t i, hipStream_t s);
