@@ -287,6 +287,29 @@ def cso_data_floor(torch, evox, w, ldx, reps=5):
     return us, 20.0 * pairs * D + 4.0 * N
 
 
+def pso_data_floor(torch, evox, w, ldx, reps=5):
+    """The data-movement floor of the PSO generation on this GPU: its 20 B per
+    element (read x, v, pbest; write x, v) streamed alone by evox_pso_stream
+    over arrays of the swarm's N x ldx floats, timed like the generation
+    kernel.  Returns its average launch duration and the algorithmic bytes
+    per launch (20 B per element of the N x D swarm)."""
+    n = w.N * ldx
+    x = torch.zeros(n, dtype=torch.float32, device="cuda")
+    v = torch.zeros_like(x)
+    p = torch.zeros_like(x)
+    evox.evox_pso_stream(x, v, p, n)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        evox.evox_pso_stream(x, v, p, n)
+    e1.record()
+    torch.cuda.synchronize()
+    us = e0.elapsed_time(e1) / reps * 1e3
+    del x, v, p
+    torch.cuda.empty_cache()
+    return us, 20.0 * w.N * w.D
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -489,6 +512,13 @@ def measure(torch, evox, w, steps, warmup, ldx):
                     "traffic": traffic_from_profile(w.name), "kernel": "k_eval",
                     "avg_launch_us": round(ms * 1e3, 2), "launches": steps,
                     "algorithmic_bytes_per_launch": bytes_per}
+    if roofline is not None and w.algo == "pso" and roofline["kernel"] == "k_pso_fused":
+        f_us, f_bytes = pso_data_floor(torch, evox, w, swarm.P.ldx)
+        floor_gbs = f_bytes / (f_us / 1e6) / 1e9
+        roofline["data_floor"] = {"kernel": "k_pso_stream (evox_pso_stream)", "avg_launch_us": round(f_us, 2),
+                                  "algorithmic_bytes_per_launch": f_bytes,
+                                  "frac": round(floor_gbs / HBM_PEAK_GBS, 4),
+                                  "achieved_over_floor": round(roofline["achieved"] / floor_gbs, 4)}
     if roofline is not None and w.algo == "cso" and not w.cso_local:
         f_us, f_bytes = cso_data_floor(torch, evox, w, swarm.P.ldx)
         roofline["data_floor"] = {"kernel": "k_pair_move (evox_pair_move)", "avg_launch_us": round(f_us, 2),

@@ -463,6 +463,16 @@ int evox_copy(const float *src, float *dst, int64_t n, void *hip_stream);
 int evox_pair_move(float *x, float *v, int64_t N, int64_t D, int64_t ldx, const int32_t *winner_of,
                    void *hip_stream);
 
+/* Diagnostic, the data-movement floor of the PSO generation: its 20 bytes
+ * per element (read x, v, pbest; write x, v; Sec. IV-B, Eq. (1)-(3) as
+ * evox_pso_step runs them) streamed with nothing else: for every q < n,
+ * v[q] = v[q] + (p[q] - x[q]), then x[q] = x[q] + v[q] (device x, v, p of n
+ * floats each, 16-byte aligned, n a multiple of 4; pass N * ldx for a swarm).
+ * One 16-byte element per thread with nontemporal loads and stores, the shape
+ * that streams fastest on gfx950.  No random numbers, fitness or selection.
+ * n = 0 does nothing. */
+int evox_pso_stream(float *x, float *v, const float *p, int64_t n, void *hip_stream);
+
 /* Diagnostic: out[4 k + m] = word m of Philox(seed, (k, c1, c2, c3)) for
  * k < n_ctr, computed by the device Philox the kernels use (device out). */
 int evox_philox_fill(uint64_t seed, uint32_t c1, uint32_t c2, uint32_t c3, int64_t n_ctr,

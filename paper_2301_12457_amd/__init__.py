@@ -28,7 +28,7 @@ EXPORTS = (
     "evox_nsga2_sort_scratch_bytes", "evox_nsga2_sort",
     "evox_cso_refresh", "evox_best", "evox_generation", "evox_set_generation", "evox_row_layout",
     "evox_default_ldx",
-    "evox_fill_normal", "evox_sgemm", "evox_copy", "evox_pair_move", "evox_philox_fill",
+    "evox_fill_normal", "evox_sgemm", "evox_copy", "evox_pso_stream", "evox_pair_move", "evox_philox_fill",
     "evox_permutation_scratch_bytes",
     "evox_permutation", "evox_argsort_u32",
     "evox_profile", "evox_profile_read", "evox_strerror", "evox_last_error",
@@ -106,6 +106,7 @@ def lib():
             "evox_fill_normal": ([u64, i64, i64, i64, ctypes.c_float, ctypes.c_float, P, P], i32),
             "evox_copy": ([P, P, i64, P], i32),
             "evox_pair_move": ([P, P, i64, i64, i64, P, P], i32),
+            "evox_pso_stream": ([P, P, P, i64, P], i32),
             "evox_sgemm": ([i32, i32, i64, i64, i64, ctypes.c_float, P, i64, P, i64, ctypes.c_float, P, i64, P],
                            i32),
             "evox_permutation_scratch_bytes": ([i64, i64], sz),
@@ -223,6 +224,12 @@ def evox_copy(src, dst, n, stream=None):
     """dst[:n] = src[:n] by the library's streaming copy (bandwidth reference)."""
     _check(lib().evox_copy(_ptr(src), _ptr(dst), n, _stream(stream)))
     return dst
+
+
+def evox_pso_stream(x, v, p, n, stream=None):
+    """v[:n] += p[:n] - x[:n]; x[:n] += v[:n]: the 20 B per element stream of
+    a PSO generation (diagnostic)."""
+    _check(lib().evox_pso_stream(_ptr(x), _ptr(v), _ptr(p), n, _stream(stream)))
 
 
 def evox_pair_move(x, v, N, D, ldx, winner_of, stream=None):

@@ -1266,6 +1266,17 @@ int evox_copy(const float *src, float *dst, int64_t n, void *hip_stream)
     return EVOX_OK;
 }
 
+int evox_pso_stream(float *x, float *v, const float *p, int64_t n, void *hip_stream)
+{
+    if (n < 0 || (n & 3)) return fail(EVOX_EINVAL, "n = %lld must be >= 0 and a multiple of 4", (long long)n);
+    if (n == 0) return EVOX_OK;
+    if (!x || !v || !p) return fail(EVOX_EINVAL, "x, v and p are required");
+    if (!aligned16(x) || !aligned16(v) || !aligned16(p)) return fail(EVOX_EALIGN, "x, v or p is not 16-byte aligned");
+    hipError_t e = launch_pso_stream(x, v, p, n, (hipStream_t)hip_stream);
+    if (e != hipSuccess) return hip_fail(e, "pso stream");
+    return EVOX_OK;
+}
+
 int evox_pair_move(float *x, float *v, int64_t N, int64_t D, int64_t ldx, const int32_t *winner_of,
                    void *hip_stream)
 {

@@ -258,6 +258,29 @@ hipError_t launch_stream_copy(const float *src, float *dst, int64_t n, hipStream
     return hipGetLastError();
 }
 
+// Diagnostic: the 20 B per element stream of a PSO generation alone, one
+// float4 per thread (grid-stride only beyond kMaxGrid blocks).
+__global__ __launch_bounds__(256) void k_pso_stream(float *x, float *v, const float *p, int64_t n4)
+{
+    for (int64_t q = (int64_t)blockIdx.x * 256 + threadIdx.x; q < n4; q += (int64_t)gridDim.x * 256) {
+        const float4 xv = ld_stream(x + 4 * q), vv = ld_stream(v + 4 * q), pv = ld_stream(p + 4 * q);
+        const float4 vn = make_float4(vv.x + (pv.x - xv.x), vv.y + (pv.y - xv.y), vv.z + (pv.z - xv.z),
+                                      vv.w + (pv.w - xv.w));
+        st_stream(v + 4 * q, vn);
+        st_stream(x + 4 * q, make_float4(xv.x + vn.x, xv.y + vn.y, xv.z + vn.z, xv.w + vn.w));
+    }
+}
+
+hipError_t launch_pso_stream(float *x, float *v, const float *p, int64_t n, hipStream_t s)
+{
+    const int64_t n4 = n / 4;
+    int64_t grid = (n4 + 255) / 256;
+    if (grid > kMaxGrid) grid = kMaxGrid;
+    if (grid < 1) grid = 1;
+    hipLaunchKernelGGL(k_pso_stream, dim3((unsigned)grid), dim3(256), 0, s, x, v, p, n4);
+    return hipGetLastError();
+}
+
 __device__ __forceinline__ uint32_t bucket_of(uint32_t key, int bits)
 {
     return bits ? key >> (32 - bits) : 0u;

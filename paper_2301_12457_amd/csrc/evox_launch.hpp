@@ -263,6 +263,9 @@ hipError_t launch_init(const InitArgs &a, hipStream_t s);
 hipError_t launch_philox_fill(uint32_t k0, uint32_t k1, uint32_t c1, uint32_t c2, uint32_t c3,
                               int64_t n, uint32_t *out, hipStream_t s);
 hipError_t launch_stream_copy(const float *src, float *dst, int64_t n, hipStream_t s);
+// The 20 B per element stream of a PSO generation (diagnostic): n floats,
+// n % 4 == 0.
+hipError_t launch_pso_stream(float *x, float *v, const float *p, int64_t n, hipStream_t s);
 // The data movement of a swarm-mean CSO generation with G lanes per row
 // (diagnostic): loser i = every index with winner_of[i] >= 0.
 hipError_t launch_pair_move(int G, float *x, float *v, int64_t N, int64_t D, int64_t ldx, const int32_t *winner_of,

@@ -162,6 +162,11 @@ def test_eval_rejects_bad_args(evox):
     assert L.evox_copy(None, None, 5, None) == evox.EINVAL
     assert L.evox_copy(0x1000, 0x2000, -1, None) == evox.EINVAL
     assert L.evox_copy(0x1004, 0x2000, 5, None) == evox.EALIGN
+    assert L.evox_pso_stream(None, None, None, 0, None) == evox.OK
+    assert L.evox_pso_stream(None, None, None, 8, None) == evox.EINVAL                 # null buffers
+    assert L.evox_pso_stream(0x1000, 0x2000, 0x3000, 6, None) == evox.EINVAL         # n % 4
+    assert L.evox_pso_stream(0x1000, 0x2000, 0x3000, -4, None) == evox.EINVAL        # n < 0
+    assert L.evox_pso_stream(0x1000, 0x2004, 0x3000, 8, None) == evox.EALIGN
     assert L.evox_fill_normal(1, 0, 3, 4, 0.0, 1.0, None, None) == evox.OK     # empty
     assert L.evox_fill_normal(1, 5, 3, 4, 0.0, 1.0, None, None) == evox.EINVAL
     assert L.evox_fill_normal(1, 5, 5, 4, 0.0, 1.0, 0x1000, None) == evox.EINVAL

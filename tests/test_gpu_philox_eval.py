@@ -103,6 +103,21 @@ def test_eval_empty_population(evox_gpu):
     torch.cuda.synchronize()
 
 
+@pytest.mark.parametrize("n", [4, 1028, 4096 * 1024 + 8])
+def test_pso_stream(evox_gpu, n):
+    """The PSO data-movement floor computes v + (p - x), then x + v, in fp32
+    (one rounding per operation, as numpy does), and touches nothing past n."""
+    g = torch.Generator().manual_seed(n)
+    x, v, p = (torch.randn(n + 8, generator=g) for _ in range(3))
+    xd, vd, pd = x.cuda(), v.cuda(), p.cuda()
+    evox_gpu.evox_pso_stream(xd, vd, pd, n)
+    xn, vn, pn = x.numpy(), v.numpy(), p.numpy()
+    v_ref = vn[:n] + (pn[:n] - xn[:n])
+    x_ref = xn[:n] + v_ref
+    assert np.array_equal(vd.cpu().numpy()[:n], v_ref) and np.array_equal(xd.cpu().numpy()[:n], x_ref)
+    assert torch.equal(vd[n:].cpu(), v[n:]) and torch.equal(xd[n:].cpu(), x[n:]) and torch.equal(pd.cpu(), p)
+
+
 @pytest.mark.parametrize("n", [1, 3, 4, 1027, 4096 * 1024 + 5])
 def test_stream_copy(evox_gpu, n):
     src = torch.randn(n + 8, device="cuda")
