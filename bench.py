@@ -325,7 +325,7 @@ def main():
                     help="also run a plain device copy of this size (HBM-counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(f"bench.py runs on one GPU only (asked for {args.gpus}): this build has no "
+        print(f"bench.py runs on one GPU only (asked for {args.gpus}): this implementation has no "
               "multi-GPU path", file=sys.stderr)
         sys.exit(2)
 

@@ -26,7 +26,7 @@
  *   - Random numbers: Philox4x32-10 (Salmon, Moraes, Dror, Shaw, "Parallel
  *     random numbers: as easy as 1, 2, 3", SC'11), written from its
  *     published definition.  The paper itself names only JAX's rbg
- *     generator (Sec. VII); the counter layout below is this build's own.
+ *     generator (Sec. VII); the counter layout below is chosen here (the paper fixes none).
  *
  * Build: gcc -O2 -ffp-contract=off -fPIC -shared (no fast-math): every float
  * operation is one IEEE rounding, fma only where fmaf() is written.
